@@ -1,0 +1,433 @@
+/*
+ * Plain CPU oracle for the VSA2 routed sparse-attention path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library links, includes
+ * or calls this file; only the test-suite, the smoke check and the CPU
+ * baseline leg of the benchmark load it.  It shares no code, header, table or
+ * helper with the HIP kernels.
+ *
+ * Paper: "Improving Video Sparse Attention with Fine-grained Router and Sparse
+ * Rebasing" (VSA2).  Every function below follows one passage of its Method
+ * section (Sec. 2) and is written for a reader checking it by eye:
+ *   - every tensor value is widened to double on read, every sum is a plain
+ *     loop in double, nothing is blocked, fused or reordered;
+ *   - inputs arrive as float arrays holding the exact input values (a bf16
+ *     value widens exactly into a float);
+ *   - layout is cube-major [batch][head][L][D] with L = N * B tokens
+ *     (Sec. 2.2 "Permutation"): token l = n*B + beta, n = (nt*Nh + nh)*Nw + nw,
+ *     beta = (bt*Bh + bh)*Bw + bw (raster order, w fastest, at every level).
+ *
+ * Readings of points the paper leaves open (the design notes list them all):
+ *   - pooled router inputs Q_r, K_r are rounded to the input dtype (RNE);
+ *   - router softmax runs over all N*G pooled keys with scale 1/sqrt(D);
+ *   - MeanPool_{GxG} is a true mean, so every P_r row sums to 1/G;
+ *   - selection decides in fp32: scores are rounded to float, ordered by
+ *     (score desc, block index asc);
+ *   - a query block with no selected block gets O = 0, LSE = -inf, dQ = 0;
+ *   - query head h reads KV head h / (Hq/Hkv).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ---------------------------------------------------------------------- */
+/* Rounding of a double to the input dtype.                                */
+/* ---------------------------------------------------------------------- */
+
+/* Round-to-nearest-even of x to bfloat16 (8 significant bits, float's
+ * exponent range), returned as the exactly representable float. */
+static double round_to_bf16(double x)
+{
+    if (x == 0.0 || isnan(x) || isinf(x)) return x;
+    double ax = fabs(x);
+    double q;
+    if (ax < ldexp(1.0, -126)) {
+        /* bf16 subnormals are multiples of 2^-133 */
+        q = nearbyint(x * ldexp(1.0, 133)) * ldexp(1.0, -133);
+    } else {
+        int e;
+        double m = frexp(x, &e);           /* x = m * 2^e, 0.5 <= |m| < 1 */
+        q = ldexp(nearbyint(ldexp(m, 8)), e - 8);  /* keep 8 bits, RNE */
+    }
+    if (fabs(q) > 3.3895313892515355e38) q = copysign(INFINITY, x);
+    return q;
+}
+
+static float round_to_dtype(double x, int dtype_bf16)
+{
+    return dtype_bf16 ? (float)round_to_bf16(x) : (float)x;
+}
+
+void vo_round_bf16(const double* in, float* out, int64_t n)
+{
+    for (int64_t i = 0; i < n; ++i) out[i] = (float)round_to_bf16(in[i]);
+}
+
+/* ---------------------------------------------------------------------- */
+/* MeanPool over sub-cubes (Eq. router_start for P = R; Eq. compress for   */
+/* P = B).                                                                 */
+/* ---------------------------------------------------------------------- */
+
+/* x: [nbh][N*B][D] cube-major.  out: [nbh][N*Gp][D] with Gp = B/P sub-cubes
+ * per cube, ordered (n, g), g = (gt*Gh + gh)*Gw + gw.  Each output row is the
+ * mean of the P = Pt*Ph*Pw tokens of its sub-cube, rounded to the dtype. */
+void vo_pool(const float* x, int64_t nbh, int T, int H, int W,
+             int Bt, int Bh, int Bw, int Pt, int Ph, int Pw, int D,
+             int dtype_bf16, float* out)
+{
+    const int Nt = T / Bt, Nh = H / Bh, Nw = W / Bw;
+    const int64_t N = (int64_t)Nt * Nh * Nw;
+    const int B = Bt * Bh * Bw;
+    const int Gt = Bt / Pt, Gh = Bh / Ph, Gw = Bw / Pw;
+    const int G = Gt * Gh * Gw;
+    const int P = Pt * Ph * Pw;
+#pragma omp parallel for schedule(static)
+    for (int64_t bh = 0; bh < nbh; ++bh) {
+        for (int64_t n = 0; n < N; ++n) {
+            for (int gt = 0; gt < Gt; ++gt)
+            for (int gh = 0; gh < Gh; ++gh)
+            for (int gw = 0; gw < Gw; ++gw) {
+                const int g = (gt * Gh + gh) * Gw + gw;
+                float* o = out + ((bh * N + n) * G + g) * (int64_t)D;
+                for (int d = 0; d < D; ++d) {
+                    double sum = 0.0;
+                    for (int rt = 0; rt < Pt; ++rt)
+                    for (int rh = 0; rh < Ph; ++rh)
+                    for (int rw = 0; rw < Pw; ++rw) {
+                        const int bt = gt * Pt + rt, bhh = gh * Ph + rh, bw = gw * Pw + rw;
+                        const int beta = (bt * Bh + bhh) * Bw + bw;
+                        sum += (double)x[((bh * N + n) * B + beta) * (int64_t)D + d];
+                    }
+                    o[d] = round_to_dtype(sum / (double)P, dtype_bf16);
+                }
+            }
+        }
+    }
+}
+
+/* ---------------------------------------------------------------------- */
+/* Router block scores (Eq. router_start .. Eq. router_end).               */
+/* ---------------------------------------------------------------------- */
+
+/* q_r: [nb][Hq][N*G][D], k_r: [nb][Hkv][N*G][D] (pooled, already rounded).
+ * rows[i] = (b*Hq + h)*N + nq names one query block.  For each listed row:
+ *   s[gq][j]  = Q_r[nq*G+gq] . K_r[j] / sqrt(D)       for all j < N*G,
+ *   lse[gq]   = log sum_j exp(s[gq][j])                (max-shifted),
+ *   P_hat     = exp(s - lse)                            (row softmax),
+ *   P_r[nk]   = (1/G^2) sum_{gq,gk} P_hat[gq][nk*G+gk]  (MeanPool_{GxG}).
+ * scores: [nrows][N]; lse_out: [nrows][G] or NULL. */
+void vo_router_scores(const float* q_r, const float* k_r, int nb, int Hq, int Hkv,
+                      int64_t N, int G, int D, const int64_t* rows, int64_t nrows,
+                      double* scores, double* lse_out)
+{
+    (void)nb;
+    const int64_t NG = N * G;
+    const int grp = Hq / Hkv;
+    const double scale = 1.0 / sqrt((double)D);
+#pragma omp parallel
+    {
+        double* s = (double*)malloc(sizeof(double) * (size_t)NG);
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t r = 0; r < nrows; ++r) {
+            const int64_t row = rows[r];
+            const int64_t bh = row / N, nq = row % N;
+            const int64_t b = bh / Hq, h = bh % Hq;
+            const int64_t hkv = h / grp;
+            const float* K = k_r + (b * Hkv + hkv) * NG * (int64_t)D;
+            double* out = scores + r * N;
+            for (int64_t nk = 0; nk < N; ++nk) out[nk] = 0.0;
+            for (int gq = 0; gq < G; ++gq) {
+                const float* qi = q_r + ((bh * N + nq) * G + gq) * (int64_t)D;
+                double m = -INFINITY;
+                for (int64_t j = 0; j < NG; ++j) {
+                    double dot = 0.0;
+                    for (int d = 0; d < D; ++d) dot += (double)qi[d] * (double)K[j * D + d];
+                    s[j] = dot * scale;
+                    if (s[j] > m) m = s[j];
+                }
+                double sum = 0.0;
+                for (int64_t j = 0; j < NG; ++j) sum += exp(s[j] - m);
+                const double lse = m + log(sum);
+                if (lse_out) lse_out[r * G + gq] = lse;
+                for (int64_t nk = 0; nk < N; ++nk)
+                    for (int gk = 0; gk < G; ++gk)
+                        out[nk] += exp(s[nk * G + gk] - lse) / ((double)G * (double)G);
+            }
+        }
+        free(s);
+    }
+}
+
+/* ---------------------------------------------------------------------- */
+/* Selection.                                                              */
+/* ---------------------------------------------------------------------- */
+
+typedef struct { float v; int32_t i; } vo_scored;
+
+/* (score desc, index asc) */
+static int cmp_desc(const void* a, const void* b)
+{
+    const vo_scored* x = (const vo_scored*)a;
+    const vo_scored* y = (const vo_scored*)b;
+    if (x->v > y->v) return -1;
+    if (x->v < y->v) return 1;
+    return (x->i > y->i) - (x->i < y->i);
+}
+
+static int cmp_int(const void* a, const void* b)
+{
+    const int32_t x = *(const int32_t*)a, y = *(const int32_t*)b;
+    return (x > y) - (x < y);
+}
+
+/* Per-query-block selection over one row of N block scores.
+ *   mode 0 (top-k):  the k best blocks (k > N keeps all N);
+ *   mode 1 (mass):   the smallest prefix of the sorted row whose sum reaches
+ *                    mass * (row total), capped at cap blocks.
+ * Scores are rounded to float first: the decision is taken in fp32.
+ * counts: [nrows]; idx: [nrows][N], selected blocks ascending, rest -1. */
+void vo_select_rows(const double* scores, int64_t nrows, int N, int mode, int k,
+                    double mass, int cap, int32_t* counts, int32_t* idx)
+{
+#pragma omp parallel
+    {
+        vo_scored* a = (vo_scored*)malloc(sizeof(vo_scored) * (size_t)N);
+#pragma omp for schedule(dynamic, 16)
+        for (int64_t r = 0; r < nrows; ++r) {
+            for (int j = 0; j < N; ++j) { a[j].v = (float)scores[r * N + j]; a[j].i = j; }
+            qsort(a, (size_t)N, sizeof(vo_scored), cmp_desc);
+            int c;
+            if (mode == 0) {
+                c = k < N ? k : N;
+            } else {
+                double total = 0.0;
+                for (int j = 0; j < N; ++j) total += (double)a[j].v;
+                const double thr = mass * total;
+                double cum = 0.0;
+                c = N;
+                for (int j = 0; j < N; ++j) {
+                    cum += (double)a[j].v;
+                    if (cum >= thr) { c = j + 1; break; }
+                }
+                if (c > cap) c = cap;
+            }
+            int32_t* out = idx + r * (int64_t)N;
+            for (int j = 0; j < c; ++j) out[j] = a[j].i;
+            qsort(out, (size_t)c, sizeof(int32_t), cmp_int);
+            for (int j = c; j < N; ++j) out[j] = -1;
+            counts[r] = c;
+        }
+        free(a);
+    }
+}
+
+/* Sequence-level top-(N*k) over the flattened N x N score map of one
+ * (batch, head) (the paper's TopK_{NK}): keeps the N*k best (query block,
+ * key block) pairs, ties broken by flat index nq*N + nk.  scores: [nseq][N*N],
+ * sel: [nseq][N*N] set to 1 for kept pairs, 0 otherwise. */
+void vo_select_seq(const double* scores, int64_t nseq, int N, int k, uint8_t* sel)
+{
+    const int64_t NN = (int64_t)N * N;
+    int64_t keep = (int64_t)N * k;
+    if (keep > NN) keep = NN;
+#pragma omp parallel
+    {
+        vo_scored* a = (vo_scored*)malloc(sizeof(vo_scored) * (size_t)NN);
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t s = 0; s < nseq; ++s) {
+            for (int64_t j = 0; j < NN; ++j) { a[j].v = (float)scores[s * NN + j]; a[j].i = (int32_t)j; }
+            qsort(a, (size_t)NN, sizeof(vo_scored), cmp_desc);
+            uint8_t* out = sel + s * NN;
+            memset(out, 0, (size_t)NN);
+            for (int64_t j = 0; j < keep; ++j) out[a[j].i] = 1;
+        }
+        free(a);
+    }
+}
+
+/* ---------------------------------------------------------------------- */
+/* Block-sparse attention forward (Sec. 2.1 masked attention; Eq.          */
+/* block_sparse).                                                          */
+/* ---------------------------------------------------------------------- */
+
+/* One query token against the keys of its selected blocks.  Fills p[] (the
+ * softmax row over the gathered keys, in CSR order), o[D] and returns the
+ * natural-log LSE.  An empty selection gives o = 0 and -inf. */
+static double token_forward(const float* qv, const float* K, const float* V, int D, int B,
+                            const int32_t* sel, int nsel, double scale, double* p, double* o)
+{
+    const int nkeys = nsel * B;
+    for (int d = 0; d < D; ++d) o[d] = 0.0;
+    if (nkeys == 0) return -INFINITY;
+    double m = -INFINITY;
+    for (int c = 0; c < nsel; ++c)
+        for (int t = 0; t < B; ++t) {
+            const int64_t j = (int64_t)sel[c] * B + t;
+            double dot = 0.0;
+            for (int d = 0; d < D; ++d) dot += (double)qv[d] * (double)K[j * D + d];
+            p[c * B + t] = dot * scale;
+            if (p[c * B + t] > m) m = p[c * B + t];
+        }
+    double sum = 0.0;
+    for (int j = 0; j < nkeys; ++j) { p[j] = exp(p[j] - m); sum += p[j]; }
+    for (int j = 0; j < nkeys; ++j) p[j] /= sum;
+    for (int c = 0; c < nsel; ++c)
+        for (int t = 0; t < B; ++t) {
+            const int64_t j = (int64_t)sel[c] * B + t;
+            for (int d = 0; d < D; ++d) o[d] += p[c * B + t] * (double)V[j * D + d];
+        }
+    return m + log(sum);
+}
+
+/* q: [nb][Hq][L][D]; k, v: [nb][Hkv][L][D]; CSR row_ptr/col_idx over rows
+ * (b*Hq + h)*N + n.  For each listed row, writes O: [nq][B][D] and
+ * LSE: [nq][B] (natural log) of its B query tokens. */
+void vo_attn_fwd(const float* q, const float* k, const float* v, int nb, int Hq, int Hkv,
+                 int64_t L, int D, int B, const int32_t* row_ptr, const int32_t* col_idx,
+                 const int64_t* qrows, int64_t nq, double* o, double* lse)
+{
+    (void)nb;
+    const int64_t N = L / B;
+    const int grp = Hq / Hkv;
+    const double scale = 1.0 / sqrt((double)D);
+#pragma omp parallel
+    {
+        double* p = (double*)malloc(sizeof(double) * (size_t)L);
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t r = 0; r < nq; ++r) {
+            const int64_t row = qrows[r];
+            const int64_t bh = row / N, n = row % N;
+            const int64_t b = bh / Hq, h = bh % Hq, hkv = h / grp;
+            const float* K = k + (b * Hkv + hkv) * L * D;
+            const float* V = v + (b * Hkv + hkv) * L * D;
+            const int32_t* sel = col_idx + row_ptr[row];
+            const int nsel = row_ptr[row + 1] - row_ptr[row];
+            for (int t = 0; t < B; ++t) {
+                const float* qv = q + (bh * L + n * B + t) * D;
+                lse[r * B + t] = token_forward(qv, K, V, D, B, sel, nsel, scale, p,
+                                               o + (r * B + t) * (int64_t)D);
+            }
+        }
+        free(p);
+    }
+}
+
+/* ---------------------------------------------------------------------- */
+/* Block-sparse attention backward.  The mask is a constant: no gradient   */
+/* reaches the router (Sec. 2.1, gradient-free routing).  With p the       */
+/* softmax row of token l over its gathered keys j:                        */
+/*   Delta_l = dO_l . O_l,  dP_j = dO_l . V_j,  dS_j = p_j (dP_j - Delta_l) */
+/*   dQ_l = scale * sum_j dS_j K_j,  dK_j += scale * dS_j Q_l,             */
+/*   dV_j += p_j dO_l  (summed over every query token that reads key j).   */
+/* ---------------------------------------------------------------------- */
+
+/* dQ for listed query blocks: qrows as in vo_attn_fwd, dq: [nq][B][D]. */
+void vo_attn_bwd_dq(const float* q, const float* k, const float* v, const float* dout,
+                    int nb, int Hq, int Hkv, int64_t L, int D, int B,
+                    const int32_t* row_ptr, const int32_t* col_idx,
+                    const int64_t* qrows, int64_t nq, double* dq)
+{
+    (void)nb;
+    const int64_t N = L / B;
+    const int grp = Hq / Hkv;
+    const double scale = 1.0 / sqrt((double)D);
+#pragma omp parallel
+    {
+        double* p = (double*)malloc(sizeof(double) * (size_t)L);
+        double* o = (double*)malloc(sizeof(double) * (size_t)D);
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t r = 0; r < nq; ++r) {
+            const int64_t row = qrows[r];
+            const int64_t bh = row / N, n = row % N;
+            const int64_t b = bh / Hq, h = bh % Hq, hkv = h / grp;
+            const float* K = k + (b * Hkv + hkv) * L * D;
+            const float* V = v + (b * Hkv + hkv) * L * D;
+            const int32_t* sel = col_idx + row_ptr[row];
+            const int nsel = row_ptr[row + 1] - row_ptr[row];
+            for (int t = 0; t < B; ++t) {
+                const int64_t tok = bh * L + n * B + t;
+                const float* qv = q + tok * D;
+                const float* dov = dout + tok * D;
+                double* g = dq + (r * B + t) * (int64_t)D;
+                for (int d = 0; d < D; ++d) g[d] = 0.0;
+                token_forward(qv, K, V, D, B, sel, nsel, scale, p, o);
+                double delta = 0.0;
+                for (int d = 0; d < D; ++d) delta += (double)dov[d] * o[d];
+                for (int c = 0; c < nsel; ++c)
+                    for (int u = 0; u < B; ++u) {
+                        const int64_t j = (int64_t)sel[c] * B + u;
+                        double dp = 0.0;
+                        for (int d = 0; d < D; ++d) dp += (double)dov[d] * (double)V[j * D + d];
+                        const double ds = p[c * B + u] * (dp - delta);
+                        for (int d = 0; d < D; ++d) g[d] += scale * ds * (double)K[j * D + d];
+                    }
+            }
+        }
+        free(p);
+        free(o);
+    }
+}
+
+/* dK and dV for listed key blocks: kvrows[i] = (b*Hkv + hkv)*N + nk.
+ * Every query token of every query head of the KV head's group whose row
+ * selects block nk contributes.  dk, dv: [nkv][B][D]. */
+void vo_attn_bwd_dkdv(const float* q, const float* k, const float* v, const float* dout,
+                      int nb, int Hq, int Hkv, int64_t L, int D, int B,
+                      const int32_t* row_ptr, const int32_t* col_idx,
+                      const int64_t* kvrows, int64_t nkv, double* dk, double* dv)
+{
+    (void)nb;
+    const int64_t N = L / B;
+    const int grp = Hq / Hkv;
+    const double scale = 1.0 / sqrt((double)D);
+#pragma omp parallel
+    {
+        double* p = (double*)malloc(sizeof(double) * (size_t)L);
+        double* o = (double*)malloc(sizeof(double) * (size_t)D);
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t r = 0; r < nkv; ++r) {
+            const int64_t krow = kvrows[r];
+            const int64_t bkv = krow / N, nk = krow % N;
+            const int64_t b = bkv / Hkv, hkv = bkv % Hkv;
+            const float* K = k + bkv * L * D;
+            const float* V = v + bkv * L * D;
+            double* gk = dk + r * (int64_t)B * D;
+            double* gv = dv + r * (int64_t)B * D;
+            for (int64_t i = 0; i < (int64_t)B * D; ++i) { gk[i] = 0.0; gv[i] = 0.0; }
+            for (int hl = 0; hl < grp; ++hl) {
+                const int64_t h = hkv * grp + hl;
+                const int64_t bh = b * Hq + h;
+                for (int64_t n = 0; n < N; ++n) {
+                    const int64_t row = bh * N + n;
+                    const int32_t* sel = col_idx + row_ptr[row];
+                    const int nsel = row_ptr[row + 1] - row_ptr[row];
+                    int pos = -1;
+                    for (int c = 0; c < nsel; ++c) if (sel[c] == nk) pos = c;
+                    if (pos < 0) continue;
+                    for (int t = 0; t < B; ++t) {
+                        const int64_t tok = bh * L + n * B + t;
+                        const float* qv = q + tok * D;
+                        const float* dov = dout + tok * D;
+                        token_forward(qv, K, V, D, B, sel, nsel, scale, p, o);
+                        double delta = 0.0;
+                        for (int d = 0; d < D; ++d) delta += (double)dov[d] * o[d];
+                        for (int u = 0; u < B; ++u) {
+                            const int64_t j = nk * B + u;
+                            const double pj = p[pos * B + u];
+                            double dp = 0.0;
+                            for (int d = 0; d < D; ++d) dp += (double)dov[d] * (double)V[j * D + d];
+                            const double ds = pj * (dp - delta);
+                            for (int d = 0; d < D; ++d) {
+                                gv[u * D + d] += pj * (double)dov[d];
+                                gk[u * D + d] += scale * ds * (double)qv[d];
+                            }
+                        }
+                    }
+                }
+            }
+        }
+        free(p);
+        free(o);
+    }
+}

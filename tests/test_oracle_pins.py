@@ -1,0 +1,430 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle.
+
+Each test checks one oracle step against a closed form, an invariant the
+paper's definitions imply, a special case that reduces to a textbook or
+library routine (torch / numpy in float64), brute force, or a value the paper
+prints.  Chosen so that a dropped term, wrong sign, wrong index or transposed
+operand in the oracle fails at least one of them.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from workload import BF16, F32, Problem, Selection, Workload, make_inputs, raster_to_cube_major, \
+    round_bf16_f32
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def small(dtype=F32, T=4, H=8, W=8, Bt=2, Bh=4, Bw=4, Rt=1, Rh=2, Rw=2, hq=2, hkv=2, D=16):
+    return Problem(1, hq, hkv, D, T, H, W, Bt, Bh, Bw, Rt, Rh, Rw, dtype)
+
+
+def rand_qkv(p, seed=0, scale=1.0):
+    rng = np.random.default_rng(seed)
+    q = (rng.standard_normal((p.batch, p.heads_q, p.L, p.head_dim)) * scale).astype(np.float32)
+    k = (rng.standard_normal((p.batch, p.heads_kv, p.L, p.head_dim)) * scale).astype(np.float32)
+    v = rng.standard_normal((p.batch, p.heads_kv, p.L, p.head_dim)).astype(np.float32)
+    do = rng.standard_normal((p.batch, p.heads_q, p.L, p.head_dim)).astype(np.float32)
+    if p.dtype == BF16:
+        q, k, v, do = (round_bf16_f32(t) for t in (q, k, v, do))
+    return q, k, v, do
+
+
+# ---------------------------------------------------------------- rounding
+
+def test_bf16_rounding_ties_and_library():
+    # ties round to even, exactly representable values stay, halfway above/below
+    one = 1.0
+    ulp = 2.0 ** -7
+    cases = {
+        one: one,
+        one + ulp / 2: one,                    # tie -> even (1.0)
+        one + 3 * ulp / 2: one + 2 * ulp,      # tie -> even (1 + 2 ulp)
+        one + ulp / 2 + 2.0 ** -30: one + ulp,  # just above the tie
+        -(one + ulp / 2): -one,
+        2.0 ** -130: 2.0 ** -130,              # bf16 subnormal, exact
+        3.0 * 2.0 ** -134: 2.0 ** -132,        # subnormal tie 1.5 ulp -> even (2 ulp)
+    }
+    got = oracle.round_bf16(np.array(list(cases.keys())))
+    assert np.array_equal(got.astype(np.float64), np.array(list(cases.values())))
+    # float32-exact values: torch's float -> bfloat16 conversion is RNE
+    x = np.random.default_rng(1).standard_normal(20000).astype(np.float32) * 7
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
+    assert np.array_equal(oracle.round_bf16(x.astype(np.float64)), ref)
+
+
+# ---------------------------------------------------------------- pooling
+
+@pytest.mark.parametrize("P", [(1, 2, 2), (2, 2, 2), (2, 4, 4), (1, 1, 1), (2, 1, 4)])
+def test_pool_affine_ramp_closed_form(P):
+    """Mean of an affine function over a sub-cube is its value at the centre."""
+    p = small(T=4, H=8, W=12, Bt=2, Bh=4, Bw=4, D=3)
+    Pt, Ph, Pw = P
+    t, h, w = np.meshgrid(np.arange(p.T), np.arange(p.H), np.arange(p.W), indexing="ij")
+    coef = np.array([[0.5, 2.0, -0.25], [1.0, -1.5, 0.125], [-2.0, 0.75, 4.0]])  # [D][t,h,w]
+    off = np.array([1.0, -3.0, 0.5])
+    x = np.stack([coef[d, 0] * t + coef[d, 1] * h + coef[d, 2] * w + off[d] for d in range(3)], -1)
+    xr = raster_to_cube_major(x.reshape(1, 1, p.L, 3).astype(np.float32), p)
+    out = oracle.pool(xr, p, Pt, Ph, Pw)
+    Gt, Gh, Gw = p.Bt // Pt, p.Bh // Ph, p.Bw // Pw
+    Nt, Nh, Nw = p.T // p.Bt, p.H // p.Bh, p.W // p.Bw
+    exp = np.zeros_like(out)
+    for nt in range(Nt):
+        for nh in range(Nh):
+            for nw in range(Nw):
+                n = (nt * Nh + nh) * Nw + nw
+                for gt in range(Gt):
+                    for gh in range(Gh):
+                        for gw in range(Gw):
+                            g = (gt * Gh + gh) * Gw + gw
+                            tc = nt * p.Bt + gt * Pt + (Pt - 1) / 2
+                            hc = nh * p.Bh + gh * Ph + (Ph - 1) / 2
+                            wc = nw * p.Bw + gw * Pw + (Pw - 1) / 2
+                            exp[0, 0, n * Gt * Gh * Gw + g] = coef @ np.array([tc, hc, wc]) + off
+    assert np.array_equal(out, exp)
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16])
+def test_pool_matches_numpy_reshape_mean(dtype):
+    p = small(dtype=dtype, T=4, H=8, W=8, D=8)
+    x = np.random.default_rng(3).standard_normal((1, 2, p.L, p.head_dim)).astype(np.float32)
+    if dtype == BF16:
+        x = round_bf16_f32(x)
+    out = oracle.pool(x, p, p.Rt, p.Rh, p.Rw)
+    # raster grid, numpy mean over the pooling windows, then (n, g) order
+    from workload import cube_major_to_raster
+    xg = cube_major_to_raster(x, p).reshape(1, 2, p.T, p.H, p.W, p.head_dim).astype(np.float64)
+    m = xg.reshape(1, 2, p.T // p.Rt, p.Rt, p.H // p.Rh, p.Rh, p.W // p.Rw, p.Rw, p.head_dim)
+    m = m.mean(axis=(3, 5, 7))                       # [1,2,T/Rt,H/Rh,W/Rw,D]
+    Gt, Gh, Gw = p.Bt // p.Rt, p.Bh // p.Rh, p.Bw // p.Rw
+    m = m.reshape(1, 2, p.T // p.Bt, Gt, p.H // p.Bh, Gh, p.W // p.Bw, Gw, p.head_dim)
+    m = m.transpose(0, 1, 2, 4, 6, 3, 5, 7, 8).reshape(1, 2, p.N * p.G, p.head_dim)
+    # float64 -> dtype with one rounding (the bf16 rounding is pinned above)
+    ref = m.astype(np.float32) if dtype == F32 else oracle.round_bf16(m)
+    assert np.array_equal(out, ref)
+
+
+# ---------------------------------------------------------------- router
+
+def _softmax64(s):
+    return torch.softmax(torch.from_numpy(s), dim=-1).numpy()
+
+
+def test_router_R_equals_B_is_coarse_softmax():
+    """G = 1: P_r is VSA's cube-level softmax(Q_c K_c^T / sqrt(D))."""
+    p = small(T=4, H=8, W=8, Bt=2, Bh=4, Bw=4, Rt=2, Rh=4, Rw=4, D=16)
+    q, k, _, _ = rand_qkv(p, 5)
+    q_r, k_r = oracle.pool(q, p, p.Rt, p.Rh, p.Rw), oracle.pool(k, p, p.Rt, p.Rh, p.Rw)
+    sc = oracle.router_scores(q_r, k_r, p).reshape(1, p.heads_q, p.N, p.N)
+    qc = q.astype(np.float64).reshape(1, p.heads_q, p.N, p.B, p.head_dim).mean(3).astype(np.float32)
+    kc = k.astype(np.float64).reshape(1, p.heads_kv, p.N, p.B, p.head_dim).mean(3).astype(np.float32)
+    ref = _softmax64(np.einsum("bhid,bhjd->bhij", qc.astype(np.float64), kc.astype(np.float64))
+                     / math.sqrt(p.head_dim))
+    np.testing.assert_allclose(sc, ref, rtol=1e-12, atol=1e-15)
+
+
+def test_router_R_one_is_block_mean_of_token_softmax():
+    """R = 1 (G = B): P_r equals P_oracle = MeanPool_{BxB}(Softmax(QK^T/sqrt(D)))."""
+    p = small(T=2, H=4, W=8, Bt=2, Bh=2, Bw=2, Rt=1, Rh=1, Rw=1, D=8)
+    q, k, _, _ = rand_qkv(p, 6)
+    q_r, k_r = oracle.pool(q, p, 1, 1, 1), oracle.pool(k, p, 1, 1, 1)
+    assert np.array_equal(q_r, q) and np.array_equal(k_r, k)
+    sc = oracle.router_scores(q_r, k_r, p).reshape(1, p.heads_q, p.N, p.N)
+    P = _softmax64(np.einsum("bhid,bhjd->bhij", q.astype(np.float64), k.astype(np.float64))
+                   / math.sqrt(p.head_dim))
+    ref = P.reshape(1, p.heads_q, p.N, p.B, p.N, p.B).mean(axis=(3, 5))
+    np.testing.assert_allclose(sc, ref, rtol=1e-12, atol=1e-16)
+
+
+def test_router_rows_sum_to_inverse_G_and_nonnegative():
+    p = small(T=4, H=8, W=8, D=16)
+    q, k, _, _ = rand_qkv(p, 7, scale=2.0)
+    q_r, k_r = oracle.pool(q, p, p.Rt, p.Rh, p.Rw), oracle.pool(k, p, p.Rt, p.Rh, p.Rw)
+    sc, lse = oracle.router_scores(q_r, k_r, p, with_lse=True)
+    assert (sc >= 0).all()
+    np.testing.assert_allclose(sc.sum(1), 1.0 / p.G, rtol=1e-12)
+    # LSE of the first pooled query, by torch
+    s0 = q_r[0, 0, :1].astype(np.float64) @ k_r[0, 0].astype(np.float64).T / math.sqrt(p.head_dim)
+    assert abs(lse[0, 0] - torch.logsumexp(torch.from_numpy(s0), -1).item()) < 1e-12
+
+
+def test_router_gqa_head_mapping():
+    """Query head h reads KV head h // (Hq/Hkv): same as MHA with K replicated."""
+    p = small(hq=4, hkv=2, D=8)
+    q, k, _, _ = rand_qkv(p, 8)
+    q_r, k_r = oracle.pool(q, p, p.Rt, p.Rh, p.Rw), oracle.pool(k, p, p.Rt, p.Rh, p.Rw)
+    sc = oracle.router_scores(q_r, k_r, p)
+    pm = p.replace(heads_kv=4)
+    sc2 = oracle.router_scores(q_r, np.repeat(k_r, 2, axis=1), pm)
+    assert np.array_equal(sc, sc2)
+
+
+def test_router_shared_means_pick_own_cube():
+    """With Q and K of a head sharing cube means, each query block's own cube
+    has the highest block score."""
+    w = Workload("t", Problem(1, 2, 2, 64, 4, 8, 8, 2, 4, 4, 1, 2, 2, F32), Selection(0, 4), 77)
+    x = make_inputs(w, shared_mean=True)
+    r = oracle.route(x["q"], x["k"], w.problem, w.select)
+    sc = r["scores"].reshape(2, w.problem.N, w.problem.N)
+    assert (sc.argmax(-1) == np.arange(w.problem.N)).all()
+
+
+# ---------------------------------------------------------------- selection
+
+def test_topk_matches_lexsort_and_ties_take_lowest_index():
+    rng = np.random.default_rng(9)
+    s = rng.random((50, 37))
+    s[3, [4, 9, 20]] = 0.99999          # exact ties at the top
+    s[4, :] = 0.5                         # all tied
+    counts, idx = oracle.select_rows(s, Selection(0, 5))
+    assert (counts == 5).all()
+    s32 = s.astype(np.float32)
+    for r in range(50):
+        order = np.lexsort((np.arange(37), -s32[r].astype(np.float64)))
+        assert np.array_equal(idx[r, :5], np.sort(order[:5]))
+        assert (idx[r, 5:] == -1).all()
+    assert np.array_equal(idx[4, :5], np.arange(5))
+    assert {4, 9, 20} <= set(idx[3, :5])
+    c2, i2 = oracle.select_rows(s, Selection(0, 100))   # k > N keeps all
+    assert (c2 == 37).all() and np.array_equal(i2[0], np.arange(37))
+
+
+def test_topk_decides_in_fp32():
+    """Scores equal after fp32 rounding tie, and the lower index wins."""
+    a = np.float64(np.float32(0.3))
+    s = np.array([[a, a + 1e-12, 0.1]])
+    _, idx = oracle.select_rows(s, Selection(0, 1))
+    assert idx[0, 0] == 0
+
+
+@pytest.mark.parametrize("mass,cap", [(0.9, 1000), (0.5, 1000), (0.9, 3), (1.0, 1000)])
+def test_mass_selection_invariants(mass, cap):
+    rng = np.random.default_rng(10)
+    s = rng.lognormal(0, 2, (40, 64))
+    counts, idx = oracle.select_rows(s, Selection(1, 0, mass, cap))
+    s32 = s.astype(np.float32).astype(np.float64)
+    for r in range(40):
+        c = counts[r]
+        sel = idx[r, :c]
+        order = np.lexsort((np.arange(64), -s32[r]))
+        assert np.array_equal(np.sort(order[:c]), sel)
+        total = s32[r].sum()
+        cum = np.cumsum(s32[r][order])
+        c_full = int(np.argmax(cum >= mass * total)) + 1 if (cum >= mass * total).any() else 64
+        assert c == min(c_full, cap)
+        if c < cap:
+            assert s32[r][sel].sum() >= mass * total * (1 - 1e-15)
+            if c > 1:
+                assert cum[c - 2] < mass * total
+
+
+def test_sequence_topk_matches_flat_sort():
+    rng = np.random.default_rng(11)
+    N, k = 12, 3
+    s = rng.random((2, N, N))
+    s[0, 0, :4] = 0.999                      # ties resolved by flat index
+    sel = oracle.select_seq(s, N, k)
+    assert sel.reshape(2, -1).sum(1).tolist() == [N * k, N * k]
+    for b in range(2):
+        flat = s[b].reshape(-1).astype(np.float32).astype(np.float64)
+        order = np.lexsort((np.arange(N * N), -flat))[: N * k]
+        ref = np.zeros(N * N, bool)
+        ref[order] = True
+        assert np.array_equal(sel[b].reshape(-1), ref)
+
+
+def test_csc_is_transpose_of_csr():
+    p = small(hq=4, hkv=2, D=8)
+    rng = np.random.default_rng(12)
+    counts = rng.integers(0, p.N + 1, p.batch * p.heads_q * p.N).astype(np.int32)
+    lists = [np.sort(rng.choice(p.N, c, replace=False)).astype(np.int32) for c in counts]
+    idx = np.full((counts.size, p.N), -1, np.int32)
+    for r, l in enumerate(lists):
+        idx[r, :l.size] = l
+    rp, ci = oracle.csr_from_selection(counts, idx)
+    kp, ki = oracle.csr_to_csc(rp, ci, p)
+    grp = p.heads_q // p.heads_kv
+    pairs = set()
+    for hkv in range(p.heads_kv):
+        for nk in range(p.N):
+            row = hkv * p.N + nk
+            ent = ki[kp[row]:kp[row + 1]]
+            assert np.all(np.diff(ent) > 0)
+            for e in ent:
+                pairs.add((hkv * grp + e // p.N, e % p.N, nk))
+    ref = {(r // p.N, r % p.N, c) for r in range(counts.size) for c in lists[r]}
+    assert pairs == ref
+
+
+# ---------------------------------------------------------------- attention
+
+def _block_mask(p, row_ptr, col_idx):
+    """Token-level boolean mask [b, Hq, L, L] of the selected block pairs."""
+    M = np.zeros((p.batch * p.heads_q, p.N, p.N), bool)
+    for r in range(p.batch * p.heads_q * p.N):
+        M[r // p.N, r % p.N, col_idx[row_ptr[r]:row_ptr[r + 1]]] = True
+    M = np.repeat(np.repeat(M, p.B, 1), p.B, 2)
+    return M.reshape(p.batch, p.heads_q, p.L, p.L)
+
+
+def _torch_ref(q, k, v, p, mask, do=None):
+    grp = p.heads_q // p.heads_kv
+    tq = torch.tensor(q, dtype=torch.float64, requires_grad=True)
+    tk = torch.tensor(k, dtype=torch.float64, requires_grad=True)
+    tv = torch.tensor(v, dtype=torch.float64, requires_grad=True)
+    kk = tk.repeat_interleave(grp, 1)
+    vv = tv.repeat_interleave(grp, 1)
+    o = torch.nn.functional.scaled_dot_product_attention(
+        tq, kk, vv, attn_mask=None if mask is None else torch.from_numpy(mask))
+    s = (tq @ kk.transpose(-1, -2)) / math.sqrt(p.head_dim)
+    if mask is not None:
+        s = s.masked_fill(~torch.from_numpy(mask), float("-inf"))
+    lse = torch.logsumexp(s, -1)
+    grads = None
+    if do is not None:
+        o.backward(torch.from_numpy(do.astype(np.float64)))
+        grads = (tq.grad.numpy(), tk.grad.numpy(), tv.grad.numpy())
+    return o.detach().numpy(), lse.detach().numpy(), grads
+
+
+def _full_csr(p):
+    nrows = p.batch * p.heads_q * p.N
+    rp = (np.arange(nrows + 1) * p.N).astype(np.int32)
+    ci = np.tile(np.arange(p.N), nrows).astype(np.int32)
+    return rp, ci
+
+
+def _random_csr(p, seed, kmin=1):
+    rng = np.random.default_rng(seed)
+    nrows = p.batch * p.heads_q * p.N
+    counts = rng.integers(kmin, p.N + 1, nrows)
+    lists = [np.sort(rng.choice(p.N, c, replace=False)) for c in counts]
+    rp = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    return rp, np.concatenate(lists).astype(np.int32)
+
+
+def test_fwd_all_blocks_is_full_attention():
+    p = small(T=2, H=8, W=8, Bt=2, Bh=2, Bw=4, D=16)
+    q, k, v, _ = rand_qkv(p, 13)
+    rp, ci = _full_csr(p)
+    o, lse = oracle.attn_fwd(q, k, v, p, rp, ci)
+    ref, lref, _ = _torch_ref(q, k, v, p, None)
+    np.testing.assert_allclose(o.reshape(ref.shape), ref, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(lse.reshape(lref.shape), lref, rtol=1e-13)
+
+
+@pytest.mark.parametrize("hq,hkv", [(2, 2), (4, 2)])
+def test_fwd_sparse_equals_dense_masked_softmax(hq, hkv):
+    """The gathered form equals Softmax(S + M) V with M = -inf off the
+    selected blocks (the paper's masked attention, Sec. 2.1)."""
+    p = small(T=2, H=8, W=8, Bt=2, Bh=2, Bw=4, hq=hq, hkv=hkv, D=16)
+    q, k, v, _ = rand_qkv(p, 14)
+    rp, ci = _random_csr(p, 15)
+    o, lse = oracle.attn_fwd(q, k, v, p, rp, ci)
+    ref, lref, _ = _torch_ref(q, k, v, p, _block_mask(p, rp, ci))
+    np.testing.assert_allclose(o.reshape(ref.shape), ref, rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(lse.reshape(lref.shape), lref, rtol=1e-12)
+
+
+def test_fwd_special_values():
+    p = small(T=2, H=8, W=8, Bt=2, Bh=2, Bw=4, D=8)
+    q, k, v, _ = rand_qkv(p, 16)
+    rp, ci = _random_csr(p, 17)
+    vc = np.broadcast_to(np.arange(p.head_dim, dtype=np.float32), v.shape).copy()
+    o, _ = oracle.attn_fwd(q, k, vc, p, rp, ci)
+    np.testing.assert_allclose(o, np.broadcast_to(np.arange(p.head_dim), o.shape), atol=1e-12)
+    o0, lse0 = oracle.attn_fwd(np.zeros_like(q), k, v, p, rp, ci)
+    for r in range(p.batch * p.heads_q * p.N):
+        sel = ci[rp[r]:rp[r + 1]]
+        keys = np.concatenate([np.arange(s * p.B, s * p.B + p.B) for s in sel])
+        h = (r // p.N) % p.heads_q
+        np.testing.assert_allclose(o0[r], np.broadcast_to(v[0, h, keys].astype(np.float64).mean(0),
+                                                          o0[r].shape), atol=1e-12)
+        np.testing.assert_allclose(lse0[r], math.log(keys.size), rtol=1e-14)
+    # empty selection: O = 0, LSE = -inf
+    rp_e = np.zeros(p.batch * p.heads_q * p.N + 1, np.int32)
+    oe, le = oracle.attn_fwd(q, k, v, p, rp_e, np.zeros(0, np.int32))
+    assert (oe == 0).all() and np.isneginf(le).all()
+
+
+@pytest.mark.parametrize("hq,hkv", [(2, 2), (4, 2)])
+def test_bwd_matches_autograd_of_masked_attention(hq, hkv):
+    p = small(T=2, H=8, W=8, Bt=2, Bh=2, Bw=4, hq=hq, hkv=hkv, D=16)
+    q, k, v, do = rand_qkv(p, 18)
+    rp, ci = _random_csr(p, 19)
+    _, _, (gq, gk, gv) = _torch_ref(q, k, v, p, _block_mask(p, rp, ci), do)
+    dq = oracle.attn_bwd_dq(q, k, v, do, p, rp, ci)
+    dk, dv = oracle.attn_bwd_dkdv(q, k, v, do, p, rp, ci)
+    np.testing.assert_allclose(dq.reshape(gq.shape), gq, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dk.reshape(gk.shape), gk, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dv.reshape(gv.shape), gv, rtol=1e-10, atol=1e-12)
+
+
+def test_bwd_finite_differences():
+    """Central differences of L = sum(dO * O) with the block lists held fixed."""
+    p = Problem(1, 2, 1, 8, 2, 4, 4, 2, 2, 2, 1, 1, 2, BF16)
+    q, k, v, do = rand_qkv(p, 20)
+    rp, ci = _random_csr(p, 21)
+    dq = oracle.attn_bwd_dq(q, k, v, do, p, rp, ci).reshape(q.shape)
+    dk, dv = oracle.attn_bwd_dkdv(q, k, v, do, p, rp, ci)
+    dk, dv = dk.reshape(k.shape), dv.reshape(v.shape)
+
+    def loss(qq, kk, vv):
+        o, _ = oracle.attn_fwd(qq, kk, vv, p, rp, ci)
+        return float((o.reshape(qq.shape) * do.astype(np.float64)).sum())
+
+    h = 2.0 ** -10     # bf16 inputs +/- h stay exact in float32
+    rng = np.random.default_rng(22)
+    for name, t, g in (("q", q, dq), ("k", k, dk), ("v", v, dv)):
+        for flat in rng.choice(t.size, 12, replace=False):
+            tp, tm = t.copy(), t.copy()
+            tp.flat[flat] += np.float32(h)
+            tm.flat[flat] -= np.float32(h)
+            args_p = {"q": q, "k": k, "v": v, name: tp}
+            args_m = {"q": q, "k": k, "v": v, name: tm}
+            fd = (loss(args_p["q"], args_p["k"], args_p["v"]) -
+                  loss(args_m["q"], args_m["k"], args_m["v"])) / (2 * h)
+            assert abs(fd - g.flat[flat]) <= 1e-5 * max(1.0, abs(g).max()), (name, flat)
+
+
+def test_bwd_sum_invariants():
+    """Rows of P sum to 1: sum_j dV_j = sum_i dO_i; rows of dS sum to 0:
+    sum_j dK_j = 0 (per head, MHA)."""
+    p = small(T=2, H=8, W=8, Bt=2, Bh=2, Bw=4, D=16)
+    q, k, v, do = rand_qkv(p, 23)
+    rp, ci = _random_csr(p, 24)
+    dk, dv = oracle.attn_bwd_dkdv(q, k, v, do, p, rp, ci)
+    dk = dk.reshape(p.heads_kv, -1, p.head_dim)
+    dv = dv.reshape(p.heads_kv, -1, p.head_dim)
+    np.testing.assert_allclose(dv.sum(1), do[0].astype(np.float64).sum(1), rtol=1e-10, atol=1e-10)
+    np.testing.assert_allclose(dk.sum(1), 0.0, atol=1e-10)
+
+
+# ---------------------------------------------------------------- paper table
+
+def test_appendix_b_sparsity_reproduces_table2():
+    """Appendix B's model 1 - (1/R^2 + K*B/L) gives Table 2's sparsity column
+    with block B = 128 tokens and router pool R = 8 tokens (token counts from
+    the evaluation setup, Sec. 3)."""
+    with open(os.path.join(HERE, "golden", "table2_sparsity.json")) as f:
+        g = json.load(f)
+    for row in g["rows"]:
+        s = 1.0 - (1.0 / g["R"] ** 2 + row["topk"] * g["B"] / row["tokens"])
+        assert round(s, 2) == row["sparsity"], row
+
+
+def test_mass_threshold_reached_exactly():
+    """The prefix stops at the first count whose sum reaches (>=) the
+    threshold; dyadic scores make the sums exact."""
+    s = np.array([[0.25, 0.5, 0.125, 0.125], [0.125, 0.125, 0.25, 0.5]])
+    counts, idx = oracle.select_rows(s, Selection(1, 0, 0.75, 10))
+    assert counts.tolist() == [2, 2]
+    assert idx[0, :2].tolist() == [0, 1] and idx[1, :2].tolist() == [2, 3]
+    counts, _ = oracle.select_rows(s, Selection(1, 0, 0.875, 10))
+    assert counts.tolist() == [3, 3]

@@ -1,0 +1,232 @@
+"""Seeded synthetic workloads for the VSA2 routed sparse-attention path.
+
+This module only describes problem shapes and draws inputs.  It holds none of
+the method's arithmetic (no pooling, scoring, selection or attention), so both
+the HIP path and the CPU oracle may take their inputs from it.
+
+The paper trains on VAE video latents that are not available here; these
+seeded tensors stand in for them.  Recipe (per tensor X in {Q, K, V} and per
+(batch, head of that tensor, cube)):
+
+    X[token] = mu[cube] + 0.5 * eps[token],   eps ~ N(0, 1) iid per element,
+    mu[cube] ~ N(0, I_D)                       (independent per tensor),
+    mu[cube] *= exp(xi[cube]), xi ~ N(0, 1)    (log-normal cube norms, "skewed"),
+
+so tokens of one cube share a mean and routing has signal.  dO ~ N(0, 1).
+All draws are float32, then rounded to the problem dtype (bf16 with
+round-to-nearest-even); the rounded values are the inputs of both sides.
+Tensors are produced directly in cube-major order [batch, head, L, D],
+L = N * B (every per-element draw is iid, so drawing in cube-major order is
+the same distribution as drawing in raster order and permuting).
+
+Streams: every (tensor, batch, head) slab has its own generator,
+numpy PCG64 seeded with SeedSequence([base_seed, tensor_id, b, h]), so the
+result does not depend on the thread count that draws it.
+"""
+from __future__ import annotations
+
+import dataclasses
+import os
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+F32, BF16 = 0, 1
+DTYPE_NAMES = {F32: "f32", BF16: "bf16"}
+
+
+@dataclasses.dataclass(frozen=True)
+class Problem:
+    """Shape of one routed sparse-attention call (notation of the paper's
+    Table 1: grid T x H x W, cube B = Bt*Bh*Bw, router pool R = Rt*Rh*Rw)."""
+    batch: int
+    heads_q: int
+    heads_kv: int
+    head_dim: int
+    T: int
+    H: int
+    W: int
+    Bt: int = 4
+    Bh: int = 4
+    Bw: int = 4
+    Rt: int = 2
+    Rh: int = 2
+    Rw: int = 2
+    dtype: int = BF16
+
+    @property
+    def L(self) -> int:
+        return self.T * self.H * self.W
+
+    @property
+    def B(self) -> int:
+        return self.Bt * self.Bh * self.Bw
+
+    @property
+    def N(self) -> int:
+        return (self.T // self.Bt) * (self.H // self.Bh) * (self.W // self.Bw)
+
+    @property
+    def R(self) -> int:
+        return self.Rt * self.Rh * self.Rw
+
+    @property
+    def G(self) -> int:
+        return (self.Bt // self.Rt) * (self.Bh // self.Rh) * (self.Bw // self.Rw)
+
+    def replace(self, **kw) -> "Problem":
+        return dataclasses.replace(self, **kw)
+
+
+@dataclasses.dataclass(frozen=True)
+class Selection:
+    """Selection rule: mode 0 = top-k per query block, 1 = smallest prefix
+    reaching `mass` of the row's score total, capped at `cap` blocks."""
+    mode: int = 0
+    k: int = 8
+    mass: float = 0.9
+    cap: int = 0
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    problem: Problem
+    select: Selection
+    seed: int
+    skewed: bool = False       # log-normal cube-mean norms
+    backward: bool = True
+
+
+# The five shapes of the routed-attention benchmark suite.
+WORKLOADS = {
+    "tiny": Workload(
+        "tiny", Problem(1, 2, 2, 64, 8, 16, 16, dtype=F32), Selection(0, 8), 1000,
+        backward=False),
+    "480p": Workload(
+        "480p", Problem(1, 12, 12, 128, 20, 32, 56), Selection(0, 70), 1001, backward=False),
+    "720p": Workload(
+        "720p", Problem(1, 40, 40, 128, 20, 48, 80), Selection(0, 120), 1002),
+    "720p-mass": Workload(
+        "720p-mass", Problem(1, 40, 40, 128, 20, 48, 80), Selection(1, 0, 0.9, 240), 1003,
+        skewed=True),
+    "gqa-long": Workload(
+        "gqa-long", Problem(1, 40, 8, 128, 40, 48, 80), Selection(0, 120), 1004),
+}
+
+
+def round_bf16_f32(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to bfloat16 (round-to-nearest-even), returned as
+    float32 holding the rounded values.  Input preparation only."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32)
+    rounded = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) & np.uint32(0xFFFF0000)
+    # keep NaN/inf patterns untouched (not produced by these generators)
+    special = (u & np.uint32(0x7F800000)) == np.uint32(0x7F800000)
+    rounded = np.where(special, u & np.uint32(0xFFFF0000), rounded)
+    return rounded.view(np.float32)
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Upper 16 bits of float32 values that are already bf16-representable."""
+    return (np.ascontiguousarray(x, dtype=np.float32).view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+
+
+def _slab(seed: int, tensor_id: int, b: int, h: int, N: int, B: int, D: int,
+          with_mean: bool, skewed: bool, out: np.ndarray) -> None:
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, tensor_id, b, h])))
+    if with_mean:
+        mu = rng.standard_normal((N, D), dtype=np.float32)
+        if skewed:
+            xi = rng.standard_normal((N, 1), dtype=np.float32)
+            mu *= np.exp(xi)
+        eps = rng.standard_normal((N, B, D), dtype=np.float32)
+        eps *= np.float32(0.5)
+        eps += mu[:, None, :]
+        out[...] = eps.reshape(N * B, D)
+    else:
+        out[...] = rng.standard_normal((N * B, D), dtype=np.float32)
+
+
+def make_tensor(p: Problem, seed: int, tensor_id: int, heads: int, with_mean: bool = True,
+                skewed: bool = False, threads: int | None = None) -> np.ndarray:
+    """One [batch, heads, L, D] float32 tensor of the recipe above, rounded to
+    the problem dtype.  tensor_id: 0 = Q, 1 = K, 2 = V, 3 = dO."""
+    out = np.empty((p.batch, heads, p.L, p.head_dim), dtype=np.float32)
+    jobs = [(b, h) for b in range(p.batch) for h in range(heads)]
+    nthr = threads or min(16, os.cpu_count() or 1)
+
+    def work(bh):
+        b, h = bh
+        _slab(seed, tensor_id, b, h, p.N, p.B, p.head_dim, with_mean, skewed, out[b, h])
+        if p.dtype == BF16:
+            out[b, h] = round_bf16_f32(out[b, h])
+
+    if nthr > 1 and len(jobs) > 1:
+        with ThreadPoolExecutor(nthr) as ex:
+            list(ex.map(work, jobs))
+    else:
+        for j in jobs:
+            work(j)
+    return out
+
+
+def make_inputs(w: Workload, with_grad: bool | None = None, threads: int | None = None,
+                shared_mean: bool = False) -> dict:
+    """Q, K, V (and dO when the workload has a backward pass) for workload w.
+
+    shared_mean=True gives Q, K and V of a head the same cube means (one draw,
+    the K/V heads of a GQA group take their first query head's means); then
+    every query block's own cube is its best match, which makes a cheap router
+    sanity check."""
+    p = w.problem
+    q = make_tensor(p, w.seed, 0, p.heads_q, True, w.skewed, threads)
+    if shared_mean:
+        if p.heads_q != p.heads_kv or w.skewed:
+            raise ValueError("shared_mean needs heads_q == heads_kv and unskewed means")
+        k = _with_means_of(q, p, w.seed, 1, threads)
+        v = _with_means_of(q, p, w.seed, 2, threads)
+    else:
+        k = make_tensor(p, w.seed, 1, p.heads_kv, True, w.skewed, threads)
+        v = make_tensor(p, w.seed, 2, p.heads_kv, True, w.skewed, threads)
+    out = {"q": q, "k": k, "v": v}
+    if with_grad if with_grad is not None else w.backward:
+        out["do"] = make_tensor(p, w.seed, 3, p.heads_q, False, False, threads)
+    return out
+
+
+def _with_means_of(ref: np.ndarray, p: Problem, seed: int, tensor_id: int, threads) -> np.ndarray:
+    """Tensor whose cube means are those of `ref` (up to its noise), fresh
+    0.5*N(0,1) token noise.  The cube mean is recovered exactly from ref's
+    generator stream, not estimated."""
+    out = np.empty_like(ref)
+    for b in range(p.batch):
+        for h in range(ref.shape[1]):
+            rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0, b, h])))
+            mu = rng.standard_normal((p.N, p.head_dim), dtype=np.float32)
+            rng2 = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, tensor_id, b, h])))
+            eps = rng2.standard_normal((p.N, p.B, p.head_dim), dtype=np.float32) * np.float32(0.5)
+            x = (eps + mu[:, None, :]).reshape(p.L, p.head_dim)
+            out[b, h] = round_bf16_f32(x) if p.dtype == BF16 else x
+    return out
+
+
+def raster_to_cube_major(x: np.ndarray, p: Problem) -> np.ndarray:
+    """[..., T*H*W (raster, w fastest), D] -> [..., N*B (cube-major), D]."""
+    lead = x.shape[:-2]
+    D = x.shape[-1]
+    Nt, Nh, Nw = p.T // p.Bt, p.H // p.Bh, p.W // p.Bw
+    y = x.reshape(*lead, Nt, p.Bt, Nh, p.Bh, Nw, p.Bw, D)
+    nd = len(lead)
+    perm = list(range(nd)) + [nd + 0, nd + 2, nd + 4, nd + 1, nd + 3, nd + 5, nd + 6]
+    return np.ascontiguousarray(y.transpose(perm)).reshape(*lead, p.L, D)
+
+
+def cube_major_to_raster(x: np.ndarray, p: Problem) -> np.ndarray:
+    lead = x.shape[:-2]
+    D = x.shape[-1]
+    Nt, Nh, Nw = p.T // p.Bt, p.H // p.Bh, p.W // p.Bw
+    y = x.reshape(*lead, Nt, Nh, Nw, p.Bt, p.Bh, p.Bw, D)
+    nd = len(lead)
+    perm = list(range(nd)) + [nd + 0, nd + 3, nd + 1, nd + 4, nd + 2, nd + 5, nd + 6]
+    return np.ascontiguousarray(y.transpose(perm)).reshape(*lead, p.L, D)
