@@ -1,0 +1,207 @@
+/*
+ * vsa2.h - C-ABI of the MI355X (gfx950) routed sparse-attention library.
+ *
+ * Implements the data-parallel hot path of VSA2 ("Improving Video Sparse
+ * Attention with Fine-grained Router and Sparse Rebasing"):
+ *
+ *   vsa2_pool      MeanPool over spatio-temporal sub-cubes
+ *                  (Sec. 2.2, Eq. router_start for the router's R-pooling;
+ *                   Eq. compress for the B-pooling of the coarse branch)
+ *   vsa2_route     the fine-grained router: pooled-query x pooled-key
+ *                  softmax, GxG score pooling, per-query-block selection,
+ *                  CSR block lists and their transpose
+ *                  (Sec. 2.2, Eq. router_start .. Eq. router_end)
+ *   vsa2_attn_fwd  block-sparse attention over the selected block pairs
+ *                  (Sec. 2.1 masked attention; Sec. 2.2 Eq. block_sparse)
+ *   vsa2_attn_bwd  its gradients dQ, dK, dV with the block mask held fixed
+ *                  (Sec. 2.1: the routing decision carries no gradient)
+ *
+ * Conventions shared by every call
+ *   Memory     Every tensor pointer is a DEVICE pointer owned by the caller.
+ *              The library never allocates device memory; calls that need
+ *              scratch space take a caller-owned workspace whose size is
+ *              returned by the matching *_workspace query.
+ *   Streams    Work is enqueued asynchronously on the caller's stream; no call
+ *              synchronises the device or reads device memory on the host.
+ *   Errors     Argument errors are detected on the host and returned before
+ *              any device work is enqueued.  A failed launch returns
+ *              VSA2_ERR_HIP.  Nothing is thrown across the ABI.
+ *   Layout     Token tensors are contiguous [batch][heads][L][D] in cube-major
+ *              token order (Sec. 2.2 "Permutation"): L = N*B, token
+ *              l = n*B + beta, cube n = (nt*Nh + nh)*Nw + nw and in-cube
+ *              offset beta = (bt*Bh + bh)*Bw + bw (w fastest at both levels).
+ *              Pointers to tensors are 16-byte aligned.
+ *   Heads      Query head h reads key/value head h / (Hq/Hkv) (Hq % Hkv == 0).
+ *   Block ids  Query-block rows are numbered (b*Hq + h)*N + n; key-block rows
+ *              (b*Hkv + h)*N + n.
+ *   Dtypes     VSA2_F32 or VSA2_BF16 inputs; outputs in the input dtype,
+ *              rounded to nearest even from fp32 accumulators.
+ *   Threads    Calls are thread-safe; the library keeps no mutable state.
+ *   Determinism  Every output is bitwise reproducible for equal inputs.
+ *
+ * Supported shapes (other values return VSA2_ERR_UNSUPPORTED):
+ *   cube B = Bt*Bh*Bw = 64 tokens; head_dim D in {64, 128};
+ *   router score-pooling G = (Bt/Rt)(Bh/Rh)(Bw/Rw) in {1, 2, 4, 8};
+ *   N = L/B <= 4096 cubes.  T, H, W must be multiples of Bt, Bh, Bw
+ *   (VSA2_ERR_SHAPE otherwise).
+ */
+#ifndef VSA2_H
+#define VSA2_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    VSA2_OK = 0,
+    VSA2_ERR_NULL = 1,         /* a required pointer is NULL                   */
+    VSA2_ERR_SHAPE = 2,        /* inconsistent or non-divisible sizes          */
+    VSA2_ERR_DTYPE = 3,        /* dtype is not VSA2_F32 / VSA2_BF16            */
+    VSA2_ERR_SELECT = 4,       /* invalid selection rule                       */
+    VSA2_ERR_CAPACITY = 5,     /* col_cap below what the selection can emit    */
+    VSA2_ERR_ALIGN = 6,        /* a tensor pointer is not 16-byte aligned      */
+    VSA2_ERR_WORKSPACE = 7,    /* workspace missing or smaller than required   */
+    VSA2_ERR_HIP = 8,          /* a HIP launch failed                          */
+    VSA2_ERR_UNSUPPORTED = 9   /* valid but outside the supported shapes       */
+} vsa2_status;
+
+typedef enum { VSA2_F32 = 0, VSA2_BF16 = 1 } vsa2_dtype;
+
+/* Problem shape, in the paper's notation (Table 1): video grid T x H x W
+ * after VAE compression, cube (Bt, Bh, Bw), router input pool (Rt, Rh, Rw). */
+typedef struct {
+    int32_t batch;
+    int32_t heads_q;     /* Hq                                   */
+    int32_t heads_kv;    /* Hkv, divides Hq                      */
+    int32_t head_dim;    /* D                                    */
+    int32_t T, H, W;
+    int32_t Bt, Bh, Bw;
+    int32_t Rt, Rh, Rw;  /* R_x divides B_x                      */
+    int32_t dtype;       /* vsa2_dtype                           */
+} vsa2_problem;
+
+typedef enum {
+    VSA2_SEL_TOPK = 0,   /* the k best key blocks of each query block         */
+    VSA2_SEL_MASS = 1    /* smallest best-first prefix whose score sum reaches
+                            mass * (row total), at most cap blocks            */
+} vsa2_sel_mode;
+
+/* Selection rule over one row of block scores P_r[n_q, :].  Order is
+ * (score desc, key-block index asc), decided on the fp32 scores. */
+typedef struct {
+    int32_t mode;        /* vsa2_sel_mode                                    */
+    int32_t k;           /* TOPK: 1 <= k; k > N keeps every block            */
+    float mass;          /* MASS: 0 < mass <= 1                              */
+    int32_t cap;         /* MASS: 1 <= cap                                   */
+} vsa2_select;
+
+/* Human-readable name of a status code (static string). */
+const char* vsa2_status_str(vsa2_status s);
+
+/*
+ * vsa2_pool - MeanPool over (Pt, Ph, Pw) sub-cubes of every B-cube
+ * (Sec. 2.2: Eq. router_start with P = R gives Q_r, K_r; Eq. compress with
+ * P = B gives the coarse Q_c, K_c, V_c).
+ *   x      [batch][heads][L][D], dtype p->dtype, cube-major.
+ *   out    [batch][heads][N*Gp][D], Gp = (Bt/Pt)(Bh/Ph)(Bw/Pw); row n*Gp + g
+ *          with g = (gt*Gh + gh)*Gw + gw.  Each value is the mean of the
+ *          Pt*Ph*Pw tokens of its sub-cube, accumulated in fp64 and rounded
+ *          (nearest even) to the dtype.
+ *   heads  number of heads of x (Hq for queries, Hkv for keys).
+ * Errors: NULL pointers, P_x not dividing B_x, bad dtype/shape, misalignment.
+ */
+vsa2_status vsa2_pool(const vsa2_problem* p, int32_t heads, const void* x,
+                      int32_t Pt, int32_t Ph, int32_t Pw, void* out, hipStream_t stream);
+
+/* Largest number of (query block, key block) pairs the rule can select:
+ * batch*Hq*N*min(k, N) for TOPK, batch*Hq*N*min(cap, N) for MASS.  col_cap
+ * of vsa2_route, and the CSC entry capacity, must be at least this. */
+vsa2_status vsa2_route_capacity(const vsa2_problem* p, const vsa2_select* s, int64_t* pairs);
+
+/* Bytes of workspace vsa2_route needs for this problem and rule. */
+vsa2_status vsa2_route_workspace(const vsa2_problem* p, const vsa2_select* s, size_t* bytes);
+
+/*
+ * vsa2_route - the fine-grained router (Sec. 2.2, Eq. router_start ..
+ * Eq. router_end) followed by selection and the sparse block lists.
+ *   q_r    [batch][Hq][N*G][D]  pooled queries (vsa2_pool with P = R).
+ *   k_r    [batch][Hkv][N*G][D] pooled keys.
+ *   For pooled query i and every pooled key j of the matching KV head:
+ *     s_ij = q_r[i].k_r[j] / sqrt(D), softmax over all N*G keys j, and
+ *     P_r[n_q, n_k] = (1/G^2) * sum over the G x G pooled pairs of the two
+ *     blocks (so every row of P_r sums to 1/G).  Two passes over the logits
+ *     (row log-sum-exp, then softmax + pooling); P_hat is never stored.
+ *   Selection per query block n_q over P_r[n_q, :] by the rule *s.
+ *   row_ptr [batch*Hq*N + 1]  CSR offsets (row_ptr[0] = 0).
+ *   col_idx [col_cap]         selected key blocks, ascending within a row.
+ *   kv_ptr  [batch*Hkv*N + 1] CSC offsets over key-block rows, or NULL.
+ *   kv_idx  [col_cap]         for each key block, the query blocks that
+ *                             selected it, value hq_local*N + n_q with
+ *                             hq_local = h mod (Hq/Hkv), ordered ascending;
+ *                             NULL together with kv_ptr to skip the CSC.
+ *   block_scores  optional [batch][Hq][N][N] fp32 output of P_r; NULL keeps
+ *                 the scores in the workspace only.
+ *   ws, ws_bytes  workspace of at least vsa2_route_workspace bytes.
+ * The number of selected pairs is row_ptr[batch*Hq*N] (device memory).
+ * Errors: NULL pointers, bad rule (k < 1, mass outside (0,1], cap < 1),
+ * col_cap below vsa2_route_capacity, small workspace, unsupported G or N.
+ */
+vsa2_status vsa2_route(const vsa2_problem* p, const vsa2_select* s,
+                       const void* q_r, const void* k_r,
+                       int32_t* row_ptr, int32_t* col_idx, int64_t col_cap,
+                       int32_t* kv_ptr, int32_t* kv_idx,
+                       float* block_scores, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Bytes of workspace vsa2_attn_fwd (pass 0) or vsa2_attn_bwd (pass 1) needs. */
+vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* bytes);
+
+/*
+ * vsa2_attn_fwd - block-sparse attention (Sec. 2.1 with a block mask M,
+ * Eq. block_sparse): for query token l of block n_q, the softmax of
+ * q_l.k_j / sqrt(D) over the keys j of the key blocks listed in CSR row
+ * n_q, times V.
+ *   q [batch][Hq][L][D], k, v [batch][Hkv][L][D]   (dtype p->dtype)
+ *   row_ptr, col_idx   CSR as produced by vsa2_route; entries outside
+ *                      [0, N) and offsets outside [0, col_cap] are skipped
+ *                      (clamped), never dereferenced.
+ *   o   [batch][Hq][L][D] output, dtype p->dtype.
+ *   lse [batch][Hq][L] fp32 natural-log log-sum-exp of each query's scaled
+ *       scores; a query block with no selected block gets o = 0, lse = -inf.
+ * Errors: NULL pointers, shape/dtype, misalignment, small workspace.
+ */
+vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, const void* v,
+                          const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
+                          void* o, float* lse, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * vsa2_attn_bwd - gradients of vsa2_attn_fwd with the block lists fixed
+ * (no gradient reaches the router, Sec. 2.1).  With p the softmax row of
+ * query l over its gathered keys:
+ *   Delta_l = dO_l . O_l,  dS_lj = p_lj (dO_l . v_j - Delta_l),
+ *   dQ_l = sum_j dS_lj k_j / sqrt(D),
+ *   dK_j = sum_l dS_lj q_l / sqrt(D),  dV_j = sum_l p_lj dO_l,
+ * where the sums over l run over every query (of every query head of the KV
+ * group) whose block selected j's block.
+ *   q, k, v, o, lse   as for vsa2_attn_fwd (o, lse from the forward call)
+ *   dout  [batch][Hq][L][D]  dO
+ *   row_ptr, col_idx  the CSR; kv_ptr, kv_idx its transpose (vsa2_route)
+ *   dq [batch][Hq][L][D], dk, dv [batch][Hkv][L][D]  outputs, dtype p->dtype;
+ *   key blocks no query selected get dk = dv = 0.
+ * Errors: as for vsa2_attn_fwd.
+ */
+vsa2_status vsa2_attn_bwd(const vsa2_problem* p, const void* q, const void* k, const void* v,
+                          const void* o, const float* lse, const void* dout,
+                          const int32_t* row_ptr, const int32_t* col_idx,
+                          const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
+                          void* dq, void* dk, void* dv, void* ws, size_t ws_bytes,
+                          hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VSA2_H */

@@ -1,0 +1,248 @@
+// The public C-ABI (vsa2.h): argument validation, workspace layout and the
+// launch sequence of each call.  Every check runs on the host before any
+// device work is enqueued; no call allocates, synchronises or reads device
+// memory.
+#include "vsa2.h"
+
+#include <math.h>
+
+#include "internal.hpp"
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct shape {
+    int64_t N, L, B, G, rows_q, rows_kv;
+};
+
+// Structural checks shared by all calls.
+vsa2_status check_problem(const vsa2_problem* p, shape* out) {
+    if (!p) return VSA2_ERR_NULL;
+    if (p->dtype != VSA2_F32 && p->dtype != VSA2_BF16) return VSA2_ERR_DTYPE;
+    if (p->batch < 1 || p->heads_q < 1 || p->heads_kv < 1 || p->head_dim < 1) return VSA2_ERR_SHAPE;
+    if (p->heads_q % p->heads_kv) return VSA2_ERR_SHAPE;
+    if (p->T < 1 || p->H < 1 || p->W < 1 || p->Bt < 1 || p->Bh < 1 || p->Bw < 1) return VSA2_ERR_SHAPE;
+    if (p->Rt < 1 || p->Rh < 1 || p->Rw < 1) return VSA2_ERR_SHAPE;
+    if (p->T % p->Bt || p->H % p->Bh || p->W % p->Bw) return VSA2_ERR_SHAPE;
+    if (p->Bt % p->Rt || p->Bh % p->Rh || p->Bw % p->Rw) return VSA2_ERR_SHAPE;
+    shape s;
+    s.B = static_cast<int64_t>(p->Bt) * p->Bh * p->Bw;
+    s.N = static_cast<int64_t>(p->T / p->Bt) * (p->H / p->Bh) * (p->W / p->Bw);
+    s.L = s.N * s.B;
+    s.G = static_cast<int64_t>(p->Bt / p->Rt) * (p->Bh / p->Rh) * (p->Bw / p->Rw);
+    s.rows_q = static_cast<int64_t>(p->batch) * p->heads_q * s.N;
+    s.rows_kv = static_cast<int64_t>(p->batch) * p->heads_kv * s.N;
+    if (s.N > (1 << 26) || s.rows_q > (int64_t(1) << 31) - 2) return VSA2_ERR_SHAPE;
+    *out = s;
+    return VSA2_OK;
+}
+
+// Shapes the attention and router kernels are built for.
+vsa2_status check_kernel_shape(const vsa2_problem* p, const shape& s) {
+    if (s.B != 64) return VSA2_ERR_UNSUPPORTED;
+    if (p->head_dim != 64 && p->head_dim != 128) return VSA2_ERR_UNSUPPORTED;
+    return VSA2_OK;
+}
+
+vsa2_status check_select(const vsa2_select* sel) {
+    if (!sel) return VSA2_ERR_NULL;
+    if (sel->mode == VSA2_SEL_TOPK) return sel->k >= 1 ? VSA2_OK : VSA2_ERR_SELECT;
+    if (sel->mode == VSA2_SEL_MASS) {
+        if (!(sel->mass > 0.f && sel->mass <= 1.f)) return VSA2_ERR_SELECT;
+        return sel->cap >= 1 ? VSA2_OK : VSA2_ERR_SELECT;
+    }
+    return VSA2_ERR_SELECT;
+}
+
+int64_t keep_per_row(const vsa2_select* sel, int64_t N) {
+    const int64_t k = sel->mode == VSA2_SEL_TOPK ? sel->k : sel->cap;
+    return k < N ? k : N;
+}
+
+struct route_ws {
+    size_t lse2, scores, counts, mask, kv_counts, total;
+};
+
+route_ws route_layout(const vsa2_problem* p, const shape& s) {
+    route_ws w;
+    size_t at = 0;
+    const int64_t words = (static_cast<int64_t>(p->heads_q / p->heads_kv) * s.N + 31) / 32;
+    w.lse2 = at;      at = align_up(at + sizeof(float) * static_cast<size_t>(s.rows_q * s.G));
+    w.scores = at;    at = align_up(at + sizeof(float) * static_cast<size_t>(s.rows_q * s.N));
+    w.counts = at;    at = align_up(at + sizeof(int32_t) * static_cast<size_t>(s.rows_q));
+    w.mask = at;      at = align_up(at + sizeof(uint32_t) * static_cast<size_t>(s.rows_kv * words));
+    w.kv_counts = at; at = align_up(at + sizeof(int32_t) * static_cast<size_t>(s.rows_kv));
+    w.total = at;
+    return w;
+}
+
+size_t bwd_ws_bytes(const shape& s, const vsa2_problem* p) {
+    return align_up(sizeof(float) * static_cast<size_t>(s.rows_q * s.B)) + (p ? 0 : 0);
+}
+
+#define VSA2_TRY_HIP(expr)                          \
+    do {                                            \
+        if ((expr) != hipSuccess) return VSA2_ERR_HIP; \
+    } while (0)
+
+}  // namespace
+
+extern "C" {
+
+const char* vsa2_status_str(vsa2_status s) {
+    switch (s) {
+        case VSA2_OK: return "ok";
+        case VSA2_ERR_NULL: return "null pointer";
+        case VSA2_ERR_SHAPE: return "invalid or inconsistent shape";
+        case VSA2_ERR_DTYPE: return "unsupported dtype";
+        case VSA2_ERR_SELECT: return "invalid selection rule";
+        case VSA2_ERR_CAPACITY: return "column capacity too small";
+        case VSA2_ERR_ALIGN: return "pointer not 16-byte aligned";
+        case VSA2_ERR_WORKSPACE: return "workspace missing or too small";
+        case VSA2_ERR_HIP: return "HIP launch failed";
+        case VSA2_ERR_UNSUPPORTED: return "shape outside the supported kernel configurations";
+    }
+    return "unknown status";
+}
+
+vsa2_status vsa2_pool(const vsa2_problem* p, int32_t heads, const void* x, int32_t Pt, int32_t Ph,
+                      int32_t Pw, void* out, hipStream_t stream) {
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if (!x || !out) return VSA2_ERR_NULL;
+    if (heads < 1 || Pt < 1 || Ph < 1 || Pw < 1) return VSA2_ERR_SHAPE;
+    if (p->Bt % Pt || p->Bh % Ph || p->Bw % Pw) return VSA2_ERR_SHAPE;
+    if (p->head_dim % 8) return VSA2_ERR_UNSUPPORTED;
+    if (!aligned16(x) || !aligned16(out)) return VSA2_ERR_ALIGN;
+    VSA2_TRY_HIP(vsa2::launch_pool(p->dtype, x, out, static_cast<int64_t>(p->batch) * heads,
+                                   static_cast<int>(s.N), p->head_dim, p->Bt, p->Bh, p->Bw, Pt, Ph, Pw,
+                                   stream));
+    return VSA2_OK;
+}
+
+vsa2_status vsa2_route_capacity(const vsa2_problem* p, const vsa2_select* sel, int64_t* pairs) {
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if ((st = check_select(sel)) != VSA2_OK) return st;
+    if (!pairs) return VSA2_ERR_NULL;
+    *pairs = s.rows_q * keep_per_row(sel, s.N);
+    return VSA2_OK;
+}
+
+vsa2_status vsa2_route_workspace(const vsa2_problem* p, const vsa2_select* sel, size_t* bytes) {
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if ((st = check_select(sel)) != VSA2_OK) return st;
+    if (!bytes) return VSA2_ERR_NULL;
+    *bytes = route_layout(p, s).total;
+    return VSA2_OK;
+}
+
+vsa2_status vsa2_route(const vsa2_problem* p, const vsa2_select* sel, const void* q_r, const void* k_r,
+                       int32_t* row_ptr, int32_t* col_idx, int64_t col_cap, int32_t* kv_ptr,
+                       int32_t* kv_idx, float* block_scores, void* ws, size_t ws_bytes,
+                       hipStream_t stream) {
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if ((st = check_select(sel)) != VSA2_OK) return st;
+    if ((st = check_kernel_shape(p, s)) != VSA2_OK) return st;
+    if (s.G != 1 && s.G != 2 && s.G != 4 && s.G != 8) return VSA2_ERR_UNSUPPORTED;
+    if (s.N > 4096) return VSA2_ERR_UNSUPPORTED;
+    if (!q_r || !k_r || !row_ptr || !col_idx) return VSA2_ERR_NULL;
+    if ((kv_ptr == nullptr) != (kv_idx == nullptr)) return VSA2_ERR_NULL;
+    if (!aligned16(q_r) || !aligned16(k_r)) return VSA2_ERR_ALIGN;
+    const int64_t keep = keep_per_row(sel, s.N);
+    if (col_cap < s.rows_q * keep) return VSA2_ERR_CAPACITY;
+    const route_ws w = route_layout(p, s);
+    if (!ws || ws_bytes < w.total) return VSA2_ERR_WORKSPACE;
+    if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
+    char* base = static_cast<char*>(ws);
+    float* lse2 = reinterpret_cast<float*>(base + w.lse2);
+    float* scores = block_scores ? block_scores : reinterpret_cast<float*>(base + w.scores);
+    int32_t* counts = reinterpret_cast<int32_t*>(base + w.counts);
+    const int N = static_cast<int>(s.N);
+
+    VSA2_TRY_HIP(vsa2::launch_route_passes(p->dtype, p->head_dim, static_cast<int>(s.G), q_r, k_r, lse2,
+                                           scores, p->batch, p->heads_q, p->heads_kv, N, stream));
+    if (sel->mode == VSA2_SEL_TOPK) {
+        VSA2_TRY_HIP(vsa2::launch_uniform_ptr(row_ptr, s.rows_q, static_cast<int>(keep), stream));
+    } else {
+        VSA2_TRY_HIP(vsa2::launch_select(0, scores, s.rows_q, N, sel->mode, sel->k, sel->mass, sel->cap,
+                                         counts, nullptr, nullptr, col_cap, stream));
+        VSA2_TRY_HIP(vsa2::launch_scan(counts, s.rows_q, row_ptr, stream));
+    }
+    VSA2_TRY_HIP(vsa2::launch_select(1, scores, s.rows_q, N, sel->mode, sel->k, sel->mass, sel->cap,
+                                     counts, row_ptr, col_idx, col_cap, stream));
+    if (kv_ptr) {
+        VSA2_TRY_HIP(vsa2::launch_csc(row_ptr, col_idx, p->batch, p->heads_q, p->heads_kv, N, col_cap,
+                                      reinterpret_cast<uint32_t*>(base + w.mask),
+                                      reinterpret_cast<int32_t*>(base + w.kv_counts), kv_ptr, kv_idx,
+                                      stream));
+    }
+    return VSA2_OK;
+}
+
+vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* bytes) {
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if (!bytes) return VSA2_ERR_NULL;
+    if (pass == 0) *bytes = 0;
+    else if (pass == 1) *bytes = bwd_ws_bytes(s, p);
+    else return VSA2_ERR_SHAPE;
+    return VSA2_OK;
+}
+
+vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, const void* v,
+                          const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
+                          float* lse, void* ws, size_t ws_bytes, hipStream_t stream) {
+    (void)ws;
+    (void)ws_bytes;
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if ((st = check_kernel_shape(p, s)) != VSA2_OK) return st;
+    if (!q || !k || !v || !row_ptr || !o || !lse) return VSA2_ERR_NULL;
+    if (!col_idx && col_cap > 0) return VSA2_ERR_NULL;
+    if (col_cap < 0) return VSA2_ERR_CAPACITY;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return VSA2_ERR_ALIGN;
+    VSA2_TRY_HIP(vsa2::launch_attn_fwd(p->dtype, p->head_dim, q, k, v, row_ptr, col_idx, col_cap, o, lse,
+                                       p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N), stream));
+    return VSA2_OK;
+}
+
+vsa2_status vsa2_attn_bwd(const vsa2_problem* p, const void* q, const void* k, const void* v, const void* o,
+                          const float* lse, const void* dout, const int32_t* row_ptr,
+                          const int32_t* col_idx, const int32_t* kv_ptr, const int32_t* kv_idx,
+                          int64_t col_cap, void* dq, void* dk, void* dv, void* ws, size_t ws_bytes,
+                          hipStream_t stream) {
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if ((st = check_kernel_shape(p, s)) != VSA2_OK) return st;
+    if (!q || !k || !v || !o || !lse || !dout || !row_ptr || !kv_ptr || !dq || !dk || !dv)
+        return VSA2_ERR_NULL;
+    if ((!col_idx || !kv_idx) && col_cap > 0) return VSA2_ERR_NULL;
+    if (col_cap < 0) return VSA2_ERR_CAPACITY;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) ||
+        !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
+        return VSA2_ERR_ALIGN;
+    const size_t need = bwd_ws_bytes(s, p);
+    if (!ws || ws_bytes < need) return VSA2_ERR_WORKSPACE;
+    if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
+    VSA2_TRY_HIP(vsa2::launch_attn_bwd(p->dtype, p->head_dim, q, k, v, o, lse, dout, row_ptr, col_idx,
+                                       kv_ptr, kv_idx, col_cap, dq, dk, dv, static_cast<float*>(ws),
+                                       p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N), stream));
+    return VSA2_OK;
+}
+
+}  // extern "C"

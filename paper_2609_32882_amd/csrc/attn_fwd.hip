@@ -1,0 +1,180 @@
+// Block-sparse attention forward (VSA2 Sec. 2.1 with a block mask, Sec. 2.2
+// Eq. block_sparse) for gfx950.
+//
+// One workgroup of two waves per query block (64 queries); wave w owns
+// queries 32w .. 32w+31.  For every key block listed in the block's CSR row:
+//   K tile  [64 keys][D]  -> LDS, row r stored at slot swap_bits_2_3(r)
+//   V tile  [64 keys][D]  -> LDS transposed, V^T [D][64 keys]
+//   S^T = K Q^T           (MFMA 32x32, Q fragments live in registers)
+//   online softmax in fp32 registers (exp2, log2(e)/sqrt(D) folded in)
+//   O^T += V^T P^T        (P rounded to the input dtype, MFMA 32x32)
+// In the transposed products a lane owns one query column, so the row max
+// and row sum need one exchange with the other half-wave and nothing else.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace vsa2 {
+
+constexpr int AF_NT = 128;
+
+template <typename T, int D>
+__global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+    const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx, int64_t col_cap,
+    T* __restrict__ o, float* __restrict__ lse, int Hq, int Hkv, int N, float c_log2) {
+    using F = typename frag_of<T>::type;
+    constexpr int E = sizeof(T);
+    constexpr int KS = D / 16;        // macro k-steps over the head dim
+    constexpr int MT = D / 32;        // 32-row tiles of O^T
+    constexpr int KRB = D * E;        // K tile row bytes
+    constexpr int VRB = 64 * E;       // V^T tile row bytes
+    using KL = tile_rows<T, D, AF_NT>;
+    using VL = tile_transposed<T, D, AF_NT>;
+    __shared__ __align__(16) char k_lds[64 * KRB];
+    __shared__ __align__(16) char v_lds[D * VRB];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+    const int64_t row = blockIdx.x;
+    const int64_t bh = row / N;
+    const int n = static_cast<int>(row % N);
+    const int b = static_cast<int>(bh / Hq), h = static_cast<int>(bh % Hq);
+    const int hkv = h / (Hq / Hkv);
+    const int64_t L = static_cast<int64_t>(N) * 64;
+    const T* kb = k + static_cast<int64_t>(b * Hkv + hkv) * L * D;
+    const T* vb = v + static_cast<int64_t>(b * Hkv + hkv) * L * D;
+    const int64_t qtok = bh * L + static_cast<int64_t>(n) * 64 + wave * 32 + (lane & 31);
+
+    int64_t e0 = row_ptr[row], e1 = row_ptr[row + 1];
+    e0 = e0 < 0 ? 0 : (e0 > col_cap ? col_cap : e0);
+    e1 = e1 < e0 ? e0 : (e1 > col_cap ? col_cap : e1);
+
+    F qf[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) load_frag(qf[ks], q + qtok * D + ks * 16 + half * 8);
+
+    f32x16_t oacc[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) oacc[mt][i] = 0.f;
+    float m = -INFINITY, l = 0.f;
+
+    KL kt;
+    VL vt;
+    for (int64_t e = e0; e < e1; ++e) {
+        const int c = col_idx[e];
+        if (c < 0 || c >= N) continue;          // malformed entry: skipped, never read
+        kt.load(kb, static_cast<int64_t>(c) * 64, L, tid);
+        vt.load(vb, static_cast<int64_t>(c) * 64, tid);
+        __syncthreads();                         // previous tile fully consumed
+        kt.store(k_lds, true, tid);
+        vt.store(v_lds, tid);
+        __syncthreads();
+
+        // S^T for 64 keys x 32 queries (two 32-key tiles)
+        f32x16_t s[2];
+#pragma unroll
+        for (int t2 = 0; t2 < 2; ++t2) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) s[t2][i] = 0.f;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                F a;
+                lds_frag<KRB>(a, k_lds, t2 * 32 + (lane & 31), ks * 16 + half * 8);
+                mma(s[t2], a, qf[ks]);
+            }
+        }
+        // online softmax over this lane's query column
+        float mx = -INFINITY;
+#pragma unroll
+        for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                s[t2][i] *= c_log2;
+                mx = fmaxf(mx, s[t2][i]);
+            }
+        mx = fmaxf(mx, swap_half(mx));
+        const float mn = fmaxf(m, mx);
+        const float alpha = exp2f(m - mn);
+        float ps = 0.f;
+#pragma unroll
+        for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const float p = exp2f(s[t2][i] - mn);
+                s[t2][i] = p;
+                ps += p;
+            }
+        l = l * alpha + ps;
+        m = mn;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) oacc[mt][i] *= alpha;
+        // O^T += V^T P^T over 4 k-steps of 16 keys: keys 16kk + 8half + (0..7)
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            F pb;
+            float pv[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) pv[i] = s[kk >> 1][(kk & 1) * 8 + i];
+            pack_frag(pb, pv);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                F a;
+                lds_frag<VRB>(a, v_lds, mt * 32 + (lane & 31), kk * 16 + half * 8);
+                mma(oacc[mt], a, pb);
+            }
+        }
+    }
+
+    const float lt = l + swap_half(l);
+    const float inv = lt > 0.f ? 1.0f / lt : 0.f;
+    T* orow = o + qtok * D;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+            const int d0 = mt * 32 + g4 * 8 + half * 4;
+            if constexpr (E == 2) {
+                const uint32_t w0 = static_cast<uint32_t>(f32_to_bf16(oacc[mt][g4 * 4 + 0] * inv)) |
+                                    (static_cast<uint32_t>(f32_to_bf16(oacc[mt][g4 * 4 + 1] * inv)) << 16);
+                const uint32_t w1 = static_cast<uint32_t>(f32_to_bf16(oacc[mt][g4 * 4 + 2] * inv)) |
+                                    (static_cast<uint32_t>(f32_to_bf16(oacc[mt][g4 * 4 + 3] * inv)) << 16);
+                *reinterpret_cast<uint2*>(orow + d0) = make_uint2(w0, w1);
+            } else {
+                *reinterpret_cast<float4*>(orow + d0) =
+                    make_float4(oacc[mt][g4 * 4 + 0] * inv, oacc[mt][g4 * 4 + 1] * inv,
+                                oacc[mt][g4 * 4 + 2] * inv, oacc[mt][g4 * 4 + 3] * inv);
+            }
+        }
+    if (half == 0) lse[qtok] = lt > 0.f ? (m + log2f(lt)) * 0.6931471805599453f : -INFINITY;
+}
+
+template <typename T, int D>
+static hipError_t launch_fwd_t(const void* q, const void* k, const void* v, const int32_t* row_ptr,
+                               const int32_t* col_idx, int64_t col_cap, void* o, float* lse,
+                               int batch, int Hq, int Hkv, int N, hipStream_t s) {
+    const int64_t rows = static_cast<int64_t>(batch) * Hq * N;
+    if (rows == 0) return hipSuccess;
+    const float c = 1.4426950408889634f / sqrtf(static_cast<float>(D));
+    hipLaunchKernelGGL((attn_fwd_kernel<T, D>), dim3(static_cast<unsigned>(rows)), dim3(AF_NT), 0, s,
+                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+                       row_ptr, col_idx, col_cap, static_cast<T*>(o), lse, Hq, Hkv, N, c);
+    return hipGetLastError();
+}
+
+hipError_t launch_attn_fwd(int dtype, int D, const void* q, const void* k, const void* v,
+                           const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
+                           float* lse, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+    if (dtype == 1) {
+        if (D == 64) return launch_fwd_t<bf16_t, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, batch, Hq, Hkv, N, s);
+        if (D == 128) return launch_fwd_t<bf16_t, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, batch, Hq, Hkv, N, s);
+    } else {
+        if (D == 64) return launch_fwd_t<float, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, batch, Hq, Hkv, N, s);
+        if (D == 128) return launch_fwd_t<float, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, batch, Hq, Hkv, N, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace vsa2

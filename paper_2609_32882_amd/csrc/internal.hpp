@@ -1,0 +1,32 @@
+// Host-side launchers of the gfx950 kernels (internal to the library; the
+// public C-ABI in vsa2.h validates arguments and calls these).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace vsa2 {
+
+hipError_t launch_pool(int dtype, const void* x, void* out, int64_t nbh, int N, int D, int Bt, int Bh,
+                       int Bw, int Pt, int Ph, int Pw, hipStream_t s);
+hipError_t launch_route_passes(int dtype, int D, int G, const void* qr, const void* kr, float* lse2,
+                               float* scores, int batch, int Hq, int Hkv, int N, hipStream_t s);
+hipError_t launch_select(int phase, const float* scores, int64_t nrows, int N, int mode, int k,
+                         float mass, int cap, int32_t* counts, const int32_t* row_ptr,
+                         int32_t* col_idx, int64_t col_cap, hipStream_t s);
+hipError_t launch_scan(const int32_t* counts, int64_t n, int32_t* ptr, hipStream_t s);
+hipError_t launch_uniform_ptr(int32_t* ptr, int64_t n, int k, hipStream_t s);
+hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
+hipError_t launch_csc(const int32_t* row_ptr, const int32_t* col_idx, int batch, int Hq, int Hkv, int N,
+                      int64_t col_cap, uint32_t* mask, int32_t* kv_counts, int32_t* kv_ptr,
+                      int32_t* kv_idx, hipStream_t s);
+hipError_t launch_attn_fwd(int dtype, int D, const void* q, const void* k, const void* v,
+                           const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
+                           float* lse, int batch, int Hq, int Hkv, int N, hipStream_t s);
+hipError_t launch_attn_bwd(int dtype, int D, const void* q, const void* k, const void* v, const void* o,
+                           const float* lse, const void* dout, const int32_t* row_ptr,
+                           const int32_t* col_idx, const int32_t* kv_ptr, const int32_t* kv_idx,
+                           int64_t col_cap, void* dq, void* dk, void* dv, float* delta, int batch,
+                           int Hq, int Hkv, int N, hipStream_t s);
+
+}  // namespace vsa2

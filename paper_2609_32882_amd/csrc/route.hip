@@ -1,0 +1,583 @@
+// Pooling and the fine-grained router (VSA2 Sec. 2.2, Eq. router_start ..
+// Eq. router_end), selection and the sparse block lists.
+//
+//   pool_kernel          MeanPool over sub-cubes, fp64 sums, one rounding
+//   route_pass_kernel    pass 1: row log-sum-exp of Q_r K_r^T / sqrt(D)
+//                        pass 2: softmax + G x G pooling into block scores
+//   select_kernel        per-row top-k / mass selection by bisection on the
+//                        fp32 bit pattern, register resident, one wave a row
+//   scan / CSC kernels   CSR offsets, and the transposed (key-block) lists
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace vsa2 {
+
+// ===========================================================================
+// Pool
+// ===========================================================================
+// One thread per (output row, 8-element chunk of D).  Output row
+// (bh*N + n)*G + g averages the Pt*Ph*Pw tokens of sub-cube g of cube n.
+template <typename T>
+__global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ x, T* __restrict__ out,
+                                                   int64_t nthreads, int D, int G, int Gh, int Gw,
+                                                   int Pt, int Ph, int Pw, int Bh, int Bw, int B) {
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (t >= nthreads) return;
+    const int chunks = D / 8;
+    const int ch = static_cast<int>(t % chunks);
+    const int64_t orow = t / chunks;                  // (bh*N + n)*G + g
+    const int g = static_cast<int>(orow % G);
+    const int64_t cube = orow / G;                   // bh*N + n
+    const int gt = g / (Gh * Gw), gh = (g / Gw) % Gh, gw = g % Gw;
+    double acc[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = 0.0;
+    for (int rt = 0; rt < Pt; ++rt)
+        for (int rh = 0; rh < Ph; ++rh)
+            for (int rw = 0; rw < Pw; ++rw) {
+                const int beta = ((gt * Pt + rt) * Bh + gh * Ph + rh) * Bw + gw * Pw + rw;
+                const T* src = x + (cube * B + beta) * D + ch * 8;
+                if constexpr (sizeof(T) == 2) {
+                    const uint4 w = *reinterpret_cast<const uint4*>(src);
+                    const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        acc[2 * i] += static_cast<double>(bf16_to_f32(u[i] & 0xffffu));
+                        acc[2 * i + 1] += static_cast<double>(bf16_to_f32(u[i] >> 16));
+                    }
+                } else {
+                    const float4 a = reinterpret_cast<const float4*>(src)[0];
+                    const float4 b = reinterpret_cast<const float4*>(src)[1];
+                    const float f[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) acc[i] += static_cast<double>(f[i]);
+                }
+            }
+    const double P = static_cast<double>(Pt * Ph * Pw);
+    T* dst = out + orow * D + ch * 8;
+    if constexpr (sizeof(T) == 2) {
+        uint32_t u[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            u[i] = static_cast<uint32_t>(f64_to_bf16(acc[2 * i] / P)) |
+                   (static_cast<uint32_t>(f64_to_bf16(acc[2 * i + 1] / P)) << 16);
+        *reinterpret_cast<uint4*>(dst) = make_uint4(u[0], u[1], u[2], u[3]);
+    } else {
+        float f[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) f[i] = __double2float_rn(acc[i] / P);
+        reinterpret_cast<float4*>(dst)[0] = make_float4(f[0], f[1], f[2], f[3]);
+        reinterpret_cast<float4*>(dst)[1] = make_float4(f[4], f[5], f[6], f[7]);
+    }
+}
+
+hipError_t launch_pool(int dtype, const void* x, void* out, int64_t nbh, int N, int D,
+                       int Bt, int Bh, int Bw, int Pt, int Ph, int Pw, hipStream_t s) {
+    const int Gt = Bt / Pt, Gh = Bh / Ph, Gw = Bw / Pw, G = Gt * Gh * Gw;
+    const int64_t nthreads = nbh * N * G * (D / 8);
+    if (nthreads == 0) return hipSuccess;
+    const int64_t blocks = (nthreads + 255) / 256;
+    const int B = Bt * Bh * Bw;
+    if (dtype == 1)
+        hipLaunchKernelGGL(pool_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s,
+                           static_cast<const bf16_t*>(x), static_cast<bf16_t*>(out), nthreads, D, G,
+                           Gh, Gw, Pt, Ph, Pw, Bh, Bw, B);
+    else
+        hipLaunchKernelGGL(pool_kernel<float>, dim3(blocks), dim3(256), 0, s,
+                           static_cast<const float*>(x), static_cast<float*>(out), nthreads, D, G,
+                           Gh, Gw, Pt, Ph, Pw, Bh, Bw, B);
+    return hipGetLastError();
+}
+
+// ===========================================================================
+// Router passes
+// ===========================================================================
+// Grid: x = tiles of 256 pooled queries, y = batch*Hq.  Four waves, each
+// owning 64 pooled queries (two 32-column tiles).  The transposed product
+// S^T = K_r Q_r^T puts one pooled query per accumulator column, so a lane
+// holds 16 keys of one query: per-query reductions are lane-local plus one
+// exchange with the other half-wave.  K_r streams through LDS in 64-key
+// tiles, stored with the bit-2/3 slot swap so each lane's 16 keys form runs
+// of 8 consecutive keys (G | 8 keys of a run make whole key blocks).
+//   PASS 1: lse2[i] = log2 sum_j 2^(s_ij * log2(e)/sqrt(D))  (log2 units)
+//   PASS 2: P_r[nq][nk] = (1/G^2) sum_{gq,gk} 2^(t - lse2)
+constexpr int RT_Q = 256;   // pooled queries per workgroup
+constexpr int RT_NT = 256;  // threads per workgroup
+
+template <typename T, int D, int G, int PASS>
+__global__ __launch_bounds__(RT_NT) void route_pass_kernel(
+    const T* __restrict__ qr, const T* __restrict__ kr, float* __restrict__ lse2,
+    float* __restrict__ scores, int Hq, int Hkv, int N, float c_log2) {
+    using F = typename frag_of<T>::type;
+    constexpr int E = sizeof(T);
+    constexpr int KS = D / 16;
+    using KT = tile_rows<T, D, RT_NT>;
+    __shared__ __align__(16) char kt_lds[64 * D * E];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+    const int bh = blockIdx.y;
+    const int b = bh / Hq, h = bh % Hq, hkv = h / (Hq / Hkv);
+    const int64_t NG = static_cast<int64_t>(N) * G;
+    const T* qbase = qr + static_cast<int64_t>(bh) * NG * D;
+    const T* kbase = kr + static_cast<int64_t>(b * Hkv + hkv) * NG * D;
+    const int64_t q0 = static_cast<int64_t>(blockIdx.x) * RT_Q + wave * 64;   // wave's first query
+
+    F qf[2][KS];
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+        const int64_t qi = q0 + qt * 32 + (lane & 31);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            if (qi < NG) load_frag(qf[qt][ks], qbase + qi * D + ks * 16 + half * 8);
+            else {
+                float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+                pack_frag(qf[qt][ks], z);
+            }
+        }
+    }
+    float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f};
+    float lq[2] = {0.f, 0.f};
+    if constexpr (PASS == 2) {
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+            const int64_t qi = q0 + qt * 32 + (lane & 31);
+            lq[qt] = qi < NG ? lse2[static_cast<int64_t>(bh) * NG + qi] : 0.f;
+        }
+    }
+
+    KT ktile;
+    for (int64_t j0 = 0; j0 < NG; j0 += 64) {
+        ktile.load(kbase, j0, NG, tid);
+        __syncthreads();
+        ktile.store(kt_lds, true, tid);
+        __syncthreads();
+        f32x16_t acc[2][2];
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+            for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc[kt][qt][v] = 0.f;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                F a;
+                lds_frag<D * E>(a, kt_lds, kt * 32 + (lane & 31), ks * 16 + half * 8);
+                mma(acc[kt][0], a, qf[0][ks]);
+                mma(acc[kt][1], a, qf[1][ks]);
+            }
+        }
+        // key of accumulator entry v in key tile kt: j0 + 32kt + 16(v/8) + 8*half + v%8
+        if constexpr (PASS == 1) {
+#pragma unroll
+            for (int qt = 0; qt < 2; ++qt) {
+                float mt = -INFINITY;
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int64_t j = j0 + kt * 32 + (v >> 3) * 16 + half * 8 + (v & 7);
+                        const float t = j < NG ? acc[kt][qt][v] * c_log2 : -INFINITY;
+                        acc[kt][qt][v] = t;
+                        mt = fmaxf(mt, t);
+                    }
+                mt = fmaxf(mt, swap_half(mt));
+                const float mn = fmaxf(m[qt], mt);
+                float s = 0.f;
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) s += exp2f(acc[kt][qt][v] - mn);
+                l[qt] = l[qt] * exp2f(m[qt] - mn) + s;
+                m[qt] = mn;
+            }
+        } else {
+            constexpr float inv_g2 = 1.0f / static_cast<float>(G * G);
+#pragma unroll
+            for (int qt = 0; qt < 2; ++qt) {
+                const int64_t qi = q0 + qt * 32 + (lane & 31);
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+                    for (int run = 0; run < 2; ++run) {
+                        // this run: keys j0 + 32kt + 16run + 8half + (0..7)
+                        float bs[8 / G];
+#pragma unroll
+                        for (int i = 0; i < 8 / G; ++i) {
+                            float s = 0.f;
+#pragma unroll
+                            for (int u = 0; u < G; ++u) {
+                                const int v = run * 8 + i * G + u;
+                                const int64_t j = j0 + kt * 32 + run * 16 + half * 8 + i * G + u;
+                                s += j < NG ? exp2f(acc[kt][qt][v] * c_log2 - lq[qt]) : 0.f;
+                            }
+                            // sum over the G pooled queries of the block (G adjacent lanes)
+#pragma unroll
+                            for (int off = 1; off < G; off <<= 1) s += __shfl_xor(s, off, 64);
+                            bs[i] = s;
+                        }
+                        if ((lane % G) == 0 && qi < NG) {
+                            const int64_t nq = qi / G;
+#pragma unroll
+                            for (int i = 0; i < 8 / G; ++i) {
+                                const int64_t j = j0 + kt * 32 + run * 16 + half * 8 + i * G;
+                                if (j < NG)
+                                    scores[(static_cast<int64_t>(bh) * N + nq) * N + j / G] = bs[i] * inv_g2;
+                            }
+                        }
+                    }
+                }
+            }
+        }
+    }
+    if constexpr (PASS == 1) {
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt) {
+            const float lt = l[qt] + swap_half(l[qt]);
+            const int64_t qi = q0 + qt * 32 + (lane & 31);
+            if (half == 0 && qi < NG) lse2[static_cast<int64_t>(bh) * NG + qi] = m[qt] + log2f(lt);
+        }
+    }
+}
+
+template <typename T, int D, int G>
+static hipError_t launch_route_passes_t(const void* qr, const void* kr, float* lse2, float* scores,
+                                        int batch, int Hq, int Hkv, int N, hipStream_t s) {
+    const int64_t NG = static_cast<int64_t>(N) * G;
+    dim3 grid(static_cast<unsigned>((NG + RT_Q - 1) / RT_Q), static_cast<unsigned>(batch * Hq));
+    const float c = 1.4426950408889634f / sqrtf(static_cast<float>(D));
+    hipLaunchKernelGGL((route_pass_kernel<T, D, G, 1>), grid, dim3(RT_NT), 0, s,
+                       static_cast<const T*>(qr), static_cast<const T*>(kr), lse2, scores, Hq, Hkv, N, c);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((route_pass_kernel<T, D, G, 2>), grid, dim3(RT_NT), 0, s,
+                       static_cast<const T*>(qr), static_cast<const T*>(kr), lse2, scores, Hq, Hkv, N, c);
+    return hipGetLastError();
+}
+
+template <typename T, int D>
+static hipError_t launch_route_passes_d(int G, const void* qr, const void* kr, float* lse2,
+                                        float* scores, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+    switch (G) {
+        case 1: return launch_route_passes_t<T, D, 1>(qr, kr, lse2, scores, batch, Hq, Hkv, N, s);
+        case 2: return launch_route_passes_t<T, D, 2>(qr, kr, lse2, scores, batch, Hq, Hkv, N, s);
+        case 4: return launch_route_passes_t<T, D, 4>(qr, kr, lse2, scores, batch, Hq, Hkv, N, s);
+        case 8: return launch_route_passes_t<T, D, 8>(qr, kr, lse2, scores, batch, Hq, Hkv, N, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_route_passes(int dtype, int D, int G, const void* qr, const void* kr, float* lse2,
+                               float* scores, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+    if (dtype == 1) {
+        if (D == 64) return launch_route_passes_d<bf16_t, 64>(G, qr, kr, lse2, scores, batch, Hq, Hkv, N, s);
+        if (D == 128) return launch_route_passes_d<bf16_t, 128>(G, qr, kr, lse2, scores, batch, Hq, Hkv, N, s);
+    } else {
+        if (D == 64) return launch_route_passes_d<float, 64>(G, qr, kr, lse2, scores, batch, Hq, Hkv, N, s);
+        if (D == 128) return launch_route_passes_d<float, 128>(G, qr, kr, lse2, scores, batch, Hq, Hkv, N, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+// ===========================================================================
+// Selection
+// ===========================================================================
+// One wave per query-block row of N scores (N <= 64*PER), held in registers:
+// element j = 64*i + lane.  Scores are >= 0, so float order equals the order
+// of their bit patterns and a 31-step bisection on the bits finds exact
+// thresholds.  Ties at the threshold go to the lowest block indices, which
+// reproduces the order (score desc, index asc).
+__device__ __forceinline__ int wave_sum_i(int x) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
+    return x;
+}
+__device__ __forceinline__ double wave_sum_d(double x) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);
+    return x;
+}
+
+// Largest threshold t (as bits) with count(x >= t) >= k: the k-th largest value.
+template <int PER>
+__device__ __forceinline__ uint32_t kth_largest_bits(const float (&x)[PER], int k) {
+    uint32_t tau = 0;
+    for (int bit = 30; bit >= 0; --bit) {
+        const uint32_t cand = tau | (1u << bit);
+        const float cf = __uint_as_float(cand);
+        int c = 0;
+#pragma unroll
+        for (int i = 0; i < PER; ++i) c += x[i] >= cf ? 1 : 0;
+        if (wave_sum_i(c) >= k) tau = cand;
+    }
+    return tau;
+}
+
+struct row_rule {
+    float tau;      // threshold value
+    int need;       // how many of the entries equal to tau are kept (lowest indices)
+    int count;      // total kept
+};
+
+template <int PER>
+__device__ row_rule decide_row(const float (&x)[PER], int N, int mode, int k, float mass, int cap) {
+    row_rule r;
+    int keep;
+    if (mode == 0) {
+        keep = k < N ? k : N;
+    } else {
+        double tot = 0.0;
+#pragma unroll
+        for (int i = 0; i < PER; ++i) tot += x[i] > 0.f ? static_cast<double>(x[i]) : 0.0;
+        tot = wave_sum_d(tot);
+        const double thr = static_cast<double>(mass) * tot;
+        if (!(thr > 0.0)) {
+            keep = 1;
+        } else {
+            // largest t with S(t) = sum_{x >= t} x >= thr
+            uint32_t tau = 0;
+            for (int bit = 30; bit >= 0; --bit) {
+                const uint32_t cand = tau | (1u << bit);
+                const float cf = __uint_as_float(cand);
+                double s = 0.0;
+#pragma unroll
+                for (int i = 0; i < PER; ++i) s += x[i] >= cf ? static_cast<double>(x[i]) : 0.0;
+                if (wave_sum_d(s) >= thr) tau = cand;
+            }
+            const float tf = __uint_as_float(tau);
+            double sg = 0.0;
+            int gt = 0, eq = 0;
+#pragma unroll
+            for (int i = 0; i < PER; ++i) {
+                if (x[i] > tf) { sg += static_cast<double>(x[i]); ++gt; }
+                else if (x[i] == tf) ++eq;
+            }
+            sg = wave_sum_d(sg);
+            gt = wave_sum_i(gt);
+            eq = wave_sum_i(eq);
+            // ties added one at a time, lowest index first, until the sum reaches thr
+            int m = 0;
+            double cum = sg;
+            while (m < eq && cum < thr) { cum += static_cast<double>(tf); ++m; }
+            keep = gt + (m > 0 ? m : (eq > 0 ? 1 : 0));
+            if (keep > N) keep = N;
+        }
+        if (keep > cap) keep = cap;
+    }
+    const uint32_t tau = kth_largest_bits<PER>(x, keep);
+    const float tf = __uint_as_float(tau);
+    int gt = 0;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) gt += x[i] > tf ? 1 : 0;
+    gt = wave_sum_i(gt);
+    r.tau = tf;
+    r.need = keep - gt;
+    r.count = keep;
+    return r;
+}
+
+// PHASE 0: counts[row] = number kept.  PHASE 1: write the kept block indices,
+// ascending, at col_idx[row_ptr[row] ...].
+template <int PER, int PHASE>
+__global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ scores, int64_t nrows,
+                                                     int N, int mode, int k, float mass, int cap,
+                                                     int32_t* __restrict__ counts,
+                                                     const int32_t* __restrict__ row_ptr,
+                                                     int32_t* __restrict__ col_idx, int64_t col_cap) {
+    const int lane = threadIdx.x & 63;
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+    if (row >= nrows) return;
+    float x[PER];
+    const float* src = scores + row * N;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+        const int j = i * 64 + lane;
+        x[i] = j < N ? src[j] : -1.0f;   // padding never reaches a threshold >= 0
+    }
+    const row_rule r = decide_row<PER>(x, N, mode, k, mass, cap);
+    if constexpr (PHASE == 0) {
+        if (lane == 0) counts[row] = r.count;
+    } else {
+        int64_t pos = row_ptr[row];
+        int ties = 0;
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const bool eq = x[i] == r.tau;
+            const uint64_t eqm = __ballot(eq);
+            const int rank = ties + __popcll(eqm & ((1ull << lane) - 1ull));
+            const bool sel = x[i] > r.tau || (eq && rank < r.need);
+            const uint64_t sm = __ballot(sel);
+            if (sel) {
+                const int64_t at = pos + __popcll(sm & ((1ull << lane) - 1ull));
+                if (at < col_cap) col_idx[at] = i * 64 + lane;
+            }
+            pos += __popcll(sm);
+            ties += __popcll(eqm);
+        }
+    }
+}
+
+template <int PER>
+static hipError_t launch_select_per(int phase, const float* scores, int64_t nrows, int N, int mode,
+                                    int k, float mass, int cap, int32_t* counts,
+                                    const int32_t* row_ptr, int32_t* col_idx, int64_t col_cap,
+                                    hipStream_t s) {
+    dim3 grid(static_cast<unsigned>((nrows + 3) / 4));
+    if (phase == 0)
+        hipLaunchKernelGGL((select_kernel<PER, 0>), grid, dim3(256), 0, s, scores, nrows, N, mode, k,
+                           mass, cap, counts, row_ptr, col_idx, col_cap);
+    else
+        hipLaunchKernelGGL((select_kernel<PER, 1>), grid, dim3(256), 0, s, scores, nrows, N, mode, k,
+                           mass, cap, counts, row_ptr, col_idx, col_cap);
+    return hipGetLastError();
+}
+
+hipError_t launch_select(int phase, const float* scores, int64_t nrows, int N, int mode, int k,
+                         float mass, int cap, int32_t* counts, const int32_t* row_ptr,
+                         int32_t* col_idx, int64_t col_cap, hipStream_t s) {
+    if (nrows == 0) return hipSuccess;
+    const int per = (N + 63) / 64;
+#define VSA2_SEL(P) \
+    if (per <= P) return launch_select_per<P>(phase, scores, nrows, N, mode, k, mass, cap, counts, row_ptr, col_idx, col_cap, s)
+    VSA2_SEL(2);
+    VSA2_SEL(4);
+    VSA2_SEL(8);
+    VSA2_SEL(16);
+    VSA2_SEL(24);
+    VSA2_SEL(32);
+    VSA2_SEL(40);
+    VSA2_SEL(48);
+    VSA2_SEL(64);
+#undef VSA2_SEL
+    return hipErrorInvalidValue;
+}
+
+// ===========================================================================
+// Offsets and the transposed lists
+// ===========================================================================
+// Exclusive scan of counts[0..n) into ptr[0..n] by one workgroup of 1024.
+__global__ __launch_bounds__(1024) void scan_kernel(const int32_t* __restrict__ counts, int64_t n,
+                                                    int32_t* __restrict__ ptr) {
+    __shared__ int32_t part[1024];
+    const int tid = threadIdx.x;
+    const int64_t per = (n + 1023) / 1024;
+    const int64_t lo = tid * per, hi = lo + per < n ? lo + per : n;
+    int32_t s = 0;
+    for (int64_t i = lo; i < hi; ++i) s += counts[i];
+    part[tid] = s;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+        const int32_t v = tid >= off ? part[tid - off] : 0;
+        __syncthreads();
+        part[tid] += v;
+        __syncthreads();
+    }
+    int32_t run = part[tid] - s;   // exclusive prefix of this thread's range
+    for (int64_t i = lo; i < hi; ++i) {
+        ptr[i] = run;
+        run += counts[i];
+    }
+    if (tid == 1023) ptr[n] = part[1023];
+}
+
+hipError_t launch_scan(const int32_t* counts, int64_t n, int32_t* ptr, hipStream_t s) {
+    hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, s, counts, n, ptr);
+    return hipGetLastError();
+}
+
+// Offsets of uniform rows: ptr[i] = i * k.
+__global__ void uniform_ptr_kernel(int32_t* __restrict__ ptr, int64_t n, int k) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i <= n) ptr[i] = static_cast<int32_t>(i * k);
+}
+
+hipError_t launch_uniform_ptr(int32_t* ptr, int64_t n, int k, hipStream_t s) {
+    hipLaunchKernelGGL(uniform_ptr_kernel, dim3(static_cast<unsigned>((n + 1 + 255) / 256)), dim3(256), 0, s,
+                       ptr, n, k);
+    return hipGetLastError();
+}
+
+__global__ void fill_u32_kernel(uint32_t* __restrict__ p, int64_t n, uint32_t v) {
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
+         i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+        p[i] = v;
+}
+
+hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s) {
+    if (n == 0) return hipSuccess;
+    int64_t blocks = (n + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    hipLaunchKernelGGL(fill_u32_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, s, p, n, v);
+    return hipGetLastError();
+}
+
+// Mark every CSR entry in the key-block bitmask: bit (hq_local*N + nq) of
+// key-block row (b*Hkv + hkv)*N + nk.  One thread per query-block row.
+__global__ void csc_mark_kernel(const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx,
+                                int64_t nrows, int N, int Hq, int Hkv, int words, int64_t col_cap,
+                                uint32_t* __restrict__ mask) {
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (row >= nrows) return;
+    const int grp = Hq / Hkv;
+    const int64_t bh = row / N;
+    const int nq = static_cast<int>(row % N);
+    const int b = static_cast<int>(bh / Hq), h = static_cast<int>(bh % Hq);
+    const int hkv = h / grp, hl = h % grp;
+    const int bit = hl * N + nq;
+    int64_t s0 = row_ptr[row], s1 = row_ptr[row + 1];
+    s0 = s0 < 0 ? 0 : (s0 > col_cap ? col_cap : s0);
+    s1 = s1 < s0 ? s0 : (s1 > col_cap ? col_cap : s1);
+    for (int64_t e = s0; e < s1; ++e) {
+        const int nk = col_idx[e];
+        if (nk < 0 || nk >= N) continue;
+        const int64_t krow = static_cast<int64_t>(b * Hkv + hkv) * N + nk;
+        atomicOr(mask + krow * words + (bit >> 5), 1u << (bit & 31));
+    }
+}
+
+__global__ void csc_count_kernel(const uint32_t* __restrict__ mask, int64_t nkrows, int words,
+                                 int32_t* __restrict__ counts) {
+    const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (r >= nkrows) return;
+    int c = 0;
+    for (int w = 0; w < words; ++w) c += __popc(mask[r * words + w]);
+    counts[r] = c;
+}
+
+__global__ void csc_emit_kernel(const uint32_t* __restrict__ mask, int64_t nkrows, int words,
+                                const int32_t* __restrict__ kv_ptr, int32_t* __restrict__ kv_idx,
+                                int64_t col_cap) {
+    const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (r >= nkrows) return;
+    int64_t pos = kv_ptr[r];
+    for (int w = 0; w < words; ++w) {
+        uint32_t m = mask[r * words + w];
+        while (m) {
+            const int bit = __ffs(m) - 1;
+            m &= m - 1;
+            if (pos < col_cap) kv_idx[pos] = w * 32 + bit;
+            ++pos;
+        }
+    }
+}
+
+hipError_t launch_csc(const int32_t* row_ptr, const int32_t* col_idx, int batch, int Hq, int Hkv, int N,
+                      int64_t col_cap, uint32_t* mask, int32_t* kv_counts, int32_t* kv_ptr,
+                      int32_t* kv_idx, hipStream_t s) {
+    const int words = (Hq / Hkv * N + 31) / 32;
+    const int64_t nkrows = static_cast<int64_t>(batch) * Hkv * N;
+    const int64_t nrows = static_cast<int64_t>(batch) * Hq * N;
+    hipError_t e = launch_fill_u32(mask, nkrows * words, 0u, s);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(csc_mark_kernel, dim3(static_cast<unsigned>((nrows + 255) / 256)), dim3(256), 0, s,
+                       row_ptr, col_idx, nrows, N, Hq, Hkv, words, col_cap, mask);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(csc_count_kernel, dim3(static_cast<unsigned>((nkrows + 255) / 256)), dim3(256), 0, s,
+                       mask, nkrows, words, kv_counts);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_scan(kv_counts, nkrows, kv_ptr, s)) != hipSuccess) return e;
+    hipLaunchKernelGGL(csc_emit_kernel, dim3(static_cast<unsigned>((nkrows + 255) / 256)), dim3(256), 0, s,
+                       mask, nkrows, words, kv_ptr, kv_idx, col_cap);
+    return hipGetLastError();
+}
+
+}  // namespace vsa2

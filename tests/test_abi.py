@@ -1,0 +1,129 @@
+"""CPU-side checks of the C-ABI library: it loads without a GPU, exports every
+symbol include/vsa2.h declares, and rejects invalid arguments on the host
+before touching the device (no compute call runs here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "vsa2.h")
+
+vsa2 = pytest.importorskip("paper_2609_32882_amd")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(vsa2_[a-z_0-9]+)\s*\(", src)))
+
+
+def header_enum(name_prefix):
+    src = open(HEADER).read()
+    return {m.group(1): int(m.group(2)) for m in re.finditer(r"\b(%s[A-Z_0-9]*)\s*=\s*(\d+)" % name_prefix, src)}
+
+
+def test_library_exports_every_declared_symbol():
+    lib = vsa2.lib()
+    decl = declared_functions()
+    assert set(decl) == set(vsa2.EXPORTS), decl
+    for name in decl:
+        assert hasattr(lib, name), name
+
+
+def test_status_codes_match_header():
+    enum = header_enum("VSA2_ERR_")
+    enum["VSA2_OK"] = 0
+    assert {v: k for k, v in enum.items()} == vsa2.STATUS_NAMES
+    for code in enum.values():
+        assert vsa2.vsa2_status_str(code)
+
+
+def test_problem_struct_layout_matches_header():
+    src = open(HEADER).read()
+    body = src[src.index("typedef struct {\n    int32_t batch;"):src.index("} vsa2_problem;")]
+    fields = re.findall(r"int32_t\s+([^;]+);", body)
+    names = [n.strip() for f in fields for n in f.split(",")]
+    assert names == [f[0] for f in vsa2.vsa2_problem._fields_]
+    assert ctypes.sizeof(vsa2.vsa2_problem) == 4 * len(names)
+    assert ctypes.sizeof(vsa2.vsa2_select) == 16
+
+
+def good():
+    return vsa2.make_problem(1, 4, 2, 128, 8, 16, 16)
+
+
+FAKE = 0x10000          # aligned, never dereferenced: every call below fails validation first
+MISALIGNED = 0x10008
+
+
+@pytest.mark.parametrize("mutate,expect", [
+    (dict(dtype=7), "VSA2_ERR_DTYPE"),
+    (dict(heads_q=3), "VSA2_ERR_SHAPE"),          # Hq % Hkv
+    (dict(T=6), "VSA2_ERR_SHAPE"),                # T % Bt
+    (dict(Rt=3), "VSA2_ERR_SHAPE"),               # Bt % Rt
+    (dict(batch=0), "VSA2_ERR_SHAPE"),
+    (dict(head_dim=96), "VSA2_ERR_UNSUPPORTED"),
+    (dict(Bw=8, W=16), "VSA2_ERR_UNSUPPORTED"),   # B = 128
+])
+def test_attn_fwd_rejects_bad_problem(mutate, expect):
+    p = good()
+    for k, v in mutate.items():
+        setattr(p, k, v)
+    st = vsa2.vsa2_attn_fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE, FAKE, None, 0, None)
+    assert vsa2.STATUS_NAMES[st] == expect
+
+
+def test_null_and_alignment_checks():
+    p = good()
+    assert vsa2.STATUS_NAMES[vsa2.vsa2_attn_fwd(p, None, FAKE, FAKE, FAKE, FAKE, 1, FAKE, FAKE, None, 0,
+                                                None)] == "VSA2_ERR_NULL"
+    assert vsa2.STATUS_NAMES[vsa2.vsa2_attn_fwd(p, MISALIGNED, FAKE, FAKE, FAKE, FAKE, 1, FAKE, FAKE,
+                                                None, 0, None)] == "VSA2_ERR_ALIGN"
+    assert vsa2.STATUS_NAMES[vsa2.vsa2_pool(p, 4, FAKE, 2, 2, 2, MISALIGNED, None)] == "VSA2_ERR_ALIGN"
+    assert vsa2.STATUS_NAMES[vsa2.vsa2_pool(p, 4, FAKE, 3, 2, 2, FAKE, None)] == "VSA2_ERR_SHAPE"
+    assert vsa2.STATUS_NAMES[vsa2.vsa2_pool(None, 4, FAKE, 2, 2, 2, FAKE, None)] == "VSA2_ERR_NULL"
+    # bwd needs a workspace for the per-query Delta
+    st = vsa2.vsa2_attn_bwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, FAKE,
+                            FAKE, FAKE, None, 0, None)
+    assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_WORKSPACE"
+
+
+def test_route_capacity_workspace_and_select_checks():
+    p = good()
+    N = (8 // 4) * (16 // 4) * (16 // 4)
+    st, cap = vsa2.vsa2_route_capacity(p, vsa2.vsa2_select(0, 5, 0.0, 0))
+    assert st == 0 and cap == 1 * 4 * N * 5
+    st, cap = vsa2.vsa2_route_capacity(p, vsa2.vsa2_select(0, 10 ** 6, 0.0, 0))
+    assert st == 0 and cap == 4 * N * N                     # k > N keeps every block
+    st, cap = vsa2.vsa2_route_capacity(p, vsa2.vsa2_select(1, 0, 0.9, 7))
+    assert st == 0 and cap == 4 * N * 7
+    for bad in (vsa2.vsa2_select(0, 0, 0, 0), vsa2.vsa2_select(1, 0, 0.0, 5),
+                vsa2.vsa2_select(1, 0, 1.5, 5), vsa2.vsa2_select(1, 0, 0.5, 0),
+                vsa2.vsa2_select(9, 1, 0.5, 1)):
+        assert vsa2.STATUS_NAMES[vsa2.vsa2_route_capacity(p, bad)[0]] == "VSA2_ERR_SELECT"
+    s = vsa2.vsa2_select(0, 5, 0.0, 0)
+    st, wsb = vsa2.vsa2_route_workspace(p, s)
+    assert st == 0 and wsb >= 4 * N * N * 4
+    # capacity below what the rule can emit
+    st = vsa2.vsa2_route(p, s, FAKE, FAKE, FAKE, FAKE, 4 * N * 5 - 1, None, None, None, FAKE, wsb, None)
+    assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_CAPACITY"
+    st = vsa2.vsa2_route(p, s, FAKE, FAKE, FAKE, FAKE, 4 * N * 5, None, None, None, FAKE, wsb - 1, None)
+    assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_WORKSPACE"
+    st = vsa2.vsa2_route(p, s, FAKE, FAKE, FAKE, FAKE, 4 * N * 5, FAKE, None, None, FAKE, wsb, None)
+    assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_NULL"          # kv_ptr without kv_idx
+    p16 = good()
+    p16.Rt, p16.Rh, p16.Rw = 1, 1, 2                         # G = 32: not built
+    st = vsa2.vsa2_route(p16, s, FAKE, FAKE, FAKE, FAKE, 10 ** 9, None, None, None, FAKE, 10 ** 12, None)
+    assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_UNSUPPORTED"
+
+
+def test_product_path_has_no_oracle_or_fallback():
+    """The binding and the library never reach the oracle or a CPU path."""
+    pkg = os.path.join(ROOT, "paper_2609_32882_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".hpp", ".h", ".cpp")):
+                src = open(os.path.join(dirpath, f)).read()
+                assert "oracle" not in src.replace("oracle-free", ""), f

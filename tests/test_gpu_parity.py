@@ -1,0 +1,153 @@
+"""GPU parity: the HIP path through the C-ABI against the CPU oracle on the
+same seeded inputs, at sizes the oracle finishes in seconds (several tiles,
+ragged router tiles, GQA, D = 64 and 128, fp32 and bf16, top-k and mass)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_32882_amd as vsa2
+from parity import assert_values, compare_selection, to_dev, to_np
+from workload import BF16, F32, Problem, Selection, Workload, WORKLOADS, make_inputs
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    "tiny": WORKLOADS["tiny"],
+    # N = 48 cubes, 384 pooled queries: one full and one ragged router tile
+    "bf16-d128": Workload("bf16-d128", Problem(1, 2, 2, 128, 8, 16, 24), Selection(0, 12), 2001),
+    "bf16-d64-gqa": Workload("bf16-d64-gqa", Problem(1, 4, 2, 64, 8, 16, 16), Selection(0, 6), 2002),
+    "bf16-mass": Workload("bf16-mass", Problem(1, 2, 2, 128, 8, 16, 24), Selection(1, 0, 0.9, 20), 2003,
+                          skewed=True),
+    # k > N keeps every block: full attention; batch 2, 2 query heads on 1 KV head
+    "bf16-full-b2": Workload("bf16-full-b2", Problem(2, 2, 1, 128, 4, 16, 16), Selection(0, 100), 2004),
+    "f32-d128-mass": Workload("f32-d128-mass", Problem(1, 2, 1, 128, 4, 16, 16, dtype=F32),
+                              Selection(1, 0, 0.5, 3), 2005, skewed=True),
+}
+
+
+@pytest.fixture(scope="module", params=list(CASES))
+def case(request):
+    w = CASES[request.param]
+    p = w.problem
+    print("\n[case %s] %s" % (w.name, p), flush=True)
+    x = make_inputs(w, with_grad=True)
+    ref = oracle.route(x["q"], x["k"], p, w.select)
+    bf = p.dtype == BF16
+    dev = {k: to_dev(v, bf) for k, v in x.items()}
+    return w, x, ref, dev
+
+
+def test_pool_matches_oracle(case):
+    w, x, ref, dev = case
+    p = w.problem
+    q_r = vsa2.pool(p, dev["q"], (p.Rt, p.Rh, p.Rw))
+    k_r = vsa2.pool(p, dev["k"], (p.Rt, p.Rh, p.Rw))
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np(q_r), ref["q_r"])
+    assert np.array_equal(to_np(k_r), ref["k_r"])
+    # coarse-branch pooling (P = B) of V as well
+    v_c = vsa2.pool(p, dev["v"], (p.Bt, p.Bh, p.Bw))
+    assert np.array_equal(to_np(v_c), oracle.pool(x["v"], p, p.Bt, p.Bh, p.Bw))
+
+
+def test_route_matches_oracle(case):
+    w, x, ref, dev = case
+    p = w.problem
+    bf = p.dtype == BF16
+    r = vsa2.route(p, w.select, to_dev(ref["q_r"], bf), to_dev(ref["k_r"], bf), with_scores=True)
+    torch.cuda.synchronize()
+    sc = to_np(r["scores"]).reshape(-1, p.N)
+    err = np.abs(sc - ref["scores"]) / (np.abs(ref["scores"]) + 1e-30)
+    big = ref["scores"] > 1e-20
+    print("scores: max rel err %.3e" % err[big].max())
+    assert err[big].max() < 2e-5
+    rp = r["row_ptr"].cpu().numpy()
+    ci = r["col_idx"].cpu().numpy()
+    assert rp[0] == 0 and (np.diff(rp) >= 0).all()
+    nnz = int(rp[-1])
+    for i in range(rp.size - 1):
+        seg = ci[rp[i]:rp[i + 1]]
+        assert (np.diff(seg) > 0).all() and (seg >= 0).all() and (seg < p.N).all()
+    counts, idx = oracle.select_rows(ref["scores"], w.select)
+    st = compare_selection(rp, ci, counts, idx, ref["scores"], mass_mode=w.select.mode == 1,
+                           mass=w.select.mass)
+    print("selection:", st)
+    # the transposed lists are exact index work on the GPU's own CSR
+    kp, ki = oracle.csr_to_csc(rp, ci[:nnz], p)
+    assert np.array_equal(r["kv_ptr"].cpu().numpy(), kp)
+    assert np.array_equal(r["kv_idx"].cpu().numpy()[:nnz], ki)
+
+
+def test_fwd_matches_oracle(case):
+    w, x, ref, dev = case
+    p = w.problem
+    rp = torch.from_numpy(ref["row_ptr"]).cuda()
+    ci = torch.from_numpy(ref["col_idx"]).cuda()
+    o, lse = vsa2.attn_fwd(p, dev["q"], dev["k"], dev["v"], rp, ci)
+    torch.cuda.synchronize()
+    o_ref, lse_ref = oracle.attn_fwd(x["q"], x["k"], x["v"], p, ref["row_ptr"], ref["col_idx"])
+    assert_values(to_np(o).reshape(o_ref.shape), o_ref, "O")
+    assert_values(to_np(lse).reshape(lse_ref.shape), lse_ref, "LSE", max_abs=1e-3, rel_l2=1e-5)
+
+
+def test_end_to_end_path(case):
+    """pool -> route -> fwd on the GPU, against the oracle's whole path."""
+    w, x, ref, dev = case
+    p = w.problem
+    q_r = vsa2.pool(p, dev["q"], (p.Rt, p.Rh, p.Rw))
+    k_r = vsa2.pool(p, dev["k"], (p.Rt, p.Rh, p.Rw))
+    r = vsa2.route(p, w.select, q_r, k_r)
+    o, lse = vsa2.attn_fwd(p, dev["q"], dev["k"], dev["v"], r["row_ptr"], r["col_idx"])
+    torch.cuda.synchronize()
+    rp = r["row_ptr"].cpu().numpy()
+    ci = r["col_idx"].cpu().numpy()[:rp[-1]]
+    # the oracle forward on the GPU's own block lists (near-ties may differ)
+    o_ref, _ = oracle.attn_fwd(x["q"], x["k"], x["v"], p, rp, ci)
+    assert_values(to_np(o).reshape(o_ref.shape), o_ref, "O (end to end)")
+
+
+def test_fwd_deterministic_and_writes_everything(case):
+    w, x, ref, dev = case
+    p = w.problem
+    rp = torch.from_numpy(ref["row_ptr"]).cuda()
+    ci = torch.from_numpy(ref["col_idx"]).cuda()
+    o1 = torch.full_like(dev["q"], float("nan"))
+    l1 = torch.full((p.batch, p.heads_q, p.L), float("nan"), device="cuda")
+    vsa2.attn_fwd(p, dev["q"], dev["k"], dev["v"], rp, ci, o=o1, lse=l1)
+    o2, l2 = vsa2.attn_fwd(p, dev["q"], dev["k"], dev["v"], rp, ci)
+    torch.cuda.synchronize()
+    assert not torch.isnan(o1).any() and not torch.isnan(l1).any()
+    assert torch.equal(o1.view(torch.int16) if o1.dtype == torch.bfloat16 else o1.view(torch.int32),
+                       o2.view(torch.int16) if o2.dtype == torch.bfloat16 else o2.view(torch.int32))
+    assert torch.equal(l1, l2)
+
+
+def test_fwd_empty_rows_and_malformed_entries():
+    """Rows with no block give O = 0 and LSE = -inf; entries outside [0, N)
+    are skipped."""
+    w = CASES["bf16-d128"]
+    p = w.problem
+    x = make_inputs(w, with_grad=False)
+    rng = np.random.default_rng(5)
+    nrows = p.batch * p.heads_q * p.N
+    counts = rng.integers(0, 5, nrows)
+    counts[::7] = 0
+    lists = [np.sort(rng.choice(p.N, c, replace=False)).astype(np.int32) for c in counts]
+    rp = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    ci = np.concatenate(lists).astype(np.int32)
+    bad = ci.copy()
+    bad_pos = rng.choice(ci.size, 10, replace=False)
+    bad[bad_pos] = np.where(np.arange(10) % 2 == 0, -3, p.N + 5)
+    keep = np.ones(ci.size, bool)
+    keep[bad_pos] = False
+    rp_clean = np.concatenate([[0], np.cumsum([keep[rp[r]:rp[r + 1]].sum() for r in range(nrows)])]).astype(np.int32)
+    o_ref, lse_ref = oracle.attn_fwd(x["q"], x["k"], x["v"], p, rp_clean, ci[keep])
+    dq, dk, dv = (to_dev(x[t], True) for t in ("q", "k", "v"))
+    o, lse = vsa2.attn_fwd(p, dq, dk, dv, torch.from_numpy(rp).cuda(), torch.from_numpy(bad).cuda())
+    torch.cuda.synchronize()
+    o_np, lse_np = to_np(o).reshape(o_ref.shape), to_np(lse).reshape(lse_ref.shape)
+    empty = np.diff(rp_clean) == 0
+    assert (o_np[empty] == 0).all() and np.isneginf(lse_np[empty]).all()
+    assert_values(o_np, o_ref, "O (ragged rows)")
+    assert np.allclose(lse_np[~empty], lse_ref[~empty], atol=1e-3)
