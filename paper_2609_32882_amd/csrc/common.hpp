@@ -200,6 +200,20 @@ struct tile_transposed {
                 r[i][w] = *reinterpret_cast<const uint4*>(
                     g + (row0 + kb * 8 + i) * (int64_t)(D * E) + dc * 8 * E + w * 16);
     }
+    // The same 8x8 blocks written untransposed: [64 rows][D] (row stride
+    // D*E), row r at slot swap_bits_2_3(r) when `permute`.
+    __device__ __forceinline__ void store_rows(char* lds, bool permute, int tid) const {
+        if (tid >= BLOCKS) return;
+        const int dc = tid % (D / 8), kb = tid / (D / 8);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int row = kb * 8 + i;
+            const int slot = permute ? swap_bits_2_3(row) : row;
+#pragma unroll
+            for (int w = 0; w < W; ++w)
+                *reinterpret_cast<uint4*>(lds + lds_tile<D * E>::offset(slot, dc * W + w)) = r[i][w];
+        }
+    }
     __device__ __forceinline__ void store(char* lds, int tid) const {
         if (tid >= BLOCKS) return;
         const int dc = tid % (D / 8), kb = tid / (D / 8);

@@ -12,6 +12,10 @@ from workload import BF16, F32, Problem, Selection, Workload, WORKLOADS, make_in
 
 pytestmark = pytest.mark.gpu
 
+
+def dtname(p):
+    return "bf16" if p.dtype == BF16 else "f32"
+
 CASES = {
     "tiny": WORKLOADS["tiny"],
     # N = 48 cubes, 384 pooled queries: one full and one ragged router tile
@@ -87,8 +91,8 @@ def test_fwd_matches_oracle(case):
     o, lse = vsa2.attn_fwd(p, dev["q"], dev["k"], dev["v"], rp, ci)
     torch.cuda.synchronize()
     o_ref, lse_ref = oracle.attn_fwd(x["q"], x["k"], x["v"], p, ref["row_ptr"], ref["col_idx"])
-    assert_values(to_np(o).reshape(o_ref.shape), o_ref, "O")
-    assert_values(to_np(lse).reshape(lse_ref.shape), lse_ref, "LSE", max_abs=1e-3, rel_l2=1e-5)
+    assert_values(to_np(o).reshape(o_ref.shape), o_ref, "O", dtname(p))
+    assert_values(to_np(lse).reshape(lse_ref.shape), lse_ref, "LSE", "f32", max_abs=1e-3, rel_l2=1e-5)
 
 
 def test_end_to_end_path(case):
@@ -104,7 +108,7 @@ def test_end_to_end_path(case):
     ci = r["col_idx"].cpu().numpy()[:rp[-1]]
     # the oracle forward on the GPU's own block lists (near-ties may differ)
     o_ref, _ = oracle.attn_fwd(x["q"], x["k"], x["v"], p, rp, ci)
-    assert_values(to_np(o).reshape(o_ref.shape), o_ref, "O (end to end)")
+    assert_values(to_np(o).reshape(o_ref.shape), o_ref, "O (end to end)", dtname(p))
 
 
 def test_fwd_deterministic_and_writes_everything(case):
@@ -151,3 +155,69 @@ def test_fwd_empty_rows_and_malformed_entries():
     assert (o_np[empty] == 0).all() and np.isneginf(lse_np[empty]).all()
     assert_values(o_np, o_ref, "O (ragged rows)")
     assert np.allclose(lse_np[~empty], lse_ref[~empty], atol=1e-3)
+
+
+def _bwd_inputs(case):
+    w, x, ref, dev = case
+    p = w.problem
+    t = {k: torch.from_numpy(ref[k]).cuda() for k in ("row_ptr", "col_idx", "kv_ptr", "kv_idx")}
+    o, lse = vsa2.attn_fwd(p, dev["q"], dev["k"], dev["v"], t["row_ptr"], t["col_idx"])
+    return w, x, ref, dev, t, o, lse
+
+
+def test_bwd_matches_oracle(case):
+    w, x, ref, dev, t, o, lse = _bwd_inputs(case)
+    p = w.problem
+    dq, dk, dv = vsa2.attn_bwd(p, dev["q"], dev["k"], dev["v"], o, lse, dev["do"], t["row_ptr"],
+                               t["col_idx"], t["kv_ptr"], t["kv_idx"])
+    torch.cuda.synchronize()
+    dq_ref = oracle.attn_bwd_dq(x["q"], x["k"], x["v"], x["do"], p, ref["row_ptr"], ref["col_idx"])
+    dk_ref, dv_ref = oracle.attn_bwd_dkdv(x["q"], x["k"], x["v"], x["do"], p, ref["row_ptr"],
+                                          ref["col_idx"])
+    assert_values(to_np(dq).reshape(dq_ref.shape), dq_ref, "dQ", dtname(p))
+    assert_values(to_np(dk).reshape(dk_ref.shape), dk_ref, "dK", dtname(p))
+    assert_values(to_np(dv).reshape(dv_ref.shape), dv_ref, "dV", dtname(p))
+
+
+def test_bwd_deterministic_sentinels_and_unselected_blocks(case):
+    """Bitwise repeatable; every output element written (NaN sentinels);
+    key blocks no query selected get dK = dV = 0."""
+    w, x, ref, dev, t, o, lse = _bwd_inputs(case)
+    p = w.problem
+    args = (p, dev["q"], dev["k"], dev["v"], o, lse, dev["do"], t["row_ptr"], t["col_idx"],
+            t["kv_ptr"], t["kv_idx"])
+    s = [torch.full_like(dev[k], float("nan")) for k in ("q", "k", "v")]
+    vsa2.attn_bwd(*args, dq=s[0], dk=s[1], dv=s[2])
+    r2 = vsa2.attn_bwd(*args)
+    torch.cuda.synchronize()
+    for a, b in zip(s, r2):
+        assert not torch.isnan(a).any()
+        iv = torch.int16 if a.dtype == torch.bfloat16 else torch.int32
+        assert torch.equal(a.view(iv), b.view(iv))
+    indeg = np.diff(ref["kv_ptr"])
+    dk_np = to_np(s[1]).reshape(-1, p.B, p.head_dim)
+    dv_np = to_np(s[2]).reshape(-1, p.B, p.head_dim)
+    assert (dk_np[indeg == 0] == 0).all() and (dv_np[indeg == 0] == 0).all()
+
+
+def test_bwd_unselected_blocks_are_zero_explicit():
+    """A block list that leaves most key blocks unselected."""
+    w = CASES["bf16-d128"]
+    p = w.problem
+    x = make_inputs(w, with_grad=True)
+    nrows = p.batch * p.heads_q * p.N
+    rp = (np.arange(nrows + 1) * 2).astype(np.int32)
+    ci = np.tile(np.array([3, 17], np.int32), nrows)
+    kp, ki = oracle.csr_to_csc(rp, ci, p)
+    dev = {k: to_dev(v, True) for k, v in x.items()}
+    tt = [torch.from_numpy(a).cuda() for a in (rp, ci, kp, ki)]
+    o, lse = vsa2.attn_fwd(p, dev["q"], dev["k"], dev["v"], tt[0], tt[1])
+    dq, dk, dv = vsa2.attn_bwd(p, dev["q"], dev["k"], dev["v"], o, lse, dev["do"], *tt)
+    torch.cuda.synchronize()
+    dk_np = to_np(dk).reshape(p.heads_kv, p.N, p.B, p.head_dim)
+    mask = np.ones(p.N, bool)
+    mask[[3, 17]] = False
+    assert (dk_np[:, mask] == 0).all() and (to_np(dv).reshape(dk_np.shape)[:, mask] == 0).all()
+    dk_ref, dv_ref = oracle.attn_bwd_dkdv(x["q"], x["k"], x["v"], x["do"], p, rp, ci)
+    assert_values(to_np(dk).reshape(dk_ref.shape), dk_ref, "dK (two blocks)")
+    assert_values(to_np(dv).reshape(dv_ref.shape), dv_ref, "dV (two blocks)")
