@@ -1,0 +1,216 @@
+#!/usr/bin/env python3
+"""Benchmark of the VSA2 routed sparse-attention hot path on one MI355X.
+
+One step = one pass of the whole path over one batch of synthetic input:
+  MeanPool_R(Q), MeanPool_R(K) -> router (two passes) + top-k selection ->
+  CSR + transposed lists -> block-sparse attention forward -> backward
+  (dQ, dK, dV), every stage a call of the C-ABI library on one stream.
+
+Prints one JSON line.  `value` is the metric's effective sparse-attention
+throughput: the algorithmic FLOPs of forward + backward over the selected
+block pairs (4*B^2*D forward and 10*B^2*D backward per pair, nnz read from the
+produced CSR) divided by the time of the WHOLE step (pool and router
+included), inputs already resident in HBM.  Per-stage times come from HIP
+events recorded on the library's stream around each call.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 MFMA (spec sheet)
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="720p")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=32,
+                    help="query-block rows (forward + dQ) in the oracle's timed sample")
+    ap.add_argument("--cpu-kv", type=int, default=8,
+                    help="key blocks (dK/dV) in the oracle's timed sample")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build runs the routed sparse-attention path on one GPU only; "
+              "--gpus %d is not supported (the path shards over heads with no exchange; "
+              "see the design notes)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_32882_amd as vsa2
+    from workload import WORKLOADS, make_inputs
+
+    w = WORKLOADS[args.workload]
+    p, sel = w.problem, w.select
+    P = vsa2.problem_from(p)
+    S = vsa2.select_from(sel)
+    N, B, G, L, D = p.N, p.B, p.G, p.L, p.head_dim
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    t0 = time.time()
+    x = make_inputs(w, with_grad=True)
+    gen_s = time.time() - t0
+    tdt = torch.bfloat16 if p.dtype == 1 else torch.float32
+    q, k, v, do = (torch.from_numpy(x[n]).to(tdt).to(dev) for n in ("q", "k", "v", "do"))
+
+    # every buffer is allocated before timing; the library allocates nothing
+    st, cap = vsa2.vsa2_route_capacity(P, S)
+    assert st == 0
+    st, rws = vsa2.vsa2_route_workspace(P, S)
+    assert st == 0
+    st, bws = vsa2.vsa2_attn_workspace(P, 1)
+    assert st == 0
+    i32 = torch.int32
+    q_r = torch.empty((p.batch, p.heads_q, N * G, D), dtype=tdt, device=dev)
+    k_r = torch.empty((p.batch, p.heads_kv, N * G, D), dtype=tdt, device=dev)
+    row_ptr = torch.empty(p.batch * p.heads_q * N + 1, dtype=i32, device=dev)
+    col_idx = torch.empty(cap, dtype=i32, device=dev)
+    kv_ptr = torch.empty(p.batch * p.heads_kv * N + 1, dtype=i32, device=dev)
+    kv_idx = torch.empty(cap, dtype=i32, device=dev)
+    rws_t = torch.empty(rws, dtype=torch.uint8, device=dev)
+    bws_t = torch.empty(max(bws, 1), dtype=torch.uint8, device=dev)
+    o = torch.empty_like(q)
+    lse = torch.empty((p.batch, p.heads_q, L), dtype=torch.float32, device=dev)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+
+    def chk(name, status):
+        if status != 0:
+            raise RuntimeError("%s -> %s" % (name, vsa2.STATUS_NAMES.get(status, status)))
+
+    stages = ("pool", "route", "fwd", "bwd")
+    ev = {s: [] for s in stages}
+
+    def step(record):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(5)] if record else None
+        if record:
+            e[0].record(stream)
+        chk("pool", vsa2.vsa2_pool(P, p.heads_q, q.data_ptr(), p.Rt, p.Rh, p.Rw, q_r.data_ptr(), sp))
+        chk("pool", vsa2.vsa2_pool(P, p.heads_kv, k.data_ptr(), p.Rt, p.Rh, p.Rw, k_r.data_ptr(), sp))
+        if record:
+            e[1].record(stream)
+        chk("route", vsa2.vsa2_route(P, S, q_r.data_ptr(), k_r.data_ptr(), row_ptr.data_ptr(),
+                                     col_idx.data_ptr(), cap, kv_ptr.data_ptr(), kv_idx.data_ptr(),
+                                     None, rws_t.data_ptr(), rws, sp))
+        if record:
+            e[2].record(stream)
+        chk("fwd", vsa2.vsa2_attn_fwd(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), row_ptr.data_ptr(),
+                                      col_idx.data_ptr(), cap, o.data_ptr(), lse.data_ptr(), None, 0,
+                                      sp))
+        if record:
+            e[3].record(stream)
+        chk("bwd", vsa2.vsa2_attn_bwd(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                      lse.data_ptr(), do.data_ptr(), row_ptr.data_ptr(),
+                                      col_idx.data_ptr(), kv_ptr.data_ptr(), kv_idx.data_ptr(), cap,
+                                      dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), bws_t.data_ptr(),
+                                      bws, sp))
+        if record:
+            e[4].record(stream)
+            for i, s in enumerate(stages):
+                ev[s].append((e[i], e[i + 1]))
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        step(True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    ms_step = wall * 1e3 / args.steps
+    stage_ms = {s: float(np.mean([a.elapsed_time(b) for a, b in ev[s]])) for s in stages}
+
+    nnz = int(row_ptr[-1].item())
+    flop_fwd = 4.0 * B * B * D * nnz
+    flop_bwd = 10.0 * B * B * D * nnz
+    attn_ms = stage_ms["fwd"] + stage_ms["bwd"]
+    value = (flop_fwd + flop_bwd) / (ms_step * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if p.dtype == 1 else PEAK_F32_TFLOPS
+    achieved_bwd = flop_bwd / (stage_ms["bwd"] * 1e-3) / 1e12
+    out = {
+        "metric": "effective sparse-attn TFLOP/s (fwd+bwd FLOPs over whole-path step time), 720p shape",
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if p.dtype == 1 else "f32",
+        "data": "synthetic (seeded cube-mean + noise video-token tensors, no trained weights)",
+        "config": {
+            "workload": w.name, "batch": p.batch, "grid_THW": [p.T, p.H, p.W], "tokens": L,
+            "heads_q": p.heads_q, "heads_kv": p.heads_kv, "head_dim": D,
+            "cube": [p.Bt, p.Bh, p.Bw], "router_pool": [p.Rt, p.Rh, p.Rw],
+            "select": ("top-%d" % sel.k) if sel.mode == 0 else ("mass-%.2f-cap-%d" % (sel.mass, sel.cap)),
+            "nnz_block_pairs": nnz, "sparsity": round(1.0 - nnz / float(p.batch * p.heads_q * N * N), 4),
+        },
+        "breakdown_ms": {s: round(stage_ms[s], 4) for s in stages},
+        "attn_fwd_bwd_ms": round(attn_ms, 4),
+        "attn_only_tflops": round((flop_fwd + flop_bwd) / (attn_ms * 1e-3) / 1e12, 3),
+        "pct_bf16_peak_attn_only": round(100.0 * (flop_fwd + flop_bwd) / (attn_ms * 1e-3) / 1e12 / peak, 2),
+        "roofline": {
+            "kernel": "vsa2_attn_bwd (delta_kernel + dkdv_kernel + dq_kernel)",
+            "bound": "mfma", "achieved": round(achieved_bwd, 3), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(achieved_bwd / peak, 4), "traffic": None,
+        },
+        "input_gen_s": round(gen_s, 1),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, x, row_ptr, col_idx, args.cpu_rows, args.cpu_kv)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(w, x, row_ptr_t, col_idx_t, nrows_sample, nkv_sample):
+    """The oracle, as it stands, on a bounded sample of the same workload:
+    forward + dQ for `nrows_sample` query-block rows and dK/dV for
+    `nkv_sample` key blocks, on the GPU's block lists.  Credited FLOPs: 4*B^2*D per pair for
+    the forward, 6*B^2*D per pair for dQ (S, dP, dQ products) and 8*B^2*D per
+    pair for dK/dV (S, dP, dV, dK products)."""
+    import oracle
+    p = w.problem
+    rp = row_ptr_t.cpu().numpy()
+    ci = col_idx_t.cpu().numpy()[:rp[-1]]
+    rng = np.random.default_rng(7)
+    nrow = p.batch * p.heads_q * p.N
+    rows = np.sort(rng.choice(nrow, nrows_sample, replace=False)).astype(np.int64)
+    kv_rows = np.sort(rng.choice(p.batch * p.heads_kv * p.N, nkv_sample, replace=False)).astype(np.int64)
+    pairs_q = int(sum(rp[r + 1] - rp[r] for r in rows))
+    kp, _ = oracle.csr_to_csc(rp, ci, p)
+    pairs_kv = int(sum(kp[r + 1] - kp[r] for r in kv_rows))
+    b2d = float(p.B * p.B * p.head_dim)
+    t0 = time.perf_counter()
+    oracle.attn_fwd(x["q"], x["k"], x["v"], p, rp, ci, rows)
+    oracle.attn_bwd_dq(x["q"], x["k"], x["v"], x["do"], p, rp, ci, rows)
+    oracle.attn_bwd_dkdv(x["q"], x["k"], x["v"], x["do"], p, rp, ci, kv_rows)
+    dt = time.perf_counter() - t0
+    flops = b2d * (10.0 * pairs_q + 8.0 * pairs_kv)
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.threads(),
+            "kind": "oracle", "seconds": round(dt, 2),
+            "sample": "%d query-block rows (fwd + dQ, %d block pairs) and %d key blocks (dK/dV, %d pairs) "
+                      "of the %s workload, fp64 C oracle with OpenMP" % (
+                          nrows_sample, pairs_q, nkv_sample, pairs_kv, w.name)}
+
+
+if __name__ == "__main__":
+    main()
