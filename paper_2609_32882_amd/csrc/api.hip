@@ -81,8 +81,16 @@ route_ws route_layout(const vsa2_problem* p, const shape& s) {
     return w;
 }
 
+size_t elem_bytes(const vsa2_problem* p) { return p->dtype == VSA2_BF16 ? 2 : 4; }
+
+// forward: the block-transposed V
+size_t fwd_ws_bytes(const shape& s, const vsa2_problem* p) {
+    return align_up(elem_bytes(p) * static_cast<size_t>(s.rows_kv * s.B) * p->head_dim);
+}
+
 size_t bwd_ws_bytes(const shape& s, const vsa2_problem* p) {
-    return align_up(sizeof(float) * static_cast<size_t>(s.rows_q * s.B)) + (p ? 0 : 0);
+    return vsa2::bwd_workspace_bytes(p->dtype, p->head_dim, p->batch, p->heads_q, p->heads_kv,
+                                     static_cast<int>(s.N));
 }
 
 #define VSA2_TRY_HIP(expr)                          \
@@ -196,7 +204,7 @@ vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* byt
     vsa2_status st = check_problem(p, &s);
     if (st != VSA2_OK) return st;
     if (!bytes) return VSA2_ERR_NULL;
-    if (pass == 0) *bytes = 0;
+    if (pass == 0) *bytes = fwd_ws_bytes(s, p);
     else if (pass == 1) *bytes = bwd_ws_bytes(s, p);
     else return VSA2_ERR_SHAPE;
     return VSA2_OK;
@@ -205,8 +213,6 @@ vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* byt
 vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, const void* v,
                           const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
                           float* lse, void* ws, size_t ws_bytes, hipStream_t stream) {
-    (void)ws;
-    (void)ws_bytes;
     shape s;
     vsa2_status st = check_problem(p, &s);
     if (st != VSA2_OK) return st;
@@ -215,8 +221,10 @@ vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, c
     if (!col_idx && col_cap > 0) return VSA2_ERR_NULL;
     if (col_cap < 0) return VSA2_ERR_CAPACITY;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return VSA2_ERR_ALIGN;
+    if (!ws || ws_bytes < fwd_ws_bytes(s, p)) return VSA2_ERR_WORKSPACE;
+    if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_attn_fwd(p->dtype, p->head_dim, q, k, v, row_ptr, col_idx, col_cap, o, lse,
-                                       p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N), stream));
+                                       ws, p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N), stream));
     return VSA2_OK;
 }
 
@@ -240,7 +248,7 @@ vsa2_status vsa2_attn_bwd(const vsa2_problem* p, const void* q, const void* k, c
     if (!ws || ws_bytes < need) return VSA2_ERR_WORKSPACE;
     if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_attn_bwd(p->dtype, p->head_dim, q, k, v, o, lse, dout, row_ptr, col_idx,
-                                       kv_ptr, kv_idx, col_cap, dq, dk, dv, static_cast<float*>(ws),
+                                       kv_ptr, kv_idx, col_cap, dq, dk, dv, ws,
                                        p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N), stream));
     return VSA2_OK;
 }

@@ -3,11 +3,17 @@
 //
 // One workgroup of two waves per query block (64 queries); wave w owns
 // queries 32w .. 32w+31.  For every key block listed in the block's CSR row:
-//   K tile  [64 keys][D]  -> LDS, row r stored at slot swap_bits_2_3(r)
-//   V tile  [64 keys][D]  -> LDS transposed, V^T [D][64 keys]
-//   S^T = K Q^T           (MFMA 32x32, Q fragments live in registers)
+//   K tile   [64 keys][D]  -> LDS, row r at slot swap_bits_2_3(r)
+//   V^T tile [D][64 keys]  -> LDS (V is block-transposed once per call by
+//                             block_transpose_kernel, so every tile is a
+//                             straight 16 KB copy)
+//   S^T = K Q^T            (MFMA 32x32, Q fragments live in registers)
 //   online softmax in fp32 registers (exp2, log2(e)/sqrt(D) folded in)
-//   O^T += V^T P^T        (P rounded to the input dtype, MFMA 32x32)
+//   O^T += V^T P^T         (P rounded to the input dtype, MFMA 32x32)
+// Tiles arrive by global_load_lds (no staging registers).  The K and V
+// buffers are refilled as soon as their last reader is done: the next K tile
+// streams in during this tile's softmax and PV product, the next V tile
+// during the next S product.
 // In the transposed products a lane owns one query column, so the row max
 // and row sum need one exchange with the other half-wave and nothing else.
 #include "common.hpp"
@@ -17,9 +23,53 @@ namespace vsa2 {
 
 constexpr int AF_NT = 128;
 
+// x [nblk][64][D] -> xt [nblk][D][64]; one workgroup per 64-row block.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void block_transpose_kernel(const T* __restrict__ x, T* __restrict__ xt,
+                                                              int64_t nblk) {
+    constexpr int PAD = 16 / sizeof(T);
+    __shared__ T tile[64][D + PAD];
+    const int64_t blk = blockIdx.x;
+    if (blk >= nblk) return;
+    const T* src = x + blk * 64 * D;
+    constexpr int VEC = 16 / sizeof(T);          // elements per 16-byte load
+    for (int i = threadIdx.x; i < 64 * D / VEC; i += 256) {
+        const int r = i / (D / VEC), c = (i % (D / VEC)) * VEC;
+        *reinterpret_cast<uint4*>(&tile[r][c]) = *reinterpret_cast<const uint4*>(src + r * D + c);
+    }
+    __syncthreads();
+    T* dst = xt + blk * 64 * D;
+    for (int i = threadIdx.x; i < 64 * D / VEC; i += 256) {
+        const int d = i / (64 / VEC), k0 = (i % (64 / VEC)) * VEC;
+        T v[VEC];
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) v[j] = tile[k0 + j][d];
+        *reinterpret_cast<uint4*>(dst + d * 64 + k0) = *reinterpret_cast<const uint4*>(v);
+    }
+}
+
+template <typename T, int D>
+hipError_t launch_block_transpose_t(const void* x, void* xt, int64_t nblk, hipStream_t s) {
+    if (nblk == 0) return hipSuccess;
+    hipLaunchKernelGGL((block_transpose_kernel<T, D>), dim3(static_cast<unsigned>(nblk)), dim3(256), 0, s,
+                       static_cast<const T*>(x), static_cast<T*>(xt), nblk);
+    return hipGetLastError();
+}
+
+hipError_t launch_block_transpose(int dtype, int D, const void* x, void* xt, int64_t nblk, hipStream_t s) {
+    if (dtype == 1) {
+        if (D == 64) return launch_block_transpose_t<bf16_t, 64>(x, xt, nblk, s);
+        if (D == 128) return launch_block_transpose_t<bf16_t, 128>(x, xt, nblk, s);
+    } else {
+        if (D == 64) return launch_block_transpose_t<float, 64>(x, xt, nblk, s);
+        if (D == 128) return launch_block_transpose_t<float, 128>(x, xt, nblk, s);
+    }
+    return hipErrorInvalidValue;
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
-    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ vt,
     const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx, int64_t col_cap,
     T* __restrict__ o, float* __restrict__ lse, int Hq, int Hkv, int N, float c_log2) {
     using F = typename frag_of<T>::type;
@@ -28,10 +78,10 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     constexpr int MT = D / 32;        // 32-row tiles of O^T
     constexpr int KRB = D * E;        // K tile row bytes
     constexpr int VRB = 64 * E;       // V^T tile row bytes
-    using KL = tile_rows<T, D, AF_NT>;
-    using VL = tile_transposed<T, D, AF_NT>;
-    __shared__ __align__(16) char k_lds[64 * KRB];
-    __shared__ __align__(16) char v_lds[D * VRB];
+    using KT = async_tile<64, KRB, 2, true>;
+    using VT = async_tile<D, VRB, 2, false>;
+    __shared__ __align__(1024) char k_lds[KT::BYTES];
+    __shared__ __align__(1024) char v_lds[VT::BYTES];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
     const int64_t row = blockIdx.x;
@@ -40,8 +90,8 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     const int b = static_cast<int>(bh / Hq), h = static_cast<int>(bh % Hq);
     const int hkv = h / (Hq / Hkv);
     const int64_t L = static_cast<int64_t>(N) * 64;
-    const T* kb = k + static_cast<int64_t>(b * Hkv + hkv) * L * D;
-    const T* vb = v + static_cast<int64_t>(b * Hkv + hkv) * L * D;
+    const char* kb = reinterpret_cast<const char*>(k + static_cast<int64_t>(b * Hkv + hkv) * L * D);
+    const char* vb = reinterpret_cast<const char*>(vt + static_cast<int64_t>(b * Hkv + hkv) * L * D);
     const int64_t qtok = bh * L + static_cast<int64_t>(n) * 64 + wave * 32 + (lane & 31);
 
     int64_t e0 = row_ptr[row], e1 = row_ptr[row + 1];
@@ -59,18 +109,29 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
         for (int i = 0; i < 16; ++i) oacc[mt][i] = 0.f;
     float m = -INFINITY, l = 0.f;
 
-    KL kt;
-    VL vt;
+    // entries outside [0, N) are loaded as block 0 and then ignored
+    auto block_of = [&](int64_t e) -> int {
+        const int c = scalar_load_i32(col_idx + e);
+        return (c >= 0 && c < N) ? c : -1;
+    };
+    const KT kt(wave, lane);
+    const VT vt_(wave, lane);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) settle(qf[ks]);   // fragments in registers before the copies start
+    int c_cur = -1;
+    if (e0 < e1) {
+        c_cur = block_of(e0);
+        const int cc = c_cur < 0 ? 0 : c_cur;
+        kt.issue(k_lds, kb + static_cast<int64_t>(cc) * 64 * KRB, wave);
+        vt_.issue(v_lds, vb + static_cast<int64_t>(cc) * 64 * KRB, wave);
+    }
     for (int64_t e = e0; e < e1; ++e) {
-        const int c = col_idx[e];
-        if (c < 0 || c >= N) continue;          // malformed entry: skipped, never read
-        kt.load(kb, static_cast<int64_t>(c) * 64, L, tid);
-        vt.load(vb, static_cast<int64_t>(c) * 64, tid);
-        __syncthreads();                         // previous tile fully consumed
-        kt.store(k_lds, true, tid);
-        vt.store(v_lds, tid);
-        __syncthreads();
+        const bool has_next = e + 1 < e1;
+        const int c_next = has_next ? block_of(e + 1) : -1;
+        const int64_t nxt_off = static_cast<int64_t>(c_next < 0 ? 0 : c_next) * 64 * KRB;
 
+        vm_wait<VT::PER_WAVE>();          // this K tile has landed (V may still stream)
+        wg_barrier();
         // S^T for 64 keys x 32 queries (two 32-key tiles)
         f32x16_t s[2];
 #pragma unroll
@@ -80,52 +141,63 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
                 F a;
-                lds_frag<KRB>(a, k_lds, t2 * 32 + (lane & 31), ks * 16 + half * 8);
+                lds_frag_s<KRB>(a, k_lds, t2 * 32 + (lane & 31), ks * 16 + half * 8);
                 mma(s[t2], a, qf[ks]);
             }
         }
-        // online softmax over this lane's query column
-        float mx = -INFINITY;
+        wg_barrier();                      // K buffer free
+        if (has_next) kt.issue(k_lds, kb + nxt_off, wave);
+
+        if (c_cur >= 0) {
+            float mx = -INFINITY;
 #pragma unroll
-        for (int t2 = 0; t2 < 2; ++t2)
+            for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                s[t2][i] *= c_log2;
-                mx = fmaxf(mx, s[t2][i]);
-            }
-        mx = fmaxf(mx, swap_half(mx));
-        const float mn = fmaxf(m, mx);
-        const float alpha = exp2f(m - mn);
-        float ps = 0.f;
+                for (int i = 0; i < 16; ++i) {
+                    s[t2][i] *= c_log2;
+                    mx = fmaxf(mx, s[t2][i]);
+                }
+            mx = fmaxf(mx, swap_half(mx));
+            const float mn = fmaxf(m, mx);
+            const float alpha = fast_exp2(m - mn);
+            float ps = 0.f;
 #pragma unroll
-        for (int t2 = 0; t2 < 2; ++t2)
+            for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const float p = exp2f(s[t2][i] - mn);
-                s[t2][i] = p;
-                ps += p;
-            }
-        l = l * alpha + ps;
-        m = mn;
+                for (int i = 0; i < 16; ++i) {
+                    const float p = fast_exp2(s[t2][i] - mn);
+                    s[t2][i] = p;
+                    ps += p;
+                }
+            l = l * alpha + ps;
+            m = mn;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+            for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) oacc[mt][i] *= alpha;
-        // O^T += V^T P^T over 4 k-steps of 16 keys: keys 16kk + 8half + (0..7)
+                for (int i = 0; i < 16; ++i) oacc[mt][i] *= alpha;
+        }
+        if (has_next) vm_wait<KT::PER_WAVE>(); else vm_wait<0>();   // V tile landed
+        wg_barrier();
+        if (c_cur >= 0) {
+            // O^T += V^T P^T over 4 k-steps of 16 keys: keys 16kk + 8half + (0..7)
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-            F pb;
-            float pv[8];
+            for (int kk = 0; kk < 4; ++kk) {
+                F pb;
+                float pv[8];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) pv[i] = s[kk >> 1][(kk & 1) * 8 + i];
-            pack_frag(pb, pv);
+                for (int i = 0; i < 8; ++i) pv[i] = s[kk >> 1][(kk & 1) * 8 + i];
+                pack_frag(pb, pv);
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                F a;
-                lds_frag<VRB>(a, v_lds, mt * 32 + (lane & 31), kk * 16 + half * 8);
-                mma(oacc[mt], a, pb);
+                for (int mt = 0; mt < MT; ++mt) {
+                    F a;
+                    lds_frag_s<VRB>(a, v_lds, mt * 32 + (lane & 31), kk * 16 + half * 8);
+                    mma(oacc[mt], a, pb);
+                }
             }
         }
+        wg_barrier();                      // V buffer free
+        if (has_next) vt_.issue(v_lds, vb + nxt_off, wave);
+        c_cur = c_next;
     }
 
     const float lt = l + swap_half(l);
@@ -137,10 +209,8 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
         for (int g4 = 0; g4 < 4; ++g4) {
             const int d0 = mt * 32 + g4 * 8 + half * 4;
             if constexpr (E == 2) {
-                const uint32_t w0 = static_cast<uint32_t>(f32_to_bf16(oacc[mt][g4 * 4 + 0] * inv)) |
-                                    (static_cast<uint32_t>(f32_to_bf16(oacc[mt][g4 * 4 + 1] * inv)) << 16);
-                const uint32_t w1 = static_cast<uint32_t>(f32_to_bf16(oacc[mt][g4 * 4 + 2] * inv)) |
-                                    (static_cast<uint32_t>(f32_to_bf16(oacc[mt][g4 * 4 + 3] * inv)) << 16);
+                const uint32_t w0 = pack2_bf16(oacc[mt][g4 * 4 + 0] * inv, oacc[mt][g4 * 4 + 1] * inv);
+                const uint32_t w1 = pack2_bf16(oacc[mt][g4 * 4 + 2] * inv, oacc[mt][g4 * 4 + 3] * inv);
                 *reinterpret_cast<uint2*>(orow + d0) = make_uint2(w0, w1);
             } else {
                 *reinterpret_cast<float4*>(orow + d0) =
@@ -154,25 +224,27 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
 template <typename T, int D>
 static hipError_t launch_fwd_t(const void* q, const void* k, const void* v, const int32_t* row_ptr,
                                const int32_t* col_idx, int64_t col_cap, void* o, float* lse,
-                               int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                               void* vt, int batch, int Hq, int Hkv, int N, hipStream_t s) {
     const int64_t rows = static_cast<int64_t>(batch) * Hq * N;
     if (rows == 0) return hipSuccess;
+    hipError_t e = launch_block_transpose_t<T, D>(v, vt, static_cast<int64_t>(batch) * Hkv * N, s);
+    if (e != hipSuccess) return e;
     const float c = 1.4426950408889634f / sqrtf(static_cast<float>(D));
     hipLaunchKernelGGL((attn_fwd_kernel<T, D>), dim3(static_cast<unsigned>(rows)), dim3(AF_NT), 0, s,
-                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(vt),
                        row_ptr, col_idx, col_cap, static_cast<T*>(o), lse, Hq, Hkv, N, c);
     return hipGetLastError();
 }
 
 hipError_t launch_attn_fwd(int dtype, int D, const void* q, const void* k, const void* v,
                            const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
-                           float* lse, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                           float* lse, void* vt, int batch, int Hq, int Hkv, int N, hipStream_t s) {
     if (dtype == 1) {
-        if (D == 64) return launch_fwd_t<bf16_t, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, batch, Hq, Hkv, N, s);
-        if (D == 128) return launch_fwd_t<bf16_t, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, batch, Hq, Hkv, N, s);
+        if (D == 64) return launch_fwd_t<bf16_t, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, vt, batch, Hq, Hkv, N, s);
+        if (D == 128) return launch_fwd_t<bf16_t, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, vt, batch, Hq, Hkv, N, s);
     } else {
-        if (D == 64) return launch_fwd_t<float, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, batch, Hq, Hkv, N, s);
-        if (D == 128) return launch_fwd_t<float, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, batch, Hq, Hkv, N, s);
+        if (D == 64) return launch_fwd_t<float, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, vt, batch, Hq, Hkv, N, s);
+        if (D == 128) return launch_fwd_t<float, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, vt, batch, Hq, Hkv, N, s);
     }
     return hipErrorInvalidValue;
 }

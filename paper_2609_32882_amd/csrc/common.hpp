@@ -20,13 +20,21 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
     return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }
 
-// Round-to-nearest-even float -> bf16 (NaN kept quiet).
-__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return static_cast<uint16_t>((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return static_cast<uint16_t>(u >> 16);
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_vt;
+typedef __attribute__((ext_vector_type(2))) float f32x2_vt;
+
+// Round-to-nearest-even float -> bf16 with the hardware conversion
+// (v_cvt_pk_bf16_f32), two values per instruction.
+__device__ __forceinline__ uint32_t pack2_bf16(float lo, float hi) {
+    const f32x2_vt v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_vt));
 }
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    return static_cast<uint16_t>(pack2_bf16(f, 0.f) & 0xffffu);
+}
+
+// 2^x with the hardware exponential (v_exp_f32).
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Round-to-nearest-even double -> bf16 in one rounding: truncate to float
 // with a sticky bit in the last place (round-to-odd), then round the float.
@@ -88,15 +96,26 @@ __device__ __forceinline__ void pack_frag(frag_bf16& f, const float* x) {
     typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4_t;
     u32x4_t w;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-        w[i] = static_cast<uint32_t>(f32_to_bf16(x[2 * i])) |
-               (static_cast<uint32_t>(f32_to_bf16(x[2 * i + 1])) << 16);
+    for (int i = 0; i < 4; ++i) w[i] = pack2_bf16(x[2 * i], x[2 * i + 1]);
     f.v = __builtin_bit_cast(bf16x8_t, w);
 }
 __device__ __forceinline__ void pack_frag(frag_f32& f, const float* x) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) f.v[i] = x[i];
 }
+
+// Make the compiler complete the loads of a fragment here (an opaque use of
+// its registers), so no wait for them is left inside a later loop.
+__device__ __forceinline__ void settle(const frag_bf16& f) {
+    typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4_t;
+    const u32x4_t u = __builtin_bit_cast(u32x4_t, f.v);
+    asm volatile("" ::"v"(u[0]), "v"(u[1]), "v"(u[2]), "v"(u[3]));
+}
+__device__ __forceinline__ void settle(const frag_f32& f) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) asm volatile("" ::"v"(f.v[i]));
+}
+__device__ __forceinline__ void settle(float x) { asm volatile("" ::"v"(x)); }
 
 // Exchange with the lane 32 positions away (the other half of the wave).
 __device__ __forceinline__ float swap_half(float x) { return __shfl_xor(x, 32, 64); }
@@ -248,5 +267,111 @@ struct tile_transposed {
         }
     }
 };
+
+}  // namespace vsa2
+
+namespace vsa2 {
+
+// ---------------------------------------------------------------------------
+// Asynchronous global -> LDS tile copies (global_load_lds_dwordx4).
+//
+// A tile is ROWS rows of RB bytes (row-major in global memory, row stride
+// RB).  One wave instruction writes 1 KB of LDS (lane l -> base + 16 l), so
+// each lane fetches whatever unit lands at its physical position.  Loads are
+// tracked by vmcnt; callers wait with vm_wait<n>() (at most n of the most
+// recent vector-memory operations still outstanding) and make the data
+// visible with a raw s_barrier.
+// ---------------------------------------------------------------------------
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    // gfx9 s_waitcnt: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14]
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+    asm volatile("" ::: "memory");
+}
+
+// Workgroup barrier without the memory fence of __syncthreads (which would
+// wait for every outstanding global_load_lds).  The empty asm statements keep
+// the compiler from moving LDS accesses across it; the caller has already
+// waited (vm_wait) for the tiles it is about to publish.
+__device__ __forceinline__ void wg_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// Wave-uniform 32-bit load through the scalar cache.  Used for block-list
+// entries inside the pipelined loops: a vector load there would be counted by
+// vmcnt together with the asynchronous tile copies and make the compiler wait
+// for all of them before its first use.
+__device__ __forceinline__ int32_t scalar_load_i32(const int32_t* p) {
+    int32_t v;
+    asm volatile("s_load_dword %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(p) : "memory");
+    return v;
+}
+
+// One global_load_lds_dwordx4: lane l copies 16 bytes from base + voff(l) to
+// LDS byte address lds + 16 l.  Issued as inline assembly so that the
+// compiler's own wait-count bookkeeping, which cannot tell the LDS buffers
+// apart, does not put a full vmcnt(0) wait in front of every LDS read; the
+// kernels order these copies themselves with vm_wait and wg_barrier.
+__device__ __forceinline__ void dma16(uint32_t lds, const void* base, int voff) {
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :
+                 : "s"(lds), "v"(voff), "s"(base)
+                 : "memory", "m0");
+}
+
+// LDS tiles are stored with a row stride of RB + 16 bytes: 16 lanes reading
+// the same 16-byte column of 16 consecutive rows then hit 16 different bank
+// groups, and every fragment address is one per-lane base plus a compile-time
+// offset (no per-fragment address registers).  Rows are permuted with
+// swap_bits_2_3 when PERM: LDS row r holds global row swap_bits_2_3(r).  A
+// tile is copied by whole 1 KB wave instructions; lanes whose destination is
+// a pad slot (or past the last row) fetch the tile's first 16 bytes again.
+// The per-lane source offsets are the same for every tile of a shape: they
+// are computed once and each issue adds a wave-uniform tile base.
+template <int ROWS, int RB, int NW, bool PERM>
+struct async_tile {
+    static constexpr int STRIDE = RB + 16;
+    static constexpr int NI = ((ROWS * STRIDE + 1023) / 1024 + NW - 1) / NW * NW;  // 1 KB instructions
+    static constexpr int BYTES = NI * 1024;        // LDS bytes to allocate
+    static constexpr int PER_WAVE = NI / NW;
+    static_assert(RB % 16 == 0, "row bytes");
+    int off[PER_WAVE];
+
+    __device__ __forceinline__ async_tile(int wave, int lane) {
+#pragma unroll
+        for (int j = 0; j < PER_WAVE; ++j) {
+            const int p = (wave * PER_WAVE + j) * 1024 + lane * 16;   // physical LDS byte
+            const int row = p / STRIDE, col = p % STRIDE;
+            const bool data = row < ROWS && col < RB;
+            off[j] = data ? (PERM ? swap_bits_2_3(row) : row) * RB + col : 0;
+        }
+    }
+    __device__ __forceinline__ void issue(char* lds, const char* g, int wave) const {
+        const uint32_t l0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)lds));
+#pragma unroll
+        for (int j = 0; j < PER_WAVE; ++j) dma16(l0 + (wave * PER_WAVE + j) * 1024, g, off[j]);
+    }
+};
+
+// Fragment of 8 consecutive elements starting at element e0 of row `row` of
+// a padded LDS tile with RB-byte rows.
+template <int RB>
+__device__ __forceinline__ void lds_frag_s(frag_bf16& f, const char* tile, int row, int e0) {
+    load_frag(f, tile + row * (RB + 16) + e0 * 2);
+}
+template <int RB>
+__device__ __forceinline__ void lds_frag_s(frag_f32& f, const char* tile, int row, int e0) {
+    const float4 a = *reinterpret_cast<const float4*>(tile + row * (RB + 16) + e0 * 4);
+    const float4 b = *reinterpret_cast<const float4*>(tile + row * (RB + 16) + e0 * 4 + 16);
+    f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
+    f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
+}
 
 }  // namespace vsa2

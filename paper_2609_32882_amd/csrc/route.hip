@@ -186,8 +186,8 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
 #pragma unroll
                 for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) s += exp2f(acc[kt][qt][v] - mn);
-                l[qt] = l[qt] * exp2f(m[qt] - mn) + s;
+                    for (int v = 0; v < 16; ++v) s += fast_exp2(acc[kt][qt][v] - mn);
+                l[qt] = l[qt] * fast_exp2(m[qt] - mn) + s;
                 m[qt] = mn;
             }
         } else {
@@ -208,7 +208,7 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
                             for (int u = 0; u < G; ++u) {
                                 const int v = run * 8 + i * G + u;
                                 const int64_t j = j0 + kt * 32 + run * 16 + half * 8 + i * G + u;
-                                s += j < NG ? exp2f(acc[kt][qt][v] * c_log2 - lq[qt]) : 0.f;
+                                s += j < NG ? fast_exp2(acc[kt][qt][v] * c_log2 - lq[qt]) : 0.f;
                             }
                             // sum over the G pooled queries of the block (G adjacent lanes)
 #pragma unroll
