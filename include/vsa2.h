@@ -156,9 +156,8 @@ vsa2_status vsa2_route(const vsa2_problem* p, const vsa2_select* s,
                        int32_t* kv_ptr, int32_t* kv_idx,
                        float* block_scores, void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Bytes of workspace vsa2_attn_fwd (pass 0) or vsa2_attn_bwd (pass 1) needs:
- * the forward keeps a block-transposed copy of V ([64-token block][D][64]),
- * the backward per-query (LSE, Delta) pairs and block-transposed Q, dO, K. */
+/* Bytes of workspace vsa2_attn_fwd (pass 0: none) or vsa2_attn_bwd (pass 1:
+ * one fp32 (LSE, Delta) pair per query token) needs. */
 vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* bytes);
 
 /*
@@ -173,8 +172,8 @@ vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* byt
  *   o   [batch][Hq][L][D] output, dtype p->dtype.
  *   lse [batch][Hq][L] fp32 natural-log log-sum-exp of each query's scaled
  *       scores; a query block with no selected block gets o = 0, lse = -inf.
- *   ws, ws_bytes  workspace of at least vsa2_attn_workspace(p, 0) bytes,
- *       256-byte aligned.
+ *   ws, ws_bytes  workspace of vsa2_attn_workspace(p, 0) bytes (zero: ws may
+ *       be NULL).
  * Errors: NULL pointers, shape/dtype, misalignment, small workspace.
  */
 vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, const void* v,

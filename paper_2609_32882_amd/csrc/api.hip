@@ -81,12 +81,8 @@ route_ws route_layout(const vsa2_problem* p, const shape& s) {
     return w;
 }
 
-size_t elem_bytes(const vsa2_problem* p) { return p->dtype == VSA2_BF16 ? 2 : 4; }
-
-// forward: the block-transposed V
-size_t fwd_ws_bytes(const shape& s, const vsa2_problem* p) {
-    return align_up(elem_bytes(p) * static_cast<size_t>(s.rows_kv * s.B) * p->head_dim);
-}
+// the forward needs no scratch memory
+size_t fwd_ws_bytes(const shape&, const vsa2_problem*) { return 0; }
 
 size_t bwd_ws_bytes(const shape& s, const vsa2_problem* p) {
     return vsa2::bwd_workspace_bytes(p->dtype, p->head_dim, p->batch, p->heads_q, p->heads_kv,
@@ -221,10 +217,10 @@ vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, c
     if (!col_idx && col_cap > 0) return VSA2_ERR_NULL;
     if (col_cap < 0) return VSA2_ERR_CAPACITY;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return VSA2_ERR_ALIGN;
-    if (!ws || ws_bytes < fwd_ws_bytes(s, p)) return VSA2_ERR_WORKSPACE;
-    if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
+    if (ws_bytes < fwd_ws_bytes(s, p)) return VSA2_ERR_WORKSPACE;
+    (void)ws;
     VSA2_TRY_HIP(vsa2::launch_attn_fwd(p->dtype, p->head_dim, q, k, v, row_ptr, col_idx, col_cap, o, lse,
-                                       ws, p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N), stream));
+                                       p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N), stream));
     return VSA2_OK;
 }
 

@@ -6,7 +6,6 @@
 //   dV = P^T dO,  dK = dS^T Q / sqrt(D),  dQ = dS K / sqrt(D)
 // Kernels, all deterministic (no atomics):
 //   stat_kernel      per query token: (LSE * log2(e), Delta)
-//   block transposes Q^T, dO^T and K^T per 64-token block (workspace)
 //   dkdv_kernel      key-block stationary: one workgroup per key block walks
 //                    the transposed (CSC) list of query blocks that selected
 //                    it; a wave owns 32 keys; one launch accumulates dV^T,
@@ -16,8 +15,11 @@
 // Products are arranged so that each lane owns one column (a key in dkdv, a
 // query in dq) and its 16 accumulator rows form two runs of 8 consecutive
 // rows (tiles stored with the bit-2/3 slot swap): a lane's P / dS values are
-// directly the B operand of the next MFMA.  Tiles stream into LDS with
-// global_load_lds; each buffer is refilled as soon as its last reader is done.
+// directly the B operand of the next MFMA.  Every tile is a row-major
+// [64 tokens][D] copy; the transposed operands (Q^T, dO^T, K^T) are read from
+// the same tiles with transposing LDS reads.  Tiles stream into LDS with
+// asynchronous global_load_lds copies; each buffer is refilled as soon as
+// its last reader is done.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -52,31 +54,28 @@ __global__ __launch_bounds__(256) void stat_kernel(const T* __restrict__ o, cons
 // ---------------------------------------------------------------------------
 // dV (GRAD = 0) or dK (GRAD = 1): one workgroup (2 waves) per key block of
 // head (b, hkv); a wave owns 32 keys.  The two gradients run as separate
-// launches so each keeps one accumulator set (64 registers) and two waves
-// fit per SIMD; the price is recomputing S once more per block pair.
-//   dV^T += dO^T P            (tiles: Q rows for S, dO^T)
-//   dK^T += Q^T dS            (tiles: Q and dO rows for S and dP, Q^T)
+// launches so each keeps one accumulator set (64 registers); the price is
+// recomputing S once more per block pair.
+//   dV^T += dO^T P    tiles Q (for S) and dO (for dO^T)
+//   dK^T += Q^T dS    tiles Q (for S and Q^T) and dO (for dP)
 // ---------------------------------------------------------------------------
 template <typename T, int D, int GRAD>
-__global__ __launch_bounds__(AB_NT, 2) void dkdv_kernel(
-    const T* __restrict__ q, const T* __restrict__ qt, const T* __restrict__ k, const T* __restrict__ v,
-    const T* __restrict__ dout, const T* __restrict__ doutt, const float2* __restrict__ stat,
+__global__ __launch_bounds__(AB_NT, GRAD == 1 ? 1 : 2) void dkdv_kernel(
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+    const T* __restrict__ dout, const float2* __restrict__ stat,
     const int32_t* __restrict__ kv_ptr, const int32_t* __restrict__ kv_idx, int64_t col_cap,
     T* __restrict__ dgrad, int Hq, int Hkv, int N, float c_log2, float scale) {
     using F = typename frag_of<T>::type;
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;
     constexpr int MT = D / 32;
-    constexpr int RRB = D * E;      // row-major tile row bytes
-    constexpr int TRB = 64 * E;     // transposed tile row bytes
-    using RT = async_tile<64, RRB, 2, true>;     // Q, dO rows (slot-swapped)
-    using TT = async_tile<D, TRB, 2, false>;     // dO^T (dV) or Q^T (dK)
+    constexpr int RB = D * E;                    // tile row bytes
+    using RT = async_tile<64, RB, 2, true>;      // Q, dO rows (slot-swapped)
     __shared__ __align__(1024) char q_lds[RT::BYTES];
-    __shared__ __align__(1024) char o_lds[GRAD == 1 ? RT::BYTES : 16];
-    __shared__ __align__(1024) char t_lds[TT::BYTES];
+    __shared__ __align__(1024) char o_lds[RT::BYTES];
     __shared__ __align__(1024) float2 st_lds[64];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+    const int tid = threadIdx.x, lane = tid & 63, wave = wave_id(), half = lane >> 5;
     const int64_t krow = blockIdx.x;                 // (b*Hkv + hkv)*N + nk
     const int64_t bkv = krow / N;
     const int nk = static_cast<int>(krow % N);
@@ -111,22 +110,20 @@ __global__ __launch_bounds__(AB_NT, 2) void dkdv_kernel(
         return bh * L + static_cast<int64_t>(ent % N) * 64;
     };
     const RT rt(wave, lane);
-    const TT tt(wave, lane);
-    auto issue_rows = [&](int64_t q0) {
+    // (LSE, Delta) of the 64 queries: 512 bytes, 16 lanes of each wave
+    auto issue_q = [&](int64_t q0) {
         const int64_t o0 = q0 < 0 ? 0 : q0;
         rt.issue(q_lds, reinterpret_cast<const char*>(q + o0 * D), wave);
-        if constexpr (GRAD == 1) rt.issue(o_lds, reinterpret_cast<const char*>(dout + o0 * D), wave);
-        // (LSE, Delta) of the 64 queries: 512 bytes, 16 lanes of each wave
         if (lane < 16)
             dma16(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)st_lds)) + wave * 256,
                   reinterpret_cast<const char*>(stat + o0) + wave * 256, lane * 16);
     };
-    auto issue_tr = [&](int64_t q0) {
+    auto issue_o = [&](int64_t q0) {
         const int64_t o0 = q0 < 0 ? 0 : q0;
-        tt.issue(t_lds, reinterpret_cast<const char*>((GRAD == 1 ? qt : doutt) + o0 * D), wave);
+        rt.issue(o_lds, reinterpret_cast<const char*>(dout + o0 * D), wave);
     };
-    constexpr int ROWS_OPS = (GRAD == 1 ? 2 : 1) * RT::PER_WAVE + 1;
-    constexpr int TR_OPS = TT::PER_WAVE;
+    constexpr int Q_OPS = RT::PER_WAVE + 1;
+    constexpr int O_OPS = RT::PER_WAVE;
 
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {   // fragments in registers before the copies start
@@ -136,15 +133,16 @@ __global__ __launch_bounds__(AB_NT, 2) void dkdv_kernel(
     int64_t q_cur = -1;
     if (e0 < e1) {
         q_cur = q0_of(e0);
-        issue_rows(q_cur);
-        issue_tr(q_cur);
+        issue_q(q_cur);
+        issue_o(q_cur);
     }
     for (int64_t e = e0; e < e1; ++e) {
         const bool has_next = e + 1 < e1;
         const int64_t q_next = has_next ? q0_of(e + 1) : -1;
         const bool valid = q_cur >= 0;
 
-        vm_wait<TR_OPS>();              // rows and stats landed
+        // dV: the dO tile may still stream in; dK: dP needs it now
+        if constexpr (GRAD == 0) vm_wait<O_OPS>(); else vm_wait<0>();
         wg_barrier();
         F fb[2][2];                     // P (dV) or dS (dK) by [query tile][k-step half]
 #pragma unroll
@@ -156,13 +154,11 @@ __global__ __launch_bounds__(AB_NT, 2) void dkdv_kernel(
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
                 F a;
-                lds_frag_s<RRB>(a, q_lds, qtile * 32 + (lane & 31), ks * 16 + half * 8);
+                lds_frag_s<RB>(a, q_lds, qtile * 32 + (lane & 31), ks * 16 + half * 8);
                 mma(s, a, kf[ks]);
                 if constexpr (GRAD == 1) {
-                    lds_frag_s<RRB>(a, o_lds, qtile * 32 + (lane & 31), ks * 16 + half * 8);
+                    lds_frag_s<RB>(a, o_lds, qtile * 32 + (lane & 31), ks * 16 + half * 8);
                     mma(dp, a, vf[ks]);
-                    // bound how far the scheduler hoists LDS reads (register pressure)
-                    __builtin_amdgcn_sched_barrier(0);
                 }
             }
             // entry i is query 32qtile + 16(i/8) + 8half + i%8
@@ -176,24 +172,35 @@ __global__ __launch_bounds__(AB_NT, 2) void dkdv_kernel(
             pack_frag(fb[qtile][0], x);
             pack_frag(fb[qtile][1], x + 8);
         }
-        wg_barrier();                   // row buffers free
-        if (has_next) issue_rows(q_next);
-        if (has_next) vm_wait<ROWS_OPS>(); else vm_wait<0>();   // transposed tile landed
         wg_barrier();
+        if constexpr (GRAD == 0) {
+            // Q tile free: stream the next one during the dV product
+            if (has_next) issue_q(q_next);
+            if (has_next) vm_wait<Q_OPS>(); else vm_wait<0>();   // dO landed
+            wg_barrier();
+        } else {
+            // dO tile free: stream the next one during the dK product
+            if (has_next) issue_o(q_next);
+        }
         if (valid) {
-            // acc^T += X^T F over the 64 queries (4 k-steps), X = dO (dV) or Q (dK)
+            // acc^T += X^T F over the 64 queries (4 k-steps); X = dO (dV) or Q (dK),
+            // read transposed from its row-major tile
+            const char* xt = GRAD == 1 ? q_lds : o_lds;
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
                     F a;
-                    lds_frag_s<TRB>(a, t_lds, mt * 32 + (lane & 31), kk * 16 + half * 8);
+                    lds_frag_tr<RB, true>(a, xt, mt * 32, kk * 16);
                     mma(acc[mt], a, fb[kk >> 1][kk & 1]);
-                    if (GRAD == 1 && mt % 2 == 1) __builtin_amdgcn_sched_barrier(0);
                 }
         }
-        wg_barrier();                   // transposed buffer free
-        if (has_next) issue_tr(q_next);
+        wg_barrier();
+        if constexpr (GRAD == 0) {
+            if (has_next) issue_o(q_next);
+        } else {
+            if (has_next) issue_q(q_next);
+        }
         q_cur = q_next;
     }
 
@@ -219,10 +226,11 @@ __global__ __launch_bounds__(AB_NT, 2) void dkdv_kernel(
 
 // ---------------------------------------------------------------------------
 // dQ: one workgroup (2 waves) per query block; wave owns 32 queries.
+// Tiles K (for S^T and, read transposed, K^T) and V (for dP^T).
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
-    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ kt, const T* __restrict__ v,
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float2* __restrict__ stat,
     const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx, int64_t col_cap,
     T* __restrict__ dq, int Hq, int Hkv, int N, float c_log2, float scale) {
@@ -230,15 +238,12 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;
     constexpr int MT = D / 32;
-    constexpr int RRB = D * E;
-    constexpr int TRB = 64 * E;
-    using RT = async_tile<64, RRB, 2, true>;     // K, V rows (slot-swapped)
-    using TT = async_tile<D, TRB, 2, false>;     // K^T
+    constexpr int RB = D * E;
+    using RT = async_tile<64, RB, 2, true>;     // K, V rows (slot-swapped)
     __shared__ __align__(1024) char k_lds[RT::BYTES];
     __shared__ __align__(1024) char v_lds[RT::BYTES];
-    __shared__ __align__(1024) char kt_lds[TT::BYTES];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+    const int tid = threadIdx.x, lane = tid & 63, wave = wave_id(), half = lane >> 5;
     const int64_t row = blockIdx.x;
     const int64_t bh = row / N;
     const int n = static_cast<int>(row % N);
@@ -246,7 +251,6 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     const int hkv = h / (Hq / Hkv);
     const int64_t L = static_cast<int64_t>(N) * 64;
     const char* kb = reinterpret_cast<const char*>(k + static_cast<int64_t>(b * Hkv + hkv) * L * D);
-    const char* ktb = reinterpret_cast<const char*>(kt + static_cast<int64_t>(b * Hkv + hkv) * L * D);
     const char* vb = reinterpret_cast<const char*>(v + static_cast<int64_t>(b * Hkv + hkv) * L * D);
     const int64_t qtok = bh * L + static_cast<int64_t>(n) * 64 + wave * 32 + (lane & 31);
 
@@ -271,19 +275,10 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
         const int c = scalar_load_i32(col_idx + e);
         return (c >= 0 && c < N) ? c : -1;
     };
-    constexpr int64_t TILE = 64 * RRB;
+    constexpr int64_t TILE = 64 * RB;
     const RT rt(wave, lane);
-    const TT tt(wave, lane);
-    auto issue_rows = [&](int c) {
-        const int64_t off = static_cast<int64_t>(c < 0 ? 0 : c) * TILE;
-        rt.issue(k_lds, kb + off, wave);
-        rt.issue(v_lds, vb + off, wave);
-    };
-    auto issue_tr = [&](int c) {
-        tt.issue(kt_lds, ktb + static_cast<int64_t>(c < 0 ? 0 : c) * TILE, wave);
-    };
-    constexpr int ROWS_OPS = 2 * RT::PER_WAVE;
-    constexpr int TR_OPS = TT::PER_WAVE;
+    auto issue_k = [&](int c) { rt.issue(k_lds, kb + static_cast<int64_t>(c < 0 ? 0 : c) * TILE, wave); };
+    auto issue_v = [&](int c) { rt.issue(v_lds, vb + static_cast<int64_t>(c < 0 ? 0 : c) * TILE, wave); };
 
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) { settle(qf[ks]); settle(of[ks]); }   // before the copies start
@@ -292,14 +287,14 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     int c_cur = -1;
     if (e0 < e1) {
         c_cur = block_of(e0);
-        issue_rows(c_cur);
-        issue_tr(c_cur);
+        issue_k(c_cur);
+        issue_v(c_cur);
     }
     for (int64_t e = e0; e < e1; ++e) {
         const bool has_next = e + 1 < e1;
         const int c_next = has_next ? block_of(e + 1) : -1;
 
-        vm_wait<TR_OPS>();              // K, V landed
+        vm_wait<0>();                   // K and V landed
         wg_barrier();
         F sb[2][2];
 #pragma unroll
@@ -311,9 +306,9 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
                 F a;
-                lds_frag_s<RRB>(a, k_lds, t2 * 32 + (lane & 31), ks * 16 + half * 8);
+                lds_frag_s<RB>(a, k_lds, t2 * 32 + (lane & 31), ks * 16 + half * 8);
                 mma(s, a, qf[ks]);
-                lds_frag_s<RRB>(a, v_lds, t2 * 32 + (lane & 31), ks * 16 + half * 8);
+                lds_frag_s<RB>(a, v_lds, t2 * 32 + (lane & 31), ks * 16 + half * 8);
                 mma(dp, a, of[ks]);
             }
             float ds[16];
@@ -325,23 +320,21 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
             pack_frag(sb[t2][0], ds);
             pack_frag(sb[t2][1], ds + 8);
         }
-        wg_barrier();                   // K, V buffers free
-        if (has_next) issue_rows(c_next);
-        if (has_next) vm_wait<ROWS_OPS>(); else vm_wait<0>();   // K^T landed
-        wg_barrier();
+        wg_barrier();                   // V buffer free: stream the next one during dQ
+        if (has_next) issue_v(c_next);
         if (c_cur >= 0) {
-            // dQ^T += K^T dS^T over the 64 keys (4 k-steps of 16)
+            // dQ^T += K^T dS^T over the 64 keys (4 k-steps of 16); K^T read transposed
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
                     F a;
-                    lds_frag_s<TRB>(a, kt_lds, mt * 32 + (lane & 31), kk * 16 + half * 8);
+                    lds_frag_tr<RB, true>(a, k_lds, mt * 32, kk * 16);
                     mma(dqa[mt], a, sb[kk >> 1][kk & 1]);
                 }
         }
-        wg_barrier();                   // K^T buffer free
-        if (has_next) issue_tr(c_next);
+        wg_barrier();                   // K buffer free
+        if (has_next) issue_k(c_next);
         c_cur = c_next;
     }
     T* dqrow = dq + qtok * D;
@@ -362,13 +355,13 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
         }
 }
 
-// Workspace of the backward call: stat [ntok] float2, then Q^T, dO^T and K^T.
+// Workspace of the backward call: per query token (LSE * log2(e), Delta).
 size_t bwd_workspace_bytes(int dtype, int D, int batch, int Hq, int Hkv, int N) {
-    const size_t E = dtype == 1 ? 2 : 4;
+    (void)dtype;
+    (void)D;
+    (void)Hkv;
     const size_t L = static_cast<size_t>(N) * 64;
-    auto al = [](size_t x) { return (x + 255) / 256 * 256; };
-    return al(8 * static_cast<size_t>(batch) * Hq * L) + 2 * al(E * batch * Hq * L * D) +
-           al(E * batch * Hkv * L * D);
+    return (8 * static_cast<size_t>(batch) * Hq * L + 255) / 256 * 256;
 }
 
 template <typename T, int D>
@@ -379,16 +372,7 @@ static hipError_t launch_bwd_t(const void* q, const void* k, const void* v, cons
                                hipStream_t s) {
     const int64_t L = static_cast<int64_t>(N) * 64;
     const int64_t ntok = static_cast<int64_t>(batch) * Hq * L;
-    auto al = [](size_t x) { return (x + 255) / 256 * 256; };
-    char* w = static_cast<char*>(ws);
-    float2* stat = reinterpret_cast<float2*>(w);
-    w += al(8 * static_cast<size_t>(ntok));
-    T* qt = reinterpret_cast<T*>(w);
-    w += al(sizeof(T) * static_cast<size_t>(ntok) * D);
-    T* dot = reinterpret_cast<T*>(w);
-    w += al(sizeof(T) * static_cast<size_t>(ntok) * D);
-    T* ktr = reinterpret_cast<T*>(w);
-
+    float2* stat = static_cast<float2*>(ws);
     const float c = kLog2e / sqrtf(static_cast<float>(D));
     const float scale = 1.0f / sqrtf(static_cast<float>(D));
     const T* Q = static_cast<const T*>(q);
@@ -400,21 +384,16 @@ static hipError_t launch_bwd_t(const void* q, const void* k, const void* v, cons
                        s, static_cast<const T*>(o), dO, lse, stat, ntok);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if ((e = launch_block_transpose(sizeof(T) == 2 ? 1 : 0, D, q, qt, ntok / 64, s)) != hipSuccess) return e;
-    if ((e = launch_block_transpose(sizeof(T) == 2 ? 1 : 0, D, dout, dot, ntok / 64, s)) != hipSuccess) return e;
-    if ((e = launch_block_transpose(sizeof(T) == 2 ? 1 : 0, D, k, ktr, static_cast<int64_t>(batch) * Hkv * N, s)) !=
-        hipSuccess)
-        return e;
     const int64_t krows = static_cast<int64_t>(batch) * Hkv * N;
-    hipLaunchKernelGGL((dkdv_kernel<T, D, 0>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s, Q, qt, K, V,
-                       dO, dot, stat, kv_ptr, kv_idx, col_cap, static_cast<T*>(dv), Hq, Hkv, N, c, scale);
+    hipLaunchKernelGGL((dkdv_kernel<T, D, 0>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s, Q, K, V,
+                       dO, stat, kv_ptr, kv_idx, col_cap, static_cast<T*>(dv), Hq, Hkv, N, c, scale);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((dkdv_kernel<T, D, 1>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s, Q, qt, K, V,
-                       dO, dot, stat, kv_ptr, kv_idx, col_cap, static_cast<T*>(dk), Hq, Hkv, N, c, scale);
+    hipLaunchKernelGGL((dkdv_kernel<T, D, 1>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s, Q, K, V,
+                       dO, stat, kv_ptr, kv_idx, col_cap, static_cast<T*>(dk), Hq, Hkv, N, c, scale);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const int64_t qrows = static_cast<int64_t>(batch) * Hq * N;
-    hipLaunchKernelGGL((dq_kernel<T, D>), dim3(static_cast<unsigned>(qrows)), dim3(AB_NT), 0, s, Q, K, ktr, V,
-                       dO, stat, row_ptr, col_idx, col_cap, static_cast<T*>(dq), Hq, Hkv, N, c, scale);
+    hipLaunchKernelGGL((dq_kernel<T, D>), dim3(static_cast<unsigned>(qrows)), dim3(AB_NT), 0, s, Q, K, V, dO,
+                       stat, row_ptr, col_idx, col_cap, static_cast<T*>(dq), Hq, Hkv, N, c, scale);
     return hipGetLastError();
 }
 

@@ -3,13 +3,12 @@
 //
 // One workgroup of two waves per query block (64 queries); wave w owns
 // queries 32w .. 32w+31.  For every key block listed in the block's CSR row:
-//   K tile   [64 keys][D]  -> LDS, row r at slot swap_bits_2_3(r)
-//   V^T tile [D][64 keys]  -> LDS (V is block-transposed once per call by
-//                             block_transpose_kernel, so every tile is a
-//                             straight 16 KB copy)
+//   K, V tiles [64 keys][D] -> LDS, row r at slot swap_bits_2_3(r)
 //   S^T = K Q^T            (MFMA 32x32, Q fragments live in registers)
 //   online softmax in fp32 registers (exp2, log2(e)/sqrt(D) folded in)
-//   O^T += V^T P^T         (P rounded to the input dtype, MFMA 32x32)
+//   O^T += V^T P^T         (P rounded to the input dtype, MFMA 32x32; the
+//                           V^T operand comes from the row-major V tile by
+//                           transposing LDS reads)
 // Tiles arrive by global_load_lds (no staging registers).  The K and V
 // buffers are refilled as soon as their last reader is done: the next K tile
 // streams in during this tile's softmax and PV product, the next V tile
@@ -23,67 +22,22 @@ namespace vsa2 {
 
 constexpr int AF_NT = 128;
 
-// x [nblk][64][D] -> xt [nblk][D][64]; one workgroup per 64-row block.
-template <typename T, int D>
-__global__ __launch_bounds__(256) void block_transpose_kernel(const T* __restrict__ x, T* __restrict__ xt,
-                                                              int64_t nblk) {
-    constexpr int PAD = 16 / sizeof(T);
-    __shared__ T tile[64][D + PAD];
-    const int64_t blk = blockIdx.x;
-    if (blk >= nblk) return;
-    const T* src = x + blk * 64 * D;
-    constexpr int VEC = 16 / sizeof(T);          // elements per 16-byte load
-    for (int i = threadIdx.x; i < 64 * D / VEC; i += 256) {
-        const int r = i / (D / VEC), c = (i % (D / VEC)) * VEC;
-        *reinterpret_cast<uint4*>(&tile[r][c]) = *reinterpret_cast<const uint4*>(src + r * D + c);
-    }
-    __syncthreads();
-    T* dst = xt + blk * 64 * D;
-    for (int i = threadIdx.x; i < 64 * D / VEC; i += 256) {
-        const int d = i / (64 / VEC), k0 = (i % (64 / VEC)) * VEC;
-        T v[VEC];
-#pragma unroll
-        for (int j = 0; j < VEC; ++j) v[j] = tile[k0 + j][d];
-        *reinterpret_cast<uint4*>(dst + d * 64 + k0) = *reinterpret_cast<const uint4*>(v);
-    }
-}
-
-template <typename T, int D>
-hipError_t launch_block_transpose_t(const void* x, void* xt, int64_t nblk, hipStream_t s) {
-    if (nblk == 0) return hipSuccess;
-    hipLaunchKernelGGL((block_transpose_kernel<T, D>), dim3(static_cast<unsigned>(nblk)), dim3(256), 0, s,
-                       static_cast<const T*>(x), static_cast<T*>(xt), nblk);
-    return hipGetLastError();
-}
-
-hipError_t launch_block_transpose(int dtype, int D, const void* x, void* xt, int64_t nblk, hipStream_t s) {
-    if (dtype == 1) {
-        if (D == 64) return launch_block_transpose_t<bf16_t, 64>(x, xt, nblk, s);
-        if (D == 128) return launch_block_transpose_t<bf16_t, 128>(x, xt, nblk, s);
-    } else {
-        if (D == 64) return launch_block_transpose_t<float, 64>(x, xt, nblk, s);
-        if (D == 128) return launch_block_transpose_t<float, 128>(x, xt, nblk, s);
-    }
-    return hipErrorInvalidValue;
-}
-
 template <typename T, int D>
 __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
-    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ vt,
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx, int64_t col_cap,
     T* __restrict__ o, float* __restrict__ lse, int Hq, int Hkv, int N, float c_log2) {
     using F = typename frag_of<T>::type;
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;        // macro k-steps over the head dim
     constexpr int MT = D / 32;        // 32-row tiles of O^T
-    constexpr int KRB = D * E;        // K tile row bytes
-    constexpr int VRB = 64 * E;       // V^T tile row bytes
+    constexpr int KRB = D * E;        // K and V tile row bytes
     using KT = async_tile<64, KRB, 2, true>;
-    using VT = async_tile<D, VRB, 2, false>;
+    using VT = KT;
     __shared__ __align__(1024) char k_lds[KT::BYTES];
     __shared__ __align__(1024) char v_lds[VT::BYTES];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+    const int tid = threadIdx.x, lane = tid & 63, wave = wave_id(), half = lane >> 5;
     const int64_t row = blockIdx.x;
     const int64_t bh = row / N;
     const int n = static_cast<int>(row % N);
@@ -91,7 +45,7 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     const int hkv = h / (Hq / Hkv);
     const int64_t L = static_cast<int64_t>(N) * 64;
     const char* kb = reinterpret_cast<const char*>(k + static_cast<int64_t>(b * Hkv + hkv) * L * D);
-    const char* vb = reinterpret_cast<const char*>(vt + static_cast<int64_t>(b * Hkv + hkv) * L * D);
+    const char* vb = reinterpret_cast<const char*>(v + static_cast<int64_t>(b * Hkv + hkv) * L * D);
     const int64_t qtok = bh * L + static_cast<int64_t>(n) * 64 + wave * 32 + (lane & 31);
 
     int64_t e0 = row_ptr[row], e1 = row_ptr[row + 1];
@@ -115,7 +69,7 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
         return (c >= 0 && c < N) ? c : -1;
     };
     const KT kt(wave, lane);
-    const VT vt_(wave, lane);
+    const KT& vt_ = kt;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) settle(qf[ks]);   // fragments in registers before the copies start
     int c_cur = -1;
@@ -190,7 +144,7 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
                     F a;
-                    lds_frag_s<VRB>(a, v_lds, mt * 32 + (lane & 31), kk * 16 + half * 8);
+                    lds_frag_tr<KRB, true>(a, v_lds, mt * 32, kk * 16);
                     mma(oacc[mt], a, pb);
                 }
             }
@@ -224,27 +178,25 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
 template <typename T, int D>
 static hipError_t launch_fwd_t(const void* q, const void* k, const void* v, const int32_t* row_ptr,
                                const int32_t* col_idx, int64_t col_cap, void* o, float* lse,
-                               void* vt, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                               int batch, int Hq, int Hkv, int N, hipStream_t s) {
     const int64_t rows = static_cast<int64_t>(batch) * Hq * N;
     if (rows == 0) return hipSuccess;
-    hipError_t e = launch_block_transpose_t<T, D>(v, vt, static_cast<int64_t>(batch) * Hkv * N, s);
-    if (e != hipSuccess) return e;
     const float c = 1.4426950408889634f / sqrtf(static_cast<float>(D));
     hipLaunchKernelGGL((attn_fwd_kernel<T, D>), dim3(static_cast<unsigned>(rows)), dim3(AF_NT), 0, s,
-                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(vt),
+                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
                        row_ptr, col_idx, col_cap, static_cast<T*>(o), lse, Hq, Hkv, N, c);
     return hipGetLastError();
 }
 
 hipError_t launch_attn_fwd(int dtype, int D, const void* q, const void* k, const void* v,
                            const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
-                           float* lse, void* vt, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                           float* lse, int batch, int Hq, int Hkv, int N, hipStream_t s) {
     if (dtype == 1) {
-        if (D == 64) return launch_fwd_t<bf16_t, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, vt, batch, Hq, Hkv, N, s);
-        if (D == 128) return launch_fwd_t<bf16_t, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, vt, batch, Hq, Hkv, N, s);
+        if (D == 64) return launch_fwd_t<bf16_t, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, batch, Hq, Hkv, N, s);
+        if (D == 128) return launch_fwd_t<bf16_t, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, batch, Hq, Hkv, N, s);
     } else {
-        if (D == 64) return launch_fwd_t<float, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, vt, batch, Hq, Hkv, N, s);
-        if (D == 128) return launch_fwd_t<float, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, vt, batch, Hq, Hkv, N, s);
+        if (D == 64) return launch_fwd_t<float, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, batch, Hq, Hkv, N, s);
+        if (D == 128) return launch_fwd_t<float, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, batch, Hq, Hkv, N, s);
     }
     return hipErrorInvalidValue;
 }

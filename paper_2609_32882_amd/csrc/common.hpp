@@ -145,6 +145,9 @@ __device__ __forceinline__ int swap_bits_2_3(int r) {
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 
+// Index of the calling wave inside its workgroup, as a wave-uniform (scalar) value.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
 // Fragment of 8 consecutive elements starting at element `e0` of row `row`
 // of a swizzled LDS tile (bf16: one 16-byte chunk; fp32: two).
 template <int ROW_BYTES>
@@ -320,9 +323,13 @@ __device__ __forceinline__ int32_t scalar_load_i32(const int32_t* p) {
 // apart, does not put a full vmcnt(0) wait in front of every LDS read; the
 // kernels order these copies themselves with vm_wait and wg_barrier.
 __device__ __forceinline__ void dma16(uint32_t lds, const void* base, int voff) {
+    const uint32_t l = __builtin_amdgcn_readfirstlane(lds);
+    const uint64_t b = reinterpret_cast<uint64_t>(base);
+    const uint64_t bs = (static_cast<uint64_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b >> 32))) << 32) |
+                        __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b));
     asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
                  :
-                 : "s"(lds), "v"(voff), "s"(base)
+                 : "s"(l), "v"(voff), "s"(bs)
                  : "memory", "m0");
 }
 
@@ -359,6 +366,49 @@ struct async_tile {
         for (int j = 0; j < PER_WAVE; ++j) dma16(l0 + (wave * PER_WAVE + j) * 1024, g, off[j]);
     }
 };
+
+// A-operand fragment of a transposed use of a row-major tile.
+//
+// The tile holds X^T row-major: LDS row = the contraction index (a key or a
+// query, stored at slot swap_bits_2_3(index) when PERM), columns = the output
+// rows m (the head dimension d), contiguous.  The MFMA 32x32x16 A operand for
+// output tile rows m0 .. m0+31 and contraction indices k0 .. k0+15 needs, in
+// lane l, X[m0 + l%32][k0 + 8(l/32) + s] for s = 0..7.  ds_read_b64_tr_b16
+// gives, within each group of 16 lanes, lane j the 4 values E[j/4 + 4c][j%4]
+// (c = 0..3) of the 16x4 block E whose row i lane i addresses.  So lane i of
+// group G (l = 16G + i) addresses contraction index k0 + 8(G/2) + 4r + i/4,
+// columns m0 + 16(G%2) + 4(i%4) .. +3, and read r = 0, 1 returns slots
+// 4r .. 4r+3.  Every address is a per-lane base plus compile-time offsets.
+template <int RB, bool PERM>
+__device__ __forceinline__ void lds_frag_tr(frag_bf16& f, const char* tile, int m0, int k0) {
+    typedef short v4i16 __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+    const int l = lane_id(), i = l & 15, G = l >> 4;
+    v4i16 r2[2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        const int k = k0 + 8 * (G >> 1) + 4 * r + (i >> 2);
+        const int row = PERM ? swap_bits_2_3(k) : k;
+        const char* p = tile + row * (RB + 16) + (m0 + 16 * (G & 1) + 4 * (i & 3)) * 2;
+        r2[r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p));
+    }
+    typedef __attribute__((__vector_size__(8 * sizeof(short)))) short s16x8_t;
+    const s16x8_t w = {r2[0][0], r2[0][1], r2[0][2], r2[0][3], r2[1][0], r2[1][1], r2[1][2], r2[1][3]};
+    f.v = __builtin_bit_cast(bf16x8_t, w);
+}
+// fp32 tiles: plain 4-byte reads of the same elements (no transposing read
+// exists for 32-bit data; only the small fp32 problems take this path).
+template <int RB, bool PERM>
+__device__ __forceinline__ void lds_frag_tr(frag_f32& f, const char* tile, int m0, int k0) {
+    const int l = lane_id();
+    const int m = m0 + (l & 31);
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+        const int k = k0 + 8 * (l >> 5) + s;
+        const int row = PERM ? swap_bits_2_3(k) : k;
+        f.v[s] = *reinterpret_cast<const float*>(tile + row * (RB + 16) + m * 4);
+    }
+}
 
 // Fragment of 8 consecutive elements starting at element e0 of row `row` of
 // a padded LDS tile with RB-byte rows.

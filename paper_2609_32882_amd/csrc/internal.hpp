@@ -20,11 +20,9 @@ hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
 hipError_t launch_csc(const int32_t* row_ptr, const int32_t* col_idx, int batch, int Hq, int Hkv, int N,
                       int64_t col_cap, uint32_t* mask, int32_t* kv_counts, int32_t* kv_ptr,
                       int32_t* kv_idx, hipStream_t s);
-hipError_t launch_block_transpose(int dtype, int D, const void* x, void* xt, int64_t nblk, hipStream_t s);
-// vt: workspace for the block-transposed V (batch*Hkv*L*D elements)
 hipError_t launch_attn_fwd(int dtype, int D, const void* q, const void* k, const void* v,
                            const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
-                           float* lse, void* vt, int batch, int Hq, int Hkv, int N, hipStream_t s);
+                           float* lse, int batch, int Hq, int Hkv, int N, hipStream_t s);
 size_t bwd_workspace_bytes(int dtype, int D, int batch, int Hq, int Hkv, int N);
 hipError_t launch_attn_bwd(int dtype, int D, const void* q, const void* k, const void* v, const void* o,
                            const float* lse, const void* dout, const int32_t* row_ptr,

@@ -81,8 +81,6 @@ def test_null_and_alignment_checks():
                                                 None)] == "VSA2_ERR_NULL"
     assert vsa2.STATUS_NAMES[vsa2.vsa2_attn_fwd(p, MISALIGNED, FAKE, FAKE, FAKE, FAKE, 1, FAKE, FAKE,
                                                 FAKE, 1 << 40, None)] == "VSA2_ERR_ALIGN"
-    assert vsa2.STATUS_NAMES[vsa2.vsa2_attn_fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, 1, FAKE, FAKE,
-                                                None, 0, None)] == "VSA2_ERR_WORKSPACE"
     assert vsa2.STATUS_NAMES[vsa2.vsa2_pool(p, 4, FAKE, 2, 2, 2, MISALIGNED, None)] == "VSA2_ERR_ALIGN"
     assert vsa2.STATUS_NAMES[vsa2.vsa2_pool(p, 4, FAKE, 3, 2, 2, FAKE, None)] == "VSA2_ERR_SHAPE"
     assert vsa2.STATUS_NAMES[vsa2.vsa2_pool(None, 4, FAKE, 2, 2, 2, FAKE, None)] == "VSA2_ERR_NULL"
