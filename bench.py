@@ -113,12 +113,12 @@ def main():
         if record:
             e[2].record(stream)
         chk("fwd", vsa2.vsa2_attn_fwd(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), row_ptr.data_ptr(),
-                                      col_idx.data_ptr(), cap, o.data_ptr(), lse.data_ptr(), None, 0,
+                                      col_idx.data_ptr(), cap, o.data_ptr(), lse.data_ptr(), None, None, 0,
                                       sp))
         if record:
             e[3].record(stream)
         chk("bwd", vsa2.vsa2_attn_bwd(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
-                                      lse.data_ptr(), do.data_ptr(), row_ptr.data_ptr(),
+                                      lse.data_ptr(), None, do.data_ptr(), row_ptr.data_ptr(),
                                       col_idx.data_ptr(), kv_ptr.data_ptr(), kv_idx.data_ptr(), cap,
                                       dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), bws_t.data_ptr(),
                                       bws, sp))

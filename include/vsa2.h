@@ -172,13 +172,20 @@ vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* byt
  *   o   [batch][Hq][L][D] output, dtype p->dtype.
  *   lse [batch][Hq][L] fp32 natural-log log-sum-exp of each query's scaled
  *       scores; a query block with no selected block gets o = 0, lse = -inf.
+ *   o_lo  optional [batch][Hq][L][D] (dtype p->dtype), NULL for the plain
+ *       path.  When given, the call runs compensated: P enters the P.V
+ *       product as two bf16 terms (about 16 significant bits instead of 8)
+ *       and o_lo receives the rounding remainder of O (o + o_lo ~ the fp32
+ *       accumulator).  Pass it to vsa2_attn_bwd to get gradients whose error
+ *       does not grow with the magnitude of the keys' common component.
  *   ws, ws_bytes  workspace of vsa2_attn_workspace(p, 0) bytes (zero: ws may
  *       be NULL).
  * Errors: NULL pointers, shape/dtype, misalignment, small workspace.
  */
 vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, const void* v,
                           const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
-                          void* o, float* lse, void* ws, size_t ws_bytes, hipStream_t stream);
+                          void* o, float* lse, void* o_lo, void* ws, size_t ws_bytes,
+                          hipStream_t stream);
 
 /*
  * vsa2_attn_bwd - gradients of vsa2_attn_fwd with the block lists fixed
@@ -190,6 +197,8 @@ vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, c
  * where the sums over l run over every query (of every query head of the KV
  * group) whose block selected j's block.
  *   q, k, v, o, lse   as for vsa2_attn_fwd (o, lse from the forward call)
+ *   o_lo  NULL, or the forward's o_lo: then Delta uses o + o_lo and dS enters
+ *         the dQ and dK products as two bf16 terms (compensated path)
  *   dout  [batch][Hq][L][D]  dO
  *   row_ptr, col_idx  the CSR; kv_ptr, kv_idx its transpose (vsa2_route)
  *   dq [batch][Hq][L][D], dk, dv [batch][Hkv][L][D]  outputs, dtype p->dtype;
@@ -197,7 +206,7 @@ vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, c
  * Errors: as for vsa2_attn_fwd.
  */
 vsa2_status vsa2_attn_bwd(const vsa2_problem* p, const void* q, const void* k, const void* v,
-                          const void* o, const float* lse, const void* dout,
+                          const void* o, const float* lse, const void* o_lo, const void* dout,
                           const int32_t* row_ptr, const int32_t* col_idx,
                           const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
                           void* dq, void* dk, void* dv, void* ws, size_t ws_bytes,

@@ -67,8 +67,8 @@ def _lib():
         L.vsa2_route_workspace.argtypes = [pp, ps, ctypes.POINTER(sz)]
         L.vsa2_route.argtypes = [pp, ps, P, P, P, P, i64, P, P, P, P, sz, P]
         L.vsa2_attn_workspace.argtypes = [pp, i32, ctypes.POINTER(sz)]
-        L.vsa2_attn_fwd.argtypes = [pp, P, P, P, P, P, i64, P, P, P, sz, P]
-        L.vsa2_attn_bwd.argtypes = [pp, P, P, P, P, P, P, P, P, P, P, i64, P, P, P, P, sz, P]
+        L.vsa2_attn_fwd.argtypes = [pp, P, P, P, P, P, i64, P, P, P, P, sz, P]
+        L.vsa2_attn_bwd.argtypes = [pp, P, P, P, P, P, P, P, P, P, P, P, i64, P, P, P, P, sz, P]
         for n in EXPORTS[1:]:
             getattr(L, n).restype = ctypes.c_int
         _L = L
@@ -125,14 +125,14 @@ def vsa2_attn_workspace(p, pass_):
     return st, n.value
 
 
-def vsa2_attn_fwd(p, q, k, v, row_ptr, col_idx, col_cap, o, lse, ws, ws_bytes, stream=0):
-    return _lib().vsa2_attn_fwd(_ref(p), q, k, v, row_ptr, col_idx, col_cap, o, lse, ws,
+def vsa2_attn_fwd(p, q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, ws, ws_bytes, stream=0):
+    return _lib().vsa2_attn_fwd(_ref(p), q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, ws,
                                 ws_bytes, stream)
 
 
-def vsa2_attn_bwd(p, q, k, v, o, lse, dout, row_ptr, col_idx, kv_ptr, kv_idx, col_cap, dq, dk, dv,
-                  ws, ws_bytes, stream=0):
-    return _lib().vsa2_attn_bwd(_ref(p), q, k, v, o, lse, dout, row_ptr, col_idx, kv_ptr,
+def vsa2_attn_bwd(p, q, k, v, o, lse, o_lo, dout, row_ptr, col_idx, kv_ptr, kv_idx, col_cap, dq,
+                  dk, dv, ws, ws_bytes, stream=0):
+    return _lib().vsa2_attn_bwd(_ref(p), q, k, v, o, lse, o_lo, dout, row_ptr, col_idx, kv_ptr,
                                 kv_idx, col_cap, dq, dk, dv, ws, ws_bytes, stream)
 
 
@@ -232,7 +232,9 @@ def route(p, s, q_r, k_r, with_csc=True, with_scores=False):
                 col_cap=cap, ws=ws)
 
 
-def attn_fwd(p, q, k, v, row_ptr, col_idx, col_cap=None, o=None, lse=None):
+def attn_fwd(p, q, k, v, row_ptr, col_idx, col_cap=None, o=None, lse=None, compensated=False,
+             o_lo=None):
+    """Returns (o, lse), or (o, lse, o_lo) when compensated."""
     torch = _torch()
     p = problem_from(p)
     N, B, _ = _dims(p)
@@ -249,15 +251,19 @@ def attn_fwd(p, q, k, v, row_ptr, col_idx, col_cap=None, o=None, lse=None):
     st, wsb = vsa2_attn_workspace(p, 0)
     _check("vsa2_attn_workspace", st)
     ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
+    if compensated and o_lo is None:
+        o_lo = torch.empty_like(q)
     _check("vsa2_attn_fwd", vsa2_attn_fwd(p, q.data_ptr(), k.data_ptr(), v.data_ptr(),
                                           row_ptr.data_ptr(), col_idx.data_ptr(), cap,
-                                          o.data_ptr(), lse.data_ptr(), ws.data_ptr(), wsb,
-                                          _stream()))
-    return o, lse
+                                          o.data_ptr(), lse.data_ptr(),
+                                          o_lo.data_ptr() if compensated else None,
+                                          ws.data_ptr(), wsb, _stream()))
+    return (o, lse, o_lo) if compensated else (o, lse)
 
 
 def attn_bwd(p, q, k, v, o, lse, do, row_ptr, col_idx, kv_ptr, kv_idx, col_cap=None,
-             dq=None, dk=None, dv=None):
+             dq=None, dk=None, dv=None, o_lo=None):
+    """dQ, dK, dV; pass the forward's o_lo for the compensated path."""
     torch = _torch()
     p = problem_from(p)
     N, B, _ = _dims(p)
@@ -275,7 +281,7 @@ def attn_bwd(p, q, k, v, o, lse, do, row_ptr, col_idx, kv_ptr, kv_idx, col_cap=N
     _check("vsa2_attn_workspace", st)
     ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
     _check("vsa2_attn_bwd", vsa2_attn_bwd(p, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
-                                          lse.data_ptr(), do.data_ptr(), row_ptr.data_ptr(),
+                                          lse.data_ptr(), _ptr(o_lo), do.data_ptr(), row_ptr.data_ptr(),
                                           col_idx.data_ptr(), kv_ptr.data_ptr(), kv_idx.data_ptr(),
                                           cap, dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
                                           ws.data_ptr(), wsb, _stream()))

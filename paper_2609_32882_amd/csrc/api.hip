@@ -208,7 +208,7 @@ vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* byt
 
 vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, const void* v,
                           const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
-                          float* lse, void* ws, size_t ws_bytes, hipStream_t stream) {
+                          float* lse, void* o_lo, void* ws, size_t ws_bytes, hipStream_t stream) {
     shape s;
     vsa2_status st = check_problem(p, &s);
     if (st != VSA2_OK) return st;
@@ -216,16 +216,17 @@ vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, c
     if (!q || !k || !v || !row_ptr || !o || !lse) return VSA2_ERR_NULL;
     if (!col_idx && col_cap > 0) return VSA2_ERR_NULL;
     if (col_cap < 0) return VSA2_ERR_CAPACITY;
-    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return VSA2_ERR_ALIGN;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(o_lo))
+        return VSA2_ERR_ALIGN;
     if (ws_bytes < fwd_ws_bytes(s, p)) return VSA2_ERR_WORKSPACE;
     (void)ws;
     VSA2_TRY_HIP(vsa2::launch_attn_fwd(p->dtype, p->head_dim, q, k, v, row_ptr, col_idx, col_cap, o, lse,
-                                       p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N), stream));
+                                       o_lo, p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N), stream));
     return VSA2_OK;
 }
 
 vsa2_status vsa2_attn_bwd(const vsa2_problem* p, const void* q, const void* k, const void* v, const void* o,
-                          const float* lse, const void* dout, const int32_t* row_ptr,
+                          const float* lse, const void* o_lo, const void* dout, const int32_t* row_ptr,
                           const int32_t* col_idx, const int32_t* kv_ptr, const int32_t* kv_idx,
                           int64_t col_cap, void* dq, void* dk, void* dv, void* ws, size_t ws_bytes,
                           hipStream_t stream) {
@@ -238,12 +239,12 @@ vsa2_status vsa2_attn_bwd(const vsa2_problem* p, const void* q, const void* k, c
     if ((!col_idx || !kv_idx) && col_cap > 0) return VSA2_ERR_NULL;
     if (col_cap < 0) return VSA2_ERR_CAPACITY;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) ||
-        !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
+        !aligned16(dq) || !aligned16(dk) || !aligned16(dv) || !aligned16(o_lo))
         return VSA2_ERR_ALIGN;
     const size_t need = bwd_ws_bytes(s, p);
     if (!ws || ws_bytes < need) return VSA2_ERR_WORKSPACE;
     if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
-    VSA2_TRY_HIP(vsa2::launch_attn_bwd(p->dtype, p->head_dim, q, k, v, o, lse, dout, row_ptr, col_idx,
+    VSA2_TRY_HIP(vsa2::launch_attn_bwd(p->dtype, p->head_dim, q, k, v, o, lse, o_lo, dout, row_ptr, col_idx,
                                        kv_ptr, kv_idx, col_cap, dq, dk, dv, ws,
                                        p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N), stream));
     return VSA2_OK;

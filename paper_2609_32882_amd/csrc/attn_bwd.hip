@@ -30,9 +30,11 @@ constexpr float kLog2e = 1.4426950408889634f;
 
 // ---------------------------------------------------------------------------
 // stat[l] = (LSE_l * log2(e), dO_l . O_l); 16 lanes per token (D <= 128).
+// With the forward's rounding remainder o_lo, O_l = o_l + o_lo_l.
 // ---------------------------------------------------------------------------
 template <typename T, int D>
-__global__ __launch_bounds__(256) void stat_kernel(const T* __restrict__ o, const T* __restrict__ dout,
+__global__ __launch_bounds__(256) void stat_kernel(const T* __restrict__ o, const T* __restrict__ o_lo,
+                                                   const T* __restrict__ dout,
                                                    const float* __restrict__ lse, float2* __restrict__ stat,
                                                    int64_t ntok) {
     constexpr int LPT = D / 8;   // lanes per token, 8 elements each
@@ -45,6 +47,11 @@ __global__ __launch_bounds__(256) void stat_kernel(const T* __restrict__ o, cons
         const T* b = dout + tok * D + part * 8;
 #pragma unroll
         for (int i = 0; i < 8; ++i) s += to_f32(a[i]) * to_f32(b[i]);
+        if (o_lo) {
+            const T* c = o_lo + tok * D + part * 8;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) s += to_f32(c[i]) * to_f32(b[i]);
+        }
     }
 #pragma unroll
     for (int off = LPT / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
@@ -59,7 +66,7 @@ __global__ __launch_bounds__(256) void stat_kernel(const T* __restrict__ o, cons
 //   dV^T += dO^T P    tiles Q (for S) and dO (for dO^T)
 //   dK^T += Q^T dS    tiles Q (for S and Q^T) and dO (for dP)
 // ---------------------------------------------------------------------------
-template <typename T, int D, int GRAD>
+template <typename T, int D, int GRAD, bool COMP>
 __global__ __launch_bounds__(AB_NT, GRAD == 1 ? 1 : 2) void dkdv_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float2* __restrict__ stat,
@@ -70,6 +77,7 @@ __global__ __launch_bounds__(AB_NT, GRAD == 1 ? 1 : 2) void dkdv_kernel(
     constexpr int KS = D / 16;
     constexpr int MT = D / 32;
     constexpr int RB = D * E;                    // tile row bytes
+    constexpr bool SPLIT = COMP && GRAD == 1 && sizeof(T) == 2;   // dS as hi + lo
     using RT = async_tile<64, RB, 2, true>;      // Q, dO rows (slot-swapped)
     __shared__ __align__(1024) char q_lds[RT::BYTES];
     __shared__ __align__(1024) char o_lds[RT::BYTES];
@@ -145,6 +153,7 @@ __global__ __launch_bounds__(AB_NT, GRAD == 1 ? 1 : 2) void dkdv_kernel(
         if constexpr (GRAD == 0) vm_wait<O_OPS>(); else vm_wait<0>();
         wg_barrier();
         F fb[2][2];                     // P (dV) or dS (dK) by [query tile][k-step half]
+        F fl[SPLIT ? 2 : 1][2];          // low part of dS (compensated)
 #pragma unroll
         for (int qtile = 0; qtile < 2; ++qtile) {
             // S = Q K^T (and dP = dO V^T) for 32 queries x this lane's key
@@ -169,8 +178,13 @@ __global__ __launch_bounds__(AB_NT, GRAD == 1 ? 1 : 2) void dkdv_kernel(
                 const float p = fast_exp2(s[i] * c_log2 - st.x);
                 x[i] = GRAD == 1 ? p * (dp[i] - st.y) : p;
             }
-            pack_frag(fb[qtile][0], x);
-            pack_frag(fb[qtile][1], x + 8);
+            if constexpr (SPLIT) {
+                pack_frag_hilo(fb[qtile][0], fl[qtile][0], x);
+                pack_frag_hilo(fb[qtile][1], fl[qtile][1], x + 8);
+            } else {
+                pack_frag(fb[qtile][0], x);
+                pack_frag(fb[qtile][1], x + 8);
+            }
         }
         wg_barrier();
         if constexpr (GRAD == 0) {
@@ -193,6 +207,7 @@ __global__ __launch_bounds__(AB_NT, GRAD == 1 ? 1 : 2) void dkdv_kernel(
                     F a;
                     lds_frag_tr<RB, true>(a, xt, mt * 32, kk * 16);
                     mma(acc[mt], a, fb[kk >> 1][kk & 1]);
+                    if constexpr (SPLIT) mma(acc[mt], a, fl[(kk >> 1) & (SPLIT ? 1 : 0)][kk & 1]);
                 }
         }
         wg_barrier();
@@ -228,7 +243,7 @@ __global__ __launch_bounds__(AB_NT, GRAD == 1 ? 1 : 2) void dkdv_kernel(
 // dQ: one workgroup (2 waves) per query block; wave owns 32 queries.
 // Tiles K (for S^T and, read transposed, K^T) and V (for dP^T).
 // ---------------------------------------------------------------------------
-template <typename T, int D>
+template <typename T, int D, bool COMP>
 __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float2* __restrict__ stat,
@@ -239,6 +254,7 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     constexpr int KS = D / 16;
     constexpr int MT = D / 32;
     constexpr int RB = D * E;
+    constexpr bool SPLIT = COMP && sizeof(T) == 2;   // dS as hi + lo
     using RT = async_tile<64, RB, 2, true>;     // K, V rows (slot-swapped)
     __shared__ __align__(1024) char k_lds[RT::BYTES];
     __shared__ __align__(1024) char v_lds[RT::BYTES];
@@ -297,6 +313,7 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
         vm_wait<0>();                   // K and V landed
         wg_barrier();
         F sb[2][2];
+        F sl[SPLIT ? 2 : 1][2];
 #pragma unroll
         for (int t2 = 0; t2 < 2; ++t2) {
             // S^T = K Q^T, dP^T = V dO^T: 32 keys x this lane's query
@@ -317,8 +334,13 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
                 const float p = fast_exp2(s[i] * c_log2 - st.x);
                 ds[i] = p * (dp[i] - st.y);
             }
-            pack_frag(sb[t2][0], ds);
-            pack_frag(sb[t2][1], ds + 8);
+            if constexpr (SPLIT) {
+                pack_frag_hilo(sb[t2][0], sl[t2][0], ds);
+                pack_frag_hilo(sb[t2][1], sl[t2][1], ds + 8);
+            } else {
+                pack_frag(sb[t2][0], ds);
+                pack_frag(sb[t2][1], ds + 8);
+            }
         }
         wg_barrier();                   // V buffer free: stream the next one during dQ
         if (has_next) issue_v(c_next);
@@ -331,6 +353,7 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
                     F a;
                     lds_frag_tr<RB, true>(a, k_lds, mt * 32, kk * 16);
                     mma(dqa[mt], a, sb[kk >> 1][kk & 1]);
+                    if constexpr (SPLIT) mma(dqa[mt], a, sl[(kk >> 1) & (SPLIT ? 1 : 0)][kk & 1]);
                 }
         }
         wg_barrier();                   // K buffer free
@@ -364,9 +387,9 @@ size_t bwd_workspace_bytes(int dtype, int D, int batch, int Hq, int Hkv, int N) 
     return (8 * static_cast<size_t>(batch) * Hq * L + 255) / 256 * 256;
 }
 
-template <typename T, int D>
+template <typename T, int D, bool COMP>
 static hipError_t launch_bwd_t(const void* q, const void* k, const void* v, const void* o, const float* lse,
-                               const void* dout, const int32_t* row_ptr, const int32_t* col_idx,
+                               const void* o_lo, const void* dout, const int32_t* row_ptr, const int32_t* col_idx,
                                const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap, void* dq,
                                void* dk, void* dv, void* ws, int batch, int Hq, int Hkv, int N,
                                hipStream_t s) {
@@ -381,30 +404,32 @@ static hipError_t launch_bwd_t(const void* q, const void* k, const void* v, cons
     const T* dO = static_cast<const T*>(dout);
     const int64_t sthreads = ntok * (D / 8);
     hipLaunchKernelGGL((stat_kernel<T, D>), dim3(static_cast<unsigned>((sthreads + 255) / 256)), dim3(256), 0,
-                       s, static_cast<const T*>(o), dO, lse, stat, ntok);
+                       s, static_cast<const T*>(o), static_cast<const T*>(o_lo), dO, lse, stat, ntok);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t krows = static_cast<int64_t>(batch) * Hkv * N;
-    hipLaunchKernelGGL((dkdv_kernel<T, D, 0>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s, Q, K, V,
+    hipLaunchKernelGGL((dkdv_kernel<T, D, 0, COMP>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s, Q, K, V,
                        dO, stat, kv_ptr, kv_idx, col_cap, static_cast<T*>(dv), Hq, Hkv, N, c, scale);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((dkdv_kernel<T, D, 1>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s, Q, K, V,
+    hipLaunchKernelGGL((dkdv_kernel<T, D, 1, COMP>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s, Q, K, V,
                        dO, stat, kv_ptr, kv_idx, col_cap, static_cast<T*>(dk), Hq, Hkv, N, c, scale);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const int64_t qrows = static_cast<int64_t>(batch) * Hq * N;
-    hipLaunchKernelGGL((dq_kernel<T, D>), dim3(static_cast<unsigned>(qrows)), dim3(AB_NT), 0, s, Q, K, V, dO,
+    hipLaunchKernelGGL((dq_kernel<T, D, COMP>), dim3(static_cast<unsigned>(qrows)), dim3(AB_NT), 0, s, Q, K, V, dO,
                        stat, row_ptr, col_idx, col_cap, static_cast<T*>(dq), Hq, Hkv, N, c, scale);
     return hipGetLastError();
 }
 
 hipError_t launch_attn_bwd(int dtype, int D, const void* q, const void* k, const void* v, const void* o,
-                           const float* lse, const void* dout, const int32_t* row_ptr,
+                           const float* lse, const void* o_lo, const void* dout, const int32_t* row_ptr,
                            const int32_t* col_idx, const int32_t* kv_ptr, const int32_t* kv_idx,
                            int64_t col_cap, void* dq, void* dk, void* dv, void* ws, int batch,
                            int Hq, int Hkv, int N, hipStream_t s) {
-#define VSA2_BWD(T, DD) \
-    return launch_bwd_t<T, DD>(q, k, v, o, lse, dout, row_ptr, col_idx, kv_ptr, kv_idx, col_cap, dq, dk, dv, \
-                               ws, batch, Hq, Hkv, N, s)
+#define VSA2_BWD(T, DD)                                                                                    \
+    return o_lo ? launch_bwd_t<T, DD, true>(q, k, v, o, lse, o_lo, dout, row_ptr, col_idx, kv_ptr, kv_idx,   \
+                                            col_cap, dq, dk, dv, ws, batch, Hq, Hkv, N, s)                   \
+                : launch_bwd_t<T, DD, false>(q, k, v, o, lse, o_lo, dout, row_ptr, col_idx, kv_ptr, kv_idx,  \
+                                             col_cap, dq, dk, dv, ws, batch, Hq, Hkv, N, s)
     if (dtype == 1) {
         if (D == 64) VSA2_BWD(bf16_t, 64);
         if (D == 128) VSA2_BWD(bf16_t, 128);

@@ -22,12 +22,16 @@ namespace vsa2 {
 
 constexpr int AF_NT = 128;
 
-template <typename T, int D>
+// COMP (compensated): P enters the PV product as two bf16 terms (hi + lo),
+// and the rounding remainder of O is written to o_lo, so that O + o_lo
+// carries about 16 significant bits for the backward's Delta = dO . O.
+template <typename T, int D, bool COMP>
 __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx, int64_t col_cap,
-    T* __restrict__ o, float* __restrict__ lse, int Hq, int Hkv, int N, float c_log2) {
+    T* __restrict__ o, float* __restrict__ lse, T* __restrict__ o_lo, int Hq, int Hkv, int N, float c_log2) {
     using F = typename frag_of<T>::type;
+    constexpr bool SPLIT = COMP && sizeof(T) == 2;
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;        // macro k-steps over the head dim
     constexpr int MT = D / 32;        // 32-row tiles of O^T
@@ -136,16 +140,17 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
             // O^T += V^T P^T over 4 k-steps of 16 keys: keys 16kk + 8half + (0..7)
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk) {
-                F pb;
+                F pb, pl;
                 float pv[8];
 #pragma unroll
                 for (int i = 0; i < 8; ++i) pv[i] = s[kk >> 1][(kk & 1) * 8 + i];
-                pack_frag(pb, pv);
+                if constexpr (SPLIT) pack_frag_hilo(pb, pl, pv); else pack_frag(pb, pv);
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
                     F a;
                     lds_frag_tr<KRB, true>(a, v_lds, mt * 32, kk * 16);
                     mma(oacc[mt], a, pb);
+                    if constexpr (SPLIT) mma(oacc[mt], a, pl);
                 }
             }
         }
@@ -162,14 +167,24 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
             const int d0 = mt * 32 + g4 * 8 + half * 4;
+            float ov[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) ov[j] = oacc[mt][g4 * 4 + j] * inv;
             if constexpr (E == 2) {
-                const uint32_t w0 = pack2_bf16(oacc[mt][g4 * 4 + 0] * inv, oacc[mt][g4 * 4 + 1] * inv);
-                const uint32_t w1 = pack2_bf16(oacc[mt][g4 * 4 + 2] * inv, oacc[mt][g4 * 4 + 3] * inv);
+                const uint32_t w0 = pack2_bf16(ov[0], ov[1]);
+                const uint32_t w1 = pack2_bf16(ov[2], ov[3]);
                 *reinterpret_cast<uint2*>(orow + d0) = make_uint2(w0, w1);
+                if constexpr (COMP) {
+                    const uint32_t r0 = pack2_bf16(ov[0] - __uint_as_float(w0 << 16),
+                                                   ov[1] - __uint_as_float(w0 & 0xffff0000u));
+                    const uint32_t r1 = pack2_bf16(ov[2] - __uint_as_float(w1 << 16),
+                                                   ov[3] - __uint_as_float(w1 & 0xffff0000u));
+                    *reinterpret_cast<uint2*>(o_lo + qtok * D + d0) = make_uint2(r0, r1);
+                }
             } else {
-                *reinterpret_cast<float4*>(orow + d0) =
-                    make_float4(oacc[mt][g4 * 4 + 0] * inv, oacc[mt][g4 * 4 + 1] * inv,
-                                oacc[mt][g4 * 4 + 2] * inv, oacc[mt][g4 * 4 + 3] * inv);
+                *reinterpret_cast<float4*>(orow + d0) = make_float4(ov[0], ov[1], ov[2], ov[3]);
+                if constexpr (COMP)
+                    *reinterpret_cast<float4*>(o_lo + qtok * D + d0) = make_float4(0.f, 0.f, 0.f, 0.f);
             }
         }
     if (half == 0) lse[qtok] = lt > 0.f ? (m + log2f(lt)) * 0.6931471805599453f : -INFINITY;
@@ -177,26 +192,32 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
 
 template <typename T, int D>
 static hipError_t launch_fwd_t(const void* q, const void* k, const void* v, const int32_t* row_ptr,
-                               const int32_t* col_idx, int64_t col_cap, void* o, float* lse,
+                               const int32_t* col_idx, int64_t col_cap, void* o, float* lse, void* o_lo,
                                int batch, int Hq, int Hkv, int N, hipStream_t s) {
     const int64_t rows = static_cast<int64_t>(batch) * Hq * N;
     if (rows == 0) return hipSuccess;
     const float c = 1.4426950408889634f / sqrtf(static_cast<float>(D));
-    hipLaunchKernelGGL((attn_fwd_kernel<T, D>), dim3(static_cast<unsigned>(rows)), dim3(AF_NT), 0, s,
-                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
-                       row_ptr, col_idx, col_cap, static_cast<T*>(o), lse, Hq, Hkv, N, c);
+    if (o_lo)
+        hipLaunchKernelGGL((attn_fwd_kernel<T, D, true>), dim3(static_cast<unsigned>(rows)), dim3(AF_NT), 0, s,
+                           static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+                           row_ptr, col_idx, col_cap, static_cast<T*>(o), lse, static_cast<T*>(o_lo), Hq, Hkv,
+                           N, c);
+    else
+        hipLaunchKernelGGL((attn_fwd_kernel<T, D, false>), dim3(static_cast<unsigned>(rows)), dim3(AF_NT), 0, s,
+                           static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+                           row_ptr, col_idx, col_cap, static_cast<T*>(o), lse, nullptr, Hq, Hkv, N, c);
     return hipGetLastError();
 }
 
 hipError_t launch_attn_fwd(int dtype, int D, const void* q, const void* k, const void* v,
                            const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
-                           float* lse, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                           float* lse, void* o_lo, int batch, int Hq, int Hkv, int N, hipStream_t s) {
     if (dtype == 1) {
-        if (D == 64) return launch_fwd_t<bf16_t, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, batch, Hq, Hkv, N, s);
-        if (D == 128) return launch_fwd_t<bf16_t, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, batch, Hq, Hkv, N, s);
+        if (D == 64) return launch_fwd_t<bf16_t, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, batch, Hq, Hkv, N, s);
+        if (D == 128) return launch_fwd_t<bf16_t, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, batch, Hq, Hkv, N, s);
     } else {
-        if (D == 64) return launch_fwd_t<float, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, batch, Hq, Hkv, N, s);
-        if (D == 128) return launch_fwd_t<float, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, batch, Hq, Hkv, N, s);
+        if (D == 64) return launch_fwd_t<float, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, batch, Hq, Hkv, N, s);
+        if (D == 128) return launch_fwd_t<float, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, batch, Hq, Hkv, N, s);
     }
     return hipErrorInvalidValue;
 }

@@ -104,6 +104,26 @@ __device__ __forceinline__ void pack_frag(frag_f32& f, const float* x) {
     for (int i = 0; i < 8; ++i) f.v[i] = x[i];
 }
 
+// Two-term split of 8 fp32 values for compensated products: hi = bf16(x),
+// lo = bf16(x - hi), so hi + lo carries about 16 significant bits and
+// A*hi + A*lo reproduces A*x to ~2^-17 relative instead of 2^-9.
+__device__ __forceinline__ void pack_frag_hilo(frag_bf16& hi, frag_bf16& lo, const float* x) {
+    typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4_t;
+    u32x4_t wh, wl;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        wh[i] = pack2_bf16(x[2 * i], x[2 * i + 1]);
+        const float h0 = __uint_as_float(wh[i] << 16), h1 = __uint_as_float(wh[i] & 0xffff0000u);
+        wl[i] = pack2_bf16(x[2 * i] - h0, x[2 * i + 1] - h1);
+    }
+    hi.v = __builtin_bit_cast(bf16x8_t, wh);
+    lo.v = __builtin_bit_cast(bf16x8_t, wl);
+}
+__device__ __forceinline__ void pack_frag_hilo(frag_f32& hi, frag_f32& lo, const float* x) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) { hi.v[i] = x[i]; lo.v[i] = 0.f; }
+}
+
 // Make the compiler complete the loads of a fragment here (an opaque use of
 // its registers), so no wait for them is left inside a later loop.
 __device__ __forceinline__ void settle(const frag_bf16& f) {
@@ -323,10 +343,13 @@ __device__ __forceinline__ int32_t scalar_load_i32(const int32_t* p) {
 // apart, does not put a full vmcnt(0) wait in front of every LDS read; the
 // kernels order these copies themselves with vm_wait and wg_barrier.
 __device__ __forceinline__ void dma16(uint32_t lds, const void* base, int voff) {
-    const uint32_t l = __builtin_amdgcn_readfirstlane(lds);
+    // readfirstlane works on (signed) 32-bit ints: both halves go back through
+    // uint32_t so the low word is zero-extended, never sign-extended.
+    const uint32_t l = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(lds)));
     const uint64_t b = reinterpret_cast<uint64_t>(base);
-    const uint64_t bs = (static_cast<uint64_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b >> 32))) << 32) |
-                        __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b));
+    const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b >> 32)));
+    const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b & 0xffffffffu)));
+    const uint64_t bs = (static_cast<uint64_t>(hi) << 32) | static_cast<uint64_t>(lo);
     asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
                  :
                  : "s"(l), "v"(voff), "s"(bs)

@@ -22,10 +22,10 @@ hipError_t launch_csc(const int32_t* row_ptr, const int32_t* col_idx, int batch,
                       int32_t* kv_idx, hipStream_t s);
 hipError_t launch_attn_fwd(int dtype, int D, const void* q, const void* k, const void* v,
                            const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
-                           float* lse, int batch, int Hq, int Hkv, int N, hipStream_t s);
+                           float* lse, void* o_lo, int batch, int Hq, int Hkv, int N, hipStream_t s);
 size_t bwd_workspace_bytes(int dtype, int D, int batch, int Hq, int Hkv, int N);
 hipError_t launch_attn_bwd(int dtype, int D, const void* q, const void* k, const void* v, const void* o,
-                           const float* lse, const void* dout, const int32_t* row_ptr,
+                           const float* lse, const void* o_lo, const void* dout, const int32_t* row_ptr,
                            const int32_t* col_idx, const int32_t* kv_ptr, const int32_t* kv_idx,
                            int64_t col_cap, void* dq, void* dk, void* dv, void* ws, int batch,
                            int Hq, int Hkv, int N, hipStream_t s);

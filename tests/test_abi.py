@@ -71,22 +71,24 @@ def test_attn_fwd_rejects_bad_problem(mutate, expect):
     p = good()
     for k, v in mutate.items():
         setattr(p, k, v)
-    st = vsa2.vsa2_attn_fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE, FAKE, FAKE, 1 << 40, None)
+    st = vsa2.vsa2_attn_fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE, FAKE, None, FAKE, 1 << 40, None)
     assert vsa2.STATUS_NAMES[st] == expect
 
 
 def test_null_and_alignment_checks():
     p = good()
-    assert vsa2.STATUS_NAMES[vsa2.vsa2_attn_fwd(p, None, FAKE, FAKE, FAKE, FAKE, 1, FAKE, FAKE, None, 0,
-                                                None)] == "VSA2_ERR_NULL"
+    assert vsa2.STATUS_NAMES[vsa2.vsa2_attn_fwd(p, None, FAKE, FAKE, FAKE, FAKE, 1, FAKE, FAKE, None,
+                                                None, 0, None)] == "VSA2_ERR_NULL"
     assert vsa2.STATUS_NAMES[vsa2.vsa2_attn_fwd(p, MISALIGNED, FAKE, FAKE, FAKE, FAKE, 1, FAKE, FAKE,
-                                                FAKE, 1 << 40, None)] == "VSA2_ERR_ALIGN"
+                                                None, FAKE, 1 << 40, None)] == "VSA2_ERR_ALIGN"
+    assert vsa2.STATUS_NAMES[vsa2.vsa2_attn_fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, 1, FAKE, FAKE,
+                                                MISALIGNED, FAKE, 1 << 40, None)] == "VSA2_ERR_ALIGN"
     assert vsa2.STATUS_NAMES[vsa2.vsa2_pool(p, 4, FAKE, 2, 2, 2, MISALIGNED, None)] == "VSA2_ERR_ALIGN"
     assert vsa2.STATUS_NAMES[vsa2.vsa2_pool(p, 4, FAKE, 3, 2, 2, FAKE, None)] == "VSA2_ERR_SHAPE"
     assert vsa2.STATUS_NAMES[vsa2.vsa2_pool(None, 4, FAKE, 2, 2, 2, FAKE, None)] == "VSA2_ERR_NULL"
     # bwd needs a workspace for the per-query Delta
-    st = vsa2.vsa2_attn_bwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, FAKE,
-                            FAKE, FAKE, None, 0, None)
+    st = vsa2.vsa2_attn_bwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, 1,
+                            FAKE, FAKE, FAKE, None, 0, None)
     assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_WORKSPACE"
 
 
