@@ -371,7 +371,10 @@ void vo_attn_bwd_dq(const float* q, const float* k, const float* v, const float*
 
 /* dK and dV for listed key blocks: kvrows[i] = (b*Hkv + hkv)*N + nk.
  * Every query token of every query head of the KV head's group whose row
- * selects block nk contributes.  dk, dv: [nkv][B][D]. */
+ * selects block nk contributes.  dk, dv: [nkv][B][D].
+ * The (key block, selecting query block) pairs are enumerated first and their
+ * contributions computed independently (in parallel), then summed per key
+ * block in pair order, so the result does not depend on the thread count. */
 void vo_attn_bwd_dkdv(const float* q, const float* k, const float* v, const float* dout,
                       int nb, int Hq, int Hkv, int64_t L, int D, int B,
                       const int32_t* row_ptr, const int32_t* col_idx,
@@ -381,48 +384,70 @@ void vo_attn_bwd_dkdv(const float* q, const float* k, const float* v, const floa
     const int64_t N = L / B;
     const int grp = Hq / Hkv;
     const double scale = 1.0 / sqrt((double)D);
+    const int64_t BD = (int64_t)B * D;
+
+    /* 1. pairs (kv index r, query-block row, position of nk in that row) */
+    int64_t npairs = 0, cap = 16;
+    int64_t* pr = (int64_t*)malloc(sizeof(int64_t) * 3 * (size_t)cap);
+    for (int64_t r = 0; r < nkv; ++r) {
+        const int64_t krow = kvrows[r];
+        const int64_t bkv = krow / N, nk = krow % N;
+        const int64_t b = bkv / Hkv, hkv = bkv % Hkv;
+        for (int hl = 0; hl < grp; ++hl) {
+            const int64_t bh = b * Hq + hkv * grp + hl;
+            for (int64_t n = 0; n < N; ++n) {
+                const int64_t row = bh * N + n;
+                for (int32_t e = row_ptr[row]; e < row_ptr[row + 1]; ++e) {
+                    if (col_idx[e] != nk) continue;
+                    if (npairs == cap) {
+                        cap *= 2;
+                        pr = (int64_t*)realloc(pr, sizeof(int64_t) * 3 * (size_t)cap);
+                    }
+                    pr[3 * npairs + 0] = r;
+                    pr[3 * npairs + 1] = row;
+                    pr[3 * npairs + 2] = e - row_ptr[row];
+                    ++npairs;
+                }
+            }
+        }
+    }
+    double* ck = (double*)calloc((size_t)(npairs > 0 ? npairs : 1) * (size_t)BD, sizeof(double));
+    double* cv = (double*)calloc((size_t)(npairs > 0 ? npairs : 1) * (size_t)BD, sizeof(double));
+
+    /* 2. contribution of each pair */
 #pragma omp parallel
     {
         double* p = (double*)malloc(sizeof(double) * (size_t)L);
         double* o = (double*)malloc(sizeof(double) * (size_t)D);
 #pragma omp for schedule(dynamic, 1)
-        for (int64_t r = 0; r < nkv; ++r) {
+        for (int64_t i = 0; i < npairs; ++i) {
+            const int64_t r = pr[3 * i], row = pr[3 * i + 1];
+            const int pos = (int)pr[3 * i + 2];
             const int64_t krow = kvrows[r];
             const int64_t bkv = krow / N, nk = krow % N;
-            const int64_t b = bkv / Hkv, hkv = bkv % Hkv;
             const float* K = k + bkv * L * D;
             const float* V = v + bkv * L * D;
-            double* gk = dk + r * (int64_t)B * D;
-            double* gv = dv + r * (int64_t)B * D;
-            for (int64_t i = 0; i < (int64_t)B * D; ++i) { gk[i] = 0.0; gv[i] = 0.0; }
-            for (int hl = 0; hl < grp; ++hl) {
-                const int64_t h = hkv * grp + hl;
-                const int64_t bh = b * Hq + h;
-                for (int64_t n = 0; n < N; ++n) {
-                    const int64_t row = bh * N + n;
-                    const int32_t* sel = col_idx + row_ptr[row];
-                    const int nsel = row_ptr[row + 1] - row_ptr[row];
-                    int pos = -1;
-                    for (int c = 0; c < nsel; ++c) if (sel[c] == nk) pos = c;
-                    if (pos < 0) continue;
-                    for (int t = 0; t < B; ++t) {
-                        const int64_t tok = bh * L + n * B + t;
-                        const float* qv = q + tok * D;
-                        const float* dov = dout + tok * D;
-                        token_forward(qv, K, V, D, B, sel, nsel, scale, p, o);
-                        double delta = 0.0;
-                        for (int d = 0; d < D; ++d) delta += (double)dov[d] * o[d];
-                        for (int u = 0; u < B; ++u) {
-                            const int64_t j = nk * B + u;
-                            const double pj = p[pos * B + u];
-                            double dp = 0.0;
-                            for (int d = 0; d < D; ++d) dp += (double)dov[d] * (double)V[j * D + d];
-                            const double ds = pj * (dp - delta);
-                            for (int d = 0; d < D; ++d) {
-                                gv[u * D + d] += pj * (double)dov[d];
-                                gk[u * D + d] += scale * ds * (double)qv[d];
-                            }
-                        }
+            const int64_t bh = row / N, n = row % N;
+            const int32_t* sel = col_idx + row_ptr[row];
+            const int nsel = row_ptr[row + 1] - row_ptr[row];
+            double* gk = ck + i * BD;
+            double* gv = cv + i * BD;
+            for (int t = 0; t < B; ++t) {
+                const int64_t tok = bh * L + n * B + t;
+                const float* qv = q + tok * D;
+                const float* dov = dout + tok * D;
+                token_forward(qv, K, V, D, B, sel, nsel, scale, p, o);
+                double delta = 0.0;
+                for (int d = 0; d < D; ++d) delta += (double)dov[d] * o[d];
+                for (int u = 0; u < B; ++u) {
+                    const int64_t j = nk * B + u;
+                    const double pj = p[pos * B + u];
+                    double dp = 0.0;
+                    for (int d = 0; d < D; ++d) dp += (double)dov[d] * (double)V[j * D + d];
+                    const double ds = pj * (dp - delta);
+                    for (int d = 0; d < D; ++d) {
+                        gv[u * D + d] += pj * (double)dov[d];
+                        gk[u * D + d] += scale * ds * (double)qv[d];
                     }
                 }
             }
@@ -430,4 +455,17 @@ void vo_attn_bwd_dkdv(const float* q, const float* k, const float* v, const floa
         free(p);
         free(o);
     }
+
+    /* 3. sum per key block, in pair order */
+    for (int64_t i = 0; i < nkv * BD; ++i) { dk[i] = 0.0; dv[i] = 0.0; }
+    for (int64_t i = 0; i < npairs; ++i) {
+        const int64_t r = pr[3 * i];
+        for (int64_t x = 0; x < BD; ++x) {
+            dk[r * BD + x] += ck[i * BD + x];
+            dv[r * BD + x] += cv[i * BD + x];
+        }
+    }
+    free(ck);
+    free(cv);
+    free(pr);
 }

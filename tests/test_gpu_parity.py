@@ -204,8 +204,9 @@ def test_compensated_forward_remainder(case):
     err = np.abs(full - o_ref).max() / max(1.0, np.abs(o_ref).max())
     print("O + o_lo max rel err %.3e" % err)
     assert err < (2e-5 if p.dtype == BF16 else 1e-5)
-    # the rounded output differs from the plain path by at most one ulp
-    assert_values(to_np(o2), to_np(o1), "O compensated vs plain", dtname(p), max_abs=1e-6, rel_l2=1e-2)
+    # the rounded output itself meets the same bar as the plain path's
+    assert_values(to_np(o2).reshape(o_ref.shape), o_ref, "O (compensated)", dtname(p))
+    assert_values(to_np(o1).reshape(o_ref.shape), o_ref, "O (plain)", dtname(p))
 
 
 def test_bwd_deterministic_sentinels_and_unselected_blocks(case):
