@@ -42,6 +42,9 @@ def parse():
                     help="query-block rows (forward + dQ) in the oracle's timed sample")
     ap.add_argument("--cpu-kv", type=int, default=8,
                     help="key blocks (dK/dV) in the oracle's timed sample")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after timing, copy a buffer of this size once (reference kernel "
+                         "for scaling hardware byte counters)")
     return ap.parse_args()
 
 
@@ -137,6 +140,14 @@ def main():
     wall = time.perf_counter() - t_start
     ms_step = wall * 1e3 / args.steps
     stage_ms = {s: float(np.mean([a.elapsed_time(b) for a, b in ev[s]])) for s in stages}
+
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     nnz = int(row_ptr[-1].item())
     flop_fwd = 4.0 * B * B * D * nnz

@@ -77,14 +77,14 @@ __global__ __launch_bounds__(AB_NT, GRAD == 1 ? 1 : 2) void dkdv_kernel(
     constexpr int KS = D / 16;
     constexpr int MT = D / 32;
     constexpr int RB = D * E;                    // tile row bytes
-    constexpr bool SPLIT = COMP && GRAD == 1 && sizeof(T) == 2;   // dS as hi + lo
+    constexpr bool SPLIT = COMP && sizeof(T) == 2;   // P (dV) or dS (dK) as hi + lo
     using RT = async_tile<64, RB, 2, true>;      // Q, dO rows (slot-swapped)
     __shared__ __align__(1024) char q_lds[RT::BYTES];
     __shared__ __align__(1024) char o_lds[RT::BYTES];
     __shared__ __align__(1024) float2 st_lds[64];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = wave_id(), half = lane >> 5;
-    const int64_t krow = blockIdx.x;                 // (b*Hkv + hkv)*N + nk
+    const int64_t krow = xcd_item(blockIdx.x, gridDim.x);   // (b*Hkv + hkv)*N + nk
     const int64_t bkv = krow / N;
     const int nk = static_cast<int>(krow % N);
     const int b = static_cast<int>(bkv / Hkv), hkv = static_cast<int>(bkv % Hkv);
@@ -153,7 +153,7 @@ __global__ __launch_bounds__(AB_NT, GRAD == 1 ? 1 : 2) void dkdv_kernel(
         if constexpr (GRAD == 0) vm_wait<O_OPS>(); else vm_wait<0>();
         wg_barrier();
         F fb[2][2];                     // P (dV) or dS (dK) by [query tile][k-step half]
-        F fl[SPLIT ? 2 : 1][2];          // low part of dS (compensated)
+        F fl[SPLIT ? 2 : 1][2];          // low parts (compensated)
 #pragma unroll
         for (int qtile = 0; qtile < 2; ++qtile) {
             // S = Q K^T (and dP = dO V^T) for 32 queries x this lane's key
@@ -260,7 +260,7 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     __shared__ __align__(1024) char v_lds[RT::BYTES];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = wave_id(), half = lane >> 5;
-    const int64_t row = blockIdx.x;
+    const int64_t row = xcd_item(blockIdx.x, gridDim.x);
     const int64_t bh = row / N;
     const int n = static_cast<int>(row % N);
     const int b = static_cast<int>(bh / Hq), h = static_cast<int>(bh % Hq);

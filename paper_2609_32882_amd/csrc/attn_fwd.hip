@@ -42,7 +42,7 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     __shared__ __align__(1024) char v_lds[VT::BYTES];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = wave_id(), half = lane >> 5;
-    const int64_t row = blockIdx.x;
+    const int64_t row = xcd_item(blockIdx.x, gridDim.x);
     const int64_t bh = row / N;
     const int n = static_cast<int>(row % N);
     const int b = static_cast<int>(bh / Hq), h = static_cast<int>(bh % Hq);

@@ -165,6 +165,18 @@ __device__ __forceinline__ int swap_bits_2_3(int r) {
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 
+// Workgroup -> work-item mapping that keeps neighbouring items on one XCD.
+// Workgroups are dispatched round-robin over the 8 XCDs (workgroup id mod 8),
+// each with its own L2.  Mapping XCD x to the contiguous range of items
+// [x*q + min(x, r), ...) (q = n / 8, r = n % 8) makes the workgroups of one
+// XCD work on the same head and nearby blocks, so the key/value tiles they
+// gather stay in that XCD's L2 instead of being fetched by all eight.
+__device__ __forceinline__ int64_t xcd_item(int64_t bid, int64_t n) {
+    const int64_t q = n >> 3, r = n & 7;
+    const int64_t x = bid & 7, i = bid >> 3;
+    return x * q + (x < r ? x : r) + i;
+}
+
 // Index of the calling wave inside its workgroup, as a wave-uniform (scalar) value.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
