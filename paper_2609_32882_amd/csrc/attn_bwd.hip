@@ -71,7 +71,7 @@ __global__ __launch_bounds__(AB_NT, GRAD == 1 ? 1 : 2) void dkdv_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float2* __restrict__ stat,
     const int32_t* __restrict__ kv_ptr, const int32_t* __restrict__ kv_idx, int64_t col_cap,
-    T* __restrict__ dgrad, int Hq, int Hkv, int N, float c_log2, float scale) {
+    T* __restrict__ dgrad, int Hq, int Hkv, int N, float c_log2, float scale, int period) {
     using F = typename frag_of<T>::type;
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;
@@ -138,15 +138,22 @@ __global__ __launch_bounds__(AB_NT, GRAD == 1 ? 1 : 2) void dkdv_kernel(
         settle(kf[ks]);
         if constexpr (GRAD == 1) settle(vf[ks]);
     }
+    // phased sweep over the query blocks (values hq_local*N + n_q)
+    const int64_t cnt = e1 - e0;
+    const int64_t s0 = sweep_start(kv_idx, e0, cnt, blockIdx.x >> 3, period, grp * N);
+    auto entry = [&](int64_t j) -> int64_t {
+        const int64_t t = s0 + j;
+        return e0 + (t >= cnt ? t - cnt : t);
+    };
     int64_t q_cur = -1;
-    if (e0 < e1) {
-        q_cur = q0_of(e0);
+    if (cnt > 0) {
+        q_cur = q0_of(entry(0));
         issue_q(q_cur);
         issue_o(q_cur);
     }
-    for (int64_t e = e0; e < e1; ++e) {
-        const bool has_next = e + 1 < e1;
-        const int64_t q_next = has_next ? q0_of(e + 1) : -1;
+    for (int64_t j = 0; j < cnt; ++j) {
+        const bool has_next = j + 1 < cnt;
+        const int64_t q_next = has_next ? q0_of(entry(j + 1)) : -1;
         const bool valid = q_cur >= 0;
 
         // dV: the dO tile may still stream in; dK: dP needs it now
@@ -248,7 +255,7 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float2* __restrict__ stat,
     const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx, int64_t col_cap,
-    T* __restrict__ dq, int Hq, int Hkv, int N, float c_log2, float scale) {
+    T* __restrict__ dq, int Hq, int Hkv, int N, float c_log2, float scale, int period) {
     using F = typename frag_of<T>::type;
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;
@@ -300,15 +307,21 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     for (int ks = 0; ks < KS; ++ks) { settle(qf[ks]); settle(of[ks]); }   // before the copies start
     settle(st.x);
     settle(st.y);
+    const int64_t cnt = e1 - e0;
+    const int64_t s0 = sweep_start(col_idx, e0, cnt, blockIdx.x >> 3, period, N);
+    auto entry = [&](int64_t j) -> int64_t {
+        const int64_t t = s0 + j;
+        return e0 + (t >= cnt ? t - cnt : t);
+    };
     int c_cur = -1;
-    if (e0 < e1) {
-        c_cur = block_of(e0);
+    if (cnt > 0) {
+        c_cur = block_of(entry(0));
         issue_k(c_cur);
         issue_v(c_cur);
     }
-    for (int64_t e = e0; e < e1; ++e) {
-        const bool has_next = e + 1 < e1;
-        const int c_next = has_next ? block_of(e + 1) : -1;
+    for (int64_t j = 0; j < cnt; ++j) {
+        const bool has_next = j + 1 < cnt;
+        const int c_next = has_next ? block_of(entry(j + 1)) : -1;
 
         vm_wait<0>();                   // K and V landed
         wg_barrier();
@@ -409,14 +422,17 @@ static hipError_t launch_bwd_t(const void* q, const void* k, const void* v, cons
     if (e != hipSuccess) return e;
     const int64_t krows = static_cast<int64_t>(batch) * Hkv * N;
     hipLaunchKernelGGL((dkdv_kernel<T, D, 0, COMP>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s, Q, K, V,
-                       dO, stat, kv_ptr, kv_idx, col_cap, static_cast<T*>(dv), Hq, Hkv, N, c, scale);
+                       dO, stat, kv_ptr, kv_idx, col_cap, static_cast<T*>(dv), Hq, Hkv, N, c, scale,
+                       resident_per_xcd<dkdv_kernel<T, D, 0, COMP>>(AB_NT));
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL((dkdv_kernel<T, D, 1, COMP>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s, Q, K, V,
-                       dO, stat, kv_ptr, kv_idx, col_cap, static_cast<T*>(dk), Hq, Hkv, N, c, scale);
+                       dO, stat, kv_ptr, kv_idx, col_cap, static_cast<T*>(dk), Hq, Hkv, N, c, scale,
+                       resident_per_xcd<dkdv_kernel<T, D, 1, COMP>>(AB_NT));
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const int64_t qrows = static_cast<int64_t>(batch) * Hq * N;
     hipLaunchKernelGGL((dq_kernel<T, D, COMP>), dim3(static_cast<unsigned>(qrows)), dim3(AB_NT), 0, s, Q, K, V, dO,
-                       stat, row_ptr, col_idx, col_cap, static_cast<T*>(dq), Hq, Hkv, N, c, scale);
+                       stat, row_ptr, col_idx, col_cap, static_cast<T*>(dq), Hq, Hkv, N, c, scale,
+                       resident_per_xcd<dq_kernel<T, D, COMP>>(AB_NT));
     return hipGetLastError();
 }
 

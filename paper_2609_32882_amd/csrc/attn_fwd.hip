@@ -29,7 +29,8 @@ template <typename T, int D, bool COMP>
 __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx, int64_t col_cap,
-    T* __restrict__ o, float* __restrict__ lse, T* __restrict__ o_lo, int Hq, int Hkv, int N, float c_log2) {
+    T* __restrict__ o, float* __restrict__ lse, T* __restrict__ o_lo, int Hq, int Hkv, int N, float c_log2,
+    int period) {
     using F = typename frag_of<T>::type;
     constexpr bool SPLIT = COMP && sizeof(T) == 2;
     constexpr int E = sizeof(T);
@@ -76,16 +77,23 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     const KT& vt_ = kt;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) settle(qf[ks]);   // fragments in registers before the copies start
+    // phased sweep: entry j of the row is e0 + (s0 + j) mod cnt
+    const int64_t cnt = e1 - e0;
+    const int64_t s0 = sweep_start(col_idx, e0, cnt, blockIdx.x >> 3, period, N);
+    auto entry = [&](int64_t j) -> int64_t {
+        const int64_t t = s0 + j;
+        return e0 + (t >= cnt ? t - cnt : t);
+    };
     int c_cur = -1;
-    if (e0 < e1) {
-        c_cur = block_of(e0);
+    if (cnt > 0) {
+        c_cur = block_of(entry(0));
         const int cc = c_cur < 0 ? 0 : c_cur;
         kt.issue(k_lds, kb + static_cast<int64_t>(cc) * 64 * KRB, wave);
         vt_.issue(v_lds, vb + static_cast<int64_t>(cc) * 64 * KRB, wave);
     }
-    for (int64_t e = e0; e < e1; ++e) {
-        const bool has_next = e + 1 < e1;
-        const int c_next = has_next ? block_of(e + 1) : -1;
+    for (int64_t j = 0; j < cnt; ++j) {
+        const bool has_next = j + 1 < cnt;
+        const int c_next = has_next ? block_of(entry(j + 1)) : -1;
         const int64_t nxt_off = static_cast<int64_t>(c_next < 0 ? 0 : c_next) * 64 * KRB;
 
         vm_wait<VT::PER_WAVE>();          // this K tile has landed (V may still stream)
@@ -201,11 +209,12 @@ static hipError_t launch_fwd_t(const void* q, const void* k, const void* v, cons
         hipLaunchKernelGGL((attn_fwd_kernel<T, D, true>), dim3(static_cast<unsigned>(rows)), dim3(AF_NT), 0, s,
                            static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
                            row_ptr, col_idx, col_cap, static_cast<T*>(o), lse, static_cast<T*>(o_lo), Hq, Hkv,
-                           N, c);
+                           N, c, resident_per_xcd<attn_fwd_kernel<T, D, true>>(AF_NT));
     else
         hipLaunchKernelGGL((attn_fwd_kernel<T, D, false>), dim3(static_cast<unsigned>(rows)), dim3(AF_NT), 0, s,
                            static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
-                           row_ptr, col_idx, col_cap, static_cast<T*>(o), lse, nullptr, Hq, Hkv, N, c);
+                           row_ptr, col_idx, col_cap, static_cast<T*>(o), lse, nullptr, Hq, Hkv, N, c,
+                           resident_per_xcd<attn_fwd_kernel<T, D, false>>(AF_NT));
     return hipGetLastError();
 }
 

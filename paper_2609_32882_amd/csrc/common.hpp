@@ -368,6 +368,28 @@ __device__ __forceinline__ void dma16(uint32_t lds, const void* base, int voff) 
                  : "memory", "m0");
 }
 
+// Start offset of a block list for a phased sweep.  The workgroups resident
+// on one XCD at the same time (about `period` of them, dispatched in order)
+// would otherwise all sweep their ascending lists from the start at different
+// times and touch the whole key (or query) range at once.  Row number `local`
+// on its XCD instead starts at the first entry >= (local mod period) * npos /
+// period and wraps around: workgroups that run together sit at about the same
+// position, so the tiles they gather are shared through the XCD's L2.  The
+// start depends only on the row number, so results stay deterministic.
+// Entries are read through the scalar cache (binary search, ~log2(n) loads).
+__device__ __forceinline__ int64_t sweep_start(const int32_t* list, int64_t e0, int64_t cnt, int64_t local,
+                                               int period, int npos) {
+    if (cnt < 2 || period < 2) return 0;
+    const int pos = static_cast<int>(((local % period) * npos) / period);
+    int64_t lo = 0, hi = cnt;
+    while (lo < hi) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (scalar_load_i32(list + e0 + mid) < pos) lo = mid + 1;
+        else hi = mid;
+    }
+    return lo == cnt ? 0 : lo;
+}
+
 // LDS tiles are stored with a row stride of RB + 16 bytes: 16 lanes reading
 // the same 16-byte column of 16 consecutive rows then hit 16 different bank
 // groups, and every fragment address is one per-lane base plus a compile-time

@@ -5,7 +5,32 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace vsa2 {
+
+// Number of workgroups of kernel `Kern` (block threads, static LDS) resident
+// per XCD at once: occupancy per CU times CUs / 8.  Used as the period of the
+// phased block-list sweep.  Cached per kernel (one instantiation each) and
+// per device.
+template <auto Kern>
+int resident_per_xcd(int block) {
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 1;
+    std::atomic<int>& slot = cache[dev & 63];
+    int v = slot.load(std::memory_order_relaxed);
+    if (v > 0) return v;
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(Kern), block, 0) !=
+            hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 1;
+    v = per_cu * cus / 8;
+    if (v < 1) v = 1;
+    slot.store(v, std::memory_order_relaxed);
+    return v;
+}
 
 hipError_t launch_pool(int dtype, const void* x, void* out, int64_t nbh, int N, int D, int Bt, int Bh,
                        int Bw, int Pt, int Ph, int Pw, hipStream_t s);
