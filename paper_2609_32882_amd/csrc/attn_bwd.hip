@@ -8,8 +8,8 @@
 //   stat_kernel      per query token: (LSE * log2(e), Delta)
 //   dkdv_kernel      key-block stationary: one workgroup per key block walks
 //                    the transposed (CSC) list of query blocks that selected
-//                    it; a wave owns 32 keys; one launch accumulates dV^T,
-//                    a second dK^T, in registers
+//                    it; a wave owns 32 keys and accumulates dV^T and dK^T
+//                    in registers
 //   dq_kernel        query-block stationary: one workgroup per query block
 //                    walks its CSR row; a wave owns 32 queries
 // Products are arranged so that each lane owns one column (a key in dkdv, a
@@ -59,29 +59,31 @@ __global__ __launch_bounds__(256) void stat_kernel(const T* __restrict__ o, cons
 }
 
 // ---------------------------------------------------------------------------
-// dV (GRAD = 0) or dK (GRAD = 1): one workgroup (2 waves) per key block of
-// head (b, hkv); a wave owns 32 keys.  The two gradients run as separate
-// launches so each keeps one accumulator set (64 registers); the price is
-// recomputing S once more per block pair.
-//   dV^T += dO^T P    tiles Q (for S) and dO (for dO^T)
-//   dK^T += Q^T dS    tiles Q (for S and Q^T) and dO (for dP)
+// dK and dV: one workgroup (2 waves) per key block of head (b, hkv); a wave
+// owns 32 keys and keeps both accumulators (dV^T, dK^T) in registers.  Per
+// selecting query block:
+//   S = Q K^T, dP = dO V^T   (Q, dO rows from LDS; K, V in registers)
+//   P = exp2(S c - LSE log2 e), dS = P (dP - Delta)
+//   dV^T += dO^T P,  dK^T += Q^T dS   (dO^T, Q^T read transposed from LDS)
+// The Q / dO / stat tiles are double-buffered: the copies of the next query
+// block stream in during the whole of the current one.
 // ---------------------------------------------------------------------------
-template <typename T, int D, int GRAD, bool COMP>
-__global__ __launch_bounds__(AB_NT, GRAD == 1 ? 1 : 2) void dkdv_kernel(
+template <typename T, int D, bool COMP>
+__global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float2* __restrict__ stat,
     const int32_t* __restrict__ kv_ptr, const int32_t* __restrict__ kv_idx, int64_t col_cap,
-    T* __restrict__ dgrad, int Hq, int Hkv, int N, float c_log2, float scale, int period) {
+    T* __restrict__ dk, T* __restrict__ dv, int Hq, int Hkv, int N, float c_log2, float scale, int period) {
     using F = typename frag_of<T>::type;
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;
     constexpr int MT = D / 32;
     constexpr int RB = D * E;                    // tile row bytes
-    constexpr bool SPLIT = COMP && sizeof(T) == 2;   // P (dV) or dS (dK) as hi + lo
+    constexpr bool SPLIT = COMP && sizeof(T) == 2;   // P and dS as hi + lo
     using RT = async_tile<64, RB, 2, true>;      // Q, dO rows (slot-swapped)
-    __shared__ __align__(1024) char q_lds[RT::BYTES];
-    __shared__ __align__(1024) char o_lds[RT::BYTES];
-    __shared__ __align__(1024) float2 st_lds[64];
+    __shared__ __align__(1024) char q_lds[2][RT::BYTES];
+    __shared__ __align__(1024) char o_lds[2][RT::BYTES];
+    __shared__ __align__(1024) float2 st_lds[2][64];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = wave_id(), half = lane >> 5;
     const int64_t krow = xcd_item(blockIdx.x, gridDim.x);   // (b*Hkv + hkv)*N + nk
@@ -96,18 +98,18 @@ __global__ __launch_bounds__(AB_NT, GRAD == 1 ? 1 : 2) void dkdv_kernel(
     e0 = e0 < 0 ? 0 : (e0 > col_cap ? col_cap : e0);
     e1 = e1 < e0 ? e0 : (e1 > col_cap ? col_cap : e1);
 
-    // K (and for dK also V) rows of this lane's key as B operands (column = key, k = d)
-    F kf[KS], vf[GRAD == 1 ? KS : 1];
+    // K and V rows of this lane's key as B operands (column = key, k = d)
+    F kf[KS], vf[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
         load_frag(kf[ks], k + ktok * D + ks * 16 + half * 8);
-        if constexpr (GRAD == 1) load_frag(vf[ks], v + ktok * D + ks * 16 + half * 8);
+        load_frag(vf[ks], v + ktok * D + ks * 16 + half * 8);
     }
-    f32x16_t acc[MT];
+    f32x16_t acc_v[MT], acc_k[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) acc[mt][i] = 0.f;
+        for (int i = 0; i < 16; ++i) { acc_v[mt][i] = 0.f; acc_k[mt][i] = 0.f; }
 
     // query-block token offset of entry e, or -1 for a malformed entry
     auto q0_of = [&](int64_t e) -> int64_t {
@@ -118,25 +120,21 @@ __global__ __launch_bounds__(AB_NT, GRAD == 1 ? 1 : 2) void dkdv_kernel(
         return bh * L + static_cast<int64_t>(ent % N) * 64;
     };
     const RT rt(wave, lane);
-    // (LSE, Delta) of the 64 queries: 512 bytes, 16 lanes of each wave
-    auto issue_q = [&](int64_t q0) {
+    // Q, dO and (LSE, Delta) of the 64 queries (512 bytes, 16 lanes of each wave)
+    auto issue = [&](int64_t q0, int buf) {
         const int64_t o0 = q0 < 0 ? 0 : q0;
-        rt.issue(q_lds, reinterpret_cast<const char*>(q + o0 * D), wave);
+        rt.issue(q_lds[buf], reinterpret_cast<const char*>(q + o0 * D), wave);
+        rt.issue(o_lds[buf], reinterpret_cast<const char*>(dout + o0 * D), wave);
         if (lane < 16)
-            dma16(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)st_lds)) + wave * 256,
+            dma16(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)st_lds[buf])) + wave * 256,
                   reinterpret_cast<const char*>(stat + o0) + wave * 256, lane * 16);
     };
-    auto issue_o = [&](int64_t q0) {
-        const int64_t o0 = q0 < 0 ? 0 : q0;
-        rt.issue(o_lds, reinterpret_cast<const char*>(dout + o0 * D), wave);
-    };
-    constexpr int Q_OPS = RT::PER_WAVE + 1;
-    constexpr int O_OPS = RT::PER_WAVE;
+    constexpr int OPS = 2 * RT::PER_WAVE + 1;    // copies per wave per query block
 
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {   // fragments in registers before the copies start
         settle(kf[ks]);
-        if constexpr (GRAD == 1) settle(vf[ks]);
+        settle(vf[ks]);
     }
     // phased sweep over the query blocks (values hq_local*N + n_q)
     const int64_t cnt = e1 - e0;
@@ -148,100 +146,101 @@ __global__ __launch_bounds__(AB_NT, GRAD == 1 ? 1 : 2) void dkdv_kernel(
     int64_t q_cur = -1;
     if (cnt > 0) {
         q_cur = q0_of(entry(0));
-        issue_q(q_cur);
-        issue_o(q_cur);
+        issue(q_cur, 0);
     }
     for (int64_t j = 0; j < cnt; ++j) {
+        const int buf = static_cast<int>(j & 1);
         const bool has_next = j + 1 < cnt;
         const int64_t q_next = has_next ? q0_of(entry(j + 1)) : -1;
-        const bool valid = q_cur >= 0;
-
-        // dV: the dO tile may still stream in; dK: dP needs it now
-        if constexpr (GRAD == 0) vm_wait<O_OPS>(); else vm_wait<0>();
+        // the other buffer was released by the barrier that ended the last step
+        if (has_next) {
+            issue(q_next, buf ^ 1);
+            vm_wait<OPS>();             // this block's copies have landed
+        } else {
+            vm_wait<0>();
+        }
         wg_barrier();
-        F fb[2][2];                     // P (dV) or dS (dK) by [query tile][k-step half]
-        F fl[SPLIT ? 2 : 1][2];          // low parts (compensated)
+        const char* qt = q_lds[buf];
+        const char* ot = o_lds[buf];
+        const float2* st = st_lds[buf];
+        if (q_cur >= 0) {
+            F pb[2][2], db[2][2];               // P and dS by [query tile][k-step half]
+            F pl[SPLIT ? 2 : 1][2], dl[SPLIT ? 2 : 1][2];   // low parts (compensated)
 #pragma unroll
-        for (int qtile = 0; qtile < 2; ++qtile) {
-            // S = Q K^T (and dP = dO V^T) for 32 queries x this lane's key
-            f32x16_t s, dp;
+            for (int qtile = 0; qtile < 2; ++qtile) {
+                // S = Q K^T and dP = dO V^T for 32 queries x this lane's key
+                f32x16_t s, dp;
 #pragma unroll
-            for (int i = 0; i < 16; ++i) { s[i] = 0.f; dp[i] = 0.f; }
+                for (int i = 0; i < 16; ++i) { s[i] = 0.f; dp[i] = 0.f; }
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                F a;
-                lds_frag_s<RB>(a, q_lds, qtile * 32 + (lane & 31), ks * 16 + half * 8);
-                mma(s, a, kf[ks]);
-                if constexpr (GRAD == 1) {
-                    lds_frag_s<RB>(a, o_lds, qtile * 32 + (lane & 31), ks * 16 + half * 8);
+                for (int ks = 0; ks < KS; ++ks) {
+                    F a;
+                    lds_frag_s<RB>(a, qt, qtile * 32 + (lane & 31), ks * 16 + half * 8);
+                    mma(s, a, kf[ks]);
+                    lds_frag_s<RB>(a, ot, qtile * 32 + (lane & 31), ks * 16 + half * 8);
                     mma(dp, a, vf[ks]);
                 }
-            }
-            // entry i is query 32qtile + 16(i/8) + 8half + i%8
-            float x[16];
+                // entry i is query 32qtile + 16(i/8) + 8half + i%8
+                float pv[16], dsv[16];
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const float2 st = st_lds[qtile * 32 + (i >> 3) * 16 + half * 8 + (i & 7)];
-                const float p = fast_exp2(s[i] * c_log2 - st.x);
-                x[i] = GRAD == 1 ? p * (dp[i] - st.y) : p;
+                for (int i = 0; i < 16; ++i) {
+                    const float2 sv = st[qtile * 32 + (i >> 3) * 16 + half * 8 + (i & 7)];
+                    pv[i] = fast_exp2(s[i] * c_log2 - sv.x);
+                    dsv[i] = pv[i] * (dp[i] - sv.y);
+                }
+                if constexpr (SPLIT) {
+                    pack_frag_hilo(pb[qtile][0], pl[qtile][0], pv);
+                    pack_frag_hilo(pb[qtile][1], pl[qtile][1], pv + 8);
+                    pack_frag_hilo(db[qtile][0], dl[qtile][0], dsv);
+                    pack_frag_hilo(db[qtile][1], dl[qtile][1], dsv + 8);
+                } else {
+                    pack_frag(pb[qtile][0], pv);
+                    pack_frag(pb[qtile][1], pv + 8);
+                    pack_frag(db[qtile][0], dsv);
+                    pack_frag(db[qtile][1], dsv + 8);
+                }
             }
-            if constexpr (SPLIT) {
-                pack_frag_hilo(fb[qtile][0], fl[qtile][0], x);
-                pack_frag_hilo(fb[qtile][1], fl[qtile][1], x + 8);
-            } else {
-                pack_frag(fb[qtile][0], x);
-                pack_frag(fb[qtile][1], x + 8);
-            }
-        }
-        wg_barrier();
-        if constexpr (GRAD == 0) {
-            // Q tile free: stream the next one during the dV product
-            if (has_next) issue_q(q_next);
-            if (has_next) vm_wait<Q_OPS>(); else vm_wait<0>();   // dO landed
-            wg_barrier();
-        } else {
-            // dO tile free: stream the next one during the dK product
-            if (has_next) issue_o(q_next);
-        }
-        if (valid) {
-            // acc^T += X^T F over the 64 queries (4 k-steps); X = dO (dV) or Q (dK),
-            // read transposed from its row-major tile
-            const char* xt = GRAD == 1 ? q_lds : o_lds;
+            // dV^T += dO^T P and dK^T += Q^T dS over the 64 queries (4 k-steps);
+            // dO^T and Q^T read transposed from their row-major tiles
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
                     F a;
-                    lds_frag_tr<RB, true>(a, xt, mt * 32, kk * 16);
-                    mma(acc[mt], a, fb[kk >> 1][kk & 1]);
-                    if constexpr (SPLIT) mma(acc[mt], a, fl[(kk >> 1) & (SPLIT ? 1 : 0)][kk & 1]);
+                    lds_frag_tr<RB, true>(a, ot, mt * 32, kk * 16);
+                    mma(acc_v[mt], a, pb[kk >> 1][kk & 1]);
+                    if constexpr (SPLIT) mma(acc_v[mt], a, pl[(kk >> 1) & (SPLIT ? 1 : 0)][kk & 1]);
+                    lds_frag_tr<RB, true>(a, qt, mt * 32, kk * 16);
+                    mma(acc_k[mt], a, db[kk >> 1][kk & 1]);
+                    if constexpr (SPLIT) mma(acc_k[mt], a, dl[(kk >> 1) & (SPLIT ? 1 : 0)][kk & 1]);
                 }
         }
-        wg_barrier();
-        if constexpr (GRAD == 0) {
-            if (has_next) issue_o(q_next);
-        } else {
-            if (has_next) issue_q(q_next);
-        }
+        wg_barrier();                   // buffer `buf` free for the step after next
         q_cur = q_next;
     }
 
     // lane holds key column (lane & 31) and d = 32mt + 8(v/4) + 4half + v%4
-    const float sc = GRAD == 1 ? scale : 1.0f;
-    T* grow = dgrad + ktok * D;
+    T* krow_k = dk + ktok * D;
+    T* krow_v = dv + ktok * D;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
             const int d0 = mt * 32 + g4 * 8 + half * 4;
+            float av[4], kx[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                av[i] = acc_v[mt][g4 * 4 + i];
+                kx[i] = acc_k[mt][g4 * 4 + i] * scale;
+            }
             if constexpr (E == 2) {
-                const uint32_t w0 = pack2_bf16(acc[mt][g4 * 4] * sc, acc[mt][g4 * 4 + 1] * sc);
-                const uint32_t w1 = pack2_bf16(acc[mt][g4 * 4 + 2] * sc, acc[mt][g4 * 4 + 3] * sc);
-                *reinterpret_cast<uint2*>(grow + d0) = make_uint2(w0, w1);
+                *reinterpret_cast<uint2*>(krow_v + d0) =
+                    make_uint2(pack2_bf16(av[0], av[1]), pack2_bf16(av[2], av[3]));
+                *reinterpret_cast<uint2*>(krow_k + d0) =
+                    make_uint2(pack2_bf16(kx[0], kx[1]), pack2_bf16(kx[2], kx[3]));
             } else {
-                *reinterpret_cast<float4*>(grow + d0) =
-                    make_float4(acc[mt][g4 * 4] * sc, acc[mt][g4 * 4 + 1] * sc, acc[mt][g4 * 4 + 2] * sc,
-                                acc[mt][g4 * 4 + 3] * sc);
+                *reinterpret_cast<float4*>(krow_v + d0) = make_float4(av[0], av[1], av[2], av[3]);
+                *reinterpret_cast<float4*>(krow_k + d0) = make_float4(kx[0], kx[1], kx[2], kx[3]);
             }
         }
 }
@@ -421,13 +420,9 @@ static hipError_t launch_bwd_t(const void* q, const void* k, const void* v, cons
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t krows = static_cast<int64_t>(batch) * Hkv * N;
-    hipLaunchKernelGGL((dkdv_kernel<T, D, 0, COMP>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s, Q, K, V,
-                       dO, stat, kv_ptr, kv_idx, col_cap, static_cast<T*>(dv), Hq, Hkv, N, c, scale,
-                       resident_per_xcd<dkdv_kernel<T, D, 0, COMP>>(AB_NT));
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((dkdv_kernel<T, D, 1, COMP>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s, Q, K, V,
-                       dO, stat, kv_ptr, kv_idx, col_cap, static_cast<T*>(dk), Hq, Hkv, N, c, scale,
-                       resident_per_xcd<dkdv_kernel<T, D, 1, COMP>>(AB_NT));
+    hipLaunchKernelGGL((dkdv_kernel<T, D, COMP>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s, Q, K, V,
+                       dO, stat, kv_ptr, kv_idx, col_cap, static_cast<T*>(dk), static_cast<T*>(dv), Hq, Hkv, N,
+                       c, scale, resident_per_xcd<dkdv_kernel<T, D, COMP>>(AB_NT));
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const int64_t qrows = static_cast<int64_t>(batch) * Hq * N;
     hipLaunchKernelGGL((dq_kernel<T, D, COMP>), dim3(static_cast<unsigned>(qrows)), dim3(AB_NT), 0, s, Q, K, V, dO,
