@@ -164,21 +164,32 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
         const char* ot = o_lds[buf];
         const float2* st = st_lds[buf];
         if (q_cur >= 0) {
-            F pb[2][2], db[2][2];               // P and dS by [query tile][k-step half]
-            F pl[SPLIT ? 2 : 1][2], dl[SPLIT ? 2 : 1][2];   // low parts (compensated)
+            // Query tiles one after the other: S / dP (8 k-steps), then P, dS,
+            // then the dV / dK products of that tile's 32 queries (2 k-steps).
+            // LDS fragments are requested one batch ahead of the products
+            // that use them (lds_order keeps the compiler from sinking them).
 #pragma unroll
             for (int qtile = 0; qtile < 2; ++qtile) {
-                // S = Q K^T and dP = dO V^T for 32 queries x this lane's key
+                const int row = qtile * 32 + (lane & 31);
                 f32x16_t s, dp;
 #pragma unroll
                 for (int i = 0; i < 16; ++i) { s[i] = 0.f; dp[i] = 0.f; }
+                F fa[2][4];
+                auto fetch = [&](F* f, int bi) {
+                    lds_frag_s<RB>(f[0], qt, row, 32 * bi + half * 8);
+                    lds_frag_s<RB>(f[1], ot, row, 32 * bi + half * 8);
+                    lds_frag_s<RB>(f[2], qt, row, 32 * bi + 16 + half * 8);
+                    lds_frag_s<RB>(f[3], ot, row, 32 * bi + 16 + half * 8);
+                };
+                fetch(fa[0], 0);
 #pragma unroll
-                for (int ks = 0; ks < KS; ++ks) {
-                    F a;
-                    lds_frag_s<RB>(a, qt, qtile * 32 + (lane & 31), ks * 16 + half * 8);
-                    mma(s, a, kf[ks]);
-                    lds_frag_s<RB>(a, ot, qtile * 32 + (lane & 31), ks * 16 + half * 8);
-                    mma(dp, a, vf[ks]);
+                for (int bi = 0; bi < KS / 2; ++bi) {
+                    if (bi + 1 < KS / 2) fetch(fa[(bi + 1) & 1], bi + 1);
+                    lds_order();
+                    mma(s, fa[bi & 1][0], kf[2 * bi]);
+                    mma(dp, fa[bi & 1][1], vf[2 * bi]);
+                    mma(s, fa[bi & 1][2], kf[2 * bi + 1]);
+                    mma(dp, fa[bi & 1][3], vf[2 * bi + 1]);
                 }
                 // entry i is query 32qtile + 16(i/8) + 8half + i%8
                 float pv[16], dsv[16];
@@ -188,32 +199,38 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
                     pv[i] = fast_exp2(s[i] * c_log2 - sv.x);
                     dsv[i] = pv[i] * (dp[i] - sv.y);
                 }
+                F pb[2], db[2], pl[SPLIT ? 2 : 1], dl[SPLIT ? 2 : 1];
                 if constexpr (SPLIT) {
-                    pack_frag_hilo(pb[qtile][0], pl[qtile][0], pv);
-                    pack_frag_hilo(pb[qtile][1], pl[qtile][1], pv + 8);
-                    pack_frag_hilo(db[qtile][0], dl[qtile][0], dsv);
-                    pack_frag_hilo(db[qtile][1], dl[qtile][1], dsv + 8);
+                    pack_frag_hilo(pb[0], pl[0], pv);
+                    pack_frag_hilo(pb[1], pl[SPLIT ? 1 : 0], pv + 8);
+                    pack_frag_hilo(db[0], dl[0], dsv);
+                    pack_frag_hilo(db[1], dl[SPLIT ? 1 : 0], dsv + 8);
                 } else {
-                    pack_frag(pb[qtile][0], pv);
-                    pack_frag(pb[qtile][1], pv + 8);
-                    pack_frag(db[qtile][0], dsv);
-                    pack_frag(db[qtile][1], dsv + 8);
+                    pack_frag(pb[0], pv);
+                    pack_frag(pb[1], pv + 8);
+                    pack_frag(db[0], dsv);
+                    pack_frag(db[1], dsv + 8);
+                }
+                // dV^T += dO^T P and dK^T += Q^T dS over this tile's 32 queries;
+                // dO^T and Q^T read transposed from the row-major tiles
+                F ta[2][2];
+                auto fetch_t = [&](F* f, int u) {
+                    const int kk = 2 * qtile + u / MT, mt = u % MT;
+                    lds_frag_tr<RB, true>(f[0], ot, mt * 32, kk * 16);
+                    lds_frag_tr<RB, true>(f[1], qt, mt * 32, kk * 16);
+                };
+                fetch_t(ta[0], 0);
+#pragma unroll
+                for (int u = 0; u < 2 * MT; ++u) {
+                    if (u + 1 < 2 * MT) fetch_t(ta[(u + 1) & 1], u + 1);
+                    lds_order();
+                    const int h = u / MT, mt = u % MT;
+                    mma(acc_v[mt], ta[u & 1][0], pb[h]);
+                    if constexpr (SPLIT) mma(acc_v[mt], ta[u & 1][0], pl[SPLIT ? h : 0]);
+                    mma(acc_k[mt], ta[u & 1][1], db[h]);
+                    if constexpr (SPLIT) mma(acc_k[mt], ta[u & 1][1], dl[SPLIT ? h : 0]);
                 }
             }
-            // dV^T += dO^T P and dK^T += Q^T dS over the 64 queries (4 k-steps);
-            // dO^T and Q^T read transposed from their row-major tiles
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    F a;
-                    lds_frag_tr<RB, true>(a, ot, mt * 32, kk * 16);
-                    mma(acc_v[mt], a, pb[kk >> 1][kk & 1]);
-                    if constexpr (SPLIT) mma(acc_v[mt], a, pl[(kk >> 1) & (SPLIT ? 1 : 0)][kk & 1]);
-                    lds_frag_tr<RB, true>(a, qt, mt * 32, kk * 16);
-                    mma(acc_k[mt], a, db[kk >> 1][kk & 1]);
-                    if constexpr (SPLIT) mma(acc_k[mt], a, dl[(kk >> 1) & (SPLIT ? 1 : 0)][kk & 1]);
-                }
         }
         wg_barrier();                   // buffer `buf` free for the step after next
         q_cur = q_next;

@@ -339,6 +339,13 @@ __device__ __forceinline__ void wg_barrier() {
     asm volatile("" ::: "memory");
 }
 
+// Scheduling fence: no instruction is moved across it by the compiler's
+// scheduler, so LDS reads written before it are issued before the MFMAs
+// after it (their waits stay at the first use).  Used to request operand
+// fragments one batch ahead of the products that consume them instead of
+// right before each one.
+__device__ __forceinline__ void lds_order() { __builtin_amdgcn_sched_barrier(0); }
+
 // Wave-uniform 32-bit load through the scalar cache.  Used for block-list
 // entries inside the pipelined loops: a vector load there would be counted by
 // vmcnt together with the asynchronous tile copies and make the compiler wait
