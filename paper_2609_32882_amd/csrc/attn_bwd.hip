@@ -345,17 +345,28 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
         F sl[SPLIT ? 2 : 1][2];
 #pragma unroll
         for (int t2 = 0; t2 < 2; ++t2) {
-            // S^T = K Q^T, dP^T = V dO^T: 32 keys x this lane's query
+            // S^T = K Q^T, dP^T = V dO^T: 32 keys x this lane's query; K and V
+            // fragments requested one k-step pair ahead of their products
+            const int row = t2 * 32 + (lane & 31);
             f32x16_t s, dp;
 #pragma unroll
             for (int i = 0; i < 16; ++i) { s[i] = 0.f; dp[i] = 0.f; }
+            F fa[2][4];
+            auto fetch = [&](F* f, int bi) {
+                lds_frag_s<RB>(f[0], k_lds, row, 32 * bi + half * 8);
+                lds_frag_s<RB>(f[1], v_lds, row, 32 * bi + half * 8);
+                lds_frag_s<RB>(f[2], k_lds, row, 32 * bi + 16 + half * 8);
+                lds_frag_s<RB>(f[3], v_lds, row, 32 * bi + 16 + half * 8);
+            };
+            fetch(fa[0], 0);
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                F a;
-                lds_frag_s<RB>(a, k_lds, t2 * 32 + (lane & 31), ks * 16 + half * 8);
-                mma(s, a, qf[ks]);
-                lds_frag_s<RB>(a, v_lds, t2 * 32 + (lane & 31), ks * 16 + half * 8);
-                mma(dp, a, of[ks]);
+            for (int bi = 0; bi < KS / 2; ++bi) {
+                if (bi + 1 < KS / 2) fetch(fa[(bi + 1) & 1], bi + 1);
+                lds_order();
+                mma(s, fa[bi & 1][0], qf[2 * bi]);
+                mma(dp, fa[bi & 1][1], of[2 * bi]);
+                mma(s, fa[bi & 1][2], qf[2 * bi + 1]);
+                mma(dp, fa[bi & 1][3], of[2 * bi + 1]);
             }
             float ds[16];
 #pragma unroll
@@ -374,16 +385,24 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
         wg_barrier();                   // V buffer free: stream the next one during dQ
         if (has_next) issue_v(c_next);
         if (c_cur >= 0) {
-            // dQ^T += K^T dS^T over the 64 keys (4 k-steps of 16); K^T read transposed
+            // dQ^T += K^T dS^T over the 64 keys (4 k-steps of 16); K^T read
+            // transposed, one k-step ahead of its products
+            F fa[2][MT];
+            auto fetch = [&](F* f, int kk) {
 #pragma unroll
-            for (int kk = 0; kk < 4; ++kk)
+                for (int mt = 0; mt < MT; ++mt) lds_frag_tr<RB, true>(f[mt], k_lds, mt * 32, kk * 16);
+            };
+            fetch(fa[0], 0);
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                if (kk + 1 < 4) fetch(fa[(kk + 1) & 1], kk + 1);
+                lds_order();
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
-                    F a;
-                    lds_frag_tr<RB, true>(a, k_lds, mt * 32, kk * 16);
-                    mma(dqa[mt], a, sb[kk >> 1][kk & 1]);
-                    if constexpr (SPLIT) mma(dqa[mt], a, sl[(kk >> 1) & (SPLIT ? 1 : 0)][kk & 1]);
+                    mma(dqa[mt], fa[kk & 1][mt], sb[kk >> 1][kk & 1]);
+                    if constexpr (SPLIT) mma(dqa[mt], fa[kk & 1][mt], sl[(kk >> 1) & (SPLIT ? 1 : 0)][kk & 1]);
                 }
+            }
         }
         wg_barrier();                   // K buffer free
         if (has_next) issue_k(c_next);

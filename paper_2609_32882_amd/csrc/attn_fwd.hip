@@ -98,17 +98,27 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
 
         vm_wait<VT::PER_WAVE>();          // this K tile has landed (V may still stream)
         wg_barrier();
-        // S^T for 64 keys x 32 queries (two 32-key tiles)
+        // S^T for 64 keys x 32 queries (two 32-key tiles); K fragments are
+        // requested one k-step pair ahead of their products
         f32x16_t s[2];
 #pragma unroll
-        for (int t2 = 0; t2 < 2; ++t2) {
+        for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
             for (int i = 0; i < 16; ++i) s[t2][i] = 0.f;
+        {
+            F fa[2][4];
+            auto fetch = [&](F* f, int bi) {
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                F a;
-                lds_frag_s<KRB>(a, k_lds, t2 * 32 + (lane & 31), ks * 16 + half * 8);
-                mma(s[t2], a, qf[ks]);
+                for (int x = 0; x < 4; ++x)
+                    lds_frag_s<KRB>(f[x], k_lds, (x & 1) * 32 + (lane & 31), (2 * bi + (x >> 1)) * 16 + half * 8);
+            };
+            fetch(fa[0], 0);
+#pragma unroll
+            for (int bi = 0; bi < KS / 2; ++bi) {
+                if (bi + 1 < KS / 2) fetch(fa[(bi + 1) & 1], bi + 1);
+                lds_order();
+#pragma unroll
+                for (int x = 0; x < 4; ++x) mma(s[x & 1], fa[bi & 1][x], qf[2 * bi + (x >> 1)]);
             }
         }
         wg_barrier();                      // K buffer free
@@ -145,20 +155,30 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
         if (has_next) vm_wait<KT::PER_WAVE>(); else vm_wait<0>();   // V tile landed
         wg_barrier();
         if (c_cur >= 0) {
-            // O^T += V^T P^T over 4 k-steps of 16 keys: keys 16kk + 8half + (0..7)
+            // O^T += V^T P^T over 4 k-steps of 16 keys: keys 16kk + 8half + (0..7);
+            // V^T fragments are requested one k-step ahead of their products
+            F pb[4], pl[SPLIT ? 4 : 1];
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk) {
-                F pb, pl;
                 float pv[8];
 #pragma unroll
                 for (int i = 0; i < 8; ++i) pv[i] = s[kk >> 1][(kk & 1) * 8 + i];
-                if constexpr (SPLIT) pack_frag_hilo(pb, pl, pv); else pack_frag(pb, pv);
+                if constexpr (SPLIT) pack_frag_hilo(pb[kk], pl[SPLIT ? kk : 0], pv); else pack_frag(pb[kk], pv);
+            }
+            F fa[2][MT];
+            auto fetch = [&](F* f, int kk) {
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) lds_frag_tr<KRB, true>(f[mt], v_lds, mt * 32, kk * 16);
+            };
+            fetch(fa[0], 0);
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                if (kk + 1 < 4) fetch(fa[(kk + 1) & 1], kk + 1);
+                lds_order();
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
-                    F a;
-                    lds_frag_tr<KRB, true>(a, v_lds, mt * 32, kk * 16);
-                    mma(oacc[mt], a, pb);
-                    if constexpr (SPLIT) mma(oacc[mt], a, pl);
+                    mma(oacc[mt], fa[kk & 1][mt], pb[kk]);
+                    if constexpr (SPLIT) mma(oacc[mt], fa[kk & 1][mt], pl[SPLIT ? kk : 0]);
                 }
             }
         }
