@@ -125,32 +125,36 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
         if (has_next) kt.issue(k_lds, kb + nxt_off, wave);
 
         if (c_cur >= 0) {
+            // Online softmax in log2 units with a lazily updated running max:
+            // the accumulators are rescaled only when the block max exceeds
+            // the running max m by more than 2^8 (any lane of the wave), so
+            // p = 2^(s c - m) <= 256.  O = sum p V / sum p is exact for any m.
             float mx = -INFINITY;
 #pragma unroll
             for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    s[t2][i] *= c_log2;
-                    mx = fmaxf(mx, s[t2][i]);
-                }
-            mx = fmaxf(mx, swap_half(mx));
-            const float mn = fmaxf(m, mx);
-            const float alpha = fast_exp2(m - mn);
+                for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[t2][i]);
+            mx = fmaxf(mx, swap_half(mx)) * c_log2;
+            if (__any(mx > m + 8.0f)) {
+                const float mn = fmaxf(m, mx);
+                const float alpha = fast_exp2(m - mn);
+                l *= alpha;
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) oacc[mt][i] *= alpha;
+                m = mn;
+            }
             float ps = 0.f;
 #pragma unroll
             for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
-                    const float p = fast_exp2(s[t2][i] - mn);
+                    const float p = fast_exp2(fmaf(s[t2][i], c_log2, -m));
                     s[t2][i] = p;
                     ps += p;
                 }
-            l = l * alpha + ps;
-            m = mn;
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) oacc[mt][i] *= alpha;
+            l += ps;
         }
         if (has_next) vm_wait<KT::PER_WAVE>(); else vm_wait<0>();   // V tile landed
         wg_barrier();
