@@ -38,9 +38,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="720p")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=32,
+    ap.add_argument("--cpu-rows", type=int, default=96,
                     help="query-block rows (forward + dQ) in the oracle's timed sample")
-    ap.add_argument("--cpu-kv", type=int, default=8,
+    ap.add_argument("--cpu-kv", type=int, default=24,
                     help="key blocks (dK/dV) in the oracle's timed sample")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, copy a buffer of this size once (reference kernel "
@@ -99,34 +99,42 @@ def main():
         if status != 0:
             raise RuntimeError("%s -> %s" % (name, vsa2.STATUS_NAMES.get(status, status)))
 
-    stages = ("pool", "route", "fwd", "bwd")
+    # the backward runs as its three C-ABI stages (exactly what vsa2_attn_bwd
+    # does) so that the dominant kernel, dK/dV, is timed on its own
+    stages = ("pool", "route", "fwd", "bwd_prep", "bwd_dkdv", "bwd_dq")
     ev = {s: [] for s in stages}
 
     def step(record):
-        e = [torch.cuda.Event(enable_timing=True) for _ in range(5)] if record else None
-        if record:
-            e[0].record(stream)
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)] if record else None
+
+        def mark(i):
+            if record:
+                e[i].record(stream)
+
+        mark(0)
         chk("pool", vsa2.vsa2_pool(P, p.heads_q, q.data_ptr(), p.Rt, p.Rh, p.Rw, q_r.data_ptr(), sp))
         chk("pool", vsa2.vsa2_pool(P, p.heads_kv, k.data_ptr(), p.Rt, p.Rh, p.Rw, k_r.data_ptr(), sp))
-        if record:
-            e[1].record(stream)
+        mark(1)
         chk("route", vsa2.vsa2_route(P, S, q_r.data_ptr(), k_r.data_ptr(), row_ptr.data_ptr(),
                                      col_idx.data_ptr(), cap, kv_ptr.data_ptr(), kv_idx.data_ptr(),
                                      None, rws_t.data_ptr(), rws, sp))
-        if record:
-            e[2].record(stream)
+        mark(2)
         chk("fwd", vsa2.vsa2_attn_fwd(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), row_ptr.data_ptr(),
                                       col_idx.data_ptr(), cap, o.data_ptr(), lse.data_ptr(), None, None, 0,
                                       sp))
+        mark(3)
+        chk("bwd_prep", vsa2.vsa2_attn_bwd_prep(P, o.data_ptr(), lse.data_ptr(), None, do.data_ptr(),
+                                                bws_t.data_ptr(), bws, sp))
+        mark(4)
+        chk("bwd_dkdv", vsa2.vsa2_attn_bwd_dkdv(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(),
+                                                kv_ptr.data_ptr(), kv_idx.data_ptr(), cap, 0, dk.data_ptr(),
+                                                dv.data_ptr(), bws_t.data_ptr(), bws, sp))
+        mark(5)
+        chk("bwd_dq", vsa2.vsa2_attn_bwd_dq(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(),
+                                            row_ptr.data_ptr(), col_idx.data_ptr(), cap, 0, dq.data_ptr(),
+                                            bws_t.data_ptr(), bws, sp))
+        mark(6)
         if record:
-            e[3].record(stream)
-        chk("bwd", vsa2.vsa2_attn_bwd(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
-                                      lse.data_ptr(), None, do.data_ptr(), row_ptr.data_ptr(),
-                                      col_idx.data_ptr(), kv_ptr.data_ptr(), kv_idx.data_ptr(), cap,
-                                      dq.data_ptr(), dk.data_ptr(), dv.data_ptr(), bws_t.data_ptr(),
-                                      bws, sp))
-        if record:
-            e[4].record(stream)
             for i, s in enumerate(stages):
                 ev[s].append((e[i], e[i + 1]))
 
@@ -150,12 +158,17 @@ def main():
         del src, dst
 
     nnz = int(row_ptr[-1].item())
-    flop_fwd = 4.0 * B * B * D * nnz
-    flop_bwd = 10.0 * B * B * D * nnz
+    b2d = float(B * B * D)
+    flop_fwd = 4.0 * b2d * nnz
+    flop_bwd = 10.0 * b2d * nnz
+    stage_ms["bwd"] = stage_ms["bwd_prep"] + stage_ms["bwd_dkdv"] + stage_ms["bwd_dq"]
     attn_ms = stage_ms["fwd"] + stage_ms["bwd"]
     value = (flop_fwd + flop_bwd) / (ms_step * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if p.dtype == 1 else PEAK_F32_TFLOPS
-    achieved_bwd = flop_bwd / (stage_ms["bwd"] * 1e-3) / 1e12
+    # dominant kernel: dK/dV.  Its algorithmic work per selected block pair is
+    # the four B x B x D products it has to form: S and dP (recomputed), dV, dK.
+    flop_dkdv = 8.0 * b2d * nnz
+    achieved = flop_dkdv / (stage_ms["bwd_dkdv"] * 1e-3) / 1e12
     out = {
         "metric": "effective sparse-attn TFLOP/s (fwd+bwd FLOPs over whole-path step time), 720p shape",
         "value": round(value, 3),
@@ -176,20 +189,56 @@ def main():
             "select": ("top-%d" % sel.k) if sel.mode == 0 else ("mass-%.2f-cap-%d" % (sel.mass, sel.cap)),
             "nnz_block_pairs": nnz, "sparsity": round(1.0 - nnz / float(p.batch * p.heads_q * N * N), 4),
         },
-        "breakdown_ms": {s: round(stage_ms[s], 4) for s in stages},
+        "breakdown_ms": {s: round(stage_ms[s], 4) for s in ("pool", "route", "fwd", "bwd") + stages[3:]},
         "attn_fwd_bwd_ms": round(attn_ms, 4),
         "attn_only_tflops": round((flop_fwd + flop_bwd) / (attn_ms * 1e-3) / 1e12, 3),
         "pct_bf16_peak_attn_only": round(100.0 * (flop_fwd + flop_bwd) / (attn_ms * 1e-3) / 1e12 / peak, 2),
         "roofline": {
-            "kernel": "vsa2_attn_bwd (delta_kernel + dkdv_kernel + dq_kernel)",
-            "bound": "mfma", "achieved": round(achieved_bwd, 3), "peak": peak, "unit": "TFLOP/s",
-            "frac": round(achieved_bwd / peak, 4), "traffic": None,
+            "kernel": "dkdv_kernel (vsa2_attn_bwd_dkdv)",
+            "bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4),
+            "traffic": dkdv_traffic(w.name),
         },
         "input_gen_s": round(gen_s, 1),
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, x, row_ptr, col_idx, args.cpu_rows, args.cpu_kv)
     print(json.dumps(out), flush=True)
+
+
+# HBM bytes per launch of the dK/dV kernel, from the hardware byte counters
+# (FETCH_SIZE, WRITE_SIZE) scaled by a plain-copy calibration; recorded in
+# the profile summary together with a hash of the kernel's sources and
+# reported only while those sources are unchanged.
+DKDV_SOURCES = ("paper_2609_32882_amd/csrc/attn_bwd.hip", "paper_2609_32882_amd/csrc/common.hpp",
+                "paper_2609_32882_amd/csrc/internal.hpp")
+
+
+def dkdv_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in DKDV_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def dkdv_traffic(workload):
+    path = os.path.join(ROOT, "profiles", "dkdv_kernel_%s_counters.md" % workload)
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and line.startswith("- `"):
+                key, val = line[3:].split("`", 1)
+                rec[key] = val.split(":", 1)[1].strip().strip("`")
+    if rec.get("source_sha256") != dkdv_source_hash():
+        return None
+    try:
+        return int(rec["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(w, x, row_ptr_t, col_idx_t, nrows_sample, nkv_sample):

@@ -212,6 +212,41 @@ vsa2_status vsa2_attn_bwd(const vsa2_problem* p, const void* q, const void* k, c
                           void* dq, void* dk, void* dv, void* ws, size_t ws_bytes,
                           hipStream_t stream);
 
+/*
+ * The backward in three stages, for callers that schedule or time them one
+ * by one.  vsa2_attn_bwd is exactly these three calls in this order on one
+ * stream; the stages communicate through ws (vsa2_attn_workspace(p, 1)
+ * bytes), which must not be reused in between.
+ *
+ * vsa2_attn_bwd_prep - per query token l: LSE_l and Delta_l = dO_l . O_l
+ *   (with o_lo given, O_l = o_l + o_lo_l), stored in ws.
+ *   o, lse, o_lo, dout  as for vsa2_attn_bwd.
+ */
+vsa2_status vsa2_attn_bwd_prep(const vsa2_problem* p, const void* o, const float* lse, const void* o_lo,
+                               const void* dout, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * vsa2_attn_bwd_dkdv - dK and dV of vsa2_attn_bwd, one key block at a time
+ *   over the query blocks of its transposed list (kv_ptr, kv_idx).
+ *   compensated  nonzero: dS and P enter the products as two bf16 terms (use
+ *                with a prep stage that was given o_lo).
+ *   ws           as written by vsa2_attn_bwd_prep.
+ *   dk, dv       [batch][Hkv][L][D] outputs, dtype p->dtype.
+ */
+vsa2_status vsa2_attn_bwd_dkdv(const vsa2_problem* p, const void* q, const void* k, const void* v,
+                               const void* dout, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
+                               int32_t compensated, void* dk, void* dv, const void* ws, size_t ws_bytes,
+                               hipStream_t stream);
+
+/*
+ * vsa2_attn_bwd_dq - dQ of vsa2_attn_bwd, one query block at a time over its
+ *   CSR row (row_ptr, col_idx).  compensated, ws as for vsa2_attn_bwd_dkdv.
+ *   dq  [batch][Hq][L][D] output, dtype p->dtype.
+ */
+vsa2_status vsa2_attn_bwd_dq(const vsa2_problem* p, const void* q, const void* k, const void* v,
+                             const void* dout, const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
+                             int32_t compensated, void* dq, const void* ws, size_t ws_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

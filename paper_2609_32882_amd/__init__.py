@@ -27,7 +27,8 @@ VSA2_SEL_TOPK, VSA2_SEL_MASS = 0, 1
 
 # Every symbol include/vsa2.h declares.
 EXPORTS = ("vsa2_status_str", "vsa2_pool", "vsa2_route_capacity", "vsa2_route_workspace",
-           "vsa2_route", "vsa2_attn_workspace", "vsa2_attn_fwd", "vsa2_attn_bwd")
+           "vsa2_route", "vsa2_attn_workspace", "vsa2_attn_fwd", "vsa2_attn_bwd",
+           "vsa2_attn_bwd_prep", "vsa2_attn_bwd_dkdv", "vsa2_attn_bwd_dq")
 
 
 class vsa2_problem(ctypes.Structure):
@@ -69,6 +70,9 @@ def _lib():
         L.vsa2_attn_workspace.argtypes = [pp, i32, ctypes.POINTER(sz)]
         L.vsa2_attn_fwd.argtypes = [pp, P, P, P, P, P, i64, P, P, P, P, sz, P]
         L.vsa2_attn_bwd.argtypes = [pp, P, P, P, P, P, P, P, P, P, P, P, i64, P, P, P, P, sz, P]
+        L.vsa2_attn_bwd_prep.argtypes = [pp, P, P, P, P, P, sz, P]
+        L.vsa2_attn_bwd_dkdv.argtypes = [pp, P, P, P, P, P, P, i64, i32, P, P, P, sz, P]
+        L.vsa2_attn_bwd_dq.argtypes = [pp, P, P, P, P, P, P, i64, i32, P, P, sz, P]
         for n in EXPORTS[1:]:
             getattr(L, n).restype = ctypes.c_int
         _L = L
@@ -134,6 +138,22 @@ def vsa2_attn_bwd(p, q, k, v, o, lse, o_lo, dout, row_ptr, col_idx, kv_ptr, kv_i
                   dk, dv, ws, ws_bytes, stream=0):
     return _lib().vsa2_attn_bwd(_ref(p), q, k, v, o, lse, o_lo, dout, row_ptr, col_idx, kv_ptr,
                                 kv_idx, col_cap, dq, dk, dv, ws, ws_bytes, stream)
+
+
+def vsa2_attn_bwd_prep(p, o, lse, o_lo, dout, ws, ws_bytes, stream=0):
+    return _lib().vsa2_attn_bwd_prep(_ref(p), o, lse, o_lo, dout, ws, ws_bytes, stream)
+
+
+def vsa2_attn_bwd_dkdv(p, q, k, v, dout, kv_ptr, kv_idx, col_cap, compensated, dk, dv, ws, ws_bytes,
+                       stream=0):
+    return _lib().vsa2_attn_bwd_dkdv(_ref(p), q, k, v, dout, kv_ptr, kv_idx, col_cap,
+                                     int(compensated), dk, dv, ws, ws_bytes, stream)
+
+
+def vsa2_attn_bwd_dq(p, q, k, v, dout, row_ptr, col_idx, col_cap, compensated, dq, ws, ws_bytes,
+                     stream=0):
+    return _lib().vsa2_attn_bwd_dq(_ref(p), q, k, v, dout, row_ptr, col_idx, col_cap,
+                                   int(compensated), dq, ws, ws_bytes, stream)
 
 
 # --------------------------------------------------------------------------
@@ -285,4 +305,40 @@ def attn_bwd(p, q, k, v, o, lse, do, row_ptr, col_idx, kv_ptr, kv_idx, col_cap=N
                                           col_idx.data_ptr(), kv_ptr.data_ptr(), kv_idx.data_ptr(),
                                           cap, dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
                                           ws.data_ptr(), wsb, _stream()))
+    return dq, dk, dv
+
+
+def attn_bwd_staged(p, q, k, v, o, lse, do, row_ptr, col_idx, kv_ptr, kv_idx, col_cap=None,
+                    dq=None, dk=None, dv=None, o_lo=None, marks=None):
+    """The backward as its three C-ABI stages (prep, dK/dV, dQ) on the current
+    stream; same results as attn_bwd.  `marks`, if given, is a list of four
+    torch.cuda.Event recorded before the first stage and after each one."""
+    torch = _torch()
+    p = problem_from(p)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(k) if dk is None else dk
+    dv = torch.empty_like(v) if dv is None else dv
+    cap = col_idx.numel() if col_cap is None else col_cap
+    st, wsb = vsa2_attn_workspace(p, 1)
+    _check("vsa2_attn_workspace", st)
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
+    comp = o_lo is not None
+    s = _stream()
+    if marks:
+        marks[0].record()
+    _check("vsa2_attn_bwd_prep", vsa2_attn_bwd_prep(p, o.data_ptr(), lse.data_ptr(), _ptr(o_lo),
+                                                    do.data_ptr(), ws.data_ptr(), wsb, s))
+    if marks:
+        marks[1].record()
+    _check("vsa2_attn_bwd_dkdv", vsa2_attn_bwd_dkdv(p, q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                                    do.data_ptr(), kv_ptr.data_ptr(),
+                                                    kv_idx.data_ptr(), cap, comp, dk.data_ptr(),
+                                                    dv.data_ptr(), ws.data_ptr(), wsb, s))
+    if marks:
+        marks[2].record()
+    _check("vsa2_attn_bwd_dq", vsa2_attn_bwd_dq(p, q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                                do.data_ptr(), row_ptr.data_ptr(), col_idx.data_ptr(),
+                                                cap, comp, dq.data_ptr(), ws.data_ptr(), wsb, s))
+    if marks:
+        marks[3].record()
     return dq, dk, dv

@@ -435,57 +435,101 @@ size_t bwd_workspace_bytes(int dtype, int D, int batch, int Hq, int Hkv, int N) 
     return (8 * static_cast<size_t>(batch) * Hq * L + 255) / 256 * 256;
 }
 
-template <typename T, int D, bool COMP>
-static hipError_t launch_bwd_t(const void* q, const void* k, const void* v, const void* o, const float* lse,
-                               const void* o_lo, const void* dout, const int32_t* row_ptr, const int32_t* col_idx,
-                               const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap, void* dq,
-                               void* dk, void* dv, void* ws, int batch, int Hq, int Hkv, int N,
-                               hipStream_t s) {
-    const int64_t L = static_cast<int64_t>(N) * 64;
-    const int64_t ntok = static_cast<int64_t>(batch) * Hq * L;
-    float2* stat = static_cast<float2*>(ws);
-    const float c = kLog2e / sqrtf(static_cast<float>(D));
-    const float scale = 1.0f / sqrtf(static_cast<float>(D));
-    const T* Q = static_cast<const T*>(q);
-    const T* K = static_cast<const T*>(k);
-    const T* V = static_cast<const T*>(v);
-    const T* dO = static_cast<const T*>(dout);
+// Stage 1: per query token (LSE * log2(e), Delta) into ws.
+template <typename T, int D>
+static hipError_t launch_prep_t(const void* o, const float* lse, const void* o_lo, const void* dout, void* ws,
+                                int batch, int Hq, int N, hipStream_t s) {
+    const int64_t ntok = static_cast<int64_t>(batch) * Hq * N * 64;
+    if (ntok == 0) return hipSuccess;
     const int64_t sthreads = ntok * (D / 8);
     hipLaunchKernelGGL((stat_kernel<T, D>), dim3(static_cast<unsigned>((sthreads + 255) / 256)), dim3(256), 0,
-                       s, static_cast<const T*>(o), static_cast<const T*>(o_lo), dO, lse, stat, ntok);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    const int64_t krows = static_cast<int64_t>(batch) * Hkv * N;
-    hipLaunchKernelGGL((dkdv_kernel<T, D, COMP>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s, Q, K, V,
-                       dO, stat, kv_ptr, kv_idx, col_cap, static_cast<T*>(dk), static_cast<T*>(dv), Hq, Hkv, N,
-                       c, scale, resident_per_xcd<dkdv_kernel<T, D, COMP>>(AB_NT));
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    const int64_t qrows = static_cast<int64_t>(batch) * Hq * N;
-    hipLaunchKernelGGL((dq_kernel<T, D, COMP>), dim3(static_cast<unsigned>(qrows)), dim3(AB_NT), 0, s, Q, K, V, dO,
-                       stat, row_ptr, col_idx, col_cap, static_cast<T*>(dq), Hq, Hkv, N, c, scale,
-                       resident_per_xcd<dq_kernel<T, D, COMP>>(AB_NT));
+                       s, static_cast<const T*>(o), static_cast<const T*>(o_lo), static_cast<const T*>(dout),
+                       lse, static_cast<float2*>(ws), ntok);
     return hipGetLastError();
 }
 
+// Stage 2: dK and dV (key-block stationary, transposed lists).
+template <typename T, int D, bool COMP>
+static hipError_t launch_dkdv_t(const void* q, const void* k, const void* v, const void* dout,
+                                const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap, void* dk,
+                                void* dv, const void* ws, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+    const int64_t krows = static_cast<int64_t>(batch) * Hkv * N;
+    if (krows == 0) return hipSuccess;
+    const float c = kLog2e / sqrtf(static_cast<float>(D));
+    const float scale = 1.0f / sqrtf(static_cast<float>(D));
+    hipLaunchKernelGGL((dkdv_kernel<T, D, COMP>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s,
+                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+                       static_cast<const T*>(dout), static_cast<const float2*>(ws), kv_ptr, kv_idx, col_cap,
+                       static_cast<T*>(dk), static_cast<T*>(dv), Hq, Hkv, N, c, scale,
+                       resident_per_xcd<dkdv_kernel<T, D, COMP>>(AB_NT));
+    return hipGetLastError();
+}
+
+// Stage 3: dQ (query-block stationary, CSR rows).
+template <typename T, int D, bool COMP>
+static hipError_t launch_dq_t(const void* q, const void* k, const void* v, const void* dout,
+                              const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* dq,
+                              const void* ws, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+    const int64_t qrows = static_cast<int64_t>(batch) * Hq * N;
+    if (qrows == 0) return hipSuccess;
+    const float c = kLog2e / sqrtf(static_cast<float>(D));
+    const float scale = 1.0f / sqrtf(static_cast<float>(D));
+    hipLaunchKernelGGL((dq_kernel<T, D, COMP>), dim3(static_cast<unsigned>(qrows)), dim3(AB_NT), 0, s,
+                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+                       static_cast<const T*>(dout), static_cast<const float2*>(ws), row_ptr, col_idx, col_cap,
+                       static_cast<T*>(dq), Hq, Hkv, N, c, scale, resident_per_xcd<dq_kernel<T, D, COMP>>(AB_NT));
+    return hipGetLastError();
+}
+
+#define VSA2_DISPATCH_TD(...)                               \
+    if (dtype == 1) {                                       \
+        if (D == 64) { using T = bf16_t; constexpr int DD = 64; __VA_ARGS__; }   \
+        if (D == 128) { using T = bf16_t; constexpr int DD = 128; __VA_ARGS__; } \
+    } else {                                                \
+        if (D == 64) { using T = float; constexpr int DD = 64; __VA_ARGS__; }    \
+        if (D == 128) { using T = float; constexpr int DD = 128; __VA_ARGS__; }  \
+    }                                                       \
+    return hipErrorInvalidValue
+
+hipError_t launch_attn_bwd_prep(int dtype, int D, const void* o, const float* lse, const void* o_lo,
+                                const void* dout, void* ws, int batch, int Hq, int N, hipStream_t s) {
+    VSA2_DISPATCH_TD(return (launch_prep_t<T, DD>(o, lse, o_lo, dout, ws, batch, Hq, N, s)));
+}
+
+hipError_t launch_attn_bwd_dkdv(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
+                                const void* dout, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
+                                void* dk, void* dv, const void* ws, int batch, int Hq, int Hkv, int N,
+                                hipStream_t s) {
+    VSA2_DISPATCH_TD(return comp ? launch_dkdv_t<T, DD, true>(q, k, v, dout, kv_ptr, kv_idx, col_cap, dk, dv, ws,
+                                                              batch, Hq, Hkv, N, s)
+                                 : launch_dkdv_t<T, DD, false>(q, k, v, dout, kv_ptr, kv_idx, col_cap, dk, dv, ws,
+                                                               batch, Hq, Hkv, N, s));
+}
+
+hipError_t launch_attn_bwd_dq(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
+                              const void* dout, const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
+                              void* dq, const void* ws, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+    VSA2_DISPATCH_TD(return comp ? launch_dq_t<T, DD, true>(q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws,
+                                                            batch, Hq, Hkv, N, s)
+                                 : launch_dq_t<T, DD, false>(q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws,
+                                                             batch, Hq, Hkv, N, s));
+}
+#undef VSA2_DISPATCH_TD
+
+// The whole backward: prep, dK/dV, dQ on one stream (compensated when o_lo).
 hipError_t launch_attn_bwd(int dtype, int D, const void* q, const void* k, const void* v, const void* o,
                            const float* lse, const void* o_lo, const void* dout, const int32_t* row_ptr,
                            const int32_t* col_idx, const int32_t* kv_ptr, const int32_t* kv_idx,
                            int64_t col_cap, void* dq, void* dk, void* dv, void* ws, int batch,
                            int Hq, int Hkv, int N, hipStream_t s) {
-#define VSA2_BWD(T, DD)                                                                                    \
-    return o_lo ? launch_bwd_t<T, DD, true>(q, k, v, o, lse, o_lo, dout, row_ptr, col_idx, kv_ptr, kv_idx,   \
-                                            col_cap, dq, dk, dv, ws, batch, Hq, Hkv, N, s)                   \
-                : launch_bwd_t<T, DD, false>(q, k, v, o, lse, o_lo, dout, row_ptr, col_idx, kv_ptr, kv_idx,  \
-                                             col_cap, dq, dk, dv, ws, batch, Hq, Hkv, N, s)
-    if (dtype == 1) {
-        if (D == 64) VSA2_BWD(bf16_t, 64);
-        if (D == 128) VSA2_BWD(bf16_t, 128);
-    } else {
-        if (D == 64) VSA2_BWD(float, 64);
-        if (D == 128) VSA2_BWD(float, 128);
-    }
-#undef VSA2_BWD
-    return hipErrorInvalidValue;
+    hipError_t e = launch_attn_bwd_prep(dtype, D, o, lse, o_lo, dout, ws, batch, Hq, N, s);
+    if (e != hipSuccess) return e;
+    const bool comp = o_lo != nullptr;
+    e = launch_attn_bwd_dkdv(dtype, D, comp, q, k, v, dout, kv_ptr, kv_idx, col_cap, dk, dv, ws, batch, Hq, Hkv,
+                             N, s);
+    if (e != hipSuccess) return e;
+    return launch_attn_bwd_dq(dtype, D, comp, q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws, batch, Hq, Hkv,
+                              N, s);
 }
 
 }  // namespace vsa2

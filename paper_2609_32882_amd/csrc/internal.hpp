@@ -54,5 +54,14 @@ hipError_t launch_attn_bwd(int dtype, int D, const void* q, const void* k, const
                            const int32_t* col_idx, const int32_t* kv_ptr, const int32_t* kv_idx,
                            int64_t col_cap, void* dq, void* dk, void* dv, void* ws, int batch,
                            int Hq, int Hkv, int N, hipStream_t s);
+hipError_t launch_attn_bwd_prep(int dtype, int D, const void* o, const float* lse, const void* o_lo,
+                                const void* dout, void* ws, int batch, int Hq, int N, hipStream_t s);
+hipError_t launch_attn_bwd_dkdv(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
+                                const void* dout, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
+                                void* dk, void* dv, const void* ws, int batch, int Hq, int Hkv, int N,
+                                hipStream_t s);
+hipError_t launch_attn_bwd_dq(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
+                              const void* dout, const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
+                              void* dq, const void* ws, int batch, int Hq, int Hkv, int N, hipStream_t s);
 
 }  // namespace vsa2

@@ -92,6 +92,32 @@ def test_null_and_alignment_checks():
     assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_WORKSPACE"
 
 
+def test_staged_backward_argument_checks():
+    """The three backward stages validate like vsa2_attn_bwd, before any
+    device work (fake pointers are never dereferenced)."""
+    p = good()
+    names = vsa2.STATUS_NAMES
+    big = 1 << 40
+    assert names[vsa2.vsa2_attn_bwd_prep(p, FAKE, FAKE, None, FAKE, None, 0, None)] == "VSA2_ERR_WORKSPACE"
+    assert names[vsa2.vsa2_attn_bwd_prep(p, None, FAKE, None, FAKE, FAKE, big, None)] == "VSA2_ERR_NULL"
+    assert names[vsa2.vsa2_attn_bwd_prep(p, FAKE, FAKE, MISALIGNED, FAKE, FAKE, big, None)] == "VSA2_ERR_ALIGN"
+    assert names[vsa2.vsa2_attn_bwd_prep(None, FAKE, FAKE, None, FAKE, FAKE, big, None)] == "VSA2_ERR_NULL"
+    assert names[vsa2.vsa2_attn_bwd_dkdv(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 0, FAKE, None, FAKE, big,
+                                         None)] == "VSA2_ERR_NULL"
+    assert names[vsa2.vsa2_attn_bwd_dkdv(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, -1, 0, FAKE, FAKE, FAKE, big,
+                                         None)] == "VSA2_ERR_CAPACITY"
+    assert names[vsa2.vsa2_attn_bwd_dkdv(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, FAKE, MISALIGNED, FAKE,
+                                         big, None)] == "VSA2_ERR_ALIGN"
+    assert names[vsa2.vsa2_attn_bwd_dkdv(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 0, FAKE, FAKE, FAKE, 0,
+                                         None)] == "VSA2_ERR_WORKSPACE"
+    assert names[vsa2.vsa2_attn_bwd_dq(p, FAKE, FAKE, FAKE, FAKE, FAKE, None, 1, 0, FAKE, FAKE, big,
+                                       None)] == "VSA2_ERR_NULL"
+    assert names[vsa2.vsa2_attn_bwd_dq(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 0, MISALIGNED, FAKE, big,
+                                       None)] == "VSA2_ERR_ALIGN"
+    assert names[vsa2.vsa2_attn_bwd_dq(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 0, FAKE, None, 0,
+                                       None)] == "VSA2_ERR_WORKSPACE"
+
+
 def test_route_capacity_workspace_and_select_checks():
     p = good()
     N = (8 // 4) * (16 // 4) * (16 // 4)

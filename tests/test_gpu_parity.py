@@ -189,6 +189,24 @@ def test_bwd_matches_oracle(case, compensated):
                       max_abs=float("inf") if loose else 2e-2)
 
 
+@pytest.mark.parametrize("compensated", [False, True], ids=["plain", "compensated"])
+def test_bwd_staged_matches_whole_call(case, compensated):
+    """prep + dK/dV + dQ as separate C-ABI calls give the same bits as
+    vsa2_attn_bwd."""
+    w, x, ref, dev, t, o, lse, o_lo = _bwd_inputs(case, compensated)
+    p = w.problem
+    args = (p, dev["q"], dev["k"], dev["v"], o, lse, dev["do"], t["row_ptr"], t["col_idx"],
+            t["kv_ptr"], t["kv_idx"])
+    a = vsa2.attn_bwd(*args, o_lo=o_lo)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    b = vsa2.attn_bwd_staged(*args, o_lo=o_lo, marks=marks)
+    torch.cuda.synchronize()
+    for x1, x2 in zip(a, b):
+        iv = torch.int16 if x1.dtype == torch.bfloat16 else torch.int32
+        assert torch.equal(x1.view(iv), x2.view(iv))
+    assert all(marks[i].elapsed_time(marks[i + 1]) >= 0 for i in range(3))
+
+
 def test_compensated_forward_remainder(case):
     """o + o_lo reproduces the fp32 accumulator: it matches the oracle's O
     to ~2^-16 relative (bf16 inputs) and o itself is unchanged."""
