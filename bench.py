@@ -78,6 +78,8 @@ def main():
     assert st == 0
     st, rws = vsa2.vsa2_route_workspace(P, S)
     assert st == 0
+    st, fws = vsa2.vsa2_attn_workspace(P, 0)
+    assert st == 0
     st, bws = vsa2.vsa2_attn_workspace(P, 1)
     assert st == 0
     i32 = torch.int32
@@ -88,6 +90,7 @@ def main():
     kv_ptr = torch.empty(p.batch * p.heads_kv * N + 1, dtype=i32, device=dev)
     kv_idx = torch.empty(cap, dtype=i32, device=dev)
     rws_t = torch.empty(rws, dtype=torch.uint8, device=dev)
+    fws_t = torch.empty(max(fws, 1), dtype=torch.uint8, device=dev)
     bws_t = torch.empty(max(bws, 1), dtype=torch.uint8, device=dev)
     o = torch.empty_like(q)
     lse = torch.empty((p.batch, p.heads_q, L), dtype=torch.float32, device=dev)
@@ -120,8 +123,8 @@ def main():
                                      None, rws_t.data_ptr(), rws, sp))
         mark(2)
         chk("fwd", vsa2.vsa2_attn_fwd(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), row_ptr.data_ptr(),
-                                      col_idx.data_ptr(), cap, o.data_ptr(), lse.data_ptr(), None, None, 0,
-                                      sp))
+                                      col_idx.data_ptr(), cap, o.data_ptr(), lse.data_ptr(), None,
+                                      fws_t.data_ptr(), fws, sp))
         mark(3)
         chk("bwd_prep", vsa2.vsa2_attn_bwd_prep(P, o.data_ptr(), lse.data_ptr(), None, do.data_ptr(),
                                                 bws_t.data_ptr(), bws, sp))

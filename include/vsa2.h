@@ -156,8 +156,12 @@ vsa2_status vsa2_route(const vsa2_problem* p, const vsa2_select* s,
                        int32_t* kv_ptr, int32_t* kv_idx,
                        float* block_scores, void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Bytes of workspace vsa2_attn_fwd (pass 0: none) or vsa2_attn_bwd (pass 1:
- * one fp32 (LSE, Delta) pair per query token) needs. */
+/* Bytes of workspace vsa2_attn_fwd (pass 0: the work order, one int32 per
+ * CSR row) or vsa2_attn_bwd (pass 1: one fp32 (LSE, Delta) pair per query
+ * token, then the work orders of the CSR and CSC rows) needs.  The work
+ * order lists the rows of each XCD's range longest first (a stable
+ * counting sort by length class), so the launch's last workgroups are
+ * short ones; rows of equal length keep their order. */
 vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* bytes);
 
 /*
@@ -178,8 +182,8 @@ vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* byt
  *       and o_lo receives the rounding remainder of O (o + o_lo ~ the fp32
  *       accumulator).  Pass it to vsa2_attn_bwd to get gradients whose error
  *       does not grow with the magnitude of the keys' common component.
- *   ws, ws_bytes  workspace of vsa2_attn_workspace(p, 0) bytes (zero: ws may
- *       be NULL).
+ *   ws, ws_bytes  workspace of vsa2_attn_workspace(p, 0) bytes, 256-byte
+ *       aligned.
  * Errors: NULL pointers, shape/dtype, misalignment, small workspace.
  */
 vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, const void* v,
@@ -230,12 +234,13 @@ vsa2_status vsa2_attn_bwd_prep(const vsa2_problem* p, const void* o, const float
  *   over the query blocks of its transposed list (kv_ptr, kv_idx).
  *   compensated  nonzero: dS and P enter the products as two bf16 terms (use
  *                with a prep stage that was given o_lo).
- *   ws           as written by vsa2_attn_bwd_prep.
+ *   ws           as written by vsa2_attn_bwd_prep (this stage also writes
+ *                its work order there).
  *   dk, dv       [batch][Hkv][L][D] outputs, dtype p->dtype.
  */
 vsa2_status vsa2_attn_bwd_dkdv(const vsa2_problem* p, const void* q, const void* k, const void* v,
                                const void* dout, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
-                               int32_t compensated, void* dk, void* dv, const void* ws, size_t ws_bytes,
+                               int32_t compensated, void* dk, void* dv, void* ws, size_t ws_bytes,
                                hipStream_t stream);
 
 /*
@@ -245,7 +250,7 @@ vsa2_status vsa2_attn_bwd_dkdv(const vsa2_problem* p, const void* q, const void*
  */
 vsa2_status vsa2_attn_bwd_dq(const vsa2_problem* p, const void* q, const void* k, const void* v,
                              const void* dout, const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
-                             int32_t compensated, void* dq, const void* ws, size_t ws_bytes, hipStream_t stream);
+                             int32_t compensated, void* dq, void* ws, size_t ws_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -82,7 +82,9 @@ route_ws route_layout(const vsa2_problem* p, const shape& s) {
 }
 
 // the forward needs no scratch memory
-size_t fwd_ws_bytes(const shape&, const vsa2_problem*) { return 0; }
+size_t fwd_ws_bytes(const shape& s, const vsa2_problem* p) {
+    return vsa2::fwd_workspace_bytes(p->batch, p->heads_q, static_cast<int>(s.N));
+}
 
 size_t bwd_ws_bytes(const shape& s, const vsa2_problem* p) {
     return vsa2::bwd_workspace_bytes(p->dtype, p->head_dim, p->batch, p->heads_q, p->heads_kv,
@@ -218,10 +220,11 @@ vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, c
     if (col_cap < 0) return VSA2_ERR_CAPACITY;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(o_lo))
         return VSA2_ERR_ALIGN;
-    if (ws_bytes < fwd_ws_bytes(s, p)) return VSA2_ERR_WORKSPACE;
-    (void)ws;
+    if (!ws || ws_bytes < fwd_ws_bytes(s, p)) return VSA2_ERR_WORKSPACE;
+    if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_attn_fwd(p->dtype, p->head_dim, q, k, v, row_ptr, col_idx, col_cap, o, lse,
-                                       o_lo, p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N), stream));
+                                       o_lo, ws, p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N),
+                                       stream));
     return VSA2_OK;
 }
 
@@ -268,7 +271,7 @@ vsa2_status vsa2_attn_bwd_prep(const vsa2_problem* p, const void* o, const float
 
 vsa2_status vsa2_attn_bwd_dkdv(const vsa2_problem* p, const void* q, const void* k, const void* v,
                                const void* dout, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
-                               int32_t compensated, void* dk, void* dv, const void* ws, size_t ws_bytes,
+                               int32_t compensated, void* dk, void* dv, void* ws, size_t ws_bytes,
                                hipStream_t stream) {
     shape s;
     vsa2_status st = check_problem(p, &s);
@@ -290,7 +293,7 @@ vsa2_status vsa2_attn_bwd_dkdv(const vsa2_problem* p, const void* q, const void*
 
 vsa2_status vsa2_attn_bwd_dq(const vsa2_problem* p, const void* q, const void* k, const void* v,
                              const void* dout, const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
-                             int32_t compensated, void* dq, const void* ws, size_t ws_bytes, hipStream_t stream) {
+                             int32_t compensated, void* dq, void* ws, size_t ws_bytes, hipStream_t stream) {
     shape s;
     vsa2_status st = check_problem(p, &s);
     if (st != VSA2_OK) return st;

@@ -73,7 +73,8 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float2* __restrict__ stat,
     const int32_t* __restrict__ kv_ptr, const int32_t* __restrict__ kv_idx, int64_t col_cap,
-    T* __restrict__ dk, T* __restrict__ dv, int Hq, int Hkv, int N, float c_log2, float scale, int period) {
+    T* __restrict__ dk, T* __restrict__ dv, int Hq, int Hkv, int N, float c_log2, float scale, int period,
+    const int32_t* __restrict__ order) {
     using F = typename frag_of<T>::type;
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;
@@ -86,7 +87,7 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
     __shared__ __align__(1024) float2 st_lds[2][64];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = wave_id(), half = lane >> 5;
-    const int64_t krow = xcd_item(blockIdx.x, gridDim.x);   // (b*Hkv + hkv)*N + nk
+    const int64_t krow = work_row(order, xcd_item(blockIdx.x, gridDim.x), gridDim.x);   // (b*Hkv + hkv)*N + nk
     const int64_t bkv = krow / N;
     const int nk = static_cast<int>(krow % N);
     const int b = static_cast<int>(bkv / Hkv), hkv = static_cast<int>(bkv % Hkv);
@@ -271,7 +272,8 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float2* __restrict__ stat,
     const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx, int64_t col_cap,
-    T* __restrict__ dq, int Hq, int Hkv, int N, float c_log2, float scale, int period) {
+    T* __restrict__ dq, int Hq, int Hkv, int N, float c_log2, float scale, int period,
+    const int32_t* __restrict__ order) {
     using F = typename frag_of<T>::type;
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;
@@ -283,7 +285,7 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     __shared__ __align__(1024) char v_lds[RT::BYTES];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = wave_id(), half = lane >> 5;
-    const int64_t row = xcd_item(blockIdx.x, gridDim.x);
+    const int64_t row = work_row(order, xcd_item(blockIdx.x, gridDim.x), gridDim.x);
     const int64_t bh = row / N;
     const int n = static_cast<int>(row % N);
     const int b = static_cast<int>(bh / Hq), h = static_cast<int>(bh % Hq);
@@ -426,13 +428,26 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
         }
 }
 
-// Workspace of the backward call: per query token (LSE * log2(e), Delta).
+// Workspace of the backward call: per query token (LSE * log2(e), Delta),
+// then the work orders of the CSR rows (dQ) and of the CSC rows (dK/dV).
+static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+size_t fwd_workspace_bytes(int batch, int Hq, int N) {
+    return align256(4 * static_cast<size_t>(batch) * Hq * N);
+}
+
+size_t bwd_ws_csr_order_offset(int batch, int Hq, int N) {
+    return align256(8 * static_cast<size_t>(batch) * Hq * N * 64);
+}
+
+size_t bwd_ws_csc_order_offset(int batch, int Hq, int N) {
+    return bwd_ws_csr_order_offset(batch, Hq, N) + align256(4 * static_cast<size_t>(batch) * Hq * N);
+}
+
 size_t bwd_workspace_bytes(int dtype, int D, int batch, int Hq, int Hkv, int N) {
     (void)dtype;
     (void)D;
-    (void)Hkv;
-    const size_t L = static_cast<size_t>(N) * 64;
-    return (8 * static_cast<size_t>(batch) * Hq * L + 255) / 256 * 256;
+    return bwd_ws_csc_order_offset(batch, Hq, N) + align256(4 * static_cast<size_t>(batch) * Hkv * N);
 }
 
 // Stage 1: per query token (LSE * log2(e), Delta) into ws.
@@ -452,16 +467,19 @@ static hipError_t launch_prep_t(const void* o, const float* lse, const void* o_l
 template <typename T, int D, bool COMP>
 static hipError_t launch_dkdv_t(const void* q, const void* k, const void* v, const void* dout,
                                 const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap, void* dk,
-                                void* dv, const void* ws, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                                void* dv, void* ws, int batch, int Hq, int Hkv, int N, hipStream_t s) {
     const int64_t krows = static_cast<int64_t>(batch) * Hkv * N;
     if (krows == 0) return hipSuccess;
+    int32_t* order = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + bwd_ws_csc_order_offset(batch, Hq, N));
+    hipError_t e = launch_lpt_order(kv_ptr, krows, col_cap, order, s);
+    if (e != hipSuccess) return e;
     const float c = kLog2e / sqrtf(static_cast<float>(D));
     const float scale = 1.0f / sqrtf(static_cast<float>(D));
     hipLaunchKernelGGL((dkdv_kernel<T, D, COMP>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s,
                        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
                        static_cast<const T*>(dout), static_cast<const float2*>(ws), kv_ptr, kv_idx, col_cap,
                        static_cast<T*>(dk), static_cast<T*>(dv), Hq, Hkv, N, c, scale,
-                       resident_per_xcd<dkdv_kernel<T, D, COMP>>(AB_NT));
+                       resident_per_xcd<dkdv_kernel<T, D, COMP>>(AB_NT), order);
     return hipGetLastError();
 }
 
@@ -469,15 +487,19 @@ static hipError_t launch_dkdv_t(const void* q, const void* k, const void* v, con
 template <typename T, int D, bool COMP>
 static hipError_t launch_dq_t(const void* q, const void* k, const void* v, const void* dout,
                               const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* dq,
-                              const void* ws, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                              void* ws, int batch, int Hq, int Hkv, int N, hipStream_t s) {
     const int64_t qrows = static_cast<int64_t>(batch) * Hq * N;
     if (qrows == 0) return hipSuccess;
+    int32_t* order = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + bwd_ws_csr_order_offset(batch, Hq, N));
+    hipError_t e = launch_lpt_order(row_ptr, qrows, col_cap, order, s);
+    if (e != hipSuccess) return e;
     const float c = kLog2e / sqrtf(static_cast<float>(D));
     const float scale = 1.0f / sqrtf(static_cast<float>(D));
     hipLaunchKernelGGL((dq_kernel<T, D, COMP>), dim3(static_cast<unsigned>(qrows)), dim3(AB_NT), 0, s,
                        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
                        static_cast<const T*>(dout), static_cast<const float2*>(ws), row_ptr, col_idx, col_cap,
-                       static_cast<T*>(dq), Hq, Hkv, N, c, scale, resident_per_xcd<dq_kernel<T, D, COMP>>(AB_NT));
+                       static_cast<T*>(dq), Hq, Hkv, N, c, scale, resident_per_xcd<dq_kernel<T, D, COMP>>(AB_NT),
+                       order);
     return hipGetLastError();
 }
 
@@ -498,7 +520,7 @@ hipError_t launch_attn_bwd_prep(int dtype, int D, const void* o, const float* ls
 
 hipError_t launch_attn_bwd_dkdv(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
                                 const void* dout, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
-                                void* dk, void* dv, const void* ws, int batch, int Hq, int Hkv, int N,
+                                void* dk, void* dv, void* ws, int batch, int Hq, int Hkv, int N,
                                 hipStream_t s) {
     VSA2_DISPATCH_TD(return comp ? launch_dkdv_t<T, DD, true>(q, k, v, dout, kv_ptr, kv_idx, col_cap, dk, dv, ws,
                                                               batch, Hq, Hkv, N, s)
@@ -508,7 +530,7 @@ hipError_t launch_attn_bwd_dkdv(int dtype, int D, bool comp, const void* q, cons
 
 hipError_t launch_attn_bwd_dq(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
                               const void* dout, const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
-                              void* dq, const void* ws, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                              void* dq, void* ws, int batch, int Hq, int Hkv, int N, hipStream_t s) {
     VSA2_DISPATCH_TD(return comp ? launch_dq_t<T, DD, true>(q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws,
                                                             batch, Hq, Hkv, N, s)
                                  : launch_dq_t<T, DD, false>(q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws,

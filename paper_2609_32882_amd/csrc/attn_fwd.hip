@@ -30,7 +30,7 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx, int64_t col_cap,
     T* __restrict__ o, float* __restrict__ lse, T* __restrict__ o_lo, int Hq, int Hkv, int N, float c_log2,
-    int period) {
+    int period, const int32_t* __restrict__ order) {
     using F = typename frag_of<T>::type;
     constexpr bool SPLIT = COMP && sizeof(T) == 2;
     constexpr int E = sizeof(T);
@@ -43,7 +43,7 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     __shared__ __align__(1024) char v_lds[VT::BYTES];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = wave_id(), half = lane >> 5;
-    const int64_t row = xcd_item(blockIdx.x, gridDim.x);
+    const int64_t row = work_row(order, xcd_item(blockIdx.x, gridDim.x), gridDim.x);
     const int64_t bh = row / N;
     const int n = static_cast<int>(row % N);
     const int b = static_cast<int>(bh / Hq), h = static_cast<int>(bh % Hq);
@@ -225,32 +225,36 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
 template <typename T, int D>
 static hipError_t launch_fwd_t(const void* q, const void* k, const void* v, const int32_t* row_ptr,
                                const int32_t* col_idx, int64_t col_cap, void* o, float* lse, void* o_lo,
-                               int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                               int32_t* order, int batch, int Hq, int Hkv, int N, hipStream_t s) {
     const int64_t rows = static_cast<int64_t>(batch) * Hq * N;
     if (rows == 0) return hipSuccess;
+    hipError_t e = launch_lpt_order(row_ptr, rows, col_cap, order, s);
+    if (e != hipSuccess) return e;
     const float c = 1.4426950408889634f / sqrtf(static_cast<float>(D));
     if (o_lo)
         hipLaunchKernelGGL((attn_fwd_kernel<T, D, true>), dim3(static_cast<unsigned>(rows)), dim3(AF_NT), 0, s,
                            static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
                            row_ptr, col_idx, col_cap, static_cast<T*>(o), lse, static_cast<T*>(o_lo), Hq, Hkv,
-                           N, c, resident_per_xcd<attn_fwd_kernel<T, D, true>>(AF_NT));
+                           N, c, resident_per_xcd<attn_fwd_kernel<T, D, true>>(AF_NT), order);
     else
         hipLaunchKernelGGL((attn_fwd_kernel<T, D, false>), dim3(static_cast<unsigned>(rows)), dim3(AF_NT), 0, s,
                            static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
                            row_ptr, col_idx, col_cap, static_cast<T*>(o), lse, nullptr, Hq, Hkv, N, c,
-                           resident_per_xcd<attn_fwd_kernel<T, D, false>>(AF_NT));
+                           resident_per_xcd<attn_fwd_kernel<T, D, false>>(AF_NT), order);
     return hipGetLastError();
 }
 
 hipError_t launch_attn_fwd(int dtype, int D, const void* q, const void* k, const void* v,
                            const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
-                           float* lse, void* o_lo, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                           float* lse, void* o_lo, void* ws, int batch, int Hq, int Hkv, int N,
+                           hipStream_t s) {
+    int32_t* order = static_cast<int32_t*>(ws);
     if (dtype == 1) {
-        if (D == 64) return launch_fwd_t<bf16_t, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, batch, Hq, Hkv, N, s);
-        if (D == 128) return launch_fwd_t<bf16_t, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, batch, Hq, Hkv, N, s);
+        if (D == 64) return launch_fwd_t<bf16_t, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, batch, Hq, Hkv, N, s);
+        if (D == 128) return launch_fwd_t<bf16_t, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, batch, Hq, Hkv, N, s);
     } else {
-        if (D == 64) return launch_fwd_t<float, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, batch, Hq, Hkv, N, s);
-        if (D == 128) return launch_fwd_t<float, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, batch, Hq, Hkv, N, s);
+        if (D == 64) return launch_fwd_t<float, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, batch, Hq, Hkv, N, s);
+        if (D == 128) return launch_fwd_t<float, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, batch, Hq, Hkv, N, s);
     }
     return hipErrorInvalidValue;
 }

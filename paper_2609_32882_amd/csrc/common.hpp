@@ -177,6 +177,15 @@ __device__ __forceinline__ int64_t xcd_item(int64_t bid, int64_t n) {
     return x * q + (x < r ? x : r) + i;
 }
 
+// Row processed by work item `item` of a launch of n items: order[item]
+// (the longest-first order of the item's XCD range), or the item itself
+// without an order (or for an out-of-range entry).
+__device__ __forceinline__ int64_t work_row(const int32_t* order, int64_t item, int64_t n) {
+    if (!order) return item;
+    const int64_t r = order[item];
+    return (r >= 0 && r < n) ? r : item;
+}
+
 // Index of the calling wave inside its workgroup, as a wave-uniform (scalar) value.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 

@@ -47,8 +47,17 @@ hipError_t launch_csc(const int32_t* row_ptr, const int32_t* col_idx, int batch,
                       int32_t* kv_idx, hipStream_t s);
 hipError_t launch_attn_fwd(int dtype, int D, const void* q, const void* k, const void* v,
                            const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
-                           float* lse, void* o_lo, int batch, int Hq, int Hkv, int N, hipStream_t s);
+                           float* lse, void* o_lo, void* ws, int batch, int Hq, int Hkv, int N,
+                           hipStream_t s);
+// Forward workspace: the work order of the CSR rows (int32 per row).
+size_t fwd_workspace_bytes(int batch, int Hq, int N);
+// Backward workspace: (LSE*log2 e, Delta) per query token, then the work
+// orders of the CSR rows (dQ) and of the CSC rows (dK/dV).
 size_t bwd_workspace_bytes(int dtype, int D, int batch, int Hq, int Hkv, int N);
+size_t bwd_ws_csr_order_offset(int batch, int Hq, int N);
+size_t bwd_ws_csc_order_offset(int batch, int Hq, int N);
+// Longest-first work order of the rows of ptr within each XCD range.
+hipError_t launch_lpt_order(const int32_t* ptr, int64_t nrows, int64_t cap, int32_t* order, hipStream_t s);
 hipError_t launch_attn_bwd(int dtype, int D, const void* q, const void* k, const void* v, const void* o,
                            const float* lse, const void* o_lo, const void* dout, const int32_t* row_ptr,
                            const int32_t* col_idx, const int32_t* kv_ptr, const int32_t* kv_idx,
@@ -58,10 +67,10 @@ hipError_t launch_attn_bwd_prep(int dtype, int D, const void* o, const float* ls
                                 const void* dout, void* ws, int batch, int Hq, int N, hipStream_t s);
 hipError_t launch_attn_bwd_dkdv(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
                                 const void* dout, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
-                                void* dk, void* dv, const void* ws, int batch, int Hq, int Hkv, int N,
+                                void* dk, void* dv, void* ws, int batch, int Hq, int Hkv, int N,
                                 hipStream_t s);
 hipError_t launch_attn_bwd_dq(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
                               const void* dout, const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
-                              void* dq, const void* ws, int batch, int Hq, int Hkv, int N, hipStream_t s);
+                              void* dq, void* ws, int batch, int Hq, int Hkv, int N, hipStream_t s);
 
 }  // namespace vsa2

@@ -92,6 +92,16 @@ def test_null_and_alignment_checks():
     assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_WORKSPACE"
 
 
+def test_forward_needs_its_work_order_workspace():
+    p = good()
+    st, n = vsa2.vsa2_attn_workspace(p, 0)
+    assert vsa2.STATUS_NAMES[st] == "VSA2_OK" and n >= 4 * p.batch * p.heads_q * 8 and n % 256 == 0
+    st = vsa2.vsa2_attn_fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, 1, FAKE, FAKE, None, None, 0, None)
+    assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_WORKSPACE"
+    st = vsa2.vsa2_attn_fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, 1, FAKE, FAKE, None, FAKE, n - 1, None)
+    assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_WORKSPACE"
+
+
 def test_staged_backward_argument_checks():
     """The three backward stages validate like vsa2_attn_bwd, before any
     device work (fake pointers are never dereferenced)."""

@@ -269,3 +269,79 @@ def test_bwd_unselected_blocks_are_zero_explicit():
     dk_ref, dv_ref = oracle.attn_bwd_dkdv(x["q"], x["k"], x["v"], x["do"], p, rp, ci)
     assert_values(to_np(dk).reshape(dk_ref.shape), dk_ref, "dK (two blocks)")
     assert_values(to_np(dv).reshape(dv_ref.shape), dv_ref, "dV (two blocks)")
+
+
+def _check_lpt_order(order, lengths):
+    """order is a permutation of each of the 8 XCD ranges, longest length
+    class first (class = len * 32 // (max_len + 1) over the range) and in row
+    order inside a class."""
+    n = lengths.size
+    q, r = divmod(n, 8)
+    for x in range(8):
+        beg = x * q + min(x, r)
+        cnt = q + (1 if x < r else 0)
+        seg = order[beg:beg + cnt].astype(np.int64)
+        assert np.array_equal(np.sort(seg), np.arange(beg, beg + cnt))
+        if cnt == 0:
+            continue
+        ln = lengths[seg]
+        cls = ln * 32 // (lengths[beg:beg + cnt].max() + 1)
+        assert (np.diff(cls) <= 0).all()
+        same = np.diff(cls) == 0
+        assert (np.diff(seg)[same] > 0).all()
+
+
+def test_work_order_and_ragged_rows():
+    """Rows of very different lengths (0 to N entries): the forward and the
+    backward put each XCD's rows longest first in their workspaces, and the
+    outputs still match the oracle (empty rows: O = 0, LSE = -inf)."""
+    w = CASES["bf16-d128"]
+    p = w.problem
+    x = make_inputs(w, with_grad=True)
+    rng = np.random.default_rng(11)
+    nrows = p.batch * p.heads_q * p.N
+    counts = rng.choice([0, 1, 2, 5, 17, p.N], size=nrows, p=[0.1, 0.2, 0.2, 0.2, 0.2, 0.1])
+    rp = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    ci = np.concatenate([np.sort(rng.choice(p.N, c, replace=False)) for c in counts]).astype(np.int32)
+    kp, ki = oracle.csr_to_csc(rp, ci, p)
+    dev = {k: to_dev(v, True) for k, v in x.items()}
+    t = {k: torch.from_numpy(np.ascontiguousarray(v)).cuda()
+         for k, v in (("rp", rp), ("ci", ci), ("kp", kp), ("ki", ki))}
+    P = vsa2.problem_from(p)
+    st, fws = vsa2.vsa2_attn_workspace(P, 0)
+    assert st == 0
+    ws = torch.full((fws // 4,), -7, dtype=torch.int32, device="cuda")
+    o = torch.empty_like(dev["q"])
+    lse = torch.empty(p.batch, p.heads_q, p.L, dtype=torch.float32, device="cuda")
+    st = vsa2.vsa2_attn_fwd(P, dev["q"].data_ptr(), dev["k"].data_ptr(), dev["v"].data_ptr(),
+                            t["rp"].data_ptr(), t["ci"].data_ptr(), t["ci"].numel(), o.data_ptr(),
+                            lse.data_ptr(), None, ws.data_ptr(), fws, 0)
+    assert st == 0
+    dq, dk, dv = vsa2.attn_bwd(p, dev["q"], dev["k"], dev["v"], o, lse, dev["do"], t["rp"], t["ci"],
+                               t["kp"], t["ki"])
+    torch.cuda.synchronize()
+    _check_lpt_order(ws.cpu().numpy()[:nrows], np.diff(rp).astype(np.int64))
+    # the backward's CSC order, read from a workspace of the staged call
+    a256 = lambda n: (n + 255) // 256 * 256
+    off = a256(8 * nrows * p.B) + a256(4 * nrows)
+    nkv = p.batch * p.heads_kv * p.N
+    bws = torch.empty(vsa2.vsa2_attn_workspace(P, 1)[1], dtype=torch.uint8, device="cuda")
+    st = vsa2.vsa2_attn_bwd_prep(P, o.data_ptr(), lse.data_ptr(), None, dev["do"].data_ptr(),
+                                 bws.data_ptr(), bws.numel(), 0)
+    assert st == 0
+    st = vsa2.vsa2_attn_bwd_dkdv(P, dev["q"].data_ptr(), dev["k"].data_ptr(), dev["v"].data_ptr(),
+                                 dev["do"].data_ptr(), t["kp"].data_ptr(), t["ki"].data_ptr(),
+                                 t["ki"].numel(), 0, torch.empty_like(dk).data_ptr(),
+                                 torch.empty_like(dv).data_ptr(), bws.data_ptr(), bws.numel(), 0)
+    assert st == 0
+    torch.cuda.synchronize()
+    kv_order = bws[off:off + 4 * nkv].view(torch.int32).cpu().numpy()
+    _check_lpt_order(kv_order, np.diff(kp).astype(np.int64))
+    o_ref, lse_ref = oracle.attn_fwd(x["q"], x["k"], x["v"], p, rp, ci)
+    assert_values(to_np(o).reshape(o_ref.shape), o_ref, "O (ragged rows)")
+    empty = np.repeat(counts == 0, p.B)
+    assert np.isneginf(lse.cpu().numpy().reshape(-1)[empty]).all()
+    dq_ref = oracle.attn_bwd_dq(x["q"], x["k"], x["v"], x["do"], p, rp, ci)
+    dk_ref, dv_ref = oracle.attn_bwd_dkdv(x["q"], x["k"], x["v"], x["do"], p, rp, ci)
+    for name, got, want in (("dQ", dq, dq_ref), ("dK", dk, dk_ref), ("dV", dv, dv_ref)):
+        assert_values(to_np(got).reshape(want.shape), want, name + " (ragged rows)")
