@@ -86,15 +86,20 @@ typedef struct {
 
 typedef enum {
     VSA2_SEL_TOPK = 0,   /* the k best key blocks of each query block         */
-    VSA2_SEL_MASS = 1    /* smallest best-first prefix whose score sum reaches
+    VSA2_SEL_MASS = 1,   /* smallest best-first prefix whose score sum reaches
                             mass * (row total), at most cap blocks            */
+    VSA2_SEL_SEQ_TOPK = 2 /* TopK_{N k} per (batch, head) (Sec. 2.2): the
+                            N*k best (query block, key block) pairs of the
+                            whole N x N map, ties to the lowest flat index
+                            n_q*N + n_k; rows get different counts (0 to N) */
 } vsa2_sel_mode;
 
-/* Selection rule over one row of block scores P_r[n_q, :].  Order is
- * (score desc, key-block index asc), decided on the fp32 scores. */
+/* Selection rule over the block scores P_r.  Order is (score desc, index
+ * asc), decided on the fp32 scores: key-block index within a row for TOPK
+ * and MASS, flat index over the sequence's map for SEQ_TOPK. */
 typedef struct {
     int32_t mode;        /* vsa2_sel_mode                                    */
-    int32_t k;           /* TOPK: 1 <= k; k > N keeps every block            */
+    int32_t k;           /* TOPK, SEQ_TOPK: 1 <= k; k >= N keeps every block */
     float mass;          /* MASS: 0 < mass <= 1                              */
     int32_t cap;         /* MASS: 1 <= cap                                   */
 } vsa2_select;
@@ -118,7 +123,8 @@ vsa2_status vsa2_pool(const vsa2_problem* p, int32_t heads, const void* x,
                       int32_t Pt, int32_t Ph, int32_t Pw, void* out, hipStream_t stream);
 
 /* Largest number of (query block, key block) pairs the rule can select:
- * batch*Hq*N*min(k, N) for TOPK, batch*Hq*N*min(cap, N) for MASS.  col_cap
+ * batch*Hq*N*min(k, N) for TOPK and SEQ_TOPK, batch*Hq*N*min(cap, N) for
+ * MASS.  col_cap
  * of vsa2_route, and the CSC entry capacity, must be at least this. */
 vsa2_status vsa2_route_capacity(const vsa2_problem* p, const vsa2_select* s, int64_t* pairs);
 
@@ -135,7 +141,8 @@ vsa2_status vsa2_route_workspace(const vsa2_problem* p, const vsa2_select* s, si
  *     P_r[n_q, n_k] = (1/G^2) * sum over the G x G pooled pairs of the two
  *     blocks (so every row of P_r sums to 1/G).  Two passes over the logits
  *     (row log-sum-exp, then softmax + pooling); P_hat is never stored.
- *   Selection per query block n_q over P_r[n_q, :] by the rule *s.
+ *   Selection by the rule *s: per query block n_q over P_r[n_q, :] (TOPK,
+ *   MASS), or over each (batch, head)'s whole map (SEQ_TOPK).
  *   row_ptr [batch*Hq*N + 1]  CSR offsets (row_ptr[0] = 0).
  *   col_idx [col_cap]         selected key blocks, ascending within a row.
  *   kv_ptr  [batch*Hkv*N + 1] CSC offsets over key-block rows, or NULL.

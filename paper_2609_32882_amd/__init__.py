@@ -23,7 +23,7 @@ STATUS_NAMES = {0: "VSA2_OK", 1: "VSA2_ERR_NULL", 2: "VSA2_ERR_SHAPE", 3: "VSA2_
                 4: "VSA2_ERR_SELECT", 5: "VSA2_ERR_CAPACITY", 6: "VSA2_ERR_ALIGN",
                 7: "VSA2_ERR_WORKSPACE", 8: "VSA2_ERR_HIP", 9: "VSA2_ERR_UNSUPPORTED"}
 VSA2_F32, VSA2_BF16 = 0, 1
-VSA2_SEL_TOPK, VSA2_SEL_MASS = 0, 1
+VSA2_SEL_TOPK, VSA2_SEL_MASS, VSA2_SEL_SEQ_TOPK = 0, 1, 2
 
 # Every symbol include/vsa2.h declares.
 EXPORTS = ("vsa2_status_str", "vsa2_pool", "vsa2_route_capacity", "vsa2_route_workspace",

@@ -51,7 +51,7 @@ vsa2_status check_kernel_shape(const vsa2_problem* p, const shape& s) {
 
 vsa2_status check_select(const vsa2_select* sel) {
     if (!sel) return VSA2_ERR_NULL;
-    if (sel->mode == VSA2_SEL_TOPK) return sel->k >= 1 ? VSA2_OK : VSA2_ERR_SELECT;
+    if (sel->mode == VSA2_SEL_TOPK || sel->mode == VSA2_SEL_SEQ_TOPK) return sel->k >= 1 ? VSA2_OK : VSA2_ERR_SELECT;
     if (sel->mode == VSA2_SEL_MASS) {
         if (!(sel->mass > 0.f && sel->mass <= 1.f)) return VSA2_ERR_SELECT;
         return sel->cap >= 1 ? VSA2_OK : VSA2_ERR_SELECT;
@@ -60,15 +60,17 @@ vsa2_status check_select(const vsa2_select* sel) {
 }
 
 int64_t keep_per_row(const vsa2_select* sel, int64_t N) {
-    const int64_t k = sel->mode == VSA2_SEL_TOPK ? sel->k : sel->cap;
+    // SEQ_TOPK keeps N*min(k, N) pairs per sequence: the same total as TOPK,
+    // spread unevenly over the rows (a row holds at most N)
+    const int64_t k = sel->mode == VSA2_SEL_MASS ? sel->cap : sel->k;
     return k < N ? k : N;
 }
 
 struct route_ws {
-    size_t lse2, scores, counts, mask, kv_counts, total;
+    size_t lse2, scores, counts, mask, kv_counts, seq, total;
 };
 
-route_ws route_layout(const vsa2_problem* p, const shape& s) {
+route_ws route_layout(const vsa2_problem* p, const shape& s, const vsa2_select* sel) {
     route_ws w;
     size_t at = 0;
     const int64_t words = (static_cast<int64_t>(p->heads_q / p->heads_kv) * s.N + 31) / 32;
@@ -77,6 +79,9 @@ route_ws route_layout(const vsa2_problem* p, const shape& s) {
     w.counts = at;    at = align_up(at + sizeof(int32_t) * static_cast<size_t>(s.rows_q));
     w.mask = at;      at = align_up(at + sizeof(uint32_t) * static_cast<size_t>(s.rows_kv * words));
     w.kv_counts = at; at = align_up(at + sizeof(int32_t) * static_cast<size_t>(s.rows_kv));
+    w.seq = at;
+    if (sel->mode == VSA2_SEL_SEQ_TOPK)
+        at = align_up(at + vsa2::seq_workspace_bytes(static_cast<int64_t>(p->batch) * p->heads_q, s.rows_q));
     w.total = at;
     return w;
 }
@@ -148,7 +153,7 @@ vsa2_status vsa2_route_workspace(const vsa2_problem* p, const vsa2_select* sel, 
     if (st != VSA2_OK) return st;
     if ((st = check_select(sel)) != VSA2_OK) return st;
     if (!bytes) return VSA2_ERR_NULL;
-    *bytes = route_layout(p, s).total;
+    *bytes = route_layout(p, s, sel).total;
     return VSA2_OK;
 }
 
@@ -168,7 +173,7 @@ vsa2_status vsa2_route(const vsa2_problem* p, const vsa2_select* sel, const void
     if (!aligned16(q_r) || !aligned16(k_r)) return VSA2_ERR_ALIGN;
     const int64_t keep = keep_per_row(sel, s.N);
     if (col_cap < s.rows_q * keep) return VSA2_ERR_CAPACITY;
-    const route_ws w = route_layout(p, s);
+    const route_ws w = route_layout(p, s, sel);
     if (!ws || ws_bytes < w.total) return VSA2_ERR_WORKSPACE;
     if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
     char* base = static_cast<char*>(ws);
@@ -179,15 +184,20 @@ vsa2_status vsa2_route(const vsa2_problem* p, const vsa2_select* sel, const void
 
     VSA2_TRY_HIP(vsa2::launch_route_passes(p->dtype, p->head_dim, static_cast<int>(s.G), q_r, k_r, lse2,
                                            scores, p->batch, p->heads_q, p->heads_kv, N, stream));
-    if (sel->mode == VSA2_SEL_TOPK) {
-        VSA2_TRY_HIP(vsa2::launch_uniform_ptr(row_ptr, s.rows_q, static_cast<int>(keep), stream));
+    if (sel->mode == VSA2_SEL_SEQ_TOPK) {
+        VSA2_TRY_HIP(vsa2::launch_select_seq(scores, static_cast<int64_t>(p->batch) * p->heads_q, N, sel->k,
+                                             base + w.seq, counts, row_ptr, col_idx, col_cap, stream));
     } else {
-        VSA2_TRY_HIP(vsa2::launch_select(0, scores, s.rows_q, N, sel->mode, sel->k, sel->mass, sel->cap,
-                                         counts, nullptr, nullptr, col_cap, stream));
-        VSA2_TRY_HIP(vsa2::launch_scan(counts, s.rows_q, row_ptr, stream));
+        if (sel->mode == VSA2_SEL_TOPK) {
+            VSA2_TRY_HIP(vsa2::launch_uniform_ptr(row_ptr, s.rows_q, static_cast<int>(keep), stream));
+        } else {
+            VSA2_TRY_HIP(vsa2::launch_select(0, scores, s.rows_q, N, sel->mode, sel->k, sel->mass, sel->cap,
+                                             counts, nullptr, nullptr, col_cap, stream));
+            VSA2_TRY_HIP(vsa2::launch_scan(counts, s.rows_q, row_ptr, stream));
+        }
+        VSA2_TRY_HIP(vsa2::launch_select(1, scores, s.rows_q, N, sel->mode, sel->k, sel->mass, sel->cap,
+                                         counts, row_ptr, col_idx, col_cap, stream));
     }
-    VSA2_TRY_HIP(vsa2::launch_select(1, scores, s.rows_q, N, sel->mode, sel->k, sel->mass, sel->cap,
-                                     counts, row_ptr, col_idx, col_cap, stream));
     if (kv_ptr) {
         VSA2_TRY_HIP(vsa2::launch_csc(row_ptr, col_idx, p->batch, p->heads_q, p->heads_kv, N, col_cap,
                                       reinterpret_cast<uint32_t*>(base + w.mask),

@@ -40,6 +40,10 @@ hipError_t launch_select(int phase, const float* scores, int64_t nrows, int N, i
                          float mass, int cap, int32_t* counts, const int32_t* row_ptr,
                          int32_t* col_idx, int64_t col_cap, hipStream_t s);
 hipError_t launch_scan(const int32_t* counts, int64_t n, int32_t* ptr, hipStream_t s);
+// Sequence-level top-(N k) selection over nseq maps of N x N scores.
+size_t seq_workspace_bytes(int64_t nseq, int64_t nrows);
+hipError_t launch_select_seq(const float* scores, int64_t nseq, int N, int k, void* ws, int32_t* counts,
+                             int32_t* row_ptr, int32_t* col_idx, int64_t col_cap, hipStream_t s);
 hipError_t launch_uniform_ptr(int32_t* ptr, int64_t n, int k, hipStream_t s);
 hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
 hipError_t launch_csc(const int32_t* row_ptr, const int32_t* col_idx, int batch, int Hq, int Hkv, int N,

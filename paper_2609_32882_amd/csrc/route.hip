@@ -452,6 +452,257 @@ hipError_t launch_select(int phase, const float* scores, int64_t nrows, int N, i
 }
 
 // ===========================================================================
+// Sequence-level selection: TopK_{N k} over each (batch, head)'s flattened
+// N x N map of block scores (Sec. 2.2, the selection over all query-block /
+// key-block pairs of a sequence).  Keeps the keep = min(N k, N^2) best pairs,
+// order (score desc, flat index n_q N + n_k asc), decided on the fp32 scores.
+//
+//   1. threshold: radix select of the keep-th largest score per sequence,
+//      8 bits at a time from the top (scores are >= 0: bit patterns order
+//      like the values).  Each pass histograms the digit of the entries that
+//      match the prefix found so far (chunked over many workgroups, LDS
+//      histograms merged with integer atomics), then one thread per sequence
+//      picks the digit.  Result: tau and need = how many entries equal to
+//      tau are kept (the ones with the lowest flat indices).
+//   2. per row: gt = #(> tau), eq = #(== tau); per sequence, an exclusive
+//      scan of eq in row order gives each row's share of the need.
+//   3. offsets (scan_kernel) and the kept indices, ascending per row.
+// ===========================================================================
+struct seq_state {
+    uint32_t prefix;   // digits of tau found so far
+    int32_t rem;       // rank of the target among the entries matching prefix
+};
+
+constexpr int SEQ_NT = 256;
+constexpr int SEQ_CHUNK = SEQ_NT * 64;   // entries per histogram workgroup
+constexpr int SEQ_HSTRIDE = 257;         // per-lane-group histogram stride (words)
+
+__global__ void seq_init_kernel(seq_state* __restrict__ st, uint32_t* __restrict__ ghist, int64_t nseq,
+                                int64_t keep) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i < nseq) {
+        st[i].prefix = 0;
+        st[i].rem = static_cast<int32_t>(keep);
+    }
+    if (i < nseq * 256) ghist[i] = 0;
+}
+
+// grid (chunks, nseq).  Histogram of digit (v >> shift) & 255 over the
+// entries of chunk blockIdx.x of sequence blockIdx.y that match the prefix.
+__global__ __launch_bounds__(SEQ_NT) void seq_hist_kernel(const float* __restrict__ scores, int64_t nn,
+                                                          const seq_state* __restrict__ st,
+                                                          uint32_t* __restrict__ ghist, int pass) {
+    // four sub-histograms per wave (lane & 3), padded so one bin of the four
+    // sits in four different banks
+    __shared__ uint32_t h[SEQ_NT / 64][4][SEQ_HSTRIDE];
+    const int tid = threadIdx.x, wave = tid >> 6, sub = tid & 3;
+    const int64_t seq = blockIdx.y;
+    const int shift = 24 - 8 * pass;
+    const uint32_t hi_mask = pass == 0 ? 0u : (0xffffffffu << (shift + 8));
+    const uint32_t want = pass == 0 ? 0u : (st[seq].prefix << (shift + 8));
+    for (int i = tid; i < (SEQ_NT / 64) * 4 * SEQ_HSTRIDE; i += SEQ_NT) (&h[0][0][0])[i] = 0;
+    __syncthreads();
+    const uint32_t* u = reinterpret_cast<const uint32_t*>(scores + seq * nn);
+    const int64_t c0 = static_cast<int64_t>(blockIdx.x) * SEQ_CHUNK;
+    const int64_t c1 = c0 + SEQ_CHUNK < nn ? c0 + SEQ_CHUNK : nn;
+    for (int64_t i = c0 + tid; i < c1; i += SEQ_NT) {
+        const uint32_t v = u[i];
+        if ((v & hi_mask) == want) atomicAdd(&h[wave][sub][(v >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    uint32_t sum = 0;
+#pragma unroll
+    for (int w = 0; w < SEQ_NT / 64; ++w)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) sum += h[w][k][tid];
+    if (sum) atomicAdd(&ghist[seq * 256 + tid], sum);
+}
+
+// One thread per sequence: the digit holding the target rank; clears the
+// histogram for the next pass.  After the last pass prefix = tau's bits and
+// rem = the number of entries equal to tau that are kept.
+__global__ void seq_pick_kernel(seq_state* __restrict__ st, uint32_t* __restrict__ ghist, int64_t nseq) {
+    const int64_t seq = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (seq >= nseq) return;
+    uint32_t* h = ghist + seq * 256;
+    int64_t r = st[seq].rem;
+    int d = 255;
+    for (; d > 0; --d) {
+        if (static_cast<int64_t>(h[d]) >= r) break;
+        r -= h[d];
+    }
+    st[seq].prefix = (st[seq].prefix << 8) | static_cast<uint32_t>(d);
+    st[seq].rem = static_cast<int32_t>(r);
+    for (int b = 0; b < 256; ++b) h[b] = 0;
+}
+
+// One wave per row (N <= 64*PER).  PHASE 0: gt[row], eq[row].  PHASE 1:
+// write the kept indices ascending at col_idx[row_ptr[row] ...]: every entry
+// > tau and the first take[row] entries == tau.
+template <int PER, int PHASE>
+__global__ __launch_bounds__(256) void seq_rows_kernel(const float* __restrict__ scores, int64_t nrows, int N,
+                                                       const seq_state* __restrict__ st,
+                                                       int32_t* __restrict__ gt, int32_t* __restrict__ eq,
+                                                       const int32_t* __restrict__ take,
+                                                       const int32_t* __restrict__ row_ptr,
+                                                       int32_t* __restrict__ col_idx, int64_t col_cap) {
+    const int lane = threadIdx.x & 63;
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+    if (row >= nrows) return;
+    const float tau = __uint_as_float(st[row / N].prefix);
+    float x[PER];
+    const float* src = scores + row * N;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+        const int j = i * 64 + lane;
+        x[i] = j < N ? src[j] : -1.0f;
+    }
+    if constexpr (PHASE == 0) {
+        int g = 0, e = 0;
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            g += x[i] > tau ? 1 : 0;
+            e += x[i] == tau ? 1 : 0;
+        }
+        g = wave_sum_i(g);
+        e = wave_sum_i(e);
+        if (lane == 0) {
+            gt[row] = g;
+            eq[row] = e;
+        }
+    } else {
+        const int need = take[row];
+        int64_t pos = row_ptr[row];
+        int ties = 0;
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const bool is_eq = x[i] == tau;
+            const uint64_t eqm = __ballot(is_eq);
+            const int rank = ties + __popcll(eqm & ((1ull << lane) - 1ull));
+            const bool sel = x[i] > tau || (is_eq && rank < need);
+            const uint64_t sm = __ballot(sel);
+            if (sel) {
+                const int64_t at = pos + __popcll(sm & ((1ull << lane) - 1ull));
+                if (at < col_cap) col_idx[at] = i * 64 + lane;
+            }
+            pos += __popcll(sm);
+            ties += __popcll(eqm);
+        }
+    }
+}
+
+// One workgroup (1024) per sequence: take[row] = the row's share of the
+// sequence's need, in row order; counts[row] = gt + take.
+__global__ __launch_bounds__(1024) void seq_take_kernel(const seq_state* __restrict__ st, int N,
+                                                        const int32_t* __restrict__ gt,
+                                                        const int32_t* __restrict__ eq,
+                                                        int32_t* __restrict__ take, int32_t* __restrict__ counts) {
+    __shared__ int32_t part[1024];
+    const int tid = threadIdx.x;
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * N;
+    const int per = (N + 1023) / 1024;
+    const int lo = tid * per < N ? tid * per : N;
+    const int hi = lo + per < N ? lo + per : N;
+    int32_t sum = 0;
+    for (int i = lo; i < hi; ++i) sum += eq[base + i];
+    part[tid] = sum;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+        const int32_t v = tid >= off ? part[tid - off] : 0;
+        __syncthreads();
+        part[tid] += v;
+        __syncthreads();
+    }
+    int64_t before = part[tid] - sum;
+    const int64_t need = st[blockIdx.x].rem;
+    for (int i = lo; i < hi; ++i) {
+        const int64_t e = eq[base + i];
+        int64_t t = need - before;
+        t = t < 0 ? 0 : (t > e ? e : t);
+        take[base + i] = static_cast<int32_t>(t);
+        counts[base + i] = gt[base + i] + static_cast<int32_t>(t);
+        before += e;
+    }
+}
+
+template <int PER>
+static hipError_t launch_seq_rows(int phase, const float* scores, int64_t nrows, int N, const seq_state* st,
+                                  int32_t* gt, int32_t* eq, const int32_t* take, const int32_t* row_ptr,
+                                  int32_t* col_idx, int64_t col_cap, hipStream_t s) {
+    dim3 grid(static_cast<unsigned>((nrows + 3) / 4));
+    if (phase == 0)
+        hipLaunchKernelGGL((seq_rows_kernel<PER, 0>), grid, dim3(256), 0, s, scores, nrows, N, st, gt, eq, take,
+                           row_ptr, col_idx, col_cap);
+    else
+        hipLaunchKernelGGL((seq_rows_kernel<PER, 1>), grid, dim3(256), 0, s, scores, nrows, N, st, gt, eq, take,
+                           row_ptr, col_idx, col_cap);
+    return hipGetLastError();
+}
+
+static hipError_t launch_seq_rows_any(int phase, const float* scores, int64_t nrows, int N, const seq_state* st,
+                                      int32_t* gt, int32_t* eq, const int32_t* take, const int32_t* row_ptr,
+                                      int32_t* col_idx, int64_t col_cap, hipStream_t s) {
+    const int per = (N + 63) / 64;
+#define VSA2_SEQ(P) \
+    if (per <= P) return launch_seq_rows<P>(phase, scores, nrows, N, st, gt, eq, take, row_ptr, col_idx, col_cap, s)
+    VSA2_SEQ(2);
+    VSA2_SEQ(4);
+    VSA2_SEQ(8);
+    VSA2_SEQ(16);
+    VSA2_SEQ(24);
+    VSA2_SEQ(32);
+    VSA2_SEQ(40);
+    VSA2_SEQ(48);
+    VSA2_SEQ(64);
+#undef VSA2_SEQ
+    return hipErrorInvalidValue;
+}
+
+size_t seq_workspace_bytes(int64_t nseq, int64_t nrows) {
+    auto a = [](size_t x) { return (x + 255) / 256 * 256; };
+    return a(sizeof(seq_state) * nseq) + a(4 * 256 * nseq) + 3 * a(4 * nrows);
+}
+
+hipError_t launch_select_seq(const float* scores, int64_t nseq, int N, int k, void* ws, int32_t* counts,
+                             int32_t* row_ptr, int32_t* col_idx, int64_t col_cap, hipStream_t s) {
+    if (nseq == 0) return hipSuccess;
+    auto a = [](size_t x) { return (x + 255) / 256 * 256; };
+    const int64_t nn = static_cast<int64_t>(N) * N;
+    const int64_t nrows = nseq * N;
+    const int64_t keep = static_cast<int64_t>(N) * k < nn ? static_cast<int64_t>(N) * k : nn;
+    char* w = static_cast<char*>(ws);
+    seq_state* st = reinterpret_cast<seq_state*>(w);
+    w += a(sizeof(seq_state) * nseq);
+    uint32_t* ghist = reinterpret_cast<uint32_t*>(w);
+    w += a(4 * 256 * nseq);
+    int32_t* gt = reinterpret_cast<int32_t*>(w);
+    w += a(4 * nrows);
+    int32_t* eq = reinterpret_cast<int32_t*>(w);
+    w += a(4 * nrows);
+    int32_t* take = reinterpret_cast<int32_t*>(w);
+
+    hipLaunchKernelGGL(seq_init_kernel, dim3(static_cast<unsigned>((nseq * 256 + 255) / 256)), dim3(256), 0, s, st,
+                       ghist, nseq, keep);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 hgrid(static_cast<unsigned>((nn + SEQ_CHUNK - 1) / SEQ_CHUNK), static_cast<unsigned>(nseq));
+    for (int pass = 0; pass < 4; ++pass) {
+        hipLaunchKernelGGL(seq_hist_kernel, hgrid, dim3(SEQ_NT), 0, s, scores, nn, st, ghist, pass);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(seq_pick_kernel, dim3(static_cast<unsigned>((nseq + 63) / 64)), dim3(64), 0, s, st,
+                           ghist, nseq);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if ((e = launch_seq_rows_any(0, scores, nrows, N, st, gt, eq, nullptr, nullptr, nullptr, 0, s)) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(seq_take_kernel, dim3(static_cast<unsigned>(nseq)), dim3(1024), 0, s, st, N, gt, eq, take,
+                       counts);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_scan(counts, nrows, row_ptr, s)) != hipSuccess) return e;
+    return launch_seq_rows_any(1, scores, nrows, N, st, gt, eq, take, row_ptr, col_idx, col_cap, s);
+}
+
+// ===========================================================================
 // Offsets and the transposed lists
 // ===========================================================================
 // Exclusive scan of counts[0..n) into ptr[0..n] by one workgroup of 1024.

@@ -102,6 +102,19 @@ def test_forward_needs_its_work_order_workspace():
     assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_WORKSPACE"
 
 
+def test_sequence_topk_rule_capacity_and_workspace():
+    p = good()                                # N = 32 cubes, 4 query heads
+    for k, want in ((5, 4 * 32 * 5), (40, 4 * 32 * 32)):
+        st, n = vsa2.vsa2_route_capacity(p, vsa2.vsa2_select(2, k, 0.0, 0))
+        assert vsa2.STATUS_NAMES[st] == "VSA2_OK" and n == want
+    st0, w0 = vsa2.vsa2_route_workspace(p, vsa2.vsa2_select(0, 5, 0.0, 0))
+    st2, w2 = vsa2.vsa2_route_workspace(p, vsa2.vsa2_select(2, 5, 0.0, 0))
+    assert st0 == st2 == 0 and w2 > w0
+    for bad in (vsa2.vsa2_select(2, 0, 0.0, 0), vsa2.vsa2_select(3, 5, 0.0, 0)):
+        st, _ = vsa2.vsa2_route_capacity(p, bad)
+        assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_SELECT"
+
+
 def test_staged_backward_argument_checks():
     """The three backward stages validate like vsa2_attn_bwd, before any
     device work (fake pointers are never dereferenced)."""

@@ -345,3 +345,80 @@ def test_work_order_and_ragged_rows():
     dk_ref, dv_ref = oracle.attn_bwd_dkdv(x["q"], x["k"], x["v"], x["do"], p, rp, ci)
     for name, got, want in (("dQ", dq, dq_ref), ("dK", dk, dk_ref), ("dV", dv, dv_ref)):
         assert_values(to_np(got).reshape(want.shape), want, name + " (ragged rows)")
+
+
+def _check_seq_selection(p, k, rp, ci, ref_scores, exact_scores=None):
+    """GPU per-sequence top-(N k) lists against the oracle's flat sort.
+    With exact_scores (the GPU's own fp32 scores) the oracle must reproduce
+    the selection bit for bit; against the oracle's fp64 scores a pair may
+    differ only if its score lies within 1e-6 (relative) of its sequence's
+    threshold."""
+    N = p.N
+    nseq = p.batch * p.heads_q
+    keep = min(N * k, N * N)
+    got = np.zeros((nseq * N, N), bool)
+    counts = np.diff(rp)
+    assert (counts >= 0).all() and (counts <= N).all()
+    for r in range(nseq * N):
+        c = ci[rp[r]:rp[r + 1]]
+        assert (np.diff(c) > 0).all() and (c >= 0).all() and (c < N).all()
+        got[r, c] = True
+    got = got.reshape(nseq, N, N)
+    assert (got.reshape(nseq, -1).sum(1) == keep).all()
+    if exact_scores is not None:
+        want = oracle.select_seq(exact_scores.reshape(nseq, N, N).astype(np.float64), N, k)
+        assert np.array_equal(got, want)
+    want = oracle.select_seq(ref_scores.reshape(nseq, N, N), N, k)
+    sc32 = ref_scores.reshape(nseq, N * N).astype(np.float32).astype(np.float64)
+    excused = 0
+    for sq in range(nseq):
+        diff = got[sq].reshape(-1) != want[sq].reshape(-1)
+        if diff.any():
+            tau = np.sort(sc32[sq])[::-1][keep - 1]
+            assert (np.abs(sc32[sq][diff] - tau) <= 1e-6 * tau).all()
+            excused += int(diff.sum())
+    print("sequence top-k: %d sequences, %d pairs each, %d near-tie differences" % (nseq, keep, excused))
+
+
+@pytest.mark.parametrize("k", [3, 11])
+def test_route_sequence_topk_matches_oracle(case, k):
+    w, x, ref, dev = case
+    p = w.problem
+    q_r = vsa2.pool(p, dev["q"], (p.Rt, p.Rh, p.Rw))
+    k_r = vsa2.pool(p, dev["k"], (p.Rt, p.Rh, p.Rw))
+    r = vsa2.route(p, Selection(2, k), q_r, k_r, with_scores=True)
+    torch.cuda.synchronize()
+    rp = r["row_ptr"].cpu().numpy()
+    ci = r["col_idx"].cpu().numpy()
+    _check_seq_selection(p, k, rp, ci, ref["scores"], r["scores"].cpu().numpy())
+    kp, ki = oracle.csr_to_csc(rp, ci[:rp[-1]], p)
+    assert np.array_equal(r["kv_ptr"].cpu().numpy(), kp)
+    assert np.array_equal(r["kv_idx"].cpu().numpy()[:rp[-1]], ki)
+
+
+def test_route_sequence_topk_all_ties():
+    """Zero pooled queries and keys make every block score equal: the rule
+    keeps the first N*k pairs in flat order, i.e. rows 0 .. k-1 whole and
+    nothing else; the forward then gives O = 0, LSE = -inf on the empty rows."""
+    w = CASES["bf16-d128"]
+    p = w.problem
+    N = p.N
+    k = 5
+    z_q = torch.zeros(p.batch, p.heads_q, N * p.G, p.head_dim, dtype=torch.bfloat16, device="cuda")
+    z_k = torch.zeros(p.batch, p.heads_kv, N * p.G, p.head_dim, dtype=torch.bfloat16, device="cuda")
+    r = vsa2.route(p, Selection(2, k), z_q, z_k, with_scores=True)
+    torch.cuda.synchronize()
+    rp = r["row_ptr"].cpu().numpy()
+    ci = r["col_idx"].cpu().numpy()
+    sc = r["scores"].cpu().numpy()
+    assert (sc == sc.reshape(-1)[0]).all()
+    counts = np.diff(rp).reshape(-1, N)
+    assert (counts[:, :k] == N).all() and (counts[:, k:] == 0).all()
+    _check_seq_selection(p, k, rp, ci, sc.astype(np.float64), sc)
+    x = make_inputs(w, with_grad=False)
+    d = {n: to_dev(x[n], True) for n in ("q", "k", "v")}
+    o, lse = vsa2.attn_fwd(p, d["q"], d["k"], d["v"], r["row_ptr"], r["col_idx"])
+    torch.cuda.synchronize()
+    lse_np = lse.cpu().numpy().reshape(-1, N, p.B)
+    assert np.isneginf(lse_np[:, k:]).all() and np.isfinite(lse_np[:, :k]).all()
+    assert (to_np(o).reshape(-1, N, p.B, p.head_dim)[:, k:] == 0).all()

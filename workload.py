@@ -81,7 +81,8 @@ class Problem:
 @dataclasses.dataclass(frozen=True)
 class Selection:
     """Selection rule: mode 0 = top-k per query block, 1 = smallest prefix
-    reaching `mass` of the row's score total, capped at `cap` blocks."""
+    reaching `mass` of the row's score total, capped at `cap` blocks, 2 =
+    the N*k best pairs of each (batch, head)'s whole N x N map."""
     mode: int = 0
     k: int = 8
     mass: float = 0.9
@@ -98,7 +99,8 @@ class Workload:
     backward: bool = True
 
 
-# The five shapes of the routed-attention benchmark suite.
+# Workload shapes: tiny, 480p, 720p, 720p with mass selection, long-clip GQA,
+# and 720p-seq (the 720p inputs under the per-sequence rule).
 WORKLOADS = {
     "tiny": Workload(
         "tiny", Problem(1, 2, 2, 64, 8, 16, 16, dtype=F32), Selection(0, 8), 1000,
@@ -112,6 +114,9 @@ WORKLOADS = {
         skewed=True),
     "gqa-long": Workload(
         "gqa-long", Problem(1, 40, 8, 128, 40, 48, 80), Selection(0, 120), 1004),
+    # the paper's own rule, TopK_{N k} per (batch, head), on the 720p inputs
+    "720p-seq": Workload(
+        "720p-seq", Problem(1, 40, 40, 128, 20, 48, 80), Selection(2, 120), 1002),
 }
 
 
