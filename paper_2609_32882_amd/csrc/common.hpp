@@ -386,14 +386,19 @@ __device__ __forceinline__ void dma16(uint32_t lds, const void* base, int voff) 
 
 // Start offset of a block list for a phased sweep.  Row number `local` on
 // its XCD starts at its first entry >= (local mod period) * npos / period and
-// wraps around, so the `period` workgroups that are resident on one XCD at
-// the same time (dispatched in order) begin evenly spread over the key (or
-// query) range instead of all sweeping their ascending lists from the low end.
-// Measured at 720p, this cuts the L2 misses of the tile gathers by ~40% over
-// ascending sweeps; random starts, or a spread over a fraction of the range,
-// do not.  The start depends only on the row number, so results stay
-// deterministic.  Entries are read through the scalar cache (binary search,
-// ~log2(n) loads).
+// wraps around, with period = the number of workgroups resident on one XCD
+// at a time.  Why this keeps co-resident workgroups on the same tiles: the
+// dispatcher starts workgroup j when an earlier one ends, so in steady state
+// the resident workgroups are J-period .. J-1 (J = next to dispatch) and
+// workgroup J-m has done about m/period of its list, i.e. has advanced
+// m*npos/period through the (evenly spread) positions.  Its start offset
+// ((J-m) mod period)*npos/period cancels that advance modulo npos: every
+// resident workgroup sits at about (J mod period)*npos/period, and the
+// tiles they gather are shared through the XCD's L2.  This needs rows of
+// (nearly) equal length; a period off by 2x in either direction loses most
+// of the effect (measured).  The start depends only on the row number, so
+// results stay deterministic.  Entries are read through the scalar cache
+// (binary search, ~log2(n) loads).
 __device__ __forceinline__ int64_t sweep_start(const int32_t* list, int64_t e0, int64_t cnt, int64_t local,
                                                int period, int npos) {
     if (cnt < 2 || period < 2) return 0;
