@@ -19,7 +19,7 @@ from workload import BF16, WORKLOADS, make_inputs
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
-FULL = ["480p", "720p", "720p-mass", "gqa-long", "720p-seq"]
+FULL = ["480p", "720p", "720p-mass", "gqa-long", "720p-seq", "720p-vsa"]
 
 
 def _dev(x):

@@ -27,6 +27,12 @@ CASES = {
     "bf16-full-b2": Workload("bf16-full-b2", Problem(2, 2, 1, 128, 4, 16, 16), Selection(0, 100), 2004),
     "f32-d128-mass": Workload("f32-d128-mass", Problem(1, 2, 1, 128, 4, 16, 16, dtype=F32),
                               Selection(1, 0, 0.5, 3), 2005, skewed=True),
+    # router pool R = B (G = 1): the coarse cube-level router of VSA
+    "bf16-router-R=B": Workload("bf16-router-R=B", Problem(1, 2, 2, 128, 8, 16, 24, Rt=4, Rh=4, Rw=4),
+                                Selection(0, 12), 2006),
+    # R = 2x2x4 (G = 4), GQA
+    "bf16-router-G4": Workload("bf16-router-G4", Problem(1, 4, 2, 64, 8, 16, 16, Rt=2, Rh=2, Rw=4),
+                               Selection(0, 6), 2007),
 }
 
 

@@ -99,8 +99,9 @@ class Workload:
     backward: bool = True
 
 
-# Workload shapes: tiny, 480p, 720p, 720p with mass selection, long-clip GQA,
-# and 720p-seq (the 720p inputs under the per-sequence rule).
+# Workload shapes: tiny, 480p, 720p, 720p with mass selection, long-clip GQA;
+# 720p-seq and 720p-vsa reuse the 720p inputs under the per-sequence rule and
+# under the coarse (R = B) router.
 WORKLOADS = {
     "tiny": Workload(
         "tiny", Problem(1, 2, 2, 64, 8, 16, 16, dtype=F32), Selection(0, 8), 1000,
@@ -117,6 +118,9 @@ WORKLOADS = {
     # the paper's own rule, TopK_{N k} per (batch, head), on the 720p inputs
     "720p-seq": Workload(
         "720p-seq", Problem(1, 40, 40, 128, 20, 48, 80), Selection(2, 120), 1002),
+    # the coarse cube-level router of VSA (router pool R = B, G = 1) on the 720p inputs
+    "720p-vsa": Workload(
+        "720p-vsa", Problem(1, 40, 40, 128, 20, 48, 80, Rt=4, Rh=4, Rw=4), Selection(0, 120), 1002),
 }
 
 
