@@ -54,8 +54,15 @@ def lib():
         L.vo_attn_bwd_dq.argtypes = [P, P, P, P, i32, i32, i32, i64, i32, i32, P, P, P, i64, P]
         L.vo_attn_bwd_dkdv.argtypes = [P, P, P, P, i32, i32, i32, i64, i32, i32, P, P, P, i64,
                                        P, P]
+        L.vo_coarse_fwd.argtypes = [P, P, P, i32, i32, i32, i32, i32, P, P]
+        L.vo_coarse_bwd.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, P, P, P]
+        L.vo_gate_merge.argtypes = [P, P, P, i64, i32, i32, i32, P]
+        L.vo_gate_merge_bwd.argtypes = [P, P, P, i64, i32, i32, i32, P, P]
+        L.vo_unpool_add.argtypes = [P, i64, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, P]
         for f in (L.vo_round_bf16, L.vo_pool, L.vo_router_scores, L.vo_select_rows,
-                  L.vo_select_seq, L.vo_attn_fwd, L.vo_attn_bwd_dq, L.vo_attn_bwd_dkdv):
+                  L.vo_select_seq, L.vo_attn_fwd, L.vo_attn_bwd_dq, L.vo_attn_bwd_dkdv,
+                  L.vo_coarse_fwd, L.vo_coarse_bwd, L.vo_gate_merge, L.vo_gate_merge_bwd,
+                  L.vo_unpool_add):
             f.restype = None
         _lib = L
     return _lib
@@ -210,3 +217,62 @@ def select_seq(scores_bh, N: int, k: int):
     sel = np.empty(s.shape, np.uint8)
     lib().vo_select_seq(_p(s), s.shape[0], N, k, _p(sel))
     return sel.reshape(-1, N, N).astype(bool)
+
+
+# --------------------------------------------------------------------------
+# Coarse branch and gated merge (Sec. 2.2 "Coarse Branch", "Gated Merge")
+# --------------------------------------------------------------------------
+
+
+def coarse_fwd(qc, kc, vc, p):
+    """Dense attention among the N cube means of each head (Eq. compress and
+    the two equations after it).  qc [b, Hq, N, D], kc, vc [b, Hkv, N, D]
+    (MeanPool_B outputs).  Returns O_c_hat [b, Hq, N, D] and the natural-log
+    LSE [b, Hq, N], float64."""
+    qc, kc, vc = _f32(qc), _f32(kc), _f32(vc)
+    N, D = p.N, p.head_dim
+    oc = np.empty((p.batch, p.heads_q, N, D), np.float64)
+    lse = np.empty((p.batch, p.heads_q, N), np.float64)
+    lib().vo_coarse_fwd(_p(qc), _p(kc), _p(vc), p.batch, p.heads_q, p.heads_kv, N, D, _p(oc), _p(lse))
+    return oc, lse
+
+
+def coarse_bwd(qc, kc, vc, doc, p):
+    """Gradients (dqc, dkc, dvc) of coarse_fwd for the output gradient doc."""
+    qc, kc, vc, doc = _f32(qc), _f32(kc), _f32(vc), _f32(doc)
+    N, D = p.N, p.head_dim
+    dqc = np.empty((p.batch, p.heads_q, N, D), np.float64)
+    dkc = np.empty((p.batch, p.heads_kv, N, D), np.float64)
+    dvc = np.empty((p.batch, p.heads_kv, N, D), np.float64)
+    lib().vo_coarse_bwd(_p(qc), _p(kc), _p(vc), _p(doc), p.batch, p.heads_q, p.heads_kv, N, D,
+                        _p(dqc), _p(dkc), _p(dvc))
+    return dqc, dkc, dvc
+
+
+def gate_merge(g, oc, of, p):
+    """O = tanh(g) * Repeat_B(O_c_hat) + O_f (Eq. gate_linear, gated merge).
+    g [b, Hq, L] gate pre-activations; oc [b, Hq, N, D]; of [b, Hq, L, D]."""
+    g, oc, of = _f32(g), _f32(oc), _f32(of)
+    out = np.empty((p.batch, p.heads_q, p.L, p.head_dim), np.float64)
+    lib().vo_gate_merge(_p(g), _p(oc), _p(of), p.batch * p.heads_q, p.N, p.B, p.head_dim, _p(out))
+    return out
+
+
+def gate_merge_bwd(g, oc, dout, p):
+    """(d O_c_hat, d g) of gate_merge for dout; d O_f is dout itself."""
+    g, oc, dout = _f32(g), _f32(oc), _f32(dout)
+    doc = np.empty((p.batch, p.heads_q, p.N, p.head_dim), np.float64)
+    dg = np.empty((p.batch, p.heads_q, p.L), np.float64)
+    lib().vo_gate_merge_bwd(_p(g), _p(oc), _p(dout), p.batch * p.heads_q, p.N, p.B, p.head_dim,
+                            _p(doc), _p(dg))
+    return doc, dg
+
+
+def unpool_add(dxc, dx, p, Pt: int, Ph: int, Pw: int):
+    """dx += the adjoint of MeanPool over (Pt, Ph, Pw) applied to dxc.
+    dxc [b, heads, N*Gp, D] and dx [b, heads, L, D], float64; dx is updated."""
+    dxc = np.ascontiguousarray(dxc, np.float64)
+    assert dx.dtype == np.float64 and dx.flags.c_contiguous
+    nbh = dx.shape[0] * dx.shape[1]
+    lib().vo_unpool_add(_p(dxc), nbh, p.T, p.H, p.W, p.Bt, p.Bh, p.Bw, Pt, Ph, Pw, p.head_dim, _p(dx))
+    return dx

@@ -469,3 +469,193 @@ void vo_attn_bwd_dkdv(const float* q, const float* k, const float* v, const floa
     free(cv);
     free(pr);
 }
+
+/* ---------------------------------------------------------------------- */
+/* Coarse branch (Sec. 2.2 "Coarse Branch", Eq. compress and the two       */
+/* equations after it): dense softmax attention among the N cube means of  */
+/* a head, P_c = Softmax(Q_c K_c^T / sqrt(D)), O_c_hat = P_c V_c; Repeat_B */
+/* then broadcasts row n to the B tokens of cube n (done by the merge).    */
+/* ---------------------------------------------------------------------- */
+
+/* qc: [nb][Hq][N][D]; kc, vc: [nb][Hkv][N][D] (MeanPool_B outputs, float).
+ * oc: [nb][Hq][N][D], lse: [nb][Hq][N] natural-log log-sum-exp of each row's
+ * scaled scores.  Query head h reads KV head h / (Hq/Hkv). */
+void vo_coarse_fwd(const float* qc, const float* kc, const float* vc, int nb, int Hq, int Hkv,
+                   int N, int D, double* oc, double* lse)
+{
+    const int grp = Hq / Hkv;
+    const double scale = 1.0 / sqrt((double)D);
+    const int64_t nrows = (int64_t)nb * Hq * N;
+#pragma omp parallel
+    {
+        double* s = (double*)malloc(sizeof(double) * (size_t)N);
+#pragma omp for schedule(static)
+        for (int64_t row = 0; row < nrows; ++row) {
+            const int64_t bh = row / N;
+            const int64_t b = bh / Hq, h = bh % Hq;
+            const int64_t kv = b * Hkv + h / grp;
+            const float* qv = qc + row * D;
+            double m = -INFINITY;
+            for (int j = 0; j < N; ++j) {
+                const float* kj = kc + (kv * N + j) * (int64_t)D;
+                double dot = 0.0;
+                for (int d = 0; d < D; ++d) dot += (double)qv[d] * (double)kj[d];
+                s[j] = dot * scale;
+                if (s[j] > m) m = s[j];
+            }
+            double sum = 0.0;
+            for (int j = 0; j < N; ++j) { s[j] = exp(s[j] - m); sum += s[j]; }
+            double* o = oc + row * D;
+            for (int d = 0; d < D; ++d) o[d] = 0.0;
+            for (int j = 0; j < N; ++j) {
+                const double pj = s[j] / sum;
+                const float* vj = vc + (kv * N + j) * (int64_t)D;
+                for (int d = 0; d < D; ++d) o[d] += pj * (double)vj[d];
+            }
+            lse[row] = m + log(sum);
+        }
+        free(s);
+    }
+}
+
+/* Gradients of vo_coarse_fwd for the output gradient doc ([nb][Hq][N][D]):
+ * with p the softmax row of coarse query i,
+ *   Delta_i = doc_i . oc_i,  dS_ij = p_ij (doc_i . vc_j - Delta_i),
+ *   dqc_i = scale sum_j dS_ij kc_j,  dkc_j = scale sum_i dS_ij qc_i,
+ *   dvc_j = sum_i p_ij doc_i,
+ * the sums over i running over every query head of j's KV group.  One task
+ * per (batch, KV head) owns its dkc / dvc rows. */
+void vo_coarse_bwd(const float* qc, const float* kc, const float* vc, const float* doc, int nb,
+                   int Hq, int Hkv, int N, int D, double* dqc, double* dkc, double* dvc)
+{
+    const int grp = Hq / Hkv;
+    const double scale = 1.0 / sqrt((double)D);
+    const int64_t nkv = (int64_t)nb * Hkv;
+#pragma omp parallel
+    {
+        double* p = (double*)malloc(sizeof(double) * (size_t)N);
+        double* o = (double*)malloc(sizeof(double) * (size_t)D);
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t kv = 0; kv < nkv; ++kv) {
+            const int64_t b = kv / Hkv, hkv = kv % Hkv;
+            double* gk = dkc + kv * N * (int64_t)D;
+            double* gv = dvc + kv * N * (int64_t)D;
+            for (int64_t x = 0; x < (int64_t)N * D; ++x) { gk[x] = 0.0; gv[x] = 0.0; }
+            for (int hl = 0; hl < grp; ++hl) {
+                const int64_t bh = b * Hq + hkv * grp + hl;
+                for (int i = 0; i < N; ++i) {
+                    const int64_t row = bh * N + i;
+                    const float* qv = qc + row * D;
+                    const float* dov = doc + row * D;
+                    double m = -INFINITY;
+                    for (int j = 0; j < N; ++j) {
+                        const float* kj = kc + (kv * N + j) * (int64_t)D;
+                        double dot = 0.0;
+                        for (int d = 0; d < D; ++d) dot += (double)qv[d] * (double)kj[d];
+                        p[j] = dot * scale;
+                        if (p[j] > m) m = p[j];
+                    }
+                    double sum = 0.0;
+                    for (int j = 0; j < N; ++j) { p[j] = exp(p[j] - m); sum += p[j]; }
+                    for (int j = 0; j < N; ++j) p[j] /= sum;
+                    for (int d = 0; d < D; ++d) o[d] = 0.0;
+                    for (int j = 0; j < N; ++j)
+                        for (int d = 0; d < D; ++d) o[d] += p[j] * (double)vc[(kv * N + j) * (int64_t)D + d];
+                    double delta = 0.0;
+                    for (int d = 0; d < D; ++d) delta += (double)dov[d] * o[d];
+                    double* gq = dqc + row * D;
+                    for (int d = 0; d < D; ++d) gq[d] = 0.0;
+                    for (int j = 0; j < N; ++j) {
+                        const float* kj = kc + (kv * N + j) * (int64_t)D;
+                        const float* vj = vc + (kv * N + j) * (int64_t)D;
+                        double dp = 0.0;
+                        for (int d = 0; d < D; ++d) dp += (double)dov[d] * (double)vj[d];
+                        const double ds = p[j] * (dp - delta);
+                        for (int d = 0; d < D; ++d) {
+                            gq[d] += scale * ds * (double)kj[d];
+                            gk[(int64_t)j * D + d] += scale * ds * (double)qv[d];
+                            gv[(int64_t)j * D + d] += p[j] * (double)dov[d];
+                        }
+                    }
+                }
+            }
+        }
+        free(p);
+        free(o);
+    }
+}
+
+/* ---------------------------------------------------------------------- */
+/* Gated merge (Sec. 2.2 "Gated Merge", Eq. gate_linear and the merge      */
+/* after it): G = tanh(X W_g), one gate per token and head; O = G * O_c +  */
+/* O_f with O_c = Repeat_B(O_c_hat).  g holds the pre-activations X W_g.   */
+/* ---------------------------------------------------------------------- */
+
+/* g: [nbh][L]; oc: [nbh][N][D]; of, out: [nbh][L][D]; token l is in cube l / B. */
+void vo_gate_merge(const float* g, const float* oc, const float* of, int64_t nbh, int N, int B,
+                   int D, double* out)
+{
+    const int64_t L = (int64_t)N * B;
+#pragma omp parallel for schedule(static)
+    for (int64_t bh = 0; bh < nbh; ++bh)
+        for (int64_t l = 0; l < L; ++l) {
+            const double gate = tanh((double)g[bh * L + l]);
+            const float* c = oc + (bh * N + l / B) * (int64_t)D;
+            const float* f = of + (bh * L + l) * (int64_t)D;
+            double* o = out + (bh * L + l) * (int64_t)D;
+            for (int d = 0; d < D; ++d) o[d] = gate * (double)c[d] + (double)f[d];
+        }
+}
+
+/* Gradients of vo_gate_merge for dout ([nbh][L][D]):
+ *   doc[n] = sum over the B tokens l of cube n of tanh(g_l) dout_l,
+ *   dg_l = (1 - tanh(g_l)^2) (dout_l . oc[n(l)]);  d(O_f) = dout. */
+void vo_gate_merge_bwd(const float* g, const float* oc, const float* dout, int64_t nbh, int N,
+                       int B, int D, double* doc, double* dg)
+{
+    const int64_t L = (int64_t)N * B;
+#pragma omp parallel for schedule(static)
+    for (int64_t bh = 0; bh < nbh; ++bh)
+        for (int64_t n = 0; n < N; ++n) {
+            double* dc = doc + (bh * N + n) * (int64_t)D;
+            const float* c = oc + (bh * N + n) * (int64_t)D;
+            for (int d = 0; d < D; ++d) dc[d] = 0.0;
+            for (int t = 0; t < B; ++t) {
+                const int64_t l = n * B + t;
+                const double gate = tanh((double)g[bh * L + l]);
+                const float* dl = dout + (bh * L + l) * (int64_t)D;
+                double dot = 0.0;
+                for (int d = 0; d < D; ++d) {
+                    dc[d] += gate * (double)dl[d];
+                    dot += (double)dl[d] * (double)c[d];
+                }
+                dg[bh * L + l] = (1.0 - gate * gate) * dot;
+            }
+        }
+}
+
+/* The adjoint of vo_pool (the gradient of MeanPool over (Pt, Ph, Pw)):
+ * every token of sub-cube (n, g) receives dxc[n*Gp + g] / P, added to dx.
+ * dxc: [nbh][N*Gp][D]; dx: [nbh][N*B][D]. */
+void vo_unpool_add(const double* dxc, int64_t nbh, int T, int H, int W, int Bt, int Bh, int Bw,
+                   int Pt, int Ph, int Pw, int D, double* dx)
+{
+    const int Nt = T / Bt, Nh = H / Bh, Nw = W / Bw;
+    const int64_t N = (int64_t)Nt * Nh * Nw;
+    const int B = Bt * Bh * Bw;
+    const int Gt = Bt / Pt, Gh = Bh / Ph, Gw = Bw / Pw;
+    const int G = Gt * Gh * Gw;
+    const double P = (double)(Pt * Ph * Pw);
+#pragma omp parallel for schedule(static)
+    for (int64_t bh = 0; bh < nbh; ++bh)
+        for (int64_t n = 0; n < N; ++n)
+            for (int bt = 0; bt < Bt; ++bt)
+            for (int bhh = 0; bhh < Bh; ++bhh)
+            for (int bw = 0; bw < Bw; ++bw) {
+                const int g = ((bt / Pt) * Gh + bhh / Ph) * Gw + bw / Pw;
+                const int beta = (bt * Bh + bhh) * Bw + bw;
+                const double* src = dxc + ((bh * N + n) * G + g) * (int64_t)D;
+                double* dst = dx + ((bh * N + n) * B + beta) * (int64_t)D;
+                for (int d = 0; d < D; ++d) dst[d] += src[d] / P;
+            }
+}

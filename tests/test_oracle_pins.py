@@ -428,3 +428,142 @@ def test_mass_threshold_reached_exactly():
     assert idx[0, :2].tolist() == [0, 1] and idx[1, :2].tolist() == [2, 3]
     counts, _ = oracle.select_rows(s, Selection(1, 0, 0.875, 10))
     assert counts.tolist() == [3, 3]
+
+
+# ---------------------------------------------------------------- coarse branch, gated merge
+
+def _torch_coarse(qc, kc, vc, doc=None):
+    """Dense softmax attention over the cube means with torch in float64,
+    KV heads repeated over their query-head group."""
+    grp = qc.shape[1] // kc.shape[1]
+    tq = torch.tensor(qc, dtype=torch.float64, requires_grad=doc is not None)
+    tk = torch.tensor(kc, dtype=torch.float64, requires_grad=doc is not None)
+    tv = torch.tensor(vc, dtype=torch.float64, requires_grad=doc is not None)
+    kk = tk.repeat_interleave(grp, dim=1)
+    vv = tv.repeat_interleave(grp, dim=1)
+    s = tq @ kk.transpose(-1, -2) / math.sqrt(qc.shape[-1])
+    o = torch.softmax(s, -1) @ vv
+    lse = torch.logsumexp(s, -1)
+    grads = None
+    if doc is not None:
+        (o * torch.tensor(doc, dtype=torch.float64)).sum().backward()
+        grads = (tq.grad.numpy(), tk.grad.numpy(), tv.grad.numpy())
+    return o.detach().numpy(), lse.detach().numpy(), grads
+
+
+@pytest.mark.parametrize("hq,hkv", [(2, 2), (4, 2)])
+def test_coarse_branch_matches_torch(hq, hkv):
+    """Coarse branch (Sec. 2.2, Eq. compress ff.): forward and gradients
+    against torch float64 softmax attention and autograd, GQA included."""
+    p = small(T=4, H=8, W=12, Bt=2, Bh=2, Bw=2, hq=hq, hkv=hkv, D=16)   # N = 48 cubes
+    rng = np.random.default_rng(40)
+    qc = rng.standard_normal((1, hq, p.N, p.head_dim)).astype(np.float32)
+    kc = rng.standard_normal((1, hkv, p.N, p.head_dim)).astype(np.float32)
+    vc = rng.standard_normal((1, hkv, p.N, p.head_dim)).astype(np.float32)
+    doc = rng.standard_normal((1, hq, p.N, p.head_dim)).astype(np.float32)
+    oc, lse = oracle.coarse_fwd(qc, kc, vc, p)
+    ref, lref, (gq, gk, gv) = _torch_coarse(qc, kc, vc, doc)
+    np.testing.assert_allclose(oc, ref, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(lse, lref, rtol=1e-13)
+    dqc, dkc, dvc = oracle.coarse_bwd(qc, kc, vc, doc, p)
+    np.testing.assert_allclose(dqc, gq, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dkc, gk, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dvc, gv, rtol=1e-10, atol=1e-12)
+
+
+def test_gate_merge_matches_torch_autograd():
+    """O = tanh(g) * Repeat_B(O_c_hat) + O_f and its gradients (d O_c_hat
+    sums the gated output gradient over each cube's B tokens)."""
+    p = small(T=2, H=8, W=8, Bt=2, Bh=2, Bw=4, hq=3, hkv=3, D=8)
+    rng = np.random.default_rng(41)
+    g = (rng.standard_normal((1, 3, p.L)) * 2).astype(np.float32)
+    oc = rng.standard_normal((1, 3, p.N, p.head_dim)).astype(np.float32)
+    of = rng.standard_normal((1, 3, p.L, p.head_dim)).astype(np.float32)
+    dout = rng.standard_normal((1, 3, p.L, p.head_dim)).astype(np.float32)
+    out = oracle.gate_merge(g, oc, of, p)
+    tg = torch.tensor(g, dtype=torch.float64, requires_grad=True)
+    toc = torch.tensor(oc, dtype=torch.float64, requires_grad=True)
+    tof = torch.tensor(of, dtype=torch.float64, requires_grad=True)
+    ref = torch.tanh(tg)[..., None] * toc.repeat_interleave(p.B, dim=2) + tof
+    np.testing.assert_allclose(out, ref.detach().numpy(), rtol=1e-14, atol=1e-14)
+    (ref * torch.tensor(dout, dtype=torch.float64)).sum().backward()
+    doc, dg = oracle.gate_merge_bwd(g, oc, dout, p)
+    np.testing.assert_allclose(doc, toc.grad.numpy(), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(dg, tg.grad.numpy(), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(tof.grad.numpy(), dout)      # d O_f = dout
+    # zero gate weights (the paper's initialisation) leave only O_f
+    np.testing.assert_array_equal(oracle.gate_merge(np.zeros_like(g), oc, of, p), of.astype(np.float64))
+
+
+@pytest.mark.parametrize("P", [(2, 2, 2), (1, 2, 4), (2, 4, 4)])
+def test_unpool_is_the_adjoint_of_pool(P):
+    """<MeanPool(x), y> = <x, Unpool(y)>, and MeanPool(Unpool(y)) = y / P."""
+    p = small(T=4, H=8, W=8, Bt=2, Bh=4, Bw=4, hq=2, hkv=2, D=8)
+    Pt, Ph, Pw = P
+    Gp = (p.Bt // Pt) * (p.Bh // Ph) * (p.Bw // Pw)
+    rng = np.random.default_rng(42)
+    # values on a 2^-12 grid: every pooled mean is exact in float32
+    x = (rng.integers(-4096, 4096, (1, 2, p.L, p.head_dim)) / 4096.0).astype(np.float32)
+    y = rng.standard_normal((1, 2, p.N * Gp, p.head_dim))
+    px = oracle.pool(x, p, Pt, Ph, Pw).astype(np.float64)
+    ux = oracle.unpool_add(y, np.zeros((1, 2, p.L, p.head_dim)), p, Pt, Ph, Pw)
+    np.testing.assert_allclose((px * y).sum(), (x.astype(np.float64) * ux).sum(), rtol=1e-12)
+    ones = (rng.integers(-64, 64, y.shape) / 8.0)
+    back = oracle.pool(oracle.unpool_add(ones, np.zeros((1, 2, p.L, p.head_dim)), p, Pt, Ph, Pw)
+                       .astype(np.float32), p, Pt, Ph, Pw)
+    np.testing.assert_array_equal(back.astype(np.float64), ones / (Pt * Ph * Pw))
+
+
+def test_full_op_gradient_finite_differences():
+    """The whole VSA2 attention op O = tanh(g) Repeat_B(Attn(Pool_B Q, Pool_B K,
+    Pool_B V)) + BlockSparseAttn(Q, K, V; M): gradients composed from the
+    oracle's steps (merge, coarse and fine backward, unpool) against central
+    differences of sum(W * O)."""
+    p = Problem(1, 2, 1, 8, 2, 4, 4, 2, 2, 2, 1, 1, 2, F32)    # N = 4 cubes of B = 8
+    rng = np.random.default_rng(43)
+    grid = lambda shape: (rng.integers(-1024, 1024, shape) / 1024.0).astype(np.float32)
+    q = grid((1, 2, p.L, p.head_dim))
+    k = grid((1, 1, p.L, p.head_dim))
+    v = grid((1, 1, p.L, p.head_dim))
+    g = grid((1, 2, p.L))
+    W = rng.standard_normal((1, 2, p.L, p.head_dim)).astype(np.float32).astype(np.float64)
+    rp, ci = _random_csr(p, 44)
+    Bt, Bh, Bw = p.Bt, p.Bh, p.Bw
+
+    def forward(qq, kk, vv, gg):
+        # float64 end to end (the oracle's merge takes float inputs, whose
+        # rounding would swamp the differences; the merge itself is pinned
+        # against torch above)
+        of, _ = oracle.attn_fwd(qq, kk, vv, p, rp, ci)
+        oc, _ = oracle.coarse_fwd(oracle.pool(qq, p, Bt, Bh, Bw), oracle.pool(kk, p, Bt, Bh, Bw),
+                                  oracle.pool(vv, p, Bt, Bh, Bw), p)
+        gate = np.tanh(gg.astype(np.float64))[..., None]
+        return gate * np.repeat(oc, p.B, axis=2) + of.reshape(qq.shape)
+
+    def loss(*a):
+        return float((forward(*a) * W).sum())
+
+    # analytic gradient, step by step
+    oc, _ = oracle.coarse_fwd(oracle.pool(q, p, Bt, Bh, Bw), oracle.pool(k, p, Bt, Bh, Bw),
+                              oracle.pool(v, p, Bt, Bh, Bw), p)
+    doc, dg = oracle.gate_merge_bwd(g, oc, W, p)
+    dqc, dkc, dvc = oracle.coarse_bwd(oracle.pool(q, p, Bt, Bh, Bw), oracle.pool(k, p, Bt, Bh, Bw),
+                                      oracle.pool(v, p, Bt, Bh, Bw), doc, p)
+    dq = oracle.attn_bwd_dq(q, k, v, W, p, rp, ci).reshape(q.shape)
+    dk, dv = oracle.attn_bwd_dkdv(q, k, v, W, p, rp, ci)
+    dk, dv = dk.reshape(k.shape).copy(), dv.reshape(v.shape).copy()
+    oracle.unpool_add(dqc, dq, p, Bt, Bh, Bw)
+    oracle.unpool_add(dkc, dk, p, Bt, Bh, Bw)
+    oracle.unpool_add(dvc, dv, p, Bt, Bh, Bw)
+    h = 2.0 ** -10
+    for name, t, gr in (("q", q, dq), ("k", k, dk), ("v", v, dv), ("g", g, dg)):
+        for flat in rng.choice(t.size, 10, replace=False):
+            args = {"q": q, "k": k, "v": v, "g": g}
+            tp, tm = t.copy(), t.copy()
+            tp.flat[flat] += np.float32(h)
+            tm.flat[flat] -= np.float32(h)
+            lp = loss(*[tp if n == name else args[n] for n in ("q", "k", "v", "g")])
+            lm = loss(*[tm if n == name else args[n] for n in ("q", "k", "v", "g")])
+            fd = (lp - lm) / (2 * h)
+            assert abs(fd - gr.flat[flat]) <= 2e-5 * max(1.0, abs(gr).max()), (name, flat, fd,
+                                                                                gr.flat[flat])
