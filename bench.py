@@ -42,6 +42,8 @@ def parse():
                     help="query-block rows (forward + dQ) in the oracle's timed sample")
     ap.add_argument("--cpu-kv", type=int, default=24,
                     help="key blocks (dK/dV) in the oracle's timed sample")
+    ap.add_argument("--no-coarse", action="store_true",
+                    help="skip the separate timing of the coarse branch and gated merge")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, copy a buffer of this size once (reference kernel "
                          "for scaling hardware byte counters)")
@@ -152,6 +154,9 @@ def main():
     ms_step = wall * 1e3 / args.steps
     stage_ms = {s: float(np.mean([a.elapsed_time(b) for a, b in ev[s]])) for s in stages}
 
+    coarse = None if args.no_coarse else time_coarse_branch(vsa2, torch, p, q, k, v, do, o, dq, dk, dv,
+                                                            stream, max(args.steps, 3))
+
     if args.calib_copy_mib:
         n = args.calib_copy_mib << 20
         src = torch.empty(n, dtype=torch.uint8, device=dev)
@@ -204,9 +209,74 @@ def main():
         },
         "input_gen_s": round(gen_s, 1),
     }
+    if coarse:
+        out["coarse_branch_ms"] = coarse
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, x, row_ptr, col_idx, args.cpu_rows, args.cpu_kv)
     print(json.dumps(out), flush=True)
+
+
+def time_coarse_branch(vsa2, torch, p, q, k, v, do, o_f, dq, dk, dv, stream, reps):
+    """The coarse branch and the gated merge (outside the fine path's step
+    and its value): MeanPool_B of Q, K, V, dense attention among the cube
+    means, tanh-gated merge, and their backward with the MeanPool adjoint
+    added onto the token gradients.  Mean ms per stage over `reps` runs."""
+    P = vsa2.problem_from(p)
+    N, D = p.N, p.head_dim
+    dev = q.device
+    tdt = q.dtype
+    Bc = (p.Bt, p.Bh, p.Bw)
+    qc = torch.empty((p.batch, p.heads_q, N, D), dtype=tdt, device=dev)
+    kc = torch.empty((p.batch, p.heads_kv, N, D), dtype=tdt, device=dev)
+    vc = torch.empty_like(kc)
+    oc = torch.empty_like(qc)
+    lse_c = torch.empty((p.batch, p.heads_q, N), dtype=torch.float32, device=dev)
+    gate = torch.randn((p.batch, p.heads_q, p.L), generator=torch.Generator(device=dev).manual_seed(9),
+                       device=dev, dtype=torch.float32)
+    merged = torch.empty_like(o_f)
+    doc, dgate = torch.empty_like(qc), torch.empty_like(gate)
+    dqc, dkc, dvc = torch.empty_like(qc), torch.empty_like(kc), torch.empty_like(vc)
+    st, wsb = vsa2.vsa2_attn_workspace(P, 2)
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    sp = stream.cuda_stream
+    names = ("pool_qkv", "coarse_fwd", "merge_fwd", "merge_bwd", "coarse_bwd", "unpool_add")
+
+    def run(e):
+        def mark(i):
+            if e is not None:
+                e[i].record(stream)
+        mark(0)
+        for src, dst, hh in ((q, qc, p.heads_q), (k, kc, p.heads_kv), (v, vc, p.heads_kv)):
+            assert vsa2.vsa2_pool(P, hh, src.data_ptr(), *Bc, dst.data_ptr(), sp) == 0
+        mark(1)
+        assert vsa2.vsa2_coarse_fwd(P, qc.data_ptr(), kc.data_ptr(), vc.data_ptr(), oc.data_ptr(),
+                                    lse_c.data_ptr(), sp) == 0
+        mark(2)
+        assert vsa2.vsa2_gate_merge(P, gate.data_ptr(), oc.data_ptr(), o_f.data_ptr(), merged.data_ptr(),
+                                    sp) == 0
+        mark(3)
+        assert vsa2.vsa2_gate_merge_bwd(P, gate.data_ptr(), oc.data_ptr(), do.data_ptr(), doc.data_ptr(),
+                                        dgate.data_ptr(), sp) == 0
+        mark(4)
+        assert vsa2.vsa2_coarse_bwd(P, qc.data_ptr(), kc.data_ptr(), vc.data_ptr(), doc.data_ptr(),
+                                    dqc.data_ptr(), dkc.data_ptr(), dvc.data_ptr(), ws.data_ptr(), wsb,
+                                    sp) == 0
+        mark(5)
+        for src, dst, hh in ((dqc, dq, p.heads_q), (dkc, dk, p.heads_kv), (dvc, dv, p.heads_kv)):
+            assert vsa2.vsa2_unpool_add(P, hh, src.data_ptr(), *Bc, dst.data_ptr(), sp) == 0
+        mark(6)
+
+    run(None)
+    torch.cuda.synchronize()
+    acc = np.zeros(len(names))
+    for _ in range(reps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
+        run(e)
+        torch.cuda.synchronize()
+        acc += [e[i].elapsed_time(e[i + 1]) for i in range(len(names))]
+    res = {n: round(float(a / reps), 4) for n, a in zip(names, acc)}
+    res["total"] = round(float(acc.sum() / reps), 4)
+    return res
 
 
 # HBM bytes per launch of the dK/dV kernel, from the hardware byte counters

@@ -164,8 +164,9 @@ vsa2_status vsa2_route(const vsa2_problem* p, const vsa2_select* s,
                        float* block_scores, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Bytes of workspace vsa2_attn_fwd (pass 0: the work order, one int32 per
- * CSR row) or vsa2_attn_bwd (pass 1: one fp32 (LSE, Delta) pair per query
- * token, then the work orders of the CSR and CSC rows) needs.  The work
+ * CSR row), vsa2_attn_bwd (pass 1: one fp32 (LSE, Delta) pair per query
+ * token, then the work orders of the CSR and CSC rows) or vsa2_coarse_bwd
+ * (pass 2: one fp32 pair per coarse query) needs.  The work
  * order lists the rows of each XCD's range longest first (a stable
  * counting sort by length class), so the launch's last workgroups are
  * short ones; rows of equal length keep their order. */
@@ -258,6 +259,66 @@ vsa2_status vsa2_attn_bwd_dkdv(const vsa2_problem* p, const void* q, const void*
 vsa2_status vsa2_attn_bwd_dq(const vsa2_problem* p, const void* q, const void* k, const void* v,
                              const void* dout, const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
                              int32_t compensated, void* dq, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Coarse branch and gated merge (Sec. 2.2, "Coarse Branch" and "Gated
+ * Merge").  With [Q_c, K_c, V_c] = MeanPool_B([Q, K, V]) (vsa2_pool with
+ * P = B, one row per cube):
+ *   O_c_hat = Softmax(Q_c K_c^T / sqrt(D)) V_c       (dense over the N cubes)
+ *   O = tanh(g) * Repeat_B(O_c_hat) + O_f            (O_f from vsa2_attn_fwd)
+ * where g = X W_g holds one gate pre-activation per token and query head.
+ * The gradients: vsa2_gate_merge_bwd gives dO_c_hat and dg (dO_f is dO
+ * itself), vsa2_coarse_bwd gives dQ_c, dK_c, dV_c, and vsa2_unpool_add adds
+ * the MeanPool adjoint of those onto the token gradients dQ, dK, dV.
+ *
+ * vsa2_coarse_fwd
+ *   q_c [batch][Hq][N][D], k_c, v_c [batch][Hkv][N][D]  (dtype p->dtype)
+ *   o_c [batch][Hq][N][D] output O_c_hat; lse_c [batch][Hq][N] fp32
+ *   natural-log log-sum-exp of each coarse query's scaled scores.  Query head
+ *   h reads KV head h / (Hq/Hkv).
+ * Errors: NULL pointers, shape/dtype, misalignment, batch*Hq > 65535.
+ */
+vsa2_status vsa2_coarse_fwd(const vsa2_problem* p, const void* q_c, const void* k_c, const void* v_c, void* o_c,
+                            float* lse_c, hipStream_t stream);
+
+/*
+ * vsa2_coarse_bwd - gradients of vsa2_coarse_fwd for do_c = dO_c_hat:
+ *   dq_c [batch][Hq][N][D], dk_c, dv_c [batch][Hkv][N][D] outputs (dk_c and
+ *   dv_c summed over the query heads of each KV group).  The softmax
+ *   statistics are recomputed (one more pass over the N x N scores) with P
+ *   and dS entering the products as two bf16 terms each: the cube means are
+ *   dominated by their common component, which amplifies one-term rounding.
+ *   ws, ws_bytes  vsa2_attn_workspace(p, 2) bytes, 256-byte aligned.
+ */
+vsa2_status vsa2_coarse_bwd(const vsa2_problem* p, const void* q_c, const void* k_c, const void* v_c,
+                            const void* do_c, void* dq_c, void* dk_c, void* dv_c, void* ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+/*
+ * vsa2_gate_merge - out[l] = tanh(gate[l]) * o_c[cube of l] + o_f[l].
+ *   gate [batch][Hq][L] fp32 pre-activations; o_c [batch][Hq][N][D];
+ *   o_f, out [batch][Hq][L][D] (out may alias o_f).
+ */
+vsa2_status vsa2_gate_merge(const vsa2_problem* p, const float* gate, const void* o_c, const void* o_f, void* out,
+                            hipStream_t stream);
+
+/*
+ * vsa2_gate_merge_bwd - for dout = dO:
+ *   do_c [batch][Hq][N][D] = sum over the B tokens l of each cube of
+ *        tanh(gate[l]) dout[l];
+ *   dgate [batch][Hq][L] fp32 = (1 - tanh(gate[l])^2) (dout[l] . o_c[cube]).
+ */
+vsa2_status vsa2_gate_merge_bwd(const vsa2_problem* p, const float* gate, const void* o_c, const void* dout,
+                                void* do_c, float* dgate, hipStream_t stream);
+
+/*
+ * vsa2_unpool_add - the MeanPool adjoint (gradient of vsa2_pool with the
+ * same Pt, Ph, Pw): every token of sub-cube (n, g) gets dx_c[n*Gp + g] /
+ * (Pt*Ph*Pw) added, in place.
+ *   dx_c [batch][heads][N*Gp][D]; dx [batch][heads][L][D] (updated).
+ */
+vsa2_status vsa2_unpool_add(const vsa2_problem* p, int32_t heads, const void* dx_c, int32_t Pt, int32_t Ph,
+                            int32_t Pw, void* dx, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -28,7 +28,9 @@ VSA2_SEL_TOPK, VSA2_SEL_MASS, VSA2_SEL_SEQ_TOPK = 0, 1, 2
 # Every symbol include/vsa2.h declares.
 EXPORTS = ("vsa2_status_str", "vsa2_pool", "vsa2_route_capacity", "vsa2_route_workspace",
            "vsa2_route", "vsa2_attn_workspace", "vsa2_attn_fwd", "vsa2_attn_bwd",
-           "vsa2_attn_bwd_prep", "vsa2_attn_bwd_dkdv", "vsa2_attn_bwd_dq")
+           "vsa2_attn_bwd_prep", "vsa2_attn_bwd_dkdv", "vsa2_attn_bwd_dq",
+           "vsa2_coarse_fwd", "vsa2_coarse_bwd", "vsa2_gate_merge", "vsa2_gate_merge_bwd",
+           "vsa2_unpool_add")
 
 
 class vsa2_problem(ctypes.Structure):
@@ -73,6 +75,11 @@ def _lib():
         L.vsa2_attn_bwd_prep.argtypes = [pp, P, P, P, P, P, sz, P]
         L.vsa2_attn_bwd_dkdv.argtypes = [pp, P, P, P, P, P, P, i64, i32, P, P, P, sz, P]
         L.vsa2_attn_bwd_dq.argtypes = [pp, P, P, P, P, P, P, i64, i32, P, P, sz, P]
+        L.vsa2_coarse_fwd.argtypes = [pp, P, P, P, P, P, P]
+        L.vsa2_coarse_bwd.argtypes = [pp, P, P, P, P, P, P, P, P, sz, P]
+        L.vsa2_gate_merge.argtypes = [pp, P, P, P, P, P]
+        L.vsa2_gate_merge_bwd.argtypes = [pp, P, P, P, P, P, P]
+        L.vsa2_unpool_add.argtypes = [pp, i32, P, i32, i32, i32, P, P]
         for n in EXPORTS[1:]:
             getattr(L, n).restype = ctypes.c_int
         _L = L
@@ -154,6 +161,26 @@ def vsa2_attn_bwd_dq(p, q, k, v, dout, row_ptr, col_idx, col_cap, compensated, d
                      stream=0):
     return _lib().vsa2_attn_bwd_dq(_ref(p), q, k, v, dout, row_ptr, col_idx, col_cap,
                                    int(compensated), dq, ws, ws_bytes, stream)
+
+
+def vsa2_coarse_fwd(p, q_c, k_c, v_c, o_c, lse_c, stream=0):
+    return _lib().vsa2_coarse_fwd(_ref(p), q_c, k_c, v_c, o_c, lse_c, stream)
+
+
+def vsa2_coarse_bwd(p, q_c, k_c, v_c, do_c, dq_c, dk_c, dv_c, ws, ws_bytes, stream=0):
+    return _lib().vsa2_coarse_bwd(_ref(p), q_c, k_c, v_c, do_c, dq_c, dk_c, dv_c, ws, ws_bytes, stream)
+
+
+def vsa2_gate_merge(p, gate, o_c, o_f, out, stream=0):
+    return _lib().vsa2_gate_merge(_ref(p), gate, o_c, o_f, out, stream)
+
+
+def vsa2_gate_merge_bwd(p, gate, o_c, dout, do_c, dgate, stream=0):
+    return _lib().vsa2_gate_merge_bwd(_ref(p), gate, o_c, dout, do_c, dgate, stream)
+
+
+def vsa2_unpool_add(p, heads, dx_c, Pt, Ph, Pw, dx, stream=0):
+    return _lib().vsa2_unpool_add(_ref(p), heads, dx_c, Pt, Ph, Pw, dx, stream)
 
 
 # --------------------------------------------------------------------------
@@ -342,3 +369,59 @@ def attn_bwd_staged(p, q, k, v, o, lse, do, row_ptr, col_idx, kv_ptr, kv_idx, co
     if marks:
         marks[3].record()
     return dq, dk, dv
+
+
+def coarse_fwd(p, q_c, k_c, v_c):
+    """O_c_hat [b, Hq, N, D] and LSE [b, Hq, N] of the coarse branch."""
+    torch = _torch()
+    p = problem_from(p)
+    N, _, _ = _dims(p)
+    o_c = torch.empty((p.batch, p.heads_q, N, p.head_dim), dtype=q_c.dtype, device=q_c.device)
+    lse = torch.empty((p.batch, p.heads_q, N), dtype=torch.float32, device=q_c.device)
+    _check("vsa2_coarse_fwd", vsa2_coarse_fwd(p, q_c.data_ptr(), k_c.data_ptr(), v_c.data_ptr(),
+                                              o_c.data_ptr(), lse.data_ptr(), _stream()))
+    return o_c, lse
+
+
+def coarse_bwd(p, q_c, k_c, v_c, do_c):
+    """(dq_c, dk_c, dv_c) of the coarse branch for do_c."""
+    torch = _torch()
+    p = problem_from(p)
+    st, wsb = vsa2_attn_workspace(p, 2)
+    _check("vsa2_attn_workspace", st)
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q_c.device)
+    dq, dk, dv = torch.empty_like(q_c), torch.empty_like(k_c), torch.empty_like(v_c)
+    _check("vsa2_coarse_bwd", vsa2_coarse_bwd(p, q_c.data_ptr(), k_c.data_ptr(), v_c.data_ptr(),
+                                              do_c.data_ptr(), dq.data_ptr(), dk.data_ptr(),
+                                              dv.data_ptr(), ws.data_ptr(), wsb, _stream()))
+    return dq, dk, dv
+
+
+def gate_merge(p, gate, o_c, o_f, out=None):
+    """O = tanh(gate) * Repeat_B(o_c) + o_f."""
+    torch = _torch()
+    p = problem_from(p)
+    out = torch.empty_like(o_f) if out is None else out
+    _check("vsa2_gate_merge", vsa2_gate_merge(p, gate.data_ptr(), o_c.data_ptr(), o_f.data_ptr(),
+                                              out.data_ptr(), _stream()))
+    return out
+
+
+def gate_merge_bwd(p, gate, o_c, dout):
+    """(do_c, dgate) of the merge for dout."""
+    torch = _torch()
+    p = problem_from(p)
+    do_c = torch.empty_like(o_c)
+    dgate = torch.empty_like(gate)
+    _check("vsa2_gate_merge_bwd", vsa2_gate_merge_bwd(p, gate.data_ptr(), o_c.data_ptr(),
+                                                      dout.data_ptr(), do_c.data_ptr(),
+                                                      dgate.data_ptr(), _stream()))
+    return do_c, dgate
+
+
+def unpool_add(p, dx_c, dx, P):
+    """dx += MeanPool adjoint of dx_c over P = (Pt, Ph, Pw), in place."""
+    p = problem_from(p)
+    _check("vsa2_unpool_add", vsa2_unpool_add(p, dx.shape[1], dx_c.data_ptr(), P[0], P[1], P[2],
+                                              dx.data_ptr(), _stream()))
+    return dx

@@ -214,6 +214,7 @@ vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* byt
     if (!bytes) return VSA2_ERR_NULL;
     if (pass == 0) *bytes = fwd_ws_bytes(s, p);
     else if (pass == 1) *bytes = bwd_ws_bytes(s, p);
+    else if (pass == 2) *bytes = align_up(8 * static_cast<size_t>(s.rows_q));   // coarse backward
     else return VSA2_ERR_SHAPE;
     return VSA2_OK;
 }
@@ -319,6 +320,81 @@ vsa2_status vsa2_attn_bwd_dq(const vsa2_problem* p, const void* q, const void* k
     VSA2_TRY_HIP(vsa2::launch_attn_bwd_dq(p->dtype, p->head_dim, compensated != 0, q, k, v, dout, row_ptr,
                                           col_idx, col_cap, dq, ws, p->batch, p->heads_q, p->heads_kv,
                                           static_cast<int>(s.N), stream));
+    return VSA2_OK;
+}
+
+vsa2_status vsa2_coarse_fwd(const vsa2_problem* p, const void* q_c, const void* k_c, const void* v_c, void* o_c,
+                            float* lse_c, hipStream_t stream) {
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if ((st = check_kernel_shape(p, s)) != VSA2_OK) return st;
+    if (!q_c || !k_c || !v_c || !o_c || !lse_c) return VSA2_ERR_NULL;
+    if (!aligned16(q_c) || !aligned16(k_c) || !aligned16(v_c) || !aligned16(o_c)) return VSA2_ERR_ALIGN;
+    if (p->batch * static_cast<int64_t>(p->heads_q) > 65535) return VSA2_ERR_UNSUPPORTED;
+    VSA2_TRY_HIP(vsa2::launch_coarse_fwd(p->dtype, p->head_dim, q_c, k_c, v_c, o_c, lse_c, p->batch, p->heads_q,
+                                         p->heads_kv, static_cast<int>(s.N), stream));
+    return VSA2_OK;
+}
+
+vsa2_status vsa2_coarse_bwd(const vsa2_problem* p, const void* q_c, const void* k_c, const void* v_c,
+                            const void* do_c, void* dq_c, void* dk_c, void* dv_c, void* ws, size_t ws_bytes,
+                            hipStream_t stream) {
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if ((st = check_kernel_shape(p, s)) != VSA2_OK) return st;
+    if (!q_c || !k_c || !v_c || !do_c || !dq_c || !dk_c || !dv_c) return VSA2_ERR_NULL;
+    if (!aligned16(q_c) || !aligned16(k_c) || !aligned16(v_c) || !aligned16(do_c) ||
+        !aligned16(dq_c) || !aligned16(dk_c) || !aligned16(dv_c))
+        return VSA2_ERR_ALIGN;
+    if (!ws || ws_bytes < align_up(8 * static_cast<size_t>(s.rows_q))) return VSA2_ERR_WORKSPACE;
+    if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
+    if (p->batch * static_cast<int64_t>(p->heads_q) > 65535) return VSA2_ERR_UNSUPPORTED;
+    VSA2_TRY_HIP(vsa2::launch_coarse_bwd(p->dtype, p->head_dim, q_c, k_c, v_c, do_c, dq_c, dk_c, dv_c, ws,
+                                         p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N), stream));
+    return VSA2_OK;
+}
+
+vsa2_status vsa2_gate_merge(const vsa2_problem* p, const float* gate, const void* o_c, const void* o_f, void* out,
+                            hipStream_t stream) {
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if ((st = check_kernel_shape(p, s)) != VSA2_OK) return st;
+    if (!gate || !o_c || !o_f || !out) return VSA2_ERR_NULL;
+    if (!aligned16(o_c) || !aligned16(o_f) || !aligned16(out)) return VSA2_ERR_ALIGN;
+    VSA2_TRY_HIP(vsa2::launch_gate_merge(p->dtype, p->head_dim, gate, o_c, o_f, out, s.rows_q * s.B,
+                                         static_cast<int>(s.B), stream));
+    return VSA2_OK;
+}
+
+vsa2_status vsa2_gate_merge_bwd(const vsa2_problem* p, const float* gate, const void* o_c, const void* dout,
+                                void* do_c, float* dgate, hipStream_t stream) {
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if ((st = check_kernel_shape(p, s)) != VSA2_OK) return st;
+    if (!gate || !o_c || !dout || !do_c || !dgate) return VSA2_ERR_NULL;
+    if (!aligned16(o_c) || !aligned16(dout) || !aligned16(do_c)) return VSA2_ERR_ALIGN;
+    VSA2_TRY_HIP(vsa2::launch_gate_merge_bwd(p->dtype, p->head_dim, gate, o_c, dout, do_c, dgate, s.rows_q,
+                                             stream));
+    return VSA2_OK;
+}
+
+vsa2_status vsa2_unpool_add(const vsa2_problem* p, int32_t heads, const void* dx_c, int32_t Pt, int32_t Ph,
+                            int32_t Pw, void* dx, hipStream_t stream) {
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if (!dx_c || !dx) return VSA2_ERR_NULL;
+    if (heads < 1 || Pt < 1 || Ph < 1 || Pw < 1) return VSA2_ERR_SHAPE;
+    if (p->Bt % Pt || p->Bh % Ph || p->Bw % Pw) return VSA2_ERR_SHAPE;
+    if (p->head_dim != 64 && p->head_dim != 128) return VSA2_ERR_UNSUPPORTED;
+    if (!aligned16(dx_c) || !aligned16(dx)) return VSA2_ERR_ALIGN;
+    VSA2_TRY_HIP(vsa2::launch_unpool_add(p->dtype, p->head_dim, dx_c, dx,
+                                         static_cast<int64_t>(p->batch) * heads * s.L, p->Bt, p->Bh, p->Bw, Pt,
+                                         Ph, Pw, stream));
     return VSA2_OK;
 }
 

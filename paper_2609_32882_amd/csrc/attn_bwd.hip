@@ -453,8 +453,7 @@ size_t bwd_workspace_bytes(int dtype, int D, int batch, int Hq, int Hkv, int N) 
 // Stage 1: per query token (LSE * log2(e), Delta) into ws.
 template <typename T, int D>
 static hipError_t launch_prep_t(const void* o, const float* lse, const void* o_lo, const void* dout, void* ws,
-                                int batch, int Hq, int N, hipStream_t s) {
-    const int64_t ntok = static_cast<int64_t>(batch) * Hq * N * 64;
+                                int64_t ntok, hipStream_t s) {
     if (ntok == 0) return hipSuccess;
     const int64_t sthreads = ntok * (D / 8);
     hipLaunchKernelGGL((stat_kernel<T, D>), dim3(static_cast<unsigned>((sthreads + 255) / 256)), dim3(256), 0,
@@ -513,9 +512,15 @@ static hipError_t launch_dq_t(const void* q, const void* k, const void* v, const
     }                                                       \
     return hipErrorInvalidValue
 
+hipError_t launch_attn_bwd_prep_tokens(int dtype, int D, const void* o, const float* lse, const void* o_lo,
+                                       const void* dout, void* ws, int64_t ntok, hipStream_t s) {
+    VSA2_DISPATCH_TD(return (launch_prep_t<T, DD>(o, lse, o_lo, dout, ws, ntok, s)));
+}
+
 hipError_t launch_attn_bwd_prep(int dtype, int D, const void* o, const float* lse, const void* o_lo,
                                 const void* dout, void* ws, int batch, int Hq, int N, hipStream_t s) {
-    VSA2_DISPATCH_TD(return (launch_prep_t<T, DD>(o, lse, o_lo, dout, ws, batch, Hq, N, s)));
+    return launch_attn_bwd_prep_tokens(dtype, D, o, lse, o_lo, dout, ws, static_cast<int64_t>(batch) * Hq * N * 64,
+                                       s);
 }
 
 hipError_t launch_attn_bwd_dkdv(int dtype, int D, bool comp, const void* q, const void* k, const void* v,

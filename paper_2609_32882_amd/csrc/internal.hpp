@@ -69,6 +69,21 @@ hipError_t launch_attn_bwd(int dtype, int D, const void* q, const void* k, const
                            int Hq, int Hkv, int N, hipStream_t s);
 hipError_t launch_attn_bwd_prep(int dtype, int D, const void* o, const float* lse, const void* o_lo,
                                 const void* dout, void* ws, int batch, int Hq, int N, hipStream_t s);
+// (LSE * log2 e, dO . O) for ntok rows of D elements.
+hipError_t launch_attn_bwd_prep_tokens(int dtype, int D, const void* o, const float* lse, const void* o_lo,
+                                       const void* dout, void* ws, int64_t ntok, hipStream_t s);
+// Coarse branch and gated merge.
+hipError_t launch_coarse_fwd(int dtype, int D, const void* qc, const void* kc, const void* vc, void* oc,
+                             float* lse, int batch, int Hq, int Hkv, int N, hipStream_t s);
+hipError_t launch_coarse_bwd(int dtype, int D, const void* qc, const void* kc, const void* vc, const void* doc,
+                             void* dqc, void* dkc, void* dvc, void* ws, int batch, int Hq, int Hkv, int N,
+                             hipStream_t s);
+hipError_t launch_gate_merge(int dtype, int D, const float* gate, const void* oc, const void* of, void* out,
+                             int64_t ntok, int B, hipStream_t s);
+hipError_t launch_gate_merge_bwd(int dtype, int D, const float* gate, const void* oc, const void* dout, void* doc,
+                                 float* dgate, int64_t ncubes, hipStream_t s);
+hipError_t launch_unpool_add(int dtype, int D, const void* dxc, void* dx, int64_t ntok, int Bt, int Bh, int Bw,
+                             int Pt, int Ph, int Pw, hipStream_t s);
 hipError_t launch_attn_bwd_dkdv(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
                                 const void* dout, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
                                 void* dk, void* dv, void* ws, int batch, int Hq, int Hkv, int N,
