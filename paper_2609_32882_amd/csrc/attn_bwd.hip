@@ -165,72 +165,90 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
         const char* ot = o_lds[buf];
         const float2* st = st_lds[buf];
         if (q_cur >= 0) {
-            // Query tiles one after the other: S / dP (8 k-steps), then P, dS,
-            // then the dV / dK products of that tile's 32 queries (2 k-steps).
-            // LDS fragments are requested one batch ahead of the products
-            // that use them (lds_order keeps the compiler from sinking them).
+            // Software pipeline over the two 32-query tiles of the block:
+            //   S/dP(tile 0) | S/dP(tile 1) + P,dS(tile 0) |
+            //   dV/dK(tile 0) + P,dS(tile 1) | dV/dK(tile 1)
+            // so the exponentials and the dS arithmetic of one tile issue
+            // while the other tile's MFMAs run (one wave per SIMD: the wave's
+            // own independent work is all there is to overlap).  LDS operand
+            // fragments are requested one step ahead of their MFMAs;
+            // lds_order keeps the compiler from moving work across steps.
+            constexpr int NB = KS / 2;           // S/dP steps per tile (2 k-steps each)
+            constexpr int NU = 2 * MT;           // dV/dK steps per tile
+            constexpr int EV = 16 / NB;          // P,dS elements per S/dP step
+            constexpr int EU = 16 / NU;          // P,dS elements per dV/dK step
+            f32x16_t s[2], dp[2];
 #pragma unroll
-            for (int qtile = 0; qtile < 2; ++qtile) {
-                const int row = qtile * 32 + (lane & 31);
-                f32x16_t s, dp;
+            for (int t = 0; t < 2; ++t)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) { s[i] = 0.f; dp[i] = 0.f; }
-                F fa[2][4];
-                auto fetch = [&](F* f, int bi) {
-                    lds_frag_s<RB>(f[0], qt, row, 32 * bi + half * 8);
-                    lds_frag_s<RB>(f[1], ot, row, 32 * bi + half * 8);
-                    lds_frag_s<RB>(f[2], qt, row, 32 * bi + 16 + half * 8);
-                    lds_frag_s<RB>(f[3], ot, row, 32 * bi + 16 + half * 8);
-                };
-                fetch(fa[0], 0);
+                for (int i = 0; i < 16; ++i) { s[t][i] = 0.f; dp[t][i] = 0.f; }
+            F pb[2][2], db[2][2], pl[2][SPLIT ? 2 : 1], dl[2][SPLIT ? 2 : 1];
+            // P and dS of elements [i0, i0 + n) of tile t, in place (s <- P,
+            // dp <- dS); element i is query 32t + 16(i/8) + 8half + i%8.
+            // A group of 8 finished elements becomes a fragment pair.
+            auto softmax_grad = [&](int t, int i0, int n) {
 #pragma unroll
-                for (int bi = 0; bi < KS / 2; ++bi) {
-                    if (bi + 1 < KS / 2) fetch(fa[(bi + 1) & 1], bi + 1);
-                    lds_order();
-                    mma(s, fa[bi & 1][0], kf[2 * bi]);
-                    mma(dp, fa[bi & 1][1], vf[2 * bi]);
-                    mma(s, fa[bi & 1][2], kf[2 * bi + 1]);
-                    mma(dp, fa[bi & 1][3], vf[2 * bi + 1]);
+                for (int i = i0; i < i0 + n; ++i) {
+                    const float2 sv = st[t * 32 + (i >> 3) * 16 + half * 8 + (i & 7)];
+                    const float pv = fast_exp2(s[t][i] * c_log2 - sv.x);
+                    s[t][i] = pv;
+                    dp[t][i] = pv * (dp[t][i] - sv.y);
                 }
-                // entry i is query 32qtile + 16(i/8) + 8half + i%8
-                float pv[16], dsv[16];
+                if (((i0 + n) & 7) == 0) {
+                    const int h = (i0 + n - 1) >> 3;
+                    float xp[8], xd[8];
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const float2 sv = st[qtile * 32 + (i >> 3) * 16 + half * 8 + (i & 7)];
-                    pv[i] = fast_exp2(s[i] * c_log2 - sv.x);
-                    dsv[i] = pv[i] * (dp[i] - sv.y);
+                    for (int i = 0; i < 8; ++i) { xp[i] = s[t][8 * h + i]; xd[i] = dp[t][8 * h + i]; }
+                    if constexpr (SPLIT) {
+                        pack_frag_hilo(pb[t][h], pl[t][SPLIT ? h : 0], xp);
+                        pack_frag_hilo(db[t][h], dl[t][SPLIT ? h : 0], xd);
+                    } else {
+                        pack_frag(pb[t][h], xp);
+                        pack_frag(db[t][h], xd);
+                    }
                 }
-                F pb[2], db[2], pl[SPLIT ? 2 : 1], dl[SPLIT ? 2 : 1];
-                if constexpr (SPLIT) {
-                    pack_frag_hilo(pb[0], pl[0], pv);
-                    pack_frag_hilo(pb[1], pl[SPLIT ? 1 : 0], pv + 8);
-                    pack_frag_hilo(db[0], dl[0], dsv);
-                    pack_frag_hilo(db[1], dl[SPLIT ? 1 : 0], dsv + 8);
-                } else {
-                    pack_frag(pb[0], pv);
-                    pack_frag(pb[1], pv + 8);
-                    pack_frag(db[0], dsv);
-                    pack_frag(db[1], dsv + 8);
-                }
-                // dV^T += dO^T P and dK^T += Q^T dS over this tile's 32 queries;
-                // dO^T and Q^T read transposed from the row-major tiles
-                F ta[2][2];
-                auto fetch_t = [&](F* f, int u) {
-                    const int kk = 2 * qtile + u / MT, mt = u % MT;
-                    lds_frag_tr<RB, true>(f[0], ot, mt * 32, kk * 16);
-                    lds_frag_tr<RB, true>(f[1], qt, mt * 32, kk * 16);
-                };
-                fetch_t(ta[0], 0);
+            };
+            F fa[2][4];
+            auto fetch_sd = [&](F* f, int t, int bi) {
+                const int row = t * 32 + (lane & 31);
+                lds_frag_s<RB>(f[0], qt, row, 32 * bi + half * 8);
+                lds_frag_s<RB>(f[1], ot, row, 32 * bi + half * 8);
+                lds_frag_s<RB>(f[2], qt, row, 32 * bi + 16 + half * 8);
+                lds_frag_s<RB>(f[3], ot, row, 32 * bi + 16 + half * 8);
+            };
+            F ta[2][2];
+            auto fetch_dk = [&](F* f, int t, int u) {
+                const int kk = 2 * t + u / MT, mt = u % MT;
+                lds_frag_tr<RB, true>(f[0], ot, mt * 32, kk * 16);
+                lds_frag_tr<RB, true>(f[1], qt, mt * 32, kk * 16);
+            };
+            // S = Q K^T and dP = dO V^T, both tiles
+            fetch_sd(fa[0], 0, 0);
 #pragma unroll
-                for (int u = 0; u < 2 * MT; ++u) {
-                    if (u + 1 < 2 * MT) fetch_t(ta[(u + 1) & 1], u + 1);
-                    lds_order();
-                    const int h = u / MT, mt = u % MT;
-                    mma(acc_v[mt], ta[u & 1][0], pb[h]);
-                    if constexpr (SPLIT) mma(acc_v[mt], ta[u & 1][0], pl[SPLIT ? h : 0]);
-                    mma(acc_k[mt], ta[u & 1][1], db[h]);
-                    if constexpr (SPLIT) mma(acc_k[mt], ta[u & 1][1], dl[SPLIT ? h : 0]);
-                }
+            for (int k = 0; k < 2 * NB; ++k) {
+                const int t = k / NB, bi = k % NB;
+                if (k + 1 < 2 * NB) fetch_sd(fa[(k + 1) & 1], (k + 1) / NB, (k + 1) % NB);
+                else fetch_dk(ta[0], 0, 0);
+                lds_order();
+                mma(s[t], fa[k & 1][0], kf[2 * bi]);
+                mma(dp[t], fa[k & 1][1], vf[2 * bi]);
+                mma(s[t], fa[k & 1][2], kf[2 * bi + 1]);
+                mma(dp[t], fa[k & 1][3], vf[2 * bi + 1]);
+                if (t == 1) softmax_grad(0, bi * EV, EV);
+            }
+            // dV^T += dO^T P and dK^T += Q^T dS, tile by tile (dO^T and Q^T
+            // read transposed from the row-major tiles)
+#pragma unroll
+            for (int k = 0; k < 2 * NU; ++k) {
+                const int t = k / NU, u = k % NU;
+                if (k + 1 < 2 * NU) fetch_dk(ta[(k + 1) & 1], (k + 1) / NU, (k + 1) % NU);
+                lds_order();
+                const int h = u / MT, mt = u % MT;
+                mma(acc_v[mt], ta[k & 1][0], pb[t][h]);
+                if constexpr (SPLIT) mma(acc_v[mt], ta[k & 1][0], pl[t][SPLIT ? h : 0]);
+                mma(acc_k[mt], ta[k & 1][1], db[t][h]);
+                if constexpr (SPLIT) mma(acc_k[mt], ta[k & 1][1], dl[t][SPLIT ? h : 0]);
+                if (t == 0) softmax_grad(1, u * EU, EU);
             }
         }
         wg_barrier();                   // buffer `buf` free for the step after next
