@@ -81,7 +81,7 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
     constexpr int MT = D / 32;
     constexpr int RB = D * E;                    // tile row bytes
     constexpr bool SPLIT = COMP && sizeof(T) == 2;   // P and dS as hi + lo
-    using RT = async_tile<64, RB, 2, true>;      // Q, dO rows (slot-swapped)
+    using RT = async_tile<64, RB, 2, true, E == 2>;      // Q, dO rows (slot-swapped)
     __shared__ __align__(1024) char q_lds[2][RT::BYTES];
     __shared__ __align__(1024) char o_lds[2][RT::BYTES];
     __shared__ __align__(1024) float2 st_lds[2][64];
@@ -298,7 +298,7 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     constexpr int MT = D / 32;
     constexpr int RB = D * E;
     constexpr bool SPLIT = COMP && sizeof(T) == 2;   // dS as hi + lo
-    using RT = async_tile<64, RB, 2, true>;     // K, V rows (slot-swapped)
+    using RT = async_tile<64, RB, 2, true, E == 2>;     // K, V rows (slot-swapped)
     __shared__ __align__(1024) char k_lds[RT::BYTES];
     __shared__ __align__(1024) char v_lds[RT::BYTES];
 

@@ -37,7 +37,7 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     constexpr int KS = D / 16;        // macro k-steps over the head dim
     constexpr int MT = D / 32;        // 32-row tiles of O^T
     constexpr int KRB = D * E;        // K and V tile row bytes
-    using KT = async_tile<64, KRB, 2, true>;
+    using KT = async_tile<64, KRB, 2, true, E == 2>;
     using VT = KT;
     __shared__ __align__(1024) char k_lds[KT::BYTES];
     __shared__ __align__(1024) char v_lds[VT::BYTES];

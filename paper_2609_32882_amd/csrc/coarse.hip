@@ -20,8 +20,9 @@ constexpr int CB_NT = 128;   // two waves, 32 rows each
 constexpr float kLog2eC = 1.4426950408889634f;
 
 // Rows row0 .. row0+63 of a [rows][D] tensor into a padded LDS tile, LDS row r
-// holding global row row0 + swap_bits_2_3(r); rows >= nrows are zero.
-template <int RB>
+// holding global row row0 + swap_bits_2_3(r) (bf16: column groups in the
+// cgroup_pos order the fragment readers expect); rows >= nrows are zero.
+template <int RB, bool CPERM>
 __device__ __forceinline__ void load_rows_sync(char* lds, const char* g, int64_t row0, int64_t nrows, int tid) {
     constexpr int CH = RB / 16;
     for (int c = tid; c < 64 * CH; c += CB_NT) {
@@ -29,7 +30,8 @@ __device__ __forceinline__ void load_rows_sync(char* lds, const char* g, int64_t
         const int64_t gr = row0 + swap_bits_2_3(r);
         uint4 v = make_uint4(0, 0, 0, 0);
         if (gr < nrows) v = *reinterpret_cast<const uint4*>(g + gr * RB + ch * 16);
-        *reinterpret_cast<uint4*>(lds + r * (RB + 16) + ch * 16) = v;
+        const int pc = CPERM ? cgroup_pos<RB>(ch >> 1) * 32 + (ch & 1) * 16 : ch * 16;
+        *reinterpret_cast<uint4*>(lds + r * (RB + 16) + pc) = v;
     }
 }
 
@@ -88,8 +90,8 @@ __global__ __launch_bounds__(CB_NT) void coarse_fwd_kernel(const T* __restrict__
     const int ntiles = (N + 63) / 64;
     for (int kt = 0; kt < ntiles; ++kt) {
         __syncthreads();                  // previous tile's readers are done
-        load_rows_sync<RB>(k_lds, kb, static_cast<int64_t>(kt) * 64, N, tid);
-        load_rows_sync<RB>(v_lds, vb, static_cast<int64_t>(kt) * 64, N, tid);
+        load_rows_sync<RB, E == 2>(k_lds, kb, static_cast<int64_t>(kt) * 64, N, tid);
+        load_rows_sync<RB, E == 2>(v_lds, vb, static_cast<int64_t>(kt) * 64, N, tid);
         __syncthreads();
         f32x16_t s[2];
 #pragma unroll
@@ -228,8 +230,8 @@ __global__ __launch_bounds__(CB_NT) void coarse_dkdv_kernel(const T* __restrict_
         const char* ob = reinterpret_cast<const char*>(doc + bh * N * D);
         for (int qt = 0; qt < ntiles; ++qt) {
             __syncthreads();
-            load_rows_sync<RB>(q_lds, qb, static_cast<int64_t>(qt) * 64, N, tid);
-            load_rows_sync<RB>(o_lds, ob, static_cast<int64_t>(qt) * 64, N, tid);
+            load_rows_sync<RB, E == 2>(q_lds, qb, static_cast<int64_t>(qt) * 64, N, tid);
+            load_rows_sync<RB, E == 2>(o_lds, ob, static_cast<int64_t>(qt) * 64, N, tid);
             if (tid < 64) {
                 const int64_t i = static_cast<int64_t>(qt) * 64 + tid;
                 st_lds[tid] = i < N ? stat[bh * N + i] : make_float2(INFINITY, 0.f);
@@ -340,8 +342,8 @@ __global__ __launch_bounds__(CB_NT) void coarse_dq_kernel(const T* __restrict__ 
     const int ntiles = (N + 63) / 64;
     for (int kt = 0; kt < ntiles; ++kt) {
         __syncthreads();
-        load_rows_sync<RB>(k_lds, kb, static_cast<int64_t>(kt) * 64, N, tid);
-        load_rows_sync<RB>(v_lds, vb, static_cast<int64_t>(kt) * 64, N, tid);
+        load_rows_sync<RB, E == 2>(k_lds, kb, static_cast<int64_t>(kt) * 64, N, tid);
+        load_rows_sync<RB, E == 2>(v_lds, vb, static_cast<int64_t>(kt) * 64, N, tid);
         __syncthreads();
 #pragma unroll
         for (int t2 = 0; t2 < 2; ++t2) {

@@ -414,20 +414,39 @@ __device__ __forceinline__ int64_t sweep_start(const int32_t* list, int64_t e0, 
 
 // LDS tiles are stored with a row stride of RB + 16 bytes: 16 lanes reading
 // the same 16-byte column of 16 consecutive rows then hit 16 different bank
-// groups, and every fragment address is one per-lane base plus a compile-time
-// offset (no per-fragment address registers).  Rows are permuted with
-// swap_bits_2_3 when PERM: LDS row r holds global row swap_bits_2_3(r).  A
-// tile is copied by whole 1 KB wave instructions; lanes whose destination is
-// a pad slot (or past the last row) fetch the tile's first 16 bytes again.
-// The per-lane source offsets are the same for every tile of a shape: they
-// are computed once and each issue adds a wave-uniform tile base.
-template <int ROWS, int RB, int NW, bool PERM>
+// groups, and every fragment address is one per-lane base plus a
+// compile-time offset (no per-fragment address registers).  Rows are
+// permuted with swap_bits_2_3 when PERM: LDS row r holds global row
+// swap_bits_2_3(r).
+//
+// bf16 tiles (CPERM) also place the 32-byte column groups of a row (16
+// elements each) out of order: group g sits at position cgroup_pos(g) =
+// (g & 1) * NG/2 + g/2 (NG = RB/32 groups), so the two 16-column halves of
+// a 32-column fragment lie half a row apart.  A transposing read
+// (lds_frag_tr) makes 32 lanes fetch 64 bytes from each of 4 consecutive
+// rows; with contiguous columns those rows' bank ranges overlap up to
+// 4-fold at this row stride, with the halves split apart at most 2-fold.
+//
+// A tile is copied by whole 1 KB wave instructions; lanes whose destination
+// is a pad slot (or past the last row) fetch the tile's first 16 bytes
+// again.  The per-lane source offsets are the same for every tile of a
+// shape: they are computed once and each issue adds a wave-uniform base.
+template <int RB>
+__host__ __device__ constexpr int cgroup_pos(int g) {
+    return (g & 1) * (RB / 64) + (g >> 1);
+}
+template <int RB>
+__host__ __device__ constexpr int cgroup_of_pos(int pos) {
+    return pos < RB / 64 ? 2 * pos : 2 * (pos - RB / 64) + 1;
+}
+
+template <int ROWS, int RB, int NW, bool PERM, bool CPERM = false>
 struct async_tile {
     static constexpr int STRIDE = RB + 16;
     static constexpr int NI = ((ROWS * STRIDE + 1023) / 1024 + NW - 1) / NW * NW;  // 1 KB instructions
     static constexpr int BYTES = NI * 1024;        // LDS bytes to allocate
     static constexpr int PER_WAVE = NI / NW;
-    static_assert(RB % 16 == 0, "row bytes");
+    static_assert(RB % 64 == 0, "row bytes");
     int off[PER_WAVE];
 
     __device__ __forceinline__ async_tile(int wave, int lane) {
@@ -436,7 +455,8 @@ struct async_tile {
             const int p = (wave * PER_WAVE + j) * 1024 + lane * 16;   // physical LDS byte
             const int row = p / STRIDE, col = p % STRIDE;
             const bool data = row < ROWS && col < RB;
-            off[j] = data ? (PERM ? swap_bits_2_3(row) : row) * RB + col : 0;
+            const int lcol = CPERM ? cgroup_of_pos<RB>(col / 32) * 32 + col % 32 : col;
+            off[j] = data ? (PERM ? swap_bits_2_3(row) : row) * RB + lcol : 0;
         }
     }
     __device__ __forceinline__ void issue(char* lds, const char* g, int wave) const {
@@ -450,14 +470,16 @@ struct async_tile {
 //
 // The tile holds X^T row-major: LDS row = the contraction index (a key or a
 // query, stored at slot swap_bits_2_3(index) when PERM), columns = the output
-// rows m (the head dimension d), contiguous.  The MFMA 32x32x16 A operand for
-// output tile rows m0 .. m0+31 and contraction indices k0 .. k0+15 needs, in
-// lane l, X[m0 + l%32][k0 + 8(l/32) + s] for s = 0..7.  ds_read_b64_tr_b16
-// gives, within each group of 16 lanes, lane j the 4 values E[j/4 + 4c][j%4]
-// (c = 0..3) of the 16x4 block E whose row i lane i addresses.  So lane i of
-// group G (l = 16G + i) addresses contraction index k0 + 8(G/2) + 4r + i/4,
-// columns m0 + 16(G%2) + 4(i%4) .. +3, and read r = 0, 1 returns slots
-// 4r .. 4r+3.  Every address is a per-lane base plus compile-time offsets.
+// rows m (the head dimension d), in the bf16 column-group order above.  The
+// MFMA 32x32x16 A operand for output tile rows m0 .. m0+31 (m0 a multiple
+// of 32) and contraction indices k0 .. k0+15 needs, in lane l,
+// X[m0 + l%32][k0 + 8(l/32) + s] for s = 0..7.  ds_read_b64_tr_b16 gives,
+// within each group of 16 lanes, lane j the 4 values E[j/4 + 4c][j%4]
+// (c = 0..3) of the 16x4 block E whose row i lane i addresses.  So lane i
+// of group G (l = 16G + i) addresses contraction index k0 + 8(G/2) + 4r +
+// i/4, columns m0 + 16(G%2) + 4(i%4) .. +3 (column group m0/16 + G%2), and
+// read r = 0, 1 returns slots 4r .. 4r+3.  Every address is a per-lane base
+// plus compile-time offsets.
 template <int RB, bool PERM>
 __device__ __forceinline__ void lds_frag_tr(frag_bf16& f, const char* tile, int m0, int k0) {
     typedef short v4i16 __attribute__((ext_vector_type(4)));
@@ -468,7 +490,8 @@ __device__ __forceinline__ void lds_frag_tr(frag_bf16& f, const char* tile, int 
     for (int r = 0; r < 2; ++r) {
         const int k = k0 + 8 * (G >> 1) + 4 * r + (i >> 2);
         const int row = PERM ? swap_bits_2_3(k) : k;
-        const char* p = tile + row * (RB + 16) + (m0 + 16 * (G & 1) + 4 * (i & 3)) * 2;
+        const int grp = cgroup_pos<RB>((m0 >> 4) + (G & 1));
+        const char* p = tile + row * (RB + 16) + grp * 32 + 8 * (i & 3);
         r2[r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p));
     }
     typedef __attribute__((__vector_size__(8 * sizeof(short)))) short s16x8_t;
@@ -489,11 +512,12 @@ __device__ __forceinline__ void lds_frag_tr(frag_f32& f, const char* tile, int m
     }
 }
 
-// Fragment of 8 consecutive elements starting at element e0 of row `row` of
-// a padded LDS tile with RB-byte rows.
+// Fragment of 8 consecutive elements starting at element e0 (a multiple of
+// 8) of row `row` of a padded LDS tile with RB-byte rows (bf16: in the
+// column-group order above).
 template <int RB>
 __device__ __forceinline__ void lds_frag_s(frag_bf16& f, const char* tile, int row, int e0) {
-    load_frag(f, tile + row * (RB + 16) + e0 * 2);
+    load_frag(f, tile + row * (RB + 16) + cgroup_pos<RB>(e0 >> 4) * 32 + (e0 & 15) * 2);
 }
 template <int RB>
 __device__ __forceinline__ void lds_frag_s(frag_f32& f, const char* tile, int row, int e0) {
