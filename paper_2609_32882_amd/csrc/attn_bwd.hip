@@ -130,7 +130,6 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
             dma16(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)st_lds[buf])) + wave * 256,
                   reinterpret_cast<const char*>(stat + o0) + wave * 256, lane * 16);
     };
-    constexpr int OPS = 2 * RT::PER_WAVE + 1;    // copies per wave per query block
 
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {   // fragments in registers before the copies start
@@ -153,14 +152,12 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
         const int buf = static_cast<int>(j & 1);
         const bool has_next = j + 1 < cnt;
         const int64_t q_next = has_next ? q0_of(entry(j + 1)) : -1;
-        // the other buffer was released by the barrier that ended the last step
-        if (has_next) {
-            issue(q_next, buf ^ 1);
-            vm_wait<OPS>();             // this block's copies have landed
-        } else {
-            vm_wait<0>();
-        }
+        // One barrier per block: after it, this block's copies (the only
+        // ones outstanding) are visible and both waves are done with the
+        // previous block, whose buffer then receives the next block's copies.
+        vm_wait<0>();
         wg_barrier();
+        if (has_next) issue(q_next, buf ^ 1);
         const char* qt = q_lds[buf];
         const char* ot = o_lds[buf];
         const float2* st = st_lds[buf];
@@ -251,7 +248,6 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
                 if (t == 0) softmax_grad(1, u * EU, EU);
             }
         }
-        wg_barrier();                   // buffer `buf` free for the step after next
         q_cur = q_next;
     }
 
