@@ -73,7 +73,7 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float2* __restrict__ stat,
     const int32_t* __restrict__ kv_ptr, const int32_t* __restrict__ kv_idx, int64_t col_cap,
-    T* __restrict__ dk, T* __restrict__ dv, int Hq, int Hkv, int N, float c_log2, float scale, int period,
+    T* __restrict__ dk, T* __restrict__ dv, int Hq, int Hkv, int N, float c_log2, float scale,
     const int32_t* __restrict__ order) {
     using F = typename frag_of<T>::type;
     constexpr int E = sizeof(T);
@@ -136,13 +136,15 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
         settle(kf[ks]);
         settle(vf[ks]);
     }
-    // phased sweep over the query blocks (values hq_local*N + n_q)
+    // Ascending sweep over the query blocks (values hq_local*N + n_q).  With
+    // the longest-first order of the key blocks, the workgroups resident
+    // together have lists of about the same length and move through the
+    // query range together, so the Q / dO tiles they gather are shared
+    // through L2 (measured at 720p: 122 GB of L2 misses; 164 GB with the
+    // phased start of the query-stationary kernels, which needs equal
+    // lengths from rows that are not reordered).
     const int64_t cnt = e1 - e0;
-    const int64_t s0 = sweep_start(kv_idx, e0, cnt, blockIdx.x >> 3, period, grp * N);
-    auto entry = [&](int64_t j) -> int64_t {
-        const int64_t t = s0 + j;
-        return e0 + (t >= cnt ? t - cnt : t);
-    };
+    auto entry = [&](int64_t j) -> int64_t { return e0 + j; };
     int64_t q_cur = -1;
     if (cnt > 0) {
         q_cur = q0_of(entry(0));
@@ -484,15 +486,14 @@ static hipError_t launch_dkdv_t(const void* q, const void* k, const void* v, con
     const int64_t krows = static_cast<int64_t>(batch) * Hkv * N;
     if (krows == 0) return hipSuccess;
     int32_t* order = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + bwd_ws_csc_order_offset(batch, Hq, N));
-    hipError_t e = launch_lpt_order(kv_ptr, krows, col_cap, order, s);
+    hipError_t e = launch_lpt_order(kv_ptr, krows, N, col_cap, order, s);
     if (e != hipSuccess) return e;
     const float c = kLog2e / sqrtf(static_cast<float>(D));
     const float scale = 1.0f / sqrtf(static_cast<float>(D));
     hipLaunchKernelGGL((dkdv_kernel<T, D, COMP>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s,
                        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
                        static_cast<const T*>(dout), static_cast<const float2*>(ws), kv_ptr, kv_idx, col_cap,
-                       static_cast<T*>(dk), static_cast<T*>(dv), Hq, Hkv, N, c, scale,
-                       resident_per_xcd<dkdv_kernel<T, D, COMP>>(AB_NT), order);
+                       static_cast<T*>(dk), static_cast<T*>(dv), Hq, Hkv, N, c, scale, order);
     return hipGetLastError();
 }
 
@@ -504,7 +505,7 @@ static hipError_t launch_dq_t(const void* q, const void* k, const void* v, const
     const int64_t qrows = static_cast<int64_t>(batch) * Hq * N;
     if (qrows == 0) return hipSuccess;
     int32_t* order = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + bwd_ws_csr_order_offset(batch, Hq, N));
-    hipError_t e = launch_lpt_order(row_ptr, qrows, col_cap, order, s);
+    hipError_t e = launch_lpt_order(row_ptr, qrows, N, col_cap, order, s);
     if (e != hipSuccess) return e;
     const float c = kLog2e / sqrtf(static_cast<float>(D));
     const float scale = 1.0f / sqrtf(static_cast<float>(D));

@@ -228,7 +228,7 @@ static hipError_t launch_fwd_t(const void* q, const void* k, const void* v, cons
                                int32_t* order, int batch, int Hq, int Hkv, int N, hipStream_t s) {
     const int64_t rows = static_cast<int64_t>(batch) * Hq * N;
     if (rows == 0) return hipSuccess;
-    hipError_t e = launch_lpt_order(row_ptr, rows, col_cap, order, s);
+    hipError_t e = launch_lpt_order(row_ptr, rows, N, col_cap, order, s);
     if (e != hipSuccess) return e;
     const float c = 1.4426950408889634f / sqrtf(static_cast<float>(D));
     if (o_lo)

@@ -277,21 +277,20 @@ def test_bwd_unselected_blocks_are_zero_explicit():
     assert_values(to_np(dv).reshape(dv_ref.shape), dv_ref, "dV (two blocks)")
 
 
-def _check_lpt_order(order, lengths):
-    """order is a permutation of each of the 8 XCD ranges, longest length
-    class first (class = len * 32 // (max_len + 1) over the range) and in row
-    order inside a class."""
+def _check_lpt_order(order, lengths, n_per_head):
+    """order is a permutation of each segment where one of the 8 XCD ranges
+    meets one head's rows, longest length class first (class = len * 32 //
+    (max_len + 1) over the segment) and in row order inside a class."""
     n = lengths.size
     q, r = divmod(n, 8)
-    for x in range(8):
-        beg = x * q + min(x, r)
-        cnt = q + (1 if x < r else 0)
-        seg = order[beg:beg + cnt].astype(np.int64)
-        assert np.array_equal(np.sort(seg), np.arange(beg, beg + cnt))
-        if cnt == 0:
+    cuts = sorted(set([x * q + min(x, r) for x in range(9)] + list(range(0, n + 1, n_per_head))))
+    for beg, end in zip(cuts[:-1], cuts[1:]):
+        if end <= beg:
             continue
+        seg = order[beg:end].astype(np.int64)
+        assert np.array_equal(np.sort(seg), np.arange(beg, end))
         ln = lengths[seg]
-        cls = ln * 32 // (lengths[beg:beg + cnt].max() + 1)
+        cls = ln * 32 // (lengths[beg:end].max() + 1)
         assert (np.diff(cls) <= 0).all()
         same = np.diff(cls) == 0
         assert (np.diff(seg)[same] > 0).all()
@@ -326,7 +325,7 @@ def test_work_order_and_ragged_rows():
     dq, dk, dv = vsa2.attn_bwd(p, dev["q"], dev["k"], dev["v"], o, lse, dev["do"], t["rp"], t["ci"],
                                t["kp"], t["ki"])
     torch.cuda.synchronize()
-    _check_lpt_order(ws.cpu().numpy()[:nrows], np.diff(rp).astype(np.int64))
+    _check_lpt_order(ws.cpu().numpy()[:nrows], np.diff(rp).astype(np.int64), p.N)
     # the backward's CSC order, read from a workspace of the staged call
     a256 = lambda n: (n + 255) // 256 * 256
     off = a256(8 * nrows * p.B) + a256(4 * nrows)
@@ -342,7 +341,7 @@ def test_work_order_and_ragged_rows():
     assert st == 0
     torch.cuda.synchronize()
     kv_order = bws[off:off + 4 * nkv].view(torch.int32).cpu().numpy()
-    _check_lpt_order(kv_order, np.diff(kp).astype(np.int64))
+    _check_lpt_order(kv_order, np.diff(kp).astype(np.int64), p.N)
     o_ref, lse_ref = oracle.attn_fwd(x["q"], x["k"], x["v"], p, rp, ci)
     assert_values(to_np(o).reshape(o_ref.shape), o_ref, "O (ragged rows)")
     empty = np.repeat(counts == 0, p.B)
