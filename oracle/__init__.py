@@ -47,17 +47,18 @@ def lib():
         i32, i64, dbl = ctypes.c_int, ctypes.c_int64, ctypes.c_double
         L.vo_round_bf16.argtypes = [P, P, i64]
         L.vo_pool.argtypes = [P, i64, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, P]
-        L.vo_router_scores.argtypes = [P, P, i32, i32, i32, i64, i32, i32, P, i64, P, P]
+        L.vo_router_scores.argtypes = [P, P, i32, i32, i32, i64, i32, i32, P, i64, P, P, P, i32, i32,
+                                       i32]
         L.vo_select_rows.argtypes = [P, i64, i32, i32, i32, dbl, i32, P, P]
         L.vo_select_seq.argtypes = [P, i64, i32, i32, P]
-        L.vo_attn_fwd.argtypes = [P, P, P, i32, i32, i32, i64, i32, i32, P, P, P, i64, P, P]
-        L.vo_attn_bwd_dq.argtypes = [P, P, P, P, i32, i32, i32, i64, i32, i32, P, P, P, i64, P]
+        L.vo_attn_fwd.argtypes = [P, P, P, i32, i32, i32, i64, i32, i32, P, P, P, i64, P, P, P]
+        L.vo_attn_bwd_dq.argtypes = [P, P, P, P, i32, i32, i32, i64, i32, i32, P, P, P, i64, P, P]
         L.vo_attn_bwd_dkdv.argtypes = [P, P, P, P, i32, i32, i32, i64, i32, i32, P, P, P, i64,
-                                       P, P]
+                                       P, P, P]
         L.vo_coarse_fwd.argtypes = [P, P, P, i32, i32, i32, i32, i32, P, P]
         L.vo_coarse_bwd.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, P, P, P]
         L.vo_gate_merge.argtypes = [P, P, P, i64, i32, i32, i32, P]
-        L.vo_gate_merge_bwd.argtypes = [P, P, P, i64, i32, i32, i32, P, P]
+        L.vo_gate_merge_bwd.argtypes = [P, P, P, i64, i32, i32, i32, P, P, P]
         L.vo_unpool_add.argtypes = [P, i64, i32, i32, i32, i32, i32, i32, i32, i32, i32, i32, P]
         for f in (L.vo_round_bf16, L.vo_pool, L.vo_router_scores, L.vo_select_rows,
                   L.vo_select_seq, L.vo_attn_fwd, L.vo_attn_bwd_dq, L.vo_attn_bwd_dkdv,
@@ -74,6 +75,11 @@ def _p(a: np.ndarray):
 
 def _f32(a):
     return np.ascontiguousarray(a, dtype=np.float32)
+
+
+def _geom(p):
+    """{T, H, W, Bt, Bh, Bw}: the real grid and the cube (padded grids)."""
+    return np.array([p.T, p.H, p.W, p.Bt, p.Bh, p.Bw], np.int32)
 
 
 def threads() -> int:
@@ -112,8 +118,9 @@ def router_scores(q_r, k_r, p, rows=None, with_lse: bool = False):
     rows = np.arange(nrow_all, dtype=np.int64) if rows is None else np.ascontiguousarray(rows, np.int64)
     out = np.empty((rows.size, p.N), np.float64)
     lse = np.empty((rows.size, p.G), np.float64)
+    g = _geom(p)
     lib().vo_router_scores(_p(q_r), _p(k_r), p.batch, p.heads_q, p.heads_kv, p.N, p.G,
-                           p.head_dim, _p(rows), rows.size, _p(out), _p(lse))
+                           p.head_dim, _p(rows), rows.size, _p(out), _p(lse), _p(g), p.Rt, p.Rh, p.Rw)
     return (out, lse) if with_lse else out
 
 
@@ -180,8 +187,9 @@ def attn_fwd(q, k, v, p, row_ptr, col_idx, rows=None):
     o = np.empty((rows.size, p.B, p.head_dim), np.float64)
     lse = np.empty((rows.size, p.B), np.float64)
     rp, ci = np.ascontiguousarray(row_ptr, np.int32), np.ascontiguousarray(col_idx, np.int32)
+    g = _geom(p)
     lib().vo_attn_fwd(_p(q), _p(k), _p(v), p.batch, p.heads_q, p.heads_kv, p.L, p.head_dim,
-                      p.B, _p(rp), _p(ci), _p(rows), rows.size, _p(o), _p(lse))
+                      p.B, _p(rp), _p(ci), _p(rows), rows.size, _p(o), _p(lse), _p(g))
     return o, lse
 
 
@@ -191,8 +199,9 @@ def attn_bwd_dq(q, k, v, do, p, row_ptr, col_idx, rows=None):
     rows = np.arange(nrow_all, dtype=np.int64) if rows is None else np.ascontiguousarray(rows, np.int64)
     dq = np.empty((rows.size, p.B, p.head_dim), np.float64)
     rp, ci = np.ascontiguousarray(row_ptr, np.int32), np.ascontiguousarray(col_idx, np.int32)
+    g = _geom(p)
     lib().vo_attn_bwd_dq(_p(q), _p(k), _p(v), _p(do), p.batch, p.heads_q, p.heads_kv, p.L,
-                         p.head_dim, p.B, _p(rp), _p(ci), _p(rows), rows.size, _p(dq))
+                         p.head_dim, p.B, _p(rp), _p(ci), _p(rows), rows.size, _p(dq), _p(g))
     return dq
 
 
@@ -204,9 +213,10 @@ def attn_bwd_dkdv(q, k, v, do, p, row_ptr, col_idx, kv_rows=None):
     dk = np.empty((kv_rows.size, p.B, p.head_dim), np.float64)
     dv = np.empty((kv_rows.size, p.B, p.head_dim), np.float64)
     rp, ci = np.ascontiguousarray(row_ptr, np.int32), np.ascontiguousarray(col_idx, np.int32)
+    g = _geom(p)
     lib().vo_attn_bwd_dkdv(_p(q), _p(k), _p(v), _p(do), p.batch, p.heads_q, p.heads_kv, p.L,
                            p.head_dim, p.B, _p(rp), _p(ci), _p(kv_rows), kv_rows.size,
-                           _p(dk), _p(dv))
+                           _p(dk), _p(dv), _p(g))
     return dk, dv
 
 
@@ -263,8 +273,9 @@ def gate_merge_bwd(g, oc, dout, p):
     g, oc, dout = _f32(g), _f32(oc), _f32(dout)
     doc = np.empty((p.batch, p.heads_q, p.N, p.head_dim), np.float64)
     dg = np.empty((p.batch, p.heads_q, p.L), np.float64)
+    geom = _geom(p)
     lib().vo_gate_merge_bwd(_p(g), _p(oc), _p(dout), p.batch * p.heads_q, p.N, p.B, p.head_dim,
-                            _p(doc), _p(dg))
+                            _p(doc), _p(dg), _p(geom))
     return doc, dg
 
 

@@ -65,23 +65,59 @@ void vo_round_bf16(const double* in, float* out, int64_t n)
 }
 
 /* ---------------------------------------------------------------------- */
+/* Padded grids (Sec. 2.2 "Kernel Implementation": each of T, H, W is      */
+/* padded up to a multiple of the cube size and padding is masked out).    */
+/* geom = {T, H, W, Bt, Bh, Bw}: the real grid and the cube.  The cube-     */
+/* major layout holds N = ceil(T/Bt) ceil(H/Bh) ceil(W/Bw) cubes of B       */
+/* tokens; token beta of cube n is real iff its grid position lies inside  */
+/* the real grid.  geom == NULL: every token is real.                      */
+/* ---------------------------------------------------------------------- */
+
+static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+static int vo_token_real(const int* geom, int64_t n, int beta)
+{
+    if (!geom) return 1;
+    const int T = geom[0], H = geom[1], W = geom[2], Bt = geom[3], Bh = geom[4], Bw = geom[5];
+    const int64_t Nh = ceil_div(H, Bh), Nw = ceil_div(W, Bw);
+    const int64_t nt = n / (Nh * Nw), nh = (n / Nw) % Nh, nw = n % Nw;
+    const int bt = beta / (Bh * Bw), bh = (beta / Bw) % Bh, bw = beta % Bw;
+    return nt * Bt + bt < T && nh * Bh + bh < H && nw * Bw + bw < W;
+}
+
+/* Number of real tokens of sub-cube g (pool size Pt x Ph x Pw) of cube n. */
+static int vo_subcube_real_count(const int* geom, int64_t n, int g, int Pt, int Ph, int Pw)
+{
+    const int Bh = geom[4], Bw = geom[5];
+    const int Gh = Bh / Ph, Gw = Bw / Pw;
+    const int gt = g / (Gh * Gw), gh = (g / Gw) % Gh, gw = g % Gw;
+    int c = 0;
+    for (int rt = 0; rt < Pt; ++rt)
+        for (int rh = 0; rh < Ph; ++rh)
+            for (int rw = 0; rw < Pw; ++rw)
+                c += vo_token_real(geom, n, ((gt * Pt + rt) * Bh + gh * Ph + rh) * Bw + gw * Pw + rw);
+    return c;
+}
+
+/* ---------------------------------------------------------------------- */
 /* MeanPool over sub-cubes (Eq. router_start for P = R; Eq. compress for   */
 /* P = B).                                                                 */
 /* ---------------------------------------------------------------------- */
 
 /* x: [nbh][N*B][D] cube-major.  out: [nbh][N*Gp][D] with Gp = B/P sub-cubes
  * per cube, ordered (n, g), g = (gt*Gh + gh)*Gw + gw.  Each output row is the
- * mean of the P = Pt*Ph*Pw tokens of its sub-cube, rounded to the dtype. */
+ * mean of the real tokens of its sub-cube (all P = Pt*Ph*Pw of them unless
+ * the grid is padded), rounded to the dtype; a sub-cube with no real token
+ * gives 0. */
 void vo_pool(const float* x, int64_t nbh, int T, int H, int W,
              int Bt, int Bh, int Bw, int Pt, int Ph, int Pw, int D,
              int dtype_bf16, float* out)
 {
-    const int Nt = T / Bt, Nh = H / Bh, Nw = W / Bw;
-    const int64_t N = (int64_t)Nt * Nh * Nw;
+    const int geom[6] = {T, H, W, Bt, Bh, Bw};
+    const int64_t N = ceil_div(T, Bt) * ceil_div(H, Bh) * ceil_div(W, Bw);
     const int B = Bt * Bh * Bw;
     const int Gt = Bt / Pt, Gh = Bh / Ph, Gw = Bw / Pw;
     const int G = Gt * Gh * Gw;
-    const int P = Pt * Ph * Pw;
 #pragma omp parallel for schedule(static)
     for (int64_t bh = 0; bh < nbh; ++bh) {
         for (int64_t n = 0; n < N; ++n) {
@@ -92,14 +128,17 @@ void vo_pool(const float* x, int64_t nbh, int T, int H, int W,
                 float* o = out + ((bh * N + n) * G + g) * (int64_t)D;
                 for (int d = 0; d < D; ++d) {
                     double sum = 0.0;
+                    int count = 0;
                     for (int rt = 0; rt < Pt; ++rt)
                     for (int rh = 0; rh < Ph; ++rh)
                     for (int rw = 0; rw < Pw; ++rw) {
                         const int bt = gt * Pt + rt, bhh = gh * Ph + rh, bw = gw * Pw + rw;
                         const int beta = (bt * Bh + bhh) * Bw + bw;
+                        if (!vo_token_real(geom, n, beta)) continue;
                         sum += (double)x[((bh * N + n) * B + beta) * (int64_t)D + d];
+                        ++count;
                     }
-                    o[d] = round_to_dtype(sum / (double)P, dtype_bf16);
+                    o[d] = count ? round_to_dtype(sum / (double)count, dtype_bf16) : 0.0f;
                 }
             }
         }
@@ -119,7 +158,7 @@ void vo_pool(const float* x, int64_t nbh, int T, int H, int W,
  * scores: [nrows][N]; lse_out: [nrows][G] or NULL. */
 void vo_router_scores(const float* q_r, const float* k_r, int nb, int Hq, int Hkv,
                       int64_t N, int G, int D, const int64_t* rows, int64_t nrows,
-                      double* scores, double* lse_out)
+                      double* scores, double* lse_out, const int* geom, int Rt, int Rh, int Rw)
 {
     (void)nb;
     const int64_t NG = N * G;
@@ -128,6 +167,10 @@ void vo_router_scores(const float* q_r, const float* k_r, int nb, int Hq, int Hk
 #pragma omp parallel
     {
         double* s = (double*)malloc(sizeof(double) * (size_t)NG);
+        uint8_t* real = (uint8_t*)malloc((size_t)NG);
+        /* pooled keys (and queries) with no real token take no part */
+        for (int64_t j = 0; j < NG; ++j)
+            real[j] = geom ? vo_subcube_real_count(geom, j / G, (int)(j % G), Rt, Rh, Rw) > 0 : 1;
 #pragma omp for schedule(dynamic, 1)
         for (int64_t r = 0; r < nrows; ++r) {
             const int64_t row = rows[r];
@@ -137,24 +180,30 @@ void vo_router_scores(const float* q_r, const float* k_r, int nb, int Hq, int Hk
             const float* K = k_r + (b * Hkv + hkv) * NG * (int64_t)D;
             double* out = scores + r * N;
             for (int64_t nk = 0; nk < N; ++nk) out[nk] = 0.0;
+            int gq_real = 0;
+            for (int gq = 0; gq < G; ++gq) gq_real += real[nq * G + gq];
             for (int gq = 0; gq < G; ++gq) {
                 const float* qi = q_r + ((bh * N + nq) * G + gq) * (int64_t)D;
                 double m = -INFINITY;
                 for (int64_t j = 0; j < NG; ++j) {
                     double dot = 0.0;
                     for (int d = 0; d < D; ++d) dot += (double)qi[d] * (double)K[j * D + d];
-                    s[j] = dot * scale;
+                    s[j] = real[j] ? dot * scale : -INFINITY;
                     if (s[j] > m) m = s[j];
                 }
                 double sum = 0.0;
                 for (int64_t j = 0; j < NG; ++j) sum += exp(s[j] - m);
                 const double lse = m + log(sum);
                 if (lse_out) lse_out[r * G + gq] = lse;
+                if (!real[nq * G + gq]) continue;
+                /* MeanPool_{GxG} over the pooled queries that hold a real
+                 * token (all G of them unless the grid is padded) */
                 for (int64_t nk = 0; nk < N; ++nk)
                     for (int gk = 0; gk < G; ++gk)
-                        out[nk] += exp(s[nk * G + gk] - lse) / ((double)G * (double)G);
+                        out[nk] += exp(s[nk * G + gk] - lse) / ((double)G * (double)gq_real);
             }
         }
+        free(real);
         free(s);
     }
 }
@@ -255,7 +304,8 @@ void vo_select_seq(const double* scores, int64_t nseq, int N, int k, uint8_t* se
  * softmax row over the gathered keys, in CSR order), o[D] and returns the
  * natural-log LSE.  An empty selection gives o = 0 and -inf. */
 static double token_forward(const float* qv, const float* K, const float* V, int D, int B,
-                            const int32_t* sel, int nsel, double scale, double* p, double* o)
+                            const int32_t* sel, int nsel, double scale, double* p, double* o,
+                            const int* geom)
 {
     const int nkeys = nsel * B;
     for (int d = 0; d < D; ++d) o[d] = 0.0;
@@ -264,11 +314,19 @@ static double token_forward(const float* qv, const float* K, const float* V, int
     for (int c = 0; c < nsel; ++c)
         for (int t = 0; t < B; ++t) {
             const int64_t j = (int64_t)sel[c] * B + t;
+            if (!vo_token_real(geom, sel[c], t)) {   /* padding key: masked out */
+                p[c * B + t] = -INFINITY;
+                continue;
+            }
             double dot = 0.0;
             for (int d = 0; d < D; ++d) dot += (double)qv[d] * (double)K[j * D + d];
             p[c * B + t] = dot * scale;
             if (p[c * B + t] > m) m = p[c * B + t];
         }
+    if (m == -INFINITY) {                        /* only padding keys selected */
+        for (int j = 0; j < nkeys; ++j) p[j] = 0.0;
+        return -INFINITY;
+    }
     double sum = 0.0;
     for (int j = 0; j < nkeys; ++j) { p[j] = exp(p[j] - m); sum += p[j]; }
     for (int j = 0; j < nkeys; ++j) p[j] /= sum;
@@ -285,7 +343,7 @@ static double token_forward(const float* qv, const float* K, const float* V, int
  * LSE: [nq][B] (natural log) of its B query tokens. */
 void vo_attn_fwd(const float* q, const float* k, const float* v, int nb, int Hq, int Hkv,
                  int64_t L, int D, int B, const int32_t* row_ptr, const int32_t* col_idx,
-                 const int64_t* qrows, int64_t nq, double* o, double* lse)
+                 const int64_t* qrows, int64_t nq, double* o, double* lse, const int* geom)
 {
     (void)nb;
     const int64_t N = L / B;
@@ -305,8 +363,13 @@ void vo_attn_fwd(const float* q, const float* k, const float* v, int nb, int Hq,
             const int nsel = row_ptr[row + 1] - row_ptr[row];
             for (int t = 0; t < B; ++t) {
                 const float* qv = q + (bh * L + n * B + t) * D;
+                if (!vo_token_real(geom, n, t)) {       /* padding query: no output */
+                    for (int d = 0; d < D; ++d) o[(r * B + t) * (int64_t)D + d] = 0.0;
+                    lse[r * B + t] = -INFINITY;
+                    continue;
+                }
                 lse[r * B + t] = token_forward(qv, K, V, D, B, sel, nsel, scale, p,
-                                               o + (r * B + t) * (int64_t)D);
+                                               o + (r * B + t) * (int64_t)D, geom);
             }
         }
         free(p);
@@ -326,7 +389,7 @@ void vo_attn_fwd(const float* q, const float* k, const float* v, int nb, int Hq,
 void vo_attn_bwd_dq(const float* q, const float* k, const float* v, const float* dout,
                     int nb, int Hq, int Hkv, int64_t L, int D, int B,
                     const int32_t* row_ptr, const int32_t* col_idx,
-                    const int64_t* qrows, int64_t nq, double* dq)
+                    const int64_t* qrows, int64_t nq, double* dq, const int* geom)
 {
     (void)nb;
     const int64_t N = L / B;
@@ -351,7 +414,8 @@ void vo_attn_bwd_dq(const float* q, const float* k, const float* v, const float*
                 const float* dov = dout + tok * D;
                 double* g = dq + (r * B + t) * (int64_t)D;
                 for (int d = 0; d < D; ++d) g[d] = 0.0;
-                token_forward(qv, K, V, D, B, sel, nsel, scale, p, o);
+                if (!vo_token_real(geom, n, t)) continue;   /* padding query: dQ = 0 */
+                token_forward(qv, K, V, D, B, sel, nsel, scale, p, o, geom);
                 double delta = 0.0;
                 for (int d = 0; d < D; ++d) delta += (double)dov[d] * o[d];
                 for (int c = 0; c < nsel; ++c)
@@ -378,7 +442,7 @@ void vo_attn_bwd_dq(const float* q, const float* k, const float* v, const float*
 void vo_attn_bwd_dkdv(const float* q, const float* k, const float* v, const float* dout,
                       int nb, int Hq, int Hkv, int64_t L, int D, int B,
                       const int32_t* row_ptr, const int32_t* col_idx,
-                      const int64_t* kvrows, int64_t nkv, double* dk, double* dv)
+                      const int64_t* kvrows, int64_t nkv, double* dk, double* dv, const int* geom)
 {
     (void)nb;
     const int64_t N = L / B;
@@ -436,7 +500,8 @@ void vo_attn_bwd_dkdv(const float* q, const float* k, const float* v, const floa
                 const int64_t tok = bh * L + n * B + t;
                 const float* qv = q + tok * D;
                 const float* dov = dout + tok * D;
-                token_forward(qv, K, V, D, B, sel, nsel, scale, p, o);
+                if (!vo_token_real(geom, n, t)) continue;   /* padding query: no contribution */
+                token_forward(qv, K, V, D, B, sel, nsel, scale, p, o, geom);
                 double delta = 0.0;
                 for (int d = 0; d < D; ++d) delta += (double)dov[d] * o[d];
                 for (int u = 0; u < B; ++u) {
@@ -609,9 +674,11 @@ void vo_gate_merge(const float* g, const float* oc, const float* of, int64_t nbh
 
 /* Gradients of vo_gate_merge for dout ([nbh][L][D]):
  *   doc[n] = sum over the B tokens l of cube n of tanh(g_l) dout_l,
- *   dg_l = (1 - tanh(g_l)^2) (dout_l . oc[n(l)]);  d(O_f) = dout. */
+ *   dg_l = (1 - tanh(g_l)^2) (dout_l . oc[n(l)]);  d(O_f) = dout.
+ * Padding tokens of a padded grid are not outputs: they add nothing and get
+ * dg = 0. */
 void vo_gate_merge_bwd(const float* g, const float* oc, const float* dout, int64_t nbh, int N,
-                       int B, int D, double* doc, double* dg)
+                       int B, int D, double* doc, double* dg, const int* geom)
 {
     const int64_t L = (int64_t)N * B;
 #pragma omp parallel for schedule(static)
@@ -622,6 +689,10 @@ void vo_gate_merge_bwd(const float* g, const float* oc, const float* dout, int64
             for (int d = 0; d < D; ++d) dc[d] = 0.0;
             for (int t = 0; t < B; ++t) {
                 const int64_t l = n * B + t;
+                if (!vo_token_real(geom, n, t)) {       /* padding token: not an output */
+                    dg[bh * L + l] = 0.0;
+                    continue;
+                }
                 const double gate = tanh((double)g[bh * L + l]);
                 const float* dl = dout + (bh * L + l) * (int64_t)D;
                 double dot = 0.0;
@@ -635,17 +706,17 @@ void vo_gate_merge_bwd(const float* g, const float* oc, const float* dout, int64
 }
 
 /* The adjoint of vo_pool (the gradient of MeanPool over (Pt, Ph, Pw)):
- * every token of sub-cube (n, g) receives dxc[n*Gp + g] / P, added to dx.
+ * every real token of sub-cube (n, g) receives dxc[n*Gp + g] / (number of
+ * real tokens of the sub-cube), added to dx; padding tokens receive nothing.
  * dxc: [nbh][N*Gp][D]; dx: [nbh][N*B][D]. */
 void vo_unpool_add(const double* dxc, int64_t nbh, int T, int H, int W, int Bt, int Bh, int Bw,
                    int Pt, int Ph, int Pw, int D, double* dx)
 {
-    const int Nt = T / Bt, Nh = H / Bh, Nw = W / Bw;
-    const int64_t N = (int64_t)Nt * Nh * Nw;
+    const int geom[6] = {T, H, W, Bt, Bh, Bw};
+    const int64_t N = ceil_div(T, Bt) * ceil_div(H, Bh) * ceil_div(W, Bw);
     const int B = Bt * Bh * Bw;
     const int Gt = Bt / Pt, Gh = Bh / Ph, Gw = Bw / Pw;
     const int G = Gt * Gh * Gw;
-    const double P = (double)(Pt * Ph * Pw);
 #pragma omp parallel for schedule(static)
     for (int64_t bh = 0; bh < nbh; ++bh)
         for (int64_t n = 0; n < N; ++n)
@@ -654,8 +725,10 @@ void vo_unpool_add(const double* dxc, int64_t nbh, int T, int H, int W, int Bt, 
             for (int bw = 0; bw < Bw; ++bw) {
                 const int g = ((bt / Pt) * Gh + bhh / Ph) * Gw + bw / Pw;
                 const int beta = (bt * Bh + bhh) * Bw + bw;
+                if (!vo_token_real(geom, n, beta)) continue;
+                const double cnt = (double)vo_subcube_real_count(geom, n, g, Pt, Ph, Pw);
                 const double* src = dxc + ((bh * N + n) * G + g) * (int64_t)D;
                 double* dst = dx + ((bh * N + n) * B + beta) * (int64_t)D;
-                for (int d = 0; d < D; ++d) dst[d] += src[d] / P;
+                for (int d = 0; d < D; ++d) dst[d] += src[d] / cnt;
             }
 }

@@ -514,12 +514,15 @@ def test_unpool_is_the_adjoint_of_pool(P):
     np.testing.assert_array_equal(back.astype(np.float64), ones / (Pt * Ph * Pw))
 
 
-def test_full_op_gradient_finite_differences():
+@pytest.mark.parametrize("grid_thw", [(2, 4, 4), (3, 3, 4)])
+def test_full_op_gradient_finite_differences(grid_thw):
     """The whole VSA2 attention op O = tanh(g) Repeat_B(Attn(Pool_B Q, Pool_B K,
     Pool_B V)) + BlockSparseAttn(Q, K, V; M): gradients composed from the
     oracle's steps (merge, coarse and fine backward, unpool) against central
-    differences of sum(W * O)."""
-    p = Problem(1, 2, 1, 8, 2, 4, 4, 2, 2, 2, 1, 1, 2, F32)    # N = 4 cubes of B = 8
+    differences of sum(W * O) over the real tokens.  The 3 x 3 x 4 grid is
+    padded to 4 x 4 x 4: the gradient of every padding token is 0."""
+    T, H, W_ = grid_thw
+    p = Problem(1, 2, 1, 8, T, H, W_, 2, 2, 2, 1, 1, 2, F32)    # cubes of B = 8
     rng = np.random.default_rng(43)
     grid = lambda shape: (rng.integers(-1024, 1024, shape) / 1024.0).astype(np.float32)
     q = grid((1, 2, p.L, p.head_dim))
@@ -527,6 +530,7 @@ def test_full_op_gradient_finite_differences():
     v = grid((1, 1, p.L, p.head_dim))
     g = grid((1, 2, p.L))
     W = rng.standard_normal((1, 2, p.L, p.head_dim)).astype(np.float32).astype(np.float64)
+    W *= p.token_real()[None, None, :, None]           # padding tokens are not outputs
     rp, ci = _random_csr(p, 44)
     Bt, Bh, Bw = p.Bt, p.Bh, p.Bw
 
@@ -556,8 +560,13 @@ def test_full_op_gradient_finite_differences():
     oracle.unpool_add(dkc, dk, p, Bt, Bh, Bw)
     oracle.unpool_add(dvc, dv, p, Bt, Bh, Bw)
     h = 2.0 ** -10
+    if p.padded:
+        real = p.token_real()
+        for gr in (dq, dk, dv):
+            assert (gr[:, :, ~real] == 0).all()
+        assert (dg[:, :, ~real] == 0).all()
     for name, t, gr in (("q", q, dq), ("k", k, dk), ("v", v, dv), ("g", g, dg)):
-        for flat in rng.choice(t.size, 10, replace=False):
+        for flat in rng.choice(t.size, 12, replace=False):
             args = {"q": q, "k": k, "v": v, "g": g}
             tp, tm = t.copy(), t.copy()
             tp.flat[flat] += np.float32(h)
@@ -567,3 +576,176 @@ def test_full_op_gradient_finite_differences():
             fd = (lp - lm) / (2 * h)
             assert abs(fd - gr.flat[flat]) <= 2e-5 * max(1.0, abs(gr).max()), (name, flat, fd,
                                                                                 gr.flat[flat])
+
+
+# ---------------------------------------------------------------- padded grids
+# A grid not divisible by the cube is padded up to whole cubes; padding
+# tokens are masked out everywhere (Sec. 2.2, kernel implementation).
+
+def padded(T=3, H=5, W=6, Bt=2, Bh=2, Bw=4, Rt=1, Rh=2, Rw=2, hq=2, hkv=2, D=8, dtype=F32):
+    p = Problem(1, hq, hkv, D, T, H, W, Bt, Bh, Bw, Rt, Rh, Rw, dtype)
+    assert p.padded
+    return p
+
+
+def _garbage_padding(x, p, seed):
+    """x with its padding tokens overwritten by large random values."""
+    y = x.copy()
+    real = p.token_real()
+    y[..., ~real, :] = np.random.default_rng(seed).standard_normal(y[..., ~real, :].shape) * 50
+    return y.astype(x.dtype)
+
+
+@pytest.mark.parametrize("P", [(1, 2, 2), (2, 2, 4), (1, 1, 1), (2, 1, 2)])
+def test_padded_pool_is_nanmean_over_real_tokens(P):
+    """Each pooled row is the mean of the sub-cube's tokens that lie in the
+    real grid (numpy nanmean over a NaN-padded grid); an all-padding sub-cube
+    pools to 0."""
+    p = padded()
+    Pt, Ph, Pw = P
+    rng = np.random.default_rng(50)
+    xr = rng.standard_normal((1, 2, p.T * p.H * p.W, p.head_dim)).astype(np.float32)
+    x = raster_to_cube_major(xr, p)
+    out = oracle.pool(_garbage_padding(x, p, 51), p, Pt, Ph, Pw)
+    g = np.full((1, 2, p.Nt * p.Bt, p.Nh * p.Bh, p.Nw * p.Bw, p.head_dim), np.nan)
+    g[:, :, :p.T, :p.H, :p.W] = xr.reshape(1, 2, p.T, p.H, p.W, p.head_dim)
+    Gt, Gh, Gw = p.Bt // Pt, p.Bh // Ph, p.Bw // Pw
+    m = g.reshape(1, 2, p.Nt, Gt, Pt, p.Nh, Gh, Ph, p.Nw, Gw, Pw, p.head_dim)
+    with np.errstate(all="ignore"):
+        import warnings
+        with warnings.catch_warnings():
+            warnings.simplefilter("ignore", RuntimeWarning)
+            m = np.nanmean(m, axis=(4, 7, 10))
+    m = np.nan_to_num(m, nan=0.0)
+    m = m.transpose(0, 1, 2, 4, 6, 3, 5, 7, 8).reshape(1, 2, -1, p.head_dim)
+    np.testing.assert_array_equal(out, m.astype(np.float32))
+    if P == (1, 1, 1):
+        assert (out[..., ~p.token_real(), :] == 0).all()
+
+
+def test_padded_router_ignores_padding_and_keeps_row_mass():
+    """Scores do not depend on what padding tokens hold, every row sums to
+    1/G, and with R = B the router is the cube-level softmax over the means of
+    each cube's real tokens."""
+    p = padded()
+    q, k, _, _ = rand_qkv(p, 52, scale=2.0)
+    pool = lambda x: oracle.pool(x, p, p.Rt, p.Rh, p.Rw)
+    sc = oracle.router_scores(pool(q), pool(k), p)
+    sc2 = oracle.router_scores(pool(_garbage_padding(q, p, 53)), pool(_garbage_padding(k, p, 54)), p)
+    np.testing.assert_array_equal(sc, sc2)
+    assert (sc >= 0).all()
+    np.testing.assert_allclose(sc.sum(1), 1.0 / p.G, rtol=1e-12)
+    # R = B (G = 1)
+    pc = padded(Rt=2, Rh=2, Rw=4)
+    real = pc.token_real().reshape(pc.N, pc.B)
+    cnt = real.sum(1)[:, None]
+
+    def cube_means(x):
+        xx = x.astype(np.float64).reshape(1, -1, pc.N, pc.B, pc.head_dim) * real[None, None, :, :, None]
+        return (xx.sum(3) / cnt).astype(np.float32)
+
+    s1 = oracle.router_scores(oracle.pool(q, pc, 2, 2, 4), oracle.pool(k, pc, 2, 2, 4), pc)
+    qc, kc = cube_means(q).astype(np.float64), cube_means(k).astype(np.float64)
+    ref = _softmax64(np.einsum("bhid,bhjd->bhij", qc, kc) / math.sqrt(pc.head_dim))
+    np.testing.assert_allclose(s1.reshape(ref.shape), ref, rtol=1e-12, atol=1e-15)
+
+
+def test_padded_router_R_one_is_block_mean_over_real_tokens():
+    """R = 1: P_r[nq, nk] is the mean over the real query tokens of cube nq
+    of the softmax mass (over real keys only) that falls on cube nk, over B."""
+    p = padded(Rt=1, Rh=1, Rw=1)
+    q, k, _, _ = rand_qkv(p, 55)
+    sc = oracle.router_scores(oracle.pool(q, p, 1, 1, 1), oracle.pool(k, p, 1, 1, 1), p)
+    real = p.token_real()
+    s = torch.from_numpy(np.einsum("bhid,bhjd->bhij", q.astype(np.float64), k.astype(np.float64))
+                         / math.sqrt(p.head_dim))
+    s = s.masked_fill(~torch.from_numpy(real)[None, None, None, :], float("-inf"))
+    P = torch.softmax(s, -1).numpy().reshape(1, p.heads_q, p.N, p.B, p.N, p.B)
+    rq = real.reshape(p.N, p.B)
+    ref = (P * rq[None, None, :, :, None, None]).sum(axis=(3, 5)) / (p.B * rq.sum(1))[None, None, :, None]
+    np.testing.assert_allclose(sc.reshape(ref.shape), ref, rtol=1e-12, atol=1e-16)
+
+
+def _padded_mask(p, rp, ci):
+    real = p.token_real()
+    return _block_mask(p, rp, ci) & real[None, None, None, :]
+
+
+@pytest.mark.parametrize("hq,hkv", [(2, 2), (4, 2)])
+def test_padded_attention_matches_masked_sdpa(hq, hkv):
+    """Forward and backward on a padded grid equal torch's masked attention
+    with the padding keys masked out, on the real queries; padding queries
+    give O = 0, LSE = -inf and dQ = 0, padding keys dK = dV = 0, and nothing
+    depends on the padding tokens' contents."""
+    p = padded(hq=hq, hkv=hkv)
+    q, k, v, do = rand_qkv(p, 56)
+    real = p.token_real()
+    rp, ci = _random_csr(p, 57)
+    o, lse = oracle.attn_fwd(q, k, v, p, rp, ci)
+    o, lse = o.reshape(q.shape), lse.reshape(q.shape[:3])
+    do_real = do * real[None, None, :, None]
+    ref, lref, (gq, gk, gv) = _torch_ref(q, k, v, p, _padded_mask(p, rp, ci), do_real)
+    np.testing.assert_allclose(o[:, :, real], ref[:, :, real], rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(lse[:, :, real], lref[:, :, real], rtol=1e-12)
+    assert (o[:, :, ~real] == 0).all() and np.isneginf(lse[:, :, ~real]).all()
+    dq = oracle.attn_bwd_dq(q, k, v, do, p, rp, ci).reshape(q.shape)
+    dk, dv = oracle.attn_bwd_dkdv(q, k, v, do, p, rp, ci)
+    np.testing.assert_allclose(dq[:, :, real], gq[:, :, real], rtol=1e-10, atol=1e-12)
+    assert (dq[:, :, ~real] == 0).all()
+    np.testing.assert_allclose(dk.reshape(gk.shape), gk, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dv.reshape(gv.shape), gv, rtol=1e-10, atol=1e-12)
+    assert (dk.reshape(k.shape)[:, :, ~real] == 0).all() and (dv.reshape(v.shape)[:, :, ~real] == 0).all()
+    gq_, gk_, gv_, gdo = (_garbage_padding(t, p, 58 + i) for i, t in enumerate((q, k, v, do)))
+    o2, _ = oracle.attn_fwd(gq_, gk_, gv_, p, rp, ci)
+    dq2 = oracle.attn_bwd_dq(gq_, gk_, gv_, gdo, p, rp, ci).reshape(q.shape)
+    dk2, dv2 = oracle.attn_bwd_dkdv(gq_, gk_, gv_, gdo, p, rp, ci)
+    np.testing.assert_array_equal(o2.reshape(q.shape), o)
+    np.testing.assert_array_equal(dq2, dq)
+    np.testing.assert_array_equal(dk2, dk)
+    np.testing.assert_array_equal(dv2, dv)
+
+
+def test_padded_gate_merge_bwd_ignores_padding_outputs():
+    """Padding tokens are not outputs: the merge backward equals autograd of
+    the merge restricted to real tokens (dg = 0 on padding)."""
+    p = padded(hq=3, hkv=3)
+    real = p.token_real()
+    rng = np.random.default_rng(62)
+    g = (rng.standard_normal((1, 3, p.L)) * 2).astype(np.float32)
+    oc = rng.standard_normal((1, 3, p.N, p.head_dim)).astype(np.float32)
+    dout = rng.standard_normal((1, 3, p.L, p.head_dim)).astype(np.float32)
+    tg = torch.tensor(g, dtype=torch.float64, requires_grad=True)
+    toc = torch.tensor(oc, dtype=torch.float64, requires_grad=True)
+    out = torch.tanh(tg)[..., None] * toc.repeat_interleave(p.B, dim=2)
+    (out[:, :, torch.from_numpy(real)] * torch.tensor(dout[:, :, real], dtype=torch.float64)).sum().backward()
+    doc, dg = oracle.gate_merge_bwd(g, oc, dout, p)
+    np.testing.assert_allclose(doc, toc.grad.numpy(), rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(dg, tg.grad.numpy(), rtol=1e-12, atol=1e-13)
+    assert (dg[:, :, ~real] == 0).all()
+
+
+@pytest.mark.parametrize("P", [(2, 2, 4), (1, 2, 2), (1, 1, 1)])
+def test_padded_unpool_is_the_adjoint_of_pool(P):
+    """<MeanPool(x), y> = <x, Unpool(y)> for the count-aware pool, padding
+    tokens receive nothing, and MeanPool(Unpool(y)) = y / (real tokens of the
+    sub-cube)."""
+    p = padded()
+    Pt, Ph, Pw = P
+    Gt, Gh, Gw = p.Bt // Pt, p.Bh // Ph, p.Bw // Pw
+    Gp = Gt * Gh * Gw
+    rng = np.random.default_rng(63)
+    x = (rng.integers(-4096, 4096, (1, 2, p.L, p.head_dim)) / 4096.0).astype(np.float32)
+    y = rng.standard_normal((1, 2, p.N * Gp, p.head_dim))
+    px = oracle.pool(x, p, Pt, Ph, Pw).astype(np.float64)
+    ux = oracle.unpool_add(y, np.zeros((1, 2, p.L, p.head_dim)), p, Pt, Ph, Pw)
+    real = p.token_real()
+    assert (ux[:, :, ~real] == 0).all()
+    np.testing.assert_allclose((px * y).sum(), (x.astype(np.float64) * ux).sum(), rtol=1e-12)
+    # real tokens per sub-cube, counted from the token mask
+    rc = real.reshape(p.N, Gt, Pt, Gh, Ph, Gw, Pw).sum(axis=(2, 4, 6)).reshape(p.N * Gp)
+    yy = rng.integers(-64, 64, y.shape) / 8.0
+    back = oracle.pool(oracle.unpool_add(yy, np.zeros((1, 2, p.L, p.head_dim)), p, Pt, Ph, Pw)
+                       .astype(np.float32), p, Pt, Ph, Pw).astype(np.float64)
+    nz = rc > 0
+    np.testing.assert_allclose(back[:, :, nz], yy[:, :, nz] / rc[nz][:, None], rtol=1e-6)
+    assert (back[:, :, ~nz] == 0).all()

@@ -56,7 +56,8 @@ class Problem:
 
     @property
     def L(self) -> int:
-        return self.T * self.H * self.W
+        """Tokens in the cube-major layout, padding included."""
+        return self.N * self.B
 
     @property
     def B(self) -> int:
@@ -64,7 +65,33 @@ class Problem:
 
     @property
     def N(self) -> int:
-        return (self.T // self.Bt) * (self.H // self.Bh) * (self.W // self.Bw)
+        return self.Nt * self.Nh * self.Nw
+
+    @property
+    def Nt(self) -> int:
+        return -(-self.T // self.Bt)
+
+    @property
+    def Nh(self) -> int:
+        return -(-self.H // self.Bh)
+
+    @property
+    def Nw(self) -> int:
+        return -(-self.W // self.Bw)
+
+    @property
+    def padded(self) -> bool:
+        return bool(self.T % self.Bt or self.H % self.Bh or self.W % self.Bw)
+
+    def token_real(self) -> np.ndarray:
+        """bool [L]: token of the cube-major layout inside the real T x H x W grid
+        (a grid not divisible by the cube is padded up, Sec. 2.2)."""
+        n = np.arange(self.N)[:, None]
+        beta = np.arange(self.B)[None, :]
+        nt, nh, nw = n // (self.Nh * self.Nw), (n // self.Nw) % self.Nh, n % self.Nw
+        bt, bh, bw = beta // (self.Bh * self.Bw), (beta // self.Bw) % self.Bh, beta % self.Bw
+        return ((nt * self.Bt + bt < self.T) & (nh * self.Bh + bh < self.H) &
+                (nw * self.Bw + bw < self.W)).reshape(-1)
 
     @property
     def R(self) -> int:
@@ -165,11 +192,15 @@ def make_tensor(p: Problem, seed: int, tensor_id: int, heads: int, with_mean: bo
     jobs = [(b, h) for b in range(p.batch) for h in range(heads)]
     nthr = threads or min(16, os.cpu_count() or 1)
 
+    real = p.token_real() if p.padded else None
+
     def work(bh):
         b, h = bh
         _slab(seed, tensor_id, b, h, p.N, p.B, p.head_dim, with_mean, skewed, out[b, h])
         if p.dtype == BF16:
             out[b, h] = round_bf16_f32(out[b, h])
+        if real is not None:
+            out[b, h][~real] = 0.0          # padding tokens hold zeros
 
     if nthr > 1 and len(jobs) > 1:
         with ThreadPoolExecutor(nthr) as ex:
@@ -221,21 +252,28 @@ def _with_means_of(ref: np.ndarray, p: Problem, seed: int, tensor_id: int, threa
 
 
 def raster_to_cube_major(x: np.ndarray, p: Problem) -> np.ndarray:
-    """[..., T*H*W (raster, w fastest), D] -> [..., N*B (cube-major), D]."""
+    """[..., T*H*W (raster, w fastest), D] -> [..., N*B (cube-major), D]; a grid
+    not divisible by the cube is padded up with zero tokens."""
     lead = x.shape[:-2]
     D = x.shape[-1]
-    Nt, Nh, Nw = p.T // p.Bt, p.H // p.Bh, p.W // p.Bw
-    y = x.reshape(*lead, Nt, p.Bt, Nh, p.Bh, Nw, p.Bw, D)
+    Nt, Nh, Nw = p.Nt, p.Nh, p.Nw
+    g = x.reshape(*lead, p.T, p.H, p.W, D)
+    if p.padded:
+        pad = [(0, 0)] * len(lead) + [(0, Nt * p.Bt - p.T), (0, Nh * p.Bh - p.H), (0, Nw * p.Bw - p.W), (0, 0)]
+        g = np.pad(g, pad)
+    y = g.reshape(*lead, Nt, p.Bt, Nh, p.Bh, Nw, p.Bw, D)
     nd = len(lead)
     perm = list(range(nd)) + [nd + 0, nd + 2, nd + 4, nd + 1, nd + 3, nd + 5, nd + 6]
     return np.ascontiguousarray(y.transpose(perm)).reshape(*lead, p.L, D)
 
 
 def cube_major_to_raster(x: np.ndarray, p: Problem) -> np.ndarray:
+    """Inverse of raster_to_cube_major (padding tokens dropped)."""
     lead = x.shape[:-2]
     D = x.shape[-1]
-    Nt, Nh, Nw = p.T // p.Bt, p.H // p.Bh, p.W // p.Bw
+    Nt, Nh, Nw = p.Nt, p.Nh, p.Nw
     y = x.reshape(*lead, Nt, Nh, Nw, p.Bt, p.Bh, p.Bw, D)
     nd = len(lead)
     perm = list(range(nd)) + [nd + 0, nd + 3, nd + 1, nd + 4, nd + 2, nd + 5, nd + 6]
-    return np.ascontiguousarray(y.transpose(perm)).reshape(*lead, p.L, D)
+    g = np.ascontiguousarray(y.transpose(perm)).reshape(*lead, Nt * p.Bt, Nh * p.Bh, Nw * p.Bw, D)
+    return np.ascontiguousarray(g[..., :p.T, :p.H, :p.W, :]).reshape(*lead, p.T * p.H * p.W, D)
