@@ -42,8 +42,26 @@
  * Supported shapes (other values return VSA2_ERR_UNSUPPORTED):
  *   cube B = Bt*Bh*Bw = 64 tokens; head_dim D in {64, 128};
  *   router score-pooling G = (Bt/Rt)(Bh/Rh)(Bw/Rw) in {1, 2, 4, 8};
- *   N = L/B <= 4096 cubes.  T, H, W must be multiples of Bt, Bh, Bw
- *   (VSA2_ERR_SHAPE otherwise).
+ *   N = L/B <= 4096 cubes for vsa2_route.
+ *
+ * Padded grids (Sec. 2.2, kernel implementation: each axis is padded up to
+ * a multiple of the cube size and the padding is masked out).  T, H, W need
+ * not be multiples of Bt, Bh, Bw: the grid holds Nt = ceil(T/Bt),
+ * Nh = ceil(H/Bh), Nw = ceil(W/Bw) cubes, N = Nt*Nh*Nw, L = N*B, and token
+ * (n, beta) is a padding token when nt*Bt + bt >= T, nh*Bh + bh >= H or
+ * nw*Bw + bw >= W.  Padding tokens may hold any finite values; no output
+ * depends on them.  Every call masks them:
+ *   vsa2_pool / vsa2_unpool_add  average over (spread to) the real tokens of
+ *       each sub-cube only; a sub-cube without one pools to 0;
+ *   vsa2_route  pooled keys without a real token get no score mass, and the
+ *       G x G pooling averages over the pooled queries that hold a real token
+ *       (every row still sums to 1/G);
+ *   vsa2_attn_fwd / _bwd  padding keys are masked out of every softmax;
+ *       padding queries give O = 0, LSE = -inf, dQ = 0; padding keys get
+ *       dK = dV = 0;
+ *   vsa2_gate_merge_bwd  padding tokens are not outputs (dgate = 0, no
+ *       contribution to dO_c_hat).
+ * Every cube holds at least one real token.
  */
 #ifndef VSA2_H
 #define VSA2_H
@@ -114,8 +132,8 @@ const char* vsa2_status_str(vsa2_status s);
  *   x      [batch][heads][L][D], dtype p->dtype, cube-major.
  *   out    [batch][heads][N*Gp][D], Gp = (Bt/Pt)(Bh/Ph)(Bw/Pw); row n*Gp + g
  *          with g = (gt*Gh + gh)*Gw + gw.  Each value is the mean of the
- *          Pt*Ph*Pw tokens of its sub-cube, accumulated in fp64 and rounded
- *          (nearest even) to the dtype.
+ *          Pt*Ph*Pw tokens of its sub-cube (of its real tokens on a padded
+ *          grid), accumulated in fp64 and rounded (nearest even) to the dtype.
  *   heads  number of heads of x (Hq for queries, Hkv for keys).
  * Errors: NULL pointers, P_x not dividing B_x, bad dtype/shape, misalignment.
  */
@@ -307,6 +325,8 @@ vsa2_status vsa2_gate_merge(const vsa2_problem* p, const float* gate, const void
  *   do_c [batch][Hq][N][D] = sum over the B tokens l of each cube of
  *        tanh(gate[l]) dout[l];
  *   dgate [batch][Hq][L] fp32 = (1 - tanh(gate[l])^2) (dout[l] . o_c[cube]).
+ * On a padded grid the sum runs over real tokens and padding tokens get
+ * dgate = 0.
  */
 vsa2_status vsa2_gate_merge_bwd(const vsa2_problem* p, const float* gate, const void* o_c, const void* dout,
                                 void* do_c, float* dgate, hipStream_t stream);
@@ -314,7 +334,9 @@ vsa2_status vsa2_gate_merge_bwd(const vsa2_problem* p, const float* gate, const 
 /*
  * vsa2_unpool_add - the MeanPool adjoint (gradient of vsa2_pool with the
  * same Pt, Ph, Pw): every token of sub-cube (n, g) gets dx_c[n*Gp + g] /
- * (Pt*Ph*Pw) added, in place.
+ * (Pt*Ph*Pw) added, in place (on a padded grid: every real token, divided
+ * by the number of real tokens of the sub-cube; padding tokens are left
+ * unchanged).
  *   dx_c [batch][heads][N*Gp][D]; dx [batch][heads][L][D] (updated).
  */
 vsa2_status vsa2_unpool_add(const vsa2_problem* p, int32_t heads, const void* dx_c, int32_t Pt, int32_t Ph,

@@ -221,7 +221,8 @@ def _ptr(t):
 
 def _dims(p):
     B = p.Bt * p.Bh * p.Bw
-    N = (p.T // p.Bt) * (p.H // p.Bh) * (p.W // p.Bw)
+    # an axis that is not a multiple of its cube size is padded up to one
+    N = (-(-p.T // p.Bt)) * (-(-p.H // p.Bh)) * (-(-p.W // p.Bw))
     G = (p.Bt // p.Rt) * (p.Bh // p.Rh) * (p.Bw // p.Rw)
     return N, B, G
 

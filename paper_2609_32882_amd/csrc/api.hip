@@ -28,11 +28,12 @@ vsa2_status check_problem(const vsa2_problem* p, shape* out) {
     if (p->heads_q % p->heads_kv) return VSA2_ERR_SHAPE;
     if (p->T < 1 || p->H < 1 || p->W < 1 || p->Bt < 1 || p->Bh < 1 || p->Bw < 1) return VSA2_ERR_SHAPE;
     if (p->Rt < 1 || p->Rh < 1 || p->Rw < 1) return VSA2_ERR_SHAPE;
-    if (p->T % p->Bt || p->H % p->Bh || p->W % p->Bw) return VSA2_ERR_SHAPE;
     if (p->Bt % p->Rt || p->Bh % p->Rh || p->Bw % p->Rw) return VSA2_ERR_SHAPE;
     shape s;
     s.B = static_cast<int64_t>(p->Bt) * p->Bh * p->Bw;
-    s.N = static_cast<int64_t>(p->T / p->Bt) * (p->H / p->Bh) * (p->W / p->Bw);
+    // a grid axis that is not a multiple of its cube size is padded up to one
+    s.N = static_cast<int64_t>((p->T + p->Bt - 1) / p->Bt) * ((p->H + p->Bh - 1) / p->Bh) *
+          ((p->W + p->Bw - 1) / p->Bw);
     s.L = s.N * s.B;
     s.G = static_cast<int64_t>(p->Bt / p->Rt) * (p->Bh / p->Rh) * (p->Bw / p->Rw);
     s.rows_q = static_cast<int64_t>(p->batch) * p->heads_q * s.N;
@@ -40,6 +41,10 @@ vsa2_status check_problem(const vsa2_problem* p, shape* out) {
     if (s.N > (1 << 26) || s.rows_q > (int64_t(1) << 31) - 2) return VSA2_ERR_SHAPE;
     *out = s;
     return VSA2_OK;
+}
+
+vsa2::cube_grid grid_of(const vsa2_problem* p) {
+    return vsa2::make_cube_grid(p->T, p->H, p->W, p->Bt, p->Bh, p->Bw);
 }
 
 // Shapes the attention and router kernels are built for.
@@ -132,8 +137,7 @@ vsa2_status vsa2_pool(const vsa2_problem* p, int32_t heads, const void* x, int32
     if (p->head_dim % 8) return VSA2_ERR_UNSUPPORTED;
     if (!aligned16(x) || !aligned16(out)) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_pool(p->dtype, x, out, static_cast<int64_t>(p->batch) * heads,
-                                   static_cast<int>(s.N), p->head_dim, p->Bt, p->Bh, p->Bw, Pt, Ph, Pw,
-                                   stream));
+                                   static_cast<int>(s.N), p->head_dim, grid_of(p), Pt, Ph, Pw, stream));
     return VSA2_OK;
 }
 
@@ -183,7 +187,8 @@ vsa2_status vsa2_route(const vsa2_problem* p, const vsa2_select* sel, const void
     const int N = static_cast<int>(s.N);
 
     VSA2_TRY_HIP(vsa2::launch_route_passes(p->dtype, p->head_dim, static_cast<int>(s.G), q_r, k_r, lse2,
-                                           scores, p->batch, p->heads_q, p->heads_kv, N, stream));
+                                           scores, p->batch, p->heads_q, p->heads_kv, N, grid_of(p), p->Rt,
+                                           p->Rh, p->Rw, stream));
     if (sel->mode == VSA2_SEL_SEQ_TOPK) {
         VSA2_TRY_HIP(vsa2::launch_select_seq(scores, static_cast<int64_t>(p->batch) * p->heads_q, N, sel->k,
                                              base + w.seq, counts, row_ptr, col_idx, col_cap, stream));
@@ -235,7 +240,7 @@ vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, c
     if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_attn_fwd(p->dtype, p->head_dim, q, k, v, row_ptr, col_idx, col_cap, o, lse,
                                        o_lo, ws, p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N),
-                                       stream));
+                                       grid_of(p), stream));
     return VSA2_OK;
 }
 
@@ -260,7 +265,8 @@ vsa2_status vsa2_attn_bwd(const vsa2_problem* p, const void* q, const void* k, c
     if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_attn_bwd(p->dtype, p->head_dim, q, k, v, o, lse, o_lo, dout, row_ptr, col_idx,
                                        kv_ptr, kv_idx, col_cap, dq, dk, dv, ws,
-                                       p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N), stream));
+                                       p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N), grid_of(p),
+                                       stream));
     return VSA2_OK;
 }
 
@@ -298,7 +304,7 @@ vsa2_status vsa2_attn_bwd_dkdv(const vsa2_problem* p, const void* q, const void*
     if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_attn_bwd_dkdv(p->dtype, p->head_dim, compensated != 0, q, k, v, dout, kv_ptr,
                                             kv_idx, col_cap, dk, dv, ws, p->batch, p->heads_q, p->heads_kv,
-                                            static_cast<int>(s.N), stream));
+                                            static_cast<int>(s.N), grid_of(p), stream));
     return VSA2_OK;
 }
 
@@ -319,7 +325,7 @@ vsa2_status vsa2_attn_bwd_dq(const vsa2_problem* p, const void* q, const void* k
     if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_attn_bwd_dq(p->dtype, p->head_dim, compensated != 0, q, k, v, dout, row_ptr,
                                           col_idx, col_cap, dq, ws, p->batch, p->heads_q, p->heads_kv,
-                                          static_cast<int>(s.N), stream));
+                                          static_cast<int>(s.N), grid_of(p), stream));
     return VSA2_OK;
 }
 
@@ -378,7 +384,7 @@ vsa2_status vsa2_gate_merge_bwd(const vsa2_problem* p, const float* gate, const 
     if (!gate || !o_c || !dout || !do_c || !dgate) return VSA2_ERR_NULL;
     if (!aligned16(o_c) || !aligned16(dout) || !aligned16(do_c)) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_gate_merge_bwd(p->dtype, p->head_dim, gate, o_c, dout, do_c, dgate, s.rows_q,
-                                             stream));
+                                             static_cast<int>(s.N), grid_of(p), stream));
     return VSA2_OK;
 }
 
@@ -393,8 +399,8 @@ vsa2_status vsa2_unpool_add(const vsa2_problem* p, int32_t heads, const void* dx
     if (p->head_dim != 64 && p->head_dim != 128) return VSA2_ERR_UNSUPPORTED;
     if (!aligned16(dx_c) || !aligned16(dx)) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_unpool_add(p->dtype, p->head_dim, dx_c, dx,
-                                         static_cast<int64_t>(p->batch) * heads * s.L, p->Bt, p->Bh, p->Bw, Pt,
-                                         Ph, Pw, stream));
+                                         static_cast<int64_t>(p->batch) * heads * s.L, static_cast<int>(s.N),
+                                         grid_of(p), Pt, Ph, Pw, stream));
     return VSA2_OK;
 }
 

@@ -20,6 +20,8 @@
 // the same tiles with transposing LDS reads.  Tiles stream into LDS with
 // asynchronous global_load_lds copies; each buffer is refilled as soon as
 // its last reader is done.
+#include <type_traits>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -30,7 +32,10 @@ constexpr float kLog2e = 1.4426950408889634f;
 
 // ---------------------------------------------------------------------------
 // stat[l] = (LSE_l * log2(e), dO_l . O_l); 16 lanes per token (D <= 128).
-// With the forward's rounding remainder o_lo, O_l = o_l + o_lo_l.
+// With the forward's rounding remainder o_lo, O_l = o_l + o_lo_l.  A token
+// without attention mass (LSE = -inf: a padding query, or an empty row)
+// gets +inf, so every probability 2^(s - stat.x) the backward forms for it
+// is 0.
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 __global__ __launch_bounds__(256) void stat_kernel(const T* __restrict__ o, const T* __restrict__ o_lo,
@@ -55,7 +60,10 @@ __global__ __launch_bounds__(256) void stat_kernel(const T* __restrict__ o, cons
     }
 #pragma unroll
     for (int off = LPT / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
-    if (tok < ntok && part == 0) stat[tok] = make_float2(lse[tok] * kLog2e, s);
+    if (tok < ntok && part == 0) {
+        const float x = lse[tok];
+        stat[tok] = make_float2(x == -INFINITY ? INFINITY : x * kLog2e, s);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -66,15 +74,18 @@ __global__ __launch_bounds__(256) void stat_kernel(const T* __restrict__ o, cons
 //   P = exp2(S c - LSE log2 e), dS = P (dP - Delta)
 //   dV^T += dO^T P,  dK^T += Q^T dS   (dO^T, Q^T read transposed from LDS)
 // The Q / dO / stat tiles are double-buffered: the copies of the next query
-// block stream in during the whole of the current one.
+// block stream in during the whole of the current one.  On a padded grid,
+// padding keys get dK = dV = 0 and padding queries (stat.x = +inf) add
+// nothing.  (PAD: the grid is padded; the masking is compiled only into
+// that variant.)
 // ---------------------------------------------------------------------------
-template <typename T, int D, bool COMP>
+template <typename T, int D, bool COMP, bool PAD>
 __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float2* __restrict__ stat,
     const int32_t* __restrict__ kv_ptr, const int32_t* __restrict__ kv_idx, int64_t col_cap,
     T* __restrict__ dk, T* __restrict__ dv, int Hq, int Hkv, int N, float c_log2, float scale,
-    const int32_t* __restrict__ order) {
+    const int32_t* __restrict__ order, cube_grid grid) {
     using F = typename frag_of<T>::type;
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;
@@ -94,6 +105,8 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
     const int grp = Hq / Hkv;
     const int64_t L = static_cast<int64_t>(N) * 64;
     const int64_t ktok = bkv * L + static_cast<int64_t>(nk) * 64 + wave * 32 + (lane & 31);
+    bool k_real = true;
+    if constexpr (PAD) k_real = (cube_real_mask(grid, nk, lane) >> (wave * 32 + (lane & 31))) & 1;
 
     int64_t e0 = kv_ptr[krow], e1 = kv_ptr[krow + 1];
     e0 = e0 < 0 ? 0 : (e0 > col_cap ? col_cap : e0);
@@ -264,8 +277,8 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
             float av[4], kx[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                av[i] = acc_v[mt][g4 * 4 + i];
-                kx[i] = acc_k[mt][g4 * 4 + i] * scale;
+                av[i] = k_real ? acc_v[mt][g4 * 4 + i] : 0.f;
+                kx[i] = k_real ? acc_k[mt][g4 * 4 + i] * scale : 0.f;
             }
             if constexpr (E == 2) {
                 *reinterpret_cast<uint2*>(krow_v + d0) =
@@ -281,15 +294,17 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
 
 // ---------------------------------------------------------------------------
 // dQ: one workgroup (2 waves) per query block; wave owns 32 queries.
-// Tiles K (for S^T and, read transposed, K^T) and V (for dP^T).
+// Tiles K (for S^T and, read transposed, K^T) and V (for dP^T).  On a
+// padded grid, padding keys get P = 0 and padding queries dQ = 0 (PAD
+// variant only).
 // ---------------------------------------------------------------------------
-template <typename T, int D, bool COMP>
+template <typename T, int D, bool COMP, bool PAD>
 __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float2* __restrict__ stat,
     const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx, int64_t col_cap,
     T* __restrict__ dq, int Hq, int Hkv, int N, float c_log2, float scale, int period,
-    const int32_t* __restrict__ order) {
+    const int32_t* __restrict__ order, cube_grid grid) {
     using F = typename frag_of<T>::type;
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;
@@ -310,6 +325,8 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     const char* kb = reinterpret_cast<const char*>(k + static_cast<int64_t>(b * Hkv + hkv) * L * D);
     const char* vb = reinterpret_cast<const char*>(v + static_cast<int64_t>(b * Hkv + hkv) * L * D);
     const int64_t qtok = bh * L + static_cast<int64_t>(n) * 64 + wave * 32 + (lane & 31);
+    bool q_real = true;
+    if constexpr (PAD) q_real = (cube_real_mask(grid, n, lane) >> (wave * 32 + (lane & 31))) & 1;
 
     int64_t e0 = row_ptr[row], e1 = row_ptr[row + 1];
     e0 = e0 < 0 ? 0 : (e0 > col_cap ? col_cap : e0);
@@ -320,6 +337,16 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     for (int ks = 0; ks < KS; ++ks) {
         load_frag(qf[ks], q + qtok * D + ks * 16 + half * 8);
         load_frag(of[ks], dout + qtok * D + ks * 16 + half * 8);
+    }
+    if constexpr (PAD) {
+        if (!q_real) {          // a padding query computes with zero vectors
+            const float z[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                pack_frag(qf[ks], z);
+                pack_frag(of[ks], z);
+            }
+        }
     }
     const float2 st = stat[qtok];
     f32x16_t dqa[MT];
@@ -359,6 +386,8 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
 
         vm_wait<0>();                   // K and V landed
         wg_barrier();
+        // padding keys of a cut cube (bit = key within the block)
+        const uint64_t kmask = PAD && c_cur >= 0 ? cube_real_mask(grid, c_cur, lane) : ~0ull;
         F sb[2][2];
         F sl[SPLIT ? 2 : 1][2];
 #pragma unroll
@@ -391,6 +420,11 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
             for (int i = 0; i < 16; ++i) {
                 const float p = fast_exp2(s[i] * c_log2 - st.x);
                 ds[i] = p * (dp[i] - st.y);
+            }
+            if constexpr (PAD) {        // branch-free: a branch here costs registers
+                const uint32_t lm = static_cast<uint32_t>(kmask >> (t2 * 32 + half * 8));
+#pragma unroll
+                for (int i = 0; i < 16; ++i) ds[i] = ((lm >> ((i >> 3) * 16 + (i & 7))) & 1u) ? ds[i] : 0.f;
             }
             if constexpr (SPLIT) {
                 pack_frag_hilo(sb[t2][0], sl[t2][0], ds);
@@ -432,14 +466,13 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
             const int d0 = mt * 32 + g4 * 8 + half * 4;
+            float x[4];                                    // a padding query has dQ = 0
+#pragma unroll
+            for (int i = 0; i < 4; ++i) x[i] = q_real ? dqa[mt][g4 * 4 + i] * scale : 0.f;
             if constexpr (E == 2) {
-                const uint32_t w0 = pack2_bf16(dqa[mt][g4 * 4 + 0] * scale, dqa[mt][g4 * 4 + 1] * scale);
-                const uint32_t w1 = pack2_bf16(dqa[mt][g4 * 4 + 2] * scale, dqa[mt][g4 * 4 + 3] * scale);
-                *reinterpret_cast<uint2*>(dqrow + d0) = make_uint2(w0, w1);
+                *reinterpret_cast<uint2*>(dqrow + d0) = make_uint2(pack2_bf16(x[0], x[1]), pack2_bf16(x[2], x[3]));
             } else {
-                *reinterpret_cast<float4*>(dqrow + d0) =
-                    make_float4(dqa[mt][g4 * 4] * scale, dqa[mt][g4 * 4 + 1] * scale,
-                                dqa[mt][g4 * 4 + 2] * scale, dqa[mt][g4 * 4 + 3] * scale);
+                *reinterpret_cast<float4*>(dqrow + d0) = make_float4(x[0], x[1], x[2], x[3]);
             }
         }
 }
@@ -482,7 +515,8 @@ static hipError_t launch_prep_t(const void* o, const float* lse, const void* o_l
 template <typename T, int D, bool COMP>
 static hipError_t launch_dkdv_t(const void* q, const void* k, const void* v, const void* dout,
                                 const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap, void* dk,
-                                void* dv, void* ws, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                                void* dv, void* ws, int batch, int Hq, int Hkv, int N, const cube_grid& cg,
+                                hipStream_t s) {
     const int64_t krows = static_cast<int64_t>(batch) * Hkv * N;
     if (krows == 0) return hipSuccess;
     int32_t* order = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + bwd_ws_csc_order_offset(batch, Hq, N));
@@ -490,10 +524,14 @@ static hipError_t launch_dkdv_t(const void* q, const void* k, const void* v, con
     if (e != hipSuccess) return e;
     const float c = kLog2e / sqrtf(static_cast<float>(D));
     const float scale = 1.0f / sqrtf(static_cast<float>(D));
-    hipLaunchKernelGGL((dkdv_kernel<T, D, COMP>), dim3(static_cast<unsigned>(krows)), dim3(AB_NT), 0, s,
-                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
-                       static_cast<const T*>(dout), static_cast<const float2*>(ws), kv_ptr, kv_idx, col_cap,
-                       static_cast<T*>(dk), static_cast<T*>(dv), Hq, Hkv, N, c, scale, order);
+    auto go = [&](auto pad) {
+        hipLaunchKernelGGL((dkdv_kernel<T, D, COMP, decltype(pad)::value>), dim3(static_cast<unsigned>(krows)),
+                           dim3(AB_NT), 0, s, static_cast<const T*>(q), static_cast<const T*>(k),
+                           static_cast<const T*>(v), static_cast<const T*>(dout), static_cast<const float2*>(ws),
+                           kv_ptr, kv_idx, col_cap, static_cast<T*>(dk), static_cast<T*>(dv), Hq, Hkv, N, c, scale,
+                           order, cg);
+    };
+    if (cg.padded) go(std::true_type{}); else go(std::false_type{});
     return hipGetLastError();
 }
 
@@ -501,7 +539,7 @@ static hipError_t launch_dkdv_t(const void* q, const void* k, const void* v, con
 template <typename T, int D, bool COMP>
 static hipError_t launch_dq_t(const void* q, const void* k, const void* v, const void* dout,
                               const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* dq,
-                              void* ws, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                              void* ws, int batch, int Hq, int Hkv, int N, const cube_grid& cg, hipStream_t s) {
     const int64_t qrows = static_cast<int64_t>(batch) * Hq * N;
     if (qrows == 0) return hipSuccess;
     int32_t* order = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + bwd_ws_csr_order_offset(batch, Hq, N));
@@ -509,11 +547,15 @@ static hipError_t launch_dq_t(const void* q, const void* k, const void* v, const
     if (e != hipSuccess) return e;
     const float c = kLog2e / sqrtf(static_cast<float>(D));
     const float scale = 1.0f / sqrtf(static_cast<float>(D));
-    hipLaunchKernelGGL((dq_kernel<T, D, COMP>), dim3(static_cast<unsigned>(qrows)), dim3(AB_NT), 0, s,
-                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
-                       static_cast<const T*>(dout), static_cast<const float2*>(ws), row_ptr, col_idx, col_cap,
-                       static_cast<T*>(dq), Hq, Hkv, N, c, scale, resident_per_xcd<dq_kernel<T, D, COMP>>(AB_NT),
-                       order);
+    auto go = [&](auto pad) {
+        constexpr bool P = decltype(pad)::value;
+        hipLaunchKernelGGL((dq_kernel<T, D, COMP, P>), dim3(static_cast<unsigned>(qrows)), dim3(AB_NT), 0, s,
+                           static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+                           static_cast<const T*>(dout), static_cast<const float2*>(ws), row_ptr, col_idx, col_cap,
+                           static_cast<T*>(dq), Hq, Hkv, N, c, scale,
+                           resident_per_xcd<dq_kernel<T, D, COMP, P>>(AB_NT), order, cg);
+    };
+    if (cg.padded) go(std::true_type{}); else go(std::false_type{});
     return hipGetLastError();
 }
 
@@ -541,20 +583,21 @@ hipError_t launch_attn_bwd_prep(int dtype, int D, const void* o, const float* ls
 hipError_t launch_attn_bwd_dkdv(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
                                 const void* dout, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
                                 void* dk, void* dv, void* ws, int batch, int Hq, int Hkv, int N,
-                                hipStream_t s) {
+                                const cube_grid& cg, hipStream_t s) {
     VSA2_DISPATCH_TD(return comp ? launch_dkdv_t<T, DD, true>(q, k, v, dout, kv_ptr, kv_idx, col_cap, dk, dv, ws,
-                                                              batch, Hq, Hkv, N, s)
+                                                              batch, Hq, Hkv, N, cg, s)
                                  : launch_dkdv_t<T, DD, false>(q, k, v, dout, kv_ptr, kv_idx, col_cap, dk, dv, ws,
-                                                               batch, Hq, Hkv, N, s));
+                                                               batch, Hq, Hkv, N, cg, s));
 }
 
 hipError_t launch_attn_bwd_dq(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
                               const void* dout, const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
-                              void* dq, void* ws, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                              void* dq, void* ws, int batch, int Hq, int Hkv, int N, const cube_grid& cg,
+                              hipStream_t s) {
     VSA2_DISPATCH_TD(return comp ? launch_dq_t<T, DD, true>(q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws,
-                                                            batch, Hq, Hkv, N, s)
+                                                            batch, Hq, Hkv, N, cg, s)
                                  : launch_dq_t<T, DD, false>(q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws,
-                                                             batch, Hq, Hkv, N, s));
+                                                             batch, Hq, Hkv, N, cg, s));
 }
 #undef VSA2_DISPATCH_TD
 
@@ -563,15 +606,15 @@ hipError_t launch_attn_bwd(int dtype, int D, const void* q, const void* k, const
                            const float* lse, const void* o_lo, const void* dout, const int32_t* row_ptr,
                            const int32_t* col_idx, const int32_t* kv_ptr, const int32_t* kv_idx,
                            int64_t col_cap, void* dq, void* dk, void* dv, void* ws, int batch,
-                           int Hq, int Hkv, int N, hipStream_t s) {
+                           int Hq, int Hkv, int N, const cube_grid& cg, hipStream_t s) {
     hipError_t e = launch_attn_bwd_prep(dtype, D, o, lse, o_lo, dout, ws, batch, Hq, N, s);
     if (e != hipSuccess) return e;
     const bool comp = o_lo != nullptr;
     e = launch_attn_bwd_dkdv(dtype, D, comp, q, k, v, dout, kv_ptr, kv_idx, col_cap, dk, dv, ws, batch, Hq, Hkv,
-                             N, s);
+                             N, cg, s);
     if (e != hipSuccess) return e;
     return launch_attn_bwd_dq(dtype, D, comp, q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws, batch, Hq, Hkv,
-                              N, s);
+                              N, cg, s);
 }
 
 }  // namespace vsa2

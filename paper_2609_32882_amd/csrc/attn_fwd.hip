@@ -15,6 +15,8 @@
 // during the next S product.
 // In the transposed products a lane owns one query column, so the row max
 // and row sum need one exchange with the other half-wave and nothing else.
+// On a padded grid the padding keys of a cut cube are masked out of the
+// softmax, and padding queries give O = 0 and LSE = -inf.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -25,12 +27,14 @@ constexpr int AF_NT = 128;
 // COMP (compensated): P enters the PV product as two bf16 terms (hi + lo),
 // and the rounding remainder of O is written to o_lo, so that O + o_lo
 // carries about 16 significant bits for the backward's Delta = dO . O.
-template <typename T, int D, bool COMP>
+// PAD: the grid is padded (the masking is compiled only into this variant,
+// so the unpadded one keeps its register budget).
+template <typename T, int D, bool COMP, bool PAD>
 __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx, int64_t col_cap,
     T* __restrict__ o, float* __restrict__ lse, T* __restrict__ o_lo, int Hq, int Hkv, int N, float c_log2,
-    int period, const int32_t* __restrict__ order) {
+    int period, const int32_t* __restrict__ order, cube_grid grid) {
     using F = typename frag_of<T>::type;
     constexpr bool SPLIT = COMP && sizeof(T) == 2;
     constexpr int E = sizeof(T);
@@ -52,6 +56,8 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     const char* kb = reinterpret_cast<const char*>(k + static_cast<int64_t>(b * Hkv + hkv) * L * D);
     const char* vb = reinterpret_cast<const char*>(v + static_cast<int64_t>(b * Hkv + hkv) * L * D);
     const int64_t qtok = bh * L + static_cast<int64_t>(n) * 64 + wave * 32 + (lane & 31);
+    bool q_real = true;
+    if constexpr (PAD) q_real = (cube_real_mask(grid, n, lane) >> (wave * 32 + (lane & 31))) & 1;
 
     int64_t e0 = row_ptr[row], e1 = row_ptr[row + 1];
     e0 = e0 < 0 ? 0 : (e0 > col_cap ? col_cap : e0);
@@ -60,6 +66,16 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     F qf[KS];
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) load_frag(qf[ks], q + qtok * D + ks * 16 + half * 8);
+    if constexpr (PAD) {
+        // a padding query computes with a zero vector (its output is 0
+        // anyway), so the wave's shared rescale decisions never depend on
+        // what the padding holds
+        if (!q_real) {
+            const float z[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) pack_frag(qf[ks], z);
+        }
+    }
 
     f32x16_t oacc[MT];
 #pragma unroll
@@ -125,6 +141,18 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
         if (has_next) kt.issue(k_lds, kb + nxt_off, wave);
 
         if (c_cur >= 0) {
+            // padding keys of a cut cube: key of entry i of tile t2 is
+            // 32 t2 + 16 (i / 8) + 8 half + i % 8
+            if constexpr (PAD) {        // branch-free: a branch here costs registers
+                const uint64_t kmask = cube_real_mask(grid, c_cur, lane);
+#pragma unroll
+                for (int t2 = 0; t2 < 2; ++t2) {
+                    const uint32_t lm = static_cast<uint32_t>(kmask >> (t2 * 32 + half * 8));
+#pragma unroll
+                    for (int i = 0; i < 16; ++i)
+                        s[t2][i] = ((lm >> ((i >> 3) * 16 + (i & 7))) & 1u) ? s[t2][i] : -INFINITY;
+                }
+            }
             // Online softmax in log2 units with a lazily updated running max:
             // the accumulators are rescaled only when the block max exceeds
             // the running max m by more than 2^8 (any lane of the wave), so
@@ -191,7 +219,7 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
         c_cur = c_next;
     }
 
-    const float lt = l + swap_half(l);
+    const float lt = q_real ? l + swap_half(l) : 0.f;     // a padding query has no output
     const float inv = lt > 0.f ? 1.0f / lt : 0.f;
     T* orow = o + qtok * D;
 #pragma unroll
@@ -201,7 +229,7 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
             const int d0 = mt * 32 + g4 * 8 + half * 4;
             float ov[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) ov[j] = oacc[mt][g4 * 4 + j] * inv;
+            for (int j = 0; j < 4; ++j) ov[j] = q_real ? oacc[mt][g4 * 4 + j] * inv : 0.f;
             if constexpr (E == 2) {
                 const uint32_t w0 = pack2_bf16(ov[0], ov[1]);
                 const uint32_t w1 = pack2_bf16(ov[2], ov[3]);
@@ -222,39 +250,47 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     if (half == 0) lse[qtok] = lt > 0.f ? (m + log2f(lt)) * 0.6931471805599453f : -INFINITY;
 }
 
+template <typename T, int D, bool COMP, bool PAD>
+static void launch_fwd_k(const void* q, const void* k, const void* v, const int32_t* row_ptr, const int32_t* col_idx,
+                         int64_t col_cap, void* o, float* lse, void* o_lo, const int32_t* order, int64_t rows, int Hq,
+                         int Hkv, int N, const cube_grid& cg, hipStream_t s) {
+    const float c = 1.4426950408889634f / sqrtf(static_cast<float>(D));
+    hipLaunchKernelGGL((attn_fwd_kernel<T, D, COMP, PAD>), dim3(static_cast<unsigned>(rows)), dim3(AF_NT), 0, s,
+                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), row_ptr,
+                       col_idx, col_cap, static_cast<T*>(o), lse, static_cast<T*>(o_lo), Hq, Hkv, N, c,
+                       resident_per_xcd<attn_fwd_kernel<T, D, COMP, PAD>>(AF_NT), order, cg);
+}
+
 template <typename T, int D>
 static hipError_t launch_fwd_t(const void* q, const void* k, const void* v, const int32_t* row_ptr,
                                const int32_t* col_idx, int64_t col_cap, void* o, float* lse, void* o_lo,
-                               int32_t* order, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                               int32_t* order, int batch, int Hq, int Hkv, int N, const cube_grid& cg,
+                               hipStream_t s) {
     const int64_t rows = static_cast<int64_t>(batch) * Hq * N;
     if (rows == 0) return hipSuccess;
     hipError_t e = launch_lpt_order(row_ptr, rows, N, col_cap, order, s);
     if (e != hipSuccess) return e;
-    const float c = 1.4426950408889634f / sqrtf(static_cast<float>(D));
-    if (o_lo)
-        hipLaunchKernelGGL((attn_fwd_kernel<T, D, true>), dim3(static_cast<unsigned>(rows)), dim3(AF_NT), 0, s,
-                           static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
-                           row_ptr, col_idx, col_cap, static_cast<T*>(o), lse, static_cast<T*>(o_lo), Hq, Hkv,
-                           N, c, resident_per_xcd<attn_fwd_kernel<T, D, true>>(AF_NT), order);
-    else
-        hipLaunchKernelGGL((attn_fwd_kernel<T, D, false>), dim3(static_cast<unsigned>(rows)), dim3(AF_NT), 0, s,
-                           static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
-                           row_ptr, col_idx, col_cap, static_cast<T*>(o), lse, nullptr, Hq, Hkv, N, c,
-                           resident_per_xcd<attn_fwd_kernel<T, D, false>>(AF_NT), order);
+    if (o_lo) {
+        if (cg.padded) launch_fwd_k<T, D, true, true>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, rows, Hq, Hkv, N, cg, s);
+        else launch_fwd_k<T, D, true, false>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, rows, Hq, Hkv, N, cg, s);
+    } else {
+        if (cg.padded) launch_fwd_k<T, D, false, true>(q, k, v, row_ptr, col_idx, col_cap, o, lse, nullptr, order, rows, Hq, Hkv, N, cg, s);
+        else launch_fwd_k<T, D, false, false>(q, k, v, row_ptr, col_idx, col_cap, o, lse, nullptr, order, rows, Hq, Hkv, N, cg, s);
+    }
     return hipGetLastError();
 }
 
 hipError_t launch_attn_fwd(int dtype, int D, const void* q, const void* k, const void* v,
                            const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
                            float* lse, void* o_lo, void* ws, int batch, int Hq, int Hkv, int N,
-                           hipStream_t s) {
+                           const cube_grid& cg, hipStream_t s) {
     int32_t* order = static_cast<int32_t*>(ws);
     if (dtype == 1) {
-        if (D == 64) return launch_fwd_t<bf16_t, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, batch, Hq, Hkv, N, s);
-        if (D == 128) return launch_fwd_t<bf16_t, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, batch, Hq, Hkv, N, s);
+        if (D == 64) return launch_fwd_t<bf16_t, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, batch, Hq, Hkv, N, cg, s);
+        if (D == 128) return launch_fwd_t<bf16_t, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, batch, Hq, Hkv, N, cg, s);
     } else {
-        if (D == 64) return launch_fwd_t<float, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, batch, Hq, Hkv, N, s);
-        if (D == 128) return launch_fwd_t<float, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, batch, Hq, Hkv, N, s);
+        if (D == 64) return launch_fwd_t<float, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, batch, Hq, Hkv, N, cg, s);
+        if (D == 128) return launch_fwd_t<float, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, batch, Hq, Hkv, N, cg, s);
     }
     return hipErrorInvalidValue;
 }

@@ -420,14 +420,17 @@ template <typename T, int D>
 __global__ __launch_bounds__(256) void gate_merge_bwd_kernel(const float* __restrict__ gate,
                                                              const T* __restrict__ oc,
                                                              const T* __restrict__ dout, T* __restrict__ doc,
-                                                             float* __restrict__ dgate) {
+                                                             float* __restrict__ dgate, int N, cube_grid grid) {
     constexpr int PER = D / 4;
     __shared__ float part[64][D + 1];
     const int tid = threadIdx.x;
     const int64_t cube = blockIdx.x;                 // (b * Hq + h) * N + n
     const int t = tid >> 2, q4 = tid & 3;
     const int64_t tok = cube * 64 + t;
-    const float gv = tanhf(gate[tok]);
+    // a padding token of a padded grid is not an output: gate 0, dgate 0
+    bool real = true;
+    if (grid.padded) real = token_in(grid, cube_extent(grid, static_cast<int>(cube % N)), t);
+    const float gv = real ? tanhf(gate[tok]) : 0.f;
     const T* dl = dout + tok * D + q4 * PER;
     const T* c = oc + cube * D + q4 * PER;
     float dot = 0.f;
@@ -435,11 +438,11 @@ __global__ __launch_bounds__(256) void gate_merge_bwd_kernel(const float* __rest
     for (int i = 0; i < PER; ++i) {
         const float x = to_f32(dl[i]);
         dot = fmaf(x, to_f32(c[i]), dot);
-        part[t][q4 * PER + i] = gv * x;
+        part[t][q4 * PER + i] = real ? gv * x : 0.f;
     }
     dot += __shfl_xor(dot, 1, 64);
     dot += __shfl_xor(dot, 2, 64);
-    if (q4 == 0) dgate[tok] = (1.0f - gv * gv) * dot;
+    if (q4 == 0) dgate[tok] = real ? (1.0f - gv * gv) * dot : 0.f;
     __syncthreads();
     for (int d = tid; d < D; d += 256) {
         float s = 0.f;
@@ -449,15 +452,17 @@ __global__ __launch_bounds__(256) void gate_merge_bwd_kernel(const float* __rest
 }
 
 // MeanPool adjoint: dx[token] += dxc[n * Gp + g(token)] / P, one thread per
-// 8 elements of a token.
+// 8 elements of a token.  On a padded grid P counts the real tokens of the
+// sub-cube and padding tokens receive nothing.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void unpool_add_kernel(const T* __restrict__ dxc, T* __restrict__ dx,
-                                                         int64_t ntok, int Bt, int Bh, int Bw, int Pt, int Ph,
-                                                         int Pw) {
+                                                         int64_t ntok, int N, int Pt, int Ph, int Pw,
+                                                         cube_grid grid) {
     constexpr int PARTS = D / 8;
     const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     const int64_t tok = t / PARTS;
     if (tok >= ntok) return;
+    const int Bt = grid.Bt, Bh = grid.Bh, Bw = grid.Bw;
     const int d0 = static_cast<int>(t % PARTS) * 8;
     const int B = Bt * Bh * Bw;
     const int64_t cube = tok / B;
@@ -465,7 +470,14 @@ __global__ __launch_bounds__(256) void unpool_add_kernel(const T* __restrict__ d
     const int bw = beta % Bw, bhh = (beta / Bw) % Bh, bt = beta / (Bw * Bh);
     const int Gh = Bh / Ph, Gw = Bw / Pw, Gp = (Bt / Pt) * Gh * Gw;
     const int g = ((bt / Pt) * Gh + bhh / Ph) * Gw + bw / Pw;
-    const float inv = 1.0f / static_cast<float>(Pt * Ph * Pw);
+    int cnt = Pt * Ph * Pw;
+    if (grid.padded) {
+        const int3 e = cube_extent(grid, static_cast<int>(cube % N));
+        if (!token_in(grid, e, beta)) return;
+        const int ot = (bt / Pt) * Pt, oh = (bhh / Ph) * Ph, ow = (bw / Pw) * Pw;   // sub-cube origin
+        cnt = min(Pt, e.x - ot) * min(Ph, e.y - oh) * min(Pw, e.z - ow);
+    }
+    const float inv = 1.0f / static_cast<float>(cnt);
     const T* src = dxc + (cube * Gp + g) * D + d0;
     T* dst = dx + tok * D + d0;
 #pragma unroll
@@ -533,21 +545,21 @@ hipError_t launch_gate_merge(int dtype, int D, const float* gate, const void* oc
 }
 
 hipError_t launch_gate_merge_bwd(int dtype, int D, const float* gate, const void* oc, const void* dout, void* doc,
-                                 float* dgate, int64_t ncubes, hipStream_t s) {
+                                 float* dgate, int64_t ncubes, int N, const cube_grid& cg, hipStream_t s) {
     if (ncubes == 0) return hipSuccess;
     VSA2_COARSE_DISPATCH(hipLaunchKernelGGL((gate_merge_bwd_kernel<T, DD>), dim3(static_cast<unsigned>(ncubes)),
                                             dim3(256), 0, s, gate, static_cast<const T*>(oc),
-                                            static_cast<const T*>(dout), static_cast<T*>(doc), dgate);
+                                            static_cast<const T*>(dout), static_cast<T*>(doc), dgate, N, cg);
                          return hipGetLastError());
 }
 
-hipError_t launch_unpool_add(int dtype, int D, const void* dxc, void* dx, int64_t ntok, int Bt, int Bh, int Bw,
-                             int Pt, int Ph, int Pw, hipStream_t s) {
+hipError_t launch_unpool_add(int dtype, int D, const void* dxc, void* dx, int64_t ntok, int N,
+                             const cube_grid& cg, int Pt, int Ph, int Pw, hipStream_t s) {
     if (ntok == 0) return hipSuccess;
     const unsigned blocks = static_cast<unsigned>((ntok * (D / 8) + 255) / 256);
     VSA2_COARSE_DISPATCH(hipLaunchKernelGGL((unpool_add_kernel<T, DD>), dim3(blocks), dim3(256), 0, s,
-                                            static_cast<const T*>(dxc), static_cast<T*>(dx), ntok, Bt, Bh, Bw, Pt,
-                                            Ph, Pw);
+                                            static_cast<const T*>(dxc), static_cast<T*>(dx), ntok, N, Pt, Ph, Pw,
+                                            cg);
                          return hipGetLastError());
 }
 #undef VSA2_COARSE_DISPATCH

@@ -6,6 +6,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "internal.hpp"
+
 namespace vsa2 {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
@@ -525,6 +527,35 @@ __device__ __forceinline__ void lds_frag_s(frag_f32& f, const char* tile, int ro
     const float4 b = *reinterpret_cast<const float4*>(tile + row * (RB + 16) + e0 * 4 + 16);
     f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
     f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
+}
+
+// ---------------------------------------------------------------------------
+// Padded grids.  Real extent (rt, rh, rw) of cube n (index within a head).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int3 cube_extent(const cube_grid& g, int n) {
+    const int nw = n % g.Nw, r = n / g.Nw;
+    const int nh = r % g.Nh, nt = r / g.Nh;
+    return make_int3(min(g.Bt, g.T - nt * g.Bt), min(g.Bh, g.H - nh * g.Bh), min(g.Bw, g.W - nw * g.Bw));
+}
+
+__device__ __forceinline__ bool cube_is_full(const cube_grid& g, int3 e) {
+    return e.x == g.Bt && e.y == g.Bh && e.z == g.Bw;
+}
+
+// Token beta (in-cube raster index) of a cube with extent e is real.
+__device__ __forceinline__ bool token_in(const cube_grid& g, int3 e, int beta) {
+    const int bw = beta % g.Bw, r = beta / g.Bw;
+    const int bh = r % g.Bh, bt = r / g.Bh;
+    return bt < e.x && bh < e.y && bw < e.z;
+}
+
+// Bit beta set for each real token of 64-token cube n.  Called by a whole
+// wave (lane = its lane index); the result is wave-uniform.
+__device__ __forceinline__ uint64_t cube_real_mask(const cube_grid& g, int n, int lane) {
+    if (!g.padded) return ~0ull;
+    const int3 e = cube_extent(g, n);
+    if (cube_is_full(g, e)) return ~0ull;
+    return __ballot(token_in(g, e, lane));
 }
 
 }  // namespace vsa2

@@ -9,6 +9,29 @@
 
 namespace vsa2 {
 
+// A T x H x W grid cut into Bt x Bh x Bw cubes (Sec. 2.2).  An axis that
+// is not a multiple of its cube size is padded up to one, so the grid holds
+// Nt x Nh x Nw cubes in cube-major order (n = (nt*Nh + nh)*Nw + nw, tokens
+// of a cube in (bt, bh, bw) raster order).  The real tokens of a cube form
+// the box [0, rt) x [0, rh) x [0, rw) of its in-cube coordinates; only the
+// last cube along a padded axis is cut, and every cube holds a real token.
+struct cube_grid {
+    int T, H, W;
+    int Bt, Bh, Bw;
+    int Nh, Nw;
+    int padded;     // some axis is not a multiple of its cube size
+};
+
+inline cube_grid make_cube_grid(int T, int H, int W, int Bt, int Bh, int Bw) {
+    cube_grid g;
+    g.T = T; g.H = H; g.W = W;
+    g.Bt = Bt; g.Bh = Bh; g.Bw = Bw;
+    g.Nh = (H + Bh - 1) / Bh;
+    g.Nw = (W + Bw - 1) / Bw;
+    g.padded = (T % Bt) || (H % Bh) || (W % Bw);
+    return g;
+}
+
 // Number of workgroups of kernel `Kern` (block threads, static LDS) resident
 // per XCD at once: occupancy per CU times CUs / 8.  Used as the period of the
 // phased block-list sweep.  Cached per kernel (one instantiation each) and
@@ -32,10 +55,11 @@ int resident_per_xcd(int block) {
     return v;
 }
 
-hipError_t launch_pool(int dtype, const void* x, void* out, int64_t nbh, int N, int D, int Bt, int Bh,
-                       int Bw, int Pt, int Ph, int Pw, hipStream_t s);
+hipError_t launch_pool(int dtype, const void* x, void* out, int64_t nbh, int N, int D, const cube_grid& cg,
+                       int Pt, int Ph, int Pw, hipStream_t s);
 hipError_t launch_route_passes(int dtype, int D, int G, const void* qr, const void* kr, float* lse2,
-                               float* scores, int batch, int Hq, int Hkv, int N, hipStream_t s);
+                               float* scores, int batch, int Hq, int Hkv, int N, const cube_grid& cg, int Rt,
+                               int Rh, int Rw, hipStream_t s);
 hipError_t launch_select(int phase, const float* scores, int64_t nrows, int N, int mode, int k,
                          float mass, int cap, int32_t* counts, const int32_t* row_ptr,
                          int32_t* col_idx, int64_t col_cap, hipStream_t s);
@@ -52,7 +76,7 @@ hipError_t launch_csc(const int32_t* row_ptr, const int32_t* col_idx, int batch,
 hipError_t launch_attn_fwd(int dtype, int D, const void* q, const void* k, const void* v,
                            const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
                            float* lse, void* o_lo, void* ws, int batch, int Hq, int Hkv, int N,
-                           hipStream_t s);
+                           const cube_grid& cg, hipStream_t s);
 // Forward workspace: the work order of the CSR rows (int32 per row).
 size_t fwd_workspace_bytes(int batch, int Hq, int N);
 // Backward workspace: (LSE*log2 e, Delta) per query token, then the work
@@ -68,7 +92,7 @@ hipError_t launch_attn_bwd(int dtype, int D, const void* q, const void* k, const
                            const float* lse, const void* o_lo, const void* dout, const int32_t* row_ptr,
                            const int32_t* col_idx, const int32_t* kv_ptr, const int32_t* kv_idx,
                            int64_t col_cap, void* dq, void* dk, void* dv, void* ws, int batch,
-                           int Hq, int Hkv, int N, hipStream_t s);
+                           int Hq, int Hkv, int N, const cube_grid& cg, hipStream_t s);
 hipError_t launch_attn_bwd_prep(int dtype, int D, const void* o, const float* lse, const void* o_lo,
                                 const void* dout, void* ws, int batch, int Hq, int N, hipStream_t s);
 // (LSE * log2 e, dO . O) for ntok rows of D elements.
@@ -83,15 +107,16 @@ hipError_t launch_coarse_bwd(int dtype, int D, const void* qc, const void* kc, c
 hipError_t launch_gate_merge(int dtype, int D, const float* gate, const void* oc, const void* of, void* out,
                              int64_t ntok, int B, hipStream_t s);
 hipError_t launch_gate_merge_bwd(int dtype, int D, const float* gate, const void* oc, const void* dout, void* doc,
-                                 float* dgate, int64_t ncubes, hipStream_t s);
-hipError_t launch_unpool_add(int dtype, int D, const void* dxc, void* dx, int64_t ntok, int Bt, int Bh, int Bw,
+                                 float* dgate, int64_t ncubes, int N, const cube_grid& cg, hipStream_t s);
+hipError_t launch_unpool_add(int dtype, int D, const void* dxc, void* dx, int64_t ntok, int N, const cube_grid& cg,
                              int Pt, int Ph, int Pw, hipStream_t s);
 hipError_t launch_attn_bwd_dkdv(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
                                 const void* dout, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
                                 void* dk, void* dv, void* ws, int batch, int Hq, int Hkv, int N,
-                                hipStream_t s);
+                                const cube_grid& cg, hipStream_t s);
 hipError_t launch_attn_bwd_dq(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
                               const void* dout, const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
-                              void* dq, void* ws, int batch, int Hq, int Hkv, int N, hipStream_t s);
+                              void* dq, void* ws, int batch, int Hq, int Hkv, int N, const cube_grid& cg,
+                              hipStream_t s);
 
 }  // namespace vsa2

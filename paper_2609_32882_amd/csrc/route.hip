@@ -7,6 +7,8 @@
 //   select_kernel        per-row top-k / mass selection by bisection on the
 //                        fp32 bit pattern, register resident, one wave a row
 //   scan / CSC kernels   CSR offsets, and the transposed (key-block) lists
+#include <type_traits>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -16,11 +18,13 @@ namespace vsa2 {
 // Pool
 // ===========================================================================
 // One thread per (output row, 8-element chunk of D).  Output row
-// (bh*N + n)*G + g averages the Pt*Ph*Pw tokens of sub-cube g of cube n.
+// (bh*N + n)*G + g averages the real tokens of sub-cube g of cube n: all
+// Pt*Ph*Pw of them unless the grid is padded, where the real tokens of a
+// sub-cube form a box and an all-padding sub-cube pools to 0.
 template <typename T>
 __global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ x, T* __restrict__ out,
-                                                   int64_t nthreads, int D, int G, int Gh, int Gw,
-                                                   int Pt, int Ph, int Pw, int Bh, int Bw, int B) {
+                                                   int64_t nthreads, int N, int D, int G, int Gh, int Gw,
+                                                   int Pt, int Ph, int Pw, int B, cube_grid grid) {
     const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     if (t >= nthreads) return;
     const int chunks = D / 8;
@@ -29,12 +33,21 @@ __global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ x, T* _
     const int g = static_cast<int>(orow % G);
     const int64_t cube = orow / G;                   // bh*N + n
     const int gt = g / (Gh * Gw), gh = (g / Gw) % Gh, gw = g % Gw;
+    const int Bh = grid.Bh, Bw = grid.Bw;
+    // real part of the sub-cube: [0, et) x [0, eh) x [0, ew) of its offsets
+    int et = Pt, eh = Ph, ew = Pw;
+    if (grid.padded) {
+        const int3 e = cube_extent(grid, static_cast<int>(cube % N));
+        et = max(0, min(Pt, e.x - gt * Pt));
+        eh = max(0, min(Ph, e.y - gh * Ph));
+        ew = max(0, min(Pw, e.z - gw * Pw));
+    }
     double acc[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[i] = 0.0;
-    for (int rt = 0; rt < Pt; ++rt)
-        for (int rh = 0; rh < Ph; ++rh)
-            for (int rw = 0; rw < Pw; ++rw) {
+    for (int rt = 0; rt < et; ++rt)
+        for (int rh = 0; rh < eh; ++rh)
+            for (int rw = 0; rw < ew; ++rw) {
                 const int beta = ((gt * Pt + rt) * Bh + gh * Ph + rh) * Bw + gw * Pw + rw;
                 const T* src = x + (cube * B + beta) * D + ch * 8;
                 if constexpr (sizeof(T) == 2) {
@@ -53,7 +66,8 @@ __global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ x, T* _
                     for (int i = 0; i < 8; ++i) acc[i] += static_cast<double>(f[i]);
                 }
             }
-    const double P = static_cast<double>(Pt * Ph * Pw);
+    const int cnt = et * eh * ew;
+    const double P = static_cast<double>(cnt > 0 ? cnt : 1);
     T* dst = out + orow * D + ch * 8;
     if constexpr (sizeof(T) == 2) {
         uint32_t u[4];
@@ -71,8 +85,9 @@ __global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ x, T* _
     }
 }
 
-hipError_t launch_pool(int dtype, const void* x, void* out, int64_t nbh, int N, int D,
-                       int Bt, int Bh, int Bw, int Pt, int Ph, int Pw, hipStream_t s) {
+hipError_t launch_pool(int dtype, const void* x, void* out, int64_t nbh, int N, int D, const cube_grid& grid,
+                       int Pt, int Ph, int Pw, hipStream_t s) {
+    const int Bt = grid.Bt, Bh = grid.Bh, Bw = grid.Bw;
     const int Gt = Bt / Pt, Gh = Bh / Ph, Gw = Bw / Pw, G = Gt * Gh * Gw;
     const int64_t nthreads = nbh * N * G * (D / 8);
     if (nthreads == 0) return hipSuccess;
@@ -80,12 +95,12 @@ hipError_t launch_pool(int dtype, const void* x, void* out, int64_t nbh, int N, 
     const int B = Bt * Bh * Bw;
     if (dtype == 1)
         hipLaunchKernelGGL(pool_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s,
-                           static_cast<const bf16_t*>(x), static_cast<bf16_t*>(out), nthreads, D, G,
-                           Gh, Gw, Pt, Ph, Pw, Bh, Bw, B);
+                           static_cast<const bf16_t*>(x), static_cast<bf16_t*>(out), nthreads, N, D, G,
+                           Gh, Gw, Pt, Ph, Pw, B, grid);
     else
         hipLaunchKernelGGL(pool_kernel<float>, dim3(blocks), dim3(256), 0, s,
-                           static_cast<const float*>(x), static_cast<float*>(out), nthreads, D, G,
-                           Gh, Gw, Pt, Ph, Pw, Bh, Bw, B);
+                           static_cast<const float*>(x), static_cast<float*>(out), nthreads, N, D, G,
+                           Gh, Gw, Pt, Ph, Pw, B, grid);
     return hipGetLastError();
 }
 
@@ -101,13 +116,31 @@ hipError_t launch_pool(int dtype, const void* x, void* out, int64_t nbh, int N, 
 // of 8 consecutive keys (G | 8 keys of a run make whole key blocks).
 //   PASS 1: lse2[i] = log2 sum_j 2^(s_ij * log2(e)/sqrt(D))  (log2 units)
 //   PASS 2: P_r[nq][nk] = (1/G^2) sum_{gq,gk} 2^(t - lse2)
+// On a padded grid, pooled tokens whose sub-cube holds no real token are
+// masked: such keys get no mass, such queries add nothing, and the G x G
+// pooling averages over the G' pooled queries of the cube that do hold one
+// (weight 1/(G G')), so every row still sums to 1/G.
 constexpr int RT_Q = 256;   // pooled queries per workgroup
 constexpr int RT_NT = 256;  // threads per workgroup
 
-template <typename T, int D, int G, int PASS>
+// Sub-cube gk (pool Rt x Rh x Rw) of a cube with real extent e holds a real
+// token iff its first token is real (the real tokens form a box).
+__device__ __forceinline__ bool subcube_real(const cube_grid& g, int3 e, int gk, int Rt, int Rh, int Rw) {
+    const int Gh = g.Bh / Rh, Gw = g.Bw / Rw;
+    const int gw = gk % Gw, r = gk / Gw;
+    const int gh = r % Gh, gt = r / Gh;
+    return gt * Rt < e.x && gh * Rh < e.y && gw * Rw < e.z;
+}
+
+// Sub-cubes of a cube with real extent e that hold a real token.
+__device__ __forceinline__ int subcubes_real(int3 e, int Rt, int Rh, int Rw) {
+    return ((e.x + Rt - 1) / Rt) * ((e.y + Rh - 1) / Rh) * ((e.z + Rw - 1) / Rw);
+}
+
+template <typename T, int D, int G, int PASS, bool PAD>
 __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
     const T* __restrict__ qr, const T* __restrict__ kr, float* __restrict__ lse2,
-    float* __restrict__ scores, int Hq, int Hkv, int N, float c_log2) {
+    float* __restrict__ scores, int Hq, int Hkv, int N, float c_log2, cube_grid grid, int Rt, int Rh, int Rw) {
     using F = typename frag_of<T>::type;
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;
@@ -137,11 +170,19 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
     }
     float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f};
     float lq[2] = {0.f, 0.f};
+    float qw[2] = {0.f, 0.f};          // pooling weight of the lane's pooled query
     if constexpr (PASS == 2) {
 #pragma unroll
         for (int qt = 0; qt < 2; ++qt) {
             const int64_t qi = q0 + qt * 32 + (lane & 31);
             lq[qt] = qi < NG ? lse2[static_cast<int64_t>(bh) * NG + qi] : 0.f;
+            qw[qt] = 1.0f / static_cast<float>(G * G);
+            if (PAD && qi < NG) {
+                const int3 e = cube_extent(grid, static_cast<int>(qi / G));
+                qw[qt] = subcube_real(grid, e, static_cast<int>(qi % G), Rt, Rh, Rw)
+                             ? 1.0f / static_cast<float>(G * subcubes_real(e, Rt, Rh, Rw))
+                             : 0.f;
+            }
         }
     }
 
@@ -151,6 +192,21 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
         __syncthreads();
         ktile.store(kt_lds, true, tid);
         __syncthreads();
+        // padded grid, bit jl: key j0 + jl exists and holds a real token
+        uint64_t kmask = 0;
+        if constexpr (PAD) {
+            const int64_t j = j0 + lane;
+            bool ok = j < NG;
+            if (ok)
+                ok = subcube_real(grid, cube_extent(grid, static_cast<int>(j / G)), static_cast<int>(j % G), Rt, Rh,
+                                  Rw);
+            kmask = __ballot(ok);
+        }
+        // key j0 + jl takes part
+        auto key_ok = [&](int jl) -> bool {
+            if constexpr (PAD) return (kmask >> jl) & 1;
+            else return j0 + jl < NG;
+        };
         f32x16_t acc[2][2];
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
@@ -175,8 +231,8 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
                 for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
                     for (int v = 0; v < 16; ++v) {
-                        const int64_t j = j0 + kt * 32 + (v >> 3) * 16 + half * 8 + (v & 7);
-                        const float t = j < NG ? acc[kt][qt][v] * c_log2 : -INFINITY;
+                        const int jl = kt * 32 + (v >> 3) * 16 + half * 8 + (v & 7);
+                        const float t = key_ok(jl) ? acc[kt][qt][v] * c_log2 : -INFINITY;
                         acc[kt][qt][v] = t;
                         mt = fmaxf(mt, t);
                     }
@@ -191,7 +247,6 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
                 m[qt] = mn;
             }
         } else {
-            constexpr float inv_g2 = 1.0f / static_cast<float>(G * G);
 #pragma unroll
             for (int qt = 0; qt < 2; ++qt) {
                 const int64_t qi = q0 + qt * 32 + (lane & 31);
@@ -207,10 +262,11 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
 #pragma unroll
                             for (int u = 0; u < G; ++u) {
                                 const int v = run * 8 + i * G + u;
-                                const int64_t j = j0 + kt * 32 + run * 16 + half * 8 + i * G + u;
-                                s += j < NG ? fast_exp2(acc[kt][qt][v] * c_log2 - lq[qt]) : 0.f;
+                                const int jl = kt * 32 + run * 16 + half * 8 + i * G + u;
+                                s += key_ok(jl) ? fast_exp2(acc[kt][qt][v] * c_log2 - lq[qt]) : 0.f;
                             }
-                            // sum over the G pooled queries of the block (G adjacent lanes)
+                            // weighted sum over the G pooled queries of the block (G adjacent lanes)
+                            s *= qw[qt];
 #pragma unroll
                             for (int off = 1; off < G; off <<= 1) s += __shfl_xor(s, off, 64);
                             bs[i] = s;
@@ -221,7 +277,7 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
                             for (int i = 0; i < 8 / G; ++i) {
                                 const int64_t j = j0 + kt * 32 + run * 16 + half * 8 + i * G;
                                 if (j < NG)
-                                    scores[(static_cast<int64_t>(bh) * N + nq) * N + j / G] = bs[i] * inv_g2;
+                                    scores[(static_cast<int64_t>(bh) * N + nq) * N + j / G] = bs[i];
                             }
                         }
                     }
@@ -241,39 +297,46 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
 
 template <typename T, int D, int G>
 static hipError_t launch_route_passes_t(const void* qr, const void* kr, float* lse2, float* scores,
-                                        int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                                        int batch, int Hq, int Hkv, int N, const cube_grid& cg, int Rt, int Rh,
+                                        int Rw, hipStream_t s) {
     const int64_t NG = static_cast<int64_t>(N) * G;
     dim3 grid(static_cast<unsigned>((NG + RT_Q - 1) / RT_Q), static_cast<unsigned>(batch * Hq));
     const float c = 1.4426950408889634f / sqrtf(static_cast<float>(D));
-    hipLaunchKernelGGL((route_pass_kernel<T, D, G, 1>), grid, dim3(RT_NT), 0, s,
-                       static_cast<const T*>(qr), static_cast<const T*>(kr), lse2, scores, Hq, Hkv, N, c);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((route_pass_kernel<T, D, G, 2>), grid, dim3(RT_NT), 0, s,
-                       static_cast<const T*>(qr), static_cast<const T*>(kr), lse2, scores, Hq, Hkv, N, c);
-    return hipGetLastError();
+    auto go = [&](auto pad) {
+        constexpr bool P = decltype(pad)::value;
+        hipLaunchKernelGGL((route_pass_kernel<T, D, G, 1, P>), grid, dim3(RT_NT), 0, s, static_cast<const T*>(qr),
+                           static_cast<const T*>(kr), lse2, scores, Hq, Hkv, N, c, cg, Rt, Rh, Rw);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((route_pass_kernel<T, D, G, 2, P>), grid, dim3(RT_NT), 0, s, static_cast<const T*>(qr),
+                           static_cast<const T*>(kr), lse2, scores, Hq, Hkv, N, c, cg, Rt, Rh, Rw);
+        return hipGetLastError();
+    };
+    return cg.padded ? go(std::true_type{}) : go(std::false_type{});
 }
 
 template <typename T, int D>
 static hipError_t launch_route_passes_d(int G, const void* qr, const void* kr, float* lse2,
-                                        float* scores, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                                        float* scores, int batch, int Hq, int Hkv, int N, const cube_grid& cg,
+                                        int Rt, int Rh, int Rw, hipStream_t s) {
     switch (G) {
-        case 1: return launch_route_passes_t<T, D, 1>(qr, kr, lse2, scores, batch, Hq, Hkv, N, s);
-        case 2: return launch_route_passes_t<T, D, 2>(qr, kr, lse2, scores, batch, Hq, Hkv, N, s);
-        case 4: return launch_route_passes_t<T, D, 4>(qr, kr, lse2, scores, batch, Hq, Hkv, N, s);
-        case 8: return launch_route_passes_t<T, D, 8>(qr, kr, lse2, scores, batch, Hq, Hkv, N, s);
+        case 1: return launch_route_passes_t<T, D, 1>(qr, kr, lse2, scores, batch, Hq, Hkv, N, cg, Rt, Rh, Rw, s);
+        case 2: return launch_route_passes_t<T, D, 2>(qr, kr, lse2, scores, batch, Hq, Hkv, N, cg, Rt, Rh, Rw, s);
+        case 4: return launch_route_passes_t<T, D, 4>(qr, kr, lse2, scores, batch, Hq, Hkv, N, cg, Rt, Rh, Rw, s);
+        case 8: return launch_route_passes_t<T, D, 8>(qr, kr, lse2, scores, batch, Hq, Hkv, N, cg, Rt, Rh, Rw, s);
         default: return hipErrorInvalidValue;
     }
 }
 
 hipError_t launch_route_passes(int dtype, int D, int G, const void* qr, const void* kr, float* lse2,
-                               float* scores, int batch, int Hq, int Hkv, int N, hipStream_t s) {
+                               float* scores, int batch, int Hq, int Hkv, int N, const cube_grid& cg, int Rt,
+                               int Rh, int Rw, hipStream_t s) {
     if (dtype == 1) {
-        if (D == 64) return launch_route_passes_d<bf16_t, 64>(G, qr, kr, lse2, scores, batch, Hq, Hkv, N, s);
-        if (D == 128) return launch_route_passes_d<bf16_t, 128>(G, qr, kr, lse2, scores, batch, Hq, Hkv, N, s);
+        if (D == 64) return launch_route_passes_d<bf16_t, 64>(G, qr, kr, lse2, scores, batch, Hq, Hkv, N, cg, Rt, Rh, Rw, s);
+        if (D == 128) return launch_route_passes_d<bf16_t, 128>(G, qr, kr, lse2, scores, batch, Hq, Hkv, N, cg, Rt, Rh, Rw, s);
     } else {
-        if (D == 64) return launch_route_passes_d<float, 64>(G, qr, kr, lse2, scores, batch, Hq, Hkv, N, s);
-        if (D == 128) return launch_route_passes_d<float, 128>(G, qr, kr, lse2, scores, batch, Hq, Hkv, N, s);
+        if (D == 64) return launch_route_passes_d<float, 64>(G, qr, kr, lse2, scores, batch, Hq, Hkv, N, cg, Rt, Rh, Rw, s);
+        if (D == 128) return launch_route_passes_d<float, 128>(G, qr, kr, lse2, scores, batch, Hq, Hkv, N, cg, Rt, Rh, Rw, s);
     }
     return hipErrorInvalidValue;
 }

@@ -33,6 +33,12 @@ def value_errors(got, ref, ulp_rel=0.0):
     relative L2 error)."""
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
+    # infinities (LSE = -inf of a query without keys: empty rows, padding
+    # queries) must match exactly; the rest is compared numerically
+    inf = np.isinf(ref) | ~np.isfinite(got)
+    if inf.any():
+        assert np.array_equal(got[inf], ref[inf]), "infinite / NaN entries differ"
+        got, ref = got[~inf], ref[~inf]
     diff = np.abs(got - ref)
     max_abs = float(diff.max()) if diff.size else 0.0
     scaled = float((diff - ulp_rel * np.abs(ref)).max()) if diff.size else 0.0

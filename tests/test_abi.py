@@ -61,7 +61,7 @@ MISALIGNED = 0x10008
 @pytest.mark.parametrize("mutate,expect", [
     (dict(dtype=7), "VSA2_ERR_DTYPE"),
     (dict(heads_q=3), "VSA2_ERR_SHAPE"),          # Hq % Hkv
-    (dict(T=6), "VSA2_ERR_SHAPE"),                # T % Bt
+    (dict(T=0), "VSA2_ERR_SHAPE"),                # empty grid
     (dict(Rt=3), "VSA2_ERR_SHAPE"),               # Bt % Rt
     (dict(batch=0), "VSA2_ERR_SHAPE"),
     (dict(head_dim=96), "VSA2_ERR_UNSUPPORTED"),
@@ -73,6 +73,16 @@ def test_attn_fwd_rejects_bad_problem(mutate, expect):
         setattr(p, k, v)
     st = vsa2.vsa2_attn_fwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE, FAKE, None, FAKE, 1 << 40, None)
     assert vsa2.STATUS_NAMES[st] == expect
+
+
+def test_grid_not_divisible_by_the_cube_is_padded_up():
+    """T, H, W need not be multiples of the cube: the grid is padded up to
+    whole cubes (N = ceil(T/Bt) ceil(H/Bh) ceil(W/Bw))."""
+    sel = vsa2.vsa2_select(0, 5, 0.0, 0)
+    for T, H, W, N in ((8, 16, 16, 32), (6, 16, 16, 32), (5, 13, 9, 2 * 4 * 3), (1, 1, 1, 1)):
+        p = vsa2.make_problem(1, 4, 2, 128, T, H, W)
+        st, n = vsa2.vsa2_route_capacity(p, sel)
+        assert vsa2.STATUS_NAMES[st] == "VSA2_OK" and n == 4 * N * min(5, N), (T, H, W)
 
 
 def test_null_and_alignment_checks():

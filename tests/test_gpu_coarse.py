@@ -24,6 +24,11 @@ CASES = {
     # two batches, N = 130: three tiles, the last with 2 rows
     "bf16-d128-b2-n130": Workload("c5", Problem(2, 2, 2, 128, 8, 260, 4), Selection(0, 20), 3005,
                                   skewed=True),
+    # grids padded up to whole cubes: cut along every axis (N = 48), and one
+    # frame (T = 1) with GQA and a 2x2x4 router pool
+    "bf16-d128-padded": Workload("c6", Problem(1, 2, 2, 128, 7, 13, 22), Selection(0, 12), 3006),
+    "f32-d64-padded-1frame-gqa": Workload("c7", Problem(1, 4, 2, 64, 1, 18, 20, Rt=2, Rh=2, Rw=4, dtype=F32),
+                                          Selection(0, 6), 3007),
 }
 
 

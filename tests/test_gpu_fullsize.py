@@ -19,7 +19,7 @@ from workload import BF16, WORKLOADS, make_inputs
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
-FULL = ["480p", "720p", "720p-mass", "gqa-long", "720p-seq", "720p-vsa"]
+FULL = ["480p", "720p", "720p-mass", "gqa-long", "720p-seq", "720p-vsa", "720p-latent"]
 
 
 def _dev(x):
@@ -84,9 +84,13 @@ def test_block_lists_structure(run):
     print("nnz %d, counts min/mean/max %d/%.1f/%d" % (nnz, counts.min(), counts.mean(), counts.max()))
 
 
-def _sample_rows(p, n, seed):
+def _sample_rows(p, n, seed, heads=None):
     rng = np.random.default_rng(seed)
-    return np.sort(rng.choice(p.batch * p.heads_q * p.N, n, replace=False)).astype(np.int64)
+    nrows = p.batch * (p.heads_q if heads is None else heads) * p.N
+    rows = rng.choice(nrows, n, replace=False)
+    if p.padded:    # the last cube of a head is cut along every padded axis
+        rows = np.union1d(rows, [p.N - 1, nrows - 1])
+    return np.sort(rows).astype(np.int64)
 
 
 def test_router_rows_against_oracle(run):
@@ -129,8 +133,7 @@ def test_backward_rows_against_oracle(run):
     rows = _sample_rows(p, 8, 3)
     dq_ref = oracle.attn_bwd_dq(x["q"], x["k"], x["v"], x["do"], p, run["rp"], run["ci"], rows)
     assert_values(to_np(dq).reshape(-1, p.B, p.head_dim)[rows], dq_ref, "dQ (sampled rows)")
-    rng = np.random.default_rng(4)
-    kvrows = np.sort(rng.choice(p.batch * p.heads_kv * p.N, 4, replace=False)).astype(np.int64)
+    kvrows = _sample_rows(p, 4, 4, heads=p.heads_kv)
     dk_ref, dv_ref = oracle.attn_bwd_dkdv(x["q"], x["k"], x["v"], x["do"], p, run["rp"], run["ci"],
                                           kvrows)
     assert_values(to_np(dk).reshape(-1, p.B, p.head_dim)[kvrows], dk_ref, "dK (sampled blocks)")

@@ -33,7 +33,18 @@ CASES = {
     # R = 2x2x4 (G = 4), GQA
     "bf16-router-G4": Workload("bf16-router-G4", Problem(1, 4, 2, 64, 8, 16, 16, Rt=2, Rh=2, Rw=4),
                                Selection(0, 6), 2007),
+    # grids that are not multiples of the 4x4x4 cube, padded up to whole cubes
+    # with the padding masked: cut along all three axes (N = 2*4*6 = 48) ...
+    "bf16-padded": Workload("bf16-padded", Problem(1, 2, 2, 128, 7, 13, 22), Selection(0, 12), 2008),
+    # ... GQA at D = 64 with mass selection on skewed inputs (N = 2*3*4) ...
+    "f32-padded-gqa-mass": Workload("f32-padded-gqa-mass", Problem(1, 4, 2, 64, 5, 10, 15, dtype=F32),
+                                    Selection(1, 0, 0.9, 12), 2009, skewed=True),
+    # ... and one frame (T = 1 < Bt: 16 real tokens per cube, half of the
+    # pooled sub-cubes empty), router pool 2x2x4 (G = 4), N = 5*5
+    "bf16-padded-1frame-G4": Workload("bf16-padded-1frame-G4",
+                                      Problem(1, 2, 2, 128, 1, 18, 20, Rt=2, Rh=2, Rw=4), Selection(0, 6), 2010),
 }
+PADDED = [name for name, w in CASES.items() if w.problem.padded]
 
 
 @pytest.fixture(scope="module", params=list(CASES))
@@ -252,6 +263,53 @@ def test_bwd_deterministic_sentinels_and_unselected_blocks(case):
     dk_np = to_np(s[1]).reshape(-1, p.B, p.head_dim)
     dv_np = to_np(s[2]).reshape(-1, p.B, p.head_dim)
     assert (dk_np[indeg == 0] == 0).all() and (dv_np[indeg == 0] == 0).all()
+
+
+def _fill_padding(t, p, seed):
+    """Copy of t [batch, heads, L, D] with its padding tokens set to large
+    random values."""
+    real = torch.from_numpy(p.token_real()).cuda()
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    noise = (torch.randn(t.shape, generator=g, device="cuda") * 40).to(t.dtype)
+    return torch.where(real[None, None, :, None], t, noise)
+
+
+@pytest.mark.parametrize("name", PADDED)
+def test_padding_contents_do_not_matter(name):
+    """Padding tokens are masked everywhere: with large random values in the
+    padding of Q, K, V and dO, pooling, routing, the forward and the backward
+    give the same bits on real tokens as with zero padding, and padding
+    queries / keys get O = 0, LSE = -inf, dQ = dK = dV = 0."""
+    w = CASES[name]
+    p = w.problem
+    print("\n[padding case %s] %s" % (name, p), flush=True)
+    x = make_inputs(w, with_grad=True)
+    bf = p.dtype == BF16
+    clean = {k: to_dev(v, bf) for k, v in x.items()}
+    dirty = {k: _fill_padding(v, p, i + 1) for i, (k, v) in enumerate(clean.items())}
+    real = torch.from_numpy(p.token_real()).cuda()
+    outs = []
+    for d in (clean, dirty):
+        R = (p.Rt, p.Rh, p.Rw)
+        q_r, k_r = vsa2.pool(p, d["q"], R), vsa2.pool(p, d["k"], R)
+        r = vsa2.route(p, w.select, q_r, k_r, with_scores=True)
+        o, lse, o_lo = vsa2.attn_fwd(p, d["q"], d["k"], d["v"], r["row_ptr"], r["col_idx"], compensated=True)
+        g = vsa2.attn_bwd(p, d["q"], d["k"], d["v"], o, lse, d["do"], r["row_ptr"], r["col_idx"],
+                          r["kv_ptr"], r["kv_idx"], o_lo=o_lo)
+        outs.append(dict(q_r=q_r, k_r=k_r, scores=r["scores"], rp=r["row_ptr"], ci=r["col_idx"], o=o, lse=lse,
+                         o_lo=o_lo, dq=g[0], dk=g[1], dv=g[2]))
+    torch.cuda.synchronize()
+    a, b = outs
+    bits = {torch.bfloat16: torch.int16, torch.float32: torch.int32, torch.int32: torch.int32}
+    nnz = int(a["rp"][-1])
+    a["ci"], b["ci"] = a["ci"][:nnz], b["ci"][:nnz]
+    for k in ("q_r", "k_r", "scores", "rp", "ci", "o", "lse", "o_lo", "dq", "dk", "dv"):
+        assert torch.equal(a[k].view(bits[a[k].dtype]), b[k].view(bits[b[k].dtype])), k
+    pad = ~real
+    assert (a["o"][:, :, pad] == 0).all() and torch.isneginf(a["lse"][:, :, pad]).all()
+    assert (a["dq"][:, :, pad] == 0).all()
+    assert (a["dk"][:, :, pad] == 0).all() and (a["dv"][:, :, pad] == 0).all()
+    assert torch.isfinite(a["lse"][:, :, real]).all()
 
 
 def test_bwd_unselected_blocks_are_zero_explicit():

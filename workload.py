@@ -148,6 +148,11 @@ WORKLOADS = {
     # the coarse cube-level router of VSA (router pool R = B, G = 1) on the 720p inputs
     "720p-vsa": Workload(
         "720p-vsa", Problem(1, 40, 40, 128, 20, 48, 80, Rt=4, Rh=4, Rw=4), Selection(0, 120), 1002),
+    # the latent grid of an 81-frame 1280x720 clip itself (21 x 45 x 80: 4x
+    # temporal, 16x spatial compression), not a multiple of the cube: padded
+    # to 24 x 48 x 80, N = 1440 cubes, top-120
+    "720p-latent": Workload(
+        "720p-latent", Problem(1, 40, 40, 128, 21, 45, 80), Selection(0, 120), 1005),
 }
 
 
@@ -248,6 +253,8 @@ def _with_means_of(ref: np.ndarray, p: Problem, seed: int, tensor_id: int, threa
             eps = rng2.standard_normal((p.N, p.B, p.head_dim), dtype=np.float32) * np.float32(0.5)
             x = (eps + mu[:, None, :]).reshape(p.L, p.head_dim)
             out[b, h] = round_bf16_f32(x) if p.dtype == BF16 else x
+            if p.padded:
+                out[b, h][~p.token_real()] = 0.0        # padding tokens hold zeros
     return out
 
 
