@@ -78,8 +78,14 @@ def _f32(a):
 
 
 def _geom(p):
-    """{T, H, W, Bt, Bh, Bw}: the real grid and the cube (padded grids)."""
-    return np.array([p.T, p.H, p.W, p.Bt, p.Bh, p.Bw], np.int32)
+    """{T, H, W, Bt, Bh, Bw, Lt}: the real grid, the cube (padded grids) and
+    the number of text tokens joined to the video (0: none)."""
+    return np.array([p.T, p.H, p.W, p.Bt, p.Bh, p.Bw, getattr(p, "text_len", 0)], np.int32)
+
+
+def _video(x, p):
+    """The video part [..., :L, :] of a joint [..., L_joint, D] tensor."""
+    return np.ascontiguousarray(x[..., :p.L, :]) if x.shape[-2] != p.L else x
 
 
 def threads() -> int:
@@ -100,8 +106,9 @@ def round_bf16(x) -> np.ndarray:
 
 def pool(x, p, Pt: int, Ph: int, Pw: int) -> np.ndarray:
     """MeanPool over (Pt, Ph, Pw) sub-cubes of every cube (Eq. router_start
-    with P = R; Eq. compress with P = B).  x: [b, h, L, D] -> [b, h, N*G, D]."""
-    x = _f32(x)
+    with P = R; Eq. compress with P = B).  x: [b, h, L, D] -> [b, h, N*G, D]
+    (of a joint video + text tensor, the video part is pooled)."""
+    x = _f32(_video(x, p))
     nb, nh, L, D = x.shape
     G = (p.Bt // Pt) * (p.Bh // Ph) * (p.Bw // Pw)
     out = np.empty((nb, nh, p.N * G, D), np.float32)
@@ -145,11 +152,13 @@ def csr_from_selection(counts, idx):
     return row_ptr.astype(np.int32), col_idx.astype(np.int32)
 
 
-def csr_to_csc(row_ptr, col_idx, p):
+def csr_to_csc(row_ptr, col_idx, p, N=None):
     """Transpose the query-block -> key-block lists into key-block ->
     (query head within the KV group, query block) lists, entries ordered by
-    (hq_local, n_q) ascending, value hq_local*N + n_q."""
-    N, grp = p.N, p.heads_q // p.heads_kv
+    (hq_local, n_q) ascending, value hq_local*N + n_q.  N: blocks per
+    sequence (default the video cubes; p.N_joint for joint lists)."""
+    N = p.N if N is None else N
+    grp = p.heads_q // p.heads_kv
     nrows = p.batch * p.heads_q * N
     mask = np.zeros((nrows, N), bool)
     counts = np.diff(row_ptr)
@@ -165,6 +174,31 @@ def csr_to_csc(row_ptr, col_idx, p):
     return kv_ptr.astype(np.int32), cols.astype(np.int32)
 
 
+def joint_lists(row_ptr, col_idx, p):
+    """Block lists of the joint video + text attention (MMDiT; Eq.
+    block_sparse extended with full video-to-text and text-to-video blocks,
+    Sec. 2.2): a video query block keeps its routed video blocks and gains
+    all M text blocks; a text query block takes every block.  Blocks are
+    numbered 0..N-1 (video cubes), N..N+M-1 (text).  Returns the joint CSR
+    (rows b*Hq*(N+M)) and CSC."""
+    N, M = p.N, p.M
+    Nj = N + M
+    text = np.arange(N, Nj, dtype=np.int32)
+    full = np.arange(Nj, dtype=np.int32)
+    lists = []
+    for bh in range(p.batch * p.heads_q):
+        for n in range(N):
+            r = bh * N + n
+            lists.append(np.concatenate([col_idx[row_ptr[r]:row_ptr[r + 1]], text]))
+        lists.extend([full] * M)
+    counts = np.array([len(x) for x in lists], np.int64)
+    rp = np.zeros(counts.size + 1, np.int64)
+    np.cumsum(counts, out=rp[1:])
+    ci = np.concatenate(lists).astype(np.int32)
+    kp, ki = csr_to_csc(rp.astype(np.int32), ci, p, Nj)
+    return rp.astype(np.int32), ci, kp, ki
+
+
 def route(q, k, p, sel):
     """The whole router: pool (P = R), block scores, selection, CSR and CSC.
     Returns a dict with q_r, k_r, scores, row_ptr, col_idx, kv_ptr, kv_idx."""
@@ -178,43 +212,50 @@ def route(q, k, p, sel):
                 kv_ptr=kv_ptr, kv_idx=kv_idx)
 
 
+def _nj(p):
+    """Blocks of one (batch, head) sequence: video cubes plus text blocks."""
+    return getattr(p, "N_joint", p.N)
+
+
 def attn_fwd(q, k, v, p, row_ptr, col_idx, rows=None):
     """Block-sparse attention forward for query-block rows (default all).
+    With text tokens (p.text_len > 0) q, k, v are joint [b, h, L_joint, D]
+    sequences and the lists are joint lists (joint_lists).
     Returns O [nrows, B, D] float64 and LSE [nrows, B] float64."""
     q, k, v = _f32(q), _f32(k), _f32(v)
-    nrow_all = p.batch * p.heads_q * p.N
+    nrow_all = p.batch * p.heads_q * _nj(p)
     rows = np.arange(nrow_all, dtype=np.int64) if rows is None else np.ascontiguousarray(rows, np.int64)
     o = np.empty((rows.size, p.B, p.head_dim), np.float64)
     lse = np.empty((rows.size, p.B), np.float64)
     rp, ci = np.ascontiguousarray(row_ptr, np.int32), np.ascontiguousarray(col_idx, np.int32)
     g = _geom(p)
-    lib().vo_attn_fwd(_p(q), _p(k), _p(v), p.batch, p.heads_q, p.heads_kv, p.L, p.head_dim,
+    lib().vo_attn_fwd(_p(q), _p(k), _p(v), p.batch, p.heads_q, p.heads_kv, _nj(p) * p.B, p.head_dim,
                       p.B, _p(rp), _p(ci), _p(rows), rows.size, _p(o), _p(lse), _p(g))
     return o, lse
 
 
 def attn_bwd_dq(q, k, v, do, p, row_ptr, col_idx, rows=None):
     q, k, v, do = _f32(q), _f32(k), _f32(v), _f32(do)
-    nrow_all = p.batch * p.heads_q * p.N
+    nrow_all = p.batch * p.heads_q * _nj(p)
     rows = np.arange(nrow_all, dtype=np.int64) if rows is None else np.ascontiguousarray(rows, np.int64)
     dq = np.empty((rows.size, p.B, p.head_dim), np.float64)
     rp, ci = np.ascontiguousarray(row_ptr, np.int32), np.ascontiguousarray(col_idx, np.int32)
     g = _geom(p)
-    lib().vo_attn_bwd_dq(_p(q), _p(k), _p(v), _p(do), p.batch, p.heads_q, p.heads_kv, p.L,
+    lib().vo_attn_bwd_dq(_p(q), _p(k), _p(v), _p(do), p.batch, p.heads_q, p.heads_kv, _nj(p) * p.B,
                          p.head_dim, p.B, _p(rp), _p(ci), _p(rows), rows.size, _p(dq), _p(g))
     return dq
 
 
 def attn_bwd_dkdv(q, k, v, do, p, row_ptr, col_idx, kv_rows=None):
     q, k, v, do = _f32(q), _f32(k), _f32(v), _f32(do)
-    nkv_all = p.batch * p.heads_kv * p.N
+    nkv_all = p.batch * p.heads_kv * _nj(p)
     kv_rows = np.arange(nkv_all, dtype=np.int64) if kv_rows is None else \
         np.ascontiguousarray(kv_rows, np.int64)
     dk = np.empty((kv_rows.size, p.B, p.head_dim), np.float64)
     dv = np.empty((kv_rows.size, p.B, p.head_dim), np.float64)
     rp, ci = np.ascontiguousarray(row_ptr, np.int32), np.ascontiguousarray(col_idx, np.int32)
     g = _geom(p)
-    lib().vo_attn_bwd_dkdv(_p(q), _p(k), _p(v), _p(do), p.batch, p.heads_q, p.heads_kv, p.L,
+    lib().vo_attn_bwd_dkdv(_p(q), _p(k), _p(v), _p(do), p.batch, p.heads_q, p.heads_kv, _nj(p) * p.B,
                            p.head_dim, p.B, _p(rp), _p(ci), _p(kv_rows), kv_rows.size,
                            _p(dk), _p(dv), _p(g))
     return dk, dv
@@ -261,21 +302,30 @@ def coarse_bwd(qc, kc, vc, doc, p):
 
 def gate_merge(g, oc, of, p):
     """O = tanh(g) * Repeat_B(O_c_hat) + O_f (Eq. gate_linear, gated merge).
-    g [b, Hq, L] gate pre-activations; oc [b, Hq, N, D]; of [b, Hq, L, D]."""
+    g [b, Hq, L] gate pre-activations; oc [b, Hq, N, D]; of [b, Hq, L, D].
+    Joint video + text sequences (L_joint tokens): the coarse branch covers
+    the video tokens only, text tokens keep O_f."""
     g, oc, of = _f32(g), _f32(oc), _f32(of)
-    out = np.empty((p.batch, p.heads_q, p.L, p.head_dim), np.float64)
-    lib().vo_gate_merge(_p(g), _p(oc), _p(of), p.batch * p.heads_q, p.N, p.B, p.head_dim, _p(out))
+    out = of.astype(np.float64)
+    gv, ofv = _f32(_video(g[..., None], p)[..., 0]), _video(of, p)
+    ov = np.empty((p.batch, p.heads_q, p.L, p.head_dim), np.float64)
+    lib().vo_gate_merge(_p(gv), _p(oc), _p(ofv), p.batch * p.heads_q, p.N, p.B, p.head_dim, _p(ov))
+    out[..., :p.L, :] = ov
     return out
 
 
 def gate_merge_bwd(g, oc, dout, p):
     """(d O_c_hat, d g) of gate_merge for dout; d O_f is dout itself."""
     g, oc, dout = _f32(g), _f32(oc), _f32(dout)
+    Lg = g.shape[-1]
+    g, dout = _f32(_video(g[..., None], p)[..., 0]), _video(dout, p)
     doc = np.empty((p.batch, p.heads_q, p.N, p.head_dim), np.float64)
-    dg = np.empty((p.batch, p.heads_q, p.L), np.float64)
+    dg = np.zeros((p.batch, p.heads_q, Lg), np.float64)      # text tokens: no gate
+    dgv = np.empty((p.batch, p.heads_q, p.L), np.float64)
     geom = _geom(p)
     lib().vo_gate_merge_bwd(_p(g), _p(oc), _p(dout), p.batch * p.heads_q, p.N, p.B, p.head_dim,
-                            _p(doc), _p(dg), _p(geom))
+                            _p(doc), _p(dgv), _p(geom))
+    dg[..., :p.L] = dgv
     return doc, dg
 
 
@@ -285,5 +335,8 @@ def unpool_add(dxc, dx, p, Pt: int, Ph: int, Pw: int):
     dxc = np.ascontiguousarray(dxc, np.float64)
     assert dx.dtype == np.float64 and dx.flags.c_contiguous
     nbh = dx.shape[0] * dx.shape[1]
-    lib().vo_unpool_add(_p(dxc), nbh, p.T, p.H, p.W, p.Bt, p.Bh, p.Bw, Pt, Ph, Pw, p.head_dim, _p(dx))
+    xv = _video(dx, p)                    # joint sequences: the video part
+    lib().vo_unpool_add(_p(dxc), nbh, p.T, p.H, p.W, p.Bt, p.Bh, p.Bw, Pt, Ph, Pw, p.head_dim, _p(xv))
+    if xv is not dx:
+        dx[..., :p.L, :] = xv
     return dx

@@ -67,10 +67,14 @@ void vo_round_bf16(const double* in, float* out, int64_t n)
 /* ---------------------------------------------------------------------- */
 /* Padded grids (Sec. 2.2 "Kernel Implementation": each of T, H, W is      */
 /* padded up to a multiple of the cube size and padding is masked out).    */
-/* geom = {T, H, W, Bt, Bh, Bw}: the real grid and the cube.  The cube-     */
-/* major layout holds N = ceil(T/Bt) ceil(H/Bh) ceil(W/Bw) cubes of B       */
-/* tokens; token beta of cube n is real iff its grid position lies inside  */
-/* the real grid.  geom == NULL: every token is real.                      */
+/* geom = {T, H, W, Bt, Bh, Bw, Lt}: the real grid, the cube and the text  */
+/* length.  The cube-major layout holds N = ceil(T/Bt) ceil(H/Bh)          */
+/* ceil(W/Bw) video cubes of B tokens; token beta of cube n is real iff    */
+/* its grid position lies inside the real grid.  With text tokens (MMDiT   */
+/* joint attention, the extension of Eq. block_sparse in Sec. 2.2) the     */
+/* sequence of a (batch, head) continues with ceil(Lt/B) text blocks of B  */
+/* tokens, of which the first Lt are real.  geom == NULL: every token is   */
+/* real.                                                                   */
 /* ---------------------------------------------------------------------- */
 
 static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -80,6 +84,9 @@ static int vo_token_real(const int* geom, int64_t n, int beta)
     if (!geom) return 1;
     const int T = geom[0], H = geom[1], W = geom[2], Bt = geom[3], Bh = geom[4], Bw = geom[5];
     const int64_t Nh = ceil_div(H, Bh), Nw = ceil_div(W, Bw);
+    const int64_t Nv = ceil_div(T, Bt) * Nh * Nw;
+    if (n >= Nv)                        /* text block n - Nv */
+        return (n - Nv) * (int64_t)(Bt * Bh * Bw) + beta < geom[6];
     const int64_t nt = n / (Nh * Nw), nh = (n / Nw) % Nh, nw = n % Nw;
     const int bt = beta / (Bh * Bw), bh = (beta / Bw) % Bh, bw = beta % Bw;
     return nt * Bt + bt < T && nh * Bh + bh < H && nw * Bw + bw < W;
@@ -113,7 +120,7 @@ void vo_pool(const float* x, int64_t nbh, int T, int H, int W,
              int Bt, int Bh, int Bw, int Pt, int Ph, int Pw, int D,
              int dtype_bf16, float* out)
 {
-    const int geom[6] = {T, H, W, Bt, Bh, Bw};
+    const int geom[7] = {T, H, W, Bt, Bh, Bw, 0};
     const int64_t N = ceil_div(T, Bt) * ceil_div(H, Bh) * ceil_div(W, Bw);
     const int B = Bt * Bh * Bw;
     const int Gt = Bt / Pt, Gh = Bh / Ph, Gw = Bw / Pw;
@@ -712,7 +719,7 @@ void vo_gate_merge_bwd(const float* g, const float* oc, const float* dout, int64
 void vo_unpool_add(const double* dxc, int64_t nbh, int T, int H, int W, int Bt, int Bh, int Bw,
                    int Pt, int Ph, int Pw, int D, double* dx)
 {
-    const int geom[6] = {T, H, W, Bt, Bh, Bw};
+    const int geom[7] = {T, H, W, Bt, Bh, Bw, 0};
     const int64_t N = ceil_div(T, Bt) * ceil_div(H, Bh) * ceil_div(W, Bw);
     const int B = Bt * Bh * Bw;
     const int Gt = Bt / Pt, Gh = Bh / Ph, Gw = Bw / Pw;

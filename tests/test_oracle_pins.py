@@ -514,24 +514,29 @@ def test_unpool_is_the_adjoint_of_pool(P):
     np.testing.assert_array_equal(back.astype(np.float64), ones / (Pt * Ph * Pw))
 
 
-@pytest.mark.parametrize("grid_thw", [(2, 4, 4), (3, 3, 4)])
-def test_full_op_gradient_finite_differences(grid_thw):
+@pytest.mark.parametrize("grid_thw,text_len", [((2, 4, 4), 0), ((3, 3, 4), 0), ((3, 3, 4), 11)])
+def test_full_op_gradient_finite_differences(grid_thw, text_len):
     """The whole VSA2 attention op O = tanh(g) Repeat_B(Attn(Pool_B Q, Pool_B K,
     Pool_B V)) + BlockSparseAttn(Q, K, V; M): gradients composed from the
     oracle's steps (merge, coarse and fine backward, unpool) against central
     differences of sum(W * O) over the real tokens.  The 3 x 3 x 4 grid is
-    padded to 4 x 4 x 4: the gradient of every padding token is 0."""
+    padded to 4 x 4 x 4: the gradient of every padding token is 0.  With 11
+    text tokens (two blocks of 8, the second padded) the fine branch is the
+    joint attention and text tokens keep O_f."""
     T, H, W_ = grid_thw
-    p = Problem(1, 2, 1, 8, T, H, W_, 2, 2, 2, 1, 1, 2, F32)    # cubes of B = 8
+    p = Problem(1, 2, 1, 8, T, H, W_, 2, 2, 2, 1, 1, 2, F32, text_len)    # cubes of B = 8
     rng = np.random.default_rng(43)
     grid = lambda shape: (rng.integers(-1024, 1024, shape) / 1024.0).astype(np.float32)
-    q = grid((1, 2, p.L, p.head_dim))
-    k = grid((1, 1, p.L, p.head_dim))
-    v = grid((1, 1, p.L, p.head_dim))
-    g = grid((1, 2, p.L))
-    W = rng.standard_normal((1, 2, p.L, p.head_dim)).astype(np.float32).astype(np.float64)
+    Lj = p.L_joint
+    q = grid((1, 2, Lj, p.head_dim))
+    k = grid((1, 1, Lj, p.head_dim))
+    v = grid((1, 1, Lj, p.head_dim))
+    g = grid((1, 2, Lj))
+    W = rng.standard_normal((1, 2, Lj, p.head_dim)).astype(np.float32).astype(np.float64)
     W *= p.token_real()[None, None, :, None]           # padding tokens are not outputs
     rp, ci = _random_csr(p, 44)
+    if text_len:
+        rp, ci, _, _ = oracle.joint_lists(rp, ci, p)
     Bt, Bh, Bw = p.Bt, p.Bh, p.Bw
 
     def forward(qq, kk, vv, gg):
@@ -541,8 +546,10 @@ def test_full_op_gradient_finite_differences(grid_thw):
         of, _ = oracle.attn_fwd(qq, kk, vv, p, rp, ci)
         oc, _ = oracle.coarse_fwd(oracle.pool(qq, p, Bt, Bh, Bw), oracle.pool(kk, p, Bt, Bh, Bw),
                                   oracle.pool(vv, p, Bt, Bh, Bw), p)
-        gate = np.tanh(gg.astype(np.float64))[..., None]
-        return gate * np.repeat(oc, p.B, axis=2) + of.reshape(qq.shape)
+        gate = np.tanh(gg[..., :p.L].astype(np.float64))[..., None]
+        out = of.reshape(qq.shape).copy()
+        out[..., :p.L, :] += gate * np.repeat(oc, p.B, axis=2)
+        return out
 
     def loss(*a):
         return float((forward(*a) * W).sum())
@@ -749,3 +756,94 @@ def test_padded_unpool_is_the_adjoint_of_pool(P):
     nz = rc > 0
     np.testing.assert_allclose(back[:, :, nz], yy[:, :, nz] / rc[nz][:, None], rtol=1e-6)
     assert (back[:, :, ~nz] == 0).all()
+
+
+# ---------------------------------------------------------------- text tokens
+# MMDiT joint attention: Eq. block_sparse extended with full video-to-text
+# and text-to-video blocks (Sec. 2.2).  One (batch, head) sequence is the
+# cube-major video followed by the text tokens padded to whole blocks.
+
+def _joint_mask(p, rp, ci):
+    """Token-level boolean mask [b, Hq, L_joint, L_joint] of the joint
+    attention, built from the video block lists and the text rule directly."""
+    L, Lj = p.L, p.L_joint
+    M = np.zeros((p.batch, p.heads_q, Lj, Lj), bool)
+    M[:, :, :L, :L] = _block_mask(p, rp, ci)       # routed video blocks
+    M[:, :, :L, L:] = True                         # video queries see all text
+    M[:, :, L:, :] = True                          # text queries see everything
+    return M & p.token_real()[None, None, None, :]  # padding keys masked
+
+
+@pytest.mark.parametrize("grid,text_len,hq,hkv", [((3, 5, 6), 37, 2, 2), ((4, 8, 8), 16, 4, 2),
+                                                  ((2, 4, 8), 5, 2, 1)])
+def test_joint_text_attention_matches_masked_sdpa(grid, text_len, hq, hkv):
+    """Joint video + text attention (forward and backward) equals torch's
+    masked SDPA over the concatenated tokens with: routed blocks among video
+    tokens, every text token for video queries, every token for text
+    queries, padding keys masked; padding queries (video or text) give
+    O = 0, LSE = -inf, no gradient."""
+    T, H, W = grid
+    p = Problem(1, hq, hkv, 8, T, H, W, 2, 2, 4, 1, 2, 2, F32, text_len)
+    q, k, v, do = rand_qkv_joint(p, 70)
+    rp, ci = _random_csr(p, 71)
+    jrp, jci, jkp, jki = oracle.joint_lists(rp, ci, p)
+    assert jrp.size == p.batch * hq * p.N_joint + 1
+    real = p.token_real()
+    o, lse = oracle.attn_fwd(q, k, v, p, jrp, jci)
+    o, lse = o.reshape(q.shape), lse.reshape(q.shape[:3])
+    ref, lref, (gq, gk, gv) = _torch_ref(q, k, v, p, _joint_mask(p, rp, ci), do * real[None, None, :, None])
+    np.testing.assert_allclose(o[:, :, real], ref[:, :, real], rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(lse[:, :, real], lref[:, :, real], rtol=1e-12)
+    assert (o[:, :, ~real] == 0).all() and np.isneginf(lse[:, :, ~real]).all()
+    dq = oracle.attn_bwd_dq(q, k, v, do, p, jrp, jci).reshape(q.shape)
+    dk, dv = oracle.attn_bwd_dkdv(q, k, v, do, p, jrp, jci)
+    np.testing.assert_allclose(dq[:, :, real], gq[:, :, real], rtol=1e-10, atol=1e-12)
+    assert (dq[:, :, ~real] == 0).all()
+    np.testing.assert_allclose(dk.reshape(gk.shape), gk, rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dv.reshape(gv.shape), gv, rtol=1e-10, atol=1e-12)
+    # the transposed joint lists are the transpose of the joint CSR
+    grp = hq // hkv
+    Nj = p.N_joint
+    for kr in range(p.batch * hkv * Nj):
+        bkv, nk = divmod(kr, Nj)
+        want = [hl * Nj + nq for hl in range(grp) for nq in range(Nj)
+                if nk in jci[jrp[(bkv * grp + hl) * Nj + nq]:jrp[(bkv * grp + hl) * Nj + nq + 1]]]
+        assert list(jki[jkp[kr]:jkp[kr + 1]]) == want
+
+
+def test_joint_text_rows_are_full_attention_and_text_len_zero_is_video_only():
+    """A text query block attends to every real token (textbook softmax
+    attention over the whole sequence), and with no text the joint lists are
+    the video lists."""
+    p = Problem(1, 2, 2, 8, 2, 4, 8, 2, 2, 4, 1, 2, 2, F32, 20)
+    q, k, v, _ = rand_qkv_joint(p, 72)
+    rp, ci = _random_csr(p, 73)
+    jrp, jci, _, _ = oracle.joint_lists(rp, ci, p)
+    o, _ = oracle.attn_fwd(q, k, v, p, jrp, jci)
+    o = o.reshape(q.shape)
+    real = p.token_real()
+    s = np.einsum("bhid,bhjd->bhij", q.astype(np.float64), k.astype(np.float64)) / math.sqrt(p.head_dim)
+    s[..., ~real] = -np.inf
+    P = _softmax64(s)
+    full = P @ v.astype(np.float64)
+    tq = np.arange(p.L, p.L_joint)[real[p.L:]]
+    np.testing.assert_allclose(o[:, :, tq], full[:, :, tq], rtol=1e-12, atol=1e-13)
+    p0 = p.replace(text_len=0)
+    jrp0, jci0, jkp0, jki0 = oracle.joint_lists(rp, ci, p0)
+    kp0, ki0 = oracle.csr_to_csc(rp, ci, p0)
+    assert np.array_equal(jrp0, rp) and np.array_equal(jci0, ci)
+    assert np.array_equal(jkp0, kp0) and np.array_equal(jki0, ki0)
+
+
+def rand_qkv_joint(p, seed):
+    """rand_qkv over the joint sequence with padding tokens zeroed."""
+    rng = np.random.default_rng(seed)
+    shp = lambda h: (p.batch, h, p.L_joint, p.head_dim)
+    q = rng.standard_normal(shp(p.heads_q)).astype(np.float32)
+    k = rng.standard_normal(shp(p.heads_kv)).astype(np.float32)
+    v = rng.standard_normal(shp(p.heads_kv)).astype(np.float32)
+    do = rng.standard_normal(shp(p.heads_q)).astype(np.float32)
+    real = p.token_real()
+    for t in (q, k, v, do):
+        t[..., ~real, :] = 0.0
+    return q, k, v, do

@@ -53,11 +53,27 @@ class Problem:
     Rh: int = 2
     Rw: int = 2
     dtype: int = BF16
+    text_len: int = 0          # text tokens joined to the video (MMDiT), 0 = none
 
     @property
     def L(self) -> int:
-        """Tokens in the cube-major layout, padding included."""
+        """Video tokens in the cube-major layout, padding included."""
         return self.N * self.B
+
+    @property
+    def M(self) -> int:
+        """Text blocks of B tokens (the last one padded)."""
+        return -(-self.text_len // self.B)
+
+    @property
+    def N_joint(self) -> int:
+        """Blocks of one (batch, head) sequence: N video cubes, then M text blocks."""
+        return self.N + self.M
+
+    @property
+    def L_joint(self) -> int:
+        """Tokens of one (batch, head) sequence: video, then text, padding included."""
+        return self.N_joint * self.B
 
     @property
     def B(self) -> int:
@@ -84,14 +100,16 @@ class Problem:
         return bool(self.T % self.Bt or self.H % self.Bh or self.W % self.Bw)
 
     def token_real(self) -> np.ndarray:
-        """bool [L]: token of the cube-major layout inside the real T x H x W grid
-        (a grid not divisible by the cube is padded up, Sec. 2.2)."""
+        """bool [L_joint]: token of the sequence that is not padding: a video
+        token inside the real T x H x W grid (a grid not divisible by the cube
+        is padded up, Sec. 2.2), or one of the first text_len text tokens."""
         n = np.arange(self.N)[:, None]
         beta = np.arange(self.B)[None, :]
         nt, nh, nw = n // (self.Nh * self.Nw), (n // self.Nw) % self.Nh, n % self.Nw
         bt, bh, bw = beta // (self.Bh * self.Bw), (beta // self.Bw) % self.Bh, beta % self.Bw
-        return ((nt * self.Bt + bt < self.T) & (nh * self.Bh + bh < self.H) &
-                (nw * self.Bw + bw < self.W)).reshape(-1)
+        video = ((nt * self.Bt + bt < self.T) & (nh * self.Bh + bh < self.H) &
+                 (nw * self.Bw + bw < self.W)).reshape(-1)
+        return np.concatenate([video, np.arange(self.M * self.B) < self.text_len])
 
     @property
     def R(self) -> int:
@@ -191,17 +209,22 @@ def _slab(seed: int, tensor_id: int, b: int, h: int, N: int, B: int, D: int,
 
 def make_tensor(p: Problem, seed: int, tensor_id: int, heads: int, with_mean: bool = True,
                 skewed: bool = False, threads: int | None = None) -> np.ndarray:
-    """One [batch, heads, L, D] float32 tensor of the recipe above, rounded to
-    the problem dtype.  tensor_id: 0 = Q, 1 = K, 2 = V, 3 = dO."""
-    out = np.empty((p.batch, heads, p.L, p.head_dim), dtype=np.float32)
+    """One [batch, heads, L_joint, D] float32 tensor of the recipe above,
+    rounded to the problem dtype: the video tokens, then (text_len > 0) the
+    text tokens, N(0,1) from a stream of their own.  tensor_id: 0 = Q, 1 = K,
+    2 = V, 3 = dO."""
+    out = np.empty((p.batch, heads, p.L_joint, p.head_dim), dtype=np.float32)
     jobs = [(b, h) for b in range(p.batch) for h in range(heads)]
     nthr = threads or min(16, os.cpu_count() or 1)
 
-    real = p.token_real() if p.padded else None
+    real = p.token_real() if (p.padded or p.text_len % p.B) else None
 
     def work(bh):
         b, h = bh
-        _slab(seed, tensor_id, b, h, p.N, p.B, p.head_dim, with_mean, skewed, out[b, h])
+        _slab(seed, tensor_id, b, h, p.N, p.B, p.head_dim, with_mean, skewed, out[b, h, :p.L])
+        if p.M:
+            rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, tensor_id, b, h, 1])))
+            out[b, h, p.L:] = rng.standard_normal((p.M * p.B, p.head_dim), dtype=np.float32)
         if p.dtype == BF16:
             out[b, h] = round_bf16_f32(out[b, h])
         if real is not None:
@@ -252,6 +275,8 @@ def _with_means_of(ref: np.ndarray, p: Problem, seed: int, tensor_id: int, threa
             rng2 = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, tensor_id, b, h])))
             eps = rng2.standard_normal((p.N, p.B, p.head_dim), dtype=np.float32) * np.float32(0.5)
             x = (eps + mu[:, None, :]).reshape(p.L, p.head_dim)
+            if p.text_len:
+                raise ValueError("shared_mean inputs have no text tokens")
             out[b, h] = round_bf16_f32(x) if p.dtype == BF16 else x
             if p.padded:
                 out[b, h][~p.token_real()] = 0.0        # padding tokens hold zeros
