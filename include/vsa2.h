@@ -62,6 +62,22 @@
  *   vsa2_gate_merge_bwd  padding tokens are not outputs (dgate = 0, no
  *       contribution to dO_c_hat).
  * Every cube holds at least one real token.
+ *
+ * Text tokens (MMDiT joint attention: Eq. block_sparse extended with full
+ * video-to-text and text-to-video blocks, Sec. 2.2).  With p->text_len =
+ * Lt > 0, every token tensor of a (batch, head) holds the joint sequence:
+ * the L = N*B video tokens (cube-major, as above), then M = ceil(Lt/B) text
+ * blocks of B tokens whose first Lt tokens are real (the rest padding, masked
+ * like grid padding).  Ljoint = (N + M)*B tokens per (batch, head); block
+ * ids N .. N+M-1 are the text blocks.
+ *   vsa2_pool, vsa2_unpool_add  read / update the video part only;
+ *   vsa2_route, vsa2_coarse_*   work on pooled video tensors, unchanged;
+ *   vsa2_joint_lists  expands the router's video lists to the joint lists:
+ *       a video query block keeps its routed video blocks and gains every
+ *       text block; a text query block takes every block;
+ *   vsa2_attn_*  take joint tensors and joint lists (rows batch*Hq*(N+M));
+ *   vsa2_gate_merge(_bwd)  apply the coarse branch to video tokens; text
+ *       tokens keep O_f (out = o_f there) and get dgate = 0.
  */
 #ifndef VSA2_H
 #define VSA2_H
@@ -100,6 +116,8 @@ typedef struct {
     int32_t Bt, Bh, Bw;
     int32_t Rt, Rh, Rw;  /* R_x divides B_x                      */
     int32_t dtype;       /* vsa2_dtype                           */
+    int32_t text_len;    /* Lt >= 0 text tokens joined to the video (MMDiT);
+                            0 = video only                          */
 } vsa2_problem;
 
 typedef enum {
@@ -129,7 +147,8 @@ const char* vsa2_status_str(vsa2_status s);
  * vsa2_pool - MeanPool over (Pt, Ph, Pw) sub-cubes of every B-cube
  * (Sec. 2.2: Eq. router_start with P = R gives Q_r, K_r; Eq. compress with
  * P = B gives the coarse Q_c, K_c, V_c).
- *   x      [batch][heads][L][D], dtype p->dtype, cube-major.
+ *   x      [batch][heads][L][D], dtype p->dtype, cube-major ([Ljoint] rows
+ *          per head with text tokens; only the video part is read).
  *   out    [batch][heads][N*Gp][D], Gp = (Bt/Pt)(Bh/Ph)(Bw/Pw); row n*Gp + g
  *          with g = (gt*Gh + gh)*Gw + gw.  Each value is the mean of the
  *          Pt*Ph*Pw tokens of its sub-cube (of its real tokens on a padded
@@ -199,6 +218,9 @@ vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* byt
  *   row_ptr, col_idx   CSR as produced by vsa2_route; entries outside
  *                      [0, N) and offsets outside [0, col_cap] are skipped
  *                      (clamped), never dereferenced.
+ *   With text tokens (p->text_len > 0) every [L] above is [Ljoint], every
+ *   N is N + M and the lists are those of vsa2_joint_lists; the same holds
+ *   for the backward calls below.
  *   o   [batch][Hq][L][D] output, dtype p->dtype.
  *   lse [batch][Hq][L] fp32 natural-log log-sum-exp of each query's scaled
  *       scores; a query block with no selected block gets o = 0, lse = -inf.
@@ -330,6 +352,36 @@ vsa2_status vsa2_gate_merge(const vsa2_problem* p, const float* gate, const void
  */
 vsa2_status vsa2_gate_merge_bwd(const vsa2_problem* p, const float* gate, const void* o_c, const void* dout,
                                 void* do_c, float* dgate, hipStream_t stream);
+
+/*
+ * Joint video + text block lists (p->text_len > 0).
+ *
+ * vsa2_joint_capacity: entries the joint CSR can hold at most for the
+ *   router's rule: vsa2_route_capacity + batch*Hq*N*M (text blocks of the
+ *   video rows) + batch*Hq*M*(N+M) (the text rows).
+ * vsa2_joint_workspace: bytes of workspace vsa2_joint_lists needs.
+ * vsa2_joint_lists: from the router's video lists (row_ptr [batch*Hq*N+1],
+ *   col_idx [col_cap]) writes
+ *     j_row_ptr [batch*Hq*(N+M) + 1], j_col_idx [j_cap]: joint query block
+ *       (b*Hq + h)*(N+M) + n lists its video blocks (n < N: the routed ones
+ *       in their order, entries outside [0, N) become -1 and are skipped by
+ *       the attention) followed by N .. N+M-1; a text block n >= N lists
+ *       0 .. N+M-1;
+ *     j_kv_ptr [batch*Hkv*(N+M) + 1], j_kv_idx [j_cap]: its transpose, value
+ *       hq_local*(N+M) + n_q ascending (the CSC of vsa2_route with N+M
+ *       blocks).
+ *   Index work only; the lists feed vsa2_attn_fwd / vsa2_attn_bwd with the
+ *   same problem.
+ * Errors: NULL pointers; text_len = 0 (VSA2_ERR_SHAPE); j_cap below
+ *   col_cap + batch*Hq*(N*M + M*(N+M)) (VSA2_ERR_CAPACITY); workspace
+ *   missing or too small.
+ */
+vsa2_status vsa2_joint_capacity(const vsa2_problem* p, const vsa2_select* s, int64_t* pairs);
+vsa2_status vsa2_joint_workspace(const vsa2_problem* p, size_t* bytes);
+vsa2_status vsa2_joint_lists(const vsa2_problem* p, const int32_t* row_ptr, const int32_t* col_idx,
+                             int64_t col_cap, int32_t* j_row_ptr, int32_t* j_col_idx, int64_t j_cap,
+                             int32_t* j_kv_ptr, int32_t* j_kv_idx, void* ws, size_t ws_bytes,
+                             hipStream_t stream);
 
 /*
  * vsa2_unpool_add - the MeanPool adjoint (gradient of vsa2_pool with the

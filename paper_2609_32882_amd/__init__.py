@@ -30,13 +30,13 @@ EXPORTS = ("vsa2_status_str", "vsa2_pool", "vsa2_route_capacity", "vsa2_route_wo
            "vsa2_route", "vsa2_attn_workspace", "vsa2_attn_fwd", "vsa2_attn_bwd",
            "vsa2_attn_bwd_prep", "vsa2_attn_bwd_dkdv", "vsa2_attn_bwd_dq",
            "vsa2_coarse_fwd", "vsa2_coarse_bwd", "vsa2_gate_merge", "vsa2_gate_merge_bwd",
-           "vsa2_unpool_add")
+           "vsa2_joint_capacity", "vsa2_joint_workspace", "vsa2_joint_lists", "vsa2_unpool_add")
 
 
 class vsa2_problem(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("batch", "heads_q", "heads_kv", "head_dim", "T", "H", "W",
-                 "Bt", "Bh", "Bw", "Rt", "Rh", "Rw", "dtype")]
+                 "Bt", "Bh", "Bw", "Rt", "Rh", "Rw", "dtype", "text_len")]
 
 
 class vsa2_select(ctypes.Structure):
@@ -80,6 +80,9 @@ def _lib():
         L.vsa2_gate_merge.argtypes = [pp, P, P, P, P, P]
         L.vsa2_gate_merge_bwd.argtypes = [pp, P, P, P, P, P, P]
         L.vsa2_unpool_add.argtypes = [pp, i32, P, i32, i32, i32, P, P]
+        L.vsa2_joint_capacity.argtypes = [pp, ps, ctypes.POINTER(i64)]
+        L.vsa2_joint_workspace.argtypes = [pp, ctypes.POINTER(sz)]
+        L.vsa2_joint_lists.argtypes = [pp, P, P, i64, P, P, i64, P, P, P, sz, P]
         for n in EXPORTS[1:]:
             getattr(L, n).restype = ctypes.c_int
         _L = L
@@ -183,13 +186,32 @@ def vsa2_unpool_add(p, heads, dx_c, Pt, Ph, Pw, dx, stream=0):
     return _lib().vsa2_unpool_add(_ref(p), heads, dx_c, Pt, Ph, Pw, dx, stream)
 
 
+def vsa2_joint_capacity(p, s):
+    n = ctypes.c_int64(0)
+    st = _lib().vsa2_joint_capacity(_ref(p), _ref(s), ctypes.byref(n))
+    return st, n.value
+
+
+def vsa2_joint_workspace(p):
+    n = ctypes.c_size_t(0)
+    st = _lib().vsa2_joint_workspace(_ref(p), ctypes.byref(n))
+    return st, n.value
+
+
+def vsa2_joint_lists(p, row_ptr, col_idx, col_cap, j_row_ptr, j_col_idx, j_cap, j_kv_ptr, j_kv_idx, ws,
+                     ws_bytes, stream=0):
+    return _lib().vsa2_joint_lists(_ref(p), row_ptr, col_idx, col_cap, j_row_ptr, j_col_idx, j_cap,
+                                   j_kv_ptr, j_kv_idx, ws, ws_bytes, stream)
+
+
 # --------------------------------------------------------------------------
 # torch-tensor helpers (device memory + streams only)
 # --------------------------------------------------------------------------
 
 def make_problem(batch, heads_q, heads_kv, head_dim, T, H, W, Bt=4, Bh=4, Bw=4, Rt=2, Rh=2, Rw=2,
-                 dtype=VSA2_BF16) -> vsa2_problem:
-    return vsa2_problem(batch, heads_q, heads_kv, head_dim, T, H, W, Bt, Bh, Bw, Rt, Rh, Rw, dtype)
+                 dtype=VSA2_BF16, text_len=0) -> vsa2_problem:
+    return vsa2_problem(batch, heads_q, heads_kv, head_dim, T, H, W, Bt, Bh, Bw, Rt, Rh, Rw, dtype,
+                        text_len)
 
 
 def problem_from(obj) -> vsa2_problem:
@@ -197,7 +219,8 @@ def problem_from(obj) -> vsa2_problem:
     if isinstance(obj, vsa2_problem):
         return obj
     return make_problem(obj.batch, obj.heads_q, obj.heads_kv, obj.head_dim, obj.T, obj.H, obj.W,
-                        obj.Bt, obj.Bh, obj.Bw, obj.Rt, obj.Rh, obj.Rw, obj.dtype)
+                        obj.Bt, obj.Bh, obj.Bw, obj.Rt, obj.Rh, obj.Rw, obj.dtype,
+                        getattr(obj, "text_len", 0))
 
 
 def select_from(obj) -> vsa2_select:
@@ -227,6 +250,14 @@ def _dims(p):
     return N, B, G
 
 
+def _joint(p):
+    """(blocks, tokens) of one (batch, head) sequence: the video cubes and
+    then the text blocks (p.text_len > 0), padding included."""
+    N, B, _ = _dims(p)
+    Nj = N + (-(-p.text_len // B))
+    return Nj, Nj * B
+
+
 def _tdtype(p):
     torch = _torch()
     return torch.bfloat16 if p.dtype == VSA2_BF16 else torch.float32
@@ -239,12 +270,13 @@ def _expect(t, shape, dtype, name):
 
 
 def pool(p, x, P, out=None):
-    """MeanPool of x [batch, heads, L, D] over sub-cubes P = (Pt, Ph, Pw)."""
+    """MeanPool of x [batch, heads, L, D] over sub-cubes P = (Pt, Ph, Pw)
+    (the video part of joint video + text sequences)."""
     p = problem_from(p)
     N, B, _ = _dims(p)
     Gp = (p.Bt // P[0]) * (p.Bh // P[1]) * (p.Bw // P[2])
     heads = x.shape[1]
-    _expect(x, (p.batch, heads, N * B, p.head_dim), _tdtype(p), "x")
+    _expect(x, (p.batch, heads, _joint(p)[1], p.head_dim), _tdtype(p), "x")
     if out is None:
         out = _torch().empty((p.batch, heads, N * Gp, p.head_dim), dtype=x.dtype, device=x.device)
     _check("vsa2_pool", vsa2_pool(p, heads, x.data_ptr(), P[0], P[1], P[2], out.data_ptr(), _stream()))
@@ -282,11 +314,11 @@ def route(p, s, q_r, k_r, with_csc=True, with_scores=False):
 
 def attn_fwd(p, q, k, v, row_ptr, col_idx, col_cap=None, o=None, lse=None, compensated=False,
              o_lo=None):
-    """Returns (o, lse), or (o, lse, o_lo) when compensated."""
+    """Returns (o, lse), or (o, lse, o_lo) when compensated.  With text
+    tokens the tensors are joint sequences and the lists joint lists."""
     torch = _torch()
     p = problem_from(p)
-    N, B, _ = _dims(p)
-    L = N * B
+    L = _joint(p)[1]
     dt = _tdtype(p)
     _expect(q, (p.batch, p.heads_q, L, p.head_dim), dt, "q")
     _expect(k, (p.batch, p.heads_kv, L, p.head_dim), dt, "k")
@@ -314,8 +346,7 @@ def attn_bwd(p, q, k, v, o, lse, do, row_ptr, col_idx, kv_ptr, kv_idx, col_cap=N
     """dQ, dK, dV; pass the forward's o_lo for the compensated path."""
     torch = _torch()
     p = problem_from(p)
-    N, B, _ = _dims(p)
-    L = N * B
+    L = _joint(p)[1]
     dt = _tdtype(p)
     for t, hh, nm in ((q, p.heads_q, "q"), (k, p.heads_kv, "k"), (v, p.heads_kv, "v"),
                       (o, p.heads_q, "o"), (do, p.heads_q, "do")):
@@ -418,6 +449,28 @@ def gate_merge_bwd(p, gate, o_c, dout):
                                                       dout.data_ptr(), do_c.data_ptr(),
                                                       dgate.data_ptr(), _stream()))
     return do_c, dgate
+
+
+def joint_lists(p, r):
+    """Joint video + text lists from the router's result r (route()).
+    Returns dict(row_ptr, col_idx, kv_ptr, kv_idx, col_cap)."""
+    torch = _torch()
+    p = problem_from(p)
+    Nj, _ = _joint(p)
+    dev = r["row_ptr"].device
+    cap = r["col_cap"] + p.batch * p.heads_q * (Nj - _dims(p)[0]) * (_dims(p)[0] + Nj)
+    st, wsb = vsa2_joint_workspace(p)
+    _check("vsa2_joint_workspace", st)
+    i32 = torch.int32
+    jrp = torch.empty(p.batch * p.heads_q * Nj + 1, dtype=i32, device=dev)
+    jci = torch.empty(max(cap, 1), dtype=i32, device=dev)
+    jkp = torch.empty(p.batch * p.heads_kv * Nj + 1, dtype=i32, device=dev)
+    jki = torch.empty(max(cap, 1), dtype=i32, device=dev)
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=dev)
+    _check("vsa2_joint_lists", vsa2_joint_lists(p, r["row_ptr"].data_ptr(), r["col_idx"].data_ptr(),
+                                                r["col_cap"], jrp.data_ptr(), jci.data_ptr(), cap,
+                                                jkp.data_ptr(), jki.data_ptr(), ws.data_ptr(), wsb, _stream()))
+    return dict(row_ptr=jrp, col_idx=jci, kv_ptr=jkp, kv_idx=jki, col_cap=cap)
 
 
 def unpool_add(p, dx_c, dx, P):

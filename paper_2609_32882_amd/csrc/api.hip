@@ -16,8 +16,13 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// N, L, rows_*: video cubes / tokens / query- and key-block rows; the
+// joint sequence (video, then M text blocks) has Nj = N + M blocks of B
+// tokens, Lj tokens, rows_qj / rows_kvj block rows (= the video ones
+// without text).
 struct shape {
     int64_t N, L, B, G, rows_q, rows_kv;
+    int64_t M, Nj, Lj, rows_qj, rows_kvj;
 };
 
 // Structural checks shared by all calls.
@@ -28,6 +33,7 @@ vsa2_status check_problem(const vsa2_problem* p, shape* out) {
     if (p->heads_q % p->heads_kv) return VSA2_ERR_SHAPE;
     if (p->T < 1 || p->H < 1 || p->W < 1 || p->Bt < 1 || p->Bh < 1 || p->Bw < 1) return VSA2_ERR_SHAPE;
     if (p->Rt < 1 || p->Rh < 1 || p->Rw < 1) return VSA2_ERR_SHAPE;
+    if (p->text_len < 0) return VSA2_ERR_SHAPE;
     if (p->Bt % p->Rt || p->Bh % p->Rh || p->Bw % p->Rw) return VSA2_ERR_SHAPE;
     shape s;
     s.B = static_cast<int64_t>(p->Bt) * p->Bh * p->Bw;
@@ -38,13 +44,18 @@ vsa2_status check_problem(const vsa2_problem* p, shape* out) {
     s.G = static_cast<int64_t>(p->Bt / p->Rt) * (p->Bh / p->Rh) * (p->Bw / p->Rw);
     s.rows_q = static_cast<int64_t>(p->batch) * p->heads_q * s.N;
     s.rows_kv = static_cast<int64_t>(p->batch) * p->heads_kv * s.N;
-    if (s.N > (1 << 26) || s.rows_q > (int64_t(1) << 31) - 2) return VSA2_ERR_SHAPE;
+    s.M = (p->text_len + s.B - 1) / s.B;
+    s.Nj = s.N + s.M;
+    s.Lj = s.Nj * s.B;
+    s.rows_qj = static_cast<int64_t>(p->batch) * p->heads_q * s.Nj;
+    s.rows_kvj = static_cast<int64_t>(p->batch) * p->heads_kv * s.Nj;
+    if (s.Nj > (1 << 26) || s.rows_qj > (int64_t(1) << 31) - 2) return VSA2_ERR_SHAPE;
     *out = s;
     return VSA2_OK;
 }
 
 vsa2::cube_grid grid_of(const vsa2_problem* p) {
-    return vsa2::make_cube_grid(p->T, p->H, p->W, p->Bt, p->Bh, p->Bw);
+    return vsa2::make_cube_grid(p->T, p->H, p->W, p->Bt, p->Bh, p->Bw, p->text_len);
 }
 
 // Shapes the attention and router kernels are built for.
@@ -93,18 +104,24 @@ route_ws route_layout(const vsa2_problem* p, const shape& s, const vsa2_select* 
 
 // the forward needs no scratch memory
 size_t fwd_ws_bytes(const shape& s, const vsa2_problem* p) {
-    return vsa2::fwd_workspace_bytes(p->batch, p->heads_q, static_cast<int>(s.N));
+    return vsa2::fwd_workspace_bytes(p->batch, p->heads_q, static_cast<int>(s.Nj));
 }
 
 size_t bwd_ws_bytes(const shape& s, const vsa2_problem* p) {
     return vsa2::bwd_workspace_bytes(p->dtype, p->head_dim, p->batch, p->heads_q, p->heads_kv,
-                                     static_cast<int>(s.N));
+                                     static_cast<int>(s.Nj));
 }
 
 #define VSA2_TRY_HIP(expr)                          \
     do {                                            \
         if ((expr) != hipSuccess) return VSA2_ERR_HIP; \
     } while (0)
+
+// entries of the joint lists beyond the video ones: the text blocks of the
+// video rows and the full text rows
+int64_t joint_extra(const vsa2_problem* p, const shape& s) {
+    return static_cast<int64_t>(p->batch) * p->heads_q * (s.N * s.M + s.M * s.Nj);
+}
 
 }  // namespace
 
@@ -137,7 +154,7 @@ vsa2_status vsa2_pool(const vsa2_problem* p, int32_t heads, const void* x, int32
     if (p->head_dim % 8) return VSA2_ERR_UNSUPPORTED;
     if (!aligned16(x) || !aligned16(out)) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_pool(p->dtype, x, out, static_cast<int64_t>(p->batch) * heads,
-                                   static_cast<int>(s.N), p->head_dim, grid_of(p), Pt, Ph, Pw, stream));
+                                   static_cast<int>(s.N), s.Lj, p->head_dim, grid_of(p), Pt, Ph, Pw, stream));
     return VSA2_OK;
 }
 
@@ -239,7 +256,7 @@ vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, c
     if (!ws || ws_bytes < fwd_ws_bytes(s, p)) return VSA2_ERR_WORKSPACE;
     if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_attn_fwd(p->dtype, p->head_dim, q, k, v, row_ptr, col_idx, col_cap, o, lse,
-                                       o_lo, ws, p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N),
+                                       o_lo, ws, p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.Nj),
                                        grid_of(p), stream));
     return VSA2_OK;
 }
@@ -265,7 +282,7 @@ vsa2_status vsa2_attn_bwd(const vsa2_problem* p, const void* q, const void* k, c
     if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_attn_bwd(p->dtype, p->head_dim, q, k, v, o, lse, o_lo, dout, row_ptr, col_idx,
                                        kv_ptr, kv_idx, col_cap, dq, dk, dv, ws,
-                                       p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N), grid_of(p),
+                                       p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.Nj), grid_of(p),
                                        stream));
     return VSA2_OK;
 }
@@ -282,7 +299,7 @@ vsa2_status vsa2_attn_bwd_prep(const vsa2_problem* p, const void* o, const float
     if (!ws || ws_bytes < need) return VSA2_ERR_WORKSPACE;
     if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_attn_bwd_prep(p->dtype, p->head_dim, o, lse, o_lo, dout, ws, p->batch,
-                                            p->heads_q, static_cast<int>(s.N), stream));
+                                            p->heads_q, static_cast<int>(s.Nj), stream));
     return VSA2_OK;
 }
 
@@ -304,7 +321,7 @@ vsa2_status vsa2_attn_bwd_dkdv(const vsa2_problem* p, const void* q, const void*
     if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_attn_bwd_dkdv(p->dtype, p->head_dim, compensated != 0, q, k, v, dout, kv_ptr,
                                             kv_idx, col_cap, dk, dv, ws, p->batch, p->heads_q, p->heads_kv,
-                                            static_cast<int>(s.N), grid_of(p), stream));
+                                            static_cast<int>(s.Nj), grid_of(p), stream));
     return VSA2_OK;
 }
 
@@ -325,7 +342,7 @@ vsa2_status vsa2_attn_bwd_dq(const vsa2_problem* p, const void* q, const void* k
     if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_attn_bwd_dq(p->dtype, p->head_dim, compensated != 0, q, k, v, dout, row_ptr,
                                           col_idx, col_cap, dq, ws, p->batch, p->heads_q, p->heads_kv,
-                                          static_cast<int>(s.N), grid_of(p), stream));
+                                          static_cast<int>(s.Nj), grid_of(p), stream));
     return VSA2_OK;
 }
 
@@ -370,8 +387,9 @@ vsa2_status vsa2_gate_merge(const vsa2_problem* p, const float* gate, const void
     if ((st = check_kernel_shape(p, s)) != VSA2_OK) return st;
     if (!gate || !o_c || !o_f || !out) return VSA2_ERR_NULL;
     if (!aligned16(o_c) || !aligned16(o_f) || !aligned16(out)) return VSA2_ERR_ALIGN;
-    VSA2_TRY_HIP(vsa2::launch_gate_merge(p->dtype, p->head_dim, gate, o_c, o_f, out, s.rows_q * s.B,
-                                         static_cast<int>(s.B), stream));
+    VSA2_TRY_HIP(vsa2::launch_gate_merge(p->dtype, p->head_dim, gate, o_c, o_f, out,
+                                         static_cast<int64_t>(p->batch) * p->heads_q * s.Lj, s.L, s.Lj,
+                                         static_cast<int>(s.N), stream));
     return VSA2_OK;
 }
 
@@ -384,7 +402,50 @@ vsa2_status vsa2_gate_merge_bwd(const vsa2_problem* p, const float* gate, const 
     if (!gate || !o_c || !dout || !do_c || !dgate) return VSA2_ERR_NULL;
     if (!aligned16(o_c) || !aligned16(dout) || !aligned16(do_c)) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_gate_merge_bwd(p->dtype, p->head_dim, gate, o_c, dout, do_c, dgate, s.rows_q,
-                                             static_cast<int>(s.N), grid_of(p), stream));
+                                             static_cast<int>(s.N), static_cast<int>(s.M), grid_of(p), stream));
+    return VSA2_OK;
+}
+
+vsa2_status vsa2_joint_capacity(const vsa2_problem* p, const vsa2_select* sel, int64_t* pairs) {
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if ((st = check_select(sel)) != VSA2_OK) return st;
+    if (!pairs) return VSA2_ERR_NULL;
+    *pairs = s.rows_q * keep_per_row(sel, s.N) + joint_extra(p, s);
+    return VSA2_OK;
+}
+
+vsa2_status vsa2_joint_workspace(const vsa2_problem* p, size_t* bytes) {
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if (!bytes) return VSA2_ERR_NULL;
+    *bytes = vsa2::joint_workspace_bytes(p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N),
+                                         static_cast<int>(s.M));
+    return VSA2_OK;
+}
+
+vsa2_status vsa2_joint_lists(const vsa2_problem* p, const int32_t* row_ptr, const int32_t* col_idx,
+                             int64_t col_cap, int32_t* j_row_ptr, int32_t* j_col_idx, int64_t j_cap,
+                             int32_t* j_kv_ptr, int32_t* j_kv_idx, void* ws, size_t ws_bytes,
+                             hipStream_t stream) {
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if (p->text_len < 1) return VSA2_ERR_SHAPE;
+    if (!row_ptr || !j_row_ptr || !j_col_idx || !j_kv_ptr || !j_kv_idx) return VSA2_ERR_NULL;
+    if (!col_idx && col_cap > 0) return VSA2_ERR_NULL;
+    if (col_cap < 0) return VSA2_ERR_CAPACITY;
+    const int64_t need = col_cap + joint_extra(p, s);
+    if (j_cap < need || need > (int64_t(1) << 31) - 1) return VSA2_ERR_CAPACITY;
+    const size_t wsb = vsa2::joint_workspace_bytes(p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.N),
+                                                   static_cast<int>(s.M));
+    if (!ws || ws_bytes < wsb) return VSA2_ERR_WORKSPACE;
+    if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
+    VSA2_TRY_HIP(vsa2::launch_joint_lists(row_ptr, col_idx, col_cap, p->batch, p->heads_q, p->heads_kv,
+                                          static_cast<int>(s.N), static_cast<int>(s.M), j_row_ptr, j_col_idx, j_cap,
+                                          j_kv_ptr, j_kv_idx, ws, stream));
     return VSA2_OK;
 }
 
@@ -399,8 +460,8 @@ vsa2_status vsa2_unpool_add(const vsa2_problem* p, int32_t heads, const void* dx
     if (p->head_dim != 64 && p->head_dim != 128) return VSA2_ERR_UNSUPPORTED;
     if (!aligned16(dx_c) || !aligned16(dx)) return VSA2_ERR_ALIGN;
     VSA2_TRY_HIP(vsa2::launch_unpool_add(p->dtype, p->head_dim, dx_c, dx,
-                                         static_cast<int64_t>(p->batch) * heads * s.L, static_cast<int>(s.N),
-                                         grid_of(p), Pt, Ph, Pw, stream));
+                                         static_cast<int64_t>(p->batch) * heads * s.L, s.L, s.Lj,
+                                         static_cast<int>(s.N), grid_of(p), Pt, Ph, Pw, stream));
     return VSA2_OK;
 }
 

@@ -393,22 +393,29 @@ __global__ __launch_bounds__(CB_NT) void coarse_dq_kernel(const T* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
-// Gated merge: out[l] = tanh(g_l) * oc[l / B] + of[l]; one thread per 8
-// elements.
+// Gated merge: out[l] = tanh(g_l) * oc[cube(l)] + of[l] for the L video
+// tokens of each sequence of Lj tokens; text tokens (l >= L) keep of[l].
+// One thread per 8 elements.
 // ---------------------------------------------------------------------------
 template <typename T, int D>
 __global__ __launch_bounds__(256) void gate_merge_kernel(const float* __restrict__ gate, const T* __restrict__ oc,
                                                          const T* __restrict__ of, T* __restrict__ out,
-                                                         int64_t ntok, int B) {
+                                                         int64_t ntok, int64_t L, int64_t Lj, int N) {
     constexpr int PARTS = D / 8;
     const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     const int64_t tok = t / PARTS;
     if (tok >= ntok) return;
     const int d0 = static_cast<int>(t % PARTS) * 8;
-    const float gv = tanhf(gate[tok]);
-    const T* c = oc + (tok / B) * D + d0;
+    const int64_t bh = tok / Lj, l = tok - bh * Lj;
     const T* f = of + tok * D + d0;
     T* o = out + tok * D + d0;
+    if (l >= L) {               // a text token: no coarse branch
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o[i] = f[i];
+        return;
+    }
+    const float gv = tanhf(gate[tok]);
+    const T* c = oc + (bh * N + l / 64) * D + d0;
 #pragma unroll
     for (int i = 0; i < 8; ++i) from_f32(o[i], fmaf(gv, to_f32(c[i]), to_f32(f[i])));
 }
@@ -416,17 +423,27 @@ __global__ __launch_bounds__(256) void gate_merge_kernel(const float* __restrict
 // Backward of the merge: one workgroup of 256 per cube.  Four threads per
 // token (D/4 elements each): dg_l = (1 - tanh(g_l)^2) (dout_l . oc_n);
 // doc[n] = sum_l tanh(g_l) dout_l, summed over the cube's 64 tokens in LDS.
+// Sequences hold N video cubes then M text blocks (Lj = (N + M) * 64
+// tokens); the workgroups past the video cubes write dg = 0 for the text
+// tokens, which have no coarse branch.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void gate_merge_bwd_kernel(const float* __restrict__ gate,
                                                              const T* __restrict__ oc,
                                                              const T* __restrict__ dout, T* __restrict__ doc,
-                                                             float* __restrict__ dgate, int N, cube_grid grid) {
+                                                             float* __restrict__ dgate, int64_t ncubes, int N,
+                                                             int M, cube_grid grid) {
     constexpr int PER = D / 4;
     __shared__ float part[64][D + 1];
     const int tid = threadIdx.x;
-    const int64_t cube = blockIdx.x;                 // (b * Hq + h) * N + n
     const int t = tid >> 2, q4 = tid & 3;
-    const int64_t tok = cube * 64 + t;
+    const int64_t Lj = static_cast<int64_t>(N + M) * 64;
+    if (blockIdx.x >= ncubes) {                      // text block (b * Hq + h) * M + m
+        const int64_t tb = blockIdx.x - ncubes;
+        if (q4 == 0) dgate[(tb / M) * Lj + static_cast<int64_t>(N) * 64 + (tb % M) * 64 + t] = 0.f;
+        return;
+    }
+    const int64_t cube = blockIdx.x;                 // (b * Hq + h) * N + n
+    const int64_t tok = (cube / N) * Lj + (cube % N) * 64 + t;
     // a padding token of a padded grid is not an output: gate 0, dgate 0
     bool real = true;
     if (grid.padded) real = token_in(grid, cube_extent(grid, static_cast<int>(cube % N)), t);
@@ -456,16 +473,16 @@ __global__ __launch_bounds__(256) void gate_merge_bwd_kernel(const float* __rest
 // sub-cube and padding tokens receive nothing.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void unpool_add_kernel(const T* __restrict__ dxc, T* __restrict__ dx,
-                                                         int64_t ntok, int N, int Pt, int Ph, int Pw,
-                                                         cube_grid grid) {
+                                                         int64_t ntok, int64_t L, int64_t Lj, int N, int Pt,
+                                                         int Ph, int Pw, cube_grid grid) {
     constexpr int PARTS = D / 8;
     const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    const int64_t tok = t / PARTS;
+    const int64_t tok = t / PARTS;                   // video token (bh, l): bh * L + l
     if (tok >= ntok) return;
     const int Bt = grid.Bt, Bh = grid.Bh, Bw = grid.Bw;
     const int d0 = static_cast<int>(t % PARTS) * 8;
     const int B = Bt * Bh * Bw;
-    const int64_t cube = tok / B;
+    const int64_t cube = tok / B;                    // bh * N + n (L = N * B)
     const int beta = static_cast<int>(tok % B);
     const int bw = beta % Bw, bhh = (beta / Bw) % Bh, bt = beta / (Bw * Bh);
     const int Gh = Bh / Ph, Gw = Bw / Pw, Gp = (Bt / Pt) * Gh * Gw;
@@ -479,7 +496,7 @@ __global__ __launch_bounds__(256) void unpool_add_kernel(const T* __restrict__ d
     }
     const float inv = 1.0f / static_cast<float>(cnt);
     const T* src = dxc + (cube * Gp + g) * D + d0;
-    T* dst = dx + tok * D + d0;
+    T* dst = dx + ((tok / L) * Lj + tok % L) * D + d0;   // sequences of Lj tokens (video first)
 #pragma unroll
     for (int i = 0; i < 8; ++i) from_f32(dst[i], fmaf(to_f32(src[i]), inv, to_f32(dst[i])));
 }
@@ -535,31 +552,33 @@ hipError_t launch_coarse_bwd(int dtype, int D, const void* qc, const void* kc, c
 }
 
 hipError_t launch_gate_merge(int dtype, int D, const float* gate, const void* oc, const void* of, void* out,
-                             int64_t ntok, int B, hipStream_t s) {
+                             int64_t ntok, int64_t L, int64_t Lj, int N, hipStream_t s) {
     if (ntok == 0) return hipSuccess;
     const unsigned blocks = static_cast<unsigned>((ntok * (D / 8) + 255) / 256);
     VSA2_COARSE_DISPATCH(hipLaunchKernelGGL((gate_merge_kernel<T, DD>), dim3(blocks), dim3(256), 0, s, gate,
                                             static_cast<const T*>(oc), static_cast<const T*>(of),
-                                            static_cast<T*>(out), ntok, B);
+                                            static_cast<T*>(out), ntok, L, Lj, N);
                          return hipGetLastError());
 }
 
 hipError_t launch_gate_merge_bwd(int dtype, int D, const float* gate, const void* oc, const void* dout, void* doc,
-                                 float* dgate, int64_t ncubes, int N, const cube_grid& cg, hipStream_t s) {
+                                 float* dgate, int64_t ncubes, int N, int M, const cube_grid& cg, hipStream_t s) {
     if (ncubes == 0) return hipSuccess;
-    VSA2_COARSE_DISPATCH(hipLaunchKernelGGL((gate_merge_bwd_kernel<T, DD>), dim3(static_cast<unsigned>(ncubes)),
+    const int64_t blocks = ncubes + ncubes / N * M;     // video cubes, then the text blocks
+    VSA2_COARSE_DISPATCH(hipLaunchKernelGGL((gate_merge_bwd_kernel<T, DD>), dim3(static_cast<unsigned>(blocks)),
                                             dim3(256), 0, s, gate, static_cast<const T*>(oc),
-                                            static_cast<const T*>(dout), static_cast<T*>(doc), dgate, N, cg);
+                                            static_cast<const T*>(dout), static_cast<T*>(doc), dgate, ncubes, N,
+                                            M, cg);
                          return hipGetLastError());
 }
 
-hipError_t launch_unpool_add(int dtype, int D, const void* dxc, void* dx, int64_t ntok, int N,
-                             const cube_grid& cg, int Pt, int Ph, int Pw, hipStream_t s) {
+hipError_t launch_unpool_add(int dtype, int D, const void* dxc, void* dx, int64_t ntok, int64_t L, int64_t Lj,
+                             int N, const cube_grid& cg, int Pt, int Ph, int Pw, hipStream_t s) {
     if (ntok == 0) return hipSuccess;
     const unsigned blocks = static_cast<unsigned>((ntok * (D / 8) + 255) / 256);
     VSA2_COARSE_DISPATCH(hipLaunchKernelGGL((unpool_add_kernel<T, DD>), dim3(blocks), dim3(256), 0, s,
-                                            static_cast<const T*>(dxc), static_cast<T*>(dx), ntok, N, Pt, Ph, Pw,
-                                            cg);
+                                            static_cast<const T*>(dxc), static_cast<T*>(dx), ntok, L, Lj, N, Pt,
+                                            Ph, Pw, cg);
                          return hipGetLastError());
 }
 #undef VSA2_COARSE_DISPATCH

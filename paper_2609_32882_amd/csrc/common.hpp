@@ -549,10 +549,15 @@ __device__ __forceinline__ bool token_in(const cube_grid& g, int3 e, int beta) {
     return bt < e.x && bh < e.y && bw < e.z;
 }
 
-// Bit beta set for each real token of 64-token cube n.  Called by a whole
-// wave (lane = its lane index); the result is wave-uniform.
+// Bit beta set for each real token of 64-token block n (a video cube, or a
+// text block when n >= Nv).  Called by a whole wave (lane = its lane index);
+// the result is wave-uniform.
 __device__ __forceinline__ uint64_t cube_real_mask(const cube_grid& g, int n, int lane) {
     if (!g.padded) return ~0ull;
+    if (n >= g.Nv) {
+        const int left = g.text_len - (n - g.Nv) * 64;     // real text tokens from this block on
+        return left >= 64 ? ~0ull : (left <= 0 ? 0ull : (~0ull >> (64 - left)));
+    }
     const int3 e = cube_extent(g, n);
     if (cube_is_full(g, e)) return ~0ull;
     return __ballot(token_in(g, e, lane));

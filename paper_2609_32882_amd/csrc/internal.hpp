@@ -15,20 +15,26 @@ namespace vsa2 {
 // of a cube in (bt, bh, bw) raster order).  The real tokens of a cube form
 // the box [0, rt) x [0, rh) x [0, rw) of its in-cube coordinates; only the
 // last cube along a padded axis is cut, and every cube holds a real token.
+// With text tokens (MMDiT joint attention) a sequence continues after the
+// Nv video cubes with text blocks of B tokens, the first text_len real.
 struct cube_grid {
     int T, H, W;
     int Bt, Bh, Bw;
     int Nh, Nw;
-    int padded;     // some axis is not a multiple of its cube size
+    int Nv;         // video cubes per sequence
+    int text_len;   // real text tokens after them
+    int padded;     // some block holds padding (a cut cube or text tail)
 };
 
-inline cube_grid make_cube_grid(int T, int H, int W, int Bt, int Bh, int Bw) {
+inline cube_grid make_cube_grid(int T, int H, int W, int Bt, int Bh, int Bw, int text_len) {
     cube_grid g;
     g.T = T; g.H = H; g.W = W;
     g.Bt = Bt; g.Bh = Bh; g.Bw = Bw;
     g.Nh = (H + Bh - 1) / Bh;
     g.Nw = (W + Bw - 1) / Bw;
-    g.padded = (T % Bt) || (H % Bh) || (W % Bw);
+    g.Nv = ((T + Bt - 1) / Bt) * g.Nh * g.Nw;
+    g.text_len = text_len;
+    g.padded = (T % Bt) || (H % Bh) || (W % Bw) || (text_len % (Bt * Bh * Bw));
     return g;
 }
 
@@ -55,8 +61,8 @@ int resident_per_xcd(int block) {
     return v;
 }
 
-hipError_t launch_pool(int dtype, const void* x, void* out, int64_t nbh, int N, int D, const cube_grid& cg,
-                       int Pt, int Ph, int Pw, hipStream_t s);
+hipError_t launch_pool(int dtype, const void* x, void* out, int64_t nbh, int N, int64_t Lj, int D,
+                       const cube_grid& cg, int Pt, int Ph, int Pw, hipStream_t s);
 hipError_t launch_route_passes(int dtype, int D, int G, const void* qr, const void* kr, float* lse2,
                                float* scores, int batch, int Hq, int Hkv, int N, const cube_grid& cg, int Rt,
                                int Rh, int Rw, hipStream_t s);
@@ -105,11 +111,18 @@ hipError_t launch_coarse_bwd(int dtype, int D, const void* qc, const void* kc, c
                              void* dqc, void* dkc, void* dvc, void* ws, int batch, int Hq, int Hkv, int N,
                              hipStream_t s);
 hipError_t launch_gate_merge(int dtype, int D, const float* gate, const void* oc, const void* of, void* out,
-                             int64_t ntok, int B, hipStream_t s);
+                             int64_t ntok, int64_t L, int64_t Lj, int N, hipStream_t s);
 hipError_t launch_gate_merge_bwd(int dtype, int D, const float* gate, const void* oc, const void* dout, void* doc,
-                                 float* dgate, int64_t ncubes, int N, const cube_grid& cg, hipStream_t s);
-hipError_t launch_unpool_add(int dtype, int D, const void* dxc, void* dx, int64_t ntok, int N, const cube_grid& cg,
-                             int Pt, int Ph, int Pw, hipStream_t s);
+                                 float* dgate, int64_t ncubes, int N, int M, const cube_grid& cg, hipStream_t s);
+hipError_t launch_unpool_add(int dtype, int D, const void* dxc, void* dx, int64_t ntok, int64_t L, int64_t Lj,
+                             int N, const cube_grid& cg, int Pt, int Ph, int Pw, hipStream_t s);
+// Joint video + text lists from the router's video lists (rows of N video
+// cubes; M text blocks per sequence).  ws: int32 counts per joint row, then
+// the CSC workspace.
+size_t joint_workspace_bytes(int batch, int Hq, int Hkv, int N, int M);
+hipError_t launch_joint_lists(const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, int batch, int Hq,
+                              int Hkv, int N, int M, int32_t* j_row_ptr, int32_t* j_col_idx, int64_t j_cap,
+                              int32_t* j_kv_ptr, int32_t* j_kv_idx, void* ws, hipStream_t s);
 hipError_t launch_attn_bwd_dkdv(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
                                 const void* dout, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
                                 void* dk, void* dv, void* ws, int batch, int Hq, int Hkv, int N,

@@ -18,13 +18,14 @@ namespace vsa2 {
 // Pool
 // ===========================================================================
 // One thread per (output row, 8-element chunk of D).  Output row
-// (bh*N + n)*G + g averages the real tokens of sub-cube g of cube n: all
+// (bh*N + n)*G + g averages the real tokens of sub-cube g of cube n (of a
+// sequence of Lj tokens: the N*B video tokens, then any text tokens): all
 // Pt*Ph*Pw of them unless the grid is padded, where the real tokens of a
 // sub-cube form a box and an all-padding sub-cube pools to 0.
 template <typename T>
 __global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ x, T* __restrict__ out,
-                                                   int64_t nthreads, int N, int D, int G, int Gh, int Gw,
-                                                   int Pt, int Ph, int Pw, int B, cube_grid grid) {
+                                                   int64_t nthreads, int N, int64_t Lj, int D, int G, int Gh,
+                                                   int Gw, int Pt, int Ph, int Pw, int B, cube_grid grid) {
     const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     if (t >= nthreads) return;
     const int chunks = D / 8;
@@ -34,6 +35,7 @@ __global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ x, T* _
     const int64_t cube = orow / G;                   // bh*N + n
     const int gt = g / (Gh * Gw), gh = (g / Gw) % Gh, gw = g % Gw;
     const int Bh = grid.Bh, Bw = grid.Bw;
+    const T* xc = x + ((cube / N) * Lj + (cube % N) * B) * D;   // the cube's first token
     // real part of the sub-cube: [0, et) x [0, eh) x [0, ew) of its offsets
     int et = Pt, eh = Ph, ew = Pw;
     if (grid.padded) {
@@ -49,7 +51,7 @@ __global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ x, T* _
         for (int rh = 0; rh < eh; ++rh)
             for (int rw = 0; rw < ew; ++rw) {
                 const int beta = ((gt * Pt + rt) * Bh + gh * Ph + rh) * Bw + gw * Pw + rw;
-                const T* src = x + (cube * B + beta) * D + ch * 8;
+                const T* src = xc + beta * D + ch * 8;
                 if constexpr (sizeof(T) == 2) {
                     const uint4 w = *reinterpret_cast<const uint4*>(src);
                     const uint32_t u[4] = {w.x, w.y, w.z, w.w};
@@ -85,8 +87,8 @@ __global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ x, T* _
     }
 }
 
-hipError_t launch_pool(int dtype, const void* x, void* out, int64_t nbh, int N, int D, const cube_grid& grid,
-                       int Pt, int Ph, int Pw, hipStream_t s) {
+hipError_t launch_pool(int dtype, const void* x, void* out, int64_t nbh, int N, int64_t Lj, int D,
+                       const cube_grid& grid, int Pt, int Ph, int Pw, hipStream_t s) {
     const int Bt = grid.Bt, Bh = grid.Bh, Bw = grid.Bw;
     const int Gt = Bt / Pt, Gh = Bh / Ph, Gw = Bw / Pw, G = Gt * Gh * Gw;
     const int64_t nthreads = nbh * N * G * (D / 8);
@@ -95,11 +97,11 @@ hipError_t launch_pool(int dtype, const void* x, void* out, int64_t nbh, int N, 
     const int B = Bt * Bh * Bw;
     if (dtype == 1)
         hipLaunchKernelGGL(pool_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s,
-                           static_cast<const bf16_t*>(x), static_cast<bf16_t*>(out), nthreads, N, D, G,
+                           static_cast<const bf16_t*>(x), static_cast<bf16_t*>(out), nthreads, N, Lj, D, G,
                            Gh, Gw, Pt, Ph, Pw, B, grid);
     else
         hipLaunchKernelGGL(pool_kernel<float>, dim3(blocks), dim3(256), 0, s,
-                           static_cast<const float*>(x), static_cast<float*>(out), nthreads, N, D, G,
+                           static_cast<const float*>(x), static_cast<float*>(out), nthreads, N, Lj, D, G,
                            Gh, Gw, Pt, Ph, Pw, B, grid);
     return hipGetLastError();
 }
@@ -892,6 +894,97 @@ hipError_t launch_csc(const int32_t* row_ptr, const int32_t* col_idx, int batch,
     hipLaunchKernelGGL(csc_emit_kernel, dim3(static_cast<unsigned>((nkrows + 255) / 256)), dim3(256), 0, s,
                        mask, nkrows, words, kv_ptr, kv_idx, col_cap);
     return hipGetLastError();
+}
+
+// ===========================================================================
+// Joint video + text lists (MMDiT joint attention)
+// ===========================================================================
+// Joint row r = bh*(N+M) + n.  A video row (n < N) lists the routed video
+// blocks of row bh*N + n in their order (entries outside [0, N) become -1,
+// which the attention skips) and then the M text blocks N .. N+M-1; a text
+// row (n >= N) lists every block 0 .. N+M-1.
+__global__ void joint_count_kernel(const int32_t* __restrict__ row_ptr, int64_t col_cap, int64_t nrows_j, int N,
+                                   int M, int32_t* __restrict__ counts) {
+    const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (r >= nrows_j) return;
+    const int Nj = N + M;
+    const int64_t bh = r / Nj;
+    const int n = static_cast<int>(r % Nj);
+    if (n >= N) {
+        counts[r] = Nj;
+        return;
+    }
+    const int64_t row = bh * N + n;
+    int64_t s0 = row_ptr[row], s1 = row_ptr[row + 1];
+    s0 = s0 < 0 ? 0 : (s0 > col_cap ? col_cap : s0);
+    s1 = s1 < s0 ? s0 : (s1 > col_cap ? col_cap : s1);
+    counts[r] = static_cast<int32_t>(s1 - s0) + M;
+}
+
+// One wave per joint row; writes stay below j_cap.
+__global__ __launch_bounds__(256) void joint_emit_kernel(const int32_t* __restrict__ row_ptr,
+                                                         const int32_t* __restrict__ col_idx, int64_t col_cap,
+                                                         int64_t nrows_j, int N, int M,
+                                                         const int32_t* __restrict__ j_row_ptr,
+                                                         int32_t* __restrict__ j_col_idx, int64_t j_cap) {
+    const int64_t r = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (r >= nrows_j) return;
+    const int Nj = N + M;
+    const int64_t bh = r / Nj;
+    const int n = static_cast<int>(r % Nj);
+    int64_t o = j_row_ptr[r];
+    o = o < 0 ? 0 : (o > j_cap ? j_cap : o);
+    auto put = [&](int64_t pos, int32_t v) {
+        if (pos < j_cap) j_col_idx[pos] = v;
+    };
+    if (n >= N) {
+        for (int i = lane; i < Nj; i += 64) put(o + i, i);
+        return;
+    }
+    const int64_t row = bh * N + n;
+    int64_t s0 = row_ptr[row], s1 = row_ptr[row + 1];
+    s0 = s0 < 0 ? 0 : (s0 > col_cap ? col_cap : s0);
+    s1 = s1 < s0 ? s0 : (s1 > col_cap ? col_cap : s1);
+    for (int64_t e = s0 + lane; e < s1; e += 64) {
+        const int32_t c = col_idx[e];
+        put(o + (e - s0), (c >= 0 && c < N) ? c : -1);
+    }
+    for (int i = lane; i < M; i += 64) put(o + (s1 - s0) + i, N + i);
+}
+
+static size_t align256b(size_t x) { return (x + 255) / 256 * 256; }
+
+size_t joint_workspace_bytes(int batch, int Hq, int Hkv, int N, int M) {
+    const int64_t Nj = static_cast<int64_t>(N) + M;
+    const int64_t words = (static_cast<int64_t>(Hq / Hkv) * Nj + 31) / 32;
+    const int64_t rows_q = static_cast<int64_t>(batch) * Hq * Nj, rows_kv = static_cast<int64_t>(batch) * Hkv * Nj;
+    return align256b(4 * static_cast<size_t>(rows_q)) + align256b(4 * static_cast<size_t>(rows_kv * words)) +
+           align256b(4 * static_cast<size_t>(rows_kv));
+}
+
+hipError_t launch_joint_lists(const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, int batch, int Hq,
+                              int Hkv, int N, int M, int32_t* j_row_ptr, int32_t* j_col_idx, int64_t j_cap,
+                              int32_t* j_kv_ptr, int32_t* j_kv_idx, void* ws, hipStream_t s) {
+    const int Nj = N + M;
+    const int64_t nrows_j = static_cast<int64_t>(batch) * Hq * Nj;
+    const int64_t rows_kv = static_cast<int64_t>(batch) * Hkv * Nj;
+    const int64_t words = (static_cast<int64_t>(Hq / Hkv) * Nj + 31) / 32;
+    char* base = static_cast<char*>(ws);
+    int32_t* counts = reinterpret_cast<int32_t*>(base);
+    uint32_t* mask = reinterpret_cast<uint32_t*>(base + align256b(4 * static_cast<size_t>(nrows_j)));
+    int32_t* kv_counts = reinterpret_cast<int32_t*>(base + align256b(4 * static_cast<size_t>(nrows_j)) +
+                                                    align256b(4 * static_cast<size_t>(rows_kv * words)));
+    if (nrows_j == 0) return hipSuccess;
+    hipLaunchKernelGGL(joint_count_kernel, dim3(static_cast<unsigned>((nrows_j + 255) / 256)), dim3(256), 0, s,
+                       row_ptr, col_cap, nrows_j, N, M, counts);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if ((e = launch_scan(counts, nrows_j, j_row_ptr, s)) != hipSuccess) return e;
+    hipLaunchKernelGGL(joint_emit_kernel, dim3(static_cast<unsigned>((nrows_j + 3) / 4)), dim3(256), 0, s, row_ptr,
+                       col_idx, col_cap, nrows_j, N, M, j_row_ptr, j_col_idx, j_cap);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    return launch_csc(j_row_ptr, j_col_idx, batch, Hq, Hkv, Nj, j_cap, mask, kv_counts, j_kv_ptr, j_kv_idx, s);
 }
 
 }  // namespace vsa2

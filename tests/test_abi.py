@@ -85,6 +85,32 @@ def test_grid_not_divisible_by_the_cube_is_padded_up():
         assert vsa2.STATUS_NAMES[st] == "VSA2_OK" and n == 4 * N * min(5, N), (T, H, W)
 
 
+def test_joint_lists_checks():
+    """Text tokens: the joint capacity adds the text blocks of the video rows
+    and the full text rows; vsa2_joint_lists needs text, enough capacity
+    and a workspace."""
+    sel = vsa2.vsa2_select(0, 5, 0.0, 0)
+    p = vsa2.make_problem(1, 4, 2, 128, 8, 16, 16, text_len=100)     # N = 32, M = 2
+    st, cap = vsa2.vsa2_joint_capacity(p, sel)
+    assert vsa2.STATUS_NAMES[st] == "VSA2_OK" and cap == 4 * 32 * 5 + 4 * (32 * 2 + 2 * 34)
+    st, wsb = vsa2.vsa2_joint_workspace(p)
+    assert vsa2.STATUS_NAMES[st] == "VSA2_OK" and wsb > 0
+    call = lambda pp, jcap, ws, wsz: vsa2.STATUS_NAMES[vsa2.vsa2_joint_lists(
+        pp, FAKE, FAKE, 4 * 32 * 5, FAKE, FAKE, jcap, FAKE, FAKE, ws, wsz, None)]
+    assert call(vsa2.make_problem(1, 4, 2, 128, 8, 16, 16), cap, FAKE, wsb) == "VSA2_ERR_SHAPE"
+    assert call(p, cap - 1, FAKE, wsb) == "VSA2_ERR_CAPACITY"
+    assert call(p, cap, None, 0) == "VSA2_ERR_WORKSPACE"
+    assert call(p, cap, FAKE, wsb - 1) == "VSA2_ERR_WORKSPACE"
+    assert vsa2.STATUS_NAMES[vsa2.vsa2_joint_lists(p, None, FAKE, 1, FAKE, FAKE, cap, FAKE, FAKE, FAKE, wsb,
+                                                   None)] == "VSA2_ERR_NULL"
+    # the attention workspaces grow with the text blocks
+    _, w0 = vsa2.vsa2_attn_workspace(vsa2.make_problem(1, 4, 2, 128, 8, 16, 16), 1)
+    _, w1 = vsa2.vsa2_attn_workspace(p, 1)
+    assert w1 > w0
+    p.text_len = -1
+    assert vsa2.STATUS_NAMES[vsa2.vsa2_joint_capacity(p, sel)[0]] == "VSA2_ERR_SHAPE"
+
+
 def test_null_and_alignment_checks():
     p = good()
     assert vsa2.STATUS_NAMES[vsa2.vsa2_attn_fwd(p, None, FAKE, FAKE, FAKE, FAKE, 1, FAKE, FAKE, None,
