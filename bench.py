@@ -66,7 +66,9 @@ def main():
     p, sel = w.problem, w.select
     P = vsa2.problem_from(p)
     S = vsa2.select_from(sel)
-    N, B, G, L, D = p.N, p.B, p.G, p.L, p.head_dim
+    N, B, G, D = p.N, p.B, p.G, p.head_dim
+    L = p.L_joint                       # tokens per (batch, head): video, then any text
+    joint = p.text_len > 0
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     t0 = time.time()
@@ -84,6 +86,11 @@ def main():
     assert st == 0
     st, bws = vsa2.vsa2_attn_workspace(P, 1)
     assert st == 0
+    if joint:                           # text tokens: the attention runs on the joint lists
+        st, jcap = vsa2.vsa2_joint_capacity(P, S)
+        assert st == 0
+        st, jws = vsa2.vsa2_joint_workspace(P)
+        assert st == 0
     i32 = torch.int32
     q_r = torch.empty((p.batch, p.heads_q, N * G, D), dtype=tdt, device=dev)
     k_r = torch.empty((p.batch, p.heads_kv, N * G, D), dtype=tdt, device=dev)
@@ -92,6 +99,16 @@ def main():
     kv_ptr = torch.empty(p.batch * p.heads_kv * N + 1, dtype=i32, device=dev)
     kv_idx = torch.empty(cap, dtype=i32, device=dev)
     rws_t = torch.empty(rws, dtype=torch.uint8, device=dev)
+    if joint:
+        Nj = p.N_joint
+        j_row_ptr = torch.empty(p.batch * p.heads_q * Nj + 1, dtype=i32, device=dev)
+        j_col_idx = torch.empty(jcap, dtype=i32, device=dev)
+        j_kv_ptr = torch.empty(p.batch * p.heads_kv * Nj + 1, dtype=i32, device=dev)
+        j_kv_idx = torch.empty(jcap, dtype=i32, device=dev)
+        jws_t = torch.empty(max(jws, 1), dtype=torch.uint8, device=dev)
+        a_rp, a_ci, a_kp, a_ki, a_cap = j_row_ptr, j_col_idx, j_kv_ptr, j_kv_idx, jcap
+    else:
+        a_rp, a_ci, a_kp, a_ki, a_cap = row_ptr, col_idx, kv_ptr, kv_idx, cap
     fws_t = torch.empty(max(fws, 1), dtype=torch.uint8, device=dev)
     bws_t = torch.empty(max(bws, 1), dtype=torch.uint8, device=dev)
     o = torch.empty_like(q)
@@ -121,22 +138,27 @@ def main():
         chk("pool", vsa2.vsa2_pool(P, p.heads_kv, k.data_ptr(), p.Rt, p.Rh, p.Rw, k_r.data_ptr(), sp))
         mark(1)
         chk("route", vsa2.vsa2_route(P, S, q_r.data_ptr(), k_r.data_ptr(), row_ptr.data_ptr(),
-                                     col_idx.data_ptr(), cap, kv_ptr.data_ptr(), kv_idx.data_ptr(),
-                                     None, rws_t.data_ptr(), rws, sp))
+                                     col_idx.data_ptr(), cap, None if joint else kv_ptr.data_ptr(),
+                                     None if joint else kv_idx.data_ptr(), None, rws_t.data_ptr(), rws, sp))
+        if joint:                       # the text blocks join every row (part of routing)
+            chk("joint_lists", vsa2.vsa2_joint_lists(P, row_ptr.data_ptr(), col_idx.data_ptr(), cap,
+                                                     j_row_ptr.data_ptr(), j_col_idx.data_ptr(), jcap,
+                                                     j_kv_ptr.data_ptr(), j_kv_idx.data_ptr(), jws_t.data_ptr(),
+                                                     jws, sp))
         mark(2)
-        chk("fwd", vsa2.vsa2_attn_fwd(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), row_ptr.data_ptr(),
-                                      col_idx.data_ptr(), cap, o.data_ptr(), lse.data_ptr(), None,
+        chk("fwd", vsa2.vsa2_attn_fwd(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), a_rp.data_ptr(),
+                                      a_ci.data_ptr(), a_cap, o.data_ptr(), lse.data_ptr(), None,
                                       fws_t.data_ptr(), fws, sp))
         mark(3)
         chk("bwd_prep", vsa2.vsa2_attn_bwd_prep(P, o.data_ptr(), lse.data_ptr(), None, do.data_ptr(),
                                                 bws_t.data_ptr(), bws, sp))
         mark(4)
         chk("bwd_dkdv", vsa2.vsa2_attn_bwd_dkdv(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(),
-                                                kv_ptr.data_ptr(), kv_idx.data_ptr(), cap, 0, dk.data_ptr(),
+                                                a_kp.data_ptr(), a_ki.data_ptr(), a_cap, 0, dk.data_ptr(),
                                                 dv.data_ptr(), bws_t.data_ptr(), bws, sp))
         mark(5)
         chk("bwd_dq", vsa2.vsa2_attn_bwd_dq(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(),
-                                            row_ptr.data_ptr(), col_idx.data_ptr(), cap, 0, dq.data_ptr(),
+                                            a_rp.data_ptr(), a_ci.data_ptr(), a_cap, 0, dq.data_ptr(),
                                             bws_t.data_ptr(), bws, sp))
         mark(6)
         if record:
@@ -165,7 +187,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    nnz = int(row_ptr[-1].item())
+    nnz = int(a_rp[-1].item())          # block pairs the attention computes (joint lists with text)
     b2d = float(B * B * D)
     flop_fwd = 4.0 * b2d * nnz
     flop_bwd = 10.0 * b2d * nnz
@@ -192,10 +214,12 @@ def main():
         "data": "synthetic (seeded cube-mean + noise video-token tensors, no trained weights)",
         "config": {
             "workload": w.name, "batch": p.batch, "grid_THW": [p.T, p.H, p.W], "tokens": L,
+            "text_tokens": p.text_len,
             "heads_q": p.heads_q, "heads_kv": p.heads_kv, "head_dim": D,
             "cube": [p.Bt, p.Bh, p.Bw], "router_pool": [p.Rt, p.Rh, p.Rw],
             "select": ("top-%d" % sel.k) if sel.mode == 0 else ("mass-%.2f-cap-%d" % (sel.mass, sel.cap)),
-            "nnz_block_pairs": nnz, "sparsity": round(1.0 - nnz / float(p.batch * p.heads_q * N * N), 4),
+            "nnz_block_pairs": nnz,
+            "sparsity": round(1.0 - nnz / float(p.batch * p.heads_q * p.N_joint * p.N_joint), 4),
         },
         "breakdown_ms": {s: round(stage_ms[s], 4) for s in ("pool", "route", "fwd", "bwd") + stages[3:]},
         "attn_fwd_bwd_ms": round(attn_ms, 4),
@@ -212,7 +236,7 @@ def main():
     if coarse:
         out["coarse_branch_ms"] = coarse
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, x, row_ptr, col_idx, args.cpu_rows, args.cpu_kv)
+        out["cpu_baseline"] = cpu_baseline(w, x, a_rp, a_ci, args.cpu_rows, args.cpu_kv)
     print(json.dumps(out), flush=True)
 
 
@@ -231,7 +255,7 @@ def time_coarse_branch(vsa2, torch, p, q, k, v, do, o_f, dq, dk, dv, stream, rep
     vc = torch.empty_like(kc)
     oc = torch.empty_like(qc)
     lse_c = torch.empty((p.batch, p.heads_q, N), dtype=torch.float32, device=dev)
-    gate = torch.randn((p.batch, p.heads_q, p.L), generator=torch.Generator(device=dev).manual_seed(9),
+    gate = torch.randn((p.batch, p.heads_q, p.L_joint), generator=torch.Generator(device=dev).manual_seed(9),
                        device=dev, dtype=torch.float32)
     merged = torch.empty_like(o_f)
     doc, dgate = torch.empty_like(qc), torch.empty_like(gate)
@@ -325,11 +349,12 @@ def cpu_baseline(w, x, row_ptr_t, col_idx_t, nrows_sample, nkv_sample):
     rp = row_ptr_t.cpu().numpy()
     ci = col_idx_t.cpu().numpy()[:rp[-1]]
     rng = np.random.default_rng(7)
-    nrow = p.batch * p.heads_q * p.N
+    Nj = p.N_joint                      # with text tokens the lists are the joint lists
+    nrow = p.batch * p.heads_q * Nj
     rows = np.sort(rng.choice(nrow, nrows_sample, replace=False)).astype(np.int64)
-    kv_rows = np.sort(rng.choice(p.batch * p.heads_kv * p.N, nkv_sample, replace=False)).astype(np.int64)
+    kv_rows = np.sort(rng.choice(p.batch * p.heads_kv * Nj, nkv_sample, replace=False)).astype(np.int64)
     pairs_q = int(sum(rp[r + 1] - rp[r] for r in rows))
-    kp, _ = oracle.csr_to_csc(rp, ci, p)
+    kp, _ = oracle.csr_to_csc(rp, ci, p, Nj)
     pairs_kv = int(sum(kp[r + 1] - kp[r] for r in kv_rows))
     b2d = float(p.B * p.B * p.head_dim)
     t0 = time.perf_counter()

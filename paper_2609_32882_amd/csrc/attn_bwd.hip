@@ -98,7 +98,7 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
     __shared__ __align__(1024) float2 st_lds[2][64];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = wave_id(), half = lane >> 5;
-    const int64_t krow = work_row(order, xcd_item(blockIdx.x, gridDim.x, N, true), gridDim.x);   // (b*Hkv + hkv)*N + nk
+    const int64_t krow = work_row(order, xcd_item(blockIdx.x, gridDim.x), gridDim.x);   // (b*Hkv + hkv)*N + nk
     const int64_t bkv = krow / N;
     const int nk = static_cast<int>(krow % N);
     const int b = static_cast<int>(bkv / Hkv), hkv = static_cast<int>(bkv % Hkv);
@@ -316,7 +316,7 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     __shared__ __align__(1024) char v_lds[RT::BYTES];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = wave_id(), half = lane >> 5;
-    const int64_t row = work_row(order, xcd_item(blockIdx.x, gridDim.x, N, false), gridDim.x);
+    const int64_t row = work_row(order, xcd_item(blockIdx.x, gridDim.x), gridDim.x);
     const int64_t bh = row / N;
     const int n = static_cast<int>(row % N);
     const int b = static_cast<int>(bh / Hq), h = static_cast<int>(bh % Hq);
@@ -520,7 +520,7 @@ static hipError_t launch_dkdv_t(const void* q, const void* k, const void* v, con
     const int64_t krows = static_cast<int64_t>(batch) * Hkv * N;
     if (krows == 0) return hipSuccess;
     int32_t* order = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + bwd_ws_csc_order_offset(batch, Hq, N));
-    hipError_t e = launch_lpt_order(kv_ptr, krows, N, col_cap, true, order, s);
+    hipError_t e = launch_lpt_order(kv_ptr, krows, N, col_cap, order, s);
     if (e != hipSuccess) return e;
     const float c = kLog2e / sqrtf(static_cast<float>(D));
     const float scale = 1.0f / sqrtf(static_cast<float>(D));
@@ -543,7 +543,7 @@ static hipError_t launch_dq_t(const void* q, const void* k, const void* v, const
     const int64_t qrows = static_cast<int64_t>(batch) * Hq * N;
     if (qrows == 0) return hipSuccess;
     int32_t* order = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + bwd_ws_csr_order_offset(batch, Hq, N));
-    hipError_t e = launch_lpt_order(row_ptr, qrows, N, col_cap, false, order, s);
+    hipError_t e = launch_lpt_order(row_ptr, qrows, N, col_cap, order, s);
     if (e != hipSuccess) return e;
     const float c = kLog2e / sqrtf(static_cast<float>(D));
     const float scale = 1.0f / sqrtf(static_cast<float>(D));

@@ -47,7 +47,7 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     __shared__ __align__(1024) char v_lds[VT::BYTES];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = wave_id(), half = lane >> 5;
-    const int64_t row = work_row(order, xcd_item(blockIdx.x, gridDim.x, N, false), gridDim.x);
+    const int64_t row = work_row(order, xcd_item(blockIdx.x, gridDim.x), gridDim.x);
     const int64_t bh = row / N;
     const int n = static_cast<int>(row % N);
     const int b = static_cast<int>(bh / Hq), h = static_cast<int>(bh % Hq);
@@ -268,7 +268,7 @@ static hipError_t launch_fwd_t(const void* q, const void* k, const void* v, cons
                                hipStream_t s) {
     const int64_t rows = static_cast<int64_t>(batch) * Hq * N;
     if (rows == 0) return hipSuccess;
-    hipError_t e = launch_lpt_order(row_ptr, rows, N, col_cap, false, order, s);
+    hipError_t e = launch_lpt_order(row_ptr, rows, N, col_cap, order, s);
     if (e != hipSuccess) return e;
     if (o_lo) {
         if (cg.padded) launch_fwd_k<T, D, true, true>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, rows, Hq, Hkv, N, cg, s);

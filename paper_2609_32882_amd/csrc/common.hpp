@@ -169,53 +169,14 @@ __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 
 // Workgroup -> work-item mapping that keeps neighbouring items on one XCD.
 // Workgroups are dispatched round-robin over the 8 XCDs (workgroup id mod 8),
-// each with its own L2.  Two layouts (heads of npos rows, n items):
-//  - contiguous: XCD x takes the range [x*q + min(x, r), ...) of all items
-//    (q = n / 8, r = n % 8), i.e. whole heads one after the other: the
-//    workgroups of one XCD work on nearby blocks of one head, whose tiles
-//    stay in that XCD's L2;
-//  - head chunks (npos a multiple of 8): XCD x takes the x-th eighth of
-//    every head, heads in order, so all XCDs work on the same head at a
-//    time and what misses L2 is shared in the last-level cache (eight
-//    different heads at a time, 8 x 39 MB at 720p, do not fit in it).
-// Measured at 720p: the query-stationary kernels are faster with contiguous
-// ranges (forward 15.4 vs 16.2 ms), the dK/dV kernel with head chunks
-// (27.7 vs 28.3 ms).  item_segment() gives the range of items an XCD works
-// through in order that holds a given item.
-__device__ __forceinline__ bool chunked_layout(bool chunks, int64_t n, int64_t npos) {
-    return chunks && (npos & 7) == 0 && n % npos == 0;
-}
-
-__device__ __forceinline__ int64_t xcd_item(int64_t bid, int64_t n, int64_t npos, bool chunks) {
+// each with its own L2.  Mapping XCD x to the contiguous range of items
+// [x*q + min(x, r), ...) (q = n / 8, r = n % 8) makes the workgroups of one
+// XCD work on the same head and nearby blocks, so the key/value tiles they
+// gather stay in that XCD's L2 instead of being fetched by all eight.
+__device__ __forceinline__ int64_t xcd_item(int64_t bid, int64_t n) {
+    const int64_t q = n >> 3, r = n & 7;
     const int64_t x = bid & 7, i = bid >> 3;
-    if (chunked_layout(chunks, n, npos)) {
-        const int64_t c = npos >> 3;
-        return (i / c) * npos + x * c + i % c;
-    }
-    const int64_t q = n >> 3, r = n & 7;
     return x * q + (x < r ? x : r) + i;
-}
-
-// [begin, end) of the items one XCD works through in order that contains
-// item s: an eighth of a head, or the part of an XCD range inside one head.
-__device__ __forceinline__ void item_segment(int64_t s, int64_t n, int64_t npos, bool chunks, int64_t* beg,
-                                             int64_t* end) {
-    const int64_t h0 = s / npos * npos, h1 = h0 + npos < n ? h0 + npos : n;
-    if (chunked_layout(chunks, n, npos)) {
-        const int64_t c = npos >> 3;
-        *beg = h0 + (s - h0) / c * c;
-        *end = *beg + c;
-        return;
-    }
-    const int64_t q = n >> 3, r = n & 7;
-    int64_t xb = 0, xe = 0;
-    for (int64_t x = 0; x < 8; ++x) {
-        xb = xe;
-        xe = (x + 1) * q + (x + 1 < r ? x + 1 : r);
-        if (s < xe) break;
-    }
-    *beg = xb > h0 ? xb : h0;
-    *end = xe < h1 ? xe : h1;
 }
 
 // Row processed by work item `item` of a launch of n items: order[item]

@@ -91,10 +91,9 @@ size_t bwd_workspace_bytes(int dtype, int D, int batch, int Hq, int Hkv, int N);
 size_t bwd_ws_csr_order_offset(int batch, int Hq, int N);
 size_t bwd_ws_csc_order_offset(int batch, int Hq, int N);
 // Longest-first work order of the rows of ptr within each piece of a head
-// (n_per_head rows) that one XCD works through in order (xcd_item with the
-// given layout).
-hipError_t launch_lpt_order(const int32_t* ptr, int64_t nrows, int64_t n_per_head, int64_t cap, bool chunks,
-                            int32_t* order, hipStream_t s);
+// (n_per_head rows) that falls into one XCD range.
+hipError_t launch_lpt_order(const int32_t* ptr, int64_t nrows, int64_t n_per_head, int64_t cap, int32_t* order,
+                            hipStream_t s);
 hipError_t launch_attn_bwd(int dtype, int D, const void* q, const void* k, const void* v, const void* o,
                            const float* lse, const void* o_lo, const void* dout, const int32_t* row_ptr,
                            const int32_t* col_idx, const int32_t* kv_ptr, const int32_t* kv_idx,

@@ -7,12 +7,12 @@
 // longest rows first makes that queue a longest-processing-time-first
 // schedule, so the last workgroups to start are short and the tail of the
 // launch stays short when row lengths vary (mass selection; key
-// in-degrees).  The rows are reordered only inside each piece of a head
-// that one XCD works through in order (item_segment: the rows xcd_item
-// gives it within one head): the rows of an XCD do not change, and
-// workgroups resident together keep working on one head, whose tiles its L2
-// holds (sorting a whole XCD range mixes its heads and, measured at 720p,
-// raised the dK/dV kernel's L2 miss share from 74% to 89%).
+// in-degrees).  The rows are reordered only inside each segment where an
+// XCD's range (the rows xcd_item gives it) meets one head's N rows: the
+// rows of an XCD do not change, and workgroups resident together keep
+// working on one head, whose tiles its L2 holds (sorting a whole XCD range
+// mixes its heads and, measured at 720p, raised the dK/dV kernel's L2 miss
+// share from 74% to 89%).
 //
 // Rows are grouped into 32 length classes, class = len * 32 / (max_len + 1)
 // over the segment, heaviest class first and row order inside a class (a
@@ -105,30 +105,34 @@ __device__ void lpt_segment(const int32_t* __restrict__ ptr, int64_t cap, int32_
 // One workgroup per head (rows [h*n_per_head, (h+1)*n_per_head)), which
 // sorts each piece of the head that falls into one XCD range.
 __global__ __launch_bounds__(PLAN_NT) void lpt_order_kernel(const int32_t* __restrict__ ptr, int64_t nrows,
-                                                            int64_t n_per_head, int64_t cap, bool chunks,
+                                                            int64_t n_per_head, int64_t cap,
                                                             int32_t* __restrict__ order) {
     __shared__ uint32_t hist[PLAN_CLASSES][PLAN_NT];
     __shared__ uint32_t part[PLAN_NT];
     __shared__ int64_t red[PLAN_NT / 64];
     const int64_t h0 = static_cast<int64_t>(blockIdx.x) * n_per_head;
     const int64_t h1 = h0 + n_per_head < nrows ? h0 + n_per_head : nrows;
+    const int64_t q = nrows >> 3, r = nrows & 7;
     int64_t s0 = h0;
     while (s0 < h1) {
-        // the piece of this head one XCD works through in order (xcd_item)
-        int64_t b0 = 0, s1 = 0;
-        item_segment(s0, nrows, n_per_head, chunks, &b0, &s1);
-        s1 = s1 < h1 ? s1 : h1;
+        // XCD range holding row s0 and its end
+        int64_t x = 0, xend = 0;
+        for (x = 0; x < 8; ++x) {
+            xend = (x + 1) * q + (x + 1 < r ? x + 1 : r);
+            if (s0 < xend) break;
+        }
+        const int64_t s1 = xend < h1 ? xend : h1;
         lpt_segment(ptr, cap, order, s0, s1 - s0, hist, part, red);
         s0 = s1;
     }
 }
 
-hipError_t launch_lpt_order(const int32_t* ptr, int64_t nrows, int64_t n_per_head, int64_t cap, bool chunks,
-                            int32_t* order, hipStream_t s) {
+hipError_t launch_lpt_order(const int32_t* ptr, int64_t nrows, int64_t n_per_head, int64_t cap, int32_t* order,
+                            hipStream_t s) {
     if (nrows <= 0) return hipSuccess;
     const int64_t heads = (nrows + n_per_head - 1) / n_per_head;
     hipLaunchKernelGGL(lpt_order_kernel, dim3(static_cast<unsigned>(heads)), dim3(PLAN_NT), 0, s, ptr, nrows,
-                       n_per_head, cap, chunks, order);
+                       n_per_head, cap, order);
     return hipGetLastError();
 }
 

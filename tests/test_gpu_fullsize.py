@@ -19,7 +19,7 @@ from workload import BF16, WORKLOADS, make_inputs
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
-FULL = ["480p", "720p", "720p-mass", "gqa-long", "720p-seq", "720p-vsa", "720p-latent"]
+FULL = ["480p", "720p", "720p-mass", "gqa-long", "720p-seq", "720p-vsa", "720p-latent", "720p-text"]
 
 
 def _dev(x):
@@ -37,16 +37,19 @@ def run(request):
     q_r = vsa2.pool(p, dev["q"], (p.Rt, p.Rh, p.Rw))
     k_r = vsa2.pool(p, dev["k"], (p.Rt, p.Rh, p.Rw))
     r = vsa2.route(p, w.select, q_r, k_r, with_scores=True)
-    f = vsa2.attn_fwd(p, dev["q"], dev["k"], dev["v"], r["row_ptr"], r["col_idx"], compensated=comp)
+    # with text tokens the attention runs on the joint lists
+    a = vsa2.joint_lists(p, r) if p.text_len else r
+    f = vsa2.attn_fwd(p, dev["q"], dev["k"], dev["v"], a["row_ptr"], a["col_idx"], compensated=comp)
     o, lse = f[0], f[1]
     o_lo = f[2] if comp else None
     g = None
     if w.backward:
-        g = vsa2.attn_bwd(p, dev["q"], dev["k"], dev["v"], o, lse, dev["do"], r["row_ptr"],
-                          r["col_idx"], r["kv_ptr"], r["kv_idx"], o_lo=o_lo)
+        g = vsa2.attn_bwd(p, dev["q"], dev["k"], dev["v"], o, lse, dev["do"], a["row_ptr"],
+                          a["col_idx"], a["kv_ptr"], a["kv_idx"], o_lo=o_lo)
     torch.cuda.synchronize()
-    out = dict(w=w, p=p, x=x, dev=dev, q_r=q_r, k_r=k_r, r=r, o=o, lse=lse, o_lo=o_lo, g=g,
-               rp=r["row_ptr"].cpu().numpy(), ci=r["col_idx"].cpu().numpy())
+    out = dict(w=w, p=p, x=x, dev=dev, q_r=q_r, k_r=k_r, r=r, a=a, o=o, lse=lse, o_lo=o_lo, g=g,
+               rp=r["row_ptr"].cpu().numpy(), ci=r["col_idx"].cpu().numpy(),
+               arp=a["row_ptr"].cpu().numpy(), aci=a["col_idx"].cpu().numpy())
     yield out
     out.clear()
     gc.collect()
@@ -81,15 +84,24 @@ def test_block_lists_structure(run):
     kp, ki = oracle.csr_to_csc(rp, c.astype(np.int32), p)
     assert np.array_equal(run["r"]["kv_ptr"].cpu().numpy(), kp)
     assert np.array_equal(run["r"]["kv_idx"].cpu().numpy()[:nnz], ki)
+    if p.text_len:      # the joint lists expand the GPU's own video lists exactly
+        jrp, jci, jkp, jki = oracle.joint_lists(rp, c.astype(np.int32), p)
+        jn = int(jrp[-1])
+        assert np.array_equal(run["arp"], jrp) and np.array_equal(run["aci"][:jn], jci)
+        assert np.array_equal(run["a"]["kv_ptr"].cpu().numpy(), jkp)
+        assert np.array_equal(run["a"]["kv_idx"].cpu().numpy()[:jn], jki)
     print("nnz %d, counts min/mean/max %d/%.1f/%d" % (nnz, counts.min(), counts.mean(), counts.max()))
 
 
-def _sample_rows(p, n, seed, heads=None):
+def _sample_rows(p, n, seed, heads=None, joint=False):
     rng = np.random.default_rng(seed)
-    nrows = p.batch * (p.heads_q if heads is None else heads) * p.N
+    Nb = p.N_joint if joint else p.N
+    nrows = p.batch * (p.heads_q if heads is None else heads) * Nb
     rows = rng.choice(nrows, n, replace=False)
     if p.padded:    # the last cube of a head is cut along every padded axis
         rows = np.union1d(rows, [p.N - 1, nrows - 1])
+    if joint and p.M:   # a text row and the last (cut) text block of the first head
+        rows = np.union1d(rows, [p.N, Nb - 1])
     return np.sort(rows).astype(np.int64)
 
 
@@ -117,8 +129,8 @@ def test_router_rows_against_oracle(run):
 
 def test_forward_rows_against_oracle(run):
     p, x = run["p"], run["x"]
-    rows = _sample_rows(p, 16, 2)
-    o_ref, lse_ref = oracle.attn_fwd(x["q"], x["k"], x["v"], p, run["rp"], run["ci"], rows)
+    rows = _sample_rows(p, 16, 2, joint=True)
+    o_ref, lse_ref = oracle.attn_fwd(x["q"], x["k"], x["v"], p, run["arp"], run["aci"], rows)
     o = to_np(run["o"]).reshape(-1, p.B, p.head_dim)[rows]
     lse = run["lse"].cpu().numpy().reshape(-1, p.B)[rows]
     assert_values(o, o_ref, "O (sampled rows)")
@@ -130,11 +142,11 @@ def test_backward_rows_against_oracle(run):
     if not w.backward:
         pytest.skip("forward-only workload")
     dq, dk, dv = run["g"]
-    rows = _sample_rows(p, 8, 3)
-    dq_ref = oracle.attn_bwd_dq(x["q"], x["k"], x["v"], x["do"], p, run["rp"], run["ci"], rows)
+    rows = _sample_rows(p, 8, 3, joint=True)
+    dq_ref = oracle.attn_bwd_dq(x["q"], x["k"], x["v"], x["do"], p, run["arp"], run["aci"], rows)
     assert_values(to_np(dq).reshape(-1, p.B, p.head_dim)[rows], dq_ref, "dQ (sampled rows)")
-    kvrows = _sample_rows(p, 4, 4, heads=p.heads_kv)
-    dk_ref, dv_ref = oracle.attn_bwd_dkdv(x["q"], x["k"], x["v"], x["do"], p, run["rp"], run["ci"],
+    kvrows = _sample_rows(p, 4, 4, heads=p.heads_kv, joint=True)
+    dk_ref, dv_ref = oracle.attn_bwd_dkdv(x["q"], x["k"], x["v"], x["do"], p, run["arp"], run["aci"],
                                           kvrows)
     assert_values(to_np(dk).reshape(-1, p.B, p.head_dim)[kvrows], dk_ref, "dK (sampled blocks)")
     assert_values(to_np(dv).reshape(-1, p.B, p.head_dim)[kvrows], dv_ref, "dV (sampled blocks)")
@@ -143,7 +155,7 @@ def test_backward_rows_against_oracle(run):
 def test_repeatable_and_fully_written(run):
     """A second pass with NaN-filled outputs reproduces every output bit."""
     p, w, dev = run["p"], run["w"], run["dev"]
-    r = run["r"]
+    r = run["a"]
     comp = run["o_lo"] is not None
     o2 = torch.full_like(dev["q"], float("nan"))
     lse2 = torch.full_like(run["lse"], float("nan"))

@@ -335,18 +335,13 @@ def test_bwd_unselected_blocks_are_zero_explicit():
     assert_values(to_np(dv).reshape(dv_ref.shape), dv_ref, "dV (two blocks)")
 
 
-def _check_lpt_order(order, lengths, n_per_head, chunks=False):
-    """order is a permutation of each segment one XCD works through in
-    order, longest length class first (class = len * 32 // (max_len + 1)
-    over the segment) and in row order inside a class.  Segments: where one
-    of the 8 contiguous XCD ranges meets one head's rows, or (chunks, heads
-    of a multiple of 8 rows) the eighths of every head."""
+def _check_lpt_order(order, lengths, n_per_head):
+    """order is a permutation of each segment where one of the 8 XCD ranges
+    meets one head's rows, longest length class first (class = len * 32 //
+    (max_len + 1) over the segment) and in row order inside a class."""
     n = lengths.size
     q, r = divmod(n, 8)
-    if chunks and n_per_head % 8 == 0 and n % n_per_head == 0:
-        cuts = list(range(0, n + 1, n_per_head // 8))
-    else:
-        cuts = sorted(set([x * q + min(x, r) for x in range(9)] + list(range(0, n + 1, n_per_head))))
+    cuts = sorted(set([x * q + min(x, r) for x in range(9)] + list(range(0, n + 1, n_per_head))))
     for beg, end in zip(cuts[:-1], cuts[1:]):
         if end <= beg:
             continue
@@ -404,8 +399,7 @@ def test_work_order_and_ragged_rows():
     assert st == 0
     torch.cuda.synchronize()
     kv_order = bws[off:off + 4 * nkv].view(torch.int32).cpu().numpy()
-    assert p.N % 8 == 0                 # the dK/dV kernel's head-chunk layout
-    _check_lpt_order(kv_order, np.diff(kp).astype(np.int64), p.N, chunks=True)
+    _check_lpt_order(kv_order, np.diff(kp).astype(np.int64), p.N)
     o_ref, lse_ref = oracle.attn_fwd(x["q"], x["k"], x["v"], p, rp, ci)
     assert_values(to_np(o).reshape(o_ref.shape), o_ref, "O (ragged rows)")
     empty = np.repeat(counts == 0, p.B)

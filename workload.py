@@ -171,6 +171,10 @@ WORKLOADS = {
     # to 24 x 48 x 80, N = 1440 cubes, top-120
     "720p-latent": Workload(
         "720p-latent", Problem(1, 40, 40, 128, 21, 45, 80), Selection(0, 120), 1005),
+    # the 720p grid joined by 512 text tokens (MMDiT joint attention: every
+    # video block also attends to the 8 text blocks, text attends to all)
+    "720p-text": Workload(
+        "720p-text", Problem(1, 40, 40, 128, 20, 48, 80, text_len=512), Selection(0, 120), 1006),
 }
 
 
