@@ -466,6 +466,18 @@ struct async_tile {
 #pragma unroll
         for (int j = 0; j < PER_WAVE; ++j) dma16(l0 + (wave * PER_WAVE + j) * 1024, g, off[j]);
     }
+    // A tile of which only the first `rows` rows (>= 1) exist in memory: the
+    // other slots are filled from the first row (never read past the end).
+    __device__ __forceinline__ void issue_rows(char* lds, const char* g, int wave, int lane, int64_t rows) const {
+        const uint32_t l0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)lds));
+#pragma unroll
+        for (int j = 0; j < PER_WAVE; ++j) {
+            const int p = (wave * PER_WAVE + j) * 1024 + lane * 16;
+            const int row = p / STRIDE;                    // LDS slot
+            const int grow = PERM ? swap_bits_2_3(row) : row;
+            dma16(l0 + (wave * PER_WAVE + j) * 1024, g, (row < ROWS && grow < rows) ? off[j] : (off[j] % RB));
+        }
+    }
 };
 
 // A-operand fragment of a transposed use of a row-major tile.

@@ -146,8 +146,8 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
     using F = typename frag_of<T>::type;
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;
-    using KT = tile_rows<T, D, RT_NT>;
-    __shared__ __align__(16) char kt_lds[64 * D * E];
+    using AT = async_tile<64, D * E, RT_NT / 64, true, E == 2>;   // K_r rows (slot-swapped)
+    __shared__ __align__(1024) char kt_lds[2][AT::BYTES];           // double buffer
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
     const int bh = blockIdx.y;
@@ -188,12 +188,26 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
         }
     }
 
-    KT ktile;
-    for (int64_t j0 = 0; j0 < NG; j0 += 64) {
-        ktile.load(kbase, j0, NG, tid);
-        __syncthreads();
-        ktile.store(kt_lds, true, tid);
-        __syncthreads();
+    // K_r tiles stream through two LDS buffers with asynchronous copies: the
+    // next tile's copy is issued before this tile's products
+    const AT at(wave, lane);
+    const int64_t ntiles = (NG + 63) / 64;
+    auto issue_tile = [&](int64_t t) {
+        const char* src = reinterpret_cast<const char*>(kbase + t * 64 * D);
+        const int64_t rows = NG - t * 64;
+        if (rows >= 64) at.issue(kt_lds[t & 1], src, wave);
+        else at.issue_rows(kt_lds[t & 1], src, wave, lane, rows);
+    };
+    for (int qt = 0; qt < 2; ++qt)
+        for (int ks = 0; ks < KS; ++ks) settle(qf[qt][ks]);   // fragments in registers before the copies start
+    issue_tile(0);
+    for (int64_t t = 0; t < ntiles; ++t) {
+        const int64_t j0 = t * 64;
+        const bool has_next = t + 1 < ntiles;
+        if (has_next) issue_tile(t + 1);
+        if (has_next) vm_wait<AT::PER_WAVE>(); else vm_wait<0>();   // tile t landed
+        wg_barrier();
+        const char* kt_l = kt_lds[t & 1];
         // padded grid, bit jl: key j0 + jl exists and holds a real token
         uint64_t kmask = 0;
         if constexpr (PAD) {
@@ -219,7 +233,7 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
                 F a;
-                lds_frag<D * E>(a, kt_lds, kt * 32 + (lane & 31), ks * 16 + half * 8);
+                lds_frag_s<D * E>(a, kt_l, kt * 32 + (lane & 31), ks * 16 + half * 8);
                 mma(acc[kt][0], a, qf[0][ks]);
                 mma(acc[kt][1], a, qf[1][ks]);
             }
@@ -286,6 +300,7 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
                 }
             }
         }
+        wg_barrier();                      // buffer t & 1 is free for tile t + 2
     }
     if constexpr (PASS == 1) {
 #pragma unroll
