@@ -149,6 +149,17 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
         settle(kf[ks]);
         settle(vf[ks]);
     }
+    // With 256-byte rows and up, the K, V fragments stay in AGPRs for the
+    // whole walk (the MFMAs read them there; in VGPRs the accumulators would
+    // push them out and every use would copy them back).  Smaller ones fit
+    // in VGPRs next to everything else.
+    if constexpr (RB >= 256) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            pin_agpr(kf[ks]);
+            pin_agpr(vf[ks]);
+        }
+    }
     // Ascending sweep over the query blocks (values hq_local*N + n_q).  With
     // the longest-first order of the key blocks, the workgroups resident
     // together have lists of about the same length and move through the

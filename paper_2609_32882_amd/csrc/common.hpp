@@ -138,6 +138,14 @@ __device__ __forceinline__ void settle(const frag_f32& f) {
     for (int i = 0; i < 8; ++i) asm volatile("" ::"v"(f.v[i]));
 }
 __device__ __forceinline__ void settle(float x) { asm volatile("" ::"v"(x)); }
+// Moves a fragment into accumulation registers (AGPRs) and keeps it there:
+// MFMAs read their A / B operands from AGPRs directly, so a loop-invariant
+// operand parked there costs no VGPRs and no copies.
+__device__ __forceinline__ void pin_agpr(frag_bf16& f) { asm volatile("" : "+a"(f.v)); }
+__device__ __forceinline__ void pin_agpr(frag_f32& f) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) asm volatile("" : "+a"(f.v[i]));
+}
 
 // Exchange with the lane 32 positions away (the other half of the wave).
 __device__ __forceinline__ float swap_half(float x) { return __shfl_xor(x, 32, 64); }
