@@ -209,10 +209,24 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
             // P and dS of elements [i0, i0 + n) of tile t, in place (s <- P,
             // dp <- dS); element i is query 32t + 16(i/8) + 8half + i%8.
             // A group of 8 finished elements becomes a fragment pair.
+            // (LSE, Delta) of the elements of softmax_grad call c (calls
+            // 0..NB-1: tile 0 in groups of EV; NB..NB+NU-1: tile 1 in groups
+            // of EU), read one step ahead into a double buffer
+            constexpr int EMAX = EV > EU ? EV : EU;
+            float2 stv[2][EMAX];
+            auto st_load = [&](int c) {
+                const int t = c < NB ? 0 : 1;
+                const int i0 = c < NB ? c * EV : (c - NB) * EU;
+                const int n = c < NB ? EV : EU;
+#pragma unroll
+                for (int i = i0; i < i0 + n; ++i) stv[c & 1][i - i0] = st[t * 32 + (i >> 3) * 16 + half * 8 + (i & 7)];
+            };
             auto softmax_grad = [&](int t, int i0, int n) {
+                const int c = t == 0 ? i0 / EV : NB + i0 / EU;
+                if (c + 1 < NB + NU) st_load(c + 1);
 #pragma unroll
                 for (int i = i0; i < i0 + n; ++i) {
-                    const float2 sv = st[t * 32 + (i >> 3) * 16 + half * 8 + (i & 7)];
+                    const float2 sv = stv[c & 1][i - i0];
                     const float pv = fast_exp2(s[t][i] * c_log2 - sv.x);
                     s[t][i] = pv;
                     dp[t][i] = pv * (dp[t][i] - sv.y);
@@ -257,6 +271,7 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
                 mma(dp[t], fa[k & 1][1], vf[2 * bi]);
                 mma(s[t], fa[k & 1][2], kf[2 * bi + 1]);
                 mma(dp[t], fa[k & 1][3], vf[2 * bi + 1]);
+                if (k == NB - 1) st_load(0);
                 if (t == 1) softmax_grad(0, bi * EV, EV);
             }
             // dV^T += dO^T P and dK^T += Q^T dS, tile by tile (dO^T and Q^T
