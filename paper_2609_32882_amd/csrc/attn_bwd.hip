@@ -5,7 +5,7 @@
 //   P = exp(S/sqrt(D) - LSE),  dP = dO V^T,  dS = P o (dP - Delta)
 //   dV = P^T dO,  dK = dS^T Q / sqrt(D),  dQ = dS K / sqrt(D)
 // Kernels, all deterministic (no atomics):
-//   stat_kernel      per query token: (LSE * log2(e), Delta)
+//   stat_kernel      per query token: LSE * log2(e) and -Delta
 //   dkdv_kernel      key-block stationary: one workgroup per key block walks
 //                    the transposed (CSC) list of query blocks that selected
 //                    it; a wave owns 32 keys and accumulates dV^T and dK^T
@@ -31,16 +31,23 @@ constexpr int AB_NT = 128;
 constexpr float kLog2e = 1.4426950408889634f;
 
 // ---------------------------------------------------------------------------
-// stat[l] = (LSE_l * log2(e), dO_l . O_l); 16 lanes per token (D <= 128).
-// With the forward's rounding remainder o_lo, O_l = o_l + o_lo_l.  A token
-// without attention mass (LSE = -inf: a padding query, or an empty row)
-// gets +inf, so every probability 2^(s - stat.x) the backward forms for it
-// is 0.
+// Per query token l: LSE_l * log2(e) and -Delta_l = -(dO_l . O_l); 16 lanes
+// per token (D <= 128).  With the forward's rounding remainder o_lo,
+// O_l = o_l + o_lo_l.  A token without attention mass (LSE = -inf: a
+// padding query, or an empty row) gets +inf, so every probability
+// 2^(s - LSE log2 e) the backward forms for it is 0.
+// Layout: per block of 64 tokens, the 64 scaled LSE values, then the 64
+// negated Deltas (stat_at gives the element offsets), so one query block's
+// statistics are one 512-byte copy and a lane's run of 8 consecutive
+// queries is one 32-byte read of each.
 // ---------------------------------------------------------------------------
+__device__ __forceinline__ int64_t stat_lse_at(int64_t tok) { return (tok >> 6) * 128 + (tok & 63); }
+__device__ __forceinline__ int64_t stat_nd_at(int64_t tok) { return (tok >> 6) * 128 + 64 + (tok & 63); }
+
 template <typename T, int D>
 __global__ __launch_bounds__(256) void stat_kernel(const T* __restrict__ o, const T* __restrict__ o_lo,
                                                    const T* __restrict__ dout,
-                                                   const float* __restrict__ lse, float2* __restrict__ stat,
+                                                   const float* __restrict__ lse, float* __restrict__ stat,
                                                    int64_t ntok) {
     constexpr int LPT = D / 8;   // lanes per token, 8 elements each
     const int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -62,7 +69,8 @@ __global__ __launch_bounds__(256) void stat_kernel(const T* __restrict__ o, cons
     for (int off = LPT / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
     if (tok < ntok && part == 0) {
         const float x = lse[tok];
-        stat[tok] = make_float2(x == -INFINITY ? INFINITY : x * kLog2e, s);
+        stat[stat_lse_at(tok)] = x == -INFINITY ? INFINITY : x * kLog2e;
+        stat[stat_nd_at(tok)] = -s;
     }
 }
 
@@ -82,7 +90,7 @@ __global__ __launch_bounds__(256) void stat_kernel(const T* __restrict__ o, cons
 template <typename T, int D, bool COMP, bool PAD>
 __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
-    const T* __restrict__ dout, const float2* __restrict__ stat,
+    const T* __restrict__ dout, const float* __restrict__ stat,
     const int32_t* __restrict__ kv_ptr, const int32_t* __restrict__ kv_idx, int64_t col_cap,
     T* __restrict__ dk, T* __restrict__ dv, int Hq, int Hkv, int N, float c_log2, float scale,
     const int32_t* __restrict__ order, cube_grid grid) {
@@ -95,7 +103,7 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
     using RT = async_tile<64, RB, 2, true, E == 2>;      // Q, dO rows (slot-swapped)
     __shared__ __align__(1024) char q_lds[2][RT::BYTES];
     __shared__ __align__(1024) char o_lds[2][RT::BYTES];
-    __shared__ __align__(1024) float2 st_lds[2][64];
+    __shared__ __align__(1024) float st_lds[2][128];   // 64 scaled LSE, then 64 -Delta
 
     const int tid = threadIdx.x, lane = tid & 63, wave = wave_id(), half = lane >> 5;
     const int64_t krow = work_row(order, xcd_item(blockIdx.x, gridDim.x), gridDim.x);   // (b*Hkv + hkv)*N + nk
@@ -134,14 +142,14 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
         return bh * L + static_cast<int64_t>(ent % N) * 64;
     };
     const RT rt(wave, lane);
-    // Q, dO and (LSE, Delta) of the 64 queries (512 bytes, 16 lanes of each wave)
+    // Q, dO and the statistics of the 64 queries (512 bytes, 16 lanes of each wave)
     auto issue = [&](int64_t q0, int buf) {
         const int64_t o0 = q0 < 0 ? 0 : q0;
         rt.issue(q_lds[buf], reinterpret_cast<const char*>(q + o0 * D), wave);
         rt.issue(o_lds[buf], reinterpret_cast<const char*>(dout + o0 * D), wave);
         if (lane < 16)
             dma16(static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)st_lds[buf])) + wave * 256,
-                  reinterpret_cast<const char*>(stat + o0) + wave * 256, lane * 16);
+                  reinterpret_cast<const char*>(stat + 2 * o0) + wave * 256, lane * 16);
     };
 
 #pragma unroll
@@ -186,7 +194,7 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
         if (has_next) issue(q_next, buf ^ 1);
         const char* qt = q_lds[buf];
         const char* ot = o_lds[buf];
-        const float2* st = st_lds[buf];
+        const float* st = st_lds[buf];
         if (q_cur >= 0) {
             // Software pipeline over the two 32-query tiles of the block:
             //   S/dP(tile 0) | S/dP(tile 1) + P,dS(tile 0) |
@@ -200,20 +208,28 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
             constexpr int NU = 2 * MT;           // dV/dK steps per tile
             constexpr int EV = 16 / NB;          // P,dS elements per S/dP step
             constexpr int EU = 16 / NU;          // P,dS elements per dV/dK step
+            // S starts from 0; dP starts from -Delta of its query (element i
+            // of tile t is query 32t + 16(i/8) + 8half + i%8), so the product
+            // leaves dP - Delta
             f32x16_t s[2], dp[2];
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) { s[t][i] = 0.f; dp[t][i] = 0.f; }
+                for (int i = 0; i < 16; ++i) s[t][i] = 0.f;
+            auto dp_init = [&](int t) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i) dp[t][i] = st[64 + t * 32 + (i >> 3) * 16 + half * 8 + (i & 7)];
+            };
+            dp_init(0);
             F pb[2][2], db[2][2], pl[2][SPLIT ? 2 : 1], dl[2][SPLIT ? 2 : 1];
             // P and dS of elements [i0, i0 + n) of tile t, in place (s <- P,
             // dp <- dS); element i is query 32t + 16(i/8) + 8half + i%8.
             // A group of 8 finished elements becomes a fragment pair.
-            // (LSE, Delta) of the elements of softmax_grad call c (calls
+            // scaled LSE of the elements of softmax_grad call c (calls
             // 0..NB-1: tile 0 in groups of EV; NB..NB+NU-1: tile 1 in groups
             // of EU), read one step ahead into a double buffer
             constexpr int EMAX = EV > EU ? EV : EU;
-            float2 stv[2][EMAX];
+            float stv[2][EMAX];
             auto st_load = [&](int c) {
                 const int t = c < NB ? 0 : 1;
                 const int i0 = c < NB ? c * EV : (c - NB) * EU;
@@ -226,10 +242,9 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
                 if (c + 1 < NB + NU) st_load(c + 1);
 #pragma unroll
                 for (int i = i0; i < i0 + n; ++i) {
-                    const float2 sv = stv[c & 1][i - i0];
-                    const float pv = fast_exp2(s[t][i] * c_log2 - sv.x);
+                    const float pv = fast_exp2(s[t][i] * c_log2 - stv[c & 1][i - i0]);
                     s[t][i] = pv;
-                    dp[t][i] = pv * (dp[t][i] - sv.y);
+                    dp[t][i] = pv * dp[t][i];
                 }
                 if (((i0 + n) & 7) == 0) {
                     const int h = (i0 + n - 1) >> 3;
@@ -266,6 +281,7 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
                 const int t = k / NB, bi = k % NB;
                 if (k + 1 < 2 * NB) fetch_sd(fa[(k + 1) & 1], (k + 1) / NB, (k + 1) % NB);
                 else fetch_dk(ta[0], 0, 0);
+                if (k == NB - 1) dp_init(1);
                 lds_order();
                 mma(s[t], fa[k & 1][0], kf[2 * bi]);
                 mma(dp[t], fa[k & 1][1], vf[2 * bi]);
@@ -327,7 +343,7 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
 template <typename T, int D, bool COMP, bool PAD>
 __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
-    const T* __restrict__ dout, const float2* __restrict__ stat,
+    const T* __restrict__ dout, const float* __restrict__ stat,
     const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx, int64_t col_cap,
     T* __restrict__ dq, int Hq, int Hkv, int N, float c_log2, float scale, int period,
     const int32_t* __restrict__ order, cube_grid grid) {
@@ -374,7 +390,7 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
             }
         }
     }
-    const float2 st = stat[qtok];
+    const float st_lse = stat[stat_lse_at(qtok)], st_nd = stat[stat_nd_at(qtok)];   // LSE log2 e, -Delta
     f32x16_t dqa[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
@@ -392,8 +408,8 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
 
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) { settle(qf[ks]); settle(of[ks]); }   // before the copies start
-    settle(st.x);
-    settle(st.y);
+    settle(st_lse);
+    settle(st_nd);
     const int64_t cnt = e1 - e0;
     const int64_t s0 = sweep_start(col_idx, e0, cnt, blockIdx.x >> 3, period, N);
     auto entry = [&](int64_t j) -> int64_t {
@@ -444,8 +460,8 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
             float ds[16];
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
-                const float p = fast_exp2(s[i] * c_log2 - st.x);
-                ds[i] = p * (dp[i] - st.y);
+                const float p = fast_exp2(s[i] * c_log2 - st_lse);
+                ds[i] = p * (dp[i] + st_nd);
             }
             if constexpr (PAD) {        // branch-free: a branch here costs registers
                 const uint32_t lm = static_cast<uint32_t>(kmask >> (t2 * 32 + half * 8));
@@ -533,7 +549,7 @@ static hipError_t launch_prep_t(const void* o, const float* lse, const void* o_l
     const int64_t sthreads = ntok * (D / 8);
     hipLaunchKernelGGL((stat_kernel<T, D>), dim3(static_cast<unsigned>((sthreads + 255) / 256)), dim3(256), 0,
                        s, static_cast<const T*>(o), static_cast<const T*>(o_lo), static_cast<const T*>(dout),
-                       lse, static_cast<float2*>(ws), ntok);
+                       lse, static_cast<float*>(ws), ntok);
     return hipGetLastError();
 }
 
@@ -553,7 +569,7 @@ static hipError_t launch_dkdv_t(const void* q, const void* k, const void* v, con
     auto go = [&](auto pad) {
         hipLaunchKernelGGL((dkdv_kernel<T, D, COMP, decltype(pad)::value>), dim3(static_cast<unsigned>(krows)),
                            dim3(AB_NT), 0, s, static_cast<const T*>(q), static_cast<const T*>(k),
-                           static_cast<const T*>(v), static_cast<const T*>(dout), static_cast<const float2*>(ws),
+                           static_cast<const T*>(v), static_cast<const T*>(dout), static_cast<const float*>(ws),
                            kv_ptr, kv_idx, col_cap, static_cast<T*>(dk), static_cast<T*>(dv), Hq, Hkv, N, c, scale,
                            order, cg);
     };
@@ -577,7 +593,7 @@ static hipError_t launch_dq_t(const void* q, const void* k, const void* v, const
         constexpr bool P = decltype(pad)::value;
         hipLaunchKernelGGL((dq_kernel<T, D, COMP, P>), dim3(static_cast<unsigned>(qrows)), dim3(AB_NT), 0, s,
                            static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
-                           static_cast<const T*>(dout), static_cast<const float2*>(ws), row_ptr, col_idx, col_cap,
+                           static_cast<const T*>(dout), static_cast<const float*>(ws), row_ptr, col_idx, col_cap,
                            static_cast<T*>(dq), Hq, Hkv, N, c, scale,
                            resident_per_xcd<dq_kernel<T, D, COMP, P>>(AB_NT), order, cg);
     };
