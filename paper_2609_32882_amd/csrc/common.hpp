@@ -510,9 +510,13 @@ __device__ __forceinline__ void lds_frag_tr(frag_bf16& f, const char* tile, int 
     v4i16 r2[2];
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
-        const int k = k0 + 8 * (G >> 1) + 4 * r + (i >> 2);
-        const int row = PERM ? swap_bits_2_3(k) : k;
-        const int grp = cgroup_pos<RB>((m0 >> 4) + (G & 1));
+        // k0 and m0 are multiples of 16 and 32: the slot swap acts on the
+        // lane's part y < 16 of the index only, and column group
+        // m0/16 + G%2 sits at position (G%2) RB/64 + m0/32, so the address
+        // is a per-lane offset plus the constant k0 (RB + 16) + m0
+        const int y = 8 * (G >> 1) + 4 * r + (i >> 2);
+        const int row = k0 + (PERM ? swap_bits_2_3(y) : y);
+        const int grp = (G & 1) * (RB / 64) + (m0 >> 5);
         const char* p = tile + row * (RB + 16) + grp * 32 + 8 * (i & 3);
         r2[r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p));
     }
