@@ -203,9 +203,8 @@ vsa2_status vsa2_route(const vsa2_problem* p, const vsa2_select* s,
 /* Bytes of workspace vsa2_attn_fwd (pass 0: the work order, one int32 per
  * CSR row), vsa2_attn_bwd (pass 1: two fp32 values per query token, its
  * LSE and its Delta, then the work orders of the CSR and CSC rows) or
- * vsa2_coarse_bwd
- * (pass 2: one fp32 pair per coarse query) needs.  The work
- * order lists the rows of each XCD's range longest first (a stable
+ * vsa2_coarse_bwd (pass 2: one fp32 pair per coarse query) needs.  The
+ * work order lists the rows of each XCD's range longest first (a stable
  * counting sort by length class), so the launch's last workgroups are
  * short ones; rows of equal length keep their order. */
 vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* bytes);
