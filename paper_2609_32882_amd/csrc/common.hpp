@@ -147,6 +147,13 @@ __device__ __forceinline__ void pin_agpr(frag_f32& f) {
     for (int i = 0; i < 8; ++i) asm volatile("" : "+a"(f.v[i]));
 }
 
+// A lane's neighbour value by a DPP lane pattern within rows of 16 lanes
+// (CTRL: 0x00-0xFF quad_perm, 0x140 row_mirror, 0x141 row_half_mirror).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+
 // Exchange with the lane 32 positions away (the other half of the wave).
 __device__ __forceinline__ float swap_half(float x) { return __shfl_xor(x, 32, 64); }
 

@@ -146,6 +146,7 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
     using F = typename frag_of<T>::type;
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;
+    static_assert(G == 1 || G == 2 || G == 4 || G == 8, "pooled tokens per cube: 1, 2, 4 or 8");
     using AT = async_tile<64, D * E, RT_NT / 64, true, E == 2>;   // K_r rows (slot-swapped)
     __shared__ __align__(1024) char kt_lds[2][AT::BYTES];           // double buffer
 
@@ -208,8 +209,9 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
         if (has_next) vm_wait<AT::PER_WAVE>(); else vm_wait<0>();   // tile t landed
         wg_barrier();
         const char* kt_l = kt_lds[t & 1];
-        // padded grid, bit jl: key j0 + jl exists and holds a real token
-        uint64_t kmask = 0;
+        // bit jl: key j0 + jl exists (and, on a padded grid, holds a real
+        // token); a tile without a missing key takes the mask-free path
+        uint64_t kmask;
         if constexpr (PAD) {
             const int64_t j = j0 + lane;
             bool ok = j < NG;
@@ -217,12 +219,10 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
                 ok = subcube_real(grid, cube_extent(grid, static_cast<int>(j / G)), static_cast<int>(j % G), Rt, Rh,
                                   Rw);
             kmask = __ballot(ok);
+        } else {
+            const int64_t nv = NG - j0;
+            kmask = nv >= 64 ? ~0ull : ((1ull << nv) - 1);
         }
-        // key j0 + jl takes part
-        auto key_ok = [&](int jl) -> bool {
-            if constexpr (PAD) return (kmask >> jl) & 1;
-            else return j0 + jl < NG;
-        };
         f32x16_t acc[2][2];
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
@@ -238,62 +238,75 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
                 mma(acc[kt][1], a, qf[1][ks]);
             }
         }
-        // key of accumulator entry v in key tile kt: j0 + 32kt + 16(v/8) + 8*half + v%8
-        if constexpr (PASS == 1) {
+        // key of accumulator entry v in key tile kt: j0 + 32kt + 16(v/8) + 8*half + v%8.
+        // Keys that are not there get score -inf, i.e. probability 0 below
+        // (a tile with a missing key is the last one or holds padding).
+        if (kmask != ~0ull) {
 #pragma unroll
-            for (int qt = 0; qt < 2; ++qt) {
-                float mt = -INFINITY;
+            for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-                for (int kt = 0; kt < 2; ++kt)
+                for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
                     for (int v = 0; v < 16; ++v) {
                         const int jl = kt * 32 + (v >> 3) * 16 + half * 8 + (v & 7);
-                        const float t = key_ok(jl) ? acc[kt][qt][v] * c_log2 : -INFINITY;
-                        acc[kt][qt][v] = t;
-                        mt = fmaxf(mt, t);
+                        acc[kt][qt][v] = ((kmask >> jl) & 1) ? acc[kt][qt][v] : -INFINITY;
                     }
-                mt = fmaxf(mt, swap_half(mt));
-                const float mn = fmaxf(m[qt], mt);
-                float s = 0.f;
+        }
+        {
+            if constexpr (PASS == 1) {
 #pragma unroll
-                for (int kt = 0; kt < 2; ++kt)
+                for (int qt = 0; qt < 2; ++qt) {
+                    // the max of the raw scores scales to the max of the
+                    // scaled ones (c > 0, rounding is monotonic)
+                    float mt = -INFINITY;
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) s += fast_exp2(acc[kt][qt][v] - mn);
-                l[qt] = l[qt] * fast_exp2(m[qt] - mn) + s;
-                m[qt] = mn;
-            }
-        } else {
+                    for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-            for (int qt = 0; qt < 2; ++qt) {
-                const int64_t qi = q0 + qt * 32 + (lane & 31);
+                        for (int v = 0; v < 16; ++v) mt = fmaxf(mt, acc[kt][qt][v]);
+                    mt = fmaxf(mt, swap_half(mt)) * c_log2;
+                    const float mn = fmaxf(m[qt], mt);
+                    float s = 0.f;
 #pragma unroll
-                for (int kt = 0; kt < 2; ++kt) {
+                    for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-                    for (int run = 0; run < 2; ++run) {
-                        // this run: keys j0 + 32kt + 16run + 8half + (0..7)
-                        float bs[8 / G];
+                        for (int v = 0; v < 16; ++v) s += fast_exp2(fmaf(acc[kt][qt][v], c_log2, -mn));
+                    l[qt] = l[qt] * fast_exp2(m[qt] - mn) + s;
+                    m[qt] = mn;
+                }
+            } else {
 #pragma unroll
-                        for (int i = 0; i < 8 / G; ++i) {
-                            float s = 0.f;
+                for (int qt = 0; qt < 2; ++qt) {
+                    const int64_t qi = q0 + qt * 32 + (lane & 31);
 #pragma unroll
-                            for (int u = 0; u < G; ++u) {
-                                const int v = run * 8 + i * G + u;
-                                const int jl = kt * 32 + run * 16 + half * 8 + i * G + u;
-                                s += key_ok(jl) ? fast_exp2(acc[kt][qt][v] * c_log2 - lq[qt]) : 0.f;
-                            }
-                            // weighted sum over the G pooled queries of the block (G adjacent lanes)
-                            s *= qw[qt];
+                    for (int kt = 0; kt < 2; ++kt) {
 #pragma unroll
-                            for (int off = 1; off < G; off <<= 1) s += __shfl_xor(s, off, 64);
-                            bs[i] = s;
-                        }
-                        if ((lane % G) == 0 && qi < NG) {
-                            const int64_t nq = qi / G;
+                        for (int run = 0; run < 2; ++run) {
+                            // this run: keys j0 + 32kt + 16run + 8half + (0..7)
+                            float bs[8 / G];
 #pragma unroll
                             for (int i = 0; i < 8 / G; ++i) {
-                                const int64_t j = j0 + kt * 32 + run * 16 + half * 8 + i * G;
-                                if (j < NG)
-                                    scores[(static_cast<int64_t>(bh) * N + nq) * N + j / G] = bs[i];
+                                float s = 0.f;
+#pragma unroll
+                                for (int u = 0; u < G; ++u)
+                                    s += fast_exp2(fmaf(acc[kt][qt][run * 8 + i * G + u], c_log2, -lq[qt]));
+                                // weighted sum over the G pooled queries of the
+                                // block (G adjacent lanes, within a row of 16):
+                                // swap neighbours, then pairs, then the two
+                                // quads of 8 (mirror: lane i meets lane 7 - i)
+                                s *= qw[qt];
+                                if constexpr (G >= 2) s += dpp_f32<0xB1>(s);     // quad_perm [1,0,3,2]
+                                if constexpr (G >= 4) s += dpp_f32<0x4E>(s);     // quad_perm [2,3,0,1]
+                                if constexpr (G >= 8) s += dpp_f32<0x141>(s);    // row_half_mirror
+                                bs[i] = s;
+                            }
+                            if ((lane % G) == 0 && qi < NG) {
+                                const int64_t nq = qi / G;
+#pragma unroll
+                                for (int i = 0; i < 8 / G; ++i) {
+                                    const int64_t j = j0 + kt * 32 + run * 16 + half * 8 + i * G;
+                                    if (j < NG)
+                                        scores[(static_cast<int64_t>(bh) * N + nq) * N + j / G] = bs[i];
+                                }
                             }
                         }
                     }
