@@ -274,40 +274,55 @@ __global__ __launch_bounds__(RT_NT) void route_pass_kernel(
                     m[qt] = mn;
                 }
             } else {
+                // block sums bsv[qt][kt][run][i] of the lane's pooled query over
+                // the G keys j0 + 32kt + 16run + 8half + iG + (0..G-1), weighted,
+                // then summed over the G pooled queries of the block (G adjacent
+                // lanes, within a row of 16): swap neighbours, then pairs, then
+                // the two quads of 8 (mirror: lane i meets lane 7 - i).  All
+                // sums first, so the lane exchanges of different blocks overlap.
+                float bsv[2][2][2][8 / G];
 #pragma unroll
-                for (int qt = 0; qt < 2; ++qt) {
-                    const int64_t qi = q0 + qt * 32 + (lane & 31);
+                for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
-                    for (int kt = 0; kt < 2; ++kt) {
+                    for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-                        for (int run = 0; run < 2; ++run) {
-                            // this run: keys j0 + 32kt + 16run + 8half + (0..7)
-                            float bs[8 / G];
+                        for (int run = 0; run < 2; ++run)
 #pragma unroll
                             for (int i = 0; i < 8 / G; ++i) {
-                                float s = 0.f;
+                                float x = 0.f;
 #pragma unroll
                                 for (int u = 0; u < G; ++u)
-                                    s += fast_exp2(fmaf(acc[kt][qt][run * 8 + i * G + u], c_log2, -lq[qt]));
-                                // weighted sum over the G pooled queries of the
-                                // block (G adjacent lanes, within a row of 16):
-                                // swap neighbours, then pairs, then the two
-                                // quads of 8 (mirror: lane i meets lane 7 - i)
-                                s *= qw[qt];
-                                if constexpr (G >= 2) s += dpp_f32<0xB1>(s);     // quad_perm [1,0,3,2]
-                                if constexpr (G >= 4) s += dpp_f32<0x4E>(s);     // quad_perm [2,3,0,1]
-                                if constexpr (G >= 8) s += dpp_f32<0x141>(s);    // row_half_mirror
-                                bs[i] = s;
+                                    x += fast_exp2(fmaf(acc[kt][qt][run * 8 + i * G + u], c_log2, -lq[qt]));
+                                bsv[qt][kt][run][i] = x * qw[qt];
                             }
-                            if ((lane % G) == 0 && qi < NG) {
-                                const int64_t nq = qi / G;
 #pragma unroll
-                                for (int i = 0; i < 8 / G; ++i) {
-                                    const int64_t j = j0 + kt * 32 + run * 16 + half * 8 + i * G;
-                                    if (j < NG)
-                                        scores[(static_cast<int64_t>(bh) * N + nq) * N + j / G] = bs[i];
-                                }
+                for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+                    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                        for (int run = 0; run < 2; ++run)
+#pragma unroll
+                            for (int i = 0; i < 8 / G; ++i) {
+                                float& x = bsv[qt][kt][run][i];
+                                if constexpr (G >= 2) x += dpp_f32<0xB1>(x);     // quad_perm [1,0,3,2]
+                                if constexpr (G >= 4) x += dpp_f32<0x4E>(x);     // quad_perm [2,3,0,1]
+                                if constexpr (G >= 8) x += dpp_f32<0x141>(x);    // row_half_mirror
                             }
+                if ((lane % G) == 0) {
+#pragma unroll
+                    for (int qt = 0; qt < 2; ++qt) {
+                        const int64_t qi = q0 + qt * 32 + (lane & 31);
+                        if (qi < NG) {
+                            float* srow = scores + (static_cast<int64_t>(bh) * N + qi / G) * N;
+#pragma unroll
+                            for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                                for (int run = 0; run < 2; ++run)
+#pragma unroll
+                                    for (int i = 0; i < 8 / G; ++i) {
+                                        const int64_t j = j0 + kt * 32 + run * 16 + half * 8 + i * G;
+                                        if (j < NG) srow[j / G] = bsv[qt][kt][run][i];
+                                    }
                         }
                     }
                 }
