@@ -405,17 +405,23 @@ __device__ __forceinline__ double wave_sum_d(double x) {
     return x;
 }
 
+// Number of the wave's entries with x > t (STRICT) or x >= t: one ballot
+// per register and a population count, no lane exchanges.
+template <int PER, bool STRICT>
+__device__ __forceinline__ int wave_count(const float (&x)[PER], float t) {
+    int c = 0;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) c += __popcll(__ballot(STRICT ? x[i] > t : x[i] >= t));
+    return c;
+}
+
 // Largest threshold t (as bits) with count(x >= t) >= k: the k-th largest value.
 template <int PER>
 __device__ __forceinline__ uint32_t kth_largest_bits(const float (&x)[PER], int k) {
     uint32_t tau = 0;
     for (int bit = 30; bit >= 0; --bit) {
         const uint32_t cand = tau | (1u << bit);
-        const float cf = __uint_as_float(cand);
-        int c = 0;
-#pragma unroll
-        for (int i = 0; i < PER; ++i) c += x[i] >= cf ? 1 : 0;
-        if (wave_sum_i(c) >= k) tau = cand;
+        if (wave_count<PER, false>(x, __uint_as_float(cand)) >= k) tau = cand;
     }
     return tau;
 }
@@ -473,10 +479,7 @@ __device__ row_rule decide_row(const float (&x)[PER], int N, int mode, int k, fl
     }
     const uint32_t tau = kth_largest_bits<PER>(x, keep);
     const float tf = __uint_as_float(tau);
-    int gt = 0;
-#pragma unroll
-    for (int i = 0; i < PER; ++i) gt += x[i] > tf ? 1 : 0;
-    gt = wave_sum_i(gt);
+    const int gt = wave_count<PER, true>(x, tf);
     r.tau = tf;
     r.need = keep - gt;
     r.count = keep;
