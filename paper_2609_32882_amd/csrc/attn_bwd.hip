@@ -83,7 +83,7 @@ __global__ __launch_bounds__(256) void stat_kernel(const T* __restrict__ o, cons
 //   dV^T += dO^T P,  dK^T += Q^T dS   (dO^T, Q^T read transposed from LDS)
 // The Q / dO / stat tiles are double-buffered: the copies of the next query
 // block stream in during the whole of the current one.  On a padded grid,
-// padding keys get dK = dV = 0 and padding queries (stat.x = +inf) add
+// padding keys get dK = dV = 0 and padding queries (scaled LSE = +inf) add
 // nothing.  (PAD: the grid is padded; the masking is compiled only into
 // that variant.)
 // ---------------------------------------------------------------------------
@@ -222,9 +222,6 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
             };
             dp_init(0);
             F pb[2][2], db[2][2], pl[2][SPLIT ? 2 : 1], dl[2][SPLIT ? 2 : 1];
-            // P and dS of elements [i0, i0 + n) of tile t, in place (s <- P,
-            // dp <- dS); element i is query 32t + 16(i/8) + 8half + i%8.
-            // A group of 8 finished elements becomes a fragment pair.
             // scaled LSE of the elements of softmax_grad call c (calls
             // 0..NB-1: tile 0 in groups of EV; NB..NB+NU-1: tile 1 in groups
             // of EU), read one step ahead into a double buffer
@@ -237,6 +234,9 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
 #pragma unroll
                 for (int i = i0; i < i0 + n; ++i) stv[c & 1][i - i0] = st[t * 32 + (i >> 3) * 16 + half * 8 + (i & 7)];
             };
+            // P and dS of elements [i0, i0 + n) of tile t, in place (s <- P,
+            // dp <- dS); element i is query 32t + 16(i/8) + 8half + i%8.
+            // A group of 8 finished elements becomes a fragment pair.
             auto softmax_grad = [&](int t, int i0, int n) {
                 const int c = t == 0 ? i0 / EV : NB + i0 / EU;
                 if (c + 1 < NB + NU) st_load(c + 1);
