@@ -179,6 +179,8 @@ def main():
     coarse = None if args.no_coarse else time_coarse_branch(vsa2, torch, p, q, k, v, do, o, dq, dk, dv,
                                                             stream, max(args.steps, 3))
 
+    mfma_peak = measure_mfma_peak(vsa2, torch, stream)
+
     if args.calib_copy_mib:
         n = args.calib_copy_mib << 20
         src = torch.empty(n, dtype=torch.uint8, device=dev)
@@ -199,6 +201,12 @@ def main():
     # the four B x B x D products it has to form: S and dP (recomputed), dV, dK.
     flop_dkdv = 8.0 * b2d * nnz
     achieved = flop_dkdv / (stage_ms["bwd_dkdv"] * 1e-3) / 1e12
+    attn_tflops = (flop_fwd + flop_bwd) / (attn_ms * 1e-3) / 1e12
+    sparsity = 1.0 - nnz / float(p.batch * p.heads_q * p.N_joint * p.N_joint)
+    E = 2 if p.dtype == 1 else 4
+    pool_bytes = float(p.batch * (p.heads_q + p.heads_kv) * N * D * E * (B + G))
+    NG = float(N * G)
+    route_flop = 2.0 * 2.0 * D * NG * NG * p.batch * p.heads_q
     out = {
         "metric": "effective sparse-attn TFLOP/s (fwd+bwd FLOPs over whole-path step time), 720p shape",
         "value": round(value, 3),
@@ -219,12 +227,23 @@ def main():
             "cube": [p.Bt, p.Bh, p.Bw], "router_pool": [p.Rt, p.Rh, p.Rw],
             "select": ("top-%d" % sel.k) if sel.mode == 0 else ("mass-%.2f-cap-%d" % (sel.mass, sel.cap)),
             "nnz_block_pairs": nnz,
-            "sparsity": round(1.0 - nnz / float(p.batch * p.heads_q * p.N_joint * p.N_joint), 4),
+            "sparsity": round(sparsity, 4),
         },
         "breakdown_ms": {s: round(stage_ms[s], 4) for s in ("pool", "route", "fwd", "bwd") + stages[3:]},
         "attn_fwd_bwd_ms": round(attn_ms, 4),
-        "attn_only_tflops": round((flop_fwd + flop_bwd) / (attn_ms * 1e-3) / 1e12, 3),
-        "pct_bf16_peak_attn_only": round(100.0 * (flop_fwd + flop_bwd) / (attn_ms * 1e-3) / 1e12 / peak, 2),
+        "attn_only_tflops": round(attn_tflops, 3),
+        "pct_bf16_peak_attn_only": round(100.0 * attn_tflops / peak, 2),
+        # the dense MFMA rate measured on this GPU by the library's probe
+        # (the published peak is the rating's denominator)
+        "mfma_peak_measured_tflops": mfma_peak,
+        "pct_measured_peak_attn_only": round(100.0 * attn_tflops / mfma_peak, 2) if mfma_peak else None,
+        # labelled derived rates: pool bytes (the video tokens of Q and K read
+        # once, the pooled rows written once) over the pool stage; the two
+        # router passes' FLOPs over the whole route stage (selection and the
+        # lists included); the attention rate scaled by the skipped blocks
+        "pool_gbs": round(pool_bytes / (stage_ms["pool"] * 1e-3) / 1e9, 1),
+        "route_pass_tflops_over_route_stage": round(route_flop / (stage_ms["route"] * 1e-3) / 1e12, 1),
+        "dense_equivalent_attn_tflops": round(attn_tflops / max(1.0 - sparsity, 1e-9), 1),
         "roofline": {
             "kernel": "dkdv_kernel (vsa2_attn_bwd_dkdv)",
             "bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
@@ -238,6 +257,27 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, x, a_rp, a_ci, args.cpu_rows, args.cpu_kv)
     print(json.dumps(out), flush=True)
+
+
+def measure_mfma_peak(vsa2, torch, stream, iters=4096, reps=5):
+    """Dense bf16 MFMA rate of this GPU (TFLOP/s, best of `reps` launches of
+    the library's probe), or None where the probe is unavailable."""
+    sink = torch.zeros(1, dtype=torch.float32, device="cuda")
+    sp = stream.cuda_stream
+    st, flops = vsa2.vsa2_mfma_peak_probe(iters, sink.data_ptr(), sp)   # warm-up
+    if st != 0:
+        return None
+    best = 0.0
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        st, flops = vsa2.vsa2_mfma_peak_probe(iters, sink.data_ptr(), sp)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        if st != 0:
+            return None
+        best = max(best, flops / (e0.elapsed_time(e1) * 1e-3) / 1e12)
+    return round(best, 1)
 
 
 def time_coarse_branch(vsa2, torch, p, q, k, v, do, o_f, dq, dk, dv, stream, reps):

@@ -394,6 +394,21 @@ vsa2_status vsa2_joint_lists(const vsa2_problem* p, const int32_t* row_ptr, cons
 vsa2_status vsa2_unpool_add(const vsa2_problem* p, int32_t heads, const void* dx_c, int32_t Pt, int32_t Ph,
                             int32_t Pw, void* dx, hipStream_t stream);
 
+/*
+ * vsa2_mfma_peak_probe - a measurement aid, not part of the attention path:
+ * the dense bf16 MFMA rate this GPU reaches, the measured counterpart of the
+ * published peak the attention kernels are rated against.  Launches one
+ * workgroup of 16 waves per CU; each wave runs `iters` rounds of 4
+ * independent 32x32x16 bf16 MFMA chains on register operands.  The caller
+ * times the launch (events on `stream`) and divides *flops by the time.
+ *   iters  rounds (>= 0; 0 launches nothing and only reports *flops = 0).
+ *   sink   device float, written only in a case no input reaches (it keeps
+ *          the chains alive); may be NULL when iters = 0.
+ *   flops  host int64: the work of the launch, CUs * 16 * 4 * iters * 32768.
+ * Errors: NULL flops (or sink with iters > 0); iters < 0 (VSA2_ERR_SHAPE).
+ */
+vsa2_status vsa2_mfma_peak_probe(int32_t iters, float* sink, int64_t* flops, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -30,7 +30,8 @@ EXPORTS = ("vsa2_status_str", "vsa2_pool", "vsa2_route_capacity", "vsa2_route_wo
            "vsa2_route", "vsa2_attn_workspace", "vsa2_attn_fwd", "vsa2_attn_bwd",
            "vsa2_attn_bwd_prep", "vsa2_attn_bwd_dkdv", "vsa2_attn_bwd_dq",
            "vsa2_coarse_fwd", "vsa2_coarse_bwd", "vsa2_gate_merge", "vsa2_gate_merge_bwd",
-           "vsa2_joint_capacity", "vsa2_joint_workspace", "vsa2_joint_lists", "vsa2_unpool_add")
+           "vsa2_joint_capacity", "vsa2_joint_workspace", "vsa2_joint_lists", "vsa2_unpool_add",
+           "vsa2_mfma_peak_probe")
 
 
 class vsa2_problem(ctypes.Structure):
@@ -83,6 +84,7 @@ def _lib():
         L.vsa2_joint_capacity.argtypes = [pp, ps, ctypes.POINTER(i64)]
         L.vsa2_joint_workspace.argtypes = [pp, ctypes.POINTER(sz)]
         L.vsa2_joint_lists.argtypes = [pp, P, P, i64, P, P, i64, P, P, P, sz, P]
+        L.vsa2_mfma_peak_probe.argtypes = [i32, P, ctypes.POINTER(i64), P]
         for n in EXPORTS[1:]:
             getattr(L, n).restype = ctypes.c_int
         _L = L
@@ -184,6 +186,13 @@ def vsa2_gate_merge_bwd(p, gate, o_c, dout, do_c, dgate, stream=0):
 
 def vsa2_unpool_add(p, heads, dx_c, Pt, Ph, Pw, dx, stream=0):
     return _lib().vsa2_unpool_add(_ref(p), heads, dx_c, Pt, Ph, Pw, dx, stream)
+
+
+def vsa2_mfma_peak_probe(iters, sink, stream=0):
+    """Launch the dense MFMA rate probe; returns (status, flops of the launch)."""
+    f = ctypes.c_int64(0)
+    st = _lib().vsa2_mfma_peak_probe(iters, sink, ctypes.byref(f), stream)
+    return st, f.value
 
 
 def vsa2_joint_capacity(p, s):

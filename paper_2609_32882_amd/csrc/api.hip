@@ -465,4 +465,11 @@ vsa2_status vsa2_unpool_add(const vsa2_problem* p, int32_t heads, const void* dx
     return VSA2_OK;
 }
 
+vsa2_status vsa2_mfma_peak_probe(int32_t iters, float* sink, int64_t* flops, hipStream_t stream) {
+    if (!flops || (iters > 0 && !sink)) return VSA2_ERR_NULL;
+    if (iters < 0) return VSA2_ERR_SHAPE;
+    VSA2_TRY_HIP(vsa2::launch_mfma_peak(iters, sink, flops, stream));
+    return VSA2_OK;
+}
+
 }  // extern "C"

@@ -214,3 +214,14 @@ def test_product_path_has_no_oracle_or_fallback():
             if f.endswith((".py", ".hip", ".hpp", ".h", ".cpp")):
                 src = open(os.path.join(dirpath, f)).read()
                 assert "oracle" not in src.replace("oracle-free", ""), f
+
+
+def test_mfma_peak_probe_checks():
+    """The dense MFMA rate probe rejects a missing flops output, a missing
+    sink when it would launch, and a negative round count, before any device
+    work."""
+    st, _ = vsa2.vsa2_mfma_peak_probe(-1, FAKE)
+    assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_SHAPE"
+    st, _ = vsa2.vsa2_mfma_peak_probe(8, None)
+    assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_NULL"
+    assert vsa2.STATUS_NAMES[vsa2.lib().vsa2_mfma_peak_probe(8, FAKE, None, None)] == "VSA2_ERR_NULL"
