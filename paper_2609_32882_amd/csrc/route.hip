@@ -22,7 +22,9 @@ namespace vsa2 {
 // sequence of Lj tokens: the N*B video tokens, then any text tokens): all
 // Pt*Ph*Pw of them unless the grid is padded, where the real tokens of a
 // sub-cube form a box and an all-padding sub-cube pools to 0.
-template <typename T>
+// FP = 2: sub-cubes of 2 x 2 x 2 tokens (the router's pool), the eight
+// loads unrolled and issued together; FP = 0: any sub-cube (runtime loops).
+template <typename T, int FP>
 __global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ x, T* __restrict__ out,
                                                    int64_t nthreads, int N, int64_t Lj, int D, int G, int Gh,
                                                    int Gw, int Pt, int Ph, int Pw, int B, cube_grid grid) {
@@ -47,27 +49,48 @@ __global__ __launch_bounds__(256) void pool_kernel(const T* __restrict__ x, T* _
     double acc[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[i] = 0.0;
-    for (int rt = 0; rt < et; ++rt)
-        for (int rh = 0; rh < eh; ++rh)
-            for (int rw = 0; rw < ew; ++rw) {
-                const int beta = ((gt * Pt + rt) * Bh + gh * Ph + rh) * Bw + gw * Pw + rw;
-                const T* src = xc + beta * D + ch * 8;
-                if constexpr (sizeof(T) == 2) {
-                    const uint4 w = *reinterpret_cast<const uint4*>(src);
-                    const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+    // adds token (rt, rh, rw) of the sub-cube when `in` (else reads it and
+    // leaves the sums as they are: its contents never reach them)
+    auto add_token = [&](int rt, int rh, int rw, bool in) {
+        const int beta = ((gt * Pt + rt) * Bh + gh * Ph + rh) * Bw + gw * Pw + rw;
+        const T* src = xc + beta * D + ch * 8;
+        double f[8];
+        if constexpr (sizeof(T) == 2) {
+            const uint4 wv = *reinterpret_cast<const uint4*>(src);
+            const uint32_t u[4] = {wv.x, wv.y, wv.z, wv.w};
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        acc[2 * i] += static_cast<double>(bf16_to_f32(u[i] & 0xffffu));
-                        acc[2 * i + 1] += static_cast<double>(bf16_to_f32(u[i] >> 16));
-                    }
-                } else {
-                    const float4 a = reinterpret_cast<const float4*>(src)[0];
-                    const float4 b = reinterpret_cast<const float4*>(src)[1];
-                    const float f[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-#pragma unroll
-                    for (int i = 0; i < 8; ++i) acc[i] += static_cast<double>(f[i]);
-                }
+            for (int i = 0; i < 4; ++i) {
+                f[2 * i] = static_cast<double>(bf16_to_f32(u[i] & 0xffffu));
+                f[2 * i + 1] = static_cast<double>(bf16_to_f32(u[i] >> 16));
             }
+        } else {
+            const float4 a = reinterpret_cast<const float4*>(src)[0];
+            const float4 b = reinterpret_cast<const float4*>(src)[1];
+            const float g[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+            for (int i = 0; i < 8; ++i) f[i] = static_cast<double>(g[i]);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] = in ? acc[i] + f[i] : acc[i];
+    };
+    if constexpr (FP > 0) {
+        // fixed bounds, no branch: for a token outside the real part of a
+        // cut sub-cube the sub-cube's first token is read (it exists in
+        // memory) and not added, so the eight loads issue together
+#pragma unroll
+        for (int rt = 0; rt < FP; ++rt)
+#pragma unroll
+            for (int rh = 0; rh < FP; ++rh)
+#pragma unroll
+                for (int rw = 0; rw < FP; ++rw) {
+                    const bool in = rt < et && rh < eh && rw < ew;
+                    add_token(in ? rt : 0, in ? rh : 0, in ? rw : 0, in);
+                }
+    } else {
+        for (int rt = 0; rt < et; ++rt)
+            for (int rh = 0; rh < eh; ++rh)
+                for (int rw = 0; rw < ew; ++rw) add_token(rt, rh, rw, true);
+    }
     const int cnt = et * eh * ew;
     const double P = static_cast<double>(cnt > 0 ? cnt : 1);
     T* dst = out + orow * D + ch * 8;
@@ -95,14 +118,18 @@ hipError_t launch_pool(int dtype, const void* x, void* out, int64_t nbh, int N, 
     if (nthreads == 0) return hipSuccess;
     const int64_t blocks = (nthreads + 255) / 256;
     const int B = Bt * Bh * Bw;
-    if (dtype == 1)
-        hipLaunchKernelGGL(pool_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s,
-                           static_cast<const bf16_t*>(x), static_cast<bf16_t*>(out), nthreads, N, Lj, D, G,
-                           Gh, Gw, Pt, Ph, Pw, B, grid);
-    else
-        hipLaunchKernelGGL(pool_kernel<float>, dim3(blocks), dim3(256), 0, s,
-                           static_cast<const float*>(x), static_cast<float*>(out), nthreads, N, Lj, D, G,
-                           Gh, Gw, Pt, Ph, Pw, B, grid);
+    auto go = [&](auto elem, auto fixed) {
+        using E = decltype(elem);
+        hipLaunchKernelGGL((pool_kernel<E, decltype(fixed)::value>), dim3(blocks), dim3(256), 0, s,
+                           static_cast<const E*>(x), static_cast<E*>(out), nthreads, N, Lj, D, G, Gh, Gw, Pt, Ph,
+                           Pw, B, grid);
+    };
+    const bool two = Pt == 2 && Ph == 2 && Pw == 2;
+    if (dtype == 1) {
+        if (two) go(bf16_t{}, std::integral_constant<int, 2>{}); else go(bf16_t{}, std::integral_constant<int, 0>{});
+    } else {
+        if (two) go(0.f, std::integral_constant<int, 2>{}); else go(0.f, std::integral_constant<int, 0>{});
+    }
     return hipGetLastError();
 }
 
