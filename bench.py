@@ -53,9 +53,9 @@ def parse():
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py: this build runs the routed sparse-attention path on one GPU only; "
-              "--gpus %d is not supported (the path shards over heads with no exchange; "
-              "see the design notes)" % args.gpus, file=sys.stderr)
+        print("bench.py: the routed sparse-attention path runs on one GPU; --gpus %d is not "
+              "supported (across GPUs the path would shard over heads with no exchange)" % args.gpus,
+              file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -17,7 +17,7 @@
  *     (Sec. 2.2 "Permutation"): token l = n*B + beta, n = (nt*Nh + nh)*Nw + nw,
  *     beta = (bt*Bh + bh)*Bw + bw (raster order, w fastest, at every level).
  *
- * Readings of points the paper leaves open (the design notes list them all):
+ * Readings of points the paper leaves open:
  *   - pooled router inputs Q_r, K_r are rounded to the input dtype (RNE);
  *   - router softmax runs over all N*G pooled keys with scale 1/sqrt(D);
  *   - MeanPool_{GxG} is a true mean, so every P_r row sums to 1/G;
