@@ -437,9 +437,11 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
             // S^T = K Q^T, dP^T = V dO^T: 32 keys x this lane's query; K and V
             // fragments requested one k-step pair ahead of their products
             const int row = t2 * 32 + (lane & 31);
+            // dP^T starts at -Delta (this lane's query), so the products
+            // accumulate dP - Delta directly
             f32x16_t s, dp;
 #pragma unroll
-            for (int i = 0; i < 16; ++i) { s[i] = 0.f; dp[i] = 0.f; }
+            for (int i = 0; i < 16; ++i) { s[i] = 0.f; dp[i] = st_nd; }
             F fa[2][4];
             auto fetch = [&](F* f, int bi) {
                 lds_frag_s<RB>(f[0], k_lds, row, 32 * bi + half * 8);
@@ -461,7 +463,7 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
                 const float p = fast_exp2(s[i] * c_log2 - st_lse);
-                ds[i] = p * (dp[i] + st_nd);
+                ds[i] = p * dp[i];
             }
             if constexpr (PAD) {        // branch-free: a branch here costs registers
                 const uint32_t lm = static_cast<uint32_t>(kmask >> (t2 * 32 + half * 8));
