@@ -208,7 +208,7 @@ def main():
     NG = float(N * G)
     route_flop = 2.0 * 2.0 * D * NG * NG * p.batch * p.heads_q
     out = {
-        "metric": "effective sparse-attn TFLOP/s (fwd+bwd FLOPs over whole-path step time), 720p shape",
+        "metric": "effective sparse-attn TFLOP/s (fwd+bwd FLOPs over whole-path step time), %s shape" % w.name,
         "value": round(value, 3),
         "unit": "TFLOP/s",
         "n_gpus": 1,

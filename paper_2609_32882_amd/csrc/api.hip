@@ -102,7 +102,7 @@ route_ws route_layout(const vsa2_problem* p, const shape& s, const vsa2_select* 
     return w;
 }
 
-// the forward needs no scratch memory
+// the forward's workspace holds its work order (one int32 per query-block row)
 size_t fwd_ws_bytes(const shape& s, const vsa2_problem* p) {
     return vsa2::fwd_workspace_bytes(p->batch, p->heads_q, static_cast<int>(s.Nj));
 }

@@ -521,7 +521,7 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
         }
 }
 
-// Workspace of the backward call: per query token (LSE * log2(e), Delta),
+// Workspace of the backward call: per query token LSE * log2(e) and -Delta,
 // then the work orders of the CSR rows (dQ) and of the CSC rows (dK/dV).
 static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
@@ -543,7 +543,7 @@ size_t bwd_workspace_bytes(int dtype, int D, int batch, int Hq, int Hkv, int N) 
     return bwd_ws_csc_order_offset(batch, Hq, N) + align256(4 * static_cast<size_t>(batch) * Hkv * N);
 }
 
-// Stage 1: per query token (LSE * log2(e), Delta) into ws.
+// Stage 1: per query token LSE * log2(e) and -Delta into ws.
 template <typename T, int D>
 static hipError_t launch_prep_t(const void* o, const float* lse, const void* o_lo, const void* dout, void* ws,
                                 int64_t ntok, hipStream_t s) {
