@@ -7,8 +7,9 @@ lower-case helpers below them take torch tensors, check dtypes/shapes,
 allocate outputs and workspaces with torch (device memory only) and call the
 C-ABI on torch's current stream.
 
-The library must have been built (paper_2609_32882_amd/build.py); importing
-this package on a machine without it raises, there is no fallback.
+The library must have been built (paper_2609_32882_amd/build.py): the first
+call into it loads libvsa2.so and raises ImportError when it is missing;
+there is no fallback.
 """
 from __future__ import annotations
 

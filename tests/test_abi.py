@@ -4,6 +4,8 @@ before touching the device (no compute call runs here)."""
 import ctypes
 import os
 import re
+import subprocess
+import sys
 
 import pytest
 
@@ -225,3 +227,20 @@ def test_mfma_peak_probe_checks():
     st, _ = vsa2.vsa2_mfma_peak_probe(8, None)
     assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_NULL"
     assert vsa2.STATUS_NAMES[vsa2.lib().vsa2_mfma_peak_probe(8, FAKE, None, None)] == "VSA2_ERR_NULL"
+
+
+def test_missing_library_fails_loudly():
+    """Without libvsa2.so the first call raises ImportError: there is no
+    silent CPU path to fall back on."""
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "import paper_2609_32882_amd as v\n"
+            "v.LIB_PATH = '/nonexistent/libvsa2.so'\n"
+            "try:\n"
+            "    v.lib()\n"
+            "except ImportError as e:\n"
+            "    print('raised', e)\n"
+            "else:\n"
+            "    print('loaded')\n") % ROOT
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=120)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.startswith("raised") and "not built" in out.stdout
