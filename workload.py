@@ -152,7 +152,7 @@ WORKLOADS = {
         "tiny", Problem(1, 2, 2, 64, 8, 16, 16, dtype=F32), Selection(0, 8), 1000,
         backward=False),
     "480p": Workload(
-        "480p", Problem(1, 12, 12, 128, 20, 32, 56), Selection(0, 70), 1001, backward=False),
+        "480p", Problem(1, 12, 12, 128, 20, 32, 56), Selection(0, 70), 1001),
     "720p": Workload(
         "720p", Problem(1, 40, 40, 128, 20, 48, 80), Selection(0, 120), 1002),
     "720p-mass": Workload(
