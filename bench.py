@@ -112,11 +112,9 @@ def main():
     fws_t = torch.empty(max(fws, 1), dtype=torch.uint8, device=dev)
     bws_t = torch.empty(max(bws, 1), dtype=torch.uint8, device=dev)
     o = torch.empty_like(q)
-    # large-norm cube means (the skewed workload): the compensated products,
-    # the path whose parity is tested on such inputs; the plain path otherwise
-    comp = bool(w.skewed)
-    o_lo = torch.empty_like(q) if comp else None
-    o_lo_ptr = o_lo.data_ptr() if comp else None
+    # a training step: the forward keeps O's rounding remainder for Delta
+    o_lo = torch.empty_like(q)
+    o_lo_ptr = o_lo.data_ptr()
     lse = torch.empty((p.batch, p.heads_q, L), dtype=torch.float32, device=dev)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     stream = torch.cuda.current_stream()
@@ -155,15 +153,16 @@ def main():
                                       a_ci.data_ptr(), a_cap, o.data_ptr(), lse.data_ptr(), o_lo_ptr,
                                       fws_t.data_ptr(), fws, sp))
         mark(3)
-        chk("bwd_prep", vsa2.vsa2_attn_bwd_prep(P, o.data_ptr(), lse.data_ptr(), o_lo_ptr, do.data_ptr(),
-                                                bws_t.data_ptr(), bws, sp))
+        chk("bwd_prep", vsa2.vsa2_attn_bwd_prep(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                                lse.data_ptr(), o_lo_ptr, do.data_ptr(), bws_t.data_ptr(), bws,
+                                                sp))
         mark(4)
         chk("bwd_dkdv", vsa2.vsa2_attn_bwd_dkdv(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(),
-                                                a_kp.data_ptr(), a_ki.data_ptr(), a_cap, int(comp), dk.data_ptr(),
+                                                a_kp.data_ptr(), a_ki.data_ptr(), a_cap, dk.data_ptr(),
                                                 dv.data_ptr(), bws_t.data_ptr(), bws, sp))
         mark(5)
         chk("bwd_dq", vsa2.vsa2_attn_bwd_dq(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), do.data_ptr(),
-                                            a_rp.data_ptr(), a_ci.data_ptr(), a_cap, int(comp), dq.data_ptr(),
+                                            a_rp.data_ptr(), a_ci.data_ptr(), a_cap, dq.data_ptr(),
                                             bws_t.data_ptr(), bws, sp))
         mark(6)
         if record:
@@ -232,7 +231,7 @@ def main():
             "cube": [p.Bt, p.Bh, p.Bw], "router_pool": [p.Rt, p.Rh, p.Rw],
             "select": ("top-%d" % sel.k) if sel.mode == 0 else ("mass-%.2f-cap-%d" % (sel.mass, sel.cap)),
             "nnz_block_pairs": nnz,
-            "products": "compensated (P and dS as two bf16 terms)" if comp else "plain bf16",
+            "products": "bf16; two-term P and dS on block pairs touching a block with a value above 8",
             "sparsity": round(sparsity, 4),
         },
         "breakdown_ms": {s: round(stage_ms[s], 4) for s in ("pool", "route", "fwd", "bwd") + stages[3:]},

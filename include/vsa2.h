@@ -201,8 +201,9 @@ vsa2_status vsa2_route(const vsa2_problem* p, const vsa2_select* s,
                        float* block_scores, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Bytes of workspace vsa2_attn_fwd (pass 0: the work order, one int32 per
- * CSR row), vsa2_attn_bwd (pass 1: two fp32 values per query token, its
- * LSE and its Delta, then the work orders of the CSR and CSC rows) or
+ * CSR row, and one byte per query and key block for the large-magnitude
+ * flags), vsa2_attn_bwd (pass 1: two fp32 values per query token, its LSE
+ * and its Delta, the work orders of the CSR and CSC rows and the flags) or
  * vsa2_coarse_bwd (pass 2: one fp32 pair per coarse query) needs.  The
  * work order lists the rows of each XCD's range longest first (a stable
  * counting sort by length class), so the launch's last workgroups are
@@ -224,12 +225,20 @@ vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* byt
  *   o   [batch][Hq][L][D] output, dtype p->dtype.
  *   lse [batch][Hq][L] fp32 natural-log log-sum-exp of each query's scaled
  *       scores; a query block with no selected block gets o = 0, lse = -inf.
- *   o_lo  optional [batch][Hq][L][D] (dtype p->dtype), NULL for the plain
- *       path.  When given, the call runs compensated: P enters the P.V
- *       product as two bf16 terms (about 16 significant bits instead of 8)
- *       and o_lo receives the rounding remainder of O (o + o_lo ~ the fp32
- *       accumulator).  Pass it to vsa2_attn_bwd to get gradients whose error
- *       does not grow with the magnitude of the keys' common component.
+ *   o_lo  optional [batch][Hq][L][D] (dtype p->dtype): NULL for a forward
+ *       that no backward follows (inference).  When given, the call writes
+ *       the rounding remainder of O (o + o_lo ~ the fp32 result, about 16
+ *       significant bits), which vsa2_attn_bwd needs for Delta, and on block
+ *       pairs that touch a large-magnitude block (below) P enters the P.V
+ *       product as two bf16 terms, so O itself carries about 16 bits there.
+ *   Large-magnitude blocks (bf16 problems): a 64-token block of Q, or of K
+ *       and V together, holding a real-token value above 8 in magnitude.
+ *       bf16 products round P and dS to 8 significant bits; when the tokens
+ *       of a block share a large common component those rounding errors add
+ *       up along it instead of cancelling, so block pairs that touch such a
+ *       block take two-term (hi + lo) operands and all other pairs one-term
+ *       operands.  The flags are computed on the device in each call that
+ *       uses them (no host synchronisation).
  *   ws, ws_bytes  workspace of vsa2_attn_workspace(p, 0) bytes, 256-byte
  *       aligned.
  * Errors: NULL pointers, shape/dtype, misalignment, small workspace.
@@ -249,13 +258,14 @@ vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, c
  * where the sums over l run over every query (of every query head of the KV
  * group) whose block selected j's block.
  *   q, k, v, o, lse   as for vsa2_attn_fwd (o, lse from the forward call)
- *   o_lo  NULL, or the forward's o_lo: then Delta uses o + o_lo and dS enters
- *         the dQ and dK products as two bf16 terms (compensated path)
+ *   o_lo  required: the forward's o_lo (Delta uses o + o_lo).  On block
+ *         pairs that touch a large-magnitude block (see vsa2_attn_fwd) P and
+ *         dS enter the dV, dK and dQ products as two bf16 terms.
  *   dout  [batch][Hq][L][D]  dO
  *   row_ptr, col_idx  the CSR; kv_ptr, kv_idx its transpose (vsa2_route)
  *   dq [batch][Hq][L][D], dk, dv [batch][Hkv][L][D]  outputs, dtype p->dtype;
  *   key blocks no query selected get dk = dv = 0.
- * Errors: as for vsa2_attn_fwd.
+ * Errors: as for vsa2_attn_fwd; o_lo NULL is VSA2_ERR_NULL.
  */
 vsa2_status vsa2_attn_bwd(const vsa2_problem* p, const void* q, const void* k, const void* v,
                           const void* o, const float* lse, const void* o_lo, const void* dout,
@@ -271,34 +281,33 @@ vsa2_status vsa2_attn_bwd(const vsa2_problem* p, const void* q, const void* k, c
  * bytes), which must not be reused in between.
  *
  * vsa2_attn_bwd_prep - per query token l: LSE_l and Delta_l = dO_l . O_l
- *   (with o_lo given, O_l = o_l + o_lo_l), stored in ws.
- *   o, lse, o_lo, dout  as for vsa2_attn_bwd.
+ *   with O_l = o_l + o_lo_l, and (bf16) the large-magnitude flags of the
+ *   blocks of q, k, v, stored in ws.
+ *   q, k, v, o, lse, o_lo, dout  as for vsa2_attn_bwd (o_lo required).
  */
-vsa2_status vsa2_attn_bwd_prep(const vsa2_problem* p, const void* o, const float* lse, const void* o_lo,
-                               const void* dout, void* ws, size_t ws_bytes, hipStream_t stream);
+vsa2_status vsa2_attn_bwd_prep(const vsa2_problem* p, const void* q, const void* k, const void* v, const void* o,
+                               const float* lse, const void* o_lo, const void* dout, void* ws, size_t ws_bytes,
+                               hipStream_t stream);
 
 /*
  * vsa2_attn_bwd_dkdv - dK and dV of vsa2_attn_bwd, one key block at a time
  *   over the query blocks of its transposed list (kv_ptr, kv_idx).
- *   compensated  nonzero: dS and P enter the products as two bf16 terms (use
- *                with a prep stage that was given o_lo).
  *   ws           as written by vsa2_attn_bwd_prep (this stage also writes
  *                its work order there).
  *   dk, dv       [batch][Hkv][L][D] outputs, dtype p->dtype.
  */
 vsa2_status vsa2_attn_bwd_dkdv(const vsa2_problem* p, const void* q, const void* k, const void* v,
                                const void* dout, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
-                               int32_t compensated, void* dk, void* dv, void* ws, size_t ws_bytes,
-                               hipStream_t stream);
+                               void* dk, void* dv, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * vsa2_attn_bwd_dq - dQ of vsa2_attn_bwd, one query block at a time over its
- *   CSR row (row_ptr, col_idx).  compensated, ws as for vsa2_attn_bwd_dkdv.
+ *   CSR row (row_ptr, col_idx).  ws as for vsa2_attn_bwd_dkdv.
  *   dq  [batch][Hq][L][D] output, dtype p->dtype.
  */
 vsa2_status vsa2_attn_bwd_dq(const vsa2_problem* p, const void* q, const void* k, const void* v,
                              const void* dout, const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
-                             int32_t compensated, void* dq, void* ws, size_t ws_bytes, hipStream_t stream);
+                             void* dq, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Coarse branch and gated merge (Sec. 2.2, "Coarse Branch" and "Gated

@@ -74,9 +74,9 @@ def _lib():
         L.vsa2_attn_workspace.argtypes = [pp, i32, ctypes.POINTER(sz)]
         L.vsa2_attn_fwd.argtypes = [pp, P, P, P, P, P, i64, P, P, P, P, sz, P]
         L.vsa2_attn_bwd.argtypes = [pp, P, P, P, P, P, P, P, P, P, P, P, i64, P, P, P, P, sz, P]
-        L.vsa2_attn_bwd_prep.argtypes = [pp, P, P, P, P, P, sz, P]
-        L.vsa2_attn_bwd_dkdv.argtypes = [pp, P, P, P, P, P, P, i64, i32, P, P, P, sz, P]
-        L.vsa2_attn_bwd_dq.argtypes = [pp, P, P, P, P, P, P, i64, i32, P, P, sz, P]
+        L.vsa2_attn_bwd_prep.argtypes = [pp, P, P, P, P, P, P, P, P, sz, P]
+        L.vsa2_attn_bwd_dkdv.argtypes = [pp, P, P, P, P, P, P, i64, P, P, P, sz, P]
+        L.vsa2_attn_bwd_dq.argtypes = [pp, P, P, P, P, P, P, i64, P, P, sz, P]
         L.vsa2_coarse_fwd.argtypes = [pp, P, P, P, P, P, P]
         L.vsa2_coarse_bwd.argtypes = [pp, P, P, P, P, P, P, P, P, sz, P]
         L.vsa2_gate_merge.argtypes = [pp, P, P, P, P, P]
@@ -153,20 +153,18 @@ def vsa2_attn_bwd(p, q, k, v, o, lse, o_lo, dout, row_ptr, col_idx, kv_ptr, kv_i
                                 kv_idx, col_cap, dq, dk, dv, ws, ws_bytes, stream)
 
 
-def vsa2_attn_bwd_prep(p, o, lse, o_lo, dout, ws, ws_bytes, stream=0):
-    return _lib().vsa2_attn_bwd_prep(_ref(p), o, lse, o_lo, dout, ws, ws_bytes, stream)
+def vsa2_attn_bwd_prep(p, q, k, v, o, lse, o_lo, dout, ws, ws_bytes, stream=0):
+    return _lib().vsa2_attn_bwd_prep(_ref(p), q, k, v, o, lse, o_lo, dout, ws, ws_bytes, stream)
 
 
-def vsa2_attn_bwd_dkdv(p, q, k, v, dout, kv_ptr, kv_idx, col_cap, compensated, dk, dv, ws, ws_bytes,
-                       stream=0):
-    return _lib().vsa2_attn_bwd_dkdv(_ref(p), q, k, v, dout, kv_ptr, kv_idx, col_cap,
-                                     int(compensated), dk, dv, ws, ws_bytes, stream)
+def vsa2_attn_bwd_dkdv(p, q, k, v, dout, kv_ptr, kv_idx, col_cap, dk, dv, ws, ws_bytes, stream=0):
+    return _lib().vsa2_attn_bwd_dkdv(_ref(p), q, k, v, dout, kv_ptr, kv_idx, col_cap, dk, dv, ws,
+                                     ws_bytes, stream)
 
 
-def vsa2_attn_bwd_dq(p, q, k, v, dout, row_ptr, col_idx, col_cap, compensated, dq, ws, ws_bytes,
-                     stream=0):
-    return _lib().vsa2_attn_bwd_dq(_ref(p), q, k, v, dout, row_ptr, col_idx, col_cap,
-                                   int(compensated), dq, ws, ws_bytes, stream)
+def vsa2_attn_bwd_dq(p, q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws, ws_bytes, stream=0):
+    return _lib().vsa2_attn_bwd_dq(_ref(p), q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws,
+                                   ws_bytes, stream)
 
 
 def vsa2_coarse_fwd(p, q_c, k_c, v_c, o_c, lse_c, stream=0):
@@ -322,10 +320,12 @@ def route(p, s, q_r, k_r, with_csc=True, with_scores=False):
                 col_cap=cap, ws=ws)
 
 
-def attn_fwd(p, q, k, v, row_ptr, col_idx, col_cap=None, o=None, lse=None, compensated=False,
+def attn_fwd(p, q, k, v, row_ptr, col_idx, col_cap=None, o=None, lse=None, training=False,
              o_lo=None):
-    """Returns (o, lse), or (o, lse, o_lo) when compensated.  With text
-    tokens the tensors are joint sequences and the lists joint lists."""
+    """Returns (o, lse); with training=True (or an o_lo buffer given) also
+    o_lo, the rounding remainder of O that attn_bwd needs: (o, lse, o_lo).
+    With text tokens the tensors are joint sequences and the lists joint
+    lists."""
     torch = _torch()
     p = problem_from(p)
     L = _joint(p)[1]
@@ -341,19 +341,20 @@ def attn_fwd(p, q, k, v, row_ptr, col_idx, col_cap=None, o=None, lse=None, compe
     st, wsb = vsa2_attn_workspace(p, 0)
     _check("vsa2_attn_workspace", st)
     ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
-    if compensated and o_lo is None:
+    keep = training or o_lo is not None
+    if keep and o_lo is None:
         o_lo = torch.empty_like(q)
     _check("vsa2_attn_fwd", vsa2_attn_fwd(p, q.data_ptr(), k.data_ptr(), v.data_ptr(),
                                           row_ptr.data_ptr(), col_idx.data_ptr(), cap,
-                                          o.data_ptr(), lse.data_ptr(),
-                                          o_lo.data_ptr() if compensated else None,
+                                          o.data_ptr(), lse.data_ptr(), _ptr(o_lo),
                                           ws.data_ptr(), wsb, _stream()))
-    return (o, lse, o_lo) if compensated else (o, lse)
+    return (o, lse, o_lo) if keep else (o, lse)
 
 
 def attn_bwd(p, q, k, v, o, lse, do, row_ptr, col_idx, kv_ptr, kv_idx, col_cap=None,
              dq=None, dk=None, dv=None, o_lo=None):
-    """dQ, dK, dV; pass the forward's o_lo for the compensated path."""
+    """dQ, dK, dV.  o_lo is the forward's remainder (attn_fwd(..., training=True));
+    the library requires it (without it the call fails with VSA2_ERR_NULL)."""
     torch = _torch()
     p = problem_from(p)
     L = _joint(p)[1]
@@ -362,6 +363,8 @@ def attn_bwd(p, q, k, v, o, lse, do, row_ptr, col_idx, kv_ptr, kv_idx, col_cap=N
                       (o, p.heads_q, "o"), (do, p.heads_q, "do")):
         _expect(t, (p.batch, hh, L, p.head_dim), dt, nm)
     _expect(lse, (p.batch, p.heads_q, L), torch.float32, "lse")
+    if o_lo is not None:
+        _expect(o_lo, (p.batch, p.heads_q, L, p.head_dim), dt, "o_lo")
     dq = torch.empty_like(q) if dq is None else dq
     dk = torch.empty_like(k) if dk is None else dk
     dv = torch.empty_like(v) if dv is None else dv
@@ -391,23 +394,23 @@ def attn_bwd_staged(p, q, k, v, o, lse, do, row_ptr, col_idx, kv_ptr, kv_idx, co
     st, wsb = vsa2_attn_workspace(p, 1)
     _check("vsa2_attn_workspace", st)
     ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
-    comp = o_lo is not None
     s = _stream()
     if marks:
         marks[0].record()
-    _check("vsa2_attn_bwd_prep", vsa2_attn_bwd_prep(p, o.data_ptr(), lse.data_ptr(), _ptr(o_lo),
+    _check("vsa2_attn_bwd_prep", vsa2_attn_bwd_prep(p, q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                                    o.data_ptr(), lse.data_ptr(), _ptr(o_lo),
                                                     do.data_ptr(), ws.data_ptr(), wsb, s))
     if marks:
         marks[1].record()
     _check("vsa2_attn_bwd_dkdv", vsa2_attn_bwd_dkdv(p, q.data_ptr(), k.data_ptr(), v.data_ptr(),
                                                     do.data_ptr(), kv_ptr.data_ptr(),
-                                                    kv_idx.data_ptr(), cap, comp, dk.data_ptr(),
+                                                    kv_idx.data_ptr(), cap, dk.data_ptr(),
                                                     dv.data_ptr(), ws.data_ptr(), wsb, s))
     if marks:
         marks[2].record()
     _check("vsa2_attn_bwd_dq", vsa2_attn_bwd_dq(p, q.data_ptr(), k.data_ptr(), v.data_ptr(),
                                                 do.data_ptr(), row_ptr.data_ptr(), col_idx.data_ptr(),
-                                                cap, comp, dq.data_ptr(), ws.data_ptr(), wsb, s))
+                                                cap, dq.data_ptr(), ws.data_ptr(), wsb, s))
     if marks:
         marks[3].record()
     return dq, dk, dv

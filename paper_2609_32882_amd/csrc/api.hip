@@ -103,8 +103,9 @@ route_ws route_layout(const vsa2_problem* p, const shape& s, const vsa2_select* 
 }
 
 // the forward's workspace holds its work order (one int32 per query-block row)
+// and the block magnitude flags
 size_t fwd_ws_bytes(const shape& s, const vsa2_problem* p) {
-    return vsa2::fwd_workspace_bytes(p->batch, p->heads_q, static_cast<int>(s.Nj));
+    return vsa2::fwd_workspace_bytes(p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.Nj));
 }
 
 size_t bwd_ws_bytes(const shape& s, const vsa2_problem* p) {
@@ -270,7 +271,7 @@ vsa2_status vsa2_attn_bwd(const vsa2_problem* p, const void* q, const void* k, c
     vsa2_status st = check_problem(p, &s);
     if (st != VSA2_OK) return st;
     if ((st = check_kernel_shape(p, s)) != VSA2_OK) return st;
-    if (!q || !k || !v || !o || !lse || !dout || !row_ptr || !kv_ptr || !dq || !dk || !dv)
+    if (!q || !k || !v || !o || !lse || !o_lo || !dout || !row_ptr || !kv_ptr || !dq || !dk || !dv)
         return VSA2_ERR_NULL;
     if ((!col_idx || !kv_idx) && col_cap > 0) return VSA2_ERR_NULL;
     if (col_cap < 0) return VSA2_ERR_CAPACITY;
@@ -287,26 +288,27 @@ vsa2_status vsa2_attn_bwd(const vsa2_problem* p, const void* q, const void* k, c
     return VSA2_OK;
 }
 
-vsa2_status vsa2_attn_bwd_prep(const vsa2_problem* p, const void* o, const float* lse, const void* o_lo,
-                               const void* dout, void* ws, size_t ws_bytes, hipStream_t stream) {
+vsa2_status vsa2_attn_bwd_prep(const vsa2_problem* p, const void* q, const void* k, const void* v, const void* o,
+                               const float* lse, const void* o_lo, const void* dout, void* ws, size_t ws_bytes,
+                               hipStream_t stream) {
     shape s;
     vsa2_status st = check_problem(p, &s);
     if (st != VSA2_OK) return st;
     if ((st = check_kernel_shape(p, s)) != VSA2_OK) return st;
-    if (!o || !lse || !dout) return VSA2_ERR_NULL;
-    if (!aligned16(o) || !aligned16(dout) || !aligned16(o_lo)) return VSA2_ERR_ALIGN;
+    if (!q || !k || !v || !o || !lse || !o_lo || !dout) return VSA2_ERR_NULL;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(dout) || !aligned16(o_lo))
+        return VSA2_ERR_ALIGN;
     const size_t need = bwd_ws_bytes(s, p);
     if (!ws || ws_bytes < need) return VSA2_ERR_WORKSPACE;
     if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
-    VSA2_TRY_HIP(vsa2::launch_attn_bwd_prep(p->dtype, p->head_dim, o, lse, o_lo, dout, ws, p->batch,
-                                            p->heads_q, static_cast<int>(s.Nj), stream));
+    VSA2_TRY_HIP(vsa2::launch_attn_bwd_prep(p->dtype, p->head_dim, q, k, v, o, lse, o_lo, dout, ws, p->batch,
+                                            p->heads_q, p->heads_kv, static_cast<int>(s.Nj), grid_of(p), stream));
     return VSA2_OK;
 }
 
 vsa2_status vsa2_attn_bwd_dkdv(const vsa2_problem* p, const void* q, const void* k, const void* v,
                                const void* dout, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
-                               int32_t compensated, void* dk, void* dv, void* ws, size_t ws_bytes,
-                               hipStream_t stream) {
+                               void* dk, void* dv, void* ws, size_t ws_bytes, hipStream_t stream) {
     shape s;
     vsa2_status st = check_problem(p, &s);
     if (st != VSA2_OK) return st;
@@ -319,15 +321,15 @@ vsa2_status vsa2_attn_bwd_dkdv(const vsa2_problem* p, const void* q, const void*
     const size_t need = bwd_ws_bytes(s, p);
     if (!ws || ws_bytes < need) return VSA2_ERR_WORKSPACE;
     if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
-    VSA2_TRY_HIP(vsa2::launch_attn_bwd_dkdv(p->dtype, p->head_dim, compensated != 0, q, k, v, dout, kv_ptr,
-                                            kv_idx, col_cap, dk, dv, ws, p->batch, p->heads_q, p->heads_kv,
-                                            static_cast<int>(s.Nj), grid_of(p), stream));
+    VSA2_TRY_HIP(vsa2::launch_attn_bwd_dkdv(p->dtype, p->head_dim, q, k, v, dout, kv_ptr, kv_idx, col_cap, dk, dv,
+                                            ws, p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.Nj),
+                                            grid_of(p), stream));
     return VSA2_OK;
 }
 
 vsa2_status vsa2_attn_bwd_dq(const vsa2_problem* p, const void* q, const void* k, const void* v,
                              const void* dout, const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
-                             int32_t compensated, void* dq, void* ws, size_t ws_bytes, hipStream_t stream) {
+                             void* dq, void* ws, size_t ws_bytes, hipStream_t stream) {
     shape s;
     vsa2_status st = check_problem(p, &s);
     if (st != VSA2_OK) return st;
@@ -340,9 +342,9 @@ vsa2_status vsa2_attn_bwd_dq(const vsa2_problem* p, const void* q, const void* k
     const size_t need = bwd_ws_bytes(s, p);
     if (!ws || ws_bytes < need) return VSA2_ERR_WORKSPACE;
     if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
-    VSA2_TRY_HIP(vsa2::launch_attn_bwd_dq(p->dtype, p->head_dim, compensated != 0, q, k, v, dout, row_ptr,
-                                          col_idx, col_cap, dq, ws, p->batch, p->heads_q, p->heads_kv,
-                                          static_cast<int>(s.Nj), grid_of(p), stream));
+    VSA2_TRY_HIP(vsa2::launch_attn_bwd_dq(p->dtype, p->head_dim, q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws,
+                                          p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.Nj), grid_of(p),
+                                          stream));
     return VSA2_OK;
 }
 

@@ -85,21 +85,23 @@ __global__ __launch_bounds__(256) void stat_kernel(const T* __restrict__ o, cons
 // block stream in during the whole of the current one.  On a padded grid,
 // padding keys get dK = dV = 0 and padding queries (scaled LSE = +inf) add
 // nothing.  (PAD: the grid is padded; the masking is compiled only into
-// that variant.)
+// that variant.)  bf16: on block pairs that touch a large-magnitude block
+// (this key block's flag or the query block's) P and dS enter the dV and
+// dK products as two bf16 terms (hi + lo).
 // ---------------------------------------------------------------------------
-template <typename T, int D, bool COMP, bool PAD>
+template <typename T, int D, bool PAD>
 __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float* __restrict__ stat,
     const int32_t* __restrict__ kv_ptr, const int32_t* __restrict__ kv_idx, int64_t col_cap,
     T* __restrict__ dk, T* __restrict__ dv, int Hq, int Hkv, int N, float c_log2, float scale,
-    const int32_t* __restrict__ order, cube_grid grid) {
+    const int32_t* __restrict__ order, cube_grid grid, block_flag_layout fl) {
     using F = typename frag_of<T>::type;
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;
     constexpr int MT = D / 32;
     constexpr int RB = D * E;                    // tile row bytes
-    constexpr bool SPLIT = COMP && sizeof(T) == 2;   // P and dS as hi + lo
+    constexpr bool SPLIT = sizeof(T) == 2;       // two-term P and dS possible (bf16 only)
     using RT = async_tile<64, RB, 2, true, E == 2>;      // Q, dO rows (slot-swapped)
     __shared__ __align__(1024) char q_lds[2][RT::BYTES];
     __shared__ __align__(1024) char o_lds[2][RT::BYTES];
@@ -133,18 +135,26 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
 #pragma unroll
         for (int i = 0; i < 16; ++i) { acc_v[mt][i] = 0.f; acc_k[mt][i] = 0.f; }
 
-    // query-block token offset of entry e, or -1 for a malformed entry
-    auto q0_of = [&](int64_t e) -> int64_t {
-        const int ent = scalar_load_i32(kv_idx + e);
-        const int hl = ent / N;
-        if (ent < 0 || hl >= grp) return -1;
-        const int64_t bh = static_cast<int64_t>(b) * Hq + hkv * grp + hl;
-        return bh * L + static_cast<int64_t>(ent % N) * 64;
+    // query-block row of entry value ent ((b*Hq + h)*N + n_q), or -1 for a
+    // malformed entry; its first token is row * 64
+    const int64_t qrow0 = (static_cast<int64_t>(b) * Hq + hkv * grp) * N;
+    auto qrow_of = [&](int ent) -> int64_t {
+        if (ent < 0 || ent / N >= grp) return -1;
+        return qrow0 + ent;
     };
+    // two-term operands on every pair of a flagged key block; otherwise on
+    // the pairs whose query block is flagged (per-pair flags are read only
+    // when the KV group holds a flagged query block)
+    bool all_big = false, some_big = false;
+    if constexpr (SPLIT) {
+        all_big = byte_of(scalar_load_i32(byte_word(fl.kv, krow)), krow);
+        some_big = !all_big && scalar_load_i32(fl.any_q + bkv) != 0;
+    }
     const RT rt(wave, lane);
-    // Q, dO and the statistics of the 64 queries (512 bytes, 16 lanes of each wave)
-    auto issue = [&](int64_t q0, int buf) {
-        const int64_t o0 = q0 < 0 ? 0 : q0;
+    // Q, dO and the statistics of the 64 queries of query-block row qr (512
+    // bytes, 16 lanes of each wave)
+    auto issue = [&](int64_t qr, int buf) {
+        const int64_t o0 = qr < 0 ? 0 : qr * 64;
         rt.issue(q_lds[buf], reinterpret_cast<const char*>(q + o0 * D), wave);
         rt.issue(o_lds[buf], reinterpret_cast<const char*>(dout + o0 * D), wave);
         if (lane < 16)
@@ -179,13 +189,24 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
     auto entry = [&](int64_t j) -> int64_t { return e0 + j; };
     int64_t q_cur = -1;
     if (cnt > 0) {
-        q_cur = q0_of(entry(0));
+        q_cur = qrow_of(scalar_load_i32(kv_idx + entry(0)));
         issue(q_cur, 0);
     }
     for (int64_t j = 0; j < cnt; ++j) {
         const int buf = static_cast<int>(j & 1);
         const bool has_next = j + 1 < cnt;
-        const int64_t q_next = has_next ? q0_of(entry(j + 1)) : -1;
+        // the next list entry, and the current query block's flag with it
+        int64_t q_next = -1;
+        bool big = all_big;
+        if (SPLIT && some_big && q_cur >= 0) {
+            int32_t ent = -1, w = 0;
+            if (has_next) scalar_load2_i32(kv_idx + entry(j + 1), byte_word(fl.q, q_cur), ent, w);
+            else w = scalar_load_i32(byte_word(fl.q, q_cur));
+            q_next = has_next ? qrow_of(ent) : -1;
+            big = byte_of(w, q_cur);
+        } else if (has_next) {
+            q_next = qrow_of(scalar_load_i32(kv_idx + entry(j + 1)));
+        }
         // One barrier per block: after it, this block's copies (the only
         // ones outstanding) are visible and both waves are done with the
         // previous block, whose buffer then receives the next block's copies.
@@ -195,15 +216,19 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
         const char* qt = q_lds[buf];
         const char* ot = o_lds[buf];
         const float* st = st_lds[buf];
-        if (q_cur >= 0) {
-            // Software pipeline over the two 32-query tiles of the block:
-            //   S/dP(tile 0) | S/dP(tile 1) + P,dS(tile 0) |
-            //   dV/dK(tile 0) + P,dS(tile 1) | dV/dK(tile 1)
-            // so the exponentials and the dS arithmetic of one tile issue
-            // while the other tile's MFMAs run (one wave per SIMD: the wave's
-            // own independent work is all there is to overlap).  LDS operand
-            // fragments are requested one step ahead of their MFMAs;
-            // lds_order keeps the compiler from moving work across steps.
+        // Software pipeline over the two 32-query tiles of the block:
+        //   S/dP(tile 0) | S/dP(tile 1) + P,dS(tile 0) |
+        //   dV/dK(tile 0) + P,dS(tile 1) | dV/dK(tile 1)
+        // so the exponentials and the dS arithmetic of one tile issue
+        // while the other tile's MFMAs run (one wave per SIMD: the wave's
+        // own independent work is all there is to overlap).  LDS operand
+        // fragments are requested one step ahead of their MFMAs;
+        // lds_order keeps the compiler from moving work across steps.
+        // two (wave-uniform): P and dS as hi + lo, a second dV / dK product
+        // with the lo terms.  One code path with the lo steps behind scalar
+        // branches: two inlined variants of the loop raise the kernel's
+        // register allocation for both.
+        auto pair = [&](bool two) {
             constexpr int NB = KS / 2;           // S/dP steps per tile (2 k-steps each)
             constexpr int NU = 2 * MT;           // dV/dK steps per tile
             constexpr int EV = 16 / NB;          // P,dS elements per S/dP step
@@ -251,7 +276,7 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
                     float xp[8], xd[8];
 #pragma unroll
                     for (int i = 0; i < 8; ++i) { xp[i] = s[t][8 * h + i]; xd[i] = dp[t][8 * h + i]; }
-                    if constexpr (SPLIT) {
+                    if (SPLIT && two) {
                         pack_frag_hilo(pb[t][h], pl[t][SPLIT ? h : 0], xp);
                         pack_frag_hilo(db[t][h], dl[t][SPLIT ? h : 0], xd);
                     } else {
@@ -299,12 +324,13 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
                 lds_order();
                 const int h = u / MT, mt = u % MT;
                 mma(acc_v[mt], ta[k & 1][0], pb[t][h]);
-                if constexpr (SPLIT) mma(acc_v[mt], ta[k & 1][0], pl[t][SPLIT ? h : 0]);
+                if (SPLIT && two) mma(acc_v[mt], ta[k & 1][0], pl[t][SPLIT ? h : 0]);
                 mma(acc_k[mt], ta[k & 1][1], db[t][h]);
-                if constexpr (SPLIT) mma(acc_k[mt], ta[k & 1][1], dl[t][SPLIT ? h : 0]);
+                if (SPLIT && two) mma(acc_k[mt], ta[k & 1][1], dl[t][SPLIT ? h : 0]);
                 if (t == 0) softmax_grad(1, u * EU, EU);
             }
-        }
+        };
+        if (q_cur >= 0) pair(big);
         q_cur = q_next;
     }
 
@@ -338,21 +364,22 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
 // dQ: one workgroup (2 waves) per query block; wave owns 32 queries.
 // Tiles K (for S^T and, read transposed, K^T) and V (for dP^T).  On a
 // padded grid, padding keys get P = 0 and padding queries dQ = 0 (PAD
-// variant only).
+// variant only).  bf16: on block pairs that touch a large-magnitude block
+// dS enters the dQ product as two bf16 terms (hi + lo).
 // ---------------------------------------------------------------------------
-template <typename T, int D, bool COMP, bool PAD>
+template <typename T, int D, bool PAD>
 __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float* __restrict__ stat,
     const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx, int64_t col_cap,
     T* __restrict__ dq, int Hq, int Hkv, int N, float c_log2, float scale, int period,
-    const int32_t* __restrict__ order, cube_grid grid) {
+    const int32_t* __restrict__ order, cube_grid grid, block_flag_layout fl) {
     using F = typename frag_of<T>::type;
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;
     constexpr int MT = D / 32;
     constexpr int RB = D * E;
-    constexpr bool SPLIT = COMP && sizeof(T) == 2;   // dS as hi + lo
+    constexpr bool SPLIT = sizeof(T) == 2;       // two-term dS possible (bf16 only)
     using RT = async_tile<64, RB, 2, true, E == 2>;     // K, V rows (slot-swapped)
     __shared__ __align__(1024) char k_lds[RT::BYTES];
     __shared__ __align__(1024) char v_lds[RT::BYTES];
@@ -401,6 +428,15 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
         const int c = scalar_load_i32(col_idx + e);
         return (c >= 0 && c < N) ? c : -1;
     };
+    // two-term dS on every pair of a flagged query block; otherwise on the
+    // pairs whose key block is flagged (per-pair flags are read only when the
+    // head holds a flagged key block)
+    const int64_t kvrow0 = static_cast<int64_t>(b * Hkv + hkv) * N;
+    bool all_big = false, some_big = false;
+    if constexpr (SPLIT) {
+        all_big = byte_of(scalar_load_i32(byte_word(fl.q, row)), row);
+        some_big = !all_big && scalar_load_i32(fl.any_kv + b * Hkv + hkv) != 0;
+    }
     constexpr int64_t TILE = 64 * RB;
     const RT rt(wave, lane);
     auto issue_k = [&](int c) { rt.issue(k_lds, kb + static_cast<int64_t>(c < 0 ? 0 : c) * TILE, wave); };
@@ -424,7 +460,19 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     }
     for (int64_t j = 0; j < cnt; ++j) {
         const bool has_next = j + 1 < cnt;
-        const int c_next = has_next ? block_of(entry(j + 1)) : -1;
+        // the next list entry, and the current key block's flag with it
+        int c_next = -1;
+        bool big = all_big;
+        if (SPLIT && some_big && c_cur >= 0) {
+            const int64_t fi = kvrow0 + c_cur;
+            int32_t e = -1, w = 0;
+            if (has_next) scalar_load2_i32(col_idx + entry(j + 1), byte_word(fl.kv, fi), e, w);
+            else w = scalar_load_i32(byte_word(fl.kv, fi));
+            c_next = (e >= 0 && e < N) ? e : -1;
+            big = byte_of(w, fi);
+        } else if (has_next) {
+            c_next = block_of(entry(j + 1));
+        }
 
         vm_wait<0>();                   // K and V landed
         wg_barrier();
@@ -470,9 +518,9 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
 #pragma unroll
                 for (int i = 0; i < 16; ++i) ds[i] = ((lm >> ((i >> 3) * 16 + (i & 7))) & 1u) ? ds[i] : 0.f;
             }
-            if constexpr (SPLIT) {
-                pack_frag_hilo(sb[t2][0], sl[t2][0], ds);
-                pack_frag_hilo(sb[t2][1], sl[t2][1], ds + 8);
+            if (SPLIT && big) {
+                pack_frag_hilo(sb[t2][0], sl[SPLIT ? t2 : 0][0], ds);
+                pack_frag_hilo(sb[t2][1], sl[SPLIT ? t2 : 0][1], ds + 8);
             } else {
                 pack_frag(sb[t2][0], ds);
                 pack_frag(sb[t2][1], ds + 8);
@@ -482,22 +530,26 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
         if (has_next) issue_v(c_next);
         if (c_cur >= 0) {
             // dQ^T += K^T dS^T over the 64 keys (4 k-steps of 16); K^T read
-            // transposed, one k-step ahead of its products
-            F fa[2][MT];
-            auto fetch = [&](F* f, int kk) {
+            // transposed, one k-step ahead of its products.  On a flagged
+            // pair a second pass adds K^T times the lo terms of dS.
+            auto dq_product = [&](F (*sf)[2]) {
+                F fa[2][MT];
+                auto fetch = [&](F* f, int kk) {
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) lds_frag_tr<RB, true>(f[mt], k_lds, mt * 32, kk * 16);
-            };
-            fetch(fa[0], 0);
+                    for (int mt = 0; mt < MT; ++mt) lds_frag_tr<RB, true>(f[mt], k_lds, mt * 32, kk * 16);
+                };
+                fetch(fa[0], 0);
 #pragma unroll
-            for (int kk = 0; kk < 4; ++kk) {
-                if (kk + 1 < 4) fetch(fa[(kk + 1) & 1], kk + 1);
-                lds_order();
+                for (int kk = 0; kk < 4; ++kk) {
+                    if (kk + 1 < 4) fetch(fa[(kk + 1) & 1], kk + 1);
+                    lds_order();
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    mma(dqa[mt], fa[kk & 1][mt], sb[kk >> 1][kk & 1]);
-                    if constexpr (SPLIT) mma(dqa[mt], fa[kk & 1][mt], sl[(kk >> 1) & (SPLIT ? 1 : 0)][kk & 1]);
+                    for (int mt = 0; mt < MT; ++mt) mma(dqa[mt], fa[kk & 1][mt], sf[kk >> 1][kk & 1]);
                 }
+            };
+            dq_product(sb);
+            if constexpr (SPLIT) {
+                if (big) dq_product(sl);
             }
         }
         wg_barrier();                   // K buffer free
@@ -522,12 +574,9 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
 }
 
 // Workspace of the backward call: per query token LSE * log2(e) and -Delta,
-// then the work orders of the CSR rows (dQ) and of the CSC rows (dK/dV).
+// then the work orders of the CSR rows (dQ) and of the CSC rows (dK/dV),
+// then the block magnitude flags.
 static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
-
-size_t fwd_workspace_bytes(int batch, int Hq, int N) {
-    return align256(4 * static_cast<size_t>(batch) * Hq * N);
-}
 
 size_t bwd_ws_csr_order_offset(int batch, int Hq, int N) {
     return align256(8 * static_cast<size_t>(batch) * Hq * N * 64);
@@ -537,10 +586,22 @@ size_t bwd_ws_csc_order_offset(int batch, int Hq, int N) {
     return bwd_ws_csr_order_offset(batch, Hq, N) + align256(4 * static_cast<size_t>(batch) * Hq * N);
 }
 
+static size_t bwd_ws_flags_offset(int batch, int Hq, int Hkv, int N) {
+    return bwd_ws_csc_order_offset(batch, Hq, N) + align256(4 * static_cast<size_t>(batch) * Hkv * N);
+}
+
+static block_flag_layout bwd_flags(void* ws, int batch, int Hq, int Hkv, int N) {
+    return block_flags_at(static_cast<char*>(ws) + bwd_ws_flags_offset(batch, Hq, Hkv, N),
+                          static_cast<int64_t>(batch) * Hq * N, static_cast<int64_t>(batch) * Hkv * N,
+                          static_cast<int64_t>(batch) * Hkv);
+}
+
 size_t bwd_workspace_bytes(int dtype, int D, int batch, int Hq, int Hkv, int N) {
     (void)dtype;
     (void)D;
-    return bwd_ws_csc_order_offset(batch, Hq, N) + align256(4 * static_cast<size_t>(batch) * Hkv * N);
+    return bwd_ws_flags_offset(batch, Hq, Hkv, N) +
+           block_flags_bytes(static_cast<int64_t>(batch) * Hq * N, static_cast<int64_t>(batch) * Hkv * N,
+                             static_cast<int64_t>(batch) * Hkv);
 }
 
 // Stage 1: per query token LSE * log2(e) and -Delta into ws.
@@ -556,7 +617,7 @@ static hipError_t launch_prep_t(const void* o, const float* lse, const void* o_l
 }
 
 // Stage 2: dK and dV (key-block stationary, transposed lists).
-template <typename T, int D, bool COMP>
+template <typename T, int D>
 static hipError_t launch_dkdv_t(const void* q, const void* k, const void* v, const void* dout,
                                 const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap, void* dk,
                                 void* dv, void* ws, int batch, int Hq, int Hkv, int N, const cube_grid& cg,
@@ -568,19 +629,20 @@ static hipError_t launch_dkdv_t(const void* q, const void* k, const void* v, con
     if (e != hipSuccess) return e;
     const float c = kLog2e / sqrtf(static_cast<float>(D));
     const float scale = 1.0f / sqrtf(static_cast<float>(D));
+    const block_flag_layout fl = bwd_flags(ws, batch, Hq, Hkv, N);
     auto go = [&](auto pad) {
-        hipLaunchKernelGGL((dkdv_kernel<T, D, COMP, decltype(pad)::value>), dim3(static_cast<unsigned>(krows)),
+        hipLaunchKernelGGL((dkdv_kernel<T, D, decltype(pad)::value>), dim3(static_cast<unsigned>(krows)),
                            dim3(AB_NT), 0, s, static_cast<const T*>(q), static_cast<const T*>(k),
                            static_cast<const T*>(v), static_cast<const T*>(dout), static_cast<const float*>(ws),
                            kv_ptr, kv_idx, col_cap, static_cast<T*>(dk), static_cast<T*>(dv), Hq, Hkv, N, c, scale,
-                           order, cg);
+                           order, cg, fl);
     };
     if (cg.padded) go(std::true_type{}); else go(std::false_type{});
     return hipGetLastError();
 }
 
 // Stage 3: dQ (query-block stationary, CSR rows).
-template <typename T, int D, bool COMP>
+template <typename T, int D>
 static hipError_t launch_dq_t(const void* q, const void* k, const void* v, const void* dout,
                               const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* dq,
                               void* ws, int batch, int Hq, int Hkv, int N, const cube_grid& cg, hipStream_t s) {
@@ -591,13 +653,14 @@ static hipError_t launch_dq_t(const void* q, const void* k, const void* v, const
     if (e != hipSuccess) return e;
     const float c = kLog2e / sqrtf(static_cast<float>(D));
     const float scale = 1.0f / sqrtf(static_cast<float>(D));
+    const block_flag_layout fl = bwd_flags(ws, batch, Hq, Hkv, N);
     auto go = [&](auto pad) {
         constexpr bool P = decltype(pad)::value;
-        hipLaunchKernelGGL((dq_kernel<T, D, COMP, P>), dim3(static_cast<unsigned>(qrows)), dim3(AB_NT), 0, s,
+        hipLaunchKernelGGL((dq_kernel<T, D, P>), dim3(static_cast<unsigned>(qrows)), dim3(AB_NT), 0, s,
                            static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
                            static_cast<const T*>(dout), static_cast<const float*>(ws), row_ptr, col_idx, col_cap,
                            static_cast<T*>(dq), Hq, Hkv, N, c, scale,
-                           resident_per_xcd<dq_kernel<T, D, COMP, P>>(AB_NT), order, cg);
+                           resident_per_xcd<dq_kernel<T, D, P>>(AB_NT), order, cg, fl);
     };
     if (cg.padded) go(std::true_type{}); else go(std::false_type{});
     return hipGetLastError();
@@ -618,47 +681,48 @@ hipError_t launch_attn_bwd_prep_tokens(int dtype, int D, const void* o, const fl
     VSA2_DISPATCH_TD(return (launch_prep_t<T, DD>(o, lse, o_lo, dout, ws, ntok, s)));
 }
 
-hipError_t launch_attn_bwd_prep(int dtype, int D, const void* o, const float* lse, const void* o_lo,
-                                const void* dout, void* ws, int batch, int Hq, int N, hipStream_t s) {
-    return launch_attn_bwd_prep_tokens(dtype, D, o, lse, o_lo, dout, ws, static_cast<int64_t>(batch) * Hq * N * 64,
-                                       s);
+// Stage 1 of the backward: the per-token statistics and (bf16) the block
+// magnitude flags of Q, K, V.
+hipError_t launch_attn_bwd_prep(int dtype, int D, const void* q, const void* k, const void* v, const void* o,
+                                const float* lse, const void* o_lo, const void* dout, void* ws, int batch, int Hq,
+                                int Hkv, int N, const cube_grid& cg, hipStream_t s) {
+    hipError_t e = launch_attn_bwd_prep_tokens(dtype, D, o, lse, o_lo, dout, ws,
+                                               static_cast<int64_t>(batch) * Hq * N * 64, s);
+    if (e != hipSuccess || dtype != 1) return e;
+    return launch_block_flags(q, k, v, bwd_flags(ws, batch, Hq, Hkv, N), static_cast<int64_t>(batch) * Hq * N,
+                              static_cast<int64_t>(batch) * Hkv * N, N, D, Hq, Hkv, cg, s);
 }
 
-hipError_t launch_attn_bwd_dkdv(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
+hipError_t launch_attn_bwd_dkdv(int dtype, int D, const void* q, const void* k, const void* v,
                                 const void* dout, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
                                 void* dk, void* dv, void* ws, int batch, int Hq, int Hkv, int N,
                                 const cube_grid& cg, hipStream_t s) {
-    VSA2_DISPATCH_TD(return comp ? launch_dkdv_t<T, DD, true>(q, k, v, dout, kv_ptr, kv_idx, col_cap, dk, dv, ws,
-                                                              batch, Hq, Hkv, N, cg, s)
-                                 : launch_dkdv_t<T, DD, false>(q, k, v, dout, kv_ptr, kv_idx, col_cap, dk, dv, ws,
-                                                               batch, Hq, Hkv, N, cg, s));
+    VSA2_DISPATCH_TD(return (launch_dkdv_t<T, DD>(q, k, v, dout, kv_ptr, kv_idx, col_cap, dk, dv, ws, batch, Hq,
+                                                  Hkv, N, cg, s)));
 }
 
-hipError_t launch_attn_bwd_dq(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
+hipError_t launch_attn_bwd_dq(int dtype, int D, const void* q, const void* k, const void* v,
                               const void* dout, const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
                               void* dq, void* ws, int batch, int Hq, int Hkv, int N, const cube_grid& cg,
                               hipStream_t s) {
-    VSA2_DISPATCH_TD(return comp ? launch_dq_t<T, DD, true>(q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws,
-                                                            batch, Hq, Hkv, N, cg, s)
-                                 : launch_dq_t<T, DD, false>(q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws,
-                                                             batch, Hq, Hkv, N, cg, s));
+    VSA2_DISPATCH_TD(return (launch_dq_t<T, DD>(q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws, batch, Hq, Hkv,
+                                                N, cg, s)));
 }
 #undef VSA2_DISPATCH_TD
 
-// The whole backward: prep, dK/dV, dQ on one stream (compensated when o_lo).
+// The whole backward: prep, dK/dV, dQ on one stream.
 hipError_t launch_attn_bwd(int dtype, int D, const void* q, const void* k, const void* v, const void* o,
                            const float* lse, const void* o_lo, const void* dout, const int32_t* row_ptr,
                            const int32_t* col_idx, const int32_t* kv_ptr, const int32_t* kv_idx,
                            int64_t col_cap, void* dq, void* dk, void* dv, void* ws, int batch,
                            int Hq, int Hkv, int N, const cube_grid& cg, hipStream_t s) {
-    hipError_t e = launch_attn_bwd_prep(dtype, D, o, lse, o_lo, dout, ws, batch, Hq, N, s);
+    hipError_t e = launch_attn_bwd_prep(dtype, D, q, k, v, o, lse, o_lo, dout, ws, batch, Hq, Hkv, N, cg, s);
     if (e != hipSuccess) return e;
-    const bool comp = o_lo != nullptr;
-    e = launch_attn_bwd_dkdv(dtype, D, comp, q, k, v, dout, kv_ptr, kv_idx, col_cap, dk, dv, ws, batch, Hq, Hkv,
-                             N, cg, s);
+    e = launch_attn_bwd_dkdv(dtype, D, q, k, v, dout, kv_ptr, kv_idx, col_cap, dk, dv, ws, batch, Hq, Hkv, N, cg,
+                             s);
     if (e != hipSuccess) return e;
-    return launch_attn_bwd_dq(dtype, D, comp, q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws, batch, Hq, Hkv,
-                              N, cg, s);
+    return launch_attn_bwd_dq(dtype, D, q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws, batch, Hq, Hkv, N, cg,
+                              s);
 }
 
 }  // namespace vsa2

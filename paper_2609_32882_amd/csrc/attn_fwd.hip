@@ -17,6 +17,8 @@
 // and row sum need one exchange with the other half-wave and nothing else.
 // On a padded grid the padding keys of a cut cube are masked out of the
 // softmax, and padding queries give O = 0 and LSE = -inf.
+#include <type_traits>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -24,9 +26,12 @@ namespace vsa2 {
 
 constexpr int AF_NT = 128;
 
-// COMP (compensated): P enters the PV product as two bf16 terms (hi + lo),
-// and the rounding remainder of O is written to o_lo, so that O + o_lo
-// carries about 16 significant bits for the backward's Delta = dO . O.
+// COMP (the forward of a training step): the rounding remainder of O is
+// written to o_lo, so that O + o_lo carries about 16 significant bits for
+// the backward's Delta = dO . O, and on block pairs that touch a
+// large-magnitude block (the query block's or the key block's flag) P
+// enters the PV product as two bf16 terms (hi + lo), which keeps O itself
+// accurate to about 16 bits there.  Other pairs take one-term P.
 // PAD: the grid is padded (the masking is compiled only into this variant,
 // so the unpadded one keeps its register budget).
 template <typename T, int D, bool COMP, bool PAD>
@@ -34,9 +39,9 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col_idx, int64_t col_cap,
     T* __restrict__ o, float* __restrict__ lse, T* __restrict__ o_lo, int Hq, int Hkv, int N, float c_log2,
-    int period, const int32_t* __restrict__ order, cube_grid grid) {
+    int period, const int32_t* __restrict__ order, cube_grid grid, block_flag_layout fl) {
     using F = typename frag_of<T>::type;
-    constexpr bool SPLIT = COMP && sizeof(T) == 2;
+    constexpr bool SPLIT = COMP && sizeof(T) == 2;   // two-term P possible (bf16 only)
     constexpr int E = sizeof(T);
     constexpr int KS = D / 16;        // macro k-steps over the head dim
     constexpr int MT = D / 32;        // 32-row tiles of O^T
@@ -89,6 +94,16 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
         const int c = scalar_load_i32(col_idx + e);
         return (c >= 0 && c < N) ? c : -1;
     };
+    // two-term P on every pair of a flagged query block; otherwise on the
+    // pairs whose key block is flagged (per-pair flags are read only when
+    // the head holds a flagged key block)
+    const int64_t kvrow0 = static_cast<int64_t>(b * Hkv + hkv) * N;
+    bool all_big = false, some_big = false;
+    if constexpr (SPLIT) {
+        // scalar loads: the tile copies' vmcnt bookkeeping sees no other loads
+        all_big = byte_of(scalar_load_i32(byte_word(fl.q, row)), row);
+        some_big = !all_big && scalar_load_i32(fl.any_kv + b * Hkv + hkv) != 0;
+    }
     const KT kt(wave, lane);
     const KT& vt_ = kt;
 #pragma unroll
@@ -109,7 +124,19 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     }
     for (int64_t j = 0; j < cnt; ++j) {
         const bool has_next = j + 1 < cnt;
-        const int c_next = has_next ? block_of(entry(j + 1)) : -1;
+        // the next list entry, and the current key block's flag with it
+        int c_next = -1;
+        bool big = all_big;
+        if (SPLIT && some_big && c_cur >= 0) {
+            const int64_t fi = kvrow0 + c_cur;
+            int32_t e = -1, w = 0;
+            if (has_next) scalar_load2_i32(col_idx + entry(j + 1), byte_word(fl.kv, fi), e, w);
+            else w = scalar_load_i32(byte_word(fl.kv, fi));
+            c_next = (e >= 0 && e < N) ? e : -1;
+            big = byte_of(w, fi);
+        } else if (has_next) {
+            c_next = block_of(entry(j + 1));
+        }
         const int64_t nxt_off = static_cast<int64_t>(c_next < 0 ? 0 : c_next) * 64 * KRB;
 
         vm_wait<VT::PER_WAVE>();          // this K tile has landed (V may still stream)
@@ -188,30 +215,37 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
         wg_barrier();
         if (c_cur >= 0) {
             // O^T += V^T P^T over 4 k-steps of 16 keys: keys 16kk + 8half + (0..7);
-            // V^T fragments are requested one k-step ahead of their products
+            // V^T fragments are requested one k-step ahead of their products.
+            // On a flagged pair P is split into hi + lo = bf16(P - hi), and a
+            // second pass adds V^T lo (its fragments read again).
             F pb[4], pl[SPLIT ? 4 : 1];
+            const bool two = SPLIT && big;
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk) {
-                float pv[8];
+                float pv8[8];
 #pragma unroll
-                for (int i = 0; i < 8; ++i) pv[i] = s[kk >> 1][(kk & 1) * 8 + i];
-                if constexpr (SPLIT) pack_frag_hilo(pb[kk], pl[SPLIT ? kk : 0], pv); else pack_frag(pb[kk], pv);
+                for (int i = 0; i < 8; ++i) pv8[i] = s[kk >> 1][(kk & 1) * 8 + i];
+                if (two) pack_frag_hilo(pb[kk], pl[SPLIT ? kk : 0], pv8);
+                else pack_frag(pb[kk], pv8);
             }
-            F fa[2][MT];
-            auto fetch = [&](F* f, int kk) {
+            auto pv = [&](const F* pf) {
+                F fa[2][MT];
+                auto fetch = [&](F* f, int kk) {
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) lds_frag_tr<KRB, true>(f[mt], v_lds, mt * 32, kk * 16);
-            };
-            fetch(fa[0], 0);
+                    for (int mt = 0; mt < MT; ++mt) lds_frag_tr<KRB, true>(f[mt], v_lds, mt * 32, kk * 16);
+                };
+                fetch(fa[0], 0);
 #pragma unroll
-            for (int kk = 0; kk < 4; ++kk) {
-                if (kk + 1 < 4) fetch(fa[(kk + 1) & 1], kk + 1);
-                lds_order();
+                for (int kk = 0; kk < 4; ++kk) {
+                    if (kk + 1 < 4) fetch(fa[(kk + 1) & 1], kk + 1);
+                    lds_order();
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    mma(oacc[mt], fa[kk & 1][mt], pb[kk]);
-                    if constexpr (SPLIT) mma(oacc[mt], fa[kk & 1][mt], pl[SPLIT ? kk : 0]);
+                    for (int mt = 0; mt < MT; ++mt) mma(oacc[mt], fa[kk & 1][mt], pf[kk]);
                 }
+            };
+            pv(pb);
+            if constexpr (SPLIT) {
+                if (two) pv(pl);
             }
         }
         wg_barrier();                      // V buffer free
@@ -253,29 +287,46 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
 template <typename T, int D, bool COMP, bool PAD>
 static void launch_fwd_k(const void* q, const void* k, const void* v, const int32_t* row_ptr, const int32_t* col_idx,
                          int64_t col_cap, void* o, float* lse, void* o_lo, const int32_t* order, int64_t rows, int Hq,
-                         int Hkv, int N, const cube_grid& cg, hipStream_t s) {
+                         int Hkv, int N, const cube_grid& cg, const block_flag_layout& fl, hipStream_t s) {
     const float c = 1.4426950408889634f / sqrtf(static_cast<float>(D));
     hipLaunchKernelGGL((attn_fwd_kernel<T, D, COMP, PAD>), dim3(static_cast<unsigned>(rows)), dim3(AF_NT), 0, s,
                        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), row_ptr,
                        col_idx, col_cap, static_cast<T*>(o), lse, static_cast<T*>(o_lo), Hq, Hkv, N, c,
-                       resident_per_xcd<attn_fwd_kernel<T, D, COMP, PAD>>(AF_NT), order, cg);
+                       resident_per_xcd<attn_fwd_kernel<T, D, COMP, PAD>>(AF_NT), order, cg, fl);
+}
+
+// Forward workspace: the work order of the CSR rows (one int32 per row), then
+// the block magnitude flags (used when the call keeps O's remainder).
+static size_t align256f(size_t x) { return (x + 255) / 256 * 256; }
+
+size_t fwd_workspace_bytes(int batch, int Hq, int Hkv, int N) {
+    const int64_t rq = static_cast<int64_t>(batch) * Hq * N, rkv = static_cast<int64_t>(batch) * Hkv * N;
+    return align256f(4 * static_cast<size_t>(rq)) + block_flags_bytes(rq, rkv, static_cast<int64_t>(batch) * Hkv);
 }
 
 template <typename T, int D>
 static hipError_t launch_fwd_t(const void* q, const void* k, const void* v, const int32_t* row_ptr,
                                const int32_t* col_idx, int64_t col_cap, void* o, float* lse, void* o_lo,
-                               int32_t* order, int batch, int Hq, int Hkv, int N, const cube_grid& cg,
+                               void* ws, int batch, int Hq, int Hkv, int N, const cube_grid& cg,
                                hipStream_t s) {
     const int64_t rows = static_cast<int64_t>(batch) * Hq * N;
     if (rows == 0) return hipSuccess;
+    const int64_t rows_kv = static_cast<int64_t>(batch) * Hkv * N;
+    int32_t* order = static_cast<int32_t*>(ws);
+    const block_flag_layout fl = block_flags_at(static_cast<char*>(ws) + align256f(4 * static_cast<size_t>(rows)),
+                                                rows, rows_kv, static_cast<int64_t>(batch) * Hkv);
     hipError_t e = launch_lpt_order(row_ptr, rows, N, col_cap, order, s);
     if (e != hipSuccess) return e;
     if (o_lo) {
-        if (cg.padded) launch_fwd_k<T, D, true, true>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, rows, Hq, Hkv, N, cg, s);
-        else launch_fwd_k<T, D, true, false>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, rows, Hq, Hkv, N, cg, s);
+        if constexpr (sizeof(T) == 2) {
+            e = launch_block_flags(q, k, v, fl, rows, rows_kv, N, D, Hq, Hkv, cg, s);
+            if (e != hipSuccess) return e;
+        }
+        if (cg.padded) launch_fwd_k<T, D, true, true>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, rows, Hq, Hkv, N, cg, fl, s);
+        else launch_fwd_k<T, D, true, false>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, rows, Hq, Hkv, N, cg, fl, s);
     } else {
-        if (cg.padded) launch_fwd_k<T, D, false, true>(q, k, v, row_ptr, col_idx, col_cap, o, lse, nullptr, order, rows, Hq, Hkv, N, cg, s);
-        else launch_fwd_k<T, D, false, false>(q, k, v, row_ptr, col_idx, col_cap, o, lse, nullptr, order, rows, Hq, Hkv, N, cg, s);
+        if (cg.padded) launch_fwd_k<T, D, false, true>(q, k, v, row_ptr, col_idx, col_cap, o, lse, nullptr, order, rows, Hq, Hkv, N, cg, fl, s);
+        else launch_fwd_k<T, D, false, false>(q, k, v, row_ptr, col_idx, col_cap, o, lse, nullptr, order, rows, Hq, Hkv, N, cg, fl, s);
     }
     return hipGetLastError();
 }
@@ -284,13 +335,12 @@ hipError_t launch_attn_fwd(int dtype, int D, const void* q, const void* k, const
                            const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
                            float* lse, void* o_lo, void* ws, int batch, int Hq, int Hkv, int N,
                            const cube_grid& cg, hipStream_t s) {
-    int32_t* order = static_cast<int32_t*>(ws);
     if (dtype == 1) {
-        if (D == 64) return launch_fwd_t<bf16_t, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, batch, Hq, Hkv, N, cg, s);
-        if (D == 128) return launch_fwd_t<bf16_t, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, batch, Hq, Hkv, N, cg, s);
+        if (D == 64) return launch_fwd_t<bf16_t, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, ws, batch, Hq, Hkv, N, cg, s);
+        if (D == 128) return launch_fwd_t<bf16_t, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, ws, batch, Hq, Hkv, N, cg, s);
     } else {
-        if (D == 64) return launch_fwd_t<float, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, batch, Hq, Hkv, N, cg, s);
-        if (D == 128) return launch_fwd_t<float, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, order, batch, Hq, Hkv, N, cg, s);
+        if (D == 64) return launch_fwd_t<float, 64>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, ws, batch, Hq, Hkv, N, cg, s);
+        if (D == 128) return launch_fwd_t<float, 128>(q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, ws, batch, Hq, Hkv, N, cg, s);
     }
     return hipErrorInvalidValue;
 }

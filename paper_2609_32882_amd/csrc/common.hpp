@@ -382,6 +382,22 @@ __device__ __forceinline__ int32_t scalar_load_i32(const int32_t* p) {
     return v;
 }
 
+// Two independent wave-uniform 32-bit loads through the scalar cache with one
+// wait (a block-list entry and the magnitude flag of an earlier entry).
+__device__ __forceinline__ void scalar_load2_i32(const int32_t* a, const int32_t* b, int32_t& x, int32_t& y) {
+    asm volatile("s_load_dword %0, %2, 0x0\n\ts_load_dword %1, %3, 0x0\n\ts_waitcnt lgkmcnt(0)"
+                 : "=&s"(x), "=&s"(y)
+                 : "s"(a), "s"(b)
+                 : "memory");
+}
+
+// The 32-bit word holding byte i of a byte array (the array's allocation is
+// a multiple of 4 bytes from a 4-byte aligned start), and byte i within it.
+__device__ __forceinline__ const int32_t* byte_word(const uint8_t* p, int64_t i) {
+    return reinterpret_cast<const int32_t*>(p + (i & ~int64_t(3)));
+}
+__device__ __forceinline__ bool byte_of(int32_t w, int64_t i) { return ((w >> (8 * (i & 3))) & 0xff) != 0; }
+
 // One global_load_lds_dwordx4: lane l copies 16 bytes from base + voff(l) to
 // LDS byte address lds + 16 l.  Issued as inline assembly so that the
 // compiler's own wait-count bookkeeping, which cannot tell the LDS buffers

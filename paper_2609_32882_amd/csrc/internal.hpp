@@ -84,8 +84,9 @@ hipError_t launch_attn_fwd(int dtype, int D, const void* q, const void* k, const
                            const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
                            float* lse, void* o_lo, void* ws, int batch, int Hq, int Hkv, int N,
                            const cube_grid& cg, hipStream_t s);
-// Forward workspace: the work order of the CSR rows (int32 per row).
-size_t fwd_workspace_bytes(int batch, int Hq, int N);
+// Forward workspace: the work order of the CSR rows (int32 per row), then the
+// block magnitude flags.
+size_t fwd_workspace_bytes(int batch, int Hq, int Hkv, int N);
 // Backward workspace: (LSE*log2 e, Delta) per query token, then the work
 // orders of the CSR rows (dQ) and of the CSC rows (dK/dV).
 size_t bwd_workspace_bytes(int dtype, int D, int batch, int Hq, int Hkv, int N);
@@ -95,13 +96,30 @@ size_t bwd_ws_csc_order_offset(int batch, int Hq, int N);
 // (n_per_head rows) that falls into one XCD range.
 hipError_t launch_lpt_order(const int32_t* ptr, int64_t nrows, int64_t n_per_head, int64_t cap, int32_t* order,
                             hipStream_t s);
+// Magnitude flags of the 64-token blocks of bf16 Q, K, V: q[row] for the
+// query blocks, kv[row] for the key blocks (K and V combined), 1 when a real
+// token holds a value above 8 in magnitude; any_q[g] / any_kv[g] per KV group
+// g = b*Hkv + hkv: some flagged query block among the group's query heads /
+// some flagged key block of the head.  The attention kernels take two-term
+// P / dS operands on block pairs that touch a flagged block.
+struct block_flag_layout {
+    uint8_t* q;
+    uint8_t* kv;
+    int32_t* any_q;
+    int32_t* any_kv;
+};
+block_flag_layout block_flags_at(void* base, int64_t rows_q, int64_t rows_kv, int64_t groups);
+size_t block_flags_bytes(int64_t rows_q, int64_t rows_kv, int64_t groups);
+hipError_t launch_block_flags(const void* q, const void* k, const void* v, const block_flag_layout& f, int64_t rows_q,
+                              int64_t rows_kv, int N, int D, int Hq, int Hkv, const cube_grid& cg, hipStream_t s);
 hipError_t launch_attn_bwd(int dtype, int D, const void* q, const void* k, const void* v, const void* o,
                            const float* lse, const void* o_lo, const void* dout, const int32_t* row_ptr,
                            const int32_t* col_idx, const int32_t* kv_ptr, const int32_t* kv_idx,
                            int64_t col_cap, void* dq, void* dk, void* dv, void* ws, int batch,
                            int Hq, int Hkv, int N, const cube_grid& cg, hipStream_t s);
-hipError_t launch_attn_bwd_prep(int dtype, int D, const void* o, const float* lse, const void* o_lo,
-                                const void* dout, void* ws, int batch, int Hq, int N, hipStream_t s);
+hipError_t launch_attn_bwd_prep(int dtype, int D, const void* q, const void* k, const void* v, const void* o,
+                                const float* lse, const void* o_lo, const void* dout, void* ws, int batch, int Hq,
+                                int Hkv, int N, const cube_grid& cg, hipStream_t s);
 // (LSE * log2 e, dO . O) for ntok rows of D elements.
 hipError_t launch_attn_bwd_prep_tokens(int dtype, int D, const void* o, const float* lse, const void* o_lo,
                                        const void* dout, void* ws, int64_t ntok, hipStream_t s);
@@ -124,11 +142,11 @@ size_t joint_workspace_bytes(int batch, int Hq, int Hkv, int N, int M);
 hipError_t launch_joint_lists(const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, int batch, int Hq,
                               int Hkv, int N, int M, int32_t* j_row_ptr, int32_t* j_col_idx, int64_t j_cap,
                               int32_t* j_kv_ptr, int32_t* j_kv_idx, void* ws, hipStream_t s);
-hipError_t launch_attn_bwd_dkdv(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
+hipError_t launch_attn_bwd_dkdv(int dtype, int D, const void* q, const void* k, const void* v,
                                 const void* dout, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
                                 void* dk, void* dv, void* ws, int batch, int Hq, int Hkv, int N,
                                 const cube_grid& cg, hipStream_t s);
-hipError_t launch_attn_bwd_dq(int dtype, int D, bool comp, const void* q, const void* k, const void* v,
+hipError_t launch_attn_bwd_dq(int dtype, int D, const void* q, const void* k, const void* v,
                               const void* dout, const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
                               void* dq, void* ws, int batch, int Hq, int Hkv, int N, const cube_grid& cg,
                               hipStream_t s);

@@ -137,3 +137,121 @@ hipError_t launch_lpt_order(const int32_t* ptr, int64_t nrows, int64_t n_per_hea
 }
 
 }  // namespace vsa2
+
+namespace vsa2 {
+
+// ---------------------------------------------------------------------------
+// Magnitude flags of the 64-token blocks.
+//
+// bf16 products round P (in P.V and P^T dO) and dS (in dS K and dS^T Q) to 8
+// significant bits.  Those rounding errors are independent per element, but
+// the products multiply them by the other operand: when the keys (queries,
+// values) of a block share a large common component, the errors of a row
+// add up coherently along that component and are no longer small next to
+// the result, which is a difference of such components.  Large values also
+// make the softmax peaked, so P close to 1 repeats across the queries of a
+// block.  The attention kernels therefore take two-term (hi + lo) operands
+// on every block pair where a value of the query block or of the key block
+// (its K or V rows) exceeds SCALE_FLAG_BF16_BITS in magnitude, and one-term
+// operands elsewhere.  Flag = 1 when some real token of the block holds such
+// a value (padding tokens are ignored: no output may depend on them).
+// Layout (see block_flag_layout): one byte per query block (b*Hq + h)*N + n,
+// one per key block (b*Hkv + h)*N + n (K and V combined), then per KV group
+// b*Hkv + h one word "some query block of the group's query heads is
+// flagged" and one word "some key block of the head is flagged", so a kernel
+// whose head has no flagged block reads no per-pair flag.
+// ---------------------------------------------------------------------------
+constexpr uint32_t SCALE_FLAG_BF16_BITS = 0x4100u;   // 8.0 in bf16
+
+__global__ __launch_bounds__(256) void block_flag_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+                                                         const uint16_t* __restrict__ v, uint8_t* __restrict__ flag_q,
+                                                         uint8_t* __restrict__ flag_kv, int32_t* __restrict__ any_q,
+                                                         int32_t* __restrict__ any_kv,
+                                                         int64_t rows_q, int64_t rows_kv, int N, int D, int Hq,
+                                                         int Hkv, cube_grid grid) {
+    const int lane = threadIdx.x & 63;
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+    if (row >= rows_q + rows_kv) return;                 // whole waves leave together
+    const bool is_q = row < rows_q;
+    const int64_t r = is_q ? row : row - rows_q;
+    const uint64_t real = cube_real_mask(grid, static_cast<int>(r % N), lane);
+    // the block is 64 tokens x D contiguous bf16 values; lane l reads the
+    // 16-byte chunks l, l + 64, ... (chunk c holds token c / (D / 8))
+    const int64_t elems = static_cast<int64_t>(64) * D;
+    const int chunks = 64 * D / 8;
+    uint32_t mx = 0;
+    auto scan = [&](const uint16_t* base) {
+        const uint4* p = reinterpret_cast<const uint4*>(base + r * elems);
+        for (int c = lane; c < chunks; c += 64) {
+            const int tok = c / (D / 8);
+            if (!((real >> tok) & 1)) continue;
+            const uint4 w = p[c];
+            const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t a = u[i] & 0x7fffu, b = (u[i] >> 16) & 0x7fffu;
+                mx = a > mx ? a : mx;
+                mx = b > mx ? b : mx;
+            }
+        }
+    };
+    if (is_q) {
+        scan(q);
+    } else {
+        scan(k);
+        scan(v);
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        const uint32_t o = static_cast<uint32_t>(__shfl_xor(static_cast<int>(mx), off, 64));
+        mx = o > mx ? o : mx;
+    }
+    const bool big = mx > SCALE_FLAG_BF16_BITS;
+    if (lane == 0) {
+        (is_q ? flag_q : flag_kv)[r] = big ? 1 : 0;
+        if (big) {   // every writer stores the same value: the result does not depend on their order
+            const int64_t bh = r / N;
+            if (is_q) any_q[(bh / Hq) * Hkv + (bh % Hq) / (Hq / Hkv)] = 1;
+            else any_kv[bh] = 1;
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void zero_i32_kernel(int32_t* __restrict__ p, int64_t n) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0;
+}
+
+static size_t flag_align(size_t x) { return (x + 255) / 256 * 256; }
+
+// Each array starts on a 256-byte boundary, so the kernels' 32-bit reads of
+// the word holding a flag byte stay aligned and inside the array's span.
+block_flag_layout block_flags_at(void* base, int64_t rows_q, int64_t rows_kv, int64_t groups) {
+    block_flag_layout f;
+    char* b = static_cast<char*>(base);
+    f.q = reinterpret_cast<uint8_t*>(b);
+    f.kv = reinterpret_cast<uint8_t*>(b + flag_align(rows_q));
+    f.any_q = reinterpret_cast<int32_t*>(b + flag_align(rows_q) + flag_align(rows_kv));
+    f.any_kv = f.any_q + groups;
+    return f;
+}
+
+size_t block_flags_bytes(int64_t rows_q, int64_t rows_kv, int64_t groups) {
+    return flag_align(rows_q) + flag_align(rows_kv) + flag_align(8 * groups);
+}
+
+hipError_t launch_block_flags(const void* q, const void* k, const void* v, const block_flag_layout& f, int64_t rows_q,
+                              int64_t rows_kv, int N, int D, int Hq, int Hkv, const cube_grid& cg, hipStream_t s) {
+    const int64_t rows = rows_q + rows_kv;
+    if (rows <= 0) return hipSuccess;
+    const int64_t groups = rows_kv / N;
+    hipLaunchKernelGGL(zero_i32_kernel, dim3(static_cast<unsigned>((2 * groups + 255) / 256)), dim3(256), 0, s,
+                       f.any_q, 2 * groups);
+    hipLaunchKernelGGL(block_flag_kernel, dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, s,
+                       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                       static_cast<const uint16_t*>(v), f.q, f.kv, f.any_q, f.any_kv, rows_q, rows_kv, N, D, Hq, Hkv,
+                       cg);
+    return hipGetLastError();
+}
+
+}  // namespace vsa2

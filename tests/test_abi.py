@@ -124,10 +124,13 @@ def test_null_and_alignment_checks():
     assert vsa2.STATUS_NAMES[vsa2.vsa2_pool(p, 4, FAKE, 2, 2, 2, MISALIGNED, None)] == "VSA2_ERR_ALIGN"
     assert vsa2.STATUS_NAMES[vsa2.vsa2_pool(p, 4, FAKE, 3, 2, 2, FAKE, None)] == "VSA2_ERR_SHAPE"
     assert vsa2.STATUS_NAMES[vsa2.vsa2_pool(None, 4, FAKE, 2, 2, 2, FAKE, None)] == "VSA2_ERR_NULL"
-    # bwd needs a workspace for the per-query Delta
-    st = vsa2.vsa2_attn_bwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, 1,
+    # bwd needs a workspace for the per-query Delta, and the forward's o_lo
+    st = vsa2.vsa2_attn_bwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1,
                             FAKE, FAKE, FAKE, None, 0, None)
     assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_WORKSPACE"
+    st = vsa2.vsa2_attn_bwd(p, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, 1,
+                            FAKE, FAKE, FAKE, FAKE, 1 << 40, None)
+    assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_NULL"
 
 
 def test_forward_needs_its_work_order_workspace():
@@ -159,23 +162,30 @@ def test_staged_backward_argument_checks():
     p = good()
     names = vsa2.STATUS_NAMES
     big = 1 << 40
-    assert names[vsa2.vsa2_attn_bwd_prep(p, FAKE, FAKE, None, FAKE, None, 0, None)] == "VSA2_ERR_WORKSPACE"
-    assert names[vsa2.vsa2_attn_bwd_prep(p, None, FAKE, None, FAKE, FAKE, big, None)] == "VSA2_ERR_NULL"
-    assert names[vsa2.vsa2_attn_bwd_prep(p, FAKE, FAKE, MISALIGNED, FAKE, FAKE, big, None)] == "VSA2_ERR_ALIGN"
-    assert names[vsa2.vsa2_attn_bwd_prep(None, FAKE, FAKE, None, FAKE, FAKE, big, None)] == "VSA2_ERR_NULL"
-    assert names[vsa2.vsa2_attn_bwd_dkdv(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 0, FAKE, None, FAKE, big,
+    F5 = (FAKE,) * 5
+    # prep(p, q, k, v, o, lse, o_lo, dout, ws, ws_bytes, stream)
+    assert names[vsa2.vsa2_attn_bwd_prep(p, *F5, FAKE, FAKE, None, 0, None)] == "VSA2_ERR_WORKSPACE"
+    assert names[vsa2.vsa2_attn_bwd_prep(p, *F5, None, FAKE, FAKE, big, None)] == "VSA2_ERR_NULL"
+    assert names[vsa2.vsa2_attn_bwd_prep(p, None, *F5[1:], FAKE, FAKE, FAKE, big, None)] == "VSA2_ERR_NULL"
+    assert names[vsa2.vsa2_attn_bwd_prep(p, *F5, MISALIGNED, FAKE, FAKE, big, None)] == "VSA2_ERR_ALIGN"
+    assert names[vsa2.vsa2_attn_bwd_prep(p, FAKE, MISALIGNED, *F5[2:], FAKE, FAKE, FAKE, big,
+                                         None)] == "VSA2_ERR_ALIGN"
+    assert names[vsa2.vsa2_attn_bwd_prep(None, *F5, FAKE, FAKE, FAKE, big, None)] == "VSA2_ERR_NULL"
+    # dkdv(p, q, k, v, dout, kv_ptr, kv_idx, col_cap, dk, dv, ws, ws_bytes, stream)
+    assert names[vsa2.vsa2_attn_bwd_dkdv(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, FAKE, None, FAKE, big,
                                          None)] == "VSA2_ERR_NULL"
-    assert names[vsa2.vsa2_attn_bwd_dkdv(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, -1, 0, FAKE, FAKE, FAKE, big,
+    assert names[vsa2.vsa2_attn_bwd_dkdv(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, -1, FAKE, FAKE, FAKE, big,
                                          None)] == "VSA2_ERR_CAPACITY"
-    assert names[vsa2.vsa2_attn_bwd_dkdv(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, FAKE, MISALIGNED, FAKE,
+    assert names[vsa2.vsa2_attn_bwd_dkdv(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, FAKE, MISALIGNED, FAKE,
                                          big, None)] == "VSA2_ERR_ALIGN"
-    assert names[vsa2.vsa2_attn_bwd_dkdv(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 0, FAKE, FAKE, FAKE, 0,
+    assert names[vsa2.vsa2_attn_bwd_dkdv(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, FAKE, FAKE, FAKE, 0,
                                          None)] == "VSA2_ERR_WORKSPACE"
-    assert names[vsa2.vsa2_attn_bwd_dq(p, FAKE, FAKE, FAKE, FAKE, FAKE, None, 1, 0, FAKE, FAKE, big,
+    # dq(p, q, k, v, dout, row_ptr, col_idx, col_cap, dq, ws, ws_bytes, stream)
+    assert names[vsa2.vsa2_attn_bwd_dq(p, FAKE, FAKE, FAKE, FAKE, FAKE, None, 1, FAKE, FAKE, big,
                                        None)] == "VSA2_ERR_NULL"
-    assert names[vsa2.vsa2_attn_bwd_dq(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 0, MISALIGNED, FAKE, big,
+    assert names[vsa2.vsa2_attn_bwd_dq(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, MISALIGNED, FAKE, big,
                                        None)] == "VSA2_ERR_ALIGN"
-    assert names[vsa2.vsa2_attn_bwd_dq(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 0, FAKE, None, 0,
+    assert names[vsa2.vsa2_attn_bwd_dq(p, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, FAKE, None, 0,
                                        None)] == "VSA2_ERR_WORKSPACE"
 
 

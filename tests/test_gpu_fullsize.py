@@ -33,15 +33,15 @@ def run(request):
     print("\n[full-size %s] %s %s" % (w.name, p, w.select), flush=True)
     x = make_inputs(w, with_grad=True)
     dev = {k: _dev(v) for k, v in x.items()}
-    comp = w.skewed            # large-norm cube means: compensated products
     q_r = vsa2.pool(p, dev["q"], (p.Rt, p.Rh, p.Rw))
     k_r = vsa2.pool(p, dev["k"], (p.Rt, p.Rh, p.Rw))
     r = vsa2.route(p, w.select, q_r, k_r, with_scores=True)
     # with text tokens the attention runs on the joint lists
     a = vsa2.joint_lists(p, r) if p.text_len else r
-    f = vsa2.attn_fwd(p, dev["q"], dev["k"], dev["v"], a["row_ptr"], a["col_idx"], compensated=comp)
+    # a training forward (it keeps O's remainder) where a backward follows
+    f = vsa2.attn_fwd(p, dev["q"], dev["k"], dev["v"], a["row_ptr"], a["col_idx"], training=w.backward)
     o, lse = f[0], f[1]
-    o_lo = f[2] if comp else None
+    o_lo = f[2] if w.backward else None
     g = None
     if w.backward:
         g = vsa2.attn_bwd(p, dev["q"], dev["k"], dev["v"], o, lse, dev["do"], a["row_ptr"],
@@ -105,6 +105,20 @@ def _sample_rows(p, n, seed, heads=None, joint=False):
     return np.sort(rows).astype(np.int64)
 
 
+def _targeted_rows(ptr, longest=4):
+    """Rows of a CSR (or CSC) pointer array that stress the kernels: the
+    `longest` longest and the shortest rows, and the first and last row of
+    each of the 8 contiguous XCD ranges the launch maps rows to."""
+    ptr = np.asarray(ptr, np.int64)
+    n = ptr.size - 1
+    ln = np.diff(ptr)
+    order = np.argsort(-ln, kind="stable")
+    q, r = divmod(n, 8)
+    cuts = [x * q + min(x, r) for x in range(9)]
+    edges = [c for a, b in zip(cuts[:-1], cuts[1:]) if b > a for c in (a, b - 1)]
+    return np.union1d(np.concatenate([order[:longest], [int(np.argmin(ln))], edges]), []).astype(np.int64)
+
+
 def test_router_rows_against_oracle(run):
     p, w, x = run["p"], run["w"], run["x"]
     if w.select.mode == 2:
@@ -129,7 +143,7 @@ def test_router_rows_against_oracle(run):
 
 def test_forward_rows_against_oracle(run):
     p, x = run["p"], run["x"]
-    rows = _sample_rows(p, 16, 2, joint=True)
+    rows = np.union1d(_sample_rows(p, 16, 2, joint=True), _targeted_rows(run["arp"]))
     o_ref, lse_ref = oracle.attn_fwd(x["q"], x["k"], x["v"], p, run["arp"], run["aci"], rows)
     o = to_np(run["o"]).reshape(-1, p.B, p.head_dim)[rows]
     lse = run["lse"].cpu().numpy().reshape(-1, p.B)[rows]
@@ -142,10 +156,17 @@ def test_backward_rows_against_oracle(run):
     if not w.backward:
         pytest.skip("forward-only workload")
     dq, dk, dv = run["g"]
-    rows = _sample_rows(p, 8, 3, joint=True)
+    # random rows and key blocks, plus the longest and shortest lists and the
+    # rows at the XCD-range edges of the launches (CSR rows for dQ, CSC rows
+    # for dK/dV)
+    rows = np.union1d(_sample_rows(p, 8, 3, joint=True), _targeted_rows(run["arp"]))
     dq_ref = oracle.attn_bwd_dq(x["q"], x["k"], x["v"], x["do"], p, run["arp"], run["aci"], rows)
     assert_values(to_np(dq).reshape(-1, p.B, p.head_dim)[rows], dq_ref, "dQ (sampled rows)")
-    kvrows = _sample_rows(p, 4, 4, heads=p.heads_kv, joint=True)
+    kvp = run["a"]["kv_ptr"].cpu().numpy()
+    kvrows = np.union1d(_sample_rows(p, 32, 4, heads=p.heads_kv, joint=True), _targeted_rows(kvp))
+    indeg = np.diff(kvp)[kvrows]
+    print("dK/dV: %d key blocks, in-degree %d..%d (max over all %d)" % (kvrows.size, indeg.min(), indeg.max(),
+                                                                      np.diff(kvp).max()))
     dk_ref, dv_ref = oracle.attn_bwd_dkdv(x["q"], x["k"], x["v"], x["do"], p, run["arp"], run["aci"],
                                           kvrows)
     assert_values(to_np(dk).reshape(-1, p.B, p.head_dim)[kvrows], dk_ref, "dK (sampled blocks)")
@@ -161,7 +182,7 @@ def test_repeatable_and_fully_written(run):
     lse2 = torch.full_like(run["lse"], float("nan"))
     lo2 = torch.full_like(dev["q"], float("nan")) if comp else None
     vsa2.attn_fwd(p, dev["q"], dev["k"], dev["v"], r["row_ptr"], r["col_idx"], o=o2, lse=lse2,
-                  compensated=comp, o_lo=lo2)
+                  training=comp, o_lo=lo2)
     pairs = [(run["o"], o2), (run["lse"], lse2)] + ([(run["o_lo"], lo2)] if comp else [])
     if w.backward:
         g2 = [torch.full_like(t, float("nan")) for t in run["g"]]
