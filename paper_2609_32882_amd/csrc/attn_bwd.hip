@@ -192,147 +192,156 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
         q_cur = qrow_of(scalar_load_i32(kv_idx + entry(0)));
         issue(q_cur, 0);
     }
-    for (int64_t j = 0; j < cnt; ++j) {
-        const int buf = static_cast<int>(j & 1);
-        const bool has_next = j + 1 < cnt;
-        // the next list entry, and the current query block's flag with it
-        int64_t q_next = -1;
-        bool big = all_big;
-        if (SPLIT && some_big && q_cur >= 0) {
-            int32_t ent = -1, w = 0;
-            if (has_next) scalar_load2_i32(kv_idx + entry(j + 1), byte_word(fl.q, q_cur), ent, w);
-            else w = scalar_load_i32(byte_word(fl.q, q_cur));
-            q_next = has_next ? qrow_of(ent) : -1;
-            big = byte_of(w, q_cur);
-        } else if (has_next) {
-            q_next = qrow_of(scalar_load_i32(kv_idx + entry(j + 1)));
-        }
-        // One barrier per block: after it, this block's copies (the only
-        // ones outstanding) are visible and both waves are done with the
-        // previous block, whose buffer then receives the next block's copies.
-        vm_wait<0>();
-        wg_barrier();
-        if (has_next) issue(q_next, buf ^ 1);
-        const char* qt = q_lds[buf];
-        const char* ot = o_lds[buf];
-        const float* st = st_lds[buf];
-        // Software pipeline over the two 32-query tiles of the block:
-        //   S/dP(tile 0) | S/dP(tile 1) + P,dS(tile 0) |
-        //   dV/dK(tile 0) + P,dS(tile 1) | dV/dK(tile 1)
-        // so the exponentials and the dS arithmetic of one tile issue
-        // while the other tile's MFMAs run (one wave per SIMD: the wave's
-        // own independent work is all there is to overlap).  LDS operand
-        // fragments are requested one step ahead of their MFMAs;
-        // lds_order keeps the compiler from moving work across steps.
-        // two (wave-uniform): P and dS as hi + lo, a second dV / dK product
-        // with the lo terms.  One code path with the lo steps behind scalar
-        // branches: two inlined variants of the loop raise the kernel's
-        // register allocation for both.
-        auto pair = [&](bool two) {
-            constexpr int NB = KS / 2;           // S/dP steps per tile (2 k-steps each)
-            constexpr int NU = 2 * MT;           // dV/dK steps per tile
-            constexpr int EV = 16 / NB;          // P,dS elements per S/dP step
-            constexpr int EU = 16 / NU;          // P,dS elements per dV/dK step
-            // S starts from 0; dP starts from -Delta of its query (element i
-            // of tile t is query 32t + 16(i/8) + 8half + i%8), so the product
-            // leaves dP - Delta
-            f32x16_t s[2], dp[2];
-#pragma unroll
-            for (int t = 0; t < 2; ++t)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) s[t][i] = 0.f;
-            auto dp_init = [&](int t) {
-#pragma unroll
-                for (int i = 0; i < 16; ++i) dp[t][i] = st[64 + t * 32 + (i >> 3) * 16 + half * 8 + (i & 7)];
-            };
-            dp_init(0);
-            F pb[2][2], db[2][2], pl[2][SPLIT ? 2 : 1], dl[2][SPLIT ? 2 : 1];
-            // scaled LSE of the elements of softmax_grad call c (calls
-            // 0..NB-1: tile 0 in groups of EV; NB..NB+NU-1: tile 1 in groups
-            // of EU), read one step ahead into a double buffer
-            constexpr int EMAX = EV > EU ? EV : EU;
-            float stv[2][EMAX];
-            auto st_load = [&](int c) {
-                const int t = c < NB ? 0 : 1;
-                const int i0 = c < NB ? c * EV : (c - NB) * EU;
-                const int n = c < NB ? EV : EU;
-#pragma unroll
-                for (int i = i0; i < i0 + n; ++i) stv[c & 1][i - i0] = st[t * 32 + (i >> 3) * 16 + half * 8 + (i & 7)];
-            };
-            // P and dS of elements [i0, i0 + n) of tile t, in place (s <- P,
-            // dp <- dS); element i is query 32t + 16(i/8) + 8half + i%8.
-            // A group of 8 finished elements becomes a fragment pair.
-            auto softmax_grad = [&](int t, int i0, int n) {
-                const int c = t == 0 ? i0 / EV : NB + i0 / EU;
-                if (c + 1 < NB + NU) st_load(c + 1);
-#pragma unroll
-                for (int i = i0; i < i0 + n; ++i) {
-                    const float pv = fast_exp2(s[t][i] * c_log2 - stv[c & 1][i - i0]);
-                    s[t][i] = pv;
-                    dp[t][i] = pv * dp[t][i];
-                }
-                if (((i0 + n) & 7) == 0) {
-                    const int h = (i0 + n - 1) >> 3;
-                    float xp[8], xd[8];
-#pragma unroll
-                    for (int i = 0; i < 8; ++i) { xp[i] = s[t][8 * h + i]; xd[i] = dp[t][8 * h + i]; }
-                    if (SPLIT && two) {
-                        pack_frag_hilo(pb[t][h], pl[t][SPLIT ? h : 0], xp);
-                        pack_frag_hilo(db[t][h], dl[t][SPLIT ? h : 0], xd);
-                    } else {
-                        pack_frag(pb[t][h], xp);
-                        pack_frag(db[t][h], xd);
+    // The walk over the list, in two versions: FL (some pair of this row may
+    // touch a large-magnitude block) reads per-pair flags and branches to the
+    // two-term steps; the other has no flag reads or branches, so its
+    // pipeline is scheduled as one piece.
+    auto walk = [&](auto flagged) {
+        constexpr bool FL = decltype(flagged)::value;
+        for (int64_t j = 0; j < cnt; ++j) {
+            const int buf = static_cast<int>(j & 1);
+            const bool has_next = j + 1 < cnt;
+            // the next list entry, and the current query block's flag with it
+            int64_t q_next = -1;
+            bool big = FL && all_big;
+            if (FL && some_big && q_cur >= 0) {
+                int32_t ent = -1, w = 0;
+                if (has_next) scalar_load2_i32(kv_idx + entry(j + 1), byte_word(fl.q, q_cur), ent, w);
+                else w = scalar_load_i32(byte_word(fl.q, q_cur));
+                q_next = has_next ? qrow_of(ent) : -1;
+                big = byte_of(w, q_cur);
+            } else if (has_next) {
+                q_next = qrow_of(scalar_load_i32(kv_idx + entry(j + 1)));
+            }
+            // One barrier per block: after it, this block's copies (the only
+            // ones outstanding) are visible and both waves are done with the
+            // previous block, whose buffer then receives the next block's copies.
+            vm_wait<0>();
+            wg_barrier();
+            if (has_next) issue(q_next, buf ^ 1);
+            const char* qt = q_lds[buf];
+            const char* ot = o_lds[buf];
+            const float* st = st_lds[buf];
+            // Software pipeline over the two 32-query tiles of the block:
+            //   S/dP(tile 0) | S/dP(tile 1) + P,dS(tile 0) |
+            //   dV/dK(tile 0) + P,dS(tile 1) | dV/dK(tile 1)
+            // so the exponentials and the dS arithmetic of one tile issue
+            // while the other tile's MFMAs run (one wave per SIMD: the wave's
+            // own independent work is all there is to overlap).  LDS operand
+            // fragments are requested one step ahead of their MFMAs;
+            // lds_order keeps the compiler from moving work across steps.
+            // two (wave-uniform): P and dS as hi + lo, a second dV / dK product
+            // with the lo terms.  One code path with the lo steps behind scalar
+            // branches: two inlined variants of the loop raise the kernel's
+            // register allocation for both.
+            auto pair = [&](bool two) {
+                constexpr int NB = KS / 2;           // S/dP steps per tile (2 k-steps each)
+                constexpr int NU = 2 * MT;           // dV/dK steps per tile
+                constexpr int EV = 16 / NB;          // P,dS elements per S/dP step
+                constexpr int EU = 16 / NU;          // P,dS elements per dV/dK step
+                // S starts from 0; dP starts from -Delta of its query (element i
+                // of tile t is query 32t + 16(i/8) + 8half + i%8), so the product
+                // leaves dP - Delta
+                f32x16_t s[2], dp[2];
+    #pragma unroll
+                for (int t = 0; t < 2; ++t)
+    #pragma unroll
+                    for (int i = 0; i < 16; ++i) s[t][i] = 0.f;
+                auto dp_init = [&](int t) {
+    #pragma unroll
+                    for (int i = 0; i < 16; ++i) dp[t][i] = st[64 + t * 32 + (i >> 3) * 16 + half * 8 + (i & 7)];
+                };
+                dp_init(0);
+                F pb[2][2], db[2][2], pl[2][SPLIT ? 2 : 1], dl[2][SPLIT ? 2 : 1];
+                // scaled LSE of the elements of softmax_grad call c (calls
+                // 0..NB-1: tile 0 in groups of EV; NB..NB+NU-1: tile 1 in groups
+                // of EU), read one step ahead into a double buffer
+                constexpr int EMAX = EV > EU ? EV : EU;
+                float stv[2][EMAX];
+                auto st_load = [&](int c) {
+                    const int t = c < NB ? 0 : 1;
+                    const int i0 = c < NB ? c * EV : (c - NB) * EU;
+                    const int n = c < NB ? EV : EU;
+    #pragma unroll
+                    for (int i = i0; i < i0 + n; ++i) stv[c & 1][i - i0] = st[t * 32 + (i >> 3) * 16 + half * 8 + (i & 7)];
+                };
+                // P and dS of elements [i0, i0 + n) of tile t, in place (s <- P,
+                // dp <- dS); element i is query 32t + 16(i/8) + 8half + i%8.
+                // A group of 8 finished elements becomes a fragment pair.
+                auto softmax_grad = [&](int t, int i0, int n) {
+                    const int c = t == 0 ? i0 / EV : NB + i0 / EU;
+                    if (c + 1 < NB + NU) st_load(c + 1);
+    #pragma unroll
+                    for (int i = i0; i < i0 + n; ++i) {
+                        const float pv = fast_exp2(s[t][i] * c_log2 - stv[c & 1][i - i0]);
+                        s[t][i] = pv;
+                        dp[t][i] = pv * dp[t][i];
                     }
+                    if (((i0 + n) & 7) == 0) {
+                        const int h = (i0 + n - 1) >> 3;
+                        float xp[8], xd[8];
+    #pragma unroll
+                        for (int i = 0; i < 8; ++i) { xp[i] = s[t][8 * h + i]; xd[i] = dp[t][8 * h + i]; }
+                        if (SPLIT && two) {
+                            pack_frag_hilo(pb[t][h], pl[t][SPLIT ? h : 0], xp);
+                            pack_frag_hilo(db[t][h], dl[t][SPLIT ? h : 0], xd);
+                        } else {
+                            pack_frag(pb[t][h], xp);
+                            pack_frag(db[t][h], xd);
+                        }
+                    }
+                };
+                F fa[2][4];
+                auto fetch_sd = [&](F* f, int t, int bi) {
+                    const int row = t * 32 + (lane & 31);
+                    lds_frag_s<RB>(f[0], qt, row, 32 * bi + half * 8);
+                    lds_frag_s<RB>(f[1], ot, row, 32 * bi + half * 8);
+                    lds_frag_s<RB>(f[2], qt, row, 32 * bi + 16 + half * 8);
+                    lds_frag_s<RB>(f[3], ot, row, 32 * bi + 16 + half * 8);
+                };
+                F ta[2][2];
+                auto fetch_dk = [&](F* f, int t, int u) {
+                    const int kk = 2 * t + u / MT, mt = u % MT;
+                    lds_frag_tr<RB, true>(f[0], ot, mt * 32, kk * 16);
+                    lds_frag_tr<RB, true>(f[1], qt, mt * 32, kk * 16);
+                };
+                // S = Q K^T and dP = dO V^T, both tiles
+                fetch_sd(fa[0], 0, 0);
+    #pragma unroll
+                for (int k = 0; k < 2 * NB; ++k) {
+                    const int t = k / NB, bi = k % NB;
+                    if (k + 1 < 2 * NB) fetch_sd(fa[(k + 1) & 1], (k + 1) / NB, (k + 1) % NB);
+                    else fetch_dk(ta[0], 0, 0);
+                    if (k == NB - 1) dp_init(1);
+                    lds_order();
+                    mma(s[t], fa[k & 1][0], kf[2 * bi]);
+                    mma(dp[t], fa[k & 1][1], vf[2 * bi]);
+                    mma(s[t], fa[k & 1][2], kf[2 * bi + 1]);
+                    mma(dp[t], fa[k & 1][3], vf[2 * bi + 1]);
+                    if (k == NB - 1) st_load(0);
+                    if (t == 1) softmax_grad(0, bi * EV, EV);
+                }
+                // dV^T += dO^T P and dK^T += Q^T dS, tile by tile (dO^T and Q^T
+                // read transposed from the row-major tiles)
+    #pragma unroll
+                for (int k = 0; k < 2 * NU; ++k) {
+                    const int t = k / NU, u = k % NU;
+                    if (k + 1 < 2 * NU) fetch_dk(ta[(k + 1) & 1], (k + 1) / NU, (k + 1) % NU);
+                    lds_order();
+                    const int h = u / MT, mt = u % MT;
+                    mma(acc_v[mt], ta[k & 1][0], pb[t][h]);
+                    if (SPLIT && two) mma(acc_v[mt], ta[k & 1][0], pl[t][SPLIT ? h : 0]);
+                    mma(acc_k[mt], ta[k & 1][1], db[t][h]);
+                    if (SPLIT && two) mma(acc_k[mt], ta[k & 1][1], dl[t][SPLIT ? h : 0]);
+                    if (t == 0) softmax_grad(1, u * EU, EU);
                 }
             };
-            F fa[2][4];
-            auto fetch_sd = [&](F* f, int t, int bi) {
-                const int row = t * 32 + (lane & 31);
-                lds_frag_s<RB>(f[0], qt, row, 32 * bi + half * 8);
-                lds_frag_s<RB>(f[1], ot, row, 32 * bi + half * 8);
-                lds_frag_s<RB>(f[2], qt, row, 32 * bi + 16 + half * 8);
-                lds_frag_s<RB>(f[3], ot, row, 32 * bi + 16 + half * 8);
-            };
-            F ta[2][2];
-            auto fetch_dk = [&](F* f, int t, int u) {
-                const int kk = 2 * t + u / MT, mt = u % MT;
-                lds_frag_tr<RB, true>(f[0], ot, mt * 32, kk * 16);
-                lds_frag_tr<RB, true>(f[1], qt, mt * 32, kk * 16);
-            };
-            // S = Q K^T and dP = dO V^T, both tiles
-            fetch_sd(fa[0], 0, 0);
-#pragma unroll
-            for (int k = 0; k < 2 * NB; ++k) {
-                const int t = k / NB, bi = k % NB;
-                if (k + 1 < 2 * NB) fetch_sd(fa[(k + 1) & 1], (k + 1) / NB, (k + 1) % NB);
-                else fetch_dk(ta[0], 0, 0);
-                if (k == NB - 1) dp_init(1);
-                lds_order();
-                mma(s[t], fa[k & 1][0], kf[2 * bi]);
-                mma(dp[t], fa[k & 1][1], vf[2 * bi]);
-                mma(s[t], fa[k & 1][2], kf[2 * bi + 1]);
-                mma(dp[t], fa[k & 1][3], vf[2 * bi + 1]);
-                if (k == NB - 1) st_load(0);
-                if (t == 1) softmax_grad(0, bi * EV, EV);
-            }
-            // dV^T += dO^T P and dK^T += Q^T dS, tile by tile (dO^T and Q^T
-            // read transposed from the row-major tiles)
-#pragma unroll
-            for (int k = 0; k < 2 * NU; ++k) {
-                const int t = k / NU, u = k % NU;
-                if (k + 1 < 2 * NU) fetch_dk(ta[(k + 1) & 1], (k + 1) / NU, (k + 1) % NU);
-                lds_order();
-                const int h = u / MT, mt = u % MT;
-                mma(acc_v[mt], ta[k & 1][0], pb[t][h]);
-                if (SPLIT && two) mma(acc_v[mt], ta[k & 1][0], pl[t][SPLIT ? h : 0]);
-                mma(acc_k[mt], ta[k & 1][1], db[t][h]);
-                if (SPLIT && two) mma(acc_k[mt], ta[k & 1][1], dl[t][SPLIT ? h : 0]);
-                if (t == 0) softmax_grad(1, u * EU, EU);
-            }
-        };
-        if (q_cur >= 0) pair(big);
-        q_cur = q_next;
-    }
+            if (q_cur >= 0) pair(FL && big);
+            q_cur = q_next;
+        }
+    };
+    if (SPLIT && (all_big || some_big)) walk(std::true_type{});
+    else walk(std::false_type{});
 
     // lane holds key column (lane & 31) and d = 32mt + 8(v/4) + 4half + v%4
     T* krow_k = dk + ktok * D;
