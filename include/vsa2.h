@@ -249,6 +249,31 @@ vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, c
                           hipStream_t stream);
 
 /*
+ * vsa2_attn_fwd_noalloc - vsa2_attn_fwd for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops or harnesses
+ * that forbid hipMalloc): the same computation and results, bit for bit,
+ * with the call's workspace (work order and block flags) in a fixed array
+ * of the library instead of a caller buffer.  The call allocates nothing.
+ *   Arguments as for vsa2_attn_fwd, without ws / ws_bytes; the stream's
+ *   device must be the current device.
+ *   Limit: the array holds VSA2_NOALLOC_SCRATCH_BYTES (2 MiB) per GPU, for
+ *   as long as the process runs; a problem whose forward workspace
+ *   (vsa2_attn_workspace(p, 0)) is larger returns VSA2_ERR_WORKSPACE before
+ *   any device work (about 6 bytes per query-block row: up to about
+ *   349,000 rows batch * heads_q * blocks with heads_kv = heads_q).
+ *   Every call on one GPU uses that GPU's one array: calls that overlap on
+ *   one GPU (concurrent streams, or two graphs replayed at once) race and
+ *   must be ordered by the caller.  Each call rewrites all of the array it
+ *   reads, so what an earlier call left there does not matter.
+ * Errors: as for vsa2_attn_fwd; VSA2_ERR_WORKSPACE for a problem beyond the
+ *   limit; VSA2_ERR_HIP if the array's device address cannot be obtained.
+ */
+#define VSA2_NOALLOC_SCRATCH_BYTES ((size_t)2 << 20)
+vsa2_status vsa2_attn_fwd_noalloc(const vsa2_problem* p, const void* q, const void* k, const void* v,
+                                  const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap,
+                                  void* o, float* lse, void* o_lo, hipStream_t stream);
+
+/*
  * vsa2_attn_bwd - gradients of vsa2_attn_fwd with the block lists fixed
  * (no gradient reaches the router, Sec. 2.1).  With p the softmax row of
  * query l over its gathered keys:

@@ -28,7 +28,7 @@ VSA2_SEL_TOPK, VSA2_SEL_MASS, VSA2_SEL_SEQ_TOPK = 0, 1, 2
 
 # Every symbol include/vsa2.h declares.
 EXPORTS = ("vsa2_status_str", "vsa2_pool", "vsa2_route_capacity", "vsa2_route_workspace",
-           "vsa2_route", "vsa2_attn_workspace", "vsa2_attn_fwd", "vsa2_attn_bwd",
+           "vsa2_route", "vsa2_attn_workspace", "vsa2_attn_fwd", "vsa2_attn_fwd_noalloc", "vsa2_attn_bwd",
            "vsa2_attn_bwd_prep", "vsa2_attn_bwd_dkdv", "vsa2_attn_bwd_dq",
            "vsa2_coarse_fwd", "vsa2_coarse_bwd", "vsa2_gate_merge", "vsa2_gate_merge_bwd",
            "vsa2_joint_capacity", "vsa2_joint_workspace", "vsa2_joint_lists", "vsa2_unpool_add",
@@ -73,6 +73,7 @@ def _lib():
         L.vsa2_route.argtypes = [pp, ps, P, P, P, P, i64, P, P, P, P, sz, P]
         L.vsa2_attn_workspace.argtypes = [pp, i32, ctypes.POINTER(sz)]
         L.vsa2_attn_fwd.argtypes = [pp, P, P, P, P, P, i64, P, P, P, P, sz, P]
+        L.vsa2_attn_fwd_noalloc.argtypes = [pp, P, P, P, P, P, i64, P, P, P, P]
         L.vsa2_attn_bwd.argtypes = [pp, P, P, P, P, P, P, P, P, P, P, P, i64, P, P, P, P, sz, P]
         L.vsa2_attn_bwd_prep.argtypes = [pp, P, P, P, P, P, P, P, P, sz, P]
         L.vsa2_attn_bwd_dkdv.argtypes = [pp, P, P, P, P, P, P, i64, P, P, P, sz, P]
@@ -145,6 +146,10 @@ def vsa2_attn_workspace(p, pass_):
 def vsa2_attn_fwd(p, q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, ws, ws_bytes, stream=0):
     return _lib().vsa2_attn_fwd(_ref(p), q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, ws,
                                 ws_bytes, stream)
+
+
+def vsa2_attn_fwd_noalloc(p, q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, stream=0):
+    return _lib().vsa2_attn_fwd_noalloc(_ref(p), q, k, v, row_ptr, col_idx, col_cap, o, lse, o_lo, stream)
 
 
 def vsa2_attn_bwd(p, q, k, v, o, lse, o_lo, dout, row_ptr, col_idx, kv_ptr, kv_idx, col_cap, dq,

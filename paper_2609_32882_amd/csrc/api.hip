@@ -6,6 +6,8 @@
 
 #include <math.h>
 
+#include <mutex>
+
 #include "internal.hpp"
 
 namespace {
@@ -256,6 +258,63 @@ vsa2_status vsa2_attn_fwd(const vsa2_problem* p, const void* q, const void* k, c
         return VSA2_ERR_ALIGN;
     if (!ws || ws_bytes < fwd_ws_bytes(s, p)) return VSA2_ERR_WORKSPACE;
     if (reinterpret_cast<uintptr_t>(ws) % kAlign) return VSA2_ERR_ALIGN;
+    VSA2_TRY_HIP(vsa2::launch_attn_fwd(p->dtype, p->head_dim, q, k, v, row_ptr, col_idx, col_cap, o, lse,
+                                       o_lo, ws, p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.Nj),
+                                       grid_of(p), stream));
+    return VSA2_OK;
+}
+
+// ---------------------------------------------------------------------------
+// vsa2_attn_fwd_noalloc: the forward with its workspace in a fixed device
+// array of the library.  Each GPU holds its own copy of `scratch` until the
+// process ends; its address on a device comes from hipGetSymbolAddress,
+// taken once per device with that device current and kept here (in host
+// code the array's name is not a device address, so it is never passed to
+// a kernel or a copy).
+// ---------------------------------------------------------------------------
+namespace {
+
+__device__ __align__(256) unsigned char scratch[VSA2_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The scratch array of the current device (set up on the first call there).
+vsa2_status scratch_of_current_device(void** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return VSA2_ERR_HIP;
+    if (dev < 0 || dev >= kMaxDevices) return VSA2_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return VSA2_ERR_HIP;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return VSA2_OK;
+}
+
+}  // namespace
+
+vsa2_status vsa2_attn_fwd_noalloc(const vsa2_problem* p, const void* q, const void* k, const void* v,
+                                  const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
+                                  float* lse, void* o_lo, hipStream_t stream) {
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if ((st = check_kernel_shape(p, s)) != VSA2_OK) return st;
+    if (!q || !k || !v || !row_ptr || !o || !lse) return VSA2_ERR_NULL;
+    if (!col_idx && col_cap > 0) return VSA2_ERR_NULL;
+    if (col_cap < 0) return VSA2_ERR_CAPACITY;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(o_lo))
+        return VSA2_ERR_ALIGN;
+    if (fwd_ws_bytes(s, p) > VSA2_NOALLOC_SCRATCH_BYTES) return VSA2_ERR_WORKSPACE;
+    void* ws = nullptr;
+    if ((st = scratch_of_current_device(&ws)) != VSA2_OK) return st;
+    // every part of the workspace the forward reads is written earlier in the
+    // same call (work order, block flags; their summary words are cleared by
+    // a fill kernel), so the previous call's contents do not matter
     VSA2_TRY_HIP(vsa2::launch_attn_fwd(p->dtype, p->head_dim, q, k, v, row_ptr, col_idx, col_cap, o, lse,
                                        o_lo, ws, p->batch, p->heads_q, p->heads_kv, static_cast<int>(s.Nj),
                                        grid_of(p), stream));
