@@ -44,6 +44,9 @@ def parse():
                     help="key blocks (dK/dV) in the oracle's timed sample")
     ap.add_argument("--no-coarse", action="store_true",
                     help="skip the separate timing of the coarse branch and gated merge")
+    ap.add_argument("--dq-atomic-probe", action="store_true",
+                    help="also time vsa2_dq_atomic_probe: the fp32 atomic dQ accumulation a fused "
+                         "single-kernel backward would need, without its arithmetic")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, copy a buffer of this size once (reference kernel "
                          "for scaling hardware byte counters)")
@@ -185,6 +188,21 @@ def main():
 
     mfma_peak = measure_mfma_peak(vsa2, torch, stream)
 
+    atomic_ms = None
+    if args.dq_atomic_probe:
+        acc = torch.zeros((p.batch, p.heads_q, L, D), dtype=torch.float32, device=dev)
+        ts = []
+        for _ in range(3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            chk("dq_atomic_probe", vsa2.vsa2_dq_atomic_probe(P, a_kp.data_ptr(), a_ki.data_ptr(), a_cap,
+                                                               acc.data_ptr(), sp))
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        atomic_ms = round(float(min(ts[1:])), 4)
+        del acc
+
     if args.calib_copy_mib:
         n = args.calib_copy_mib << 20
         src = torch.empty(n, dtype=torch.uint8, device=dev)
@@ -236,6 +254,7 @@ def main():
         },
         "breakdown_ms": {s: round(stage_ms[s], 4) for s in ("pool", "route", "fwd", "bwd") + stages[3:]},
         "attn_fwd_bwd_ms": round(attn_ms, 4),
+        **({"fused_bwd_dq_atomic_floor_ms": atomic_ms} if atomic_ms is not None else {}),
         "attn_only_tflops": round(attn_tflops, 3),
         "pct_bf16_peak_attn_only": round(100.0 * attn_tflops / peak, 2),
         # the dense MFMA rate measured on this GPU by the library's probe

@@ -443,6 +443,20 @@ vsa2_status vsa2_unpool_add(const vsa2_problem* p, int32_t heads, const void* dx
  */
 vsa2_status vsa2_mfma_peak_probe(int32_t iters, float* sink, int64_t* flops, hipStream_t stream);
 
+/*
+ * vsa2_dq_atomic_probe - a measurement aid, not part of the attention path:
+ * the atomic traffic a fused backward (dK, dV and dQ in one key-stationary
+ * pass, the alternative to the two-kernel backward of vsa2_attn_bwd) would
+ * spend on dQ alone.  For every entry of every key block's transposed list
+ * (kv_ptr, kv_idx from vsa2_route) it adds 1.0 with an fp32 atomic to every
+ * element of the listed query block's 64 x D tile of acc, and does nothing
+ * else; the caller times the launch.
+ *   acc  [batch][Hq][L][D] fp32 device buffer (accumulates entry counts).
+ * Errors: NULL pointers, shape, negative col_cap, misaligned acc.
+ */
+vsa2_status vsa2_dq_atomic_probe(const vsa2_problem* p, const int32_t* kv_ptr, const int32_t* kv_idx,
+                                 int64_t col_cap, float* acc, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -32,7 +32,7 @@ EXPORTS = ("vsa2_status_str", "vsa2_pool", "vsa2_route_capacity", "vsa2_route_wo
            "vsa2_attn_bwd_prep", "vsa2_attn_bwd_dkdv", "vsa2_attn_bwd_dq",
            "vsa2_coarse_fwd", "vsa2_coarse_bwd", "vsa2_gate_merge", "vsa2_gate_merge_bwd",
            "vsa2_joint_capacity", "vsa2_joint_workspace", "vsa2_joint_lists", "vsa2_unpool_add",
-           "vsa2_mfma_peak_probe")
+           "vsa2_mfma_peak_probe", "vsa2_dq_atomic_probe")
 
 
 class vsa2_problem(ctypes.Structure):
@@ -87,6 +87,7 @@ def _lib():
         L.vsa2_joint_workspace.argtypes = [pp, ctypes.POINTER(sz)]
         L.vsa2_joint_lists.argtypes = [pp, P, P, i64, P, P, i64, P, P, P, sz, P]
         L.vsa2_mfma_peak_probe.argtypes = [i32, P, ctypes.POINTER(i64), P]
+        L.vsa2_dq_atomic_probe.argtypes = [pp, P, P, i64, P, P]
         for n in EXPORTS[1:]:
             getattr(L, n).restype = ctypes.c_int
         _L = L
@@ -190,6 +191,10 @@ def vsa2_gate_merge_bwd(p, gate, o_c, dout, do_c, dgate, stream=0):
 
 def vsa2_unpool_add(p, heads, dx_c, Pt, Ph, Pw, dx, stream=0):
     return _lib().vsa2_unpool_add(_ref(p), heads, dx_c, Pt, Ph, Pw, dx, stream)
+
+
+def vsa2_dq_atomic_probe(p, kv_ptr, kv_idx, col_cap, acc, stream=0):
+    return _lib().vsa2_dq_atomic_probe(_ref(p), kv_ptr, kv_idx, col_cap, acc, stream)
 
 
 def vsa2_mfma_peak_probe(iters, sink, stream=0):

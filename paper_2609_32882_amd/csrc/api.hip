@@ -533,4 +533,19 @@ vsa2_status vsa2_mfma_peak_probe(int32_t iters, float* sink, int64_t* flops, hip
     return VSA2_OK;
 }
 
+vsa2_status vsa2_dq_atomic_probe(const vsa2_problem* p, const int32_t* kv_ptr, const int32_t* kv_idx,
+                                 int64_t col_cap, float* acc, hipStream_t stream) {
+    shape s;
+    vsa2_status st = check_problem(p, &s);
+    if (st != VSA2_OK) return st;
+    if ((st = check_kernel_shape(p, s)) != VSA2_OK) return st;
+    if (!kv_ptr || !acc) return VSA2_ERR_NULL;
+    if (!kv_idx && col_cap > 0) return VSA2_ERR_NULL;
+    if (col_cap < 0) return VSA2_ERR_CAPACITY;
+    if (!aligned16(acc)) return VSA2_ERR_ALIGN;
+    VSA2_TRY_HIP(vsa2::launch_dq_atomic_probe(kv_ptr, kv_idx, col_cap, acc, p->batch, p->heads_q, p->heads_kv,
+                                              static_cast<int>(s.Nj), p->head_dim, stream));
+    return VSA2_OK;
+}
+
 }  // extern "C"

@@ -122,136 +122,144 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
         kt.issue(k_lds, kb + static_cast<int64_t>(cc) * 64 * KRB, wave);
         vt_.issue(v_lds, vb + static_cast<int64_t>(cc) * 64 * KRB, wave);
     }
-    for (int64_t j = 0; j < cnt; ++j) {
-        const bool has_next = j + 1 < cnt;
-        // the next list entry, and the current key block's flag with it
-        int c_next = -1;
-        bool big = all_big;
-        if (SPLIT && some_big && c_cur >= 0) {
-            const int64_t fi = kvrow0 + c_cur;
-            int32_t e = -1, w = 0;
-            if (has_next) scalar_load2_i32(col_idx + entry(j + 1), byte_word(fl.kv, fi), e, w);
-            else w = scalar_load_i32(byte_word(fl.kv, fi));
-            c_next = (e >= 0 && e < N) ? e : -1;
-            big = byte_of(w, fi);
-        } else if (has_next) {
-            c_next = block_of(entry(j + 1));
-        }
-        const int64_t nxt_off = static_cast<int64_t>(c_next < 0 ? 0 : c_next) * 64 * KRB;
+    // The walk in two compiled versions: FL (some pair of this row may touch
+    // a large-magnitude block) reads per-pair flags and may take two-term
+    // steps; the other has neither, so its loop is scheduled without them.
+    auto walk = [&](auto flagged) {
+        constexpr bool FL = decltype(flagged)::value;
+        for (int64_t j = 0; j < cnt; ++j) {
+            const bool has_next = j + 1 < cnt;
+            // the next list entry, and the current key block's flag with it
+            int c_next = -1;
+            bool big = FL && all_big;
+            if (FL && some_big && c_cur >= 0) {
+                const int64_t fi = kvrow0 + c_cur;
+                int32_t e = -1, w = 0;
+                if (has_next) scalar_load2_i32(col_idx + entry(j + 1), byte_word(fl.kv, fi), e, w);
+                else w = scalar_load_i32(byte_word(fl.kv, fi));
+                c_next = (e >= 0 && e < N) ? e : -1;
+                big = byte_of(w, fi);
+            } else if (has_next) {
+                c_next = block_of(entry(j + 1));
+            }
+            const int64_t nxt_off = static_cast<int64_t>(c_next < 0 ? 0 : c_next) * 64 * KRB;
 
-        vm_wait<VT::PER_WAVE>();          // this K tile has landed (V may still stream)
-        wg_barrier();
-        // S^T for 64 keys x 32 queries (two 32-key tiles); K fragments are
-        // requested one k-step pair ahead of their products
-        f32x16_t s[2];
-#pragma unroll
-        for (int t2 = 0; t2 < 2; ++t2)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) s[t2][i] = 0.f;
-        {
-            F fa[2][4];
-            auto fetch = [&](F* f, int bi) {
-#pragma unroll
-                for (int x = 0; x < 4; ++x)
-                    lds_frag_s<KRB>(f[x], k_lds, (x & 1) * 32 + (lane & 31), (2 * bi + (x >> 1)) * 16 + half * 8);
-            };
-            fetch(fa[0], 0);
-#pragma unroll
-            for (int bi = 0; bi < KS / 2; ++bi) {
-                if (bi + 1 < KS / 2) fetch(fa[(bi + 1) & 1], bi + 1);
-                lds_order();
-#pragma unroll
-                for (int x = 0; x < 4; ++x) mma(s[x & 1], fa[bi & 1][x], qf[2 * bi + (x >> 1)]);
-            }
-        }
-        wg_barrier();                      // K buffer free
-        if (has_next) kt.issue(k_lds, kb + nxt_off, wave);
-
-        if (c_cur >= 0) {
-            // padding keys of a cut cube: key of entry i of tile t2 is
-            // 32 t2 + 16 (i / 8) + 8 half + i % 8
-            if constexpr (PAD) {        // branch-free: a branch here costs registers
-                const uint64_t kmask = cube_real_mask(grid, c_cur, lane);
-#pragma unroll
-                for (int t2 = 0; t2 < 2; ++t2) {
-                    const uint32_t lm = static_cast<uint32_t>(kmask >> (t2 * 32 + half * 8));
-#pragma unroll
-                    for (int i = 0; i < 16; ++i)
-                        s[t2][i] = ((lm >> ((i >> 3) * 16 + (i & 7))) & 1u) ? s[t2][i] : -INFINITY;
-                }
-            }
-            // Online softmax in log2 units with a lazily updated running max:
-            // the accumulators are rescaled only when the block max exceeds
-            // the running max m by more than 2^8 (any lane of the wave), so
-            // p = 2^(s c - m) <= 256.  O = sum p V / sum p is exact for any m.
-            float mx = -INFINITY;
-#pragma unroll
+            vm_wait<VT::PER_WAVE>();          // this K tile has landed (V may still stream)
+            wg_barrier();
+            // S^T for 64 keys x 32 queries (two 32-key tiles); K fragments are
+            // requested one k-step pair ahead of their products
+            f32x16_t s[2];
+    #pragma unroll
             for (int t2 = 0; t2 < 2; ++t2)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[t2][i]);
-            mx = fmaxf(mx, swap_half(mx)) * c_log2;
-            if (__any(mx > m + 8.0f)) {
-                const float mn = fmaxf(m, mx);
-                const float alpha = fast_exp2(m - mn);
-                l *= alpha;
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) oacc[mt][i] *= alpha;
-                m = mn;
-            }
-            float ps = 0.f;
-#pragma unroll
-            for (int t2 = 0; t2 < 2; ++t2)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const float p = fast_exp2(fmaf(s[t2][i], c_log2, -m));
-                    s[t2][i] = p;
-                    ps += p;
-                }
-            l += ps;
-        }
-        if (has_next) vm_wait<KT::PER_WAVE>(); else vm_wait<0>();   // V tile landed
-        wg_barrier();
-        if (c_cur >= 0) {
-            // O^T += V^T P^T over 4 k-steps of 16 keys: keys 16kk + 8half + (0..7);
-            // V^T fragments are requested one k-step ahead of their products.
-            // On a flagged pair P is split into hi + lo = bf16(P - hi), and a
-            // second pass adds V^T lo (its fragments read again).
-            F pb[4], pl[SPLIT ? 4 : 1];
-            const bool two = SPLIT && big;
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk) {
-                float pv8[8];
-#pragma unroll
-                for (int i = 0; i < 8; ++i) pv8[i] = s[kk >> 1][(kk & 1) * 8 + i];
-                if (two) pack_frag_hilo(pb[kk], pl[SPLIT ? kk : 0], pv8);
-                else pack_frag(pb[kk], pv8);
-            }
-            auto pv = [&](const F* pf) {
-                F fa[2][MT];
-                auto fetch = [&](F* f, int kk) {
-#pragma unroll
-                    for (int mt = 0; mt < MT; ++mt) lds_frag_tr<KRB, true>(f[mt], v_lds, mt * 32, kk * 16);
+    #pragma unroll
+                for (int i = 0; i < 16; ++i) s[t2][i] = 0.f;
+            {
+                F fa[2][4];
+                auto fetch = [&](F* f, int bi) {
+    #pragma unroll
+                    for (int x = 0; x < 4; ++x)
+                        lds_frag_s<KRB>(f[x], k_lds, (x & 1) * 32 + (lane & 31), (2 * bi + (x >> 1)) * 16 + half * 8);
                 };
                 fetch(fa[0], 0);
-#pragma unroll
-                for (int kk = 0; kk < 4; ++kk) {
-                    if (kk + 1 < 4) fetch(fa[(kk + 1) & 1], kk + 1);
+    #pragma unroll
+                for (int bi = 0; bi < KS / 2; ++bi) {
+                    if (bi + 1 < KS / 2) fetch(fa[(bi + 1) & 1], bi + 1);
                     lds_order();
-#pragma unroll
-                    for (int mt = 0; mt < MT; ++mt) mma(oacc[mt], fa[kk & 1][mt], pf[kk]);
+    #pragma unroll
+                    for (int x = 0; x < 4; ++x) mma(s[x & 1], fa[bi & 1][x], qf[2 * bi + (x >> 1)]);
                 }
-            };
-            pv(pb);
-            if constexpr (SPLIT) {
-                if (two) pv(pl);
             }
+            wg_barrier();                      // K buffer free
+            if (has_next) kt.issue(k_lds, kb + nxt_off, wave);
+
+            if (c_cur >= 0) {
+                // padding keys of a cut cube: key of entry i of tile t2 is
+                // 32 t2 + 16 (i / 8) + 8 half + i % 8
+                if constexpr (PAD) {        // branch-free: a branch here costs registers
+                    const uint64_t kmask = cube_real_mask(grid, c_cur, lane);
+    #pragma unroll
+                    for (int t2 = 0; t2 < 2; ++t2) {
+                        const uint32_t lm = static_cast<uint32_t>(kmask >> (t2 * 32 + half * 8));
+    #pragma unroll
+                        for (int i = 0; i < 16; ++i)
+                            s[t2][i] = ((lm >> ((i >> 3) * 16 + (i & 7))) & 1u) ? s[t2][i] : -INFINITY;
+                    }
+                }
+                // Online softmax in log2 units with a lazily updated running max:
+                // the accumulators are rescaled only when the block max exceeds
+                // the running max m by more than 2^8 (any lane of the wave), so
+                // p = 2^(s c - m) <= 256.  O = sum p V / sum p is exact for any m.
+                float mx = -INFINITY;
+    #pragma unroll
+                for (int t2 = 0; t2 < 2; ++t2)
+    #pragma unroll
+                    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[t2][i]);
+                mx = fmaxf(mx, swap_half(mx)) * c_log2;
+                if (__any(mx > m + 8.0f)) {
+                    const float mn = fmaxf(m, mx);
+                    const float alpha = fast_exp2(m - mn);
+                    l *= alpha;
+    #pragma unroll
+                    for (int mt = 0; mt < MT; ++mt)
+    #pragma unroll
+                        for (int i = 0; i < 16; ++i) oacc[mt][i] *= alpha;
+                    m = mn;
+                }
+                float ps = 0.f;
+    #pragma unroll
+                for (int t2 = 0; t2 < 2; ++t2)
+    #pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        const float p = fast_exp2(fmaf(s[t2][i], c_log2, -m));
+                        s[t2][i] = p;
+                        ps += p;
+                    }
+                l += ps;
+            }
+            if (has_next) vm_wait<KT::PER_WAVE>(); else vm_wait<0>();   // V tile landed
+            wg_barrier();
+            if (c_cur >= 0) {
+                // O^T += V^T P^T over 4 k-steps of 16 keys: keys 16kk + 8half + (0..7);
+                // V^T fragments are requested one k-step ahead of their products.
+                // On a flagged pair P is split into hi + lo = bf16(P - hi), and a
+                // second pass adds V^T lo (its fragments read again).
+                F pb[4], pl[SPLIT ? 4 : 1];
+                const bool two = SPLIT && FL && big;
+    #pragma unroll
+                for (int kk = 0; kk < 4; ++kk) {
+                    float pv8[8];
+    #pragma unroll
+                    for (int i = 0; i < 8; ++i) pv8[i] = s[kk >> 1][(kk & 1) * 8 + i];
+                    if (two) pack_frag_hilo(pb[kk], pl[SPLIT ? kk : 0], pv8);
+                    else pack_frag(pb[kk], pv8);
+                }
+                auto pv = [&](const F* pf) {
+                    F fa[2][MT];
+                    auto fetch = [&](F* f, int kk) {
+    #pragma unroll
+                        for (int mt = 0; mt < MT; ++mt) lds_frag_tr<KRB, true>(f[mt], v_lds, mt * 32, kk * 16);
+                    };
+                    fetch(fa[0], 0);
+    #pragma unroll
+                    for (int kk = 0; kk < 4; ++kk) {
+                        if (kk + 1 < 4) fetch(fa[(kk + 1) & 1], kk + 1);
+                        lds_order();
+    #pragma unroll
+                        for (int mt = 0; mt < MT; ++mt) mma(oacc[mt], fa[kk & 1][mt], pf[kk]);
+                    }
+                };
+                pv(pb);
+                if constexpr (SPLIT) {
+                    if (two) pv(pl);
+                }
+            }
+            wg_barrier();                      // V buffer free
+            if (has_next) vt_.issue(v_lds, vb + nxt_off, wave);
+            c_cur = c_next;
         }
-        wg_barrier();                      // V buffer free
-        if (has_next) vt_.issue(v_lds, vb + nxt_off, wave);
-        c_cur = c_next;
-    }
+    };
+    if (SPLIT && (all_big || some_big)) walk(std::true_type{});
+    else walk(std::false_type{});
 
     const float lt = q_real ? l + swap_half(l) : 0.f;     // a padding query has no output
     const float inv = lt > 0.f ? 1.0f / lt : 0.f;

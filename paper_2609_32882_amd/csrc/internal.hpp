@@ -80,6 +80,10 @@ hipError_t launch_csc(const int32_t* row_ptr, const int32_t* col_idx, int batch,
                       int64_t col_cap, uint32_t* mask, int32_t* kv_counts, int32_t* kv_ptr,
                       int32_t* kv_idx, hipStream_t s);
 hipError_t launch_mfma_peak(int iters, float* sink, int64_t* flops, hipStream_t s);
+// fp32 atomic adds of one 64 x D tile per transposed-list entry (a fused
+// backward's dQ accumulation, without its arithmetic).
+hipError_t launch_dq_atomic_probe(const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap, float* acc,
+                                  int batch, int Hq, int Hkv, int N, int D, hipStream_t s);
 hipError_t launch_attn_fwd(int dtype, int D, const void* q, const void* k, const void* v,
                            const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, void* o,
                            float* lse, void* o_lo, void* ws, int batch, int Hq, int Hkv, int N,

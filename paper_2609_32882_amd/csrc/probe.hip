@@ -47,4 +47,43 @@ hipError_t launch_mfma_peak(int iters, float* sink, int64_t* flops, hipStream_t 
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Atomic-accumulation floor of a fused backward: the dQ traffic a single
+// key-stationary kernel would need if it added each pair's dQ tile (64
+// queries x D, fp32) into an fp32 accumulator with atomics, without any of
+// the arithmetic.  One workgroup per key block walks its transposed list
+// and adds 1.0 to every element of each listed query block's tile.
+// ---------------------------------------------------------------------------
+constexpr int ATOMIC_NT = 256;
+
+__global__ __launch_bounds__(ATOMIC_NT) void dq_atomic_probe_kernel(const int32_t* __restrict__ kv_ptr,
+                                                                    const int32_t* __restrict__ kv_idx,
+                                                                    int64_t col_cap, float* __restrict__ acc,
+                                                                    int Hq, int Hkv, int N, int D) {
+    const int64_t krow = blockIdx.x;
+    const int64_t bkv = krow / N;
+    const int b = static_cast<int>(bkv / Hkv), hkv = static_cast<int>(bkv % Hkv);
+    const int grp = Hq / Hkv;
+    int64_t e0 = kv_ptr[krow], e1 = kv_ptr[krow + 1];
+    e0 = e0 < 0 ? 0 : (e0 > col_cap ? col_cap : e0);
+    e1 = e1 < e0 ? e0 : (e1 > col_cap ? col_cap : e1);
+    const int64_t qrow0 = (static_cast<int64_t>(b) * Hq + hkv * grp) * N;
+    const int tile = 64 * D;
+    for (int64_t e = e0; e < e1; ++e) {
+        const int ent = kv_idx[e];
+        if (ent < 0 || ent / N >= grp) continue;
+        float* dst = acc + (qrow0 + ent) * tile;
+        for (int i = threadIdx.x; i < tile; i += ATOMIC_NT) unsafeAtomicAdd(dst + i, 1.0f);
+    }
+}
+
+hipError_t launch_dq_atomic_probe(const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap, float* acc,
+                                  int batch, int Hq, int Hkv, int N, int D, hipStream_t s) {
+    const int64_t krows = static_cast<int64_t>(batch) * Hkv * N;
+    if (krows == 0) return hipSuccess;
+    hipLaunchKernelGGL(dq_atomic_probe_kernel, dim3(static_cast<unsigned>(krows)), dim3(ATOMIC_NT), 0, s, kv_ptr,
+                       kv_idx, col_cap, acc, Hq, Hkv, N, D);
+    return hipGetLastError();
+}
+
 }  // namespace vsa2

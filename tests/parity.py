@@ -124,3 +124,50 @@ def compare_selection(gpu_ptr, gpu_idx, ora_counts, ora_idx, ora_scores, rows=No
         if rel <= 1e-6:
             stats["excused_rel_1e6"] += 1
     return stats
+
+
+def attn_fp32_logit_bounds(q, k, v, do, scale, D, kmask=None):
+    """First-order worst-case effect of fp32 accumulation in the score and
+    dP products on softmax attention of m queries over n keys (all float64
+    host arrays: q, do [m, D]; k, v [n, D]).  A D-term dot product of exact
+    products accumulated in fp32 is off by at most gamma * sum |terms|,
+    gamma = (D + 3) 2^-24 (n u / (1 - n u) with the scaling and the
+    exponent's multiply-add), so every score of query l is off by at most
+    d_l = gamma max_j sum_d |q_ld k_jd| scale, P_lj by 2 d_l P_lj (the
+    normaliser moves with the scores), and the outputs by
+      O:  sum_j |dP_lj| |v_j|
+      dS: |dP_lj| |dP_lj - Delta_l| + P_lj (gamma sum_d |dO_ld v_jd| + |dDelta_l|)
+      dQ: sum_j |ddS_lj| |k_j| scale,  dK: sum_l |ddS_lj| |q_l| scale,
+      dV: sum_l |dP_lj| |dO_l|.
+    kmask (bool [n]) leaves keys out of the softmax (padding).
+    Returns the element-wise bounds (eO, edQ, edK, edV)."""
+    gam = (D + 3) * 2.0 ** -24
+    A = (np.abs(q) @ np.abs(k).T) * scale
+    S = (q @ k.T) * scale
+    if kmask is not None:
+        S = np.where(kmask[None, :], S, -np.inf)
+        A = np.where(kmask[None, :], A, 0.0)
+    P = np.exp(S - S.max(1, keepdims=True))
+    P /= P.sum(1, keepdims=True)
+    dl = gam * A.max(1, keepdims=True)
+    eP = 2.0 * dl * P
+    eO = eP @ np.abs(v)
+    dPv = do @ v.T
+    Delta = (P * dPv).sum(1, keepdims=True)
+    eDelta = (np.abs(do) * eO).sum(1, keepdims=True)
+    edS = eP * np.abs(dPv - Delta) + P * (gam * (np.abs(do) @ np.abs(v).T) + eDelta)
+    return eO, edS @ np.abs(k) * scale, edS.T @ np.abs(q) * scale, eP.T @ np.abs(do)
+
+
+def assert_values_bound(got, ref, name, dtype, extra):
+    """assert_values with the element-wise bound widened by a derived
+    per-element term `extra` (same shape as ref)."""
+    got = np.asarray(got, np.float64).reshape(ref.shape)
+    ref = np.asarray(ref, np.float64)
+    diff = np.abs(got - ref) - ULP_REL[dtype] * np.abs(ref)
+    ratio = float((diff / (MAX_ABS + extra)).max())
+    den = float(np.sqrt((ref ** 2).sum()))
+    rel = float(np.sqrt(((got - ref) ** 2).sum()) / den) if den > 0 else 0.0
+    print("%s: max (err - ulp) / (2e-2 + derived bound) = %.3f, max derived bound %.3e, rel_l2=%.3e" % (
+        name, ratio, float(np.max(extra)), rel))
+    assert ratio <= 1.0 and rel <= REL_L2, (name, ratio, rel)
