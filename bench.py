@@ -186,6 +186,20 @@ def main():
     coarse = None if args.no_coarse else time_coarse_branch(vsa2, torch, p, q, k, v, do, o, dq, dk, dv,
                                                             stream, max(args.steps, 3))
 
+    # the inference forward (no remainder kept, so no two-term products and
+    # no block flags), the path of forward-only use, timed on its own
+    inf_ts = []
+    for _ in range(max(args.steps, 3)):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        chk("fwd", vsa2.vsa2_attn_fwd(P, q.data_ptr(), k.data_ptr(), v.data_ptr(), a_rp.data_ptr(),
+                                      a_ci.data_ptr(), a_cap, o.data_ptr(), lse.data_ptr(), None,
+                                      fws_t.data_ptr(), fws, sp))
+        e1.record(stream)
+        inf_ts.append((e0, e1))
+    torch.cuda.synchronize()
+    inference_fwd_ms = float(np.mean([a.elapsed_time(b) for a, b in inf_ts]))
+
     mfma_peak = measure_mfma_peak(vsa2, torch, stream)
 
     atomic_ms = None
@@ -254,6 +268,7 @@ def main():
         },
         "breakdown_ms": {s: round(stage_ms[s], 4) for s in ("pool", "route", "fwd", "bwd") + stages[3:]},
         "attn_fwd_bwd_ms": round(attn_ms, 4),
+        "inference_fwd_ms": round(inference_fwd_ms, 4),
         **({"fused_bwd_dq_atomic_floor_ms": atomic_ms} if atomic_ms is not None else {}),
         "attn_only_tflops": round(attn_tflops, 3),
         "pct_bf16_peak_attn_only": round(100.0 * attn_tflops / peak, 2),
