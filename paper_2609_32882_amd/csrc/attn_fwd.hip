@@ -205,52 +205,58 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
                         for (int i = 0; i < 16; ++i) oacc[mt][i] *= alpha;
                     m = mn;
                 }
-                float ps = 0.f;
-    #pragma unroll
-                for (int t2 = 0; t2 < 2; ++t2)
-    #pragma unroll
-                    for (int i = 0; i < 16; ++i) {
-                        const float p = fast_exp2(fmaf(s[t2][i], c_log2, -m));
-                        s[t2][i] = p;
-                        ps += p;
-                    }
-                l += ps;
             }
             if (has_next) vm_wait<KT::PER_WAVE>(); else vm_wait<0>();   // V tile landed
             wg_barrier();
             if (c_cur >= 0) {
-                // O^T += V^T P^T over 4 k-steps of 16 keys: keys 16kk + 8half + (0..7);
-                // V^T fragments are requested one k-step ahead of their products.
+                // O^T += V^T P^T over 4 k-steps of 16 keys: keys 16kk + 8half + (0..7).
+                // The probabilities of k-step kk + 1 (exponentials, row sum,
+                // bf16 packing) are formed after the products of k-step kk in
+                // program order, so they issue while those MFMAs run; V^T
+                // fragments are requested one k-step ahead of their products.
                 // On a flagged pair P is split into hi + lo = bf16(P - hi), and a
                 // second pass adds V^T lo (its fragments read again).
                 F pb[4], pl[SPLIT ? 4 : 1];
                 const bool two = SPLIT && FL && big;
-    #pragma unroll
-                for (int kk = 0; kk < 4; ++kk) {
+                float ps = 0.f;
+                auto make_p = [&](int kk) {
                     float pv8[8];
     #pragma unroll
-                    for (int i = 0; i < 8; ++i) pv8[i] = s[kk >> 1][(kk & 1) * 8 + i];
+                    for (int i = 0; i < 8; ++i) {
+                        const float p = fast_exp2(fmaf(s[kk >> 1][(kk & 1) * 8 + i], c_log2, -m));
+                        pv8[i] = p;
+                        ps += p;
+                    }
                     if (two) pack_frag_hilo(pb[kk], pl[SPLIT ? kk : 0], pv8);
                     else pack_frag(pb[kk], pv8);
-                }
-                auto pv = [&](const F* pf) {
-                    F fa[2][MT];
-                    auto fetch = [&](F* f, int kk) {
-    #pragma unroll
-                        for (int mt = 0; mt < MT; ++mt) lds_frag_tr<KRB, true>(f[mt], v_lds, mt * 32, kk * 16);
-                    };
-                    fetch(fa[0], 0);
-    #pragma unroll
-                    for (int kk = 0; kk < 4; ++kk) {
-                        if (kk + 1 < 4) fetch(fa[(kk + 1) & 1], kk + 1);
-                        lds_order();
-    #pragma unroll
-                        for (int mt = 0; mt < MT; ++mt) mma(oacc[mt], fa[kk & 1][mt], pf[kk]);
-                    }
                 };
-                pv(pb);
+                F fa[2][MT];
+                auto fetch = [&](F* f, int kk) {
+    #pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) lds_frag_tr<KRB, true>(f[mt], v_lds, mt * 32, kk * 16);
+                };
+                make_p(0);
+                fetch(fa[0], 0);
+    #pragma unroll
+                for (int kk = 0; kk < 4; ++kk) {
+                    if (kk + 1 < 4) fetch(fa[(kk + 1) & 1], kk + 1);
+                    lds_order();
+    #pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) mma(oacc[mt], fa[kk & 1][mt], pb[kk]);
+                    if (kk + 1 < 4) make_p(kk + 1);
+                }
+                l += ps;
                 if constexpr (SPLIT) {
-                    if (two) pv(pl);
+                    if (two) {
+                        fetch(fa[0], 0);
+    #pragma unroll
+                        for (int kk = 0; kk < 4; ++kk) {
+                            if (kk + 1 < 4) fetch(fa[(kk + 1) & 1], kk + 1);
+                            lds_order();
+    #pragma unroll
+                            for (int mt = 0; mt < MT; ++mt) mma(oacc[mt], fa[kk & 1][mt], pl[kk]);
+                        }
+                    }
                 }
             }
             wg_barrier();                      // V buffer free
