@@ -254,3 +254,17 @@ def test_missing_library_fails_loudly():
     out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=120)
     assert out.returncode == 0, out.stderr
     assert out.stdout.startswith("raised") and "not built" in out.stdout
+
+
+def test_router_rejects_more_than_4096_blocks():
+    """N = 4096 cubes is the router's largest (tested on the GPU at that
+    size); one more row of cubes is refused before any device work."""
+    s = vsa2.vsa2_select(0, 8, 0.0, 0)
+    from workload import Problem
+    ok = vsa2.problem_from(Problem(1, 1, 1, 64, 64, 64, 64))          # N = 4096
+    big = vsa2.problem_from(Problem(1, 1, 1, 64, 64, 64, 68))         # N = 16 x 16 x 17 = 4352
+    st = vsa2.vsa2_route(big, s, FAKE, FAKE, FAKE, FAKE, 10 ** 9, None, None, None, FAKE, 10 ** 12, None)
+    assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_UNSUPPORTED"
+    st = vsa2.vsa2_route(ok, s, FAKE, FAKE, FAKE, FAKE, 10 ** 9, None, None, None, FAKE, 0, None)
+    assert vsa2.STATUS_NAMES[st] == "VSA2_ERR_WORKSPACE"                # past the size check
+
