@@ -20,7 +20,9 @@
  *   Memory     Every tensor pointer is a DEVICE pointer owned by the caller.
  *              The library never allocates device memory; calls that need
  *              scratch space take a caller-owned workspace whose size is
- *              returned by the matching *_workspace query.
+ *              returned by the matching *_workspace query (except
+ *              vsa2_attn_fwd_noalloc, which uses a fixed array of the
+ *              library instead).
  *   Streams    Work is enqueued asynchronously on the caller's stream; no call
  *              synchronises the device or reads device memory on the host.
  *   Errors     Argument errors are detected on the host and returned before
@@ -36,7 +38,9 @@
  *              (b*Hkv + h)*N + n.
  *   Dtypes     VSA2_F32 or VSA2_BF16 inputs; outputs in the input dtype,
  *              rounded to nearest even from fp32 accumulators.
- *   Threads    Calls are thread-safe; the library keeps no mutable state.
+ *   Threads    Calls are thread-safe; the library keeps no mutable state
+ *              other than the per-GPU array of vsa2_attn_fwd_noalloc (whose
+ *              overlapping calls on one GPU race, see there).
  *   Determinism  Every output is bitwise reproducible for equal inputs.
  *
  * Supported shapes (other values return VSA2_ERR_UNSUPPORTED):
