@@ -3,7 +3,7 @@
 //
 // One workgroup of two waves per query block (64 queries); wave w owns
 // queries 32w .. 32w+31.  For every key block listed in the block's CSR row:
-//   K, V tiles [64 keys][D] -> LDS, row r at slot swap_bits_2_3(r)
+//   K, V tiles [64 keys][D] -> LDS, key r at LDS row tile_slot(r)
 //   S^T = K Q^T            (MFMA 32x32, Q fragments live in registers)
 //   online softmax in fp32 registers (exp2, log2(e)/sqrt(D) folded in)
 //   O^T += V^T P^T         (P rounded to the input dtype, MFMA 32x32; the

@@ -20,14 +20,14 @@ constexpr int CB_NT = 128;   // two waves, 32 rows each
 constexpr float kLog2eC = 1.4426950408889634f;
 
 // Rows row0 .. row0+63 of a [rows][D] tensor into a padded LDS tile, LDS row r
-// holding global row row0 + swap_bits_2_3(r) (bf16: column groups in the
+// holding global row row0 + tile_row_at(r) (bf16: column groups in the
 // cgroup_pos order the fragment readers expect); rows >= nrows are zero.
 template <int RB, bool CPERM>
 __device__ __forceinline__ void load_rows_sync(char* lds, const char* g, int64_t row0, int64_t nrows, int tid) {
     constexpr int CH = RB / 16;
     for (int c = tid; c < 64 * CH; c += CB_NT) {
         const int r = c / CH, ch = c % CH;
-        const int64_t gr = row0 + swap_bits_2_3(r);
+        const int64_t gr = row0 + tile_row_at(r);
         uint4 v = make_uint4(0, 0, 0, 0);
         if (gr < nrows) v = *reinterpret_cast<const uint4*>(g + gr * RB + ch * 16);
         const int pc = CPERM ? cgroup_pos<RB>(ch >> 1) * 32 + (ch & 1) * 16 : ch * 16;

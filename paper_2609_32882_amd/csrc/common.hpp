@@ -157,21 +157,6 @@ __device__ __forceinline__ float dpp_f32(float x) {
 // Exchange with the lane 32 positions away (the other half of the wave).
 __device__ __forceinline__ float swap_half(float x) { return __shfl_xor(x, 32, 64); }
 
-// ---------------------------------------------------------------------------
-// LDS tiles of 64 rows x ROW_BYTES bytes (ROW_BYTES a multiple of 128),
-// addressed in 16-byte chunks with an XOR swizzle of the chunk index by the
-// row's low 3 bits, so that lanes reading the same logical chunk of
-// consecutive rows hit different banks.
-// ---------------------------------------------------------------------------
-template <int ROW_BYTES>
-struct lds_tile {
-    static constexpr int CHUNKS = ROW_BYTES / 16;
-    static constexpr int BYTES = 64 * ROW_BYTES;
-    __device__ static __forceinline__ int offset(int row, int chunk) {
-        return row * ROW_BYTES + (chunk ^ (row & 7)) * 16;
-    }
-};
-
 // Key-row slot permutation used by the "transposed" formulations: swapping
 // bits 2 and 3 of a row index inside each 32-row tile makes the accumulator
 // rows held by one lane (8*(v/4) + 4*(l/32) + v%4) map to two runs of 8
@@ -179,6 +164,24 @@ struct lds_tile {
 __device__ __forceinline__ int swap_bits_2_3(int r) {
     return (r & ~0xc) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
+
+// Physical LDS row of tile row y in the padded tiles below, and its inverse.
+// Inside each 16-row block, y = 8c + 4b + a (a < 4) sits at row 8c + 2a + b:
+// the four rows a transposing read takes together from one half-wave
+// (y = 4j .. 4j+3) land 2 rows = 8 banks apart, and any 16 consecutive
+// rows still fill all 16 bank groups of 16 bytes.
+__host__ __device__ constexpr int tile_slot(int y) {
+    return (y & ~15) | ((y & 8) | ((y & 3) << 1) | ((y >> 2) & 1));
+}
+__host__ __device__ constexpr int tile_row_at(int p) {
+    return (p & ~15) | ((p & 8) | (((p >> 1) & 3)) | ((p & 1) << 2));
+}
+constexpr bool tile_slot_is_permutation() {
+    for (int y = 0; y < 64; ++y)
+        if (tile_row_at(tile_slot(y)) != y || (tile_slot(y) >> 4) != (y >> 4)) return false;
+    return true;
+}
+static_assert(tile_slot_is_permutation(), "tile_slot must permute rows inside 16-row blocks");
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 
@@ -205,133 +208,6 @@ __device__ __forceinline__ int64_t work_row(const int32_t* order, int64_t item, 
 
 // Index of the calling wave inside its workgroup, as a wave-uniform (scalar) value.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
-
-// Fragment of 8 consecutive elements starting at element `e0` of row `row`
-// of a swizzled LDS tile (bf16: one 16-byte chunk; fp32: two).
-template <int ROW_BYTES>
-__device__ __forceinline__ void lds_frag(frag_bf16& f, const char* tile, int row, int e0) {
-    load_frag(f, tile + lds_tile<ROW_BYTES>::offset(row, e0 >> 3));
-}
-template <int ROW_BYTES>
-__device__ __forceinline__ void lds_frag(frag_f32& f, const char* tile, int row, int e0) {
-    const float4 a = *reinterpret_cast<const float4*>(tile + lds_tile<ROW_BYTES>::offset(row, e0 >> 2));
-    const float4 b = *reinterpret_cast<const float4*>(tile + lds_tile<ROW_BYTES>::offset(row, (e0 >> 2) + 1));
-    f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
-    f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
-}
-
-// ---------------------------------------------------------------------------
-// Cooperative copy of a 64-row x D tile from global memory into LDS.
-// `load` issues the global reads into registers (rows >= nrows read as 0);
-// `store` writes them to a swizzled LDS tile.  Straight copies keep the
-// [row][D] layout, optionally placing row r at slot swap_bits_2_3(r);
-// transposed copies write the [D][64] layout (each thread moves one 8x8
-// block through registers).
-// ---------------------------------------------------------------------------
-template <typename T, int D, int NT>
-struct tile_rows {
-    static constexpr int E = sizeof(T);
-    static constexpr int RB = D * E;           // bytes per row
-    static constexpr int CH = RB / 16;          // 16-byte chunks per row
-    static constexpr int PER = 64 * CH / NT;    // chunks per thread
-    static_assert(PER >= 1 && (64 * CH) % NT == 0, "tile / thread count mismatch");
-    uint4 r[PER];
-
-    __device__ __forceinline__ void load(const T* base, int64_t row0, int64_t nrows, int tid) {
-        const char* g = reinterpret_cast<const char*>(base);
-#pragma unroll
-        for (int i = 0; i < PER; ++i) {
-            const int id = i * NT + tid;
-            const int row = id / CH, ch = id % CH;
-            if (row0 + row < nrows)
-                r[i] = *reinterpret_cast<const uint4*>(g + (row0 + row) * RB + ch * 16);
-            else
-                r[i] = make_uint4(0, 0, 0, 0);
-        }
-    }
-    __device__ __forceinline__ void store(char* lds, bool permute, int tid) const {
-#pragma unroll
-        for (int i = 0; i < PER; ++i) {
-            const int id = i * NT + tid;
-            const int row = id / CH, ch = id % CH;
-            const int slot = permute ? swap_bits_2_3(row) : row;
-            *reinterpret_cast<uint4*>(lds + lds_tile<RB>::offset(slot, ch)) = r[i];
-        }
-    }
-};
-
-template <typename T, int D, int NT>
-struct tile_transposed {
-    static constexpr int E = sizeof(T);
-    static constexpr int RB = 64 * E;           // bytes per LDS row (one d)
-    static constexpr int W = 8 * E / 16;        // 16-byte words per 8-element run
-    static constexpr int BLOCKS = 8 * (D / 8);  // 8x8 blocks in the tile
-    static_assert(BLOCKS <= NT, "one 8x8 block per thread");
-    uint4 r[8][W];
-
-    __device__ __forceinline__ void load(const T* base, int64_t row0, int tid) {
-        if (tid >= BLOCKS) return;
-        const int dc = tid % (D / 8), kb = tid / (D / 8);
-        const char* g = reinterpret_cast<const char*>(base);
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-#pragma unroll
-            for (int w = 0; w < W; ++w)
-                r[i][w] = *reinterpret_cast<const uint4*>(
-                    g + (row0 + kb * 8 + i) * (int64_t)(D * E) + dc * 8 * E + w * 16);
-    }
-    // The same 8x8 blocks written untransposed: [64 rows][D] (row stride
-    // D*E), row r at slot swap_bits_2_3(r) when `permute`.
-    __device__ __forceinline__ void store_rows(char* lds, bool permute, int tid) const {
-        if (tid >= BLOCKS) return;
-        const int dc = tid % (D / 8), kb = tid / (D / 8);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int row = kb * 8 + i;
-            const int slot = permute ? swap_bits_2_3(row) : row;
-#pragma unroll
-            for (int w = 0; w < W; ++w)
-                *reinterpret_cast<uint4*>(lds + lds_tile<D * E>::offset(slot, dc * W + w)) = r[i][w];
-        }
-    }
-    __device__ __forceinline__ void store(char* lds, int tid) const {
-        if (tid >= BLOCKS) return;
-        const int dc = tid % (D / 8), kb = tid / (D / 8);
-        if constexpr (E == 2) {
-            // r[i] = 8 bf16 of key kb*8+i: word a = (d 2a, d 2a+1)
-            const uint32_t* in[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) in[i] = reinterpret_cast<const uint32_t*>(&r[i][0]);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const int a = j >> 1;
-                uint32_t o[4];
-#pragma unroll
-                for (int m = 0; m < 4; ++m) {
-                    const uint32_t x = in[2 * m][a], y = in[2 * m + 1][a];
-                    o[m] = (j & 1) ? ((x >> 16) | (y & 0xffff0000u)) : ((x & 0xffffu) | (y << 16));
-                }
-                *reinterpret_cast<uint4*>(lds + lds_tile<RB>::offset(dc * 8 + j, kb)) =
-                    make_uint4(o[0], o[1], o[2], o[3]);
-            }
-        } else {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                float col[8];
-#pragma unroll
-                for (int i = 0; i < 8; ++i) col[i] = reinterpret_cast<const float*>(&r[i][0])[j];
-                *reinterpret_cast<float4*>(lds + lds_tile<RB>::offset(dc * 8 + j, 2 * kb)) =
-                    make_float4(col[0], col[1], col[2], col[3]);
-                *reinterpret_cast<float4*>(lds + lds_tile<RB>::offset(dc * 8 + j, 2 * kb + 1)) =
-                    make_float4(col[4], col[5], col[6], col[7]);
-            }
-        }
-    }
-};
-
-}  // namespace vsa2
-
-namespace vsa2 {
 
 // ---------------------------------------------------------------------------
 // Asynchronous global -> LDS tile copies (global_load_lds_dwordx4).
@@ -445,20 +321,25 @@ __device__ __forceinline__ int64_t sweep_start(const int32_t* list, int64_t e0, 
     return lo == cnt ? 0 : lo;
 }
 
-// LDS tiles are stored with a row stride of RB + 16 bytes: 16 lanes reading
-// the same 16-byte column of 16 consecutive rows then hit 16 different bank
-// groups, and every fragment address is one per-lane base plus a
-// compile-time offset (no per-fragment address registers).  Rows are
-// permuted with swap_bits_2_3 when PERM: LDS row r holds global row
-// swap_bits_2_3(r).
+// LDS tiles are stored with a row stride of RB + 16 bytes (64 banks of 4
+// bytes: each row starts 4 banks after the previous one), and every fragment
+// address is one per-lane base plus a compile-time offset (no per-fragment
+// address registers).  When PERM, tile row y sits at LDS row tile_slot(y).
+// Fragment readers take rows in the slot-swapped view of the MFMA layouts
+// (lds_frag_s row s = tile row swap_bits_2_3(s)).
 //
 // bf16 tiles (CPERM) also place the 32-byte column groups of a row (16
 // elements each) out of order: group g sits at position cgroup_pos(g) =
 // (g & 1) * NG/2 + g/2 (NG = RB/32 groups), so the two 16-column halves of
-// a 32-column fragment lie half a row apart.  A transposing read
-// (lds_frag_tr) makes 32 lanes fetch 64 bytes from each of 4 consecutive
-// rows; with contiguous columns those rows' bank ranges overlap up to
-// 4-fold at this row stride, with the halves split apart at most 2-fold.
+// a 32-column fragment lie half a row apart.
+// Bank conflicts: a 16-byte row read (lds_frag_s) serves 16 lanes per
+// clock, which read one column of 16 consecutive tile rows: tile_slot
+// permutes inside 16-row blocks, so they occupy 16 distinct bank groups.  A
+// transposing read (lds_frag_tr) serves a half-wave per clock, 32 bytes of
+// each column half of 4 tile rows y = 4j .. 4j+3: tile_slot places them 2
+// LDS rows (8 banks) apart, so the 8 pieces fill the 64 banks once.  (With
+// the rows in slot-swapped order they were 1 LDS row apart and overlapped
+// 2-fold: 2 extra clocks per read, measured with SQ_LDS_BANK_CONFLICT.)
 //
 // A tile is copied by whole 1 KB wave instructions; lanes whose destination
 // is a pad slot (or past the last row) fetch the tile's first 16 bytes
@@ -489,7 +370,7 @@ struct async_tile {
             const int row = p / STRIDE, col = p % STRIDE;
             const bool data = row < ROWS && col < RB;
             const int lcol = CPERM ? cgroup_of_pos<RB>(col / 32) * 32 + col % 32 : col;
-            off[j] = data ? (PERM ? swap_bits_2_3(row) : row) * RB + lcol : 0;
+            off[j] = data ? (PERM ? tile_row_at(row) : row) * RB + lcol : 0;
         }
     }
     __device__ __forceinline__ void issue(char* lds, const char* g, int wave) const {
@@ -505,7 +386,7 @@ struct async_tile {
         for (int j = 0; j < PER_WAVE; ++j) {
             const int p = (wave * PER_WAVE + j) * 1024 + lane * 16;
             const int row = p / STRIDE;                    // LDS slot
-            const int grow = PERM ? swap_bits_2_3(row) : row;
+            const int grow = PERM ? tile_row_at(row) : row;
             dma16(l0 + (wave * PER_WAVE + j) * 1024, g, (row < ROWS && grow < rows) ? off[j] : (off[j] % RB));
         }
     }
@@ -514,7 +395,7 @@ struct async_tile {
 // A-operand fragment of a transposed use of a row-major tile.
 //
 // The tile holds X^T row-major: LDS row = the contraction index (a key or a
-// query, stored at slot swap_bits_2_3(index) when PERM), columns = the output
+// query, stored at LDS row tile_slot(index) when PERM), columns = the output
 // rows m (the head dimension d), in the bf16 column-group order above.  The
 // MFMA 32x32x16 A operand for output tile rows m0 .. m0+31 (m0 a multiple
 // of 32) and contraction indices k0 .. k0+15 needs, in lane l,
@@ -533,12 +414,13 @@ __device__ __forceinline__ void lds_frag_tr(frag_bf16& f, const char* tile, int 
     v4i16 r2[2];
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
-        // k0 and m0 are multiples of 16 and 32: the slot swap acts on the
-        // lane's part y < 16 of the index only, and column group
-        // m0/16 + G%2 sits at position (G%2) RB/64 + m0/32, so the address
-        // is a per-lane offset plus the constant k0 (RB + 16) + m0
+        // k0 and m0 are multiples of 16 and 32: the slot permutation acts
+        // on the lane's part y < 16 of the index only (tile_slot(y) =
+        // 8(G/2) + 2(i/4) + r), and column group m0/16 + G%2 sits at
+        // position (G%2) RB/64 + m0/32, so the address is a per-lane offset
+        // plus the constant k0 (RB + 16) + m0
         const int y = 8 * (G >> 1) + 4 * r + (i >> 2);
-        const int row = k0 + (PERM ? swap_bits_2_3(y) : y);
+        const int row = k0 + (PERM ? tile_slot(y) : y);
         const int grp = (G & 1) * (RB / 64) + (m0 >> 5);
         const char* p = tile + row * (RB + 16) + grp * 32 + 8 * (i & 3);
         r2[r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p));
@@ -556,20 +438,23 @@ __device__ __forceinline__ void lds_frag_tr(frag_f32& f, const char* tile, int m
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
         const int k = k0 + 8 * (l >> 5) + s;
-        const int row = PERM ? swap_bits_2_3(k) : k;
+        const int row = PERM ? tile_slot(k) : k;
         f.v[s] = *reinterpret_cast<const float*>(tile + row * (RB + 16) + m * 4);
     }
 }
 
 // Fragment of 8 consecutive elements starting at element e0 (a multiple of
-// 8) of row `row` of a padded LDS tile with RB-byte rows (bf16: in the
+// 8) of row s of the slot-swapped view of a padded, slot-permuted LDS tile
+// with RB-byte rows (tile row swap_bits_2_3(s), bf16 columns in the
 // column-group order above).
 template <int RB>
-__device__ __forceinline__ void lds_frag_s(frag_bf16& f, const char* tile, int row, int e0) {
+__device__ __forceinline__ void lds_frag_s(frag_bf16& f, const char* tile, int s, int e0) {
+    const int row = tile_slot(swap_bits_2_3(s));
     load_frag(f, tile + row * (RB + 16) + cgroup_pos<RB>(e0 >> 4) * 32 + (e0 & 15) * 2);
 }
 template <int RB>
-__device__ __forceinline__ void lds_frag_s(frag_f32& f, const char* tile, int row, int e0) {
+__device__ __forceinline__ void lds_frag_s(frag_f32& f, const char* tile, int s, int e0) {
+    const int row = tile_slot(swap_bits_2_3(s));
     const float4 a = *reinterpret_cast<const float4*>(tile + row * (RB + 16) + e0 * 4);
     const float4 b = *reinterpret_cast<const float4*>(tile + row * (RB + 16) + e0 * 4 + 16);
     f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
