@@ -27,7 +27,7 @@ __device__ __forceinline__ void load_rows_sync(char* lds, const char* g, int64_t
     constexpr int CH = RB / 16;
     for (int c = tid; c < 64 * CH; c += CB_NT) {
         const int r = c / CH, ch = c % CH;
-        const int64_t gr = row0 + tile_row_at(r);
+        const int64_t gr = row0 + tile_row_at<RB>(r);
         uint4 v = make_uint4(0, 0, 0, 0);
         if (gr < nrows) v = *reinterpret_cast<const uint4*>(g + gr * RB + ch * 16);
         const int pc = CPERM ? cgroup_pos<RB>(ch >> 1) * 32 + (ch & 1) * 16 : ch * 16;

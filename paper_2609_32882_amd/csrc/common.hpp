@@ -165,23 +165,39 @@ __device__ __forceinline__ int swap_bits_2_3(int r) {
     return (r & ~0xc) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
 
-// Physical LDS row of tile row y in the padded tiles below, and its inverse.
-// Inside each 16-row block, y = 8c + 4b + a (a < 4) sits at row 8c + 2a + b:
-// the four rows a transposing read takes together from one half-wave
-// (y = 4j .. 4j+3) land 2 rows = 8 banks apart, and any 16 consecutive
-// rows still fill all 16 bank groups of 16 bytes.
+// Physical LDS row of tile row y in the padded tiles below (row stride
+// RB + 16 bytes), and its inverse.  Inside each 16-row block, y = 8c + 4b + a
+// (a < 4) moves to a row chosen so that the four rows a transposing read
+// takes together from one half-wave (y = 4j .. 4j+3, i.e. fixed c and b)
+// leave the 64 banks' 8-bank pieces they read disjoint, while any 16
+// consecutive rows still fill all 16 bank groups of 16 bytes:
+// - stride RB + 16 = 4 banks mod 64 (RB = 256, 512): row 8c + 2a + b, the
+//   four rows 8 banks apart;
+// - stride 36 banks (RB = 128): row 8(a/2) + 4c + 2(a%2) + b, the four rows
+//   at bank offsets {0, 8, 32, 40} + const (their second 32-byte pieces sit
+//   16 banks further).
+template <int RB>
+__host__ __device__ constexpr int tile_slot_of(int c, int b, int a) {
+    return RB == 128 ? 8 * (a >> 1) + 4 * c + 2 * (a & 1) + b : 8 * c + 2 * a + b;
+}
+template <int RB>
 __host__ __device__ constexpr int tile_slot(int y) {
-    return (y & ~15) | ((y & 8) | ((y & 3) << 1) | ((y >> 2) & 1));
+    return (y & ~15) | tile_slot_of<RB>((y >> 3) & 1, (y >> 2) & 1, y & 3);
 }
+template <int RB>
 __host__ __device__ constexpr int tile_row_at(int p) {
-    return (p & ~15) | ((p & 8) | (((p >> 1) & 3)) | ((p & 1) << 2));
+    const int q = p & 15;
+    return (p & ~15) | (RB == 128 ? 8 * ((q >> 2) & 1) + 4 * (q & 1) + ((q >> 1) & 1) + 2 * ((q >> 3) & 1)
+                                  : (q & 8) + 4 * (q & 1) + ((q >> 1) & 3));
 }
+template <int RB>
 constexpr bool tile_slot_is_permutation() {
     for (int y = 0; y < 64; ++y)
-        if (tile_row_at(tile_slot(y)) != y || (tile_slot(y) >> 4) != (y >> 4)) return false;
+        if (tile_row_at<RB>(tile_slot<RB>(y)) != y || (tile_slot<RB>(y) >> 4) != (y >> 4)) return false;
     return true;
 }
-static_assert(tile_slot_is_permutation(), "tile_slot must permute rows inside 16-row blocks");
+static_assert(tile_slot_is_permutation<128>() && tile_slot_is_permutation<256>() &&
+                  tile_slot_is_permutation<512>(), "tile_slot must permute rows inside 16-row blocks");
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 
@@ -324,7 +340,7 @@ __device__ __forceinline__ int64_t sweep_start(const int32_t* list, int64_t e0, 
 // LDS tiles are stored with a row stride of RB + 16 bytes (64 banks of 4
 // bytes: each row starts 4 banks after the previous one), and every fragment
 // address is one per-lane base plus a compile-time offset (no per-fragment
-// address registers).  When PERM, tile row y sits at LDS row tile_slot(y).
+// address registers).  When PERM, tile row y sits at LDS row tile_slot<RB>(y).
 // Fragment readers take rows in the slot-swapped view of the MFMA layouts
 // (lds_frag_s row s = tile row swap_bits_2_3(s)).
 //
@@ -334,12 +350,13 @@ __device__ __forceinline__ int64_t sweep_start(const int32_t* list, int64_t e0, 
 // a 32-column fragment lie half a row apart.
 // Bank conflicts: a 16-byte row read (lds_frag_s) serves 16 lanes per
 // clock, which read one column of 16 consecutive tile rows: tile_slot
-// permutes inside 16-row blocks, so they occupy 16 distinct bank groups.  A
-// transposing read (lds_frag_tr) serves a half-wave per clock, 32 bytes of
-// each column half of 4 tile rows y = 4j .. 4j+3: tile_slot places them 2
-// LDS rows (8 banks) apart, so the 8 pieces fill the 64 banks once.  (With
-// the rows in slot-swapped order they were 1 LDS row apart and overlapped
-// 2-fold: 2 extra clocks per read, measured with SQ_LDS_BANK_CONFLICT.)
+// permutes inside 16-row blocks and a row starts 4 (or 36) banks after the
+// previous one, so they occupy 16 distinct bank groups.  A transposing read
+// (lds_frag_tr) serves a half-wave per clock, 32 bytes of each column half
+// of 4 tile rows y = 4j .. 4j+3: tile_slot places them so that the 8 pieces
+// fill the 64 banks once.  (With the rows in slot-swapped order they
+// overlapped 2-fold: 2 extra clocks per read, measured with
+// SQ_LDS_BANK_CONFLICT.)
 //
 // A tile is copied by whole 1 KB wave instructions; lanes whose destination
 // is a pad slot (or past the last row) fetch the tile's first 16 bytes
@@ -370,7 +387,7 @@ struct async_tile {
             const int row = p / STRIDE, col = p % STRIDE;
             const bool data = row < ROWS && col < RB;
             const int lcol = CPERM ? cgroup_of_pos<RB>(col / 32) * 32 + col % 32 : col;
-            off[j] = data ? (PERM ? tile_row_at(row) : row) * RB + lcol : 0;
+            off[j] = data ? (PERM ? tile_row_at<RB>(row) : row) * RB + lcol : 0;
         }
     }
     __device__ __forceinline__ void issue(char* lds, const char* g, int wave) const {
@@ -386,7 +403,7 @@ struct async_tile {
         for (int j = 0; j < PER_WAVE; ++j) {
             const int p = (wave * PER_WAVE + j) * 1024 + lane * 16;
             const int row = p / STRIDE;                    // LDS slot
-            const int grow = PERM ? tile_row_at(row) : row;
+            const int grow = PERM ? tile_row_at<RB>(row) : row;
             dma16(l0 + (wave * PER_WAVE + j) * 1024, g, (row < ROWS && grow < rows) ? off[j] : (off[j] % RB));
         }
     }
@@ -415,12 +432,11 @@ __device__ __forceinline__ void lds_frag_tr(frag_bf16& f, const char* tile, int 
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
         // k0 and m0 are multiples of 16 and 32: the slot permutation acts
-        // on the lane's part y < 16 of the index only (tile_slot(y) =
-        // 8(G/2) + 2(i/4) + r), and column group m0/16 + G%2 sits at
-        // position (G%2) RB/64 + m0/32, so the address is a per-lane offset
-        // plus the constant k0 (RB + 16) + m0
-        const int y = 8 * (G >> 1) + 4 * r + (i >> 2);
-        const int row = k0 + (PERM ? tile_slot(y) : y);
+        // on the lane's part y = 8(G/2) + 4r + i/4 < 16 of the index only,
+        // where it adds r to a per-lane row, and column group m0/16 + G%2
+        // sits at position (G%2) RB/64 + m0/32, so the address is a per-lane
+        // offset plus the constant (k0 + r)(RB + 16) + m0
+        const int row = k0 + (PERM ? tile_slot_of<RB>(G >> 1, r, i >> 2) : 8 * (G >> 1) + 4 * r + (i >> 2));
         const int grp = (G & 1) * (RB / 64) + (m0 >> 5);
         const char* p = tile + row * (RB + 16) + grp * 32 + 8 * (i & 3);
         r2[r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p));
@@ -438,7 +454,7 @@ __device__ __forceinline__ void lds_frag_tr(frag_f32& f, const char* tile, int m
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
         const int k = k0 + 8 * (l >> 5) + s;
-        const int row = PERM ? tile_slot(k) : k;
+        const int row = PERM ? tile_slot<RB>(k) : k;
         f.v[s] = *reinterpret_cast<const float*>(tile + row * (RB + 16) + m * 4);
     }
 }
@@ -449,12 +465,12 @@ __device__ __forceinline__ void lds_frag_tr(frag_f32& f, const char* tile, int m
 // column-group order above).
 template <int RB>
 __device__ __forceinline__ void lds_frag_s(frag_bf16& f, const char* tile, int s, int e0) {
-    const int row = tile_slot(swap_bits_2_3(s));
+    const int row = tile_slot<RB>(swap_bits_2_3(s));
     load_frag(f, tile + row * (RB + 16) + cgroup_pos<RB>(e0 >> 4) * 32 + (e0 & 15) * 2);
 }
 template <int RB>
 __device__ __forceinline__ void lds_frag_s(frag_f32& f, const char* tile, int s, int e0) {
-    const int row = tile_slot(swap_bits_2_3(s));
+    const int row = tile_slot<RB>(swap_bits_2_3(s));
     const float4 a = *reinterpret_cast<const float4*>(tile + row * (RB + 16) + e0 * 4);
     const float4 b = *reinterpret_cast<const float4*>(tile + row * (RB + 16) + e0 * 4 + 16);
     f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
