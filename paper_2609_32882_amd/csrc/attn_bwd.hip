@@ -86,8 +86,10 @@ __global__ __launch_bounds__(256) void stat_kernel(const T* __restrict__ o, cons
 // padding keys get dK = dV = 0 and padding queries (scaled LSE = +inf) add
 // nothing.  (PAD: the grid is padded; the masking is compiled only into
 // that variant.)  bf16: on block pairs that touch a large-magnitude block
-// (this key block's flag or the query block's) P and dS enter the dV and
-// dK products as two bf16 terms (hi + lo).
+// (this key block's flag or the query block's) P enters the dV product as
+// two bf16 terms (hi + lo); dS enters the dK product as two terms on those
+// pairs and on every pair of a query block whose row touches a flagged
+// block (the row flag).
 // ---------------------------------------------------------------------------
 template <typename T, int D, bool PAD>
 __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
@@ -142,13 +144,14 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
         if (ent < 0 || ent / N >= grp) return -1;
         return qrow0 + ent;
     };
-    // two-term operands on every pair of a flagged key block; otherwise on
-    // the pairs whose query block is flagged (per-pair flags are read only
-    // when the KV group holds a flagged query block)
+    // two-term operands on every pair of a flagged key block; otherwise P on
+    // the pairs whose query block is flagged and dS on the pairs whose query
+    // block has the row flag (per-pair flags are read only when some query
+    // block of the KV group has the row flag, which its own flag implies)
     bool all_big = false, some_big = false;
     if constexpr (SPLIT) {
         all_big = byte_of(scalar_load_i32(byte_word(fl.kv, krow)), krow);
-        some_big = !all_big && scalar_load_i32(fl.any_q + bkv) != 0;
+        some_big = !all_big && scalar_load_i32(fl.any_row + bkv) != 0;
     }
     const RT rt(wave, lane);
     // Q, dO and the statistics of the 64 queries of query-block row qr (512
@@ -201,15 +204,17 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
         for (int64_t j = 0; j < cnt; ++j) {
             const int buf = static_cast<int>(j & 1);
             const bool has_next = j + 1 < cnt;
-            // the next list entry, and the current query block's flag with it
+            // the next list entry, and the current query block's flags with it
             int64_t q_next = -1;
-            bool big = FL && all_big;
+            bool big_p = FL && all_big, big_s = FL && all_big;
             if (FL && some_big && q_cur >= 0) {
                 int32_t ent = -1, w = 0;
-                if (has_next) scalar_load2_i32(kv_idx + entry(j + 1), byte_word(fl.q, q_cur), ent, w);
-                else w = scalar_load_i32(byte_word(fl.q, q_cur));
+                if (has_next) scalar_load2_i32(kv_idx + entry(j + 1), byte_word(fl.qrow, q_cur), ent, w);
+                else w = scalar_load_i32(byte_word(fl.qrow, q_cur));
                 q_next = has_next ? qrow_of(ent) : -1;
-                big = byte_of(w, q_cur);
+                const int code = byte_val(w, q_cur);
+                big_p = (code & 1) != 0;
+                big_s = (code & 2) != 0;
             } else if (has_next) {
                 q_next = qrow_of(scalar_load_i32(kv_idx + entry(j + 1)));
             }
@@ -230,11 +235,11 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
             // own independent work is all there is to overlap).  LDS operand
             // fragments are requested one step ahead of their MFMAs;
             // lds_order keeps the compiler from moving work across steps.
-            // two (wave-uniform): P and dS as hi + lo, a second dV / dK product
-            // with the lo terms.  One code path with the lo steps behind scalar
-            // branches: two inlined variants of the loop raise the kernel's
-            // register allocation for both.
-            auto pair = [&](bool two) {
+            // two_p, two_s (wave-uniform): P (dS) as hi + lo, a second dV (dK)
+            // product with the lo terms.  One code path with the lo steps behind
+            // scalar branches: inlined variants of the loop raise the kernel's
+            // register allocation for all of them.
+            auto pair = [&](bool two_p, bool two_s) {
                 constexpr int NB = KS / 2;           // S/dP steps per tile (2 k-steps each)
                 constexpr int NU = 2 * MT;           // dV/dK steps per tile
                 constexpr int EV = 16 / NB;          // P,dS elements per S/dP step
@@ -282,13 +287,10 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
                         float xp[8], xd[8];
     #pragma unroll
                         for (int i = 0; i < 8; ++i) { xp[i] = s[t][8 * h + i]; xd[i] = dp[t][8 * h + i]; }
-                        if (SPLIT && two) {
-                            pack_frag_hilo(pb[t][h], pl[t][SPLIT ? h : 0], xp);
-                            pack_frag_hilo(db[t][h], dl[t][SPLIT ? h : 0], xd);
-                        } else {
-                            pack_frag(pb[t][h], xp);
-                            pack_frag(db[t][h], xd);
-                        }
+                        if (SPLIT && two_p) pack_frag_hilo(pb[t][h], pl[t][SPLIT ? h : 0], xp);
+                        else pack_frag(pb[t][h], xp);
+                        if (SPLIT && two_s) pack_frag_hilo(db[t][h], dl[t][SPLIT ? h : 0], xd);
+                        else pack_frag(db[t][h], xd);
                     }
                 };
                 F fa[2][4];
@@ -330,13 +332,13 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
                     lds_order();
                     const int h = u / MT, mt = u % MT;
                     mma(acc_v[mt], ta[k & 1][0], pb[t][h]);
-                    if (SPLIT && two) mma(acc_v[mt], ta[k & 1][0], pl[t][SPLIT ? h : 0]);
+                    if (SPLIT && two_p) mma(acc_v[mt], ta[k & 1][0], pl[t][SPLIT ? h : 0]);
                     mma(acc_k[mt], ta[k & 1][1], db[t][h]);
-                    if (SPLIT && two) mma(acc_k[mt], ta[k & 1][1], dl[t][SPLIT ? h : 0]);
+                    if (SPLIT && two_s) mma(acc_k[mt], ta[k & 1][1], dl[t][SPLIT ? h : 0]);
                     if (t == 0) softmax_grad(1, u * EU, EU);
                 }
             };
-            if (q_cur >= 0) pair(FL && big);
+            if (q_cur >= 0) pair(FL && big_p, FL && big_s);
             q_cur = q_next;
         }
     };
@@ -373,8 +375,9 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
 // dQ: one workgroup (2 waves) per query block; wave owns 32 queries.
 // Tiles K (for S^T and, read transposed, K^T) and V (for dP^T).  On a
 // padded grid, padding keys get P = 0 and padding queries dQ = 0 (PAD
-// variant only).  bf16: on block pairs that touch a large-magnitude block
-// dS enters the dQ product as two bf16 terms (hi + lo).
+// variant only).  bf16: when this query block's row touches a
+// large-magnitude block (its own flag or a listed key block's), dS enters
+// every dQ product of the row as two bf16 terms (hi + lo).
 // ---------------------------------------------------------------------------
 template <typename T, int D, bool PAD>
 __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
@@ -437,14 +440,21 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
         const int c = scalar_load_i32(col_idx + e);
         return (c >= 0 && c < N) ? c : -1;
     };
-    // two-term dS on every pair of a flagged query block; otherwise on the
-    // pairs whose key block is flagged (per-pair flags are read only when the
-    // head holds a flagged key block)
+    // two-term dS on every pair of a row that touches a flagged block: the
+    // query block's own flag, else (only when the head holds a flagged key
+    // block) a scan of the listed key blocks' flags, 64 entries per step
     const int64_t kvrow0 = static_cast<int64_t>(b * Hkv + hkv) * N;
-    bool all_big = false, some_big = false;
+    bool big = false;
     if constexpr (SPLIT) {
-        all_big = byte_of(scalar_load_i32(byte_word(fl.q, row)), row);
-        some_big = !all_big && scalar_load_i32(fl.any_kv + b * Hkv + hkv) != 0;
+        big = byte_of(scalar_load_i32(byte_word(fl.q, row)), row);
+        if (!big && scalar_load_i32(fl.any_kv + b * Hkv + hkv) != 0) {
+            bool hit = false;
+            for (int64_t e = e0 + lane; e < e1; e += 64) {
+                const int c = col_idx[e];
+                if (c >= 0 && c < N && fl.kv[kvrow0 + c]) hit = true;
+            }
+            big = __any(hit);
+        }
     }
     constexpr int64_t TILE = 64 * RB;
     const RT rt(wave, lane);
@@ -469,19 +479,7 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
     }
     for (int64_t j = 0; j < cnt; ++j) {
         const bool has_next = j + 1 < cnt;
-        // the next list entry, and the current key block's flag with it
-        int c_next = -1;
-        bool big = all_big;
-        if (SPLIT && some_big && c_cur >= 0) {
-            const int64_t fi = kvrow0 + c_cur;
-            int32_t e = -1, w = 0;
-            if (has_next) scalar_load2_i32(col_idx + entry(j + 1), byte_word(fl.kv, fi), e, w);
-            else w = scalar_load_i32(byte_word(fl.kv, fi));
-            c_next = (e >= 0 && e < N) ? e : -1;
-            big = byte_of(w, fi);
-        } else if (has_next) {
-            c_next = block_of(entry(j + 1));
-        }
+        const int c_next = has_next ? block_of(entry(j + 1)) : -1;
 
         vm_wait<0>();                   // K and V landed
         wg_barrier();
@@ -639,6 +637,10 @@ static hipError_t launch_dkdv_t(const void* q, const void* k, const void* v, con
     const float c = kLog2e / sqrtf(static_cast<float>(D));
     const float scale = 1.0f / sqrtf(static_cast<float>(D));
     const block_flag_layout fl = bwd_flags(ws, batch, Hq, Hkv, N);
+    if constexpr (sizeof(T) == 2) {   // the row flags of the query blocks (two-term dS)
+        e = launch_row_flags(fl, kv_ptr, kv_idx, col_cap, static_cast<int64_t>(batch) * Hq * N, krows, N, Hq, Hkv, s);
+        if (e != hipSuccess) return e;
+    }
     auto go = [&](auto pad) {
         hipLaunchKernelGGL((dkdv_kernel<T, D, decltype(pad)::value>), dim3(static_cast<unsigned>(krows)),
                            dim3(AB_NT), 0, s, static_cast<const T*>(q), static_cast<const T*>(k),

@@ -87,7 +87,7 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int i = 0; i < 16; ++i) oacc[mt][i] = 0.f;
-    float m = -INFINITY, l = 0.f;
+    float m = -INFINITY, l = 0.f, lr = 0.f;   // row sums of p: exact (LSE), as rounded for the products (O)
 
     // entries outside [0, N) are loaded as block 0 and then ignored
     auto block_of = [&](int64_t e) -> int {
@@ -199,6 +199,7 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
                     const float mn = fmaxf(m, mx);
                     const float alpha = fast_exp2(m - mn);
                     l *= alpha;
+                    lr *= alpha;
     #pragma unroll
                     for (int mt = 0; mt < MT; ++mt)
     #pragma unroll
@@ -218,7 +219,15 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
                 // second pass adds V^T lo (its fragments read again).
                 F pb[4], pl[SPLIT ? 4 : 1];
                 const bool two = SPLIT && FL && big;
-                float ps = 0.f;
+                float ps = 0.f, pr = 0.f;
+                // Two row sums: ps of the probabilities themselves (for the
+                // LSE, which the backward's recomputed P relies on) and pr of
+                // the probabilities as the products take them (rounded to the
+                // input dtype; hi + lo on a two-term pair).  O = sum p V / pr
+                // is a weighted mean of V with exactly the weights the MFMAs
+                // used, so a component that all value rows share passes
+                // through without P's rounding error (which would otherwise
+                // reach Delta = dO . O in the backward).
                 auto make_p = [&](int kk) {
                     float pv8[8];
     #pragma unroll
@@ -227,8 +236,13 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
                         pv8[i] = p;
                         ps += p;
                     }
-                    if (two) pack_frag_hilo(pb[kk], pl[SPLIT ? kk : 0], pv8);
-                    else pack_frag(pb[kk], pv8);
+                    if (two) {
+                        pack_frag_hilo(pb[kk], pl[SPLIT ? kk : 0], pv8);
+                        pr = frag_sum(pl[SPLIT ? kk : 0], pr);
+                    } else {
+                        pack_frag(pb[kk], pv8);
+                    }
+                    pr = frag_sum(pb[kk], pr);
                 };
                 F fa[2][MT];
                 auto fetch = [&](F* f, int kk) {
@@ -246,6 +260,7 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
                     if (kk + 1 < 4) make_p(kk + 1);
                 }
                 l += ps;
+                lr += pr;
                 if constexpr (SPLIT) {
                     if (two) {
                         fetch(fa[0], 0);
@@ -268,7 +283,8 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
     else walk(std::false_type{});
 
     const float lt = q_real ? l + swap_half(l) : 0.f;     // a padding query has no output
-    const float inv = lt > 0.f ? 1.0f / lt : 0.f;
+    const float lrt = q_real ? lr + swap_half(lr) : 0.f;
+    const float inv = lrt > 0.f ? 1.0f / lrt : 0.f;
     T* orow = o + qtok * D;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)

@@ -126,6 +126,28 @@ __device__ __forceinline__ void pack_frag_hilo(frag_f32& hi, frag_f32& lo, const
     for (int i = 0; i < 8; ++i) { hi.v[i] = x[i]; lo.v[i] = 0.f; }
 }
 
+// acc plus the sum of a fragment's 8 values as stored (bf16: four v_dot2
+// against (1, 1), which add the rounded values in fp32).  Each word goes
+// through a scalar first: this compiler turns __builtin_bit_cast of a
+// vector element inside an unrolled loop into a cast of element 0.
+__device__ __forceinline__ float frag_sum(const frag_bf16& f, float acc) {
+    typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4_t;
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    const u32x4_t w = __builtin_bit_cast(u32x4_t, f.v);
+    const bf16x2_t one = __builtin_bit_cast(bf16x2_t, 0x3f803f80u);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t word = w[i];
+        acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, word), one, acc, false);
+    }
+    return acc;
+}
+__device__ __forceinline__ float frag_sum(const frag_f32& f, float acc) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc += f.v[i];
+    return acc;
+}
+
 // Make the compiler complete the loads of a fragment here (an opaque use of
 // its registers), so no wait for them is left inside a later loop.
 __device__ __forceinline__ void settle(const frag_bf16& f) {
@@ -289,6 +311,7 @@ __device__ __forceinline__ const int32_t* byte_word(const uint8_t* p, int64_t i)
     return reinterpret_cast<const int32_t*>(p + (i & ~int64_t(3)));
 }
 __device__ __forceinline__ bool byte_of(int32_t w, int64_t i) { return ((w >> (8 * (i & 3))) & 0xff) != 0; }
+__device__ __forceinline__ int byte_val(int32_t w, int64_t i) { return (w >> (8 * (i & 3))) & 0xff; }
 
 // One global_load_lds_dwordx4: lane l copies 16 bytes from base + voff(l) to
 // LDS byte address lds + 16 l.  Issued as inline assembly so that the

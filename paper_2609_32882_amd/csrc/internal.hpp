@@ -111,11 +111,15 @@ struct block_flag_layout {
     uint8_t* kv;
     int32_t* any_q;
     int32_t* any_kv;
+    uint8_t* qrow;       // per query block: bit 0 its own flag, bit 1 its row touches a flagged block
+    int32_t* any_row;    // per KV group: some query block of the group has bit 1
 };
 block_flag_layout block_flags_at(void* base, int64_t rows_q, int64_t rows_kv, int64_t groups);
 size_t block_flags_bytes(int64_t rows_q, int64_t rows_kv, int64_t groups);
 hipError_t launch_block_flags(const void* q, const void* k, const void* v, const block_flag_layout& f, int64_t rows_q,
                               int64_t rows_kv, int N, int D, int Hq, int Hkv, const cube_grid& cg, hipStream_t s);
+hipError_t launch_row_flags(const block_flag_layout& f, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
+                            int64_t rows_q, int64_t rows_kv, int N, int Hq, int Hkv, hipStream_t s);
 hipError_t launch_attn_bwd(int dtype, int D, const void* q, const void* k, const void* v, const void* o,
                            const float* lse, const void* o_lo, const void* dout, const int32_t* row_ptr,
                            const int32_t* col_idx, const int32_t* kv_ptr, const int32_t* kv_idx,

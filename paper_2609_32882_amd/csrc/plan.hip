@@ -160,6 +160,16 @@ namespace vsa2 {
 // b*Hkv + h one word "some query block of the group's query heads is
 // flagged" and one word "some key block of the head is flagged", so a kernel
 // whose head has no flagged block reads no per-pair flag.
+//
+// Row flags (the backward's dS): dS = P (dP - Delta), and Delta = dO . O is
+// large in every row that attends to a large-magnitude block, so the dS of
+// that row's other pairs are large as well even where both blocks of the
+// pair are small; rounded to one bf16 term they add an error coherent along
+// the queries' (keys') common component to dK (dQ).  The backward therefore
+// takes two-term dS on every pair of a query block whose row touches a
+// flagged block (its own flag included), and keeps the pair rule for P.
+// One byte per query block: bit 0 its own flag, bit 1 the row flag; one
+// word per KV group: some query block of the group has the row flag.
 // ---------------------------------------------------------------------------
 constexpr uint32_t SCALE_FLAG_BF16_BITS = 0x4100u;   // 8.0 in bf16
 
@@ -222,6 +232,53 @@ __global__ __launch_bounds__(256) void zero_i32_kernel(int32_t* __restrict__ p, 
     if (i < n) p[i] = 0;
 }
 
+// Row flags, first step: byte = 3 for a flagged query block, 0 otherwise;
+// the group word is set for a flagged query block.
+__global__ __launch_bounds__(256) void row_flag_init_kernel(const uint8_t* __restrict__ flag_q,
+                                                            uint8_t* __restrict__ qrow, int32_t* __restrict__ any_row,
+                                                            int64_t rows_q, int N, int Hq, int Hkv) {
+    const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (r >= rows_q) return;
+    const bool f = flag_q[r] != 0;
+    qrow[r] = f ? 3 : 0;
+    if (f) {     // every writer stores the same value
+        const int64_t bh = r / N;
+        any_row[(bh / Hq) * Hkv + (bh % Hq) / (Hq / Hkv)] = 1;
+    }
+}
+
+// Row flags, second step: one wave per key block; a flagged key block sets
+// bit 1 of every query block in its transposed list (entries
+// hq_local * N + n_q, as the dK/dV kernel reads them; entries outside
+// [0, grp*N) are skipped).  Concurrent writers of one byte all store
+// (bit 0 from the first step) | 2, so the result does not depend on order.
+__global__ __launch_bounds__(256) void row_flag_scatter_kernel(const uint8_t* __restrict__ flag_kv,
+                                                               const int32_t* __restrict__ kv_ptr,
+                                                               const int32_t* __restrict__ kv_idx, int64_t col_cap,
+                                                               uint8_t* __restrict__ qrow,
+                                                               int32_t* __restrict__ any_row, int64_t rows_kv, int N,
+                                                               int Hq, int Hkv) {
+    const int lane = threadIdx.x & 63;
+    const int64_t r = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+    if (r >= rows_kv || !flag_kv[r]) return;          // wave-uniform
+    int64_t e0 = kv_ptr[r], e1 = kv_ptr[r + 1];
+    e0 = e0 < 0 ? 0 : (e0 > col_cap ? col_cap : e0);
+    e1 = e1 < e0 ? e0 : (e1 > col_cap ? col_cap : e1);
+    const int grp = Hq / Hkv;
+    const int64_t bkv = r / N;
+    const int64_t b = bkv / Hkv, hkv = bkv % Hkv;
+    const int64_t qrow0 = (b * Hq + hkv * grp) * N;
+    bool any = false;
+    for (int64_t e = e0 + lane; e < e1; e += 64) {
+        const int ent = kv_idx[e];
+        if (ent < 0 || ent / N >= grp) continue;
+        uint8_t* c = qrow + qrow0 + ent;
+        *c = static_cast<uint8_t>(*c | 2);
+        any = true;
+    }
+    if (__any(any) && lane == 0) any_row[bkv] = 1;
+}
+
 static size_t flag_align(size_t x) { return (x + 255) / 256 * 256; }
 
 // Each array starts on a 256-byte boundary, so the kernels' 32-bit reads of
@@ -233,11 +290,13 @@ block_flag_layout block_flags_at(void* base, int64_t rows_q, int64_t rows_kv, in
     f.kv = reinterpret_cast<uint8_t*>(b + flag_align(rows_q));
     f.any_q = reinterpret_cast<int32_t*>(b + flag_align(rows_q) + flag_align(rows_kv));
     f.any_kv = f.any_q + groups;
+    f.qrow = reinterpret_cast<uint8_t*>(b + flag_align(rows_q) + flag_align(rows_kv) + flag_align(8 * groups));
+    f.any_row = reinterpret_cast<int32_t*>(b + 2 * flag_align(rows_q) + flag_align(rows_kv) + flag_align(8 * groups));
     return f;
 }
 
 size_t block_flags_bytes(int64_t rows_q, int64_t rows_kv, int64_t groups) {
-    return flag_align(rows_q) + flag_align(rows_kv) + flag_align(8 * groups);
+    return 2 * flag_align(rows_q) + flag_align(rows_kv) + flag_align(8 * groups) + flag_align(4 * groups);
 }
 
 hipError_t launch_block_flags(const void* q, const void* k, const void* v, const block_flag_layout& f, int64_t rows_q,
@@ -251,6 +310,21 @@ hipError_t launch_block_flags(const void* q, const void* k, const void* v, const
                        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                        static_cast<const uint16_t*>(v), f.q, f.kv, f.any_q, f.any_kv, rows_q, rows_kv, N, D, Hq, Hkv,
                        cg);
+    return hipGetLastError();
+}
+
+// Row flags from the block flags (which the same workspace already holds)
+// and the transposed lists.
+hipError_t launch_row_flags(const block_flag_layout& f, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
+                            int64_t rows_q, int64_t rows_kv, int N, int Hq, int Hkv, hipStream_t s) {
+    if (rows_q <= 0 || rows_kv <= 0) return hipSuccess;
+    const int64_t groups = rows_kv / N;
+    hipLaunchKernelGGL(zero_i32_kernel, dim3(static_cast<unsigned>((groups + 255) / 256)), dim3(256), 0, s,
+                       f.any_row, groups);
+    hipLaunchKernelGGL(row_flag_init_kernel, dim3(static_cast<unsigned>((rows_q + 255) / 256)), dim3(256), 0, s,
+                       f.q, f.qrow, f.any_row, rows_q, N, Hq, Hkv);
+    hipLaunchKernelGGL(row_flag_scatter_kernel, dim3(static_cast<unsigned>((rows_kv + 3) / 4)), dim3(256), 0, s,
+                       f.kv, kv_ptr, kv_idx, col_cap, f.qrow, f.any_row, rows_kv, N, Hq, Hkv);
     return hipGetLastError();
 }
 

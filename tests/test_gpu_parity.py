@@ -273,11 +273,14 @@ def test_bwd_deterministic_sentinels_and_unselected_blocks(case):
 
 
 def test_block_flags_rule():
-    """The large-magnitude flags the backward's prep stage writes (index
-    work, bit-exact): a block is flagged iff a real token holds a value above
-    8 in magnitude (8 itself is not), padding tokens never count, K and V
-    flag their key block together, and the per-KV-group summary words say
-    whether any block of the group is flagged."""
+    """The large-magnitude flags the backward writes (index work, bit-exact):
+    a block is flagged iff a real token holds a value above 8 in magnitude
+    (8 itself is not), padding tokens never count, K and V flag their key
+    block together, and the per-KV-group summary words say whether any block
+    of the group is flagged (prep stage); the row byte of a query block
+    holds its own flag (bit 0) and whether its block list touches a flagged
+    block, its own flag included (bit 1), with one word per KV group saying
+    whether any of the group's query blocks has bit 1 (dK/dV stage)."""
     a256 = lambda n: (n + 255) // 256 * 256
     for name in ("bf16-padded", "bf16-d64-gqa", "bf16-mass"):
         w = CASES[name]
@@ -302,6 +305,13 @@ def test_block_flags_rule():
                                      o.data_ptr(), lse.data_ptr(), o.data_ptr(), dev["do"].data_ptr(),
                                      bws.data_ptr(), bwsb, 0)
         assert st == 0
+        ref = oracle.route(x["q"], x["k"], p, w.select)
+        lists = {k: torch.from_numpy(ref[k]).cuda() for k in ("kv_ptr", "kv_idx")}
+        dk, dv = torch.empty_like(dev["k"]), torch.empty_like(dev["v"])
+        st = vsa2.vsa2_attn_bwd_dkdv(P, dev["q"].data_ptr(), dev["k"].data_ptr(), dev["v"].data_ptr(),
+                                     dev["do"].data_ptr(), lists["kv_ptr"].data_ptr(), lists["kv_idx"].data_ptr(),
+                                     lists["kv_idx"].numel(), dk.data_ptr(), dv.data_ptr(), bws.data_ptr(), bwsb, 0)
+        assert st == 0
         torch.cuda.synchronize()
         nq, nkv, groups = p.batch * p.heads_q * p.N, p.batch * p.heads_kv * p.N, p.batch * p.heads_kv
         off = a256(8 * nq * p.B) + a256(4 * nq) + a256(4 * nkv)
@@ -318,6 +328,20 @@ def test_block_flags_rule():
         any_kv = fkv.reshape(groups, p.N).any(-1)
         assert np.array_equal(words[:groups], any_q.astype(np.int32))
         assert np.array_equal(words[groups:], any_kv.astype(np.int32))
+        # row flags: own flag, or some block of the row's list flagged
+        rp, ci = ref["row_ptr"], ref["col_idx"]
+        fq_flat, fkv_flat = fq.reshape(-1), fkv.reshape(-1)
+        rowf = np.zeros(nq, bool)
+        for r in range(nq):
+            bh = r // p.N
+            kvbase = ((bh // p.heads_q) * p.heads_kv + (bh % p.heads_q) // grp) * p.N
+            rowf[r] = fq_flat[r] or fkv_flat[kvbase + ci[rp[r]:rp[r + 1]]].any()
+        qoff = off + a256(nq) + a256(nkv) + a256(8 * groups)
+        got_row = raw[qoff:qoff + nq]
+        any_row = raw[qoff + a256(nq):][:4 * groups].view(np.int32)
+        print("   row flags: %d / %d query blocks" % (int(rowf.sum()), nq))
+        assert np.array_equal(got_row, (fq_flat.astype(np.uint8) | (2 * rowf).astype(np.uint8)))
+        assert np.array_equal(any_row, rowf.reshape(p.batch, p.heads_kv, grp * p.N).any(-1).reshape(-1).astype(np.int32))
         assert fq.reshape(-1)[p.heads_q * p.N - 1] and fkv[0, 0, tok[200] // p.B]
 
 
