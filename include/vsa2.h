@@ -207,7 +207,8 @@ vsa2_status vsa2_route(const vsa2_problem* p, const vsa2_select* s,
 /* Bytes of workspace vsa2_attn_fwd (pass 0: the work order, one int32 per
  * CSR row, and one byte per query and key block for the large-magnitude
  * flags), vsa2_attn_bwd (pass 1: two fp32 values per query token, its LSE
- * and its Delta, the work orders of the CSR and CSC rows and the flags) or
+ * and its Delta, the work orders of the CSR and CSC rows, the flags and one
+ * more byte per query block for the row flags, see vsa2_attn_bwd) or
  * vsa2_coarse_bwd (pass 2: one fp32 pair per coarse query) needs.  The
  * work order lists the rows of each XCD's range longest first (a stable
  * counting sort by length class), so the launch's last workgroups are
@@ -229,6 +230,9 @@ vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* byt
  *   o   [batch][Hq][L][D] output, dtype p->dtype.
  *   lse [batch][Hq][L] fp32 natural-log log-sum-exp of each query's scaled
  *       scores; a query block with no selected block gets o = 0, lse = -inf.
+ *       O is the sum of p V over the sum of p as the products take them
+ *       (rounded to the input dtype), a weighted mean with the weights the
+ *       products used; lse uses the unrounded sum.
  *   o_lo  optional [batch][Hq][L][D] (dtype p->dtype): NULL for a forward
  *       that no backward follows (inference).  When given, the call writes
  *       the rounding remainder of O (o + o_lo ~ the fp32 result, about 16
@@ -288,8 +292,11 @@ vsa2_status vsa2_attn_fwd_noalloc(const vsa2_problem* p, const void* q, const vo
  * group) whose block selected j's block.
  *   q, k, v, o, lse   as for vsa2_attn_fwd (o, lse from the forward call)
  *   o_lo  required: the forward's o_lo (Delta uses o + o_lo).  On block
- *         pairs that touch a large-magnitude block (see vsa2_attn_fwd) P and
- *         dS enter the dV, dK and dQ products as two bf16 terms.
+ *         pairs that touch a large-magnitude block (see vsa2_attn_fwd) P
+ *         enters the dV product as two bf16 terms; dS enters the dK and dQ
+ *         products as two terms on every pair of a query block whose list
+ *         touches a large-magnitude block (its own flag included): Delta is
+ *         large in such a row, and with it every dS of the row.
  *   dout  [batch][Hq][L][D]  dO
  *   row_ptr, col_idx  the CSR; kv_ptr, kv_idx its transpose (vsa2_route)
  *   dq [batch][Hq][L][D], dk, dv [batch][Hkv][L][D]  outputs, dtype p->dtype;
@@ -322,7 +329,8 @@ vsa2_status vsa2_attn_bwd_prep(const vsa2_problem* p, const void* q, const void*
  * vsa2_attn_bwd_dkdv - dK and dV of vsa2_attn_bwd, one key block at a time
  *   over the query blocks of its transposed list (kv_ptr, kv_idx).
  *   ws           as written by vsa2_attn_bwd_prep (this stage also writes
- *                its work order there).
+ *                its work order and the query blocks' row flags there; the
+ *                dQ stage derives its rows' flags from its own lists).
  *   dk, dv       [batch][Hkv][L][D] outputs, dtype p->dtype.
  */
 vsa2_status vsa2_attn_bwd_dkdv(const vsa2_problem* p, const void* q, const void* k, const void* v,
