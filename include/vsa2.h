@@ -240,7 +240,7 @@ vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* byt
  *       pairs that touch a large-magnitude block (below) P enters the P.V
  *       product as two bf16 terms, so O itself carries about 16 bits there.
  *   Large-magnitude blocks (bf16 problems): a 64-token block of Q, or of K
- *       and V together, holding a real-token value above 8 in magnitude.
+ *       and V together, holding a real-token value above 7 in magnitude.
  *       bf16 products round P and dS to 8 significant bits; when the tokens
  *       of a block share a large common component those rounding errors add
  *       up along it instead of cancelling, so block pairs that touch such a

@@ -171,7 +171,7 @@ namespace vsa2 {
 // One byte per query block: bit 0 its own flag, bit 1 the row flag; one
 // word per KV group: some query block of the group has the row flag.
 // ---------------------------------------------------------------------------
-constexpr uint32_t SCALE_FLAG_BF16_BITS = 0x4100u;   // 8.0 in bf16
+constexpr uint32_t SCALE_FLAG_BF16_BITS = 0x40E0u;   // 7.0 in bf16
 
 __global__ __launch_bounds__(256) void block_flag_kernel(const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                                                          const uint16_t* __restrict__ v, uint8_t* __restrict__ flag_q,

@@ -22,7 +22,7 @@ NEAR_TIE_REL = 4e-5
 # bf16 attention: a 64-token block of Q, or of K and V together, is
 # "large-magnitude" when a real token holds a value above this; block pairs
 # that touch such a block take two-term (hi + lo) P and dS operands
-BIG_VALUE = 8.0
+BIG_VALUE = 7.0
 
 
 def block_flags(x, p):

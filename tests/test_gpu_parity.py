@@ -274,8 +274,8 @@ def test_bwd_deterministic_sentinels_and_unselected_blocks(case):
 
 def test_block_flags_rule():
     """The large-magnitude flags the backward writes (index work, bit-exact):
-    a block is flagged iff a real token holds a value above 8 in magnitude
-    (8 itself is not), padding tokens never count, K and V flag their key
+    a block is flagged iff a real token holds a value above 7 in magnitude
+    (7 itself is not), padding tokens never count, K and V flag their key
     block together, and the per-KV-group summary words say whether any block
     of the group is flagged (prep stage); the row byte of a query block
     holds its own flag (bit 0) and whether its block list touches a flagged
@@ -288,8 +288,8 @@ def test_block_flags_rule():
         x = make_inputs(w, with_grad=True)
         real = p.token_real()
         tok = np.flatnonzero(real)
-        x["q"][0, 0, tok[3], 5] = 8.0                 # exactly 8: not flagged
-        x["q"][0, p.heads_q - 1, tok[-1], 2] = -8.0625  # just above: flagged
+        x["q"][0, 0, tok[3], 5] = 7.0                 # exactly 7: not flagged
+        x["q"][0, p.heads_q - 1, tok[-1], 2] = -7.03125  # just above (next bf16 value): flagged
         x["v"][0, 0, tok[200], 0] = 9.0               # V flags its key block
         if p.padded:                                   # padding never counts
             x["k"][0, 1, np.flatnonzero(~real)[0], 7] = 100.0

@@ -65,6 +65,11 @@ REGRESSION = [
     Workload("mixed-rows-b2", Problem(2, 4, 2, 64, 6, 10, 12), Selection(0, 16), 3112, skewed=True),
     Workload("mixed-rows-cap5", Problem(2, 4, 2, 128, 2, 14, 5, Rt=4, Rh=4, Rw=4), Selection(1, 0, 0.9, 5), 3115,
              skewed=True),
+    # a query block with values up to 7.06 in a row with no flagged block
+    # and a peaked softmax (cap 2): over the bar with the magnitude threshold
+    # at 8 even under the rules above
+    Workload("near-threshold-cap2", Problem(1, 4, 2, 64, 9, 10, 11, Rt=4, Rh=4, Rw=4), Selection(1, 0, 0.9, 2), 3326,
+             skewed=True),
 ]
 
 
