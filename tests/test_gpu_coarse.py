@@ -9,6 +9,7 @@ import torch
 import oracle
 import paper_2609_32882_amd as vsa2
 from parity import assert_values, assert_values_bound, attn_fp32_logit_bounds, to_dev, to_np
+from sweep_cases import CASES as SWEEP_CASES
 from workload import BF16, F32, Problem, Selection, Workload, make_inputs
 
 pytestmark = pytest.mark.gpu
@@ -30,6 +31,10 @@ CASES = {
     "f32-d64-padded-1frame-gqa": Workload("c7", Problem(1, 4, 2, 64, 1, 18, 20, Rt=2, Rh=2, Rw=4, dtype=F32),
                                           Selection(0, 6), 3007),
 }
+
+
+# ten text-free configurations of the fine path's seeded random sweep
+CASES.update({w.name: w for w in [c for c in SWEEP_CASES if c.problem.text_len == 0][:10]})
 
 
 def dtname(p):
