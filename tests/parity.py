@@ -3,6 +3,8 @@ from __future__ import annotations
 
 import numpy as np
 
+import oracle
+
 # Parity bar for outputs and gradients (bf16 inputs, fp32 accumulation):
 # |got - ref| <= MAX_ABS + ulp_rel * |ref| element-wise, and relative L2 error
 # <= REL_L2.  The ulp_rel term is the output dtype's own rounding (outputs are
@@ -171,3 +173,36 @@ def assert_values_bound(got, ref, name, dtype, extra):
     print("%s: max (err - ulp) / (2e-2 + derived bound) = %.3f, max derived bound %.3e, rel_l2=%.3e" % (
         name, ratio, float(np.max(extra)), rel))
     assert ratio <= 1.0 and rel <= REL_L2, (name, ratio, rel)
+
+
+def check_seq_selection(p, k, rp, ci, ref_scores, exact_scores=None):
+    """GPU per-sequence top-(N k) lists against the oracle's flat sort.
+    With exact_scores (the GPU's own fp32 scores) the oracle must reproduce
+    the selection bit for bit; against the oracle's fp64 scores a pair may
+    differ only if its score lies within 1e-6 (relative) of its sequence's
+    threshold."""
+    N = p.N
+    nseq = p.batch * p.heads_q
+    keep = min(N * k, N * N)
+    got = np.zeros((nseq * N, N), bool)
+    counts = np.diff(rp)
+    assert (counts >= 0).all() and (counts <= N).all()
+    for r in range(nseq * N):
+        c = ci[rp[r]:rp[r + 1]]
+        assert (np.diff(c) > 0).all() and (c >= 0).all() and (c < N).all()
+        got[r, c] = True
+    got = got.reshape(nseq, N, N)
+    assert (got.reshape(nseq, -1).sum(1) == keep).all()
+    if exact_scores is not None:
+        want = oracle.select_seq(exact_scores.reshape(nseq, N, N).astype(np.float64), N, k)
+        assert np.array_equal(got, want)
+    want = oracle.select_seq(ref_scores.reshape(nseq, N, N), N, k)
+    sc32 = ref_scores.reshape(nseq, N * N).astype(np.float32).astype(np.float64)
+    excused = 0
+    for sq in range(nseq):
+        diff = got[sq].reshape(-1) != want[sq].reshape(-1)
+        if diff.any():
+            tau = np.sort(sc32[sq])[::-1][keep - 1]
+            assert (np.abs(sc32[sq][diff] - tau) <= 1e-6 * tau).all()
+            excused += int(diff.sum())
+    print("sequence top-k: %d sequences, %d pairs each, %d near-tie differences" % (nseq, keep, excused))

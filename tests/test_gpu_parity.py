@@ -7,7 +7,7 @@ import torch
 
 import oracle
 import paper_2609_32882_amd as vsa2
-from parity import assert_values, block_flags, compare_selection, to_dev, to_np
+from parity import assert_values, block_flags, check_seq_selection, compare_selection, to_dev, to_np
 from workload import BF16, F32, Problem, Selection, Workload, WORKLOADS, make_inputs
 
 pytestmark = pytest.mark.gpu
@@ -492,39 +492,6 @@ def test_work_order_and_ragged_rows():
         assert_values(to_np(got).reshape(want.shape), want, name + " (ragged rows)")
 
 
-def _check_seq_selection(p, k, rp, ci, ref_scores, exact_scores=None):
-    """GPU per-sequence top-(N k) lists against the oracle's flat sort.
-    With exact_scores (the GPU's own fp32 scores) the oracle must reproduce
-    the selection bit for bit; against the oracle's fp64 scores a pair may
-    differ only if its score lies within 1e-6 (relative) of its sequence's
-    threshold."""
-    N = p.N
-    nseq = p.batch * p.heads_q
-    keep = min(N * k, N * N)
-    got = np.zeros((nseq * N, N), bool)
-    counts = np.diff(rp)
-    assert (counts >= 0).all() and (counts <= N).all()
-    for r in range(nseq * N):
-        c = ci[rp[r]:rp[r + 1]]
-        assert (np.diff(c) > 0).all() and (c >= 0).all() and (c < N).all()
-        got[r, c] = True
-    got = got.reshape(nseq, N, N)
-    assert (got.reshape(nseq, -1).sum(1) == keep).all()
-    if exact_scores is not None:
-        want = oracle.select_seq(exact_scores.reshape(nseq, N, N).astype(np.float64), N, k)
-        assert np.array_equal(got, want)
-    want = oracle.select_seq(ref_scores.reshape(nseq, N, N), N, k)
-    sc32 = ref_scores.reshape(nseq, N * N).astype(np.float32).astype(np.float64)
-    excused = 0
-    for sq in range(nseq):
-        diff = got[sq].reshape(-1) != want[sq].reshape(-1)
-        if diff.any():
-            tau = np.sort(sc32[sq])[::-1][keep - 1]
-            assert (np.abs(sc32[sq][diff] - tau) <= 1e-6 * tau).all()
-            excused += int(diff.sum())
-    print("sequence top-k: %d sequences, %d pairs each, %d near-tie differences" % (nseq, keep, excused))
-
-
 @pytest.mark.parametrize("k", [3, 11])
 def test_route_sequence_topk_matches_oracle(case, k):
     w, x, ref, dev = case
@@ -535,7 +502,7 @@ def test_route_sequence_topk_matches_oracle(case, k):
     torch.cuda.synchronize()
     rp = r["row_ptr"].cpu().numpy()
     ci = r["col_idx"].cpu().numpy()
-    _check_seq_selection(p, k, rp, ci, ref["scores"], r["scores"].cpu().numpy())
+    check_seq_selection(p, k, rp, ci, ref["scores"], r["scores"].cpu().numpy())
     kp, ki = oracle.csr_to_csc(rp, ci[:rp[-1]], p)
     assert np.array_equal(r["kv_ptr"].cpu().numpy(), kp)
     assert np.array_equal(r["kv_idx"].cpu().numpy()[:rp[-1]], ki)
@@ -559,7 +526,7 @@ def test_route_sequence_topk_all_ties():
     assert (sc == sc.reshape(-1)[0]).all()
     counts = np.diff(rp).reshape(-1, N)
     assert (counts[:, :k] == N).all() and (counts[:, k:] == 0).all()
-    _check_seq_selection(p, k, rp, ci, sc.astype(np.float64), sc)
+    check_seq_selection(p, k, rp, ci, sc.astype(np.float64), sc)
     x = make_inputs(w, with_grad=False)
     d = {n: to_dev(x[n], True) for n in ("q", "k", "v")}
     o, lse = vsa2.attn_fwd(p, d["q"], d["k"], d["v"], r["row_ptr"], r["col_idx"])

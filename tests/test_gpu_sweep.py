@@ -14,9 +14,9 @@ import torch
 
 import oracle
 import paper_2609_32882_amd as vsa2
-from parity import assert_values, compare_selection, to_dev, to_np
+from parity import assert_values, check_seq_selection, compare_selection, to_dev, to_np
 from sweep_cases import CASES, REGRESSION
-from workload import BF16, make_inputs
+from workload import BF16, Selection, make_inputs
 
 pytestmark = pytest.mark.gpu
 
@@ -72,3 +72,42 @@ def test_random_configuration_against_oracle(w):
     dk_ref, dv_ref = oracle.attn_bwd_dkdv(x["q"], x["k"], x["v"], x["do"], p, lrp, lci)
     for name, got, want in (("dQ", g[0], dq_ref), ("dK", g[1], dk_ref), ("dV", g[2], dv_ref)):
         assert_values(to_np(got).reshape(want.shape), want, name, dtname(p))
+
+
+SEQ_K = {w.name: int(np.random.default_rng(w.seed).integers(1, w.problem.N + 2)) for w in CASES}
+
+
+@pytest.mark.parametrize("w", CASES, ids=[w.name for w in CASES])
+def test_random_configuration_sequence_rule(w):
+    """The per-sequence rule (the N k best pairs of each (batch, head)'s
+    N x N block-score map, k drawn per configuration, up to past N) on the
+    same configurations: the selection bit for bit against the oracle's flat
+    sort of the GPU's own scores and within the near-tie window of the
+    oracle's, the transposed lists exact, and the forward over the GPU's
+    lists (rows of 0 .. N blocks) against the oracle's."""
+    p = w.problem
+    k = SEQ_K[w.name]
+    print("\n[%s seq k=%d] %s" % (w.name, k, p), flush=True)
+    x = make_inputs(w, with_grad=False)
+    bf = p.dtype == BF16
+    dev = {n: to_dev(x[n], bf) for n in ("q", "k", "v")}
+    q_r = vsa2.pool(p, dev["q"], (p.Rt, p.Rh, p.Rw))
+    k_r = vsa2.pool(p, dev["k"], (p.Rt, p.Rh, p.Rw))
+    r = vsa2.route(p, Selection(2, k), q_r, k_r, with_scores=True)
+    torch.cuda.synchronize()
+    rp = r["row_ptr"].cpu().numpy()
+    ci = r["col_idx"].cpu().numpy()
+    ref_scores = oracle.router_scores(to_np(q_r), to_np(k_r), p)
+    check_seq_selection(p, k, rp, ci, ref_scores, r["scores"].cpu().numpy())
+    nnz = int(rp[-1])
+    kp, ki = oracle.csr_to_csc(rp, ci[:nnz], p)
+    assert np.array_equal(r["kv_ptr"].cpu().numpy(), kp)
+    assert np.array_equal(r["kv_idx"].cpu().numpy()[:nnz], ki)
+    if p.text_len:
+        lrp, lci, _, _ = oracle.joint_lists(rp, ci[:nnz], p)
+    else:
+        lrp, lci = rp, ci[:nnz]
+    o, lse = vsa2.attn_fwd(p, dev["q"], dev["k"], dev["v"], torch.from_numpy(lrp).cuda(), torch.from_numpy(lci).cuda())
+    torch.cuda.synchronize()
+    o_ref, _ = oracle.attn_fwd(x["q"], x["k"], x["v"], p, lrp, lci)
+    assert_values(to_np(o).reshape(o_ref.shape), o_ref, "O (sequence rule)", dtname(p))
