@@ -1,7 +1,8 @@
 """The allocation-free forward (vsa2_attn_fwd_noalloc, workspace in the
 library's fixed per-GPU array) against vsa2_attn_fwd with a caller
 workspace: the same bits for O, LSE and O's remainder, on two calls in a
-row, the second with a smaller problem; and the size limit."""
+row, the second with a smaller problem; captured in a HIP graph and
+replayed with other calls in between; and the size limit."""
 import numpy as np
 import pytest
 import torch
@@ -56,6 +57,53 @@ def test_noalloc_forward_matches_workspace_forward_twice():
     print("\n[no-alloc forward] %s then %s" % (CASES[0].problem, CASES[1].problem), flush=True)
     _run(CASES[0])
     _run(CASES[1])      # smaller: the array still holds the first call's larger contents
+
+
+@pytest.mark.gpu
+def test_noalloc_forward_in_a_hip_graph():
+    """The call captured in a HIP graph (it allocates nothing, so it can be):
+    three replays, each after eager work that refills the outputs with NaN
+    and runs the allocation-free forward of another problem (which rewrites
+    the library's array), give the eager call's bits every time."""
+    w, w2 = CASES
+    p, p2 = w.problem, w2.problem
+    print("\n[no-alloc forward in a graph] %s" % p, flush=True)
+
+    def setup(w):
+        p = w.problem
+        x = make_inputs(w, with_grad=False)
+        ref = oracle.route(x["q"], x["k"], p, w.select)
+        dev = {n: to_dev(x[n], True) for n in ("q", "k", "v")}
+        dev["rp"] = torch.from_numpy(ref["row_ptr"]).cuda()
+        dev["ci"] = torch.from_numpy(ref["col_idx"]).cuda()
+        dev["o"] = torch.full_like(dev["q"], float("nan"))
+        dev["o_lo"] = torch.full_like(dev["q"], float("nan"))
+        dev["lse"] = torch.full((p.batch, p.heads_q, p.L), float("nan"), device="cuda")
+        return dev
+
+    def call(P, d, stream):
+        return vsa2.vsa2_attn_fwd_noalloc(P, d["q"].data_ptr(), d["k"].data_ptr(), d["v"].data_ptr(),
+                                          d["rp"].data_ptr(), d["ci"].data_ptr(), d["ci"].numel(), d["o"].data_ptr(),
+                                          d["lse"].data_ptr(), d["o_lo"].data_ptr(), stream)
+
+    P, P2 = vsa2.problem_from(p), vsa2.problem_from(p2)
+    d, d2 = setup(w), setup(w2)
+    assert call(P, d, torch.cuda.current_stream().cuda_stream) == 0        # eager reference
+    torch.cuda.synchronize()
+    want = [t.clone() for t in (d["o"], d["lse"], d["o_lo"])]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        st = call(P, d, torch.cuda.current_stream().cuda_stream)
+    assert st == 0
+    for rep in range(3):
+        for t in (d["o"], d["lse"], d["o_lo"]):
+            t.fill_(float("nan"))
+        assert call(P2, d2, torch.cuda.current_stream().cuda_stream) == 0
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(want, (d["o"], d["lse"], d["o_lo"])):
+            assert torch.equal(_bits(a), _bits(b)), "replay %d" % rep
 
 
 def test_noalloc_forward_rejects_problems_beyond_its_array():
