@@ -195,12 +195,14 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
         q_cur = qrow_of(scalar_load_i32(kv_idx + entry(0)));
         issue(q_cur, 0);
     }
-    // The walk over the list, in two versions: FL (some pair of this row may
-    // touch a large-magnitude block) reads per-pair flags and branches to the
-    // two-term steps; the other has no flag reads or branches, so its
-    // pipeline is scheduled as one piece.
-    auto walk = [&](auto flagged) {
-        constexpr bool FL = decltype(flagged)::value;
+    // The walk over the list, in three versions: a flagged key block takes
+    // two-term P and dS on every pair (no flag reads, no branches); FL (some
+    // pair may touch a large-magnitude block or a flagged row) reads per-pair
+    // flags and branches to the two-term steps; the third has neither, so
+    // its pipeline is scheduled as one piece.
+    auto walk = [&](auto mode) {
+        constexpr int MODE = decltype(mode)::value;
+        constexpr bool FL = MODE == 1;
         for (int64_t j = 0; j < cnt; ++j) {
             const int buf = static_cast<int>(j & 1);
             const bool has_next = j + 1 < cnt;
@@ -338,12 +340,16 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
                     if (t == 0) softmax_grad(1, u * EU, EU);
                 }
             };
-            if (q_cur >= 0) pair(FL && big_p, FL && big_s);
+            if (q_cur >= 0) {
+                if constexpr (MODE == 2) pair(true, true);
+                else pair(FL && big_p, FL && big_s);
+            }
             q_cur = q_next;
         }
     };
-    if (SPLIT && (all_big || some_big)) walk(std::true_type{});
-    else walk(std::false_type{});
+    if (SPLIT && all_big) walk(std::integral_constant<int, 2>{});
+    else if (SPLIT && some_big) walk(std::integral_constant<int, 1>{});
+    else walk(std::integral_constant<int, 0>{});
 
     // lane holds key column (lane & 31) and d = 32mt + 8(v/4) + 4half + v%4
     T* krow_k = dk + ktok * D;
