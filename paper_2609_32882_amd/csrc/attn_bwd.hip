@@ -140,8 +140,9 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
     // query-block row of entry value ent ((b*Hq + h)*N + n_q), or -1 for a
     // malformed entry; its first token is row * 64
     const int64_t qrow0 = (static_cast<int64_t>(b) * Hq + hkv * grp) * N;
+    const int ent_end = grp * N;
     auto qrow_of = [&](int ent) -> int64_t {
-        if (ent < 0 || ent / N >= grp) return -1;
+        if (ent < 0 || ent >= ent_end) return -1;
         return qrow0 + ent;
     };
     // two-term operands on every pair of a flagged key block; otherwise P on

@@ -332,6 +332,43 @@ __device__ __forceinline__ void dma16(uint32_t lds, const void* base, int voff) 
                  : "memory", "m0");
 }
 
+// A run of NR (1..4) such copies on one M0 value.  The instruction's
+// offset field (13-bit signed) moves the LDS and the global address alike,
+// so copy i of the run carries offset 1024 i and writes LDS bytes
+// lds + 1024 i + 16 l.  Its global source is base + voff[i] + 1024 i: the
+// caller passes base = the tile's address - 3072 and voff[i] = the byte
+// offset + 1024 (3 - i), which keeps every voff unsigned.  One M0 write per
+// four copies instead of one per copy.
+constexpr int DMA_RUN = 4;
+constexpr int DMA_BIAS = 1024 * (DMA_RUN - 1);
+template <int NR>
+__device__ __forceinline__ void dma16_run(uint32_t lds, uint64_t base, const int* voff) {
+    static_assert(NR >= 1 && NR <= DMA_RUN, "run length");
+    const uint32_t l = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(lds)));
+    const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(base >> 32)));
+    const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(base & 0xffffffffu)));
+    const uint64_t bs = (static_cast<uint64_t>(hi) << 32) | static_cast<uint64_t>(lo);
+    if constexpr (NR == 1)
+        asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                     : : "s"(l), "v"(voff[0]), "s"(bs) : "memory", "m0");
+    else if constexpr (NR == 2)
+        asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %3\n\t"
+                     "global_load_lds_dwordx4 %2, %3 offset:1024"
+                     : : "s"(l), "v"(voff[0]), "v"(voff[1]), "s"(bs) : "memory", "m0");
+    else if constexpr (NR == 3)
+        asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %4\n\t"
+                     "global_load_lds_dwordx4 %2, %4 offset:1024\n\t"
+                     "global_load_lds_dwordx4 %3, %4 offset:2048"
+                     : : "s"(l), "v"(voff[0]), "v"(voff[1]), "v"(voff[2]), "s"(bs) : "memory", "m0");
+    else
+        asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %5\n\t"
+                     "global_load_lds_dwordx4 %2, %5 offset:1024\n\t"
+                     "global_load_lds_dwordx4 %3, %5 offset:2048\n\t"
+                     "global_load_lds_dwordx4 %4, %5 offset:3072"
+                     : : "s"(l), "v"(voff[0]), "v"(voff[1]), "v"(voff[2]), "v"(voff[3]), "s"(bs)
+                     : "memory", "m0");
+}
+
 // Start offset of a block list for a phased sweep.  Row number `local` on
 // its XCD starts at its first entry >= (local mod period) * npos / period and
 // wraps around, with period = the number of workgroups resident on one XCD
@@ -401,7 +438,10 @@ struct async_tile {
     static constexpr int BYTES = NI * 1024;        // LDS bytes to allocate
     static constexpr int PER_WAVE = NI / NW;
     static_assert(RB % 64 == 0, "row bytes");
+    // per copy j: the source byte offset within the tile, plus the run
+    // bias of dma16_run (1024 (3 - j mod 4))
     int off[PER_WAVE];
+    static constexpr int bias(int j) { return DMA_BIAS - 1024 * (j % DMA_RUN); }
 
     __device__ __forceinline__ async_tile(int wave, int lane) {
 #pragma unroll
@@ -410,13 +450,19 @@ struct async_tile {
             const int row = p / STRIDE, col = p % STRIDE;
             const bool data = row < ROWS && col < RB;
             const int lcol = CPERM ? cgroup_of_pos<RB>(col / 32) * 32 + col % 32 : col;
-            off[j] = data ? (PERM ? tile_row_at<RB>(row) : row) * RB + lcol : 0;
+            off[j] = (data ? (PERM ? tile_row_at<RB>(row) : row) * RB + lcol : 0) + bias(j);
         }
     }
     __device__ __forceinline__ void issue(char* lds, const char* g, int wave) const {
-        const uint32_t l0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)lds));
+        const uint32_t l0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void_t*)lds)) +
+                            wave * PER_WAVE * 1024;
+        const uint64_t b = reinterpret_cast<uint64_t>(g) - DMA_BIAS;
 #pragma unroll
-        for (int j = 0; j < PER_WAVE; ++j) dma16(l0 + (wave * PER_WAVE + j) * 1024, g, off[j]);
+        for (int j = 0; j < PER_WAVE; j += DMA_RUN) {
+            constexpr int R = PER_WAVE % DMA_RUN;
+            if (j + DMA_RUN <= PER_WAVE) dma16_run<DMA_RUN>(l0 + j * 1024, b, off + j);
+            else dma16_run<R == 0 ? 1 : R>(l0 + j * 1024, b, off + j);
+        }
     }
     // A tile of which only the first `rows` rows (>= 1) exist in memory: the
     // other slots are filled from the first row (never read past the end).
@@ -427,7 +473,8 @@ struct async_tile {
             const int p = (wave * PER_WAVE + j) * 1024 + lane * 16;
             const int row = p / STRIDE;                    // LDS slot
             const int grow = PERM ? tile_row_at<RB>(row) : row;
-            dma16(l0 + (wave * PER_WAVE + j) * 1024, g, (row < ROWS && grow < rows) ? off[j] : (off[j] % RB));
+            const int raw = off[j] - bias(j);
+            dma16(l0 + (wave * PER_WAVE + j) * 1024, g, (row < ROWS && grow < rows) ? raw : (raw % RB));
         }
     }
 };
