@@ -236,17 +236,21 @@ vsa2_status vsa2_attn_workspace(const vsa2_problem* p, int32_t pass, size_t* byt
  *   o_lo  optional [batch][Hq][L][D] (dtype p->dtype): NULL for a forward
  *       that no backward follows (inference).  When given, the call writes
  *       the rounding remainder of O (o + o_lo ~ the fp32 result, about 16
- *       significant bits), which vsa2_attn_bwd needs for Delta, and on block
- *       pairs that touch a large-magnitude block (below) P enters the P.V
- *       product as two bf16 terms, so O itself carries about 16 bits there.
+ *       significant bits), which vsa2_attn_bwd needs for Delta, and on every
+ *       block pair of a query block whose list touches a large-magnitude
+ *       block (below; its own flag included) P enters the P.V product as two
+ *       bf16 terms, so O itself carries about 16 bits in such a row (where
+ *       one-term P on its small pairs would still reach Delta, weighted by
+ *       how far each pair's dO . v lies from the row's mean).
  *   Large-magnitude blocks (bf16 problems): a 64-token block of Q, or of K
  *       and V together, holding a real-token value above 7 in magnitude.
  *       bf16 products round P and dS to 8 significant bits; when the tokens
  *       of a block share a large common component those rounding errors add
- *       up along it instead of cancelling, so block pairs that touch such a
- *       block take two-term (hi + lo) operands and all other pairs one-term
- *       operands.  The flags are computed on the device in each call that
- *       uses them (no host synchronisation).
+ *       up along it instead of cancelling, so the rows and block pairs that
+ *       touch such a block take two-term (hi + lo) operands (the rules of
+ *       each call are given with it) and all others one-term operands.  The
+ *       flags are computed on the device in each call that uses them (no
+ *       host synchronisation).
  *   ws, ws_bytes  workspace of vsa2_attn_workspace(p, 0) bytes, 256-byte
  *       aligned.
  * Errors: NULL pointers, shape/dtype, misalignment, small workspace.
@@ -295,8 +299,10 @@ vsa2_status vsa2_attn_fwd_noalloc(const vsa2_problem* p, const void* q, const vo
  *         pairs that touch a large-magnitude block (see vsa2_attn_fwd) P
  *         enters the dV product as two bf16 terms; dS enters the dK and dQ
  *         products as two terms on every pair of a query block whose list
- *         touches a large-magnitude block (its own flag included): Delta is
- *         large in such a row, and with it every dS of the row.
+ *         touches a large-magnitude block (its own flag included) or one of
+ *         whose queries (with attention mass) has |Delta| above 16: dS is
+ *         then a small difference of large terms, which one-term rounding
+ *         would not keep to the gradients' accuracy.
  *   dout  [batch][Hq][L][D]  dO
  *   row_ptr, col_idx  the CSR; kv_ptr, kv_idx its transpose (vsa2_route)
  *   dq [batch][Hq][L][D], dk, dv [batch][Hkv][L][D]  outputs, dtype p->dtype;

@@ -88,8 +88,9 @@ __global__ __launch_bounds__(256) void stat_kernel(const T* __restrict__ o, cons
 // that variant.)  bf16: on block pairs that touch a large-magnitude block
 // (this key block's flag or the query block's) P enters the dV product as
 // two bf16 terms (hi + lo); dS enters the dK product as two terms on those
-// pairs and on every pair of a query block whose row touches a flagged
-// block (the row flag).
+// pairs and on every pair of a query block with the row flag (its row
+// touches a flagged block, or one of its queries has |Delta| above
+// DELTA_FLAG).
 // ---------------------------------------------------------------------------
 template <typename T, int D, bool PAD>
 __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
@@ -383,8 +384,9 @@ __global__ __launch_bounds__(AB_NT, 1) void dkdv_kernel(
 // Tiles K (for S^T and, read transposed, K^T) and V (for dP^T).  On a
 // padded grid, padding keys get P = 0 and padding queries dQ = 0 (PAD
 // variant only).  bf16: when this query block's row touches a
-// large-magnitude block (its own flag or a listed key block's), dS enters
-// every dQ product of the row as two bf16 terms (hi + lo).
+// large-magnitude block (its own flag or a listed key block's) or one of
+// its queries has |Delta| above DELTA_FLAG, dS enters every dQ product of
+// the row as two bf16 terms (hi + lo).
 // ---------------------------------------------------------------------------
 template <typename T, int D, bool PAD>
 __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
@@ -447,13 +449,20 @@ __global__ __launch_bounds__(AB_NT, 2) void dq_kernel(
         const int c = scalar_load_i32(col_idx + e);
         return (c >= 0 && c < N) ? c : -1;
     };
-    // two-term dS on every pair of a row that touches a flagged block: the
-    // query block's own flag, else (only when the head holds a flagged key
-    // block) a scan of the listed key blocks' flags, 64 entries per step
+    // two-term dS on every pair of a row that touches a flagged block or
+    // has a large Delta: the query block's own flag, else a query of the
+    // block with |Delta| above DELTA_FLAG (and attention mass: scaled LSE
+    // below +inf), else (only when the head holds a flagged key block) a
+    // scan of the listed key blocks' flags, 64 entries per step.  Both waves
+    // read the same values, so the decision is the workgroup's.
     const int64_t kvrow0 = static_cast<int64_t>(b * Hkv + hkv) * N;
     bool big = false;
     if constexpr (SPLIT) {
         big = byte_of(scalar_load_i32(byte_word(fl.q, row)), row);
+        if (!big) {
+            const float ls = stat[row * 128 + lane], nd = stat[row * 128 + 64 + lane];
+            big = __any(ls != INFINITY && fabsf(nd) > DELTA_FLAG);
+        }
         if (!big && scalar_load_i32(fl.any_kv + b * Hkv + hkv) != 0) {
             bool hit = false;
             for (int64_t e = e0 + lane; e < e1; e += 64) {
@@ -645,7 +654,8 @@ static hipError_t launch_dkdv_t(const void* q, const void* k, const void* v, con
     const float scale = 1.0f / sqrtf(static_cast<float>(D));
     const block_flag_layout fl = bwd_flags(ws, batch, Hq, Hkv, N);
     if constexpr (sizeof(T) == 2) {   // the row flags of the query blocks (two-term dS)
-        e = launch_row_flags(fl, kv_ptr, kv_idx, col_cap, static_cast<int64_t>(batch) * Hq * N, krows, N, Hq, Hkv, s);
+        e = launch_row_flags(fl, static_cast<const float*>(ws), kv_ptr, kv_idx, col_cap,
+                             static_cast<int64_t>(batch) * Hq * N, krows, N, Hq, Hkv, s);
         if (e != hipSuccess) return e;
     }
     auto go = [&](auto pad) {

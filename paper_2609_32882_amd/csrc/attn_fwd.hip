@@ -28,10 +28,13 @@ constexpr int AF_NT = 128;
 
 // COMP (the forward of a training step): the rounding remainder of O is
 // written to o_lo, so that O + o_lo carries about 16 significant bits for
-// the backward's Delta = dO . O, and on block pairs that touch a
-// large-magnitude block (the query block's or the key block's flag) P
-// enters the PV product as two bf16 terms (hi + lo), which keeps O itself
-// accurate to about 16 bits there.  Other pairs take one-term P.
+// the backward's Delta = dO . O, and on every block pair of a row that
+// touches a large-magnitude block (the query block's own flag or a listed
+// key block's) P enters the PV product as two bf16 terms (hi + lo), which
+// keeps O itself accurate to about 16 bits there: in such a row the
+// rounding of P on a small pair, weighted by how far that pair's dO . V
+// lies from the row's mean, reaches Delta as well.  Other rows take
+// one-term P.
 // PAD: the grid is padded (the masking is compiled only into this variant,
 // so the unpadded one keeps its register budget).
 template <typename T, int D, bool COMP, bool PAD>
@@ -94,15 +97,22 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
         const int c = scalar_load_i32(col_idx + e);
         return (c >= 0 && c < N) ? c : -1;
     };
-    // two-term P on every pair of a flagged query block; otherwise on the
-    // pairs whose key block is flagged (per-pair flags are read only when
-    // the head holds a flagged key block)
+    // two-term P on every pair of a row that touches a flagged block: the
+    // query block's own flag, else (only when the head holds a flagged key
+    // block) a scan of the listed key blocks' flags, 64 entries per step;
+    // all of it completes before the first tile copy is issued
     const int64_t kvrow0 = static_cast<int64_t>(b * Hkv + hkv) * N;
-    bool all_big = false, some_big = false;
+    bool big = false;
     if constexpr (SPLIT) {
-        // scalar loads: the tile copies' vmcnt bookkeeping sees no other loads
-        all_big = byte_of(scalar_load_i32(byte_word(fl.q, row)), row);
-        some_big = !all_big && scalar_load_i32(fl.any_kv + b * Hkv + hkv) != 0;
+        big = byte_of(scalar_load_i32(byte_word(fl.q, row)), row);
+        if (!big && scalar_load_i32(fl.any_kv + b * Hkv + hkv) != 0) {
+            bool hit = false;
+            for (int64_t e = e0 + lane; e < e1; e += 64) {
+                const int c = col_idx[e];
+                if (c >= 0 && c < N && fl.kv[kvrow0 + c]) hit = true;
+            }
+            big = __any(hit);
+        }
     }
     const KT kt(wave, lane);
     const KT& vt_ = kt;
@@ -122,26 +132,13 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
         kt.issue(k_lds, kb + static_cast<int64_t>(cc) * 64 * KRB, wave);
         vt_.issue(v_lds, vb + static_cast<int64_t>(cc) * 64 * KRB, wave);
     }
-    // The walk in two compiled versions: FL (some pair of this row may touch
-    // a large-magnitude block) reads per-pair flags and may take two-term
-    // steps; the other has neither, so its loop is scheduled without them.
-    auto walk = [&](auto flagged) {
-        constexpr bool FL = decltype(flagged)::value;
+    // The walk in two compiled versions: TWO (every pair two-term) and the
+    // one-term walk, each scheduled as one piece.
+    auto walk = [&](auto two_term) {
+        constexpr bool TWO = decltype(two_term)::value;
         for (int64_t j = 0; j < cnt; ++j) {
             const bool has_next = j + 1 < cnt;
-            // the next list entry, and the current key block's flag with it
-            int c_next = -1;
-            bool big = FL && all_big;
-            if (FL && some_big && c_cur >= 0) {
-                const int64_t fi = kvrow0 + c_cur;
-                int32_t e = -1, w = 0;
-                if (has_next) scalar_load2_i32(col_idx + entry(j + 1), byte_word(fl.kv, fi), e, w);
-                else w = scalar_load_i32(byte_word(fl.kv, fi));
-                c_next = (e >= 0 && e < N) ? e : -1;
-                big = byte_of(w, fi);
-            } else if (has_next) {
-                c_next = block_of(entry(j + 1));
-            }
+            const int c_next = has_next ? block_of(entry(j + 1)) : -1;
             const int64_t nxt_off = static_cast<int64_t>(c_next < 0 ? 0 : c_next) * 64 * KRB;
 
             vm_wait<VT::PER_WAVE>();          // this K tile has landed (V may still stream)
@@ -218,7 +215,7 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
                 // On a flagged pair P is split into hi + lo = bf16(P - hi), and a
                 // second pass adds V^T lo (its fragments read again).
                 F pb[4], pl[SPLIT ? 4 : 1];
-                const bool two = SPLIT && FL && big;
+                constexpr bool two = SPLIT && TWO;
                 float ps = 0.f, pr = 0.f;
                 // Two row sums: ps of the probabilities themselves (for the
                 // LSE, which the backward's recomputed P relies on) and pr of
@@ -279,7 +276,7 @@ __global__ __launch_bounds__(AF_NT, 2) void attn_fwd_kernel(
             c_cur = c_next;
         }
     };
-    if (SPLIT && (all_big || some_big)) walk(std::true_type{});
+    if (SPLIT && big) walk(std::true_type{});
     else walk(std::false_type{});
 
     const float lt = q_real ? l + swap_half(l) : 0.f;     // a padding query has no output

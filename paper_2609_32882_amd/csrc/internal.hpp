@@ -102,24 +102,32 @@ hipError_t launch_lpt_order(const int32_t* ptr, int64_t nrows, int64_t n_per_hea
                             hipStream_t s);
 // Magnitude flags of the 64-token blocks of bf16 Q, K, V: q[row] for the
 // query blocks, kv[row] for the key blocks (K and V combined), 1 when a real
-// token holds a value above 8 in magnitude; any_q[g] / any_kv[g] per KV group
+// token holds a value above 7 in magnitude; any_q[g] / any_kv[g] per KV group
 // g = b*Hkv + hkv: some flagged query block among the group's query heads /
 // some flagged key block of the head.  The attention kernels take two-term
-// P / dS operands on block pairs that touch a flagged block.
+// P / dS operands where these flags (and the row flags) say so.
 struct block_flag_layout {
     uint8_t* q;
     uint8_t* kv;
     int32_t* any_q;
     int32_t* any_kv;
-    uint8_t* qrow;       // per query block: bit 0 its own flag, bit 1 its row touches a flagged block
+    // per query block: bit 0 its own flag; bit 1 two-term dS for its row
+    // (its list touches a flagged block, its own flag included, or one of
+    // its queries has |Delta| above DELTA_FLAG)
+    uint8_t* qrow;
     int32_t* any_row;    // per KV group: some query block of the group has bit 1
 };
+// Rows whose Delta = dO . O exceeds this in magnitude at some query take
+// two-term dS: dS = P (dP - Delta) is then a small difference of large
+// terms whose one-term rounding the gradients amplify.
+constexpr float DELTA_FLAG = 16.0f;
 block_flag_layout block_flags_at(void* base, int64_t rows_q, int64_t rows_kv, int64_t groups);
 size_t block_flags_bytes(int64_t rows_q, int64_t rows_kv, int64_t groups);
 hipError_t launch_block_flags(const void* q, const void* k, const void* v, const block_flag_layout& f, int64_t rows_q,
                               int64_t rows_kv, int N, int D, int Hq, int Hkv, const cube_grid& cg, hipStream_t s);
-hipError_t launch_row_flags(const block_flag_layout& f, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
-                            int64_t rows_q, int64_t rows_kv, int N, int Hq, int Hkv, hipStream_t s);
+hipError_t launch_row_flags(const block_flag_layout& f, const float* stat, const int32_t* kv_ptr,
+                            const int32_t* kv_idx, int64_t col_cap, int64_t rows_q, int64_t rows_kv, int N, int Hq,
+                            int Hkv, hipStream_t s);
 hipError_t launch_attn_bwd(int dtype, int D, const void* q, const void* k, const void* v, const void* o,
                            const float* lse, const void* o_lo, const void* dout, const int32_t* row_ptr,
                            const int32_t* col_idx, const int32_t* kv_ptr, const int32_t* kv_idx,

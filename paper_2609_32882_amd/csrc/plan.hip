@@ -232,18 +232,27 @@ __global__ __launch_bounds__(256) void zero_i32_kernel(int32_t* __restrict__ p, 
     if (i < n) p[i] = 0;
 }
 
-// Row flags, first step: byte = 3 for a flagged query block, 0 otherwise;
-// the group word is set for a flagged query block.
+// Row flags, first step (one wave per query block): bit 0 = the block's own
+// flag, bit 1 = its own flag or |Delta| above DELTA_FLAG at one of its
+// queries with attention mass (scaled LSE below +inf; padding queries and
+// empty rows have none); the group word is set for bit 1.  The statistics
+// hold, per 64-token block, 64 scaled LSE values then 64 negated Deltas.
 __global__ __launch_bounds__(256) void row_flag_init_kernel(const uint8_t* __restrict__ flag_q,
+                                                            const float* __restrict__ stat,
                                                             uint8_t* __restrict__ qrow, int32_t* __restrict__ any_row,
                                                             int64_t rows_q, int N, int Hq, int Hkv) {
-    const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (r >= rows_q) return;
+    const int lane = threadIdx.x & 63;
+    const int64_t r = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+    if (r >= rows_q) return;                          // wave-uniform
+    const float ls = stat[r * 128 + lane], nd = stat[r * 128 + 64 + lane];
+    const bool dbig = __any(ls != INFINITY && fabsf(nd) > DELTA_FLAG);
     const bool f = flag_q[r] != 0;
-    qrow[r] = f ? 3 : 0;
-    if (f) {     // every writer stores the same value
-        const int64_t bh = r / N;
-        any_row[(bh / Hq) * Hkv + (bh % Hq) / (Hq / Hkv)] = 1;
+    if (lane == 0) {
+        qrow[r] = static_cast<uint8_t>((f ? 1 : 0) | (f || dbig ? 2 : 0));
+        if (f || dbig) {     // every writer stores the same value
+            const int64_t bh = r / N;
+            any_row[(bh / Hq) * Hkv + (bh % Hq) / (Hq / Hkv)] = 1;
+        }
     }
 }
 
@@ -313,16 +322,17 @@ hipError_t launch_block_flags(const void* q, const void* k, const void* v, const
     return hipGetLastError();
 }
 
-// Row flags from the block flags (which the same workspace already holds)
-// and the transposed lists.
-hipError_t launch_row_flags(const block_flag_layout& f, const int32_t* kv_ptr, const int32_t* kv_idx, int64_t col_cap,
-                            int64_t rows_q, int64_t rows_kv, int N, int Hq, int Hkv, hipStream_t s) {
+// Row flags from the block flags (which the same workspace already holds),
+// the statistics (Deltas) and the transposed lists.
+hipError_t launch_row_flags(const block_flag_layout& f, const float* stat, const int32_t* kv_ptr,
+                            const int32_t* kv_idx, int64_t col_cap, int64_t rows_q, int64_t rows_kv, int N, int Hq,
+                            int Hkv, hipStream_t s) {
     if (rows_q <= 0 || rows_kv <= 0) return hipSuccess;
     const int64_t groups = rows_kv / N;
     hipLaunchKernelGGL(zero_i32_kernel, dim3(static_cast<unsigned>((groups + 255) / 256)), dim3(256), 0, s,
                        f.any_row, groups);
-    hipLaunchKernelGGL(row_flag_init_kernel, dim3(static_cast<unsigned>((rows_q + 255) / 256)), dim3(256), 0, s,
-                       f.q, f.qrow, f.any_row, rows_q, N, Hq, Hkv);
+    hipLaunchKernelGGL(row_flag_init_kernel, dim3(static_cast<unsigned>((rows_q + 3) / 4)), dim3(256), 0, s,
+                       f.q, stat, f.qrow, f.any_row, rows_q, N, Hq, Hkv);
     hipLaunchKernelGGL(row_flag_scatter_kernel, dim3(static_cast<unsigned>((rows_kv + 3) / 4)), dim3(256), 0, s,
                        f.kv, kv_ptr, kv_idx, col_cap, f.qrow, f.any_row, rows_kv, N, Hq, Hkv);
     return hipGetLastError();

@@ -4,16 +4,20 @@ code with the HIP path).
 
 Everything is computed in fp64 except the roundings the kernels apply:
 - forward: P rounded to bf16 before the P.V product (hi + lo, i.e. about 16
-  bits, on a two-term pair); O divided by the sum of the rounded P
+  bits, on a two-term pair: with p_row_rule every pair of a row that touches
+  a flagged block, else the pairs that touch one); O divided by the sum of
+  the rounded P
   (rounded_sum=True) or of the unrounded P; O stored as o + o_lo (two bf16
   terms), which Delta = dO . O reads;
 - backward: dS = P (dP - Delta) rounded to bf16 (hi + lo on a two-term
   pair) before the dS.K (dQ) and dS^T.Q (dK) products, with P the exact
   softmax (the kernels recompute it in fp32 from the LSE);
 - outputs rounded to bf16.
-A pair is two-term for P when its query block or its key block (K or V) is
-flagged (a real-token value above `tau`); for dS also when the query
-block's row touches a flagged block and row_rule=True.  fp32 accumulation
+A block is flagged when a real token holds a value above `tau`.  A pair is
+two-term for dS when its query block or its key block (K or V) is flagged,
+and on every pair of the row when row_rule=True and the row touches a
+flagged block, or when one of the row's queries has |Delta| above
+delta_tau.  fp32 accumulation
 is not modelled (its error is far below these roundings on the inputs
 studied).
 
@@ -46,7 +50,7 @@ def block_flags(x, p, tau):
     return amax(x["q"]) > tau, (amax(x["k"]) > tau) | (amax(x["v"]) > tau)
 
 
-def model_errors(w, tau=7.0, row_rule=True, rounded_sum=True):
+def model_errors(w, tau=7.0, row_rule=True, rounded_sum=True, p_row_rule=True, delta_tau=16.0):
     """(dQ max share, dK max share, dQ rel-L2, dK rel-L2) of the modelled
     kernels on workload w (bf16, no text tokens)."""
     p = w.problem
@@ -90,13 +94,16 @@ def model_errors(w, tau=7.0, row_rule=True, rounded_sum=True):
                 # forward: O from the rounded P, divided by either sum
                 O = np.zeros((B, D))
                 lr = np.zeros((B, 1))
-                for j, two in enumerate(pair):
+                two_p = pair | pair.any() if p_row_rule else pair
+                for j, two in enumerate(two_p):
                     pj = pu[:, j * B:(j + 1) * B]
                     pr = _two(pj) if two else _bf(pj)
                     O += pr @ v[j * B:(j + 1) * B]
                     lr += pr.sum(1, keepdims=True)
                 O /= lr if rounded_sum else pu.sum(1, keepdims=True)
                 delta = (do * _two(O)).sum(1, keepdims=True)
+                if delta_tau is not None and qreal.any() and np.abs(delta[qreal]).max() > delta_tau:
+                    row = True
                 dS = P * (dP - delta)
                 dS[~qreal] = 0
                 acc = np.zeros((B, D))

@@ -59,4 +59,14 @@ REGRESSION = [
     # at 8 even under the rules above
     Workload("near-threshold-cap2", Problem(1, 4, 2, 64, 9, 10, 11, Rt=4, Rh=4, Rw=4), Selection(1, 0, 0.9, 2), 3326,
              skewed=True),
+    # two-term P only on the pairs that touch a flagged block: a row whose
+    # other pairs are flagged takes one-term P on the rest, and that rounding,
+    # weighted by how far each pair's dO . V lies from the row's mean,
+    # reaches Delta (|Delta| up to 319 here): dQ over the bar
+    Workload("one-term-p-in-flagged-row", Problem(1, 4, 2, 64, 9, 19, 20, Rt=2, Rh=2, Rw=4),
+             Selection(1, 0, 0.99, 9), 9202231, skewed=True),
+    # a row with no flagged block (values up to 6.6) but |Delta| up to 19
+    # and a peaked softmax (cap 2): one-term dS puts dK over the bar
+    Workload("large-delta-unflagged-row", Problem(1, 2, 1, 64, 5, 10, 5, Rt=4, Rh=4, Rw=4),
+             Selection(1, 0, 0.99, 2), 9202154, skewed=True),
 ]

@@ -278,8 +278,9 @@ def test_block_flags_rule():
     (7 itself is not), padding tokens never count, K and V flag their key
     block together, and the per-KV-group summary words say whether any block
     of the group is flagged (prep stage); the row byte of a query block
-    holds its own flag (bit 0) and whether its block list touches a flagged
-    block, its own flag included (bit 1), with one word per KV group saying
+    holds its own flag (bit 0) and, in bit 1, whether its block list touches
+    a flagged block, its own flag included, or one of its queries has
+    |Delta| = |dO . (O + o_lo)| above 16, with one word per KV group saying
     whether any of the group's query blocks has bit 1 (dK/dV stage)."""
     a256 = lambda n: (n + 255) // 256 * 256
     for name in ("bf16-padded", "bf16-d64-gqa", "bf16-mass"):
@@ -294,12 +295,18 @@ def test_block_flags_rule():
         if p.padded:                                   # padding never counts
             x["k"][0, 1, np.flatnonzero(~real)[0], 7] = 100.0
         fq, fkv = block_flags(x, p)
+        # O (passed as o and as o_lo, so O + o_lo = 2 O): zero, except a
+        # multiple of dO at a few real queries, far above (2.0) and far below
+        # (0.02) the Delta threshold
+        o_np = np.zeros_like(x["q"])
+        for hh, t, c in ((0, tok[70], 2.0), (p.heads_q - 1, tok[len(tok) // 2], 2.0), (1, tok[5], 0.02)):
+            o_np[0, hh, t] = x["do"][0, hh, t] * c
         dev = {k: to_dev(v, True) for k, v in x.items()}
         P = vsa2.problem_from(p)
         st, bwsb = vsa2.vsa2_attn_workspace(P, 1)
         assert st == 0
         bws = torch.zeros(bwsb, dtype=torch.uint8, device="cuda")
-        o = torch.zeros_like(dev["q"])
+        o = to_dev(o_np, True)
         lse = torch.zeros(p.batch, p.heads_q, p.L, dtype=torch.float32, device="cuda")
         st = vsa2.vsa2_attn_bwd_prep(P, dev["q"].data_ptr(), dev["k"].data_ptr(), dev["v"].data_ptr(),
                                      o.data_ptr(), lse.data_ptr(), o.data_ptr(), dev["do"].data_ptr(),
@@ -336,6 +343,12 @@ def test_block_flags_rule():
             bh = r // p.N
             kvbase = ((bh // p.heads_q) * p.heads_kv + (bh % p.heads_q) // grp) * p.N
             rowf[r] = fq_flat[r] or fkv_flat[kvbase + ci[rp[r]:rp[r + 1]]].any()
+        ob = to_np(o).astype(np.float64)
+        delta = (2 * ob * to_np(dev["do"]).astype(np.float64)).sum(-1)     # [b, h, L]
+        assert np.all((np.abs(delta) > 40) | (np.abs(delta) < 8))          # far from the threshold
+        dbig = (np.abs(delta) > 16).reshape(nq, p.B).any(-1)
+        assert dbig.sum() == 2
+        rowf |= dbig
         qoff = off + a256(nq) + a256(nkv) + a256(8 * groups)
         got_row = raw[qoff:qoff + nq]
         any_row = raw[qoff + a256(nq):][:4 * groups].view(np.int32)
