@@ -923,6 +923,41 @@ __global__ void csc_mark_kernel(const int32_t* __restrict__ row_ptr, const int32
     }
 }
 
+// The same marks built per (KV group, 32-bit word of its query-block bits):
+// the workgroup's 32 query-block rows (8 threads each) set their bits of
+// every key block in LDS (N words), then the workgroup writes those N words.
+// Every mask word is written exactly once, by one workgroup, so neither
+// global atomics nor a zero fill are needed.  Grid: groups x words.
+constexpr int CSC_LDS_MAX_N = 16384;   // N words of LDS (64 KB)
+__global__ __launch_bounds__(256) void csc_mark_lds_kernel(const int32_t* __restrict__ row_ptr,
+                                                           const int32_t* __restrict__ col_idx, int N, int Hq,
+                                                           int Hkv, int words, int64_t col_cap,
+                                                           uint32_t* __restrict__ mask) {
+    extern __shared__ uint32_t marks[];
+    const int grp = Hq / Hkv;
+    const int64_t g = blockIdx.x / words;             // b*Hkv + hkv
+    const int w = static_cast<int>(blockIdx.x % words);
+    const int b = static_cast<int>(g / Hkv), hkv = static_cast<int>(g % Hkv);
+    for (int i = threadIdx.x; i < N; i += blockDim.x) marks[i] = 0u;
+    __syncthreads();
+    const int r = threadIdx.x >> 3, sub = threadIdx.x & 7;
+    const int bit = w * 32 + r;                       // hl*N + nq
+    if (bit < grp * N) {
+        const int hl = bit / N, nq = bit % N;
+        const int64_t row = (static_cast<int64_t>(b) * Hq + hkv * grp + hl) * N + nq;
+        int64_t s0 = row_ptr[row], s1 = row_ptr[row + 1];
+        s0 = s0 < 0 ? 0 : (s0 > col_cap ? col_cap : s0);
+        s1 = s1 < s0 ? s0 : (s1 > col_cap ? col_cap : s1);
+        for (int64_t e = s0 + sub; e < s1; e += 8) {
+            const int nk = col_idx[e];
+            if (nk >= 0 && nk < N) atomicOr(&marks[nk], 1u << r);
+        }
+    }
+    __syncthreads();
+    uint32_t* out = mask + g * N * words + w;         // mask[(g*N + nk)*words + w]
+    for (int i = threadIdx.x; i < N; i += blockDim.x) out[static_cast<int64_t>(i) * words] = marks[i];
+}
+
 __global__ void csc_count_kernel(const uint32_t* __restrict__ mask, int64_t nkrows, int words,
                                  int32_t* __restrict__ counts) {
     const int64_t r = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -955,10 +990,16 @@ hipError_t launch_csc(const int32_t* row_ptr, const int32_t* col_idx, int batch,
     const int words = (Hq / Hkv * N + 31) / 32;
     const int64_t nkrows = static_cast<int64_t>(batch) * Hkv * N;
     const int64_t nrows = static_cast<int64_t>(batch) * Hq * N;
-    hipError_t e = launch_fill_u32(mask, nkrows * words, 0u, s);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(csc_mark_kernel, dim3(static_cast<unsigned>((nrows + 255) / 256)), dim3(256), 0, s,
-                       row_ptr, col_idx, nrows, N, Hq, Hkv, words, col_cap, mask);
+    hipError_t e;
+    const int64_t wgs = static_cast<int64_t>(batch) * Hkv * words;
+    if (N <= CSC_LDS_MAX_N && wgs <= 0x7fffffff) {
+        hipLaunchKernelGGL(csc_mark_lds_kernel, dim3(static_cast<unsigned>(wgs)), dim3(256),
+                           static_cast<size_t>(N) * 4, s, row_ptr, col_idx, N, Hq, Hkv, words, col_cap, mask);
+    } else {
+        if ((e = launch_fill_u32(mask, nkrows * words, 0u, s)) != hipSuccess) return e;
+        hipLaunchKernelGGL(csc_mark_kernel, dim3(static_cast<unsigned>((nrows + 255) / 256)), dim3(256), 0, s,
+                           row_ptr, col_idx, nrows, N, Hq, Hkv, words, col_cap, mask);
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(csc_count_kernel, dim3(static_cast<unsigned>((nkrows + 255) / 256)), dim3(256), 0, s,
                        mask, nkrows, words, kv_counts);
