@@ -843,29 +843,44 @@ hipError_t launch_select_seq(const float* scores, int64_t nseq, int N, int k, vo
 // ===========================================================================
 // Offsets and the transposed lists
 // ===========================================================================
-// Exclusive scan of counts[0..n) into ptr[0..n] by one workgroup of 1024.
+// Exclusive scan of counts[0..n) into ptr[0..n] by one workgroup of 16
+// waves.  Wave w owns the contiguous segment [w seg, (w + 1) seg) and reads
+// it 64 consecutive counts at a time (coalesced): a first pass sums each
+// segment, the 16 totals give each wave its starting carry, and a second
+// pass writes the offsets with a wave prefix sum per 64 counts.
 __global__ __launch_bounds__(1024) void scan_kernel(const int32_t* __restrict__ counts, int64_t n,
                                                     int32_t* __restrict__ ptr) {
-    __shared__ int32_t part[1024];
-    const int tid = threadIdx.x;
-    const int64_t per = (n + 1023) / 1024;
-    const int64_t lo = tid * per, hi = lo + per < n ? lo + per : n;
+    __shared__ int32_t tot[16];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int64_t seg = (n + 15) / 16;
+    const int64_t lo = w * seg, hi = lo + seg < n ? lo + seg : n;
     int32_t s = 0;
-    for (int64_t i = lo; i < hi; ++i) s += counts[i];
-    part[tid] = s;
+#pragma unroll 8
+    for (int64_t i = lo + lane; i < hi; i += 64) s += counts[i];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+    if (lane == 0) tot[w] = s;
     __syncthreads();
-    for (int off = 1; off < 1024; off <<= 1) {
-        const int32_t v = tid >= off ? part[tid - off] : 0;
-        __syncthreads();
-        part[tid] += v;
-        __syncthreads();
+    int32_t carry = 0;
+    for (int j = 0; j < w; ++j) carry += tot[j];
+#pragma unroll 4
+    for (int64_t base = lo; base < hi; base += 64) {
+        const int64_t i = base + lane;
+        const int32_t x = i < hi ? counts[i] : 0;
+        int32_t incl = x;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int32_t y = __shfl_up(incl, off, 64);
+            if (lane >= off) incl += y;
+        }
+        if (i < hi) ptr[i] = carry + incl - x;
+        carry += __shfl(incl, 63, 64);
     }
-    int32_t run = part[tid] - s;   // exclusive prefix of this thread's range
-    for (int64_t i = lo; i < hi; ++i) {
-        ptr[i] = run;
-        run += counts[i];
+    if (threadIdx.x == 0) {
+        int32_t t = 0;
+        for (int j = 0; j < 16; ++j) t += tot[j];
+        ptr[n] = t;
     }
-    if (tid == 1023) ptr[n] = part[1023];
 }
 
 hipError_t launch_scan(const int32_t* counts, int64_t n, int32_t* ptr, hipStream_t s) {
