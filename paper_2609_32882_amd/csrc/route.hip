@@ -944,7 +944,8 @@ __global__ void csc_mark_kernel(const int32_t* __restrict__ row_ptr, const int32
 // Every mask word is written exactly once, by one workgroup, so neither
 // global atomics nor a zero fill are needed.  Grid: groups x words.
 constexpr int CSC_LDS_MAX_N = 16384;   // N words of LDS (64 KB)
-__global__ __launch_bounds__(256) void csc_mark_lds_kernel(const int32_t* __restrict__ row_ptr,
+constexpr int CSC_NT = 256;            // 32 rows x 8 threads
+__global__ __launch_bounds__(CSC_NT) void csc_mark_lds_kernel(const int32_t* __restrict__ row_ptr,
                                                            const int32_t* __restrict__ col_idx, int N, int Hq,
                                                            int Hkv, int words, int64_t col_cap,
                                                            uint32_t* __restrict__ mask) {
@@ -953,9 +954,9 @@ __global__ __launch_bounds__(256) void csc_mark_lds_kernel(const int32_t* __rest
     const int64_t g = blockIdx.x / words;             // b*Hkv + hkv
     const int w = static_cast<int>(blockIdx.x % words);
     const int b = static_cast<int>(g / Hkv), hkv = static_cast<int>(g % Hkv);
-    for (int i = threadIdx.x; i < N; i += blockDim.x) marks[i] = 0u;
+    for (int i = threadIdx.x; i < N; i += CSC_NT) marks[i] = 0u;
     __syncthreads();
-    const int r = threadIdx.x >> 3, sub = threadIdx.x & 7;
+    const int r = threadIdx.x >> 3, sub = threadIdx.x & 7;   // r < 32
     const int bit = w * 32 + r;                       // hl*N + nq
     if (bit < grp * N) {
         const int hl = bit / N, nq = bit % N;
@@ -970,7 +971,7 @@ __global__ __launch_bounds__(256) void csc_mark_lds_kernel(const int32_t* __rest
     }
     __syncthreads();
     uint32_t* out = mask + g * N * words + w;         // mask[(g*N + nk)*words + w]
-    for (int i = threadIdx.x; i < N; i += blockDim.x) out[static_cast<int64_t>(i) * words] = marks[i];
+    for (int i = threadIdx.x; i < N; i += CSC_NT) out[static_cast<int64_t>(i) * words] = marks[i];
 }
 
 __global__ void csc_count_kernel(const uint32_t* __restrict__ mask, int64_t nkrows, int words,
@@ -1008,7 +1009,7 @@ hipError_t launch_csc(const int32_t* row_ptr, const int32_t* col_idx, int batch,
     hipError_t e;
     const int64_t wgs = static_cast<int64_t>(batch) * Hkv * words;
     if (N <= CSC_LDS_MAX_N && wgs <= 0x7fffffff) {
-        hipLaunchKernelGGL(csc_mark_lds_kernel, dim3(static_cast<unsigned>(wgs)), dim3(256),
+        hipLaunchKernelGGL(csc_mark_lds_kernel, dim3(static_cast<unsigned>(wgs)), dim3(CSC_NT),
                            static_cast<size_t>(N) * 4, s, row_ptr, col_idx, N, Hq, Hkv, words, col_cap, mask);
     } else {
         if ((e = launch_fill_u32(mask, nkrows * words, 0u, s)) != hipSuccess) return e;
