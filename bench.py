@@ -263,7 +263,7 @@ def main():
             "cube": [p.Bt, p.Bh, p.Bw], "router_pool": [p.Rt, p.Rh, p.Rw],
             "select": ("top-%d" % sel.k) if sel.mode == 0 else ("mass-%.2f-cap-%d" % (sel.mass, sel.cap)),
             "nnz_block_pairs": nnz,
-            "products": "bf16; two-term P on block pairs touching a block with a value above 7, two-term dS on rows touching one",
+            "products": "bf16; two-term P on every pair of a row touching a block with a value above 7 (dV product: on the pairs touching one), two-term dS on such rows and on rows with |Delta| above 16",
             "sparsity": round(sparsity, 4),
         },
         "breakdown_ms": {s: round(stage_ms[s], 4) for s in ("pool", "route", "fwd", "bwd") + stages[3:]},
