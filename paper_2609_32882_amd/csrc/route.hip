@@ -579,7 +579,9 @@ hipError_t launch_select(int phase, const float* scores, int64_t nrows, int N, i
     VSA2_SEL(2);
     VSA2_SEL(4);
     VSA2_SEL(8);
+    VSA2_SEL(12);
     VSA2_SEL(16);
+    VSA2_SEL(20);
     VSA2_SEL(24);
     VSA2_SEL(32);
     VSA2_SEL(40);
